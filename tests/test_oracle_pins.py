@@ -1,0 +1,528 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+published generator outputs, printed byte counts, closed forms, textbook
+reductions, invariants and brute force on tiny inputs."""
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from conftest import read_golden, read_golden_lines
+from oracle import awsrc_oracle as O
+
+
+# ---------------------------------------------------------------- generator
+def test_splitmix64_published_vectors():
+    want = [int(x, 16) for x in read_golden_lines("splitmix64_key0.txt")]
+    assert [O.splitmix64(0, n) for n in range(len(want))] == want
+
+
+def _splitmix64_numpy(key, counters):
+    """Independent numpy uint64 implementation (wrapping arithmetic)."""
+    with np.errstate(over="ignore"):
+        z = np.uint64(key) + (counters.astype(np.uint64) + np.uint64(1)) * np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+@pytest.mark.parametrize("key", [0, 1, 0xDEADBEEFCAFEF00D, (1 << 64) - 1])
+def test_splitmix64_two_implementations(key):
+    rng = np.random.default_rng(key & 0xFFFF)
+    n = np.concatenate([np.arange(2000), rng.integers(0, 1 << 62, 2000)]).astype(np.uint64)
+    got = _splitmix64_numpy(key, n)
+    for i in range(0, len(n), 97):
+        assert int(got[i]) == O.splitmix64(key, int(n[i]))
+
+
+def test_gen_basis_worked_example():
+    g = read_golden("gen_v1_key0_s0_C64_P4.txt")
+    word = int(g["sign_word"][0], 16)
+    sigma, cols = O.gen_basis(0, 0, 64, 4)
+    assert cols == [int(c) for c in g["columns"]]
+    assert all(sigma[j] == (-1 if (word >> j) & 1 else 1) for j in range(64))
+
+
+@pytest.mark.parametrize("C,P", [(4, 2), (16, 4), (64, 8), (128, 8), (64, 64), (32, 1)])
+def test_gen_basis_properties(C, P):
+    for s in range(40):
+        sigma, cols = O.gen_basis(7, s, C, P)
+        assert len(cols) == P and len(set(cols)) == P
+        assert all(0 <= c < C for c in cols)
+        assert set(np.unique(sigma)) <= {-1, 1}
+    # signs of C=128 use two words; the second half must differ from the first
+    if C == 128:
+        sig, _ = O.gen_basis(0, 3, 128, 1)
+        w0, w1 = O.basis_word(0, 3, 0), O.basis_word(0, 3, 1)
+        assert all(sig[64 + j] == (-1 if (w1 >> j) & 1 else 1) for j in range(64))
+        assert all(sig[j] == (-1 if (w0 >> j) & 1 else 1) for j in range(64))
+
+
+def test_gen_basis_full_selection_is_permutation():
+    # P = C draws every column exactly once
+    for s in range(10):
+        _, cols = O.gen_basis(3, s, 16, 16)
+        assert sorted(cols) == list(range(16))
+
+
+# ---------------------------------------------------------------- Hadamard
+@pytest.mark.parametrize("C", [1, 2, 4, 8, 16, 32, 64, 128])
+def test_hadamard_orthogonal(C):
+    H = O.hadamard(C)
+    assert np.array_equal(H @ H.T, C * np.eye(C, dtype=np.int64))
+
+
+def test_hadamard_sylvester_recursion():
+    H = np.array([[1]], dtype=np.int64)
+    for k in range(7):
+        H = np.block([[H, H], [H, -H]])
+        assert np.array_equal(H, O.hadamard(2 ** (k + 1)))
+
+
+def test_basis_columns_orthonormal():
+    B = O.basis_matrix(0, 5, 64, 8)
+    assert np.allclose(B.T @ B, np.eye(8), atol=1e-15)
+
+
+# ---------------------------------------------------------------- backbone
+def test_rtn_closed_form_group():
+    # w_k = (k mod 16)/4 - 1: min -1, max 2.75, (max-min)/15 = 0.25 exactly,
+    # zero point rint(1/0.25) = 4, codes k mod 16, reconstruction exact.
+    k = np.arange(128)
+    W = ((k % 16) * 0.25 - 1.0).astype(np.float32)[None, :]
+    codes, scale, zero, W0 = O.rtn_backbone(W)
+    assert scale[0, 0] == 0x3400 and zero[0, 0] == 4
+    q = np.empty(128, np.int64)
+    q[0::2] = codes[0] & 15
+    q[1::2] = codes[0] >> 4
+    assert np.array_equal(q, k % 16)
+    assert np.array_equal(W0, W)
+
+
+def test_rtn_half_even_tie():
+    # scale 1.0 (max-min = 15), zero point 0; w = 2.5 -> rint -> 2, w = 3.5 -> 4
+    W = np.zeros((1, 128), np.float32)
+    W[0, 1] = 15.0
+    W[0, 2] = 2.5
+    W[0, 3] = 3.5
+    codes, scale, zero, W0 = O.rtn_backbone(W)
+    assert scale[0, 0] == 0x3C00 and zero[0, 0] == 0
+    assert W0[0, 2] == 2.0 and W0[0, 3] == 4.0 and W0[0, 1] == 15.0
+
+
+def test_rtn_degenerate_group():
+    W = np.full((1, 128), 0.5, np.float32)
+    codes, scale, zero, W0 = O.rtn_backbone(W)
+    assert scale[0, 0] == 0x3C00 and zero[0, 0] == 0 and np.all(codes == 0) and np.all(W0 == 0)
+
+
+def test_rtn_nearest_code_exact_rational():
+    """Every code is a nearest integer of w/s + z, checked in exact rational
+    arithmetic (independent of float rounding except at exact ties)."""
+    rng = np.random.default_rng(0)
+    W = (rng.standard_normal((8, 256)) * 0.02).astype(np.float32)
+    W[3, :128] *= 100
+    codes, scale, zero, W0 = O.rtn_backbone(W)
+    for r in range(8):
+        for g in range(2):
+            s = Fraction(float(np.array([scale[r, g]], np.uint16).view(np.float16)[0]))
+            z = int(zero[r, g])
+            grp = W[r, g * 128:(g + 1) * 128]
+            mn, mx = Fraction(float(grp.min())), Fraction(float(grp.max()))
+            # the stored scale is the fp16 rounding of (max-min)/15 within fp16/fp32 error
+            assert abs(s - (mx - mn) / 15) <= (mx - mn) / 15 * Fraction(1, 1024)
+            assert 0 <= z <= 15 and abs(Fraction(z) - (-mn / s)) <= Fraction(1, 2) + Fraction(1, 10 ** 6)
+            for i in range(128):
+                col = g * 128 + i
+                q = int((codes[r, col // 2] >> (4 * (col % 2))) & 15)
+                x = Fraction(float(grp[i])) / s + z
+                if 0 < q < 15:
+                    assert abs(x - q) <= Fraction(1, 2) + Fraction(1, 10 ** 6)
+                elif q == 0:
+                    assert x <= Fraction(1, 2) + Fraction(1, 10 ** 6)
+                else:
+                    assert x >= Fraction(29, 2) - Fraction(1, 10 ** 6)
+                assert float(W0[r, col]) == float((q - z) * s)
+
+
+# ---------------------------------------------------------------- fit
+def _random_problem(rng, N, C, per_element=True):
+    R = rng.standard_normal((N, C)) * 0.01
+    D = np.exp(rng.standard_normal((N, C)) * 1.5) if per_element else np.tile(
+        np.exp(rng.standard_normal(C) * 1.5), (N, 1))
+    return R, D
+
+
+@pytest.mark.parametrize("lam", [0.0, 1e-6, 0.3])
+def test_fit_matches_lstsq(lam):
+    """Eq. (3) is the least-squares problem [D^1/2 B; sqrt(eps) I] a ~ [D^1/2 r; 0]."""
+    rng = np.random.default_rng(1)
+    R, D = _random_problem(rng, 20, 64)
+    B = O.basis_matrix(0, 9, 64, 8)
+    alpha, G, b = O.fit(R, D, B, lam)
+    for t in range(20):
+        eps = lam * D[t].mean()
+        A = np.vstack([np.sqrt(D[t])[:, None] * B, math.sqrt(eps) * np.eye(8)])
+        y = np.concatenate([np.sqrt(D[t]) * R[t], np.zeros(8)])
+        ref = np.linalg.lstsq(A, y, rcond=None)[0]
+        assert np.allclose(alpha[t], ref, rtol=1e-10, atol=1e-14 * np.abs(ref).max())
+
+
+def test_fit_first_order_optimality():
+    """The objective of Eq. (3) does not decrease along any coordinate direction."""
+    rng = np.random.default_rng(2)
+    R, D = _random_problem(rng, 5, 32)
+    B = O.basis_matrix(1, 2, 32, 4)
+    lam = 1e-3
+    alpha, _, _ = O.fit(R, D, B, lam)
+
+    def obj(t, a):
+        return float(np.sum(D[t] * (B @ a - R[t]) ** 2) + lam * D[t].mean() * np.sum(a * a))
+
+    for t in range(5):
+        f0 = obj(t, alpha[t])
+        for p in range(4):
+            for h in (1e-5, -1e-5):
+                e = np.zeros(4)
+                e[p] = h * max(1e-3, abs(alpha[t][p]))
+                assert obj(t, alpha[t] + e) >= f0 - 1e-18
+
+
+def test_gram_and_projection_via_walsh_hadamard():
+    """G_pq = WHT(d)[c_p xor c_q]/C and b_p = WHT(sigma*d*r)[c_p]/sqrt(C)
+    (sign cancellation and the Sylvester xor identity H[j,a]H[j,b] = H[j,a^b])."""
+
+    def fwht(v):  # fast Walsh-Hadamard transform, natural order
+        v = v.astype(np.float64).copy()
+        h = 1
+        while h < len(v):
+            for i in range(0, len(v), 2 * h):
+                a, b = v[i:i + h].copy(), v[i + h:i + 2 * h].copy()
+                v[i:i + h], v[i + h:i + 2 * h] = a + b, a - b
+            h *= 2
+        return v
+
+    rng = np.random.default_rng(3)
+    C, P = 64, 8
+    R, D = _random_problem(rng, 6, C)
+    for s in range(4):
+        sigma, cols = O.gen_basis(0, s, C, P)
+        B = O.basis_matrix(0, s, C, P)
+        _, G, b = O.fit(R, D, B, 0.0)
+        for t in range(6):
+            wd = fwht(D[t])
+            Gx = np.array([[wd[cp ^ cq] / C for cq in cols] for cp in cols])
+            assert np.allclose(G[t], Gx, rtol=1e-12, atol=1e-15)
+            wu = fwht(sigma * D[t] * R[t])
+            assert np.allclose(b[t], wu[cols] / math.sqrt(C), rtol=1e-12, atol=1e-16)
+            assert np.isclose(G[t][0, 0], D[t].mean(), rtol=1e-13)
+
+
+# ---------------------------------------------------------------- quantize / score
+def test_gain_coefficient_space_identity():
+    """sum_j d(r^2 - (r - B a)^2) = 2 a^T b - a^T (B^T D B) a for any a."""
+    rng = np.random.default_rng(4)
+    R, D = _random_problem(rng, 30, 64)
+    B = O.basis_matrix(0, 3, 64, 8)
+    alpha, G, b = O.fit(R, D, B, 1e-6)
+    q, bits, sc = O.quantize(alpha, 4)
+    ah = sc[:, None] * q
+    g_def = O.weighted_gain(R, D, ah @ B.T)
+    G0 = G - (1e-6 * D.mean(axis=1))[:, None, None] * np.eye(8)
+    g_cs = 2 * np.einsum("np,np->n", ah, b) - np.einsum("np,npq,nq->n", ah, G0, ah)
+    assert np.allclose(g_def, g_cs, rtol=1e-11, atol=1e-20)
+
+
+def test_quantize_properties():
+    rng = np.random.default_rng(5)
+    alpha = rng.standard_normal((500, 8)) * 0.05
+    alpha[0] = 0
+    for b in (2, 3, 4, 8):
+        qmax = 2 ** (b - 1) - 1
+        q, bits, sc = O.quantize(alpha, b)
+        assert np.all(np.abs(q) <= qmax)
+        assert np.all(np.abs(q[1:]).max(axis=1) == qmax)
+        assert bits[0] == 0 and np.all(q[0] == 0)
+        # scale is fp16(fp32(m/qmax)): within half an fp16 ulp (plus fp32 rounding) of m/qmax
+        m = np.abs(alpha[1:]).max(axis=1)
+        assert np.all(np.abs(sc[1:] - m / qmax) <= (m / qmax) * (2.0 ** -11 + 2.0 ** -24))
+        # each code is a nearest integer of alpha/scale
+        x = alpha[1:] / sc[1:, None]
+        assert np.all(np.abs(x - q[1:]) <= 0.5 + 1e-12)
+
+
+def test_quantize_fp16_double_rounding():
+    """The scale rounds m/qmax to fp32 first, then to fp16 (both to nearest even)."""
+    # v sits just above an fp16 midpoint in float64 but rounds onto it in fp32:
+    # 1 + 2^-11 is the fp16 midpoint between 1 and 1+2^-10; fp32 of 1 + 2^-11 + 2^-40
+    # is exactly the midpoint, which then ties to even (1.0); direct rounding gives 1+2^-10.
+    v = 1 + 2.0 ** -11 + 2.0 ** -40
+    q, bits, sc = O.quantize(np.array([[7 * v, 0.0]]), 4)
+    assert bits[0] == 0x3C00
+    assert np.float16(v) != np.float16(1.0)  # the direct rounding would differ
+
+
+def test_quantize_saturates_fp16():
+    q, bits, sc = O.quantize(np.array([[1e6, -3e5]]), 4)
+    assert bits[0] == 0x7BFF and q[0, 0] == 7
+
+
+# ---------------------------------------------------------------- exact cases
+def test_exact_reconstruction_full_basis():
+    """P = C, unit weights, eps = 0, unquantized: every seed reproduces r exactly."""
+    rng = np.random.default_rng(6)
+    C = 16
+    R = rng.standard_normal((12, C))
+    D = np.ones((12, C))
+    p = O.Params(C=C, P=C, b=4, S=6, ridge_lambda=0.0)
+    enc = O.encode_tiles(R, D, p, quantize_coeffs=False, keep_all=True)
+    energy = np.sum(R * R, axis=1)
+    assert np.allclose(enc["all_gains"], energy[:, None], rtol=1e-12)
+    for t in range(12):
+        B = O.basis_matrix(0, int(enc["seed"][t]), C, C)
+        assert np.allclose(B @ enc["alpha"][t], R[t], atol=1e-12)
+
+
+def test_orthonormal_basis_quantized_parseval():
+    """P = C, unit weights, eps = 0: alpha* = B^T r, and the quantized gain is
+    |r|^2 - |alpha* - alpha_hat|^2 (Parseval for an orthonormal basis)."""
+    rng = np.random.default_rng(7)
+    C = 16
+    R = rng.standard_normal((40, C)) * 0.1
+    D = np.ones((40, C))
+    p = O.Params(C=C, P=C, b=3, S=5, ridge_lambda=0.0)
+    enc = O.encode_tiles(R, D, p, keep_all=True)
+    for s in range(5):
+        B = O.basis_matrix(0, s, C, C)
+        a_star = R @ B
+        q, bits, sc = O.quantize(a_star, 3)
+        want = np.sum(R * R, axis=1) - np.sum((a_star - sc[:, None] * q) ** 2, axis=1)
+        assert np.allclose(enc["all_gains"][:, s], want, rtol=1e-11, atol=1e-15)
+
+
+def test_ls_bound_and_zero_tile():
+    """eps = 0: no quantized reconstruction beats the least-squares optimum b^T G^-1 b;
+    an all-zero tile gives gain 0 for every seed and keeps seed 0 (lowest wins ties)."""
+    rng = np.random.default_rng(8)
+    R, D = _random_problem(rng, 64, 64)
+    R[5] = 0
+    p = O.Params(C=64, P=8, b=4, S=16, ridge_lambda=0.0)
+    enc = O.encode_tiles(R, D, p, keep_all=True)
+    for s in range(16):
+        B = O.basis_matrix(0, s, 64, 8)
+        alpha, G, b = O.fit(R, D, B, 0.0)
+        bound = np.einsum("np,np->n", alpha, b)
+        assert np.all(enc["all_gains"][:, s] <= bound * (1 + 1e-12) + 1e-30)
+    assert enc["seed"][5] == 0 and enc["gain"][5] == 0 and enc["scale"][5] == 0
+    assert np.all(enc["codes"][5] == 0)
+
+
+def test_tie_keeps_lowest_seed():
+    rng = np.random.default_rng(9)
+    R, D = _random_problem(rng, 10, 16)
+    B0 = O.basis_matrix(0, 0, 16, 2)
+    B1 = O.basis_matrix(0, 1, 16, 2)
+    enc = O.encode_tiles(R, D, O.Params(C=16, P=2, b=4, S=3), bases=[B1, B0, B1])
+    assert np.all(np.isin(enc["seed"], [0, 1]))
+
+
+# ---------------------------------------------------------------- brute force
+def _solve_small(G, b):
+    """Cramer's rule in plain Python for P <= 2."""
+    if len(b) == 1:
+        return [b[0] / G[0][0]]
+    det = G[0][0] * G[1][1] - G[0][1] * G[1][0]
+    return [(b[0] * G[1][1] - G[0][1] * b[1]) / det, (G[0][0] * b[1] - b[0] * G[1][0]) / det]
+
+
+def _brute_error(r, d, sigma, cols, lam, b):
+    C = len(r)
+    P = len(cols)
+    col = [[sigma[j] * (-1 if bin(j & c).count("1") % 2 else 1) / math.sqrt(C) for j in range(C)]
+           for c in cols]
+    eps = lam * sum(d) / C
+    G = [[sum(d[j] * col[p][j] * col[q][j] for j in range(C)) + (eps if p == q else 0.0)
+          for q in range(P)] for p in range(P)]
+    bb = [sum(d[j] * col[p][j] * r[j] for j in range(C)) for p in range(P)]
+    a = _solve_small(G, bb)
+    qmax = 2 ** (b - 1) - 1
+    m = max(abs(x) for x in a)
+    sc = float(np.float16(np.float32(m / qmax)))
+    q = [max(-qmax, min(qmax, round(x / sc))) for x in a] if sc > 0 else [0] * P
+    rhat = [sum(sc * q[p] * col[p][j] for p in range(P)) for j in range(C)]
+    return sum(d[j] * (r[j] - rhat[j]) ** 2 for j in range(C))
+
+
+@pytest.mark.parametrize("C,P", [(4, 1), (4, 2), (8, 2)])
+def test_brute_force_selection(C, P):
+    """Over an exhaustive basis set (every sign pattern x every ordered column
+    choice) the oracle's choice attains the minimum post-quantization weighted
+    error computed independently in plain Python."""
+    rng = np.random.default_rng(10 + C + P)
+    H = O.hadamard(C)
+    signs = list(itertools.product([1, -1], repeat=C))
+    if C == 8:
+        signs = signs[::5]
+    colsets = list(itertools.permutations(range(C), P))
+    combos = [(np.array(sg), list(cs)) for sg in signs for cs in colsets]
+    bases = [(sg[:, None] * H[:, cs]).astype(np.float64) / math.sqrt(C) for sg, cs in combos]
+    R, D = _random_problem(rng, 6, C)
+    lam = 1e-6
+    enc = O.encode_tiles(R, D, O.Params(C=C, P=P, b=3, S=len(bases), ridge_lambda=lam), bases=bases)
+    for t in range(6):
+        errs = [_brute_error(list(R[t]), list(D[t]), sg, cs, lam, 3) for sg, cs in combos]
+        best = min(errs)
+        chosen = errs[int(enc["seed"][t])]
+        energy = float(np.sum(D[t] * R[t] ** 2))
+        assert chosen <= best + 1e-12 * energy
+        assert abs((energy - chosen) - enc["gain"][t]) <= 1e-10 * energy
+
+
+# ---------------------------------------------------------------- accounting
+def test_paper_byte_accounting():
+    g = read_golden("paper_accounting.txt")
+    L, h, K = int(g["record_bytes"][0]), int(g["header_bytes"][0]), int(g["K"][0])
+    n_mod, N = int(g["n_modules"][0]), int(g["n_scope"][0])
+    C, P, b, S = (int(g[k][0]) for k in "CPbS")
+    assert h + L * K == int(g["sidecar_bytes"][0])
+    assert round(8 * (h + L * K) / N, 3) == float(g["delta_scope_bpw"][0])
+    T = N // C
+    p = O.Params(C=C, P=P, b=b, S=S, idx_bits=0)
+    assert O.index_bits(p, T) == 28
+    for b_e in range(1, 9):
+        assert O.record_bytes(p, T, scale_bits=b_e) == L
+    assert O.record_bytes(p, T, scale_bits=9) == L + 1
+    assert O.header_bytes(n_mod) == h
+    # the 4.23-bpw prefix: K records fit a budget of h + L*K bytes
+    assert O.prefix_K(h + L * K, h, L, 10 ** 9) == K
+    assert O.prefix_K(h + L * K + L - 1, h, L, 10 ** 9) == K
+
+
+def test_small_config_record_size():
+    # 32-bit index + 6-bit seed + 4x4-bit codes + 16-bit scale = 70 bits -> 9 bytes
+    assert O.record_bytes(O.Params(C=64, P=4, b=4, S=64), 1024) == 9
+    assert O.record_bytes(O.Params(C=64, P=8, b=4, S=256), 352256) == 11
+    assert O.record_bytes(O.Params(C=128, P=8, b=3, S=1024), 3809280) == 11
+    assert O.record_bytes(O.Params(C=64, P=8, b=4, S=512), 43352064) == 12
+
+
+def test_prefix_K_rules():
+    assert O.prefix_K(1327, 48, 9, 1000) == (1327 - 48) // 9
+    assert O.prefix_K(1327, 48, 9, 3) == 3
+    with pytest.raises(ValueError):
+        O.prefix_K(47, 48, 9, 10)
+    assert O.budget_bytes(0.162, 65536) == 1327
+
+
+# ---------------------------------------------------------------- records / stream
+def test_record_worked_example():
+    g = read_golden("rec_v1_example.txt")
+    rec = O.pack_record(int(g["idx"][0]), int(g["seed"][0]), [int(c) for c in g["codes"]],
+                        int(g["scale"][0], 16), 32, 6, 4, 9)
+    assert rec == bytes(int(x, 16) for x in g["bytes"])
+    assert O.unpack_record(rec, 32, 6, 4, 4) == (int(g["idx"][0]), 5, [1, -1, 7, -7], 0x3C00)
+
+
+@pytest.mark.parametrize("ib,S,P,b", [(32, 64, 4, 4), (28, 16, 4, 4), (32, 1024, 8, 3), (20, 65536, 16, 8),
+                                      (32, 2, 1, 2)])
+def test_record_round_trip_extremes(ib, S, P, b):
+    sb = O.seed_bits(S)
+    L = (ib + sb + P * b + 16 + 7) // 8
+    qmax = 2 ** (b - 1) - 1
+    for idx in (0, (1 << ib) - 1, 12345 % (1 << ib)):
+        for seed in (0, S - 1):
+            for codes in ([qmax] * P, [-qmax] * P, [(-1) ** i * (i % (qmax + 1)) for i in range(P)]):
+                for sc in (0x0001, 0x7BFF, 0x3C00, 0x0000):
+                    rec = O.pack_record(idx, seed, codes, sc, ib, sb, b, L)
+                    assert len(rec) == L
+                    assert O.unpack_record(rec, ib, sb, P, b) == (idx, seed, codes, sc)
+
+
+def test_stream_header_layout():
+    p = O.Params(C=16, P=4, b=4, S=16, basis_key=0x0123456789ABCDEF, idx_bits=0)
+    mods = [(2048, 11008)] * 108
+    hdr = O.stream_header(p, mods, per_module=False)
+    assert len(hdr) == 904
+    hd = O.parse_header(hdr)
+    # 28-bit index + 4-bit seed + 16 code bits + 16-bit fp16 scale = 64 bits; the
+    # paper's 7-byte record needs a scale exponent of at most 8 bits instead
+    assert hd["T_total"] == 108 * 2048 * 11008 // 16 and hd["L_rec"] == 8 and hd["basis_key"] == p.basis_key
+    assert hd["idx_bits"] == 28 and hd["seed_bits"] == 4 and hd["modules"][107] == (2048, 11008)
+
+
+def test_rank_order_ties_and_eligibility():
+    gain = np.array([0.5, 2.0, -1.0, 2.0, 0.0, 0.5, 3.0])
+    order = O.rank_order(gain, np.arange(7))
+    assert list(order) == [6, 1, 3, 0, 5]
+
+
+# ---------------------------------------------------------------- end to end
+def _small_module(seed=0, rows=8, cols=256, d_col=True):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((rows, cols)) * 0.02).astype(np.float32)
+    d = np.exp(rng.standard_normal(cols)) if d_col else np.exp(rng.standard_normal((rows, cols)))
+    return W, d
+
+
+def _encode_module(W, d, p):
+    codes, scale, zero, W0 = O.rtn_backbone(W)
+    R = O.residual(W, W0)
+    rows, cols = W.shape
+    enc = O.encode_tiles(O.tiles(R, p.C), O.tile_weights(d, rows, cols, p.C), p)
+    return W0, enc
+
+
+def test_prefix_decodability_every_prefix():
+    """Every record-boundary prefix decodes against the same W0: the weighted
+    error drops by exactly the listed gains, and the empty prefix is W0 itself."""
+    W, d = _small_module()
+    p = O.Params(C=64, P=4, b=4, S=16)
+    W0, enc = _encode_module(W, d, p)
+    stream, K, n_elig = O.build_stream(p, [W.shape], enc, bpw=8.0, per_module=False)
+    h = O.header_bytes(1)
+    L = O.record_bytes(p, enc["gain"].size)
+    assert K == n_elig and len(stream) == h + K * L
+    order = O.rank_order(enc["gain"], np.arange(enc["gain"].size))
+    e0 = O.weighted_error(W, W0.astype(np.float64), d)
+    prev = e0
+    for k in range(K + 1):
+        (What,) = O.decode_add(stream[:h + k * L], [W0])
+        if k == 0:
+            assert np.array_equal(What, W0.astype(np.float64))
+        e = O.weighted_error(W, What, d)
+        want = e0 - float(np.sum(enc["gain"][order[:k]]))
+        assert abs(e - want) <= 1e-9 * e0
+        assert e <= prev * (1 + 1e-12)
+        prev = e
+
+
+def test_per_module_quota_and_determinism():
+    p = O.Params(C=64, P=4, b=4, S=8)
+    mods, encs = [], []
+    for s in range(3):
+        W, d = _small_module(seed=s, rows=4 + 4 * s)
+        W0, enc = _encode_module(W, d, p)
+        mods.append(W.shape)
+        encs.append(enc)
+    cat = {k: np.concatenate([e[k] for e in encs]) for k in ("seed", "codes", "scale", "gain")}
+    s1, K, _ = O.build_stream(p, mods, cat, bpw=0.5, per_module=True)
+    s2, K2, _ = O.build_stream(p, mods, cat, bpw=0.5, per_module=True)
+    assert s1 == s2 and K == K2
+    L = O.record_bytes(p, sum(r * c // 64 for r, c in mods))
+    want = sum(min(int(np.sum(e["gain"] > 0)), O.budget_bytes(0.5, r * c) // L) for e, (r, c) in zip(encs, mods))
+    assert K == want and len(s1) == O.header_bytes(3) + K * L
+    # sections follow module order
+    hd = O.parse_header(s1)
+    idx = [O.unpack_record(s1[hd["h"] + i * L: hd["h"] + (i + 1) * L], 32, 3, 4, 4)[0] for i in range(K)]
+    mod_of = np.searchsorted(np.cumsum([r * c // 64 for r, c in mods]), idx, side="right")
+    assert np.all(np.diff(mod_of) >= 0)
+
+
+def test_encode_deterministic():
+    W, d = _small_module(seed=4, d_col=False)
+    p = O.Params(C=64, P=8, b=4, S=8)
+    a = _encode_module(W, d, p)[1]
+    b = _encode_module(W, d, p)[1]
+    for k in ("seed", "codes", "scale", "gain"):
+        assert np.array_equal(a[k], b[k])
