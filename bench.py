@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""One-GPU benchmark of the AWSRC codec hot path on MI355X.
+
+A step is one pass of the whole path over one synthetic module set already
+resident in HBM: RTN-INT4 backbone, encoder seed search over all tiles and
+seeds, gain ranking + serialization under the byte budget, and decode-add of
+the resulting stream onto W0.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload down3b]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "encoded tile-seed candidates/sec + decode-add GB/s (fraction of roofline), 1 GPU"
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+PEAK_VALU_TOPS = 78.6            # fp32 vector lane-ops/s (157.3 TFLOP/s counting FMA as 2)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def ops_per_candidate(C: int, P: int, per_element: bool) -> float:
+    """Algorithmic fp32 operations per (tile, seed): projection (cheapest of the
+    direct P*C form and a length-C fast Walsh-Hadamard transform), solve with a
+    precomputed factor, quantization and the coefficient-space score; per-element
+    weights add the Gram gather and a P x P Cholesky factorization."""
+    proj = min(P * C, C * int(math.log2(C)))
+    ops = proj + 2 * P * P + 6 * P + 9
+    if per_element:
+        ops += P * (P + 1) / 2 + P ** 3 / 6 + P * P / 2 + P / 3
+    return float(ops)
+
+
+def cpu_baseline(wl, inputs, seconds: float):
+    """The oracle as it stands, on a bounded sample of the same workload's tiles."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import awsrc_oracle as O
+
+    m = wl.modules[0]
+    W32 = inputs[0]["W32"].cpu().numpy()
+    d = inputs[0]["d"].cpu().numpy()
+    op = O.Params(C=wl.C, P=wl.P, b=wl.b, S=wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                  idx_bits=wl.idx_bits)
+    with threadpool_limits(limits=1):
+        _, _, _, W0o = O.rtn_backbone(W32)
+        R = O.tiles(O.residual(W32, W0o), wl.C)
+        D = O.tile_weights(d, m.rows, m.cols, wl.C)
+        n = 128
+        t0 = time.perf_counter()
+        O.encode_tiles(R[:n], D[:n], op)
+        t_pilot = time.perf_counter() - t0
+        n2 = int(min(R.shape[0], max(n, n * seconds / max(t_pilot, 1e-3))))
+        t0 = time.perf_counter()
+        O.encode_tiles(R[:n2], D[:n2], op)
+        dt = time.perf_counter() - t0
+    return {"value": n2 * wl.S / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n2} of {R.shape[0]} tiles of {m.name} ({m.rows}x{m.cols}), all {wl.S} seeds, "
+                      f"fp64 numpy, 1 thread, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="down3b")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        log("bench.py measures a single GPU: the codec has no cross-GPU step in this build "
+            "(run with --gpus 1)")
+        return 2
+
+    import torch
+
+    import paper_2608_23144_amd as awsrc
+    from synth import gen_module_inputs, workload
+
+    wl = workload(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                          idx_bits=wl.idx_bits)
+    mods = wl.modules
+    log(f"[bench] workload {wl.name}: {len(mods)} module(s), {wl.n_weights} weights, T={wl.n_tiles}, S={wl.S}")
+    inputs = [gen_module_inputs(wl, m, dev) for m in mods]
+    T = wl.n_tiles
+    seed = torch.empty(T, dtype=torch.int16, device=dev)
+    codes = torch.empty(T, wl.P, dtype=torch.int8, device=dev)
+    scale = torch.empty(T, dtype=torch.int16, device=dev)
+    gain = torch.empty(T, dtype=torch.float64, device=dev)
+    bb, enc_out, ws = [], [], []
+    off = 0
+    for m, inp in zip(mods, inputs):
+        t_m = m.rows * m.cols // wl.C
+        bb.append((torch.empty(m.rows, m.cols // 2, dtype=torch.uint8, device=dev),
+                   torch.empty(m.rows, m.cols // 128, dtype=torch.int16, device=dev),
+                   torch.empty(m.rows, m.cols // 128, dtype=torch.uint8, device=dev),
+                   torch.empty(m.rows, m.cols, dtype=torch.float32, device=dev)))
+        enc_out.append({"seed": seed[off:off + t_m], "codes": codes[off:off + t_m], "scale": scale[off:off + t_m],
+                        "gain": gain[off:off + t_m], "alpha": None})
+        d_mode = awsrc.AWSRC_D_PER_COL if inp["d"].dim() == 1 else awsrc.AWSRC_D_PER_ELEM
+        ws.append(torch.empty(awsrc.encode_workspace_bytes(p, inp["W"], d_mode), dtype=torch.uint8, device=dev))
+        off += t_m
+    shapes = [(m.rows, m.cols) for m in mods]
+    mode = awsrc.AWSRC_MODE_GLOBAL if wl.mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
+    bpw = max(wl.budgets)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    acc = {"backbone": 0.0, "encode": 0.0, "rank": 0.0, "decode_prepare": 0.0, "decode_apply": 0.0}
+    last = {}
+
+    def step(record: bool):
+        ev[0].record(stream)
+        for inp, b in zip(inputs, bb):
+            awsrc.awsrc_backbone_rtn(inp["W"], out=b)
+        ev[1].record(stream)
+        for inp, b, e, w in zip(inputs, bb, enc_out, ws):
+            awsrc.awsrc_encode_tiles(p, inp["W"], b[3], inp["d"], out=e, workspace=w)
+        ev[2].record(stream)
+        s, K, ne = awsrc.awsrc_rank_prefix(p, shapes, mode, bpw, seed, codes, scale, gain)
+        ev[3].record(stream)
+        plan, dws = awsrc.awsrc_decode_prepare(s, [b[3] for b in bb])
+        ev[4].record(stream)
+        awsrc.awsrc_decode_apply(plan)
+        ev[5].record(stream)
+        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), L=plan.L_rec)
+        if record:
+            torch.cuda.synchronize()
+            for k, (a, b) in zip(acc, zip(ev[:-1], ev[1:])):
+                acc[k] += a.elapsed_time(b)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
+    # wall clock over exactly K steps; stage events are read after each step
+    t_wall = 0.0
+    for _ in range(args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        step(True)
+        t_wall += time.perf_counter() - t0
+    ms_step = 1e3 * t_wall / args.steps
+    stage_ms = {k: v / args.steps for k, v in acc.items()}
+    cand = wl.candidates
+    value = cand / (ms_step / 1e3)
+
+    per_elem = wl.d_mode == "elem"
+    opc = ops_per_candidate(wl.C, wl.P, per_elem)
+    enc_s = stage_ms["encode"] / 1e3
+    achieved = cand * opc / enc_s / 1e12
+    K, L = last["K"], last["L"]
+    dec_bytes = K * (L + 2 * wl.C * 4)
+    dec_gbs = dec_bytes / (stage_ms["decode_apply"] / 1e3) / 1e9 if stage_ms["decode_apply"] > 0 else None
+    n_groups = wl.n_weights // 128
+    bb_bytes = wl.n_weights * (2 if wl.w_dtype == "bf16" else 4) + wl.n_weights // 2 + 3 * n_groups + 4 * wl.n_weights
+    bb_gbs = bb_bytes / (stage_ms["backbone"] / 1e3) / 1e9
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "modules": [f"{r}x{c}" for r, c in shapes], "C": wl.C, "P": wl.P,
+                   "b": wl.b, "S": wl.S, "weights": wl.d_mode, "mode": wl.mode, "bpw": bpw, "tiles": T,
+                   "candidates": cand},
+        "roofline": {"bound": "alu", "kernel": "awsrc_encode_tiles (basis, factors, screen, finalize)",
+                     "achieved": achieved, "peak": PEAK_VALU_TOPS, "unit": "Tops/s",
+                     "frac": achieved / PEAK_VALU_TOPS, "traffic": None,
+                     "ops_per_candidate": opc},
+        "encode_candidates_per_s": cand / enc_s,
+        "decode_add": {"records": K, "bytes": dec_bytes, "ms": stage_ms["decode_apply"], "GB/s": dec_gbs,
+                       "frac_hbm": (dec_gbs / PEAK_HBM_GBS) if dec_gbs else None},
+        "backbone": {"bytes": bb_bytes, "ms": stage_ms["backbone"], "GB/s": bb_gbs, "frac_hbm": bb_gbs / PEAK_HBM_GBS},
+        "stage_ms": stage_ms,
+        "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

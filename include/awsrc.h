@@ -1,0 +1,246 @@
+/*
+ * awsrc.h - C ABI of the AWSRC hot path on AMD Instinct MI355X (gfx950).
+ *
+ * AWSRC (activation-weighted seeded residual coding, arXiv 2608.23144) repairs
+ * a quantized weight matrix: the residual R = W - W0 left by a backbone
+ * quantizer (Eq. (1)) is cut into row-wise tiles of C input coordinates; for
+ * each tile and each seed s a seeded signed-Hadamard basis B_s (Eq. (2)) is
+ * fitted by activation-weighted ridge least squares (Eq. (3)), the P
+ * coefficients are rounded to b bits with one scale per tile, and the seed
+ * with the lowest post-quantization weighted error is kept (Sec. 3.2).
+ * Records are ranked by weighted-error reduction per serialized byte
+ * (Eq. (4), Sec. 3.3) and serialized as fixed-size records after a header
+ * (Eq. (5), Sec. 3.4); the decoder regenerates B_s and adds B_s alpha_hat onto
+ * W0 (Sec. 3.2).
+ *
+ * Conventions shared by every call:
+ *  - Pointers are DEVICE pointers (HIP device memory owned by the caller)
+ *    unless marked "host".  Matrices are row-major: rows = output features,
+ *    cols = input features; tiles run along cols.
+ *  - Work is enqueued on the caller's hipStream_t, passed as void* (NULL = the
+ *    null stream).  Calls return once the work is enqueued, except where a
+ *    call says it synchronizes.
+ *  - The library never allocates device memory.  Calls that need scratch
+ *    space take (workspace, ws_bytes): with workspace == NULL the call only
+ *    stores the required byte count in *ws_bytes and returns AWSRC_OK;
+ *    otherwise *ws_bytes must be at least that count.  The workspace must stay
+ *    valid until the enqueued work has finished.
+ *  - Every call returns an awsrc_status.  Nothing is launched when a call
+ *    returns an error found during argument validation.  awsrc_last_error()
+ *    returns a text description of the calling thread's last error.
+ *  - The library keeps no mutable global state besides that per-thread error
+ *    text, so calls on different streams may run concurrently provided their
+ *    buffers do not overlap.
+ *
+ * Conventions fixed where the paper leaves the choice open (the generator,
+ * scale format, tie rules, backbone recipe and byte layouts) are documented
+ * at the call that uses them.
+ */
+#ifndef AWSRC_H
+#define AWSRC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AWSRC_ABI_VERSION 1
+
+typedef int32_t awsrc_status;
+enum {
+  AWSRC_OK = 0,
+  AWSRC_EINVAL = -1,   /* bad shape, parameter or pointer                        */
+  AWSRC_ENOSPC = -2,   /* workspace or output capacity too small, budget < header */
+  AWSRC_ECORRUPT = -3, /* stream failed validation (nothing was written)          */
+  AWSRC_EDEVICE = -4   /* a HIP runtime call failed                               */
+};
+
+enum { AWSRC_DTYPE_F32 = 0, AWSRC_DTYPE_BF16 = 1 };
+enum { AWSRC_D_PER_COL = 0, AWSRC_D_PER_ELEM = 1 };
+enum { AWSRC_MODE_GLOBAL = 0, AWSRC_MODE_PER_MODULE = 1 };
+enum { AWSRC_SCALE_FP16 = 0 };
+
+/*
+ * Codec parameters (the (C, P, b, S) of Sec. 3.1 plus generator and ridge).
+ *  C            tile length: a power of two in 16..128.
+ *  P            basis columns per seed: 1..min(C, 16).
+ *  b            coefficient bits: 2..8; codes lie in [-(2^(b-1)-1), 2^(b-1)-1].
+ *  S            number of seeds: 2..65536.
+ *  scale_fmt    AWSRC_SCALE_FP16: one fp16 scale per tile,
+ *               scale = f16(f32(max_p |alpha*_p| / qmax)), both roundings to
+ *               nearest even, saturating at 65504.
+ *  idx_bits     width of the tile-index field: 1..32, or 0 for
+ *               ceil(log2 T_total) as in Eq. (5).
+ *  gen_version  1: B_s = diag(sigma_s) H_C[:, c_s] / sqrt(C) with H_C the
+ *               Sylvester Hadamard matrix in natural order and (sigma_s, c_s)
+ *               drawn from the splitmix64 counter stream keyed by basis_key
+ *               (word i of seed s is output s*2^32 + i; sign j is bit j%64 of
+ *               word j/64; column p maps word ceil(C/64)+p into [0, C-p) by the
+ *               multiply-shift of its high 32 bits and takes the m-th smallest
+ *               column not yet drawn).  Eq. (2) with the seeded coordinate
+ *               permutation of Sec. 3.1 left out.
+ *  reserved     must be 0.
+ *  basis_key    generator key, stored in the stream header.
+ *  ridge_lambda eps_t = ridge_lambda * mean_j d_{t,j} in Eq. (3); >= 0.
+ */
+typedef struct awsrc_params {
+  int32_t C, P, b, S;
+  int32_t scale_fmt;
+  int32_t idx_bits;
+  int32_t gen_version;
+  int32_t reserved;
+  uint64_t basis_key;
+  double ridge_lambda;
+} awsrc_params;
+
+int32_t awsrc_abi_version(void);
+const char* awsrc_last_error(void);
+
+/*
+ * Backbone quantizer W0 = Q(W) of Eq. (1): asymmetric RTN-INT4 with groups of
+ * `group` consecutive input columns (Sec. 4: RTN with group size 128).
+ * fp32 arithmetic, correctly rounded, per group:
+ *   s32 = (max - min) / 15; s16 = f16(s32) saturating; s = f32(s16);
+ *   z = clamp(rint(-min / s), 0, 15); q = clamp(rint(w / s) + z, 0, 15);
+ *   W0 = f32(q - z) * s.   A group with s16 == 0 stores s16 = 1, z = 0, q = 0.
+ *  W          [rows, cols] fp32 or bf16 (w_dtype).
+ *  group      64, 128 or 256; cols % group == 0.
+ *  codes      [rows, cols/2] u8, even column in the low nibble.
+ *  scale_f16  [rows, cols/group] fp16 bit patterns.
+ *  zero       [rows, cols/group] u8.
+ *  W0_or_null [rows, cols] fp32 dequantized backbone, or NULL to skip.
+ */
+awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, int64_t cols,
+                                int32_t group, uint8_t* codes, uint16_t* scale_f16, uint8_t* zero,
+                                float* W0_or_null, void* stream);
+
+/*
+ * Encoder seed search (Sec. 3.2, Eq. (2)-(4) numerator) for every tile of one
+ * module.  Tile t = row * (cols / C) + block holds r_t = f32(W - W0) over
+ * columns [block*C, block*C + C) of that row and coordinate weights d_t.  For
+ * every seed the encoder fits Eq. (3), quantizes the coefficients, and scores
+ * gain = sum_j d_j (r_j^2 - (r_j - rhat_j)^2); it keeps the seed with the
+ * largest gain, the lowest seed winning exact ties.  All S seeds are screened
+ * in fp32; the seeds whose screened gain lies close to the best are re-scored
+ * in fp64 and the outputs come from that fp64 pass.
+ *  W        [rows, cols] fp32 or bf16 (w_dtype); W0 [rows, cols] fp32.
+ *  d        AWSRC_D_PER_COL: [cols] activation second moments shared by all
+ *           rows; AWSRC_D_PER_ELEM: [rows, cols] per-element weights.  d > 0.
+ *  cols % C == 0.  T = rows * cols / C.
+ *  seed_out [T] u16, code_out [T, P] i8, scale_out [T] fp16 bits,
+ *  gain_out [T] f64 (weighted error reduction of the stored record; an
+ *  all-zero record has gain 0), alpha_or_null [T, P] fp32 unquantized fit of
+ *  the chosen seed, or NULL.
+ *  Workspace: two-phase query as described above.
+ */
+awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_dtype,
+                                const float* W0, int64_t rows, int64_t cols, const float* d,
+                                int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                                uint16_t* scale_out, double* gain_out, float* alpha_or_null,
+                                void* workspace, size_t* ws_bytes, void* stream);
+
+/*
+ * Byte-budgeted, gain-ranked record selection and serialization (Eq. (4),
+ * Sec. 3.3, Eq. (5)).  The per-tile encoder outputs of n_modules modules are
+ * given concatenated in module order (global tile index = tiles of earlier
+ * modules + local tile index).  Records with gain > 0 are eligible and are
+ * ordered by decreasing gain (= decreasing rho, the record size being fixed),
+ * ties by the lower global tile index.
+ *  AWSRC_MODE_GLOBAL (P variant): budget = floor(bpw_budget * N / 8) bytes
+ *    with N the total weight count; K = min(eligible, (budget - h) / L_rec);
+ *    budget < h gives AWSRC_ENOSPC.  Every record-boundary prefix of the
+ *    stream is itself the stream of a smaller budget.
+ *  AWSRC_MODE_PER_MODULE (U variant): module m keeps
+ *    min(eligible_m, floor(bpw_budget * N_m / 8) / L_rec) records; sections
+ *    follow module order; the header is counted once, globally.
+ * Stream layout (little-endian): a header of h = 40 + 8 * n_modules bytes
+ *   magic "AWSR" | version u16 = 1 | flags u16 (bits 0-3 gen_version, 4-7
+ *   scale_fmt, bit 8 per-module mode) | C u16 | P u8 | b u8 | S u32 |
+ *   idx_bits u8 | seed_bits u8 | scale_bits u8 | L_rec u8 | basis_key u64 |
+ *   T_total u64 | n_modules u32 | then rows u32, cols u32 per module,
+ * followed by K records of L_rec = ceil((idx_bits + ceil(log2 S) + P*b + 16)/8)
+ * bytes: one LSB-first bit stream of tile index, seed, P two's-complement
+ * b-bit codes and the fp16 scale bits, zero padded.
+ *  module_rows, module_cols  host arrays [n_modules]; cols % C == 0.
+ *  stream_out     device buffer of stream_cap bytes; stream_cap < h + K*L_rec
+ *                 gives AWSRC_ENOSPC.
+ *  stream_len, K, n_eligible  host outputs (n_eligible may be NULL).
+ * This call synchronizes with `stream` (it returns K).
+ */
+awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modules,
+                               const int64_t* module_rows, const int64_t* module_cols,
+                               int32_t mode, double bpw_budget, const uint16_t* seed,
+                               const int8_t* code, const uint16_t* scale, const double* gain,
+                               uint8_t* stream_out, uint64_t stream_cap, uint64_t* stream_len,
+                               int64_t* K, int64_t* n_eligible, void* workspace, size_t* ws_bytes,
+                               void* stream);
+
+/*
+ * Decoder (Sec. 3.2): for each record of a stream (or of any record-boundary
+ * prefix of one, Sec. 3.3) regenerate B_s from the header's basis key and add
+ * B_s (scale * q) onto that tile of W0, in place.  Tiles without a record are
+ * not touched; an empty stream leaves W0 bit-identical.
+ *
+ * awsrc_decode_add = awsrc_decode_prepare + awsrc_decode_apply.
+ *  stream_bytes  device pointer to stream_len bytes; K = (stream_len - h) / L_rec.
+ *  W0_ptrs       host array [n_modules] of device pointers to each module's
+ *                W0, [rows, cols] in w0_dtype; bf16 targets are rounded to
+ *                nearest even after the fp32 add.
+ *  rows, cols    host arrays [n_modules]; must match the stream header.
+ * The header and every record are validated before anything is written (magic,
+ * version, parameters, length on a record boundary, tile index < T_total,
+ * seed < S, codes within +-qmax, finite non-negative scale, no tile twice); a
+ * failure returns AWSRC_ECORRUPT and leaves W0 unchanged.  This call
+ * synchronizes with `stream` (to read the header and the validation result).
+ */
+awsrc_status awsrc_decode_add(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,
+                              void* const* W0_ptrs, const int64_t* rows, const int64_t* cols,
+                              int32_t w0_dtype, void* workspace, size_t* ws_bytes, void* stream);
+
+/* Host-side description of a validated stream, filled by awsrc_decode_prepare. */
+typedef struct awsrc_decode_plan {
+  int32_t C, P, b, S;
+  int32_t idx_bits, seed_bits, L_rec, n_modules;
+  int32_t w0_dtype, reserved;
+  int64_t K;
+  uint64_t T_total;
+  uint64_t h;
+  const uint8_t* records;   /* device pointer to the first record */
+  void* workspace;          /* the workspace the plan's tables live in */
+} awsrc_decode_plan;
+
+/*
+ * Validation half of awsrc_decode_add: reads and checks the header, checks
+ * every record on the device, and builds the basis, module and pointer tables
+ * in the workspace (two-phase size query as above; the query itself reads the
+ * header and so synchronizes).  Synchronizes with `stream`.  On AWSRC_OK the
+ * plan and workspace stay valid for any number of awsrc_decode_apply calls as
+ * long as the stream bytes, the workspace and the W0 buffers are unchanged.
+ */
+awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,
+                                  void* const* W0_ptrs, const int64_t* rows, const int64_t* cols,
+                                  int32_t w0_dtype, awsrc_decode_plan* plan, void* workspace,
+                                  size_t* ws_bytes, void* stream);
+
+/*
+ * Apply half of awsrc_decode_add: one asynchronous kernel launch that adds
+ * every record of a prepared stream onto W0 (each call adds again).
+ */
+awsrc_status awsrc_decode_apply(const awsrc_decode_plan* plan, void* stream);
+
+/* Host-only helpers (no device needed). */
+/* L_rec in bytes for T_total tiles; -1 if p is invalid. */
+int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total);
+/* h = 40 + 8 * n_modules; -1 if n_modules < 1. */
+int64_t awsrc_header_bytes(int32_t n_modules);
+/* floor(bpw * n_weights / 8) in IEEE double; -1 on invalid input. */
+int64_t awsrc_budget_bytes(double bpw, int64_t n_weights);
+/* min(n_eligible, (budget_bytes - h) / L_rec); AWSRC_ENOSPC if budget < h, -1 on bad input. */
+int64_t awsrc_prefix_K(int64_t budget_bytes, int64_t h, int64_t L_rec, int64_t n_eligible);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AWSRC_H */

@@ -1,0 +1,408 @@
+// extern "C" entry points of libawsrc: argument validation, workspace layout
+// and kernel orchestration.  Every step of the codec itself runs in the HIP
+// kernels of basis.hip, backbone.hip, encode*.hip, rank.hip and decode.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "awsrc_internal.h"
+
+using namespace awsrc;
+
+namespace {
+
+thread_local std::string g_err;
+
+awsrc_status fail(awsrc_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess) return fail(AWSRC_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+int ceil_log2_u64(uint64_t n) {
+  int b = 0;
+  while (b < 64 && (1ull << b) < n) ++b;
+  return b;
+}
+
+bool pow2_c(int C) { return C == 16 || C == 32 || C == 64 || C == 128; }
+
+awsrc_status check_params(const awsrc_params* p) {
+  if (!p) return fail(AWSRC_EINVAL, "params is NULL");
+  if (!pow2_c(p->C)) return fail(AWSRC_EINVAL, "C=%d: must be 16, 32, 64 or 128", p->C);
+  if (p->P < 1 || p->P > kMaxP || p->P > p->C) return fail(AWSRC_EINVAL, "P=%d out of range 1..min(C,16)", p->P);
+  if (p->b < 2 || p->b > 8) return fail(AWSRC_EINVAL, "b=%d out of range 2..8", p->b);
+  if (p->S < 2 || p->S > 65536) return fail(AWSRC_EINVAL, "S=%d out of range 2..65536", p->S);
+  if (p->scale_fmt != AWSRC_SCALE_FP16) return fail(AWSRC_EINVAL, "scale_fmt=%d unsupported", p->scale_fmt);
+  if (p->idx_bits < 0 || p->idx_bits > 32) return fail(AWSRC_EINVAL, "idx_bits=%d out of range 0..32", p->idx_bits);
+  if (p->gen_version != 1) return fail(AWSRC_EINVAL, "gen_version=%d unsupported", p->gen_version);
+  if (p->reserved != 0) return fail(AWSRC_EINVAL, "reserved field must be 0");
+  if (!(p->ridge_lambda >= 0.0) || !isfinite(p->ridge_lambda)) return fail(AWSRC_EINVAL, "ridge_lambda must be finite and >= 0");
+  return AWSRC_OK;
+}
+
+int index_bits(const awsrc_params* p, uint64_t T_total) {
+  return p->idx_bits ? p->idx_bits : ceil_log2_u64(T_total);
+}
+
+int64_t rec_bytes(int ib, int S, int P, int b) {
+  return (ib + ceil_log2_u64((uint64_t)S) + P * b + 16 + 7) / 8;
+}
+
+void put_le(std::vector<uint8_t>& v, uint64_t x, int n) {
+  for (int i = 0; i < n; ++i) v.push_back((uint8_t)(x >> (8 * i)));
+}
+uint64_t get_le(const uint8_t* p, int n) {
+  uint64_t x = 0;
+  for (int i = 0; i < n; ++i) x |= (uint64_t)p[i] << (8 * i);
+  return x;
+}
+
+constexpr int kHeaderFixed = 40;
+
+}  // namespace
+
+extern "C" int32_t awsrc_abi_version(void) { return AWSRC_ABI_VERSION; }
+extern "C" const char* awsrc_last_error(void) { return g_err.c_str(); }
+
+extern "C" int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total) {
+  if (check_params(p) != AWSRC_OK || T_total < 1) return -1;
+  return rec_bytes(index_bits(p, (uint64_t)T_total), p->S, p->P, p->b);
+}
+
+extern "C" int64_t awsrc_header_bytes(int32_t n_modules) {
+  return n_modules < 1 ? -1 : kHeaderFixed + 8 * (int64_t)n_modules;
+}
+
+extern "C" int64_t awsrc_budget_bytes(double bpw, int64_t n_weights) {
+  if (!(bpw >= 0.0) || !isfinite(bpw) || n_weights < 0) return -1;
+  return (int64_t)floor((bpw * (double)n_weights) / 8.0);
+}
+
+extern "C" int64_t awsrc_prefix_K(int64_t budget_bytes, int64_t h, int64_t L_rec, int64_t n_eligible) {
+  if (h < 0 || L_rec < 1 || n_eligible < 0) return -1;
+  if (budget_bytes < h) return AWSRC_ENOSPC;
+  const int64_t k = (budget_bytes - h) / L_rec;
+  return k < n_eligible ? k : n_eligible;
+}
+
+// ---------------------------------------------------------------- backbone
+extern "C" awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, int64_t cols,
+                                           int32_t group, uint8_t* codes, uint16_t* scale_f16,
+                                           uint8_t* zero, float* W0_or_null, void* stream) {
+  if (w_dtype != AWSRC_DTYPE_F32 && w_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w_dtype %d", w_dtype);
+  if (group != 64 && group != 128 && group != 256) return fail(AWSRC_EINVAL, "group=%d: must be 64, 128 or 256", group);
+  if (rows < 0 || cols < 1 || cols % group) return fail(AWSRC_EINVAL, "cols=%lld must be a positive multiple of group", (long long)cols);
+  if (rows == 0) return AWSRC_OK;
+  if (!W || !codes || !scale_f16 || !zero) return fail(AWSRC_EINVAL, "NULL buffer");
+  HIPCHK(launch_backbone(W, w_dtype, rows, cols, group, codes, scale_f16, zero, W0_or_null,
+                         (hipStream_t)stream));
+  return AWSRC_OK;
+}
+
+// ---------------------------------------------------------------- encode
+extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_dtype,
+                                           const float* W0, int64_t rows, int64_t cols, const float* d,
+                                           int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                                           uint16_t* scale_out, double* gain_out, float* alpha_or_null,
+                                           void* workspace, size_t* ws_bytes, void* stream) {
+  awsrc_status st = check_params(p);
+  if (st) return st;
+  if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
+  if (w_dtype != AWSRC_DTYPE_F32 && w_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w_dtype %d", w_dtype);
+  if (d_mode != AWSRC_D_PER_COL && d_mode != AWSRC_D_PER_ELEM) return fail(AWSRC_EINVAL, "bad d_mode %d", d_mode);
+  if (rows < 0 || cols < 1 || cols % p->C) return fail(AWSRC_EINVAL, "cols=%lld must be a positive multiple of C=%d", (long long)cols, p->C);
+  if (!encode_supported(p->C, p->P)) return fail(AWSRC_EINVAL, "unsupported (C, P)");
+  const int64_t nb = cols / p->C;
+  const int64_t T = rows * nb;
+  if (T > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "too many tiles in one module");
+  const int PB = p->P <= 4 ? 4 : (p->P <= 8 ? 8 : 16);
+  const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
+  const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
+  const size_t b_tg = align_up((size_t)T * kTop * 4, 256);
+  const size_t b_ts = align_up((size_t)T * kTop * 2, 256);
+  const size_t need = b_basis + b_fac + b_tg + b_ts + 256;
+  if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
+  if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
+  if (T == 0) return AWSRC_OK;
+  if (!W || !W0 || !d || !seed_out || !code_out || !scale_out || !gain_out) return fail(AWSRC_EINVAL, "NULL buffer");
+  char* ws = static_cast<char*>(workspace);
+  ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(ws), 256));
+  EncodeArgs a{};
+  a.W = W; a.w_dtype = w_dtype; a.W0 = W0; a.d = d; a.d_mode = d_mode;
+  a.rows = rows; a.cols = cols; a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
+  a.lambda = p->ridge_lambda;
+  a.basis = carve_basis(ws, p->S, p->P);
+  ws += b_basis;
+  a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
+  ws += b_fac;
+  a.top_gain = reinterpret_cast<float*>(ws);
+  ws += b_tg;
+  a.top_seed = reinterpret_cast<uint16_t*>(ws);
+  a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
+  a.alpha_out = alpha_or_null;
+  hipStream_t s = (hipStream_t)stream;
+  HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, a.basis, s));
+  if (d_mode == AWSRC_D_PER_COL) HIPCHK(launch_col_factors(a, s));
+  HIPCHK(launch_encode_screen(a, s));
+  HIPCHK(launch_encode_finalize(a, s));
+  return AWSRC_OK;
+}
+
+// ---------------------------------------------------------------- rank + serialize
+extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modules,
+                                          const int64_t* module_rows, const int64_t* module_cols,
+                                          int32_t mode, double bpw_budget, const uint16_t* seed,
+                                          const int8_t* code, const uint16_t* scale, const double* gain,
+                                          uint8_t* stream_out, uint64_t stream_cap, uint64_t* stream_len,
+                                          int64_t* K_out, int64_t* n_eligible, void* workspace,
+                                          size_t* ws_bytes, void* stream) {
+  awsrc_status st = check_params(p);
+  if (st) return st;
+  if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
+  if (n_modules < 1 || !module_rows || !module_cols) return fail(AWSRC_EINVAL, "bad module table");
+  if (mode != AWSRC_MODE_GLOBAL && mode != AWSRC_MODE_PER_MODULE) return fail(AWSRC_EINVAL, "bad mode %d", mode);
+  if (!(bpw_budget >= 0.0) || !isfinite(bpw_budget)) return fail(AWSRC_EINVAL, "bpw_budget must be finite and >= 0");
+  std::vector<int64_t> toff(n_modules + 1, 0);
+  int64_t N = 0;
+  for (int m = 0; m < n_modules; ++m) {
+    const int64_t r = module_rows[m], c = module_cols[m];
+    if (r < 1 || c < 1 || c % p->C) return fail(AWSRC_EINVAL, "module %d: shape %lldx%lld invalid for C=%d", m, (long long)r, (long long)c, p->C);
+    if (r > UINT32_MAX || c > UINT32_MAX) return fail(AWSRC_EINVAL, "module %d too large for the header", m);
+    toff[m + 1] = toff[m] + r * (c / p->C);
+    N += r * c;
+  }
+  const int64_t T_total = toff[n_modules];
+  if (T_total > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "more than 2^32 tiles");
+  const int ib = index_bits(p, (uint64_t)T_total);
+  if (ib < 32 && (uint64_t)T_total > (1ull << ib)) return fail(AWSRC_EINVAL, "idx_bits=%d cannot address %lld tiles", ib, (long long)T_total);
+  const int sb = ceil_log2_u64((uint64_t)p->S);
+  const int64_t L = rec_bytes(ib, p->S, p->P, p->b);
+  if (L > 255) return fail(AWSRC_EINVAL, "record too large");
+  const int64_t h = kHeaderFixed + 8 * (int64_t)n_modules;
+
+  // per-segment record caps from the byte budget
+  std::vector<int64_t> seg_t0, seg_n, seg_cap;
+  if (mode == AWSRC_MODE_GLOBAL) {
+    const int64_t budget = awsrc_budget_bytes(bpw_budget, N);
+    if (budget < h) return fail(AWSRC_ENOSPC, "budget %lld bytes < header %lld bytes", (long long)budget, (long long)h);
+    seg_t0.push_back(0); seg_n.push_back(T_total); seg_cap.push_back((budget - h) / L);
+  } else {
+    for (int m = 0; m < n_modules; ++m) {
+      seg_t0.push_back(toff[m]);
+      seg_n.push_back(toff[m + 1] - toff[m]);
+      seg_cap.push_back(awsrc_budget_bytes(bpw_budget, module_rows[m] * module_cols[m]) / L);
+    }
+  }
+  size_t max_n = 0, max_k = 0;
+  for (size_t i = 0; i < seg_n.size(); ++i) {
+    const int64_t k = seg_cap[i] < seg_n[i] ? seg_cap[i] : seg_n[i];
+    if ((size_t)seg_n[i] > max_n) max_n = (size_t)seg_n[i];
+    if ((size_t)k > max_k) max_k = (size_t)k;
+  }
+  const size_t need = 256 + 256 + rank_ws_bytes(max_n, max_k);
+  if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
+  if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
+  if (!seed || !code || !scale || !gain || !stream_out || !stream_len || !K_out) return fail(AWSRC_EINVAL, "NULL buffer");
+  if (stream_cap < (uint64_t)h) return fail(AWSRC_ENOSPC, "stream capacity below the header size");
+
+  char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
+  uint64_t* counter = reinterpret_cast<uint64_t*>(ws);
+  const RankWs rw = carve_rank(ws + 256, max_n, max_k);
+  hipStream_t s = (hipStream_t)stream;
+
+  int64_t K_total = 0, elig_total = 0;
+  for (size_t i = 0; i < seg_n.size(); ++i) {
+    HIPCHK(hipMemsetAsync(counter, 0, 8, s));
+    HIPCHK(launch_count_eligible(gain + seg_t0[i], seg_n[i], counter, s));
+    uint64_t ne = 0;
+    HIPCHK(hipMemcpyAsync(&ne, counter, 8, hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    const int64_t k = (int64_t)ne < seg_cap[i] ? (int64_t)ne : seg_cap[i];
+    elig_total += (int64_t)ne;
+    if ((uint64_t)(h + (K_total + k) * L) > stream_cap) return fail(AWSRC_ENOSPC, "stream capacity %llu < %lld bytes", (unsigned long long)stream_cap, (long long)(h + (K_total + k) * L));
+    if (k > 0) {
+      HIPCHK(launch_select_sorted(gain, seg_t0[i], seg_n[i], k, rw, s));
+      HIPCHK(launch_pack(rw.vals_a, k, seed, code, scale, p->P, p->b, ib, sb, (int)L,
+                         stream_out + h + K_total * L, s));
+    }
+    K_total += k;
+  }
+  // header: fixed fields, then the module table
+  std::vector<uint8_t> hdr;
+  hdr.reserve(h);
+  hdr.push_back('A'); hdr.push_back('W'); hdr.push_back('S'); hdr.push_back('R');
+  put_le(hdr, 1, 2);
+  put_le(hdr, (uint64_t)(p->gen_version & 0xF) | ((uint64_t)(p->scale_fmt & 0xF) << 4) |
+                  ((mode == AWSRC_MODE_PER_MODULE ? 1ull : 0ull) << 8), 2);
+  put_le(hdr, (uint64_t)p->C, 2);
+  put_le(hdr, (uint64_t)p->P, 1);
+  put_le(hdr, (uint64_t)p->b, 1);
+  put_le(hdr, (uint64_t)p->S, 4);
+  put_le(hdr, (uint64_t)ib, 1);
+  put_le(hdr, (uint64_t)sb, 1);
+  put_le(hdr, 16, 1);
+  put_le(hdr, (uint64_t)L, 1);
+  put_le(hdr, p->basis_key, 8);
+  put_le(hdr, (uint64_t)T_total, 8);
+  put_le(hdr, (uint64_t)n_modules, 4);
+  for (int m = 0; m < n_modules; ++m) {
+    put_le(hdr, (uint64_t)module_rows[m], 4);
+    put_le(hdr, (uint64_t)module_cols[m], 4);
+  }
+  HIPCHK(hipMemcpyAsync(stream_out, hdr.data(), hdr.size(), hipMemcpyHostToDevice, s));
+  HIPCHK(hipStreamSynchronize(s));
+  *stream_len = (uint64_t)(h + K_total * L);
+  *K_out = K_total;
+  if (n_eligible) *n_eligible = elig_total;
+  return AWSRC_OK;
+}
+
+// ---------------------------------------------------------------- decode
+namespace {
+
+struct DecodeLayout {
+  size_t basis, bitmap, err, off, cols, ptr, total;
+};
+
+DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod) {
+  DecodeLayout l;
+  l.basis = align_up(basis_bytes(S, P), 256);
+  l.bitmap = align_up((size_t)((T_total + 31) / 32) * 4, 256);
+  l.err = 256;
+  l.off = align_up((size_t)(nmod + 1) * 8, 256);
+  l.cols = align_up((size_t)nmod * 8, 256);
+  l.ptr = align_up((size_t)nmod * 8, 256);
+  l.total = 256 + l.basis + l.bitmap + l.err + l.off + l.cols + l.ptr;
+  return l;
+}
+
+DecodeArgs decode_args(const awsrc_decode_plan* pl) {
+  const DecodeLayout l = decode_layout(pl->S, pl->P, pl->T_total, (uint32_t)pl->n_modules);
+  char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(pl->workspace), 256));
+  DecodeArgs a{};
+  a.recs = pl->records;
+  a.K = pl->K;
+  a.C = pl->C; a.P = pl->P; a.b = pl->b; a.S = pl->S;
+  a.idx_bits = pl->idx_bits; a.seed_bits = pl->seed_bits; a.L_rec = pl->L_rec;
+  a.T_total = pl->T_total;
+  a.n_modules = pl->n_modules;
+  a.w0_dtype = pl->w0_dtype;
+  a.basis = carve_basis(ws, pl->S, pl->P);
+  ws += l.basis;
+  a.bitmap = reinterpret_cast<uint32_t*>(ws); ws += l.bitmap;
+  a.errors = reinterpret_cast<unsigned long long*>(ws); ws += l.err;
+  a.mod_tile_off = reinterpret_cast<const uint64_t*>(ws); ws += l.off;
+  a.mod_cols = reinterpret_cast<const int64_t*>(ws); ws += l.cols;
+  a.mod_ptr = reinterpret_cast<void* const*>(ws);
+  return a;
+}
+
+}  // namespace
+
+extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,
+                                             void* const* W0_ptrs, const int64_t* rows, const int64_t* cols,
+                                             int32_t w0_dtype, awsrc_decode_plan* plan, void* workspace,
+                                             size_t* ws_bytes, void* stream) {
+  if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
+  if (!stream_bytes) return fail(AWSRC_EINVAL, "stream is NULL");
+  if (n_modules < 1 || !rows || !cols) return fail(AWSRC_EINVAL, "bad module table");
+  if (w0_dtype != AWSRC_DTYPE_F32 && w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w0_dtype %d", w0_dtype);
+  if (stream_len < (uint64_t)kHeaderFixed) return fail(AWSRC_ECORRUPT, "stream shorter than a header");
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t fx[kHeaderFixed];
+  HIPCHK(hipMemcpyAsync(fx, stream_bytes, kHeaderFixed, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  if (memcmp(fx, "AWSR", 4) != 0) return fail(AWSRC_ECORRUPT, "bad magic");
+  if (get_le(fx + 4, 2) != 1) return fail(AWSRC_ECORRUPT, "unsupported stream version");
+  const uint32_t flags = (uint32_t)get_le(fx + 6, 2);
+  const int C = (int)get_le(fx + 8, 2), P = fx[10], b = fx[11];
+  const int64_t S = (int64_t)get_le(fx + 12, 4);
+  const int ib = fx[16], sb = fx[17], scb = fx[18], L = fx[19];
+  const uint64_t key = get_le(fx + 20, 8);
+  const uint64_t T_total = get_le(fx + 28, 8);
+  const uint32_t nmod = (uint32_t)get_le(fx + 36, 4);
+  if ((flags & 0xF) != 1 || ((flags >> 4) & 0xF) != AWSRC_SCALE_FP16 || (flags & ~0x1FFu)) return fail(AWSRC_ECORRUPT, "bad flags 0x%x", flags);
+  if (!pow2_c(C) || P < 1 || P > kMaxP || P > C || b < 2 || b > 8 || S < 2 || S > 65536)
+    return fail(AWSRC_ECORRUPT, "bad codec parameters in header");
+  if (sb != ceil_log2_u64((uint64_t)S) || scb != 16 || ib > 32 || (ib == 0 && T_total > 1))
+    return fail(AWSRC_ECORRUPT, "bad field widths in header");
+  if (L != rec_bytes(ib, (int)S, P, b)) return fail(AWSRC_ECORRUPT, "record size %d inconsistent with header", L);
+  if ((int32_t)nmod != n_modules) return fail(AWSRC_ECORRUPT, "header has %u modules, caller %d", nmod, n_modules);
+  const uint64_t h = kHeaderFixed + 8ull * nmod;
+  if (stream_len < h) return fail(AWSRC_ECORRUPT, "stream shorter than its header");
+  if ((stream_len - h) % (uint64_t)L) return fail(AWSRC_ECORRUPT, "stream does not end on a record boundary");
+  std::vector<uint8_t> mt(8 * (size_t)nmod);
+  HIPCHK(hipMemcpyAsync(mt.data(), stream_bytes + kHeaderFixed, mt.size(), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  std::vector<uint64_t> toff(nmod + 1, 0);
+  std::vector<int64_t> mcols(nmod);
+  for (uint32_t m = 0; m < nmod; ++m) {
+    const int64_t r = (int64_t)get_le(&mt[8 * m], 4), c = (int64_t)get_le(&mt[8 * m + 4], 4);
+    if (r != rows[m] || c != cols[m]) return fail(AWSRC_ECORRUPT, "module %u shape %lldx%lld differs from caller's", m, (long long)r, (long long)c);
+    if (c % C) return fail(AWSRC_ECORRUPT, "module %u cols not a multiple of C", m);
+    toff[m + 1] = toff[m] + (uint64_t)r * (uint64_t)(c / C);
+    mcols[m] = c;
+  }
+  if (toff[nmod] != T_total) return fail(AWSRC_ECORRUPT, "T_total inconsistent with the module table");
+  if (ib < 32 && T_total > (1ull << ib)) return fail(AWSRC_ECORRUPT, "index field too narrow");
+  const int64_t K = (int64_t)((stream_len - h) / (uint64_t)L);
+  const DecodeLayout lay = decode_layout((int)S, P, T_total, nmod);
+  if (!workspace) { *ws_bytes = lay.total; return AWSRC_OK; }
+  if (*ws_bytes < lay.total) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, lay.total);
+  if (!plan) return fail(AWSRC_EINVAL, "plan is NULL");
+  if (!W0_ptrs) return fail(AWSRC_EINVAL, "W0_ptrs is NULL");
+  for (int m = 0; m < n_modules; ++m)
+    if (!W0_ptrs[m]) return fail(AWSRC_EINVAL, "W0 pointer %d is NULL", m);
+
+  awsrc_decode_plan pl{};
+  pl.C = C; pl.P = P; pl.b = b; pl.S = (int32_t)S;
+  pl.idx_bits = ib; pl.seed_bits = sb; pl.L_rec = L; pl.n_modules = (int32_t)nmod;
+  pl.w0_dtype = w0_dtype;
+  pl.K = K; pl.T_total = T_total; pl.h = h;
+  pl.records = stream_bytes + h;
+  pl.workspace = workspace;
+  const DecodeArgs a = decode_args(&pl);
+  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), toff.data(), (nmod + 1) * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(const_cast<int64_t*>(a.mod_cols), mcols.data(), nmod * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(const_cast<void**>(a.mod_ptr), W0_ptrs, nmod * sizeof(void*), hipMemcpyHostToDevice, s));
+  HIPCHK(launch_gen_basis(key, C, P, (int)S, a.basis, s));
+  HIPCHK(launch_decode_validate(a, s));
+  unsigned long long nerr = 0;
+  HIPCHK(hipMemcpyAsync(&nerr, a.errors, 8, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  if (nerr) return fail(AWSRC_ECORRUPT, "%llu invalid or duplicate records", nerr);
+  *plan = pl;
+  return AWSRC_OK;
+}
+
+extern "C" awsrc_status awsrc_decode_apply(const awsrc_decode_plan* plan, void* stream) {
+  if (!plan || !plan->workspace) return fail(AWSRC_EINVAL, "plan is NULL or not prepared");
+  if (plan->K == 0) return AWSRC_OK;
+  HIPCHK(launch_decode_apply(decode_args(plan), (hipStream_t)stream));
+  return AWSRC_OK;
+}
+
+extern "C" awsrc_status awsrc_decode_add(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,
+                                         void* const* W0_ptrs, const int64_t* rows, const int64_t* cols,
+                                         int32_t w0_dtype, void* workspace, size_t* ws_bytes, void* stream) {
+  awsrc_decode_plan plan{};
+  awsrc_status st = awsrc_decode_prepare(stream_bytes, stream_len, n_modules, W0_ptrs, rows, cols, w0_dtype,
+                                         &plan, workspace, ws_bytes, stream);
+  if (st != AWSRC_OK || !workspace) return st;
+  return awsrc_decode_apply(&plan, stream);
+}

@@ -1,0 +1,140 @@
+// Internal declarations shared by the AWSRC HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/awsrc.h"
+
+namespace awsrc {
+
+constexpr int kMaxP = 16;        // basis columns per seed
+constexpr int kMaxC = 128;       // tile length
+constexpr int kTop = 4;          // screened candidates kept per tile for the fp64 re-score
+
+// splitmix64 (Steele, Lea & Flood 2014): output n of the stream started at
+// state `key`; the state advances by the golden-ratio increment before each
+// output, which then passes through the variant-13 mixer.
+__host__ __device__ __forceinline__ uint64_t splitmix64(uint64_t key, uint64_t n) {
+  uint64_t z = key + (n + 1ull) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Device tables of the S seeded bases (generator version 1):
+//   sign[s][w]      sign words, bit j%64 of word j/64 set <=> sigma_j = -1
+//   mask[s][p][w]   bit j set <=> B_s[j, p] < 0, i.e. sigma_j xor parity(j & c_p)
+//   col[s][p]       the P selected Hadamard columns (draw order)
+struct BasisTables {
+  uint64_t* sign;
+  uint64_t* mask;
+  uint8_t* col;
+};
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+inline size_t basis_bytes(int S, int P) {
+  return align_up((size_t)S * 2 * 8, 256) + align_up((size_t)S * P * 2 * 8, 256) +
+         align_up((size_t)S * kMaxP, 256);
+}
+
+inline BasisTables carve_basis(void* base, int S, int P) {
+  char* p = static_cast<char*>(base);
+  BasisTables t;
+  t.sign = reinterpret_cast<uint64_t*>(p);
+  p += align_up((size_t)S * 2 * 8, 256);
+  t.mask = reinterpret_cast<uint64_t*>(p);
+  p += align_up((size_t)S * P * 2 * 8, 256);
+  t.col = reinterpret_cast<uint8_t*>(p);
+  return t;
+}
+
+// Number of floats per (column block, seed) entry of the per-column factor
+// table: packed lower Cholesky factor of G = B^T D B + eps I, the reciprocal
+// diagonal, and eps.
+inline int colfac_stride(int P) {
+  int n = P * (P + 1) / 2 + P + 1;
+  return (n + 3) & ~3;
+}
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipSuccess or the first HIP error.
+hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, BasisTables t, hipStream_t st);
+
+hipError_t launch_backbone(const void* W, int w_dtype, int64_t rows, int64_t cols, int group,
+                           uint8_t* codes, uint16_t* scale, uint8_t* zero, float* W0,
+                           hipStream_t st);
+
+struct EncodeArgs {
+  const void* W;
+  int w_dtype;
+  const float* W0;
+  const float* d;
+  int d_mode;
+  int64_t rows, cols;
+  int C, P, b, S;
+  double lambda;
+  BasisTables basis;
+  float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
+  float* top_gain;     // [T][kTop] screened gains, descending
+  uint16_t* top_seed;  // [T][kTop]
+  uint16_t* seed_out;
+  int8_t* code_out;
+  uint16_t* scale_out;
+  double* gain_out;
+  float* alpha_out;
+};
+
+bool encode_supported(int C, int P);
+hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st);
+hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);
+hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- ranking
+struct RankWs {
+  uint64_t* keys_a;      // [cap] sort keys (ping)
+  uint64_t* keys_b;      // [cap] (pong)
+  uint32_t* vals_a;      // [cap] global tile index (ping)
+  uint32_t* vals_b;      // [cap]
+  uint32_t* hist;        // [256 * max_blocks] digit-major block histograms / offsets
+  uint64_t* blk_a;       // [max_blocks + 1] per-block counts / offsets
+  uint64_t* blk_b;       // [max_blocks + 1]
+  uint64_t* state;       // select state: prefix, mask, remaining, eligible count, hist[256]
+  size_t cap;
+  size_t max_blocks;
+};
+size_t rank_ws_bytes(size_t n_tiles, size_t k_cap);
+RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap);
+
+hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st);
+// Stable top-K of one tile segment, ordered by (gain desc, tile asc); writes
+// the global tile indices of the K records into ws.vals_a[0..K).
+hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
+                                const RankWs& ws, hipStream_t st);
+hipError_t launch_pack(const uint32_t* tiles, int64_t K, const uint16_t* seed, const int8_t* code,
+                       const uint16_t* scale, int P, int b, int idx_bits, int seed_bits,
+                       int L_rec, uint8_t* out, hipStream_t st);
+
+// ---------------------------------------------------------------- decoding
+struct DecodeArgs {
+  const uint8_t* recs;   // first record
+  int64_t K;
+  int C, P, b, S;
+  int idx_bits, seed_bits, L_rec;
+  uint64_t T_total;
+  int n_modules;
+  const uint64_t* mod_tile_off;  // [n_modules + 1]
+  const int64_t* mod_cols;       // [n_modules]
+  void* const* mod_ptr;          // [n_modules] device pointers
+  int w0_dtype;
+  BasisTables basis;
+  uint32_t* bitmap;              // [ceil(T_total / 32)]
+  unsigned long long* errors;    // [1]
+};
+hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st);
+hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st);
+
+}  // namespace awsrc

@@ -1,0 +1,499 @@
+// Encoder seed search (Sec. 3.2): for every tile r_t and every seed s, fit the
+// activation-weighted ridge least squares of Eq. (3) in the basis B_s of
+// Eq. (2), quantize the coefficients with one fp16 scale, and score the
+// weighted error reduction of the quantized reconstruction (numerator of
+// Eq. (4)); keep the seed with the largest reduction.
+//
+// Two passes share one set of tables:
+//  * screen   - every (tile, seed) in fp32, one lane per tile; the seed loop
+//               is uniform across the wavefront, so basis patterns and the
+//               per-column factors are scalar loads.  The four best screened
+//               seeds of each tile are kept.
+//  * finalize - the screened seeds whose fp32 gain lies within a small margin
+//               of the best are re-scored in fp64 with the complete chain
+//               (projection, Gram matrix, Cholesky solve, quantization,
+//               gain in its definition form); outputs come from that pass.
+//
+// Identities used (they follow from B_s having orthonormal +-1/sqrt(C)
+// columns of a Sylvester Hadamard matrix):
+//  * G = B^T D B has entries (1/C) sum_j d_j (-1)^popcount(j & (c_p xor c_q)),
+//    independent of the sign pattern, so for per-column weights G and its
+//    Cholesky factor depend only on (column block, seed);
+//  * for per-element weights G_pq = WHT(d_t)[c_p xor c_q] / C, one fast
+//    Walsh-Hadamard transform of d_t per tile;
+//  * sum_j d_j (r_j^2 - (r_j - [B a]_j)^2) = 2 a^T b - a^T G0 a with
+//    b = B^T D r and G0 = B^T D B (screening only).
+#include <math.h>
+
+#include "awsrc_internal.h"
+
+namespace awsrc {
+
+namespace {
+
+template <int C>
+struct InvSqrtC;
+template <> struct InvSqrtC<16> { static constexpr float v = 0.25f; };
+template <> struct InvSqrtC<32> { static constexpr float v = 0.17677669529663688f; };
+template <> struct InvSqrtC<64> { static constexpr float v = 0.125f; };
+template <> struct InvSqrtC<128> { static constexpr float v = 0.08838834764831845f; };
+
+__device__ __forceinline__ float load_w_any(const void* W, int dt, int64_t i) {
+  if (dt == AWSRC_DTYPE_F32) return static_cast<const float*>(W)[i];
+  return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
+}
+
+__device__ __forceinline__ int tri(int p, int q) { return p * (p + 1) / 2 + q; }
+
+// fp16 scale of Sec. 3.2: f16(f32(v)) with saturation at 65504; returns bits.
+__device__ __forceinline__ uint16_t scale_bits_from_f32(float v) {
+  uint16_t hb = __half_as_ushort(__float2half_rn(v));
+  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;
+  return hb;
+}
+
+// In-register fast Walsh-Hadamard transform, natural (Sylvester) order.
+template <int C, typename T>
+__device__ __forceinline__ void fwht(T (&v)[C]) {
+#pragma unroll
+  for (int h = 1; h < C; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < C; i += 2 * h)
+#pragma unroll
+      for (int k = i; k < i + h; ++k) {
+        const T x = v[k], y = v[k + h];
+        v[k] = x + y;
+        v[k + h] = x - y;
+      }
+}
+
+}  // namespace
+
+// ----------------------------------------------------------------------------
+// Per-column factor table: for each (column block, seed), G = B^T D B + eps I
+// in fp64, its Cholesky factor stored in fp32 for the screen:
+//   [packed lower L (PB(PB+1)/2)] [1/L_pp (PB)] [eps]
+// Padding columns p >= P get an identity row so that the padded system solves
+// to alpha_p = 0.
+template <int C, int PB>
+__global__ void k_col_factors(EncodeArgs a, int nb, int stride) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= nb * a.S) return;
+  const int blk = idx / a.S;
+  const int s = idx - blk * a.S;
+  const float* dblk = a.d + (int64_t)blk * C;
+  const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
+  double sumd = 0.0;
+  for (int j = 0; j < C; ++j) sumd += (double)dblk[j];
+  const double eps = a.lambda * (sumd / C);
+  double G[PB][PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p)
+#pragma unroll
+    for (int q = 0; q <= p; ++q) {
+      double g;
+      if (p < a.P && q < a.P) {
+        const int x = cs[p] ^ cs[q];
+        double acc = 0.0;
+        for (int j = 0; j < C; ++j) acc += (__popc((unsigned)(j & x)) & 1) ? -(double)dblk[j] : (double)dblk[j];
+        g = acc / C + (p == q ? eps : 0.0);
+      } else {
+        g = (p == q) ? 1.0 : 0.0;
+      }
+      G[p][q] = g;
+    }
+  // Cholesky (G is SPD: d > 0 and the columns are orthonormal)
+  double L[PB][PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p)
+#pragma unroll
+    for (int q = 0; q <= p; ++q) {
+      double acc = G[p][q];
+#pragma unroll
+      for (int k = 0; k < q; ++k) acc -= L[p][k] * L[q][k];
+      if (p == q) L[p][p] = sqrt(fmax(acc, 1e-300));
+      else L[p][q] = acc / L[q][q];
+    }
+  float* out = a.colfac + (size_t)idx * stride;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+#pragma unroll
+    for (int q = 0; q <= p; ++q) out[tri(p, q)] = (float)L[p][q];
+    out[PB * (PB + 1) / 2 + p] = (float)(1.0 / L[p][p]);
+  }
+  out[PB * (PB + 1) / 2 + PB] = (float)eps;
+}
+
+// ----------------------------------------------------------------------------
+// fp32 screen of all seeds.  Wavefront = 64 consecutive rows of one column
+// block; lane = tile.  Keeps the kTop best (gain, seed) per tile, ties to the
+// lower seed.
+template <int C, int PB, bool PE>
+__global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
+  const int nb = (int)(a.cols / C);
+  const int blk = blockIdx.x % nb;
+  const int64_t row = (int64_t)(blockIdx.x / nb) * 64 + threadIdx.x;
+  const bool active = row < a.rows;
+  const int64_t rr = active ? row : a.rows - 1;
+  const int64_t off = rr * a.cols + (int64_t)blk * C;
+  const int P = a.P;
+  float u[C];
+  float wd[PE ? C : 1];
+#pragma unroll
+  for (int j = 0; j < C; ++j) {
+    const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
+    const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
+    u[j] = dj * r;
+    if constexpr (PE) wd[j] = dj;
+  }
+  if constexpr (PE) fwht<C>(wd);
+  const float qmax = (float)((1 << (a.b - 1)) - 1);
+  const float inv_qmax = 1.0f / qmax;
+  const float invC = 1.0f / C;
+  float tg[kTop];
+  int ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+
+  for (int s = 0; s < a.S; ++s) {
+    // projection b = B_s^T (d .* r)
+    float bv[PB];
+    const uint64_t* mk = a.basis.mask + (size_t)s * P * 2;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      float acc = 0.0f;
+      if (p < P) {
+        const uint64_t m0 = mk[2 * p], m1 = mk[2 * p + 1];
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+          const uint64_t m = (j < 64) ? m0 : m1;
+          acc += ((m >> (j & 63)) & 1ull) ? -u[j] : u[j];
+        }
+      }
+      bv[p] = acc * InvSqrtC<C>::v;
+    }
+    // Cholesky factor of G = B^T D B + eps I
+    float L[PB][PB], inv[PB], eps;
+    if constexpr (PE) {
+      const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
+      int c[PB];
+#pragma unroll
+      for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
+      eps = (float)a.lambda * wd[0] * invC;
+#pragma unroll
+      for (int p = 0; p < PB; ++p)
+#pragma unroll
+        for (int q = 0; q <= p; ++q) {
+          float acc;
+          if (p < P && q < P) acc = wd[c[p] ^ c[q]] * invC + (p == q ? eps : 0.0f);
+          else acc = (p == q) ? 1.0f : 0.0f;
+#pragma unroll
+          for (int k = 0; k < q; ++k) acc -= L[p][k] * L[q][k];
+          if (p == q) {
+            L[p][p] = sqrtf(fmaxf(acc, 1e-30f));
+            inv[p] = 1.0f / L[p][p];
+          } else {
+            L[p][q] = acc * inv[q];
+          }
+        }
+    } else {
+      const float* f = a.colfac + ((size_t)blk * a.S + s) * stride;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) {
+#pragma unroll
+        for (int q = 0; q <= p; ++q) L[p][q] = f[tri(p, q)];
+        inv[p] = f[PB * (PB + 1) / 2 + p];
+      }
+      eps = f[PB * (PB + 1) / 2 + PB];
+    }
+    // solve L L^T alpha = b
+    float z[PB], al[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      float acc = bv[p];
+#pragma unroll
+      for (int k = 0; k < p; ++k) acc -= L[p][k] * z[k];
+      z[p] = acc * inv[p];
+    }
+#pragma unroll
+    for (int p = PB - 1; p >= 0; --p) {
+      float acc = z[p];
+#pragma unroll
+      for (int k = p + 1; k < PB; ++k) acc -= L[k][p] * al[k];
+      al[p] = acc * inv[p];
+    }
+    // quantize with one fp16 scale and score
+    float m = 0.0f;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
+    const float sc = __half2float(__ushort_as_half(scale_bits_from_f32(m * inv_qmax)));
+    float g = 0.0f;
+    if (sc > 0.0f) {
+      const float isc = 1.0f / sc;
+      float q[PB], t1 = 0.0f, qq = 0.0f;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) {
+        q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+        t1 += q[p] * bv[p];
+        qq += q[p] * q[p];
+      }
+      float quad = 0.0f;
+#pragma unroll
+      for (int k = 0; k < PB; ++k) {
+        float y = 0.0f;
+#pragma unroll
+        for (int i = k; i < PB; ++i) y += L[i][k] * q[i];
+        quad += y * y;
+      }
+      quad -= eps * qq;
+      g = sc * (2.0f * t1 - sc * quad);
+    }
+    // keep the best kTop, earlier (lower) seeds first among equals
+    float cg = g;
+    int cs_ = s;
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      if (cg > tg[k]) {
+        const float tgk = tg[k];
+        const int tsk = ts[k];
+        tg[k] = cg; ts[k] = cs_;
+        cg = tgk; cs_ = tsk;
+      }
+    }
+  }
+  if (active) {
+    const int64_t t = row * nb + blk;
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      a.top_gain[t * kTop + k] = tg[k];
+      a.top_seed[t * kTop + k] = (uint16_t)ts[k];
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// fp64 re-score of the screened candidates; writes the encoder outputs.
+template <int C, int PB, bool PE>
+__global__ __launch_bounds__(64) void k_finalize(EncodeArgs a) {
+  const int nb = (int)(a.cols / C);
+  const int blk = blockIdx.x % nb;
+  const int64_t row = (int64_t)(blockIdx.x / nb) * 64 + threadIdx.x;
+  if (row >= a.rows) return;
+  const int64_t off = row * a.cols + (int64_t)blk * C;
+  const int64_t t = row * nb + blk;
+  const int P = a.P;
+  float r[C], dd[C];
+  float e32 = 0.0f;
+  double sumd = 0.0;
+#pragma unroll
+  for (int j = 0; j < C; ++j) {
+    r[j] = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
+    dd[j] = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
+    e32 += dd[j] * r[j] * r[j];
+    sumd += (double)dd[j];
+  }
+  const double eps = a.lambda * (sumd / C);
+  const double isq = 1.0 / sqrt((double)C);
+  const int qmax = (1 << (a.b - 1)) - 1;
+
+  float tg[kTop];
+  int ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) { tg[k] = a.top_gain[t * kTop + k]; ts[k] = a.top_seed[t * kTop + k]; }
+  const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
+
+  double best_g = -INFINITY;
+  int best_s = 0x7FFFFFFF;
+  int best_q[PB];
+  uint16_t best_bits = 0;
+  double best_al[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) { best_q[p] = 0; best_al[p] = 0.0; }
+
+  for (int k = 0; k < kTop; ++k) {
+    if (k > 0 && !(tg[k] >= thr)) continue;
+    if (!(tg[k] > -INFINITY) && k > 0) continue;
+    const int s = ts[k];
+    const uint64_t* mk = a.basis.mask + (size_t)s * P * 2;
+    const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
+    double bv[PB];
+    double G[PB][PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      double acc = 0.0;
+      if (p < P) {
+        const uint64_t m0 = mk[2 * p], m1 = mk[2 * p + 1];
+        for (int j = 0; j < C; ++j) {
+          const double uj = (double)dd[j] * (double)r[j];
+          const uint64_t m = (j < 64) ? m0 : m1;
+          acc += ((m >> (j & 63)) & 1ull) ? -uj : uj;
+        }
+      }
+      bv[p] = acc * isq;
+    }
+#pragma unroll
+    for (int p = 0; p < PB; ++p)
+#pragma unroll
+      for (int q = 0; q <= p; ++q) {
+        double g;
+        if (p < P && q < P) {
+          const int x = cs[p] ^ cs[q];
+          double acc = 0.0;
+          for (int j = 0; j < C; ++j) acc += (__popc((unsigned)(j & x)) & 1) ? -(double)dd[j] : (double)dd[j];
+          g = acc / C + (p == q ? eps : 0.0);
+        } else {
+          g = (p == q) ? 1.0 : 0.0;
+        }
+        G[p][q] = g;
+      }
+    // Cholesky solve in fp64
+    double L[PB][PB], z[PB], al[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p)
+#pragma unroll
+      for (int q = 0; q <= p; ++q) {
+        double acc = G[p][q];
+#pragma unroll
+        for (int kk = 0; kk < q; ++kk) acc -= L[p][kk] * L[q][kk];
+        if (p == q) L[p][p] = sqrt(fmax(acc, 1e-300));
+        else L[p][q] = acc / L[q][q];
+      }
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      double acc = bv[p];
+#pragma unroll
+      for (int kk = 0; kk < p; ++kk) acc -= L[p][kk] * z[kk];
+      z[p] = acc / L[p][p];
+    }
+#pragma unroll
+    for (int p = PB - 1; p >= 0; --p) {
+      double acc = z[p];
+#pragma unroll
+      for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
+      al[p] = acc / L[p][p];
+    }
+    // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
+    double m = 0.0;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
+    uint16_t bits = 0;
+    double sc = 0.0;
+    if (m > 0.0) {
+      bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
+      sc = (double)__half2float(__ushort_as_half(bits));
+      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
+    }
+    int q[PB];
+    double ah[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      double qv = 0.0;
+      if (sc > 0.0) qv = fmin(fmax(rint(al[p] / sc), (double)-qmax), (double)qmax);
+      q[p] = (int)qv;
+      ah[p] = sc * qv;
+    }
+    // gain in its definition form: sum_j d_j (r_j^2 - (r_j - rhat_j)^2)
+    double gsum = 0.0;
+    for (int j = 0; j < C; ++j) {
+      double rh = 0.0;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) {
+        if (p < P) {
+          const uint64_t mm = (j < 64) ? mk[2 * p] : mk[2 * p + 1];
+          const double bjp = ((mm >> (j & 63)) & 1ull) ? -isq : isq;
+          rh += bjp * ah[p];
+        }
+      }
+      const double rj = (double)r[j];
+      const double e = rj - rh;
+      gsum += (double)dd[j] * (rj * rj - e * e);
+    }
+    if (gsum > best_g || (gsum == best_g && s < best_s)) {
+      best_g = gsum;
+      best_s = s;
+      best_bits = bits;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = al[p]; }
+    }
+  }
+  a.seed_out[t] = (uint16_t)best_s;
+  a.scale_out[t] = best_bits;
+  a.gain_out[t] = best_g;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    if (p < P) {
+      a.code_out[t * P + p] = (int8_t)best_q[p];
+      if (a.alpha_out) a.alpha_out[t * P + p] = (float)best_al[p];
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+static int pad_p(int P) { return P <= 4 ? 4 : (P <= 8 ? 8 : 16); }
+
+bool encode_supported(int C, int P) {
+  return (C == 16 || C == 32 || C == 64 || C == 128) && P >= 1 && P <= kMaxP && P <= C;
+}
+
+template <int C, int PB>
+static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
+  const int nb = (int)(a.cols / C);
+  const int n = nb * a.S;
+  hipLaunchKernelGGL((k_col_factors<C, PB>), dim3((n + 63) / 64), dim3(64), 0, st, a, nb,
+                     colfac_stride(PB));
+  return hipGetLastError();
+}
+
+template <int C, int PB>
+static hipError_t run_screen(const EncodeArgs& a, hipStream_t st) {
+  const int nb = (int)(a.cols / C);
+  const int64_t waves = nb * ((a.rows + 63) / 64);
+  if (a.d_mode == AWSRC_D_PER_ELEM)
+    hipLaunchKernelGGL((k_screen_valu<C, PB, true>), dim3((unsigned)waves), dim3(64), 0, st, a,
+                       colfac_stride(PB));
+  else
+    hipLaunchKernelGGL((k_screen_valu<C, PB, false>), dim3((unsigned)waves), dim3(64), 0, st, a,
+                       colfac_stride(PB));
+  return hipGetLastError();
+}
+
+template <int C, int PB>
+static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
+  const int nb = (int)(a.cols / C);
+  const int64_t waves = nb * ((a.rows + 63) / 64);
+  if (a.d_mode == AWSRC_D_PER_ELEM)
+    hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)waves), dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)waves), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+#define AWSRC_DISPATCH(FN, a, st)                                       \
+  do {                                                                  \
+    const int pb_ = pad_p((a).P);                                       \
+    switch ((a).C) {                                                    \
+      case 16:                                                          \
+        if (pb_ == 4) return FN<16, 4>(a, st);                          \
+        if (pb_ == 8) return FN<16, 8>(a, st);                          \
+        return FN<16, 16>(a, st);                                       \
+      case 32:                                                          \
+        if (pb_ == 4) return FN<32, 4>(a, st);                          \
+        if (pb_ == 8) return FN<32, 8>(a, st);                          \
+        return FN<32, 16>(a, st);                                       \
+      case 64:                                                          \
+        if (pb_ == 4) return FN<64, 4>(a, st);                          \
+        if (pb_ == 8) return FN<64, 8>(a, st);                          \
+        return FN<64, 16>(a, st);                                       \
+      case 128:                                                         \
+        if (pb_ == 4) return FN<128, 4>(a, st);                         \
+        if (pb_ == 8) return FN<128, 8>(a, st);                         \
+        return FN<128, 16>(a, st);                                      \
+      default: return hipErrorInvalidValue;                             \
+    }                                                                   \
+  } while (0)
+
+hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_factors, a, st); }
+hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_screen, a, st); }
+hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_finalize, a, st); }
+
+}  // namespace awsrc

@@ -1,0 +1,408 @@
+// Gain-ranked record selection and serialization (Eq. (4), Sec. 3.3, Eq. (5)).
+//
+// With a fixed record size, ordering by rho_t = gain_t / L_rec is ordering by
+// gain.  The positive fp64 gains are mapped to their IEEE bit patterns, which
+// order like the values.  For a segment of tiles and a record count K:
+//  1. radix select (8 passes of 8 bits, most significant first) finds the K-th
+//     largest key k* and how many records equal to k* are taken;
+//  2. a stable compaction keeps every key > k* and the first such equal keys
+//     in tile order (so equal gains keep the lower tile index);
+//  3. a stable least-significant-digit radix sort of the K survivors by
+//     decreasing key leaves equal keys in increasing tile order;
+//  4. records are bit-packed at fixed offsets h + i * L_rec.
+#include "awsrc_internal.h"
+
+namespace awsrc {
+
+constexpr int kThreads = 256;
+constexpr int kRounds = 16;
+constexpr int kItems = kThreads * kRounds;  // items per block in compaction and sorting
+
+__device__ __forceinline__ uint64_t gain_key(double g) {
+  return g > 0.0 ? (uint64_t)__double_as_longlong(g) : 0ull;
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int lane = threadIdx.x & 63;
+  return lane ? (~0ull >> (64 - lane)) : 0ull;
+}
+
+// Exclusive block scan of a 0/1 flag over kThreads threads; returns the
+// exclusive prefix for this thread and the block total in *total.
+__device__ __forceinline__ uint32_t block_scan_flag(bool f, uint32_t* sh_w, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const uint64_t bal = __ballot(f);
+  const uint32_t in_wave = __popcll(bal & lanemask_lt());
+  if (lane == 0) sh_w[w] = __popcll(bal);
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < kThreads / 64; ++k) {
+    const uint32_t c = sh_w[k];
+    before += (k < w) ? c : 0u;
+    tot += c;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + in_wave;
+}
+
+// ---------------------------------------------------------------- eligibility
+__global__ void k_count_eligible(const double* __restrict__ gain, int64_t n, uint64_t* counter) {
+  uint32_t c = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    c += gain[i] > 0.0 ? 1u : 0u;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
+  if ((threadIdx.x & 63) == 0 && c) atomicAdd((unsigned long long*)counter, (unsigned long long)c);
+}
+
+hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st) {
+  int64_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_count_eligible, dim3((unsigned)blocks), dim3(kThreads), 0, st, gain, n,
+                     counter);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- radix select
+// state: [0] prefix, [1] mask, [2] remaining, [3] unused, [4..260) histogram
+__global__ void k_select_init(uint64_t* state, int64_t K) {
+  const int t = threadIdx.x;
+  if (t == 0) { state[0] = 0; state[1] = 0; state[2] = (uint64_t)K; state[3] = 0; }
+  state[4 + t] = 0;
+}
+
+__global__ void k_select_hist(const double* __restrict__ gain, int64_t n, uint64_t* state,
+                              int shift) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const uint64_t prefix = state[0], mask = state[1];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = gain_key(gain[i]);
+    if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd((unsigned long long*)&state[4 + threadIdx.x], (unsigned long long)h[threadIdx.x]);
+}
+
+__global__ void k_select_pick(uint64_t* state, int shift) {
+  if (threadIdx.x == 0) {
+    uint64_t cum = 0;
+    const uint64_t rem = state[2];
+    for (int bin = 255; bin >= 0; --bin) {
+      const uint64_t c = state[4 + bin];
+      if (cum + c >= rem) {
+        state[0] |= (uint64_t)bin << shift;
+        state[1] |= 255ull << shift;
+        state[2] = rem - cum;
+        break;
+      }
+      cum += c;
+    }
+  }
+  __syncthreads();
+  state[4 + threadIdx.x] = 0;
+}
+
+// ---------------------------------------------------------------- compaction
+__global__ __launch_bounds__(kThreads) void k_compact_count(const double* __restrict__ gain, int64_t n,
+                                                            const uint64_t* __restrict__ state,
+                                                            uint64_t* blk_gt, uint64_t* blk_eq) {
+  const uint64_t kstar = state[0];
+  uint32_t gt = 0, eq = 0;
+  const int64_t base = (int64_t)blockIdx.x * kItems;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t i = base + r * kThreads + threadIdx.x;
+    if (i < n) {
+      const uint64_t k = gain_key(gain[i]);
+      gt += k > kstar;
+      eq += k == kstar;
+    }
+  }
+  __shared__ uint32_t s_gt[kThreads / 64], s_eq[kThreads / 64];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    gt += __shfl_xor(gt, off, 64);
+    eq += __shfl_xor(eq, off, 64);
+  }
+  if ((threadIdx.x & 63) == 0) { s_gt[threadIdx.x >> 6] = gt; s_eq[threadIdx.x >> 6] = eq; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t a = 0, b = 0;
+    for (int k = 0; k < kThreads / 64; ++k) { a += s_gt[k]; b += s_eq[k]; }
+    blk_gt[blockIdx.x] = a;
+    blk_eq[blockIdx.x] = b;
+  }
+}
+
+// Single block: eq offsets (exclusive scan of blk_eq) and selected offsets.
+// On exit blk_gt[b] = first output slot of block b, blk_eq[b] = number of
+// equal keys in earlier blocks.
+__global__ __launch_bounds__(1024) void k_compact_scan(uint64_t* blk_gt, uint64_t* blk_eq, int64_t nblk,
+                                                       const uint64_t* __restrict__ state) {
+  __shared__ uint64_t sh[1024];
+  const uint64_t rem = state[2];
+  uint64_t carry_eq = 0, carry_sel = 0;
+  for (int64_t c0 = 0; c0 < nblk; c0 += 1024) {
+    const int64_t i = c0 + threadIdx.x;
+    const uint64_t gt = i < nblk ? blk_gt[i] : 0, eq = i < nblk ? blk_eq[i] : 0;
+    // inclusive scan of eq
+    sh[threadIdx.x] = eq;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const uint64_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
+      __syncthreads();
+      sh[threadIdx.x] += v;
+      __syncthreads();
+    }
+    const uint64_t eq_excl = carry_eq + sh[threadIdx.x] - eq;
+    const uint64_t eq_tot = sh[1023];
+    __syncthreads();
+    uint64_t take_eq = 0;
+    if (rem > eq_excl) take_eq = (rem - eq_excl) < eq ? (rem - eq_excl) : eq;
+    const uint64_t sel = gt + take_eq;
+    sh[threadIdx.x] = sel;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const uint64_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
+      __syncthreads();
+      sh[threadIdx.x] += v;
+      __syncthreads();
+    }
+    const uint64_t sel_excl = carry_sel + sh[threadIdx.x] - sel;
+    const uint64_t sel_tot = sh[1023];
+    __syncthreads();
+    if (i < nblk) { blk_gt[i] = sel_excl; blk_eq[i] = eq_excl; }
+    carry_eq += eq_tot;
+    carry_sel += sel_tot;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_compact_write(const double* __restrict__ gain, int64_t t0, int64_t n,
+                                                            const uint64_t* __restrict__ state,
+                                                            const uint64_t* __restrict__ sel_off,
+                                                            const uint64_t* __restrict__ eq_off,
+                                                            uint64_t* __restrict__ keys_out,
+                                                            uint32_t* __restrict__ vals_out) {
+  __shared__ uint32_t sh_w[kThreads / 64];
+  const uint64_t kstar = state[0];
+  const uint64_t rem = state[2];
+  uint64_t eq_run = eq_off[blockIdx.x];
+  uint64_t sel_run = sel_off[blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * kItems;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t i = base + r * kThreads + threadIdx.x;
+    uint64_t k = 0;
+    if (i < n) k = gain_key(gain[i]);
+    const bool gt = (i < n) && k > kstar;
+    const bool eq = (i < n) && k == kstar;
+    uint32_t eq_tot, sel_tot;
+    const uint32_t eq_rank = block_scan_flag(eq, sh_w, &eq_tot);
+    const bool take = gt || (eq && (eq_run + eq_rank) < rem);
+    const uint32_t pos = block_scan_flag(take, sh_w, &sel_tot);
+    if (take) {
+      keys_out[sel_run + pos] = ~k;  // ascending ~key = descending gain
+      vals_out[sel_run + pos] = (uint32_t)(t0 + i);
+    }
+    eq_run += eq_tot;
+    sel_run += sel_tot;
+  }
+}
+
+// ---------------------------------------------------------------- LSD radix sort
+__global__ __launch_bounds__(kThreads) void k_sort_hist(const uint64_t* __restrict__ keys, int64_t n, int shift,
+                                                        uint32_t* __restrict__ hist, int64_t nblk) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kItems;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t i = base + r * kThreads + threadIdx.x;
+    if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
+}
+
+// Exclusive scan of n u32 values in place (single block).
+__global__ __launch_bounds__(1024) void k_scan_u32(uint32_t* v, int64_t n) {
+  __shared__ uint32_t sh[1024];
+  uint32_t carry = 0;
+  for (int64_t c0 = 0; c0 < n; c0 += 1024) {
+    const int64_t i = c0 + threadIdx.x;
+    const uint32_t x = i < n ? v[i] : 0u;
+    sh[threadIdx.x] = x;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const uint32_t y = threadIdx.x >= off ? sh[threadIdx.x - off] : 0u;
+      __syncthreads();
+      sh[threadIdx.x] += y;
+      __syncthreads();
+    }
+    if (i < n) v[i] = carry + sh[threadIdx.x] - x;
+    const uint32_t tot = sh[1023];
+    __syncthreads();
+    carry += tot;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_sort_scatter(const uint64_t* __restrict__ kin,
+                                                           const uint32_t* __restrict__ vin, int64_t n,
+                                                           int shift, const uint32_t* __restrict__ offs,
+                                                           int64_t nblk, uint64_t* __restrict__ kout,
+                                                           uint32_t* __restrict__ vout) {
+  __shared__ uint32_t run[256];
+  __shared__ uint32_t wcnt[kThreads / 64][256];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  run[threadIdx.x] = offs[(int64_t)threadIdx.x * nblk + blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * kItems;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t i = base + r * kThreads + threadIdx.x;
+    const bool valid = i < n;
+    uint64_t k = 0;
+    uint32_t v = 0;
+    if (valid) { k = kin[i]; v = vin[i]; }
+    const uint32_t dg = (uint32_t)(k >> shift) & 255u;
+    uint64_t match = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (dg >> b) & 1u;
+      const uint64_t bb = __ballot(valid && bit);
+      match &= bit ? bb : ~bb;
+    }
+    const uint32_t rank = __popcll(match & lanemask_lt());
+    const uint32_t cnt = __popcll(match);
+#pragma unroll
+    for (int q = 0; q < kThreads / 64; ++q) wcnt[q][threadIdx.x] = 0;
+    __syncthreads();
+    if (valid && rank == 0) wcnt[w][dg] = cnt;
+    __syncthreads();
+    if (valid) {
+      uint32_t pos = run[dg] + rank;
+      for (int q = 0; q < w; ++q) pos += wcnt[q][dg];
+      kout[pos] = k;
+      vout[pos] = v;
+    }
+    __syncthreads();
+    uint32_t add = 0;
+#pragma unroll
+    for (int q = 0; q < kThreads / 64; ++q) add += wcnt[q][threadIdx.x];
+    run[threadIdx.x] += add;
+    __syncthreads();
+  }
+  (void)lane;
+}
+
+// ---------------------------------------------------------------- workspace
+size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
+  const size_t cap = k_cap ? k_cap : 1;
+  const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
+  const size_t nb_s = (cap + kItems - 1) / kItems + 1;
+  const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
+  size_t b = 0;
+  b += align_up(cap * 8, 256) * 2;
+  b += align_up(cap * 4, 256) * 2;
+  b += align_up(256 * max_blocks * 4, 256);
+  b += align_up((max_blocks + 1) * 8, 256) * 2;
+  b += align_up(264 * 8, 256);
+  return b;
+}
+
+RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
+  const size_t cap = k_cap ? k_cap : 1;
+  const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
+  const size_t nb_s = (cap + kItems - 1) / kItems + 1;
+  const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
+  char* p = static_cast<char*>(base);
+  RankWs w;
+  w.keys_a = reinterpret_cast<uint64_t*>(p); p += align_up(cap * 8, 256);
+  w.keys_b = reinterpret_cast<uint64_t*>(p); p += align_up(cap * 8, 256);
+  w.vals_a = reinterpret_cast<uint32_t*>(p); p += align_up(cap * 4, 256);
+  w.vals_b = reinterpret_cast<uint32_t*>(p); p += align_up(cap * 4, 256);
+  w.hist = reinterpret_cast<uint32_t*>(p); p += align_up(256 * max_blocks * 4, 256);
+  w.blk_a = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
+  w.blk_b = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
+  w.state = reinterpret_cast<uint64_t*>(p);
+  w.cap = cap;
+  w.max_blocks = max_blocks;
+  return w;
+}
+
+hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
+                                const RankWs& ws, hipStream_t st) {
+  if (K <= 0) return hipSuccess;
+  const double* g = gain + t0;
+  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(256), 0, st, ws.state, K);
+  int64_t hb = (n + kThreads - 1) / kThreads;
+  if (hb > 2048) hb = 2048;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, shift);
+    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(256), 0, st, ws.state, shift);
+  }
+  const int64_t nbc = (n + kItems - 1) / kItems;
+  hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state,
+                     ws.blk_a, ws.blk_b);
+  hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
+  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
+                     ws.blk_a, ws.blk_b, ws.keys_a, ws.vals_a);
+  // sort the K survivors: 8 stable passes, ascending on ~key
+  const int64_t nbs = (K + kItems - 1) / kItems;
+  uint64_t* ki = ws.keys_a;
+  uint64_t* ko = ws.keys_b;
+  uint32_t* vi = ws.vals_a;
+  uint32_t* vo = ws.vals_b;
+  for (int shift = 0; shift < 64; shift += 8) {
+    hipLaunchKernelGGL(k_sort_hist, dim3((unsigned)nbs), dim3(kThreads), 0, st, ki, K, shift, ws.hist, nbs);
+    hipLaunchKernelGGL(k_scan_u32, dim3(1), dim3(1024), 0, st, ws.hist, 256 * nbs);
+    hipLaunchKernelGGL(k_sort_scatter, dim3((unsigned)nbs), dim3(kThreads), 0, st, ki, vi, K, shift,
+                       ws.hist, nbs, ko, vo);
+    uint64_t* tk = ki; ki = ko; ko = tk;
+    uint32_t* tv = vi; vi = vo; vo = tv;
+  }
+  // 8 passes (even) leave the result in the "a" buffers
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- packing
+__device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v, int nbits) {
+  if (nbits <= 0) return;
+  const int o = pos & 63, k = pos >> 6;
+  w[k] |= v << o;
+  if (o + nbits > 64) w[k + 1] |= v >> (64 - o);
+  pos += nbits;
+}
+
+__global__ void k_pack(const uint32_t* __restrict__ tiles, int64_t K, const uint16_t* __restrict__ seed,
+                       const int8_t* __restrict__ code, const uint16_t* __restrict__ scale, int P, int b,
+                       int idx_bits, int seed_bits, int L, uint8_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= K) return;
+  const uint32_t t = tiles[i];
+  uint64_t w[3] = {0, 0, 0};
+  int pos = 0;
+  put_bits(w, pos, (uint64_t)t, idx_bits);
+  put_bits(w, pos, (uint64_t)seed[t], seed_bits);
+  const uint64_t cm = (1ull << b) - 1ull;
+  for (int p = 0; p < P; ++p) put_bits(w, pos, (uint64_t)(int64_t)code[(int64_t)t * P + p] & cm, b);
+  put_bits(w, pos, (uint64_t)scale[t], 16);
+  uint8_t* o = out + i * L;
+  for (int k = 0; k < L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
+}
+
+hipError_t launch_pack(const uint32_t* tiles, int64_t K, const uint16_t* seed, const int8_t* code,
+                       const uint16_t* scale, int P, int b, int idx_bits, int seed_bits, int L_rec,
+                       uint8_t* out, hipStream_t st) {
+  if (K <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, tiles, K, seed, code,
+                     scale, P, b, idx_bits, seed_bits, L_rec, out);
+  return hipGetLastError();
+}
+
+}  // namespace awsrc

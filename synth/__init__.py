@@ -10,5 +10,6 @@ from .workloads import (  # noqa: F401
     WORKLOADS,
     workload,
     gen_module_inputs,
+    gen_records,
     round_half_even_count,
 )

@@ -171,7 +171,8 @@ def gen_activation(wl: Workload, m: Module, device="cpu") -> torch.Tensor:
 def gen_fisher(wl: Workload, m: Module, device="cpu") -> torch.Tensor:
     """Per-element Fisher proxy: mean of 64 squared N(0,1) draws ~ Gamma(32, rate 32)."""
     seed = _seed(m, FIELD_FISHER)
-    devs = [torch.device(device)] if torch.device(device).type == "cuda" else []
+    dv = torch.device(device)
+    devs = [dv.index if dv.index is not None else torch.cuda.current_device()] if dv.type == "cuda" else []
     with torch.random.fork_rng(devices=devs):
         torch.manual_seed(seed)
         if devs:
@@ -195,3 +196,25 @@ def gen_module_inputs(wl: Workload, m: Module, device="cpu") -> Dict[str, torch.
         F = gen_fisher(wl, m, device)
         d = (0.5 * a)[None, :] + 0.5 * F
     return {"W": W, "W32": W.to(torch.float32), "d": d.contiguous()}
+
+
+def gen_records(T: int, P: int, b: int, S: int, seed: int, device="cpu",
+                frac_nonpositive: float = 0.3, frac_ties: float = 0.1) -> Dict[str, torch.Tensor]:
+    """Random per-tile records shaped like encoder outputs, for ranking and
+    decoding tests: seeds in [0, S), codes in [-qmax, qmax], positive finite
+    fp16 scale bit patterns, fp64 gains with a share of non-positive values
+    and a share of exactly repeated values (ties)."""
+    g = _gen(seed, device)
+    qmax = (1 << (b - 1)) - 1
+    seeds = torch.randint(0, S, (T,), generator=g, device=device, dtype=torch.int64)
+    codes = torch.randint(-qmax, qmax + 1, (T, P), generator=g, device=device, dtype=torch.int64)
+    scale = torch.randint(0x0400, 0x2C00, (T,), generator=g, device=device, dtype=torch.int64)
+    gain = torch.exp(torch.randn(T, generator=g, device=device, dtype=torch.float64) * 2.0 - 12.0)
+    u = torch.rand(T, generator=g, device=device, dtype=torch.float64)
+    gain = torch.where(u < frac_nonpositive * 0.5, -gain, gain)
+    gain = torch.where((u >= frac_nonpositive * 0.5) & (u < frac_nonpositive), torch.zeros_like(gain), gain)
+    v = torch.rand(T, generator=g, device=device, dtype=torch.float64)
+    tie_val = torch.exp(torch.randint(-14, -10, (T,), generator=g, device=device).to(torch.float64))
+    gain = torch.where((v < frac_ties) & (u >= frac_nonpositive), tie_val, gain)
+    return {"seed": seeds.to(torch.int16), "codes": codes.to(torch.int8), "scale": scale.to(torch.int16),
+            "gain": gain}

@@ -1,0 +1,373 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle.
+
+Every test feeds both sides the same seeded synthetic tensors.  Bars:
+* backbone codes, scales, zero points and W0: bit-exact;
+* encoder seed: equal to the oracle's, or the oracle's gain for the GPU's
+  seed lies within 1e-6 (relative) of the oracle's best gain;
+* where seeds agree: codes and fp16 scale bit-exact unless the oracle flags
+  a coefficient within 1e-9 of a rounding midpoint; gain within 1e-10 of the
+  tile's weighted energy; unquantized coefficients within 1e-4 of max |alpha*|;
+* streams built from the same records: byte-identical;
+* repaired weights: fp32 targets within 2^-22 relative (one fp32 rounding of
+  the add), bf16 targets within one bf16 half-ulp; untouched tiles bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import awsrc_oracle as O
+from synth import WORKLOADS, Module, gen_module_inputs, gen_records, workload
+
+pytestmark = pytest.mark.gpu
+
+awsrc = pytest.importorskip("paper_2608_23144_amd")
+
+DEV = "cuda"
+
+
+def _u16(t):
+    return (t.to(torch.int32) & 0xFFFF).cpu().numpy()
+
+
+def _params(wl, **kw):
+    return awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                             idx_bits=wl.idx_bits, **kw)
+
+
+def _oparams(wl):
+    return O.Params(C=wl.C, P=wl.P, b=wl.b, S=wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                    idx_bits=wl.idx_bits)
+
+
+def _gpu_module(wl, m, want_alpha=True):
+    inp = gen_module_inputs(wl, m, DEV)
+    codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(inp["W"])
+    enc = awsrc.awsrc_encode_tiles(_params(wl), inp["W"], W0, inp["d"], want_alpha=want_alpha)
+    torch.cuda.synchronize()
+    return inp, (codes, scale, zero, W0), enc
+
+
+def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx):
+    """Oracle on a subset of tiles of one module, with every seed's gain kept."""
+    W32 = inp["W32"].cpu().numpy()
+    d = inp["d"].cpu().numpy()
+    _, _, _, W0o = O.rtn_backbone(W32)
+    assert np.array_equal(W0o, W0_gpu.cpu().numpy())
+    R = O.tiles(O.residual(W32, W0o), wl.C)[tiles_idx]
+    D = O.tile_weights(d, m.rows, m.cols, wl.C)[tiles_idx]
+    op = _oparams(wl)
+    orc = O.encode_tiles(R, D, op, keep_all=True)
+    g_seed = _u16(enc["seed"])[tiles_idx]
+    g_codes = enc["codes"].cpu().numpy()[tiles_idx]
+    g_scale = _u16(enc["scale"])[tiles_idx]
+    g_gain = enc["gain"].cpu().numpy()[tiles_idx]
+    g_alpha = enc["alpha"].cpu().numpy()[tiles_idx] if enc.get("alpha") is not None else None
+    n_seed_diff = 0
+    for i in range(len(tiles_idx)):
+        e = orc["energy"][i]
+        gmax = orc["gain"][i]
+        s_g, s_o = int(g_seed[i]), int(orc["seed"][i])
+        g_at = orc["all_gains"][i, s_g]
+        assert abs(g_at - gmax) <= 1e-6 * abs(gmax) + 1e-13 * e, (i, s_g, s_o, g_at, gmax)
+        if s_g == s_o:
+            if not (orc["flag_half"][i] or orc["flag_scale"][i]):
+                assert np.array_equal(g_codes[i], orc["codes"][i]), (i, g_codes[i], orc["codes"][i])
+                assert g_scale[i] == orc["scale"][i], (i, g_scale[i], orc["scale"][i])
+            assert abs(g_gain[i] - gmax) <= 1e-10 * e + 1e-300, (i, g_gain[i], gmax)
+            if g_alpha is not None:
+                amax = np.abs(orc["alpha"][i]).max()
+                assert np.abs(g_alpha[i] - orc["alpha"][i]).max() <= 1e-4 * amax + 1e-30
+        else:
+            n_seed_diff += 1
+            q, bits, g, _ = O.candidate(R[i], D[i], op, s_g)
+            assert abs(g_gain[i] - g) <= 1e-10 * e + 1e-300
+    return n_seed_diff
+
+
+# ------------------------------------------------------------------ backbone
+@pytest.mark.parametrize("group", [64, 128, 256])
+@pytest.mark.parametrize("name,rows,cols", [("linear256", 256, 256), ("down3b", 130, 11008),
+                                            ("block3b", 3, 2048)])
+def test_backbone_bit_exact(name, rows, cols, group):
+    wl = workload(name)
+    m = Module("t", rows, cols, 0, 5, 5)
+    W = gen_module_inputs(wl, m, DEV)["W"]
+    codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(W, group=group)
+    co, so, zo, W0o = O.rtn_backbone(W.to(torch.float32).cpu().numpy(), group=group)
+    assert np.array_equal(codes.cpu().numpy(), co)
+    assert np.array_equal(_u16(scale), so)
+    assert np.array_equal(zero.cpu().numpy(), zo)
+    assert np.array_equal(W0.cpu().numpy(), W0o)
+
+
+def test_backbone_edge_groups():
+    W = torch.randn(4, 512, dtype=torch.float32) * 0.02
+    W[0, :128] = 0.5                      # degenerate group
+    W[1, :128] = torch.arange(128) % 16 * 0.25 - 1.0   # exact grid
+    W[2, 128:256] = 0
+    W[2, 128] = 15.0
+    W[2, 129] = 2.5                       # half-even tie
+    W[3, 256:384] *= 1e7                  # scale saturates at 65504
+    Wd = W.to(DEV)
+    codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(Wd)
+    co, so, zo, W0o = O.rtn_backbone(W.numpy())
+    assert np.array_equal(codes.cpu().numpy(), co) and np.array_equal(_u16(scale), so)
+    assert np.array_equal(zero.cpu().numpy(), zo) and np.array_equal(W0.cpu().numpy(), W0o)
+
+
+# ------------------------------------------------------------------ encoder
+def test_encode_linear256_full():
+    """Small fp32 layer (C=64, S=64, P=4, b=4, per-column weights): every tile."""
+    wl = WORKLOADS["linear256"]
+    m = wl.modules[0]
+    inp, bb, enc = _gpu_module(wl, m)
+    nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(m.rows * m.cols // wl.C))
+    assert nd <= 2
+
+
+@pytest.mark.parametrize("C,P,b,S,rows,cols,d_mode", [
+    (64, 8, 4, 32, 67, 512, "elem"),    # ragged wavefront, per-element weights
+    (128, 8, 3, 24, 5, 256, "col"),
+    (32, 4, 4, 16, 1, 64, "elem"),      # one row
+    (16, 4, 4, 16, 9, 128, "col"),      # the paper's P_F operating point shape
+    (64, 3, 5, 10, 20, 128, "col"),     # padded P
+    (128, 2, 4, 2, 8, 256, "col"),      # the paper's U operating point shape
+    (64, 16, 8, 8, 4, 128, "elem"),
+])
+def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
+    wl = workload("block3b", C=C, P=P, b=b, S=S, d_mode=d_mode)
+    m = Module("t", rows, cols, 0, 2, 2)
+    inp, bb, enc = _gpu_module(wl, m)
+    T = rows * cols // C
+    nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T))
+    assert nd <= max(1, T // 50)
+
+
+def test_encode_zero_residual_tiles():
+    """Tiles whose residual is exactly zero keep seed 0, an all-zero record and gain 0."""
+    wl = workload("linear256", S=8)
+    W = torch.zeros(64, 256, dtype=torch.float32, device=DEV)
+    W[:, 128:] = torch.randn(64, 128, device=DEV) * 0.02
+    d = torch.exp(torch.randn(256, device=DEV))
+    codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(W)
+    enc = awsrc.awsrc_encode_tiles(_params(wl), W, W0, d)
+    nb = 256 // 64
+    seed = _u16(enc["seed"]).reshape(64, nb)
+    gain = enc["gain"].cpu().numpy().reshape(64, nb)
+    assert np.all(seed[:, :2] == 0) and np.all(gain[:, :2] == 0)
+    assert np.all(enc["codes"].cpu().numpy().reshape(64, nb, -1)[:, :2] == 0)
+    assert np.all(_u16(enc["scale"]).reshape(64, nb)[:, :2] == 0)
+
+
+@pytest.mark.parametrize("name,n_tiles", [("down3b", 400), ("block3b", 300), ("layer32b", 60)])
+def test_encode_full_size_sampled(name, n_tiles):
+    """Full-size modules of the 3B / 32B workloads; the oracle checks sampled tiles."""
+    wl = WORKLOADS[name]
+    mods = wl.modules if name != "block3b" else (wl.modules[1], wl.modules[6])
+    if name == "layer32b":
+        mods = (wl.modules[1], wl.modules[6])
+    rng = np.random.default_rng(0)
+    for m in mods:
+        inp, bb, enc = _gpu_module(wl, m)
+        T = m.rows * m.cols // wl.C
+        idx = np.unique(np.concatenate([rng.integers(0, T, n_tiles), [0, T - 1]]))
+        nd = _check_encode_sample(wl, m, inp, bb[3], enc, idx)
+        assert nd <= max(1, len(idx) // 50)
+        del inp, bb, enc
+        torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ ranking
+@pytest.mark.parametrize("mode", ["global", "per_module"])
+@pytest.mark.parametrize("bpw", [0.05, 0.162, 2.0, 64.0])
+def test_rank_stream_byte_exact(mode, bpw):
+    op = O.Params(C=64, P=8, b=4, S=256)
+    p = awsrc.make_params(64, 8, 4, 256)
+    mods = [(64, 512), (8, 11008), (200, 128)]
+    T = sum(r * c // 64 for r, c in mods)
+    rec = gen_records(T, 8, 4, 256, seed=11)
+    h = O.header_bytes(len(mods))
+    if mode == "global" and O.budget_bytes(bpw, sum(r * c for r, c in mods)) < h:
+        pytest.skip("budget below header")
+    enc = {"seed": rec["seed"].numpy().astype(np.int64) & 0xFFFF, "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    want, K_o, ne_o = O.build_stream(op, mods, enc, bpw, per_module=(mode == "per_module"))
+    dev = {k: v.to(DEV) for k, v in rec.items()}
+    m = awsrc.AWSRC_MODE_GLOBAL if mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
+    s, K, ne = awsrc.awsrc_rank_prefix(p, mods, m, bpw, dev["seed"], dev["codes"], dev["scale"], dev["gain"])
+    assert (K, ne) == (K_o, ne_o)
+    assert bytes(s.cpu().numpy().tobytes()) == want
+
+
+def test_rank_large_segment_with_ties():
+    """Many exact ties straddling the cut: equal gains keep the lower tile index."""
+    op = O.Params(C=64, P=4, b=4, S=64)
+    p = awsrc.make_params(64, 4, 4, 64)
+    mods = [(4096, 4096)]
+    T = 4096 * 64
+    rec = gen_records(T, 4, 4, 64, seed=5, frac_ties=0.6)
+    enc = {"seed": rec["seed"].numpy().astype(np.int64), "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    for bpw in (0.01, 0.3):
+        want, K_o, _ = O.build_stream(op, mods, enc, bpw, per_module=False)
+        dev = {k: v.to(DEV) for k, v in rec.items()}
+        s, K, _ = awsrc.awsrc_rank_prefix(p, mods, awsrc.AWSRC_MODE_GLOBAL, bpw, dev["seed"], dev["codes"],
+                                          dev["scale"], dev["gain"])
+        assert K == K_o and bytes(s.cpu().numpy().tobytes()) == want
+
+
+def test_rank_no_eligible_records():
+    p = awsrc.make_params(64, 4, 4, 64)
+    rec = gen_records(64, 4, 4, 64, seed=1)
+    gain = -torch.abs(rec["gain"]).to(DEV)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(16, 256)], awsrc.AWSRC_MODE_GLOBAL, 8.0, rec["seed"].to(DEV),
+                                       rec["codes"].to(DEV), rec["scale"].to(DEV), gain)
+    assert K == 0 and ne == 0 and s.numel() == O.header_bytes(1)
+
+
+# ------------------------------------------------------------------ decoding
+def _oracle_stream(C, P, b, S, mods, bpw, seed, key=0):
+    op = O.Params(C=C, P=P, b=b, S=S, basis_key=key)
+    T = sum(r * c // C for r, c in mods)
+    rec = gen_records(T, P, b, S, seed=seed)
+    enc = {"seed": rec["seed"].numpy().astype(np.int64) & 0xFFFF, "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    stream, K, _ = O.build_stream(op, mods, enc, bpw, per_module=False)
+    return stream, K, enc
+
+
+@pytest.mark.parametrize("C,P,b,S,dtype", [(64, 8, 4, 256, torch.float32), (64, 4, 4, 64, torch.bfloat16),
+                                           (128, 8, 3, 1024, torch.float32), (16, 4, 4, 16, torch.float32),
+                                           (32, 16, 8, 7, torch.bfloat16)])
+def test_decode_matches_oracle(C, P, b, S, dtype):
+    mods = [(33, 512), (8, 1024)]
+    stream, K, enc = _oracle_stream(C, P, b, S, mods, 2.0, seed=3, key=0x1234)
+    g = torch.Generator().manual_seed(9)
+    W0s = [(torch.randn(r, c, generator=g) * 0.02).to(dtype) for r, c in mods]
+    want = O.decode_add(stream, [w.to(torch.float32).numpy() for w in W0s])
+    dev = [w.to(DEV) for w in W0s]
+    sb = torch.tensor(list(stream), dtype=torch.uint8, device=DEV)
+    awsrc.awsrc_decode_add(sb, dev)
+    hd = O.parse_header(stream)
+    touched = [np.zeros((r, c // C), bool) for r, c in mods]
+    offs = np.cumsum([0] + [r * c // C for r, c in mods])
+    L = hd["L_rec"]
+    for k in range(K):
+        t = O.unpack_record(stream[hd["h"] + k * L: hd["h"] + (k + 1) * L], hd["idx_bits"], hd["seed_bits"], P, b)[0]
+        mi = int(np.searchsorted(offs, t, side="right") - 1)
+        rr, bb = divmod(int(t - offs[mi]), mods[mi][1] // C)
+        touched[mi][rr, bb] = True
+    for w0, got, ref, tm, (r, c) in zip(W0s, dev, want, touched, mods):
+        got = got.to(torch.float32).cpu().numpy()
+        mask = np.repeat(tm, C, axis=1)
+        assert np.array_equal(got[~mask], w0.to(torch.float32).numpy()[~mask])
+        tol = 2.0 ** -22 if dtype == torch.float32 else 2.0 ** -8
+        w0f = w0.to(torch.float32).numpy().astype(np.float64)
+        mag = np.abs(w0f) + np.abs(ref - w0f)     # operands of the add
+        assert np.all(np.abs(got - ref)[mask] <= tol * mag[mask] + 1e-30)
+
+
+def test_decode_prefixes_and_empty_stream():
+    C, P, b, S = 64, 8, 4, 256
+    mods = [(64, 1024)]
+    stream, K, enc = _oracle_stream(C, P, b, S, mods, 4.0, seed=4)
+    hd = O.parse_header(stream)
+    g = torch.Generator().manual_seed(2)
+    W0 = torch.randn(64, 1024, generator=g) * 0.02
+    for k in (0, 1, K // 3, K):
+        pre = stream[:hd["h"] + k * hd["L_rec"]]
+        want = O.decode_add(pre, [W0.numpy()])[0]
+        dev = W0.to(DEV)
+        awsrc.awsrc_decode_add(torch.tensor(list(pre), dtype=torch.uint8, device=DEV), [dev])
+        got = dev.cpu().numpy()
+        if k == 0:
+            assert np.array_equal(got, W0.numpy())
+        w0f = W0.numpy().astype(np.float64)
+        assert np.all(np.abs(got - want) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(want - w0f)) + 1e-30)
+
+
+def _corrupt_cases(stream, hd):
+    h, L = hd["h"], hd["L_rec"]
+    bad = {}
+    b = bytearray(stream); b[0] = ord("X"); bad["magic"] = bytes(b)
+    bad["truncated"] = stream[:-1]
+    b = bytearray(stream); b[h:h + L] = stream[h + L:h + 2 * L]; bad["duplicate_tile"] = bytes(b)
+    b = bytearray(stream); b[h:h + 4] = (hd["T_total"] + 5).to_bytes(4, "little"); bad["tile_out_of_range"] = bytes(b)
+    b = bytearray(stream); b[h + L - 1] |= 0x7C; bad["inf_scale"] = bytes(b)
+    b = bytearray(stream); b[12:16] = (3).to_bytes(4, "little"); bad["header_S"] = bytes(b)
+    return bad
+
+
+def test_decode_rejects_corrupt_streams():
+    C, P, b, S = 64, 8, 4, 256
+    mods = [(32, 512)]
+    stream, K, enc = _oracle_stream(C, P, b, S, mods, 4.0, seed=8)
+    assert K >= 2
+    hd = O.parse_header(stream)
+    W0 = torch.randn(32, 512) * 0.02
+    for name, bs in _corrupt_cases(stream, hd).items():
+        dev = W0.to(DEV)
+        with pytest.raises(awsrc.AwsrcError) as ei:
+            awsrc.awsrc_decode_add(torch.tensor(list(bs), dtype=torch.uint8, device=DEV), [dev])
+        assert ei.value.status == awsrc.AWSRC_ECORRUPT, name
+        assert torch.equal(dev.cpu(), W0), name
+
+
+# ------------------------------------------------------------------ end to end
+def test_pipeline_linear256_matches_oracle():
+    """backbone -> encode -> rank (0.162 bpw) -> decode on the GPU, against the
+    same chain in the oracle: identical stream bytes and repaired weights."""
+    wl = WORKLOADS["linear256"]
+    m = wl.modules[0]
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m)
+    p = _params(wl)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_GLOBAL, 0.162, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    W32 = inp["W32"].cpu().numpy()
+    d = inp["d"].cpu().numpy()
+    _, _, _, W0o = O.rtn_backbone(W32)
+    R = O.residual(W32, W0o)
+    op = _oparams(wl)
+    orc = O.encode_tiles(O.tiles(R, wl.C), O.tile_weights(d, m.rows, m.cols, wl.C), op)
+    want, K_o, ne_o = O.build_stream(op, [(m.rows, m.cols)], orc, 0.162, per_module=False)
+    assert (K, ne) == (K_o, ne_o)
+    assert bytes(s.cpu().numpy().tobytes()) == want
+    What = W0.clone()
+    awsrc.awsrc_decode_add(s, [What])
+    ref = O.decode_add(want, [W0o])[0]
+    w0f = W0o.astype(np.float64)
+    assert np.all(np.abs(What.cpu().numpy() - ref) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(ref - w0f)) + 1e-30)
+    # the repair lowers the weighted error by exactly the retained gains
+    e0 = O.weighted_error(W32, W0o.astype(np.float64), d)
+    e1 = O.weighted_error(W32, What.cpu().numpy().astype(np.float64), d)
+    kept = np.sort(orc["gain"][orc["gain"] > 0])[::-1][:K]
+    assert abs((e0 - e1) - kept.sum()) <= 1e-5 * e0
+
+
+def test_pipeline_down3b_properties():
+    """Full-size 3B down projection, per-module quota (U variant): stream
+    structure holds at size and decoding removes exactly the retained gains."""
+    wl = WORKLOADS["down3b"]
+    m = wl.modules[0]
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m, want_alpha=False)
+    p = _params(wl)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_PER_MODULE, 0.162, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    gain = enc["gain"].cpu().numpy()
+    L = O.record_bytes(_oparams(wl), gain.size)
+    assert ne == int((gain > 0).sum())
+    assert K == min(ne, O.budget_bytes(0.162, m.rows * m.cols) // L)
+    hd = O.parse_header(bytes(s[:O.header_bytes(1)].cpu().numpy().tobytes()))
+    assert hd["L_rec"] == L == 11 and len(s) == hd["h"] + K * L
+    order = O.rank_order(gain, np.arange(gain.size))[:K]
+    raw = s[hd["h"]:].cpu().numpy().reshape(K, L)
+    idx = raw[:, :4].copy().view("<u4").ravel()
+    assert np.array_equal(idx, order)
+    # weighted error drop equals the sum of retained gains (fp64 on the GPU)
+    What = W0.clone()
+    awsrc.awsrc_decode_add(s, [What])
+    W = inp["W32"].double()
+    dd = inp["d"].double()[None, :]
+    e0 = (dd * (W - W0.double()) ** 2).sum().item()
+    e1 = (dd * (W - What.double()) ** 2).sum().item()
+    assert abs((e0 - e1) - gain[order].sum()) <= 1e-6 * e0
