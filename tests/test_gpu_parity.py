@@ -128,7 +128,7 @@ def test_encode_linear256_full():
 @pytest.mark.parametrize("C,P,b,S,rows,cols,d_mode", [
     (64, 8, 4, 32, 67, 512, "elem"),    # ragged wavefront, per-element weights
     (128, 8, 3, 24, 5, 256, "col"),
-    (32, 4, 4, 16, 1, 64, "elem"),      # one row
+    (32, 4, 4, 16, 1, 128, "elem"),     # one row
     (16, 4, 4, 16, 9, 128, "col"),      # the paper's P_F operating point shape
     (64, 3, 5, 10, 20, 128, "col"),     # padded P
     (128, 2, 4, 2, 8, 256, "col"),      # the paper's U operating point shape
