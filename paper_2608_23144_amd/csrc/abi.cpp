@@ -130,12 +130,14 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const int64_t nb = cols / p->C;
   const int64_t T = rows * nb;
   if (T > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "too many tiles in one module");
-  const int PB = p->P <= 4 ? 4 : (p->P <= 8 ? 8 : 16);
+  const int PB = factor_pb(p->C, p->P);
   const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
+  const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
+  const size_t b_frag = screen_mfma_supported(p->C, p->P) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
   const size_t b_tg = align_up((size_t)T * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * kTop * 2, 256);
-  const size_t need = b_basis + b_fac + b_tg + b_ts + 256;
+  const size_t need = b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
   if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
   if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
   if (T == 0) return AWSRC_OK;
@@ -150,6 +152,10 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   ws += b_basis;
   a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
   ws += b_fac;
+  a.wd64 = b_wd ? reinterpret_cast<double*>(ws) : nullptr;
+  ws += b_wd;
+  a.frag = b_frag ? static_cast<void*>(ws) : nullptr;
+  ws += b_frag;
   a.top_gain = reinterpret_cast<float*>(ws);
   ws += b_tg;
   a.top_seed = reinterpret_cast<uint16_t*>(ws);

@@ -79,6 +79,8 @@ struct EncodeArgs {
   double lambda;
   BasisTables basis;
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
+  double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
+  void* frag;          // +-1 basis fragments of the matrix-core screen
   float* top_gain;     // [T][kTop] screened gains, descending
   uint16_t* top_seed;  // [T][kTop]
   uint16_t* seed_out;
@@ -89,6 +91,10 @@ struct EncodeArgs {
 };
 
 bool encode_supported(int C, int P);
+bool screen_mfma_supported(int C, int P);
+int factor_pb(int C, int P);                 // padded P of the per-column factor table
+size_t mfma_frag_bytes(int C, int S);
+hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st);
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);

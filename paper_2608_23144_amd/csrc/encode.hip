@@ -272,25 +272,46 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 }
 
 // ----------------------------------------------------------------------------
+// fp64 Walsh-Hadamard transform of each column block's weights (per-column
+// mode): the Gram entries of every seed are gathers from it.
+template <int C>
+__global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __restrict__ out) {
+  const int blk = blockIdx.x * blockDim.x + threadIdx.x;
+  if (blk >= nb) return;
+  double v[C];
+#pragma unroll
+  for (int j = 0; j < C; ++j) v[j] = (double)d[(int64_t)blk * C + j];
+  fwht<C>(v);
+#pragma unroll
+  for (int j = 0; j < C; ++j) out[(int64_t)blk * C + j] = v[j];
+}
+
+// ----------------------------------------------------------------------------
 // fp64 re-score of the screened candidates; writes the encoder outputs.
+// For one (tile, seed): b = WHT(sigma .* d .* r)[c] / sqrt(C) and
+// G_pq = WHT(d)[c_p xor c_q] / C (+ eps on the diagonal), Cholesky solve,
+// fp16-scale quantization, and the gain 2 a^T b - a^T G0 a of the quantized
+// coefficients a (G0 = G without the ridge), all in fp64.  Each lane keeps
+// its transformed vector in a private LDS row for the data-dependent gathers.
 template <int C, int PB, bool PE>
-__global__ __launch_bounds__(64) void k_finalize(EncodeArgs a) {
+__global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __restrict__ wdb) {
+  constexpr int NT = (C == 128) ? 32 : 64;  // rows per workgroup (keeps the LDS rows under 64 KiB)
+  extern __shared__ double fsh[];
+  double* my = fsh + threadIdx.x * (C + 1);
   const int nb = (int)(a.cols / C);
   const int blk = blockIdx.x % nb;
-  const int64_t row = (int64_t)(blockIdx.x / nb) * 64 + threadIdx.x;
+  const int64_t row = (int64_t)(blockIdx.x / nb) * NT + threadIdx.x;
   if (row >= a.rows) return;
   const int64_t off = row * a.cols + (int64_t)blk * C;
   const int64_t t = row * nb + blk;
   const int P = a.P;
-  float r[C], dd[C];
   float e32 = 0.0f;
   double sumd = 0.0;
-#pragma unroll
   for (int j = 0; j < C; ++j) {
-    r[j] = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
-    dd[j] = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
-    e32 += dd[j] * r[j] * r[j];
-    sumd += (double)dd[j];
+    const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
+    const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
+    e32 += dj * r * r;
+    sumd += (double)dj;
   }
   const double eps = a.lambda * (sumd / C);
   const double isq = 1.0 / sqrt((double)C);
@@ -306,71 +327,81 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a) {
   int best_s = 0x7FFFFFFF;
   int best_q[PB];
   uint16_t best_bits = 0;
-  double best_al[PB];
+  float best_al[PB];
 #pragma unroll
-  for (int p = 0; p < PB; ++p) { best_q[p] = 0; best_al[p] = 0.0; }
+  for (int p = 0; p < PB; ++p) { best_q[p] = 0; best_al[p] = 0.f; }
 
   for (int k = 0; k < kTop; ++k) {
-    if (k > 0 && !(tg[k] >= thr)) continue;
-    if (!(tg[k] > -INFINITY) && k > 0) continue;
+    if (k > 0 && !(tg[k] >= thr && tg[k] > -INFINITY)) continue;
     const int s = ts[k];
-    const uint64_t* mk = a.basis.mask + (size_t)s * P * 2;
+    const uint64_t* sw = a.basis.sign + (size_t)s * 2;
     const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
-    double bv[PB];
-    double G[PB][PB];
+    int c[PB];
 #pragma unroll
-    for (int p = 0; p < PB; ++p) {
-      double acc = 0.0;
-      if (p < P) {
-        const uint64_t m0 = mk[2 * p], m1 = mk[2 * p + 1];
-        for (int j = 0; j < C; ++j) {
-          const double uj = (double)dd[j] * (double)r[j];
-          const uint64_t m = (j < 64) ? m0 : m1;
-          acc += ((m >> (j & 63)) & 1ull) ? -uj : uj;
-        }
+    for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
+    // projection through the fast transform of sigma .* d .* r
+    {
+      double v[C];
+      const uint64_t s0 = sw[0], s1 = sw[1];
+#pragma unroll
+      for (int j = 0; j < C; ++j) {
+        const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
+        const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
+        const double u = (double)dj * (double)r;
+        const uint64_t sg = (j < 64) ? (s0 >> j) : (s1 >> (j - 64));
+        v[j] = (sg & 1ull) ? -u : u;
       }
-      bv[p] = acc * isq;
+      fwht<C>(v);
+#pragma unroll
+      for (int j = 0; j < C; ++j) my[j] = v[j];
     }
+    double bv[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? my[c[p]] * isq : 0.0;
+    // Gram entries
+    const double* wd;
+    if constexpr (PE) {
+      double v[C];
+#pragma unroll
+      for (int j = 0; j < C; ++j) v[j] = (double)a.d[off + j];
+      fwht<C>(v);
+#pragma unroll
+      for (int j = 0; j < C; ++j) my[j] = v[j];
+      wd = my;
+    } else {
+      wd = wdb + (int64_t)blk * C;
+    }
+    double L[PB][PB], inv[PB];
 #pragma unroll
     for (int p = 0; p < PB; ++p)
 #pragma unroll
       for (int q = 0; q <= p; ++q) {
-        double g;
-        if (p < P && q < P) {
-          const int x = cs[p] ^ cs[q];
-          double acc = 0.0;
-          for (int j = 0; j < C; ++j) acc += (__popc((unsigned)(j & x)) & 1) ? -(double)dd[j] : (double)dd[j];
-          g = acc / C + (p == q ? eps : 0.0);
-        } else {
-          g = (p == q) ? 1.0 : 0.0;
-        }
-        G[p][q] = g;
-      }
-    // Cholesky solve in fp64
-    double L[PB][PB], z[PB], al[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p)
-#pragma unroll
-      for (int q = 0; q <= p; ++q) {
-        double acc = G[p][q];
+        double acc;
+        if (p < P && q < P) acc = wd[c[p] ^ c[q]] / C + (p == q ? eps : 0.0);
+        else acc = (p == q) ? 1.0 : 0.0;
 #pragma unroll
         for (int kk = 0; kk < q; ++kk) acc -= L[p][kk] * L[q][kk];
-        if (p == q) L[p][p] = sqrt(fmax(acc, 1e-300));
-        else L[p][q] = acc / L[q][q];
+        if (p == q) {
+          L[p][p] = sqrt(fmax(acc, 1e-300));
+          inv[p] = 1.0 / L[p][p];
+        } else {
+          L[p][q] = acc * inv[q];
+        }
       }
+    double z[PB], al[PB];
 #pragma unroll
     for (int p = 0; p < PB; ++p) {
       double acc = bv[p];
 #pragma unroll
       for (int kk = 0; kk < p; ++kk) acc -= L[p][kk] * z[kk];
-      z[p] = acc / L[p][p];
+      z[p] = acc * inv[p];
     }
 #pragma unroll
     for (int p = PB - 1; p >= 0; --p) {
       double acc = z[p];
 #pragma unroll
       for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
-      al[p] = acc / L[p][p];
+      al[p] = acc * inv[p];
     }
     // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
     double m = 0.0;
@@ -392,28 +423,24 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a) {
       q[p] = (int)qv;
       ah[p] = sc * qv;
     }
-    // gain in its definition form: sum_j d_j (r_j^2 - (r_j - rhat_j)^2)
-    double gsum = 0.0;
-    for (int j = 0; j < C; ++j) {
-      double rh = 0.0;
+    // gain = 2 a^T b - a^T G0 a, with a^T G0 a = |L^T a|^2 - eps |a|^2
+    double t1 = 0.0, aa = 0.0, quad = 0.0;
 #pragma unroll
-      for (int p = 0; p < PB; ++p) {
-        if (p < P) {
-          const uint64_t mm = (j < 64) ? mk[2 * p] : mk[2 * p + 1];
-          const double bjp = ((mm >> (j & 63)) & 1ull) ? -isq : isq;
-          rh += bjp * ah[p];
-        }
-      }
-      const double rj = (double)r[j];
-      const double e = rj - rh;
-      gsum += (double)dd[j] * (rj * rj - e * e);
+    for (int p = 0; p < PB; ++p) { t1 += ah[p] * bv[p]; aa += ah[p] * ah[p]; }
+#pragma unroll
+    for (int kk = 0; kk < PB; ++kk) {
+      double y = 0.0;
+#pragma unroll
+      for (int i = kk; i < PB; ++i) y += L[i][kk] * ah[i];
+      quad += y * y;
     }
+    const double gsum = 2.0 * t1 - (quad - eps * aa);
     if (gsum > best_g || (gsum == best_g && s < best_s)) {
       best_g = gsum;
       best_s = s;
       best_bits = bits;
 #pragma unroll
-      for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = al[p]; }
+      for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = (float)al[p]; }
     }
   }
   a.seed_out[t] = (uint16_t)best_s;
@@ -423,7 +450,7 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a) {
   for (int p = 0; p < PB; ++p) {
     if (p < P) {
       a.code_out[t * P + p] = (int8_t)best_q[p];
-      if (a.alpha_out) a.alpha_out[t * P + p] = (float)best_al[p];
+      if (a.alpha_out) a.alpha_out[t * P + p] = best_al[p];
     }
   }
 }
@@ -434,6 +461,8 @@ static int pad_p(int P) { return P <= 4 ? 4 : (P <= 8 ? 8 : 16); }
 bool encode_supported(int C, int P) {
   return (C == 16 || C == 32 || C == 64 || C == 128) && P >= 1 && P <= kMaxP && P <= C;
 }
+
+int factor_pb(int C, int P) { return screen_mfma_supported(C, P) ? 8 : pad_p(P); }
 
 template <int C, int PB>
 static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
@@ -459,18 +488,24 @@ static hipError_t run_screen(const EncodeArgs& a, hipStream_t st) {
 
 template <int C, int PB>
 static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
+  constexpr int NT = (C == 128) ? 32 : 64;
   const int nb = (int)(a.cols / C);
-  const int64_t waves = nb * ((a.rows + 63) / 64);
-  if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)waves), dim3(64), 0, st, a);
-  else
-    hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)waves), dim3(64), 0, st, a);
+  const int64_t groups = nb * ((a.rows + NT - 1) / NT);
+  const size_t lds = (size_t)NT * (C + 1) * sizeof(double);
+  if (a.d_mode == AWSRC_D_PER_ELEM) {
+    hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)groups), dim3(NT), lds, st, a,
+                       (const double*)nullptr);
+  } else {
+    hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
+    hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)groups), dim3(NT), lds, st, a,
+                       (const double*)a.wd64);
+  }
   return hipGetLastError();
 }
 
 #define AWSRC_DISPATCH(FN, a, st)                                       \
   do {                                                                  \
-    const int pb_ = pad_p((a).P);                                       \
+    const int pb_ = PBSEL((a).C, (a).P);                                \
     switch ((a).C) {                                                    \
       case 16:                                                          \
         if (pb_ == 4) return FN<16, 4>(a, st);                          \
@@ -492,8 +527,15 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
     }                                                                   \
   } while (0)
 
+#define PBSEL(C_, P_) factor_pb(C_, P_)
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_factors, a, st); }
-hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_screen, a, st); }
+hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st) {
+  if (screen_mfma_supported(a.C, a.P)) return launch_encode_screen_mfma(a, a.frag, st);
+  AWSRC_DISPATCH(run_screen, a, st);
+}
+#undef PBSEL
+#define PBSEL(C_, P_) pad_p(P_)
 hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_finalize, a, st); }
+#undef PBSEL
 
 }  // namespace awsrc

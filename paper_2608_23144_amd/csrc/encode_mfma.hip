@@ -1,0 +1,328 @@
+// Encoder seed search with the projection on the matrix cores (C = 64, P <= 8).
+//
+// For a tile t and seed s the projection b = B_s^T (d .* r) (Eq. (3)) is a dot
+// product of u_t = d_t .* r_t with +-1/sqrt(C) basis columns.  Stacking the
+// P columns of two seeds as 16 rows and 64 tiles of one column block as
+// columns turns one step into a dense [16 x 64] * [64 x 64] product:
+//
+//   * u is split exactly into three bf16 parts (u = hi + mid + lo, each part
+//     truncated from the remainder of the previous one, which loses nothing
+//     for an fp32 u), and the +-1 basis entries are exact in bf16, so three
+//     v_mfma_f32_16x16x32_bf16 per (tile group, K step) give b with fp32
+//     accumulation;
+//   * the u fragments stay in registers for the whole seed loop; the +-1
+//     fragments of each seed pair are read, already laid out per lane, from a
+//     table built once per launch;
+//   * the 16 x 64 result is transposed through LDS so that each lane holds
+//     the P coefficients of its own tile, with the seed uniform across the
+//     wavefront: per-column Cholesky factors are then scalar loads, and the
+//     solve, quantization, score and top-k bookkeeping run on the vector ALUs
+//     exactly as in the VALU screen.
+//
+// MFMA operand layout for 16x16x32 bf16 on gfx950: lane l supplies row
+// (A) / column (B) l % 16 and the K slice 8*(l/16) .. 8*(l/16)+7; the 16x16
+// fp32 result leaves rows 4*(l/16) .. 4*(l/16)+3 of column l % 16 in lane l.
+// Both operands use the same coordinate for (lane group, element), so the
+// sum over K is the same whichever order the hardware visits K in.
+#include <math.h>
+
+#include "awsrc_internal.h"
+
+namespace awsrc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+__device__ __forceinline__ float load_w_any2(const void* W, int dt, int64_t i) {
+  if (dt == AWSRC_DTYPE_F32) return static_cast<const float*>(W)[i];
+  return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
+}
+
+__device__ __forceinline__ uint16_t scale_bits_f32(float v) {
+  uint16_t hb = __half_as_ushort(__float2half_rn(v));
+  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;
+  return hb;
+}
+
+__device__ __forceinline__ int tri2(int p, int q) { return p * (p + 1) / 2 + q; }
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Exact three-way bf16 split of eight fp32 values, packed two per dword.
+__device__ __forceinline__ void split3(const float (&u)[8], u32x4& hi, u32x4& mid, u32x4& lo) {
+  uint32_t h[8], m[8], l[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t ub = __float_as_uint(u[e]);
+    h[e] = ub & 0xFFFF0000u;
+    const float r1 = u[e] - __uint_as_float(h[e]);
+    m[e] = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(m[e]);
+    l[e] = __float_as_uint(r2) & 0xFFFF0000u;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    hi[i] = (h[2 * i] >> 16) | h[2 * i + 1];
+    mid[i] = (m[2 * i] >> 16) | m[2 * i + 1];
+    lo[i] = (l[2 * i] >> 16) | l[2 * i + 1];
+  }
+}
+
+}  // namespace
+
+// ----------------------------------------------------------------------------
+// +-1 basis fragments: frag[pair][ks][lane] = 8 bf16 (4 dwords) of row
+// m = lane % 16 (seed 2*pair + m/8, column m % 8) at coordinates
+// 32*ks + 8*(lane/16) + e.  Rows of absent seeds or columns are zero.
+__global__ void k_mfma_frags(BasisTables bt, int C, int P, int S, u32x4* __restrict__ frag) {
+  const int nks = C / 32;
+  const int64_t n = (int64_t)((S + 1) / 2) * nks * 64;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int lane = (int)(i % 64);
+  const int ks = (int)((i / 64) % nks);
+  const int pair = (int)(i / (64 * nks));
+  const int m = lane & 15;
+  const int s = 2 * pair + (m >> 3);
+  const int p = m & 7;
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (s < S && p < P) {
+    const int j0 = 32 * ks + 8 * (lane >> 4);
+    const uint64_t mk = bt.mask[((size_t)s * P + p) * 2 + (j0 >> 6)] >> (j0 & 63);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = ((mk >> (2 * q)) & 1ull) ? 0xBF80u : 0x3F80u;
+      const uint32_t hi = ((mk >> (2 * q + 1)) & 1ull) ? 0xBF80u : 0x3F80u;
+      v[q] = lo | (hi << 16);
+    }
+  }
+  frag[i] = v;
+}
+
+// ----------------------------------------------------------------------------
+// Screen: one wavefront (one workgroup) = 64 consecutive rows of one column
+// block; lane = tile during the per-candidate stage.
+template <bool PE>
+__global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4* __restrict__ frag,
+                                                      int stride) {
+  constexpr int C = 64;
+  constexpr int PB = 8;
+  constexpr int TS = 12;  // LDS stride (floats) of one tile's coefficients
+  __shared__ __attribute__((aligned(16))) float tb[2 * 64 * TS];
+  __shared__ float wdl[PE ? 64 * (C + 1) : 1];
+  const int lane = threadIdx.x;
+  const int nbk_cols = (int)(a.cols / C);
+  const int blk = blockIdx.x % nbk_cols;
+  const int64_t row0 = (int64_t)(blockIdx.x / nbk_cols) * 64;
+  const int n = lane & 15, g = lane >> 4;
+
+  // ---- u = d .* r fragments for the 4 groups of 16 tiles, split in three bf16 parts
+  u32x4 uh[4][2], um[4][2], ul[4][2];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    const int64_t row = row0 + 16 * nb + n;
+    const bool valid = row < a.rows;
+    const int64_t rr = valid ? row : a.rows - 1;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int jc = 32 * ks + 8 * g;
+      const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
+      float u[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float r = load_w_any2(a.W, a.w_dtype, base + e) - a.W0[base + e];
+        const float dj = PE ? a.d[base + e] : a.d[(int64_t)blk * C + jc + e];
+        u[e] = valid ? dj * r : 0.0f;
+      }
+      split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
+    }
+  }
+  const int64_t my_row = row0 + lane;
+  const bool my_valid = my_row < a.rows;
+  const int64_t my_off = (my_valid ? my_row : a.rows - 1) * a.cols + (int64_t)blk * C;
+  const int P = a.P;
+  if constexpr (PE) {
+    // WHT of this lane's tile weights, for the Gram gathers G_pq = WHT(d)[c_p ^ c_q] / C
+    float wd[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) wd[j] = a.d[my_off + j];
+#pragma unroll
+    for (int h = 1; h < C; h <<= 1)
+#pragma unroll
+      for (int i = 0; i < C; i += 2 * h)
+#pragma unroll
+        for (int k = i; k < i + h; ++k) {
+          const float x = wd[k], y = wd[k + h];
+          wd[k] = x + y;
+          wd[k + h] = x - y;
+        }
+#pragma unroll
+    for (int j = 0; j < C; ++j) wdl[lane * (C + 1) + j] = wd[j];
+  }
+  const float qmax = (float)((1 << (a.b - 1)) - 1);
+  const float inv_qmax = 1.0f / qmax;
+  const float invC = 1.0f / C;
+  const float lam = (float)a.lambda;
+  float tg[kTop];
+  int ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+
+  const int n_pairs = (a.S + 1) / 2;
+  for (int pair = 0; pair < n_pairs; ++pair) {
+    const u32x4* fp = frag + (size_t)pair * 2 * 64 + lane;
+    const bf16x8 A0 = as_bf16x8(fp[0]);
+    const bf16x8 A1 = as_bf16x8(fp[64]);
+    f32x4 acc[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(uh[nb][0]), c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(um[nb][0]), c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(ul[nb][0]), c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(uh[nb][1]), c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(um[nb][1]), c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(ul[nb][1]), c, 0, 0, 0);
+      acc[nb] = c;
+    }
+    // rows 4g..4g+3 = (seed g/2, columns 4(g&1)..+3) of tiles 16nb + n
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 64 + 16 * nb + n) * TS + 4 * (g & 1)]) = acc[nb];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int s = 2 * pair + k;
+      if (s >= a.S) break;
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS]);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4]);
+      float bv[PB] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+#pragma unroll
+      for (int p = 0; p < PB; ++p) bv[p] *= 0.125f;  // 1/sqrt(64)
+      float L[PB][PB], inv[PB], eps;
+      if constexpr (PE) {
+        const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
+        int c[PB];
+#pragma unroll
+        for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
+        const float* wrow = &wdl[lane * (C + 1)];
+        eps = lam * wrow[0] * invC;
+#pragma unroll
+        for (int p = 0; p < PB; ++p)
+#pragma unroll
+          for (int q = 0; q <= p; ++q) {
+            float acc2;
+            if (p < P && q < P) acc2 = wrow[c[p] ^ c[q]] * invC + (p == q ? eps : 0.0f);
+            else acc2 = (p == q) ? 1.0f : 0.0f;
+#pragma unroll
+            for (int kk = 0; kk < q; ++kk) acc2 -= L[p][kk] * L[q][kk];
+            if (p == q) {
+              L[p][p] = sqrtf(fmaxf(acc2, 1e-30f));
+              inv[p] = 1.0f / L[p][p];
+            } else {
+              L[p][q] = acc2 * inv[q];
+            }
+          }
+      } else {
+        const float* f = a.colfac + ((size_t)blk * a.S + s) * stride;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+#pragma unroll
+          for (int q = 0; q <= p; ++q) L[p][q] = f[tri2(p, q)];
+          inv[p] = f[PB * (PB + 1) / 2 + p];
+        }
+        eps = f[PB * (PB + 1) / 2 + PB];
+      }
+      float z[PB], al[PB];
+#pragma unroll
+      for (int p = 0; p < PB; ++p) {
+        float t = bv[p];
+#pragma unroll
+        for (int kk = 0; kk < p; ++kk) t -= L[p][kk] * z[kk];
+        z[p] = t * inv[p];
+      }
+#pragma unroll
+      for (int p = PB - 1; p >= 0; --p) {
+        float t = z[p];
+#pragma unroll
+        for (int kk = p + 1; kk < PB; ++kk) t -= L[kk][p] * al[kk];
+        al[p] = t * inv[p];
+      }
+      float m = 0.0f;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
+      const float sc = __half2float(__ushort_as_half(scale_bits_f32(m * inv_qmax)));
+      float gsc = 0.0f;
+      if (sc > 0.0f) {
+        const float isc = 1.0f / sc;
+        float q[PB], t1 = 0.0f, qq = 0.0f;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+          q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+          t1 += q[p] * bv[p];
+          qq += q[p] * q[p];
+        }
+        float quad = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < PB; ++kk) {
+          float y = 0.0f;
+#pragma unroll
+          for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
+          quad += y * y;
+        }
+        quad -= eps * qq;
+        gsc = sc * (2.0f * t1 - sc * quad);
+      }
+      float cg = gsc;
+      int cs_ = s;
+#pragma unroll
+      for (int kk = 0; kk < kTop; ++kk) {
+        if (cg > tg[kk]) {
+          const float tgk = tg[kk];
+          const int tsk = ts[kk];
+          tg[kk] = cg; ts[kk] = cs_;
+          cg = tgk; cs_ = tsk;
+        }
+      }
+    }
+    // the next pair overwrites tb: finish these reads first
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  }
+  if (my_valid) {
+    const int64_t t = my_row * nbk_cols + blk;
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      a.top_gain[t * kTop + k] = tg[k];
+      a.top_seed[t * kTop + k] = (uint16_t)ts[k];
+    }
+  }
+}
+
+bool screen_mfma_supported(int C, int P) { return C == 64 && P >= 1 && P <= 8; }
+
+size_t mfma_frag_bytes(int C, int S) { return (size_t)((S + 1) / 2) * (C / 32) * 64 * 16; }
+
+hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
+  const int64_t n = (int64_t)((a.S + 1) / 2) * (a.C / 32) * 64;
+  hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
+                     static_cast<u32x4*>(frag));
+  const int nb = (int)(a.cols / a.C);
+  const int64_t waves = nb * ((a.rows + 63) / 64);
+  if (a.d_mode == AWSRC_D_PER_ELEM)
+    hipLaunchKernelGGL(k_screen_mfma64<true>, dim3((unsigned)waves), dim3(64), 0, st, a,
+                       static_cast<const u32x4*>(frag), colfac_stride(8));
+  else
+    hipLaunchKernelGGL(k_screen_mfma64<false>, dim3((unsigned)waves), dim3(64), 0, st, a,
+                       static_cast<const u32x4*>(frag), colfac_stride(8));
+  return hipGetLastError();
+}
+
+}  // namespace awsrc
