@@ -128,7 +128,7 @@ awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, in
  *  W        [rows, cols] fp32 or bf16 (w_dtype); W0 [rows, cols] fp32.
  *  d        AWSRC_D_PER_COL: [cols] activation second moments shared by all
  *           rows; AWSRC_D_PER_ELEM: [rows, cols] per-element weights.  d > 0.
- *  cols % C == 0.  T = rows * cols / C.
+ *  cols % C == 0.  T = rows * cols / C.  W, W0 and d are 16-byte aligned.
  *  seed_out [T] u16, code_out [T, P] i8, scale_out [T] fp16 bits,
  *  gain_out [T] f64 (weighted error reduction of the stored record; an
  *  all-zero record has gain 0), alpha_or_null [T, P] fp32 unquantized fit of

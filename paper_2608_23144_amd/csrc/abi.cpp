@@ -142,6 +142,8 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
   if (T == 0) return AWSRC_OK;
   if (!W || !W0 || !d || !seed_out || !code_out || !scale_out || !gain_out) return fail(AWSRC_EINVAL, "NULL buffer");
+  if ((reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(W0) | reinterpret_cast<uintptr_t>(d)) & 15)
+    return fail(AWSRC_EINVAL, "W, W0 and d must be 16-byte aligned");
   char* ws = static_cast<char*>(workspace);
   ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(ws), 256));
   EncodeArgs a{};
@@ -281,8 +283,11 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
 // ---------------------------------------------------------------- decode
 namespace {
 
+// Workspace: basis tables | tile bitmap | error counter | module tables
+// (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
+// host-to-device copy fills them).
 struct DecodeLayout {
-  size_t basis, bitmap, err, off, cols, ptr, total;
+  size_t basis, bitmap, err, tables, total;
 };
 
 DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod) {
@@ -290,10 +295,8 @@ DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod) {
   l.basis = align_up(basis_bytes(S, P), 256);
   l.bitmap = align_up((size_t)((T_total + 31) / 32) * 4, 256);
   l.err = 256;
-  l.off = align_up((size_t)(nmod + 1) * 8, 256);
-  l.cols = align_up((size_t)nmod * 8, 256);
-  l.ptr = align_up((size_t)nmod * 8, 256);
-  l.total = 256 + l.basis + l.bitmap + l.err + l.off + l.cols + l.ptr;
+  l.tables = align_up((size_t)(3 * nmod + 1) * 8, 256);
+  l.total = 256 + l.basis + l.bitmap + l.err + l.tables;
   return l;
 }
 
@@ -312,9 +315,10 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   ws += l.basis;
   a.bitmap = reinterpret_cast<uint32_t*>(ws); ws += l.bitmap;
   a.errors = reinterpret_cast<unsigned long long*>(ws); ws += l.err;
-  a.mod_tile_off = reinterpret_cast<const uint64_t*>(ws); ws += l.off;
-  a.mod_cols = reinterpret_cast<const int64_t*>(ws); ws += l.cols;
-  a.mod_ptr = reinterpret_cast<void* const*>(ws);
+  const uint32_t n = (uint32_t)pl->n_modules;
+  a.mod_tile_off = reinterpret_cast<const uint64_t*>(ws);
+  a.mod_cols = reinterpret_cast<const int64_t*>(ws + 8 * (size_t)(n + 1));
+  a.mod_ptr = reinterpret_cast<void* const*>(ws + 8 * (size_t)(2 * n + 1));
   return a;
 }
 
@@ -328,11 +332,13 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   if (!stream_bytes) return fail(AWSRC_EINVAL, "stream is NULL");
   if (n_modules < 1 || !rows || !cols) return fail(AWSRC_EINVAL, "bad module table");
   if (w0_dtype != AWSRC_DTYPE_F32 && w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w0_dtype %d", w0_dtype);
-  if (stream_len < (uint64_t)kHeaderFixed) return fail(AWSRC_ECORRUPT, "stream shorter than a header");
+  const uint64_t h_caller = kHeaderFixed + 8ull * (uint64_t)n_modules;
+  if (stream_len < h_caller) return fail(AWSRC_ECORRUPT, "stream shorter than a header for %d modules", n_modules);
   hipStream_t s = (hipStream_t)stream;
-  uint8_t fx[kHeaderFixed];
-  HIPCHK(hipMemcpyAsync(fx, stream_bytes, kHeaderFixed, hipMemcpyDeviceToHost, s));
+  std::vector<uint8_t> hdr(h_caller);
+  HIPCHK(hipMemcpyAsync(hdr.data(), stream_bytes, h_caller, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
+  const uint8_t* fx = hdr.data();
   if (memcmp(fx, "AWSR", 4) != 0) return fail(AWSRC_ECORRUPT, "bad magic");
   if (get_le(fx + 4, 2) != 1) return fail(AWSRC_ECORRUPT, "unsupported stream version");
   const uint32_t flags = (uint32_t)get_le(fx + 6, 2);
@@ -350,13 +356,12 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   if (L != rec_bytes(ib, (int)S, P, b)) return fail(AWSRC_ECORRUPT, "record size %d inconsistent with header", L);
   if ((int32_t)nmod != n_modules) return fail(AWSRC_ECORRUPT, "header has %u modules, caller %d", nmod, n_modules);
   const uint64_t h = kHeaderFixed + 8ull * nmod;
-  if (stream_len < h) return fail(AWSRC_ECORRUPT, "stream shorter than its header");
   if ((stream_len - h) % (uint64_t)L) return fail(AWSRC_ECORRUPT, "stream does not end on a record boundary");
-  std::vector<uint8_t> mt(8 * (size_t)nmod);
-  HIPCHK(hipMemcpyAsync(mt.data(), stream_bytes + kHeaderFixed, mt.size(), hipMemcpyDeviceToHost, s));
-  HIPCHK(hipStreamSynchronize(s));
-  std::vector<uint64_t> toff(nmod + 1, 0);
-  std::vector<int64_t> mcols(nmod);
+  const uint8_t* mt = fx + kHeaderFixed;
+  // host copy of the module tables: tile offsets [n+1] | cols [n] | W0 pointers [n]
+  std::vector<uint64_t> tabs(3 * (size_t)nmod + 1, 0);
+  uint64_t* toff = tabs.data();
+  int64_t* mcols = reinterpret_cast<int64_t*>(tabs.data() + nmod + 1);
   for (uint32_t m = 0; m < nmod; ++m) {
     const int64_t r = (int64_t)get_le(&mt[8 * m], 4), c = (int64_t)get_le(&mt[8 * m + 4], 4);
     if (r != rows[m] || c != cols[m]) return fail(AWSRC_ECORRUPT, "module %u shape %lldx%lld differs from caller's", m, (long long)r, (long long)c);
@@ -383,9 +388,8 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   pl.records = stream_bytes + h;
   pl.workspace = workspace;
   const DecodeArgs a = decode_args(&pl);
-  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), toff.data(), (nmod + 1) * 8, hipMemcpyHostToDevice, s));
-  HIPCHK(hipMemcpyAsync(const_cast<int64_t*>(a.mod_cols), mcols.data(), nmod * 8, hipMemcpyHostToDevice, s));
-  HIPCHK(hipMemcpyAsync(const_cast<void**>(a.mod_ptr), W0_ptrs, nmod * sizeof(void*), hipMemcpyHostToDevice, s));
+  memcpy(tabs.data() + 2 * (size_t)nmod + 1, W0_ptrs, nmod * sizeof(void*));
+  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), tabs.data(), tabs.size() * 8, hipMemcpyHostToDevice, s));
   HIPCHK(launch_gen_basis(key, C, P, (int)S, a.basis, s));
   HIPCHK(launch_decode_validate(a, s));
   unsigned long long nerr = 0;

@@ -9,6 +9,33 @@
 
 namespace awsrc {
 
+// Position of the m-th zero bit (0-based) among the low `width` bits of w.
+__device__ __forceinline__ int nth_zero(uint64_t w, int m, int width) {
+  uint64_t z = ~w;
+  if (width < 64) z &= (1ull << width) - 1ull;
+  int pos = 0;
+#pragma unroll
+  for (int half = 32; half >= 1; half >>= 1) {
+    const uint64_t lowmask = (1ull << half) - 1ull;
+    const int cnt = __popcll(z & lowmask);
+    if (m >= cnt) { m -= cnt; z >>= half; pos += half; }
+  }
+  return pos;
+}
+
+// Bit j of the result is parity(j & c) for j = 64*w .. 64*w + 63: the XOR of
+// the patterns "bit b of j" over the set bits b of c.
+__device__ __forceinline__ uint64_t hadamard_neg_word(int c, int w) {
+  const uint64_t pat[6] = {0xAAAAAAAAAAAAAAAAull, 0xCCCCCCCCCCCCCCCCull, 0xF0F0F0F0F0F0F0F0ull,
+                           0xFF00FF00FF00FF00ull, 0xFFFF0000FFFF0000ull, 0xFFFFFFFF00000000ull};
+  uint64_t x = 0ull;
+#pragma unroll
+  for (int b = 0; b < 6; ++b)
+    if ((c >> b) & 1) x ^= pat[b];
+  if (((c >> 6) & 1) && w == 1) x = ~x;
+  return x;
+}
+
 __global__ void k_gen_basis(uint64_t key, int C, int P, int S, uint64_t* __restrict__ sign,
                             uint64_t* __restrict__ mask, uint8_t* __restrict__ col) {
   const int s = blockIdx.x * blockDim.x + threadIdx.x;
@@ -20,28 +47,22 @@ __global__ void k_gen_basis(uint64_t key, int C, int P, int S, uint64_t* __restr
   if (C < 64) sw[0] &= (1ull << C) - 1ull;
   sign[2 * (size_t)s] = sw[0];
   sign[2 * (size_t)s + 1] = sw[1];
-
+  const uint64_t valid0 = C < 64 ? (1ull << C) - 1ull : ~0ull;
   uint64_t used[2] = {0ull, 0ull};
   for (int p = 0; p < P; ++p) {
     const uint64_t v = splitmix64(key, base + (uint64_t)(nw + p));
-    const uint32_t m = (uint32_t)(((v >> 32) * (uint64_t)(C - p)) >> 32);  // Lemire, [0, C-p)
-    int c = 0;
-    uint32_t seen = 0;
-    for (int j = 0; j < C; ++j) {  // the m-th smallest column not drawn yet
-      if ((used[j >> 6] >> (j & 63)) & 1ull) continue;
-      if (seen == m) { c = j; break; }
-      ++seen;
-    }
+    int m = (int)(((v >> 32) * (uint64_t)(C - p)) >> 32);  // Lemire multiply-shift into [0, C-p)
+    // the m-th smallest column not drawn yet
+    const int w0 = C < 64 ? C : 64;
+    const int z0 = w0 - __popcll(used[0] & valid0);
+    int c;
+    if (m < z0) c = nth_zero(used[0], m, w0);
+    else c = 64 + nth_zero(used[1], m - z0, 64);
     used[c >> 6] |= 1ull << (c & 63);
     col[(size_t)s * kMaxP + p] = (uint8_t)c;
     for (int w = 0; w < 2; ++w) {
       uint64_t mk = 0ull;
-      for (int jj = 0; jj < 64; ++jj) {
-        const int j = 64 * w + jj;
-        if (j >= C) break;
-        const uint64_t neg = ((uint64_t)__popc((unsigned)(j & c)) & 1ull) ^ ((sw[w] >> jj) & 1ull);
-        mk |= neg << jj;
-      }
+      if (w < nw) mk = (hadamard_neg_word(c, w) ^ sw[w]) & (w == 0 ? valid0 : ~0ull);
       mask[((size_t)s * P + p) * 2 + w] = mk;
     }
   }

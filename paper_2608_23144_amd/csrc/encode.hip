@@ -70,6 +70,21 @@ __device__ __forceinline__ void fwht(T (&v)[C]) {
 }  // namespace
 
 // ----------------------------------------------------------------------------
+// fp64 Walsh-Hadamard transform of each column block's weights (per-column
+// mode): the Gram entries of every seed are gathers from it.
+template <int C>
+__global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __restrict__ out) {
+  const int blk = blockIdx.x * blockDim.x + threadIdx.x;
+  if (blk >= nb) return;
+  double v[C];
+#pragma unroll
+  for (int j = 0; j < C; ++j) v[j] = (double)d[(int64_t)blk * C + j];
+  fwht<C>(v);
+#pragma unroll
+  for (int j = 0; j < C; ++j) out[(int64_t)blk * C + j] = v[j];
+}
+
+// ----------------------------------------------------------------------------
 // Per-column factor table: for each (column block, seed), G = B^T D B + eps I
 // in fp64, its Cholesky factor stored in fp32 for the screen:
 //   [packed lower L (PB(PB+1)/2)] [1/L_pp (PB)] [eps]
@@ -81,25 +96,17 @@ __global__ void k_col_factors(EncodeArgs a, int nb, int stride) {
   if (idx >= nb * a.S) return;
   const int blk = idx / a.S;
   const int s = idx - blk * a.S;
-  const float* dblk = a.d + (int64_t)blk * C;
+  const double* wd = a.wd64 + (int64_t)blk * C;  // WHT(d) of this block: G_pq = wd[c_p ^ c_q] / C
   const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
-  double sumd = 0.0;
-  for (int j = 0; j < C; ++j) sumd += (double)dblk[j];
-  const double eps = a.lambda * (sumd / C);
+  const double eps = a.lambda * (wd[0] / C);
   double G[PB][PB];
 #pragma unroll
   for (int p = 0; p < PB; ++p)
 #pragma unroll
     for (int q = 0; q <= p; ++q) {
       double g;
-      if (p < a.P && q < a.P) {
-        const int x = cs[p] ^ cs[q];
-        double acc = 0.0;
-        for (int j = 0; j < C; ++j) acc += (__popc((unsigned)(j & x)) & 1) ? -(double)dblk[j] : (double)dblk[j];
-        g = acc / C + (p == q ? eps : 0.0);
-      } else {
-        g = (p == q) ? 1.0 : 0.0;
-      }
+      if (p < a.P && q < a.P) g = wd[cs[p] ^ cs[q]] / C + (p == q ? eps : 0.0);
+      else g = (p == q) ? 1.0 : 0.0;
       G[p][q] = g;
     }
   // Cholesky (G is SPD: d > 0 and the columns are orthonormal)
@@ -272,27 +279,58 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 }
 
 // ----------------------------------------------------------------------------
-// fp64 Walsh-Hadamard transform of each column block's weights (per-column
-// mode): the Gram entries of every seed are gathers from it.
-template <int C>
-__global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __restrict__ out) {
-  const int blk = blockIdx.x * blockDim.x + threadIdx.x;
-  if (blk >= nb) return;
-  double v[C];
-#pragma unroll
-  for (int j = 0; j < C; ++j) v[j] = (double)d[(int64_t)blk * C + j];
-  fwht<C>(v);
-#pragma unroll
-  for (int j = 0; j < C; ++j) out[(int64_t)blk * C + j] = v[j];
-}
-
-// ----------------------------------------------------------------------------
 // fp64 re-score of the screened candidates; writes the encoder outputs.
 // For one (tile, seed): b = WHT(sigma .* d .* r)[c] / sqrt(C) and
 // G_pq = WHT(d)[c_p xor c_q] / C (+ eps on the diagonal), Cholesky solve,
 // fp16-scale quantization, and the gain 2 a^T b - a^T G0 a of the quantized
 // coefficients a (G0 = G without the ridge), all in fp64.  Each lane keeps
 // its transformed vector in a private LDS row for the data-dependent gathers.
+// Loads 8 consecutive weights of W (fp32 or bf16) starting at element i.
+__device__ __forceinline__ void load8_w(const void* W, int dt, int64_t i, float (&w)[8]) {
+  if (dt == AWSRC_DTYPE_F32) {
+    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(W) + i);
+    const float4 x = p[0], y = p[1];
+    w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w; w[4] = y.x; w[5] = y.y; w[6] = y.z; w[7] = y.w;
+  } else {
+    const uint4 x = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(W) + i);
+    const uint32_t v[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      w[2 * k] = __uint_as_float(v[k] << 16);
+      w[2 * k + 1] = __uint_as_float(v[k] & 0xFFFF0000u);
+    }
+  }
+}
+
+__device__ __forceinline__ void load8_f(const float* p, float (&w)[8]) {
+  const float4 x = reinterpret_cast<const float4*>(p)[0], y = reinterpret_cast<const float4*>(p)[1];
+  w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w; w[4] = y.x; w[5] = y.y; w[6] = y.z; w[7] = y.w;
+}
+
+// u_j = d_j r_j in fp64 (exact: a product of two fp32 values) into the lane's LDS row.
+template <int C, bool PE>
+__device__ __forceinline__ void tile_u64(const EncodeArgs& a, int64_t off, int blk, double* my, float* e32,
+                                          double* sumd) {
+  float e = 0.0f;
+  double sd = 0.0;
+#pragma unroll 2
+  for (int j0 = 0; j0 < C; j0 += 8) {
+    float w[8], w0[8], dj[8];
+    load8_w(a.W, a.w_dtype, off + j0, w);
+    load8_f(a.W0 + off + j0, w0);
+    load8_f(PE ? a.d + off + j0 : a.d + (int64_t)blk * C + j0, dj);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float r = w[k] - w0[k];
+      e += dj[k] * r * r;
+      sd += (double)dj[k];
+      my[j0 + k] = (double)dj[k] * (double)r;
+    }
+  }
+  *e32 = e;
+  *sumd = sd;
+}
+
 template <int C, int PB, bool PE>
 __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __restrict__ wdb) {
   constexpr int NT = (C == 128) ? 32 : 64;  // rows per workgroup (keeps the LDS rows under 64 KiB)
@@ -305,14 +343,10 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
   const int64_t off = row * a.cols + (int64_t)blk * C;
   const int64_t t = row * nb + blk;
   const int P = a.P;
-  float e32 = 0.0f;
-  double sumd = 0.0;
-  for (int j = 0; j < C; ++j) {
-    const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
-    const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
-    e32 += dj * r * r;
-    sumd += (double)dj;
-  }
+  float e32;
+  double sumd;
+  tile_u64<C, PE>(a, off, blk, my, &e32, &sumd);
+  bool row_is_u = true;  // my[] holds u (true) or a transformed vector (false)
   const double eps = a.lambda * (sumd / C);
   const double isq = 1.0 / sqrt((double)C);
   const int qmax = (1 << (a.b - 1)) - 1;
@@ -339,21 +373,25 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
     int c[PB];
 #pragma unroll
     for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
-    // projection through the fast transform of sigma .* d .* r
+    // projection through the fast transform of sigma .* u
+    if (!row_is_u) {
+      float e_, *ep = &e_;
+      double sd_;
+      tile_u64<C, PE>(a, off, blk, my, ep, &sd_);
+    }
     {
       double v[C];
       const uint64_t s0 = sw[0], s1 = sw[1];
 #pragma unroll
       for (int j = 0; j < C; ++j) {
-        const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
-        const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
-        const double u = (double)dj * (double)r;
+        const double u = my[j];
         const uint64_t sg = (j < 64) ? (s0 >> j) : (s1 >> (j - 64));
         v[j] = (sg & 1ull) ? -u : u;
       }
       fwht<C>(v);
 #pragma unroll
       for (int j = 0; j < C; ++j) my[j] = v[j];
+      row_is_u = false;
     }
     double bv[PB];
 #pragma unroll
@@ -363,7 +401,12 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
     if constexpr (PE) {
       double v[C];
 #pragma unroll
-      for (int j = 0; j < C; ++j) v[j] = (double)a.d[off + j];
+      for (int j0 = 0; j0 < C; j0 += 8) {
+        float dj[8];
+        load8_f(a.d + off + j0, dj);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[j0 + k] = (double)dj[k];
+      }
       fwht<C>(v);
 #pragma unroll
       for (int j = 0; j < C; ++j) my[j] = v[j];
@@ -468,6 +511,7 @@ template <int C, int PB>
 static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
   const int nb = (int)(a.cols / C);
   const int n = nb * a.S;
+  hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
   hipLaunchKernelGGL((k_col_factors<C, PB>), dim3((n + 63) / 64), dim3(64), 0, st, a, nb,
                      colfac_stride(PB));
   return hipGetLastError();
@@ -496,7 +540,6 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)nullptr);
   } else {
-    hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
     hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)a.wd64);
   }

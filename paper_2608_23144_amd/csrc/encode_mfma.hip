@@ -171,11 +171,20 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
 #pragma unroll
   for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
 
+  // Post-processing runs in "raw" units: b is left unscaled by 1/sqrt(C) = 1/8,
+  // so alpha, the scale and the gain come out 8, 8 and 64 times larger; the
+  // codes and the seed order are unchanged (scaling by a power of two commutes
+  // with the roundings), and the kept gains are rescaled once at the end.
   const int n_pairs = (a.S + 1) / 2;
+  const u32x4* fp = frag + lane;
+  u32x4 F0 = fp[0], F1 = fp[64];
   for (int pair = 0; pair < n_pairs; ++pair) {
-    const u32x4* fp = frag + (size_t)pair * 2 * 64 + lane;
-    const bf16x8 A0 = as_bf16x8(fp[0]);
-    const bf16x8 A1 = as_bf16x8(fp[64]);
+    const bf16x8 A0 = as_bf16x8(F0);
+    const bf16x8 A1 = as_bf16x8(F1);
+    if (pair + 1 < n_pairs) {  // fragments of the next pair, in flight during this one
+      F0 = fp[(size_t)(pair + 1) * 128];
+      F1 = fp[(size_t)(pair + 1) * 128 + 64];
+    }
     f32x4 acc[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
@@ -203,9 +212,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
       if (s >= a.S) break;
       const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS]);
       const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4]);
-      float bv[PB] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
-#pragma unroll
-      for (int p = 0; p < PB; ++p) bv[p] *= 0.125f;  // 1/sqrt(64)
+      const float bv[PB] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
       float L[PB][PB], inv[PB], eps;
       if constexpr (PE) {
         const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
@@ -225,7 +232,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
             for (int kk = 0; kk < q; ++kk) acc2 -= L[p][kk] * L[q][kk];
             if (p == q) {
               L[p][p] = sqrtf(fmaxf(acc2, 1e-30f));
-              inv[p] = 1.0f / L[p][p];
+              inv[p] = __builtin_amdgcn_rcpf(L[p][p]);
             } else {
               L[p][q] = acc2 * inv[q];
             }
@@ -259,38 +266,34 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
 #pragma unroll
       for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
       const float sc = __half2float(__ushort_as_half(scale_bits_f32(m * inv_qmax)));
-      float gsc = 0.0f;
-      if (sc > 0.0f) {
-        const float isc = 1.0f / sc;
-        float q[PB], t1 = 0.0f, qq = 0.0f;
+      const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+      float q[PB], t1 = 0.0f, qq = 0.0f;
 #pragma unroll
-        for (int p = 0; p < PB; ++p) {
-          q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
-          t1 += q[p] * bv[p];
-          qq += q[p] * q[p];
-        }
-        float quad = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < PB; ++kk) {
-          float y = 0.0f;
-#pragma unroll
-          for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
-          quad += y * y;
-        }
-        quad -= eps * qq;
-        gsc = sc * (2.0f * t1 - sc * quad);
+      for (int p = 0; p < PB; ++p) {
+        q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+        t1 += q[p] * bv[p];
+        qq += q[p] * q[p];
       }
-      float cg = gsc;
-      int cs_ = s;
+      float quad = 0.0f;
 #pragma unroll
-      for (int kk = 0; kk < kTop; ++kk) {
-        if (cg > tg[kk]) {
-          const float tgk = tg[kk];
-          const int tsk = ts[kk];
-          tg[kk] = cg; ts[kk] = cs_;
-          cg = tgk; cs_ = tsk;
-        }
+      for (int kk = 0; kk < PB; ++kk) {
+        float y = 0.0f;
+#pragma unroll
+        for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
+        quad += y * y;
       }
+      quad -= eps * qq;
+      const float gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
+      // branch-free insertion into the descending top list (earlier seeds first on ties)
+      const bool c0 = gsc > tg[0], c1 = gsc > tg[1], c2 = gsc > tg[2], c3 = gsc > tg[3];
+      tg[3] = c2 ? tg[2] : (c3 ? gsc : tg[3]);
+      ts[3] = c2 ? ts[2] : (c3 ? s : ts[3]);
+      tg[2] = c1 ? tg[1] : (c2 ? gsc : tg[2]);
+      ts[2] = c1 ? ts[1] : (c2 ? s : ts[2]);
+      tg[1] = c0 ? tg[0] : (c1 ? gsc : tg[1]);
+      ts[1] = c0 ? ts[0] : (c1 ? s : ts[1]);
+      tg[0] = c0 ? gsc : tg[0];
+      ts[0] = c0 ? s : ts[0];
     }
     // the next pair overwrites tb: finish these reads first
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -300,7 +303,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
     const int64_t t = my_row * nbk_cols + blk;
 #pragma unroll
     for (int k = 0; k < kTop; ++k) {
-      a.top_gain[t * kTop + k] = tg[k];
+      a.top_gain[t * kTop + k] = tg[k] * (1.0f / 64.0f);  // back to gain units
       a.top_seed[t * kTop + k] = (uint16_t)ts[k];
     }
   }

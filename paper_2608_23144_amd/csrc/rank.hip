@@ -16,10 +16,16 @@ namespace awsrc {
 
 constexpr int kThreads = 256;
 constexpr int kRounds = 16;
-constexpr int kItems = kThreads * kRounds;  // items per block in compaction and sorting
+constexpr int kItems = kThreads * kRounds;  // items per block in the compaction
+constexpr int kSortRounds = 4;
+constexpr int kSortItems = kThreads * kSortRounds;  // items per block in the radix sort
+constexpr int kSelBits = 12;                // radix-select digit width
+constexpr int kSelBins = 1 << kSelBits;
 
+// Positive doubles order like their bit patterns; the top (sign) bit is set on
+// eligible keys so that every eligible key exceeds every ineligible (zero) key.
 __device__ __forceinline__ uint64_t gain_key(double g) {
-  return g > 0.0 ? (uint64_t)__double_as_longlong(g) : 0ull;
+  return g > 0.0 ? ((uint64_t)__double_as_longlong(g) | (1ull << 63)) : 0ull;
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
@@ -49,19 +55,27 @@ __device__ __forceinline__ uint32_t block_scan_flag(bool f, uint32_t* sh_w, uint
 }
 
 // ---------------------------------------------------------------- eligibility
-__global__ void k_count_eligible(const double* __restrict__ gain, int64_t n, uint64_t* counter) {
+__global__ __launch_bounds__(kThreads) void k_count_eligible(const double* __restrict__ gain, int64_t n,
+                                                             uint64_t* counter) {
+  __shared__ uint32_t sw[kThreads / 64];
   uint32_t c = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     c += gain[i] > 0.0 ? 1u : 0u;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
-  if ((threadIdx.x & 63) == 0 && c) atomicAdd((unsigned long long*)counter, (unsigned long long)c);
+  if ((threadIdx.x & 63) == 0) sw[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int k = 0; k < kThreads / 64; ++k) t += sw[k];
+    if (t) atomicAdd((unsigned long long*)counter, (unsigned long long)t);
+  }
 }
 
 hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st) {
   int64_t blocks = (n + kThreads - 1) / kThreads;
-  if (blocks > 4096) blocks = 4096;
+  if (blocks > 512) blocks = 512;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_count_eligible, dim3((unsigned)blocks), dim3(kThreads), 0, st, gain, n,
                      counter);
@@ -69,60 +83,96 @@ hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counte
 }
 
 // ---------------------------------------------------------------- radix select
-// state: [0] prefix, [1] mask, [2] remaining, [3] unused, [4..260) histogram
+// state: [0] prefix, [1] mask, [2] remaining, [3] done, [4 ..) histogram.
+// Each pass histograms the next digit of the keys that match the prefix so
+// far; the pick moves into the bin holding the remaining-th largest key.  When
+// that whole bin is taken the search stops early: every key in the bin is
+// selected, so the lower digits no longer matter.
 __global__ void k_select_init(uint64_t* state, int64_t K) {
-  const int t = threadIdx.x;
-  if (t == 0) { state[0] = 0; state[1] = 0; state[2] = (uint64_t)K; state[3] = 0; }
-  state[4 + t] = 0;
+  if (threadIdx.x == 0) { state[0] = 0; state[1] = 0; state[2] = (uint64_t)K; state[3] = 0; }
+  for (int b = threadIdx.x; b < kSelBins; b += blockDim.x) state[4 + b] = 0;
 }
 
-__global__ void k_select_hist(const double* __restrict__ gain, int64_t n, uint64_t* state,
-                              int shift) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
+__global__ __launch_bounds__(256) void k_select_hist(const double* __restrict__ gain, int64_t n,
+                                                     uint64_t* state, int shift, int width) {
+  if (state[3]) return;
+  __shared__ uint32_t h[kSelBins];
+  for (int b = threadIdx.x; b < kSelBins; b += blockDim.x) h[b] = 0;
   __syncthreads();
   const uint64_t prefix = state[0], mask = state[1];
+  const uint64_t dm = (1ull << width) - 1ull;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t k = gain_key(gain[i]);
-    if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & 255u], 1u);
+    if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
   }
   __syncthreads();
-  if (h[threadIdx.x]) atomicAdd((unsigned long long*)&state[4 + threadIdx.x], (unsigned long long)h[threadIdx.x]);
+  for (int b = threadIdx.x; b < (1 << width); b += blockDim.x)
+    if (h[b]) atomicAdd((unsigned long long*)&state[4 + b], (unsigned long long)h[b]);
 }
 
-__global__ void k_select_pick(uint64_t* state, int shift) {
-  if (threadIdx.x == 0) {
-    uint64_t cum = 0;
-    const uint64_t rem = state[2];
-    for (int bin = 255; bin >= 0; --bin) {
+// One block of 1024 threads: thread t owns bins counted from the top.
+__global__ __launch_bounds__(1024) void k_select_pick(uint64_t* state, int shift, int width) {
+  if (state[3]) return;
+  __shared__ uint64_t sc[1024];
+  __shared__ uint64_t found[3];
+  const int nbins = 1 << width;
+  const int bpt = nbins >= 1024 ? nbins / 1024 : 1;
+  const int t = threadIdx.x;
+  const uint64_t rem = state[2];
+  uint64_t local = 0;
+  for (int i = 0; i < bpt; ++i) {
+    const int r = t * bpt + i;  // rank from the top
+    if (r < nbins) local += state[4 + (nbins - 1 - r)];
+  }
+  sc[t] = local;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const uint64_t v = t >= off ? sc[t - off] : 0;
+    __syncthreads();
+    sc[t] += v;
+    __syncthreads();
+  }
+  const uint64_t excl = sc[t] - local;
+  if (excl < rem && rem <= sc[t]) {
+    uint64_t cum = excl;
+    for (int i = 0; i < bpt; ++i) {
+      const int r = t * bpt + i;
+      if (r >= nbins) break;
+      const int bin = nbins - 1 - r;
       const uint64_t c = state[4 + bin];
       if (cum + c >= rem) {
-        state[0] |= (uint64_t)bin << shift;
-        state[1] |= 255ull << shift;
-        state[2] = rem - cum;
+        found[0] = (uint64_t)bin;
+        found[1] = rem - cum;
+        found[2] = (c == rem - cum) ? 1ull : 0ull;
         break;
       }
       cum += c;
     }
   }
   __syncthreads();
-  state[4 + threadIdx.x] = 0;
+  if (t == 0) {
+    state[0] |= found[0] << shift;
+    state[1] |= ((1ull << width) - 1ull) << shift;
+    state[2] = found[1];
+    state[3] = found[2];
+  }
+  for (int b = t; b < nbins; b += 1024) state[4 + b] = 0;
 }
 
 // ---------------------------------------------------------------- compaction
 __global__ __launch_bounds__(kThreads) void k_compact_count(const double* __restrict__ gain, int64_t n,
                                                             const uint64_t* __restrict__ state,
                                                             uint64_t* blk_gt, uint64_t* blk_eq) {
-  const uint64_t kstar = state[0];
+  const uint64_t prefix = state[0], mask = state[1];
   uint32_t gt = 0, eq = 0;
   const int64_t base = (int64_t)blockIdx.x * kItems;
   for (int r = 0; r < kRounds; ++r) {
     const int64_t i = base + r * kThreads + threadIdx.x;
     if (i < n) {
-      const uint64_t k = gain_key(gain[i]);
-      gt += k > kstar;
-      eq += k == kstar;
+      const uint64_t k = gain_key(gain[i]) & mask;
+      gt += k > prefix;
+      eq += k == prefix;
     }
   }
   __shared__ uint32_t s_gt[kThreads / 64], s_eq[kThreads / 64];
@@ -191,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
                                                             uint64_t* __restrict__ keys_out,
                                                             uint32_t* __restrict__ vals_out) {
   __shared__ uint32_t sh_w[kThreads / 64];
-  const uint64_t kstar = state[0];
+  const uint64_t prefix = state[0], mask = state[1];
   const uint64_t rem = state[2];
   uint64_t eq_run = eq_off[blockIdx.x];
   uint64_t sel_run = sel_off[blockIdx.x];
@@ -200,8 +250,8 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
     const int64_t i = base + r * kThreads + threadIdx.x;
     uint64_t k = 0;
     if (i < n) k = gain_key(gain[i]);
-    const bool gt = (i < n) && k > kstar;
-    const bool eq = (i < n) && k == kstar;
+    const bool gt = (i < n) && (k & mask) > prefix;
+    const bool eq = (i < n) && (k & mask) == prefix;
     uint32_t eq_tot, sel_tot;
     const uint32_t eq_rank = block_scan_flag(eq, sh_w, &eq_tot);
     const bool take = gt || (eq && (eq_run + eq_rank) < rem);
@@ -221,8 +271,8 @@ __global__ __launch_bounds__(kThreads) void k_sort_hist(const uint64_t* __restri
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kItems;
-  for (int r = 0; r < kRounds; ++r) {
+  const int64_t base = (int64_t)blockIdx.x * kSortItems;
+  for (int r = 0; r < kSortRounds; ++r) {
     const int64_t i = base + r * kThreads + threadIdx.x;
     if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
   }
@@ -230,25 +280,28 @@ __global__ __launch_bounds__(kThreads) void k_sort_hist(const uint64_t* __restri
   hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
 }
 
-// Exclusive scan of n u32 values in place (single block).
+// Exclusive scan of n u32 values in place (single block): each thread scans a
+// contiguous chunk serially, one block-wide scan combines the chunk totals.
 __global__ __launch_bounds__(1024) void k_scan_u32(uint32_t* v, int64_t n) {
   __shared__ uint32_t sh[1024];
-  uint32_t carry = 0;
-  for (int64_t c0 = 0; c0 < n; c0 += 1024) {
-    const int64_t i = c0 + threadIdx.x;
-    const uint32_t x = i < n ? v[i] : 0u;
-    sh[threadIdx.x] = x;
+  const int64_t per = (n + 1023) / 1024;
+  const int64_t b0 = threadIdx.x * per;
+  const int64_t b1 = b0 + per < n ? b0 + per : n;
+  uint32_t tot = 0;
+  for (int64_t i = b0; i < b1; ++i) tot += v[i];
+  sh[threadIdx.x] = tot;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const uint32_t y = threadIdx.x >= off ? sh[threadIdx.x - off] : 0u;
     __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-      const uint32_t y = threadIdx.x >= off ? sh[threadIdx.x - off] : 0u;
-      __syncthreads();
-      sh[threadIdx.x] += y;
-      __syncthreads();
-    }
-    if (i < n) v[i] = carry + sh[threadIdx.x] - x;
-    const uint32_t tot = sh[1023];
+    sh[threadIdx.x] += y;
     __syncthreads();
-    carry += tot;
+  }
+  uint32_t run = sh[threadIdx.x] - tot;
+  for (int64_t i = b0; i < b1; ++i) {
+    const uint32_t x = v[i];
+    v[i] = run;
+    run += x;
   }
 }
 
@@ -262,8 +315,8 @@ __global__ __launch_bounds__(kThreads) void k_sort_scatter(const uint64_t* __res
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   run[threadIdx.x] = offs[(int64_t)threadIdx.x * nblk + blockIdx.x];
-  const int64_t base = (int64_t)blockIdx.x * kItems;
-  for (int r = 0; r < kRounds; ++r) {
+  const int64_t base = (int64_t)blockIdx.x * kSortItems;
+  for (int r = 0; r < kSortRounds; ++r) {
     const int64_t i = base + r * kThreads + threadIdx.x;
     const bool valid = i < n;
     uint64_t k = 0;
@@ -304,21 +357,21 @@ __global__ __launch_bounds__(kThreads) void k_sort_scatter(const uint64_t* __res
 size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
   const size_t cap = k_cap ? k_cap : 1;
   const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
-  const size_t nb_s = (cap + kItems - 1) / kItems + 1;
+  const size_t nb_s = (cap + kSortItems - 1) / kSortItems + 1;
   const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
   size_t b = 0;
   b += align_up(cap * 8, 256) * 2;
   b += align_up(cap * 4, 256) * 2;
   b += align_up(256 * max_blocks * 4, 256);
   b += align_up((max_blocks + 1) * 8, 256) * 2;
-  b += align_up(264 * 8, 256);
+  b += align_up((4 + kSelBins) * 8, 256);
   return b;
 }
 
 RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
   const size_t cap = k_cap ? k_cap : 1;
   const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
-  const size_t nb_s = (cap + kItems - 1) / kItems + 1;
+  const size_t nb_s = (cap + kSortItems - 1) / kSortItems + 1;
   const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
   char* p = static_cast<char*>(base);
   RankWs w;
@@ -339,13 +392,16 @@ hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64
                                 const RankWs& ws, hipStream_t st) {
   if (K <= 0) return hipSuccess;
   const double* g = gain + t0;
-  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(256), 0, st, ws.state, K);
+  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(1024), 0, st, ws.state, K);
   int64_t hb = (n + kThreads - 1) / kThreads;
-  if (hb > 2048) hb = 2048;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, shift);
-    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(256), 0, st, ws.state, shift);
+  if (hb > 512) hb = 512;
+  // digits from the top: 12, 12, 12, 12, 12 and 4 bits
+  for (int shift = 52; shift >= 0; shift -= kSelBits) {
+    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, shift, kSelBits);
+    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(1024), 0, st, ws.state, shift, kSelBits);
   }
+  hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, 0, 4);
+  hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(1024), 0, st, ws.state, 0, 4);
   const int64_t nbc = (n + kItems - 1) / kItems;
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state,
                      ws.blk_a, ws.blk_b);
@@ -353,7 +409,7 @@ hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
                      ws.blk_a, ws.blk_b, ws.keys_a, ws.vals_a);
   // sort the K survivors: 8 stable passes, ascending on ~key
-  const int64_t nbs = (K + kItems - 1) / kItems;
+  const int64_t nbs = (K + kSortItems - 1) / kSortItems;
   uint64_t* ki = ws.keys_a;
   uint64_t* ko = ws.keys_b;
   uint32_t* vi = ws.vals_a;
