@@ -111,6 +111,7 @@ const char* awsrc_last_error(void);
  *  scale_f16  [rows, cols/group] fp16 bit patterns.
  *  zero       [rows, cols/group] u8.
  *  W0_or_null [rows, cols] fp32 dequantized backbone, or NULL to skip.
+ *  W and W0 are 16-byte aligned, codes 4-byte aligned.
  */
 awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, int64_t cols,
                                 int32_t group, uint8_t* codes, uint16_t* scale_f16, uint8_t* zero,
@@ -184,10 +185,11 @@ awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modules,
  * not touched; an empty stream leaves W0 bit-identical.
  *
  * awsrc_decode_add = awsrc_decode_prepare + awsrc_decode_apply.
- *  stream_bytes  device pointer to stream_len bytes; K = (stream_len - h) / L_rec.
+ *  stream_bytes  device pointer (8-byte aligned) to stream_len bytes;
+ *                K = (stream_len - h) / L_rec.
  *  W0_ptrs       host array [n_modules] of device pointers to each module's
- *                W0, [rows, cols] in w0_dtype; bf16 targets are rounded to
- *                nearest even after the fp32 add.
+ *                W0, [rows, cols] in w0_dtype, 16-byte aligned; bf16
+ *                targets are rounded to nearest even after the fp32 add.
  *  rows, cols    host arrays [n_modules]; must match the stream header.
  * The header and every record are validated before anything is written (magic,
  * version, parameters, length on a record boundary, tile index < T_total,

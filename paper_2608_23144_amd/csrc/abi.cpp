@@ -109,6 +109,9 @@ extern "C" awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64
   if (rows < 0 || cols < 1 || cols % group) return fail(AWSRC_EINVAL, "cols=%lld must be a positive multiple of group", (long long)cols);
   if (rows == 0) return AWSRC_OK;
   if (!W || !codes || !scale_f16 || !zero) return fail(AWSRC_EINVAL, "NULL buffer");
+  if ((reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(W0_or_null)) & 15 ||
+      reinterpret_cast<uintptr_t>(codes) & 3)
+    return fail(AWSRC_EINVAL, "W and W0 must be 16-byte aligned, codes 4-byte aligned");
   HIPCHK(launch_backbone(W, w_dtype, rows, cols, group, codes, scale_f16, zero, W0_or_null,
                          (hipStream_t)stream));
   return AWSRC_OK;
@@ -244,8 +247,9 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
     elig_total += (int64_t)ne;
     if ((uint64_t)(h + (K_total + k) * L) > stream_cap) return fail(AWSRC_ENOSPC, "stream capacity %llu < %lld bytes", (unsigned long long)stream_cap, (long long)(h + (K_total + k) * L));
     if (k > 0) {
-      HIPCHK(launch_select_sorted(gain, seg_t0[i], seg_n[i], k, rw, s));
-      HIPCHK(launch_pack(rw.vals_a, k, seed, code, scale, p->P, p->b, ib, sb, (int)L,
+      const SortItem* sorted = nullptr;
+      HIPCHK(launch_select_sorted(gain, seg_t0[i], seg_n[i], k, rw, &sorted, s));
+      HIPCHK(launch_pack(sorted, k, seed, code, scale, p->P, p->b, ib, sb, (int)L,
                          stream_out + h + K_total * L, s));
     }
     K_total += k;
@@ -330,6 +334,7 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
                                              size_t* ws_bytes, void* stream) {
   if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
   if (!stream_bytes) return fail(AWSRC_EINVAL, "stream is NULL");
+  if (reinterpret_cast<uintptr_t>(stream_bytes) & 7) return fail(AWSRC_EINVAL, "stream must be 8-byte aligned");
   if (n_modules < 1 || !rows || !cols) return fail(AWSRC_EINVAL, "bad module table");
   if (w0_dtype != AWSRC_DTYPE_F32 && w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w0_dtype %d", w0_dtype);
   const uint64_t h_caller = kHeaderFixed + 8ull * (uint64_t)n_modules;
@@ -377,8 +382,12 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   if (*ws_bytes < lay.total) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, lay.total);
   if (!plan) return fail(AWSRC_EINVAL, "plan is NULL");
   if (!W0_ptrs) return fail(AWSRC_EINVAL, "W0_ptrs is NULL");
-  for (int m = 0; m < n_modules; ++m)
+  const uintptr_t w0_align = 16;
+  for (int m = 0; m < n_modules; ++m) {
     if (!W0_ptrs[m]) return fail(AWSRC_EINVAL, "W0 pointer %d is NULL", m);
+    if (reinterpret_cast<uintptr_t>(W0_ptrs[m]) % w0_align)
+      return fail(AWSRC_EINVAL, "W0 pointer %d must be 16-byte aligned", m);
+  }
 
   awsrc_decode_plan pl{};
   pl.C = C; pl.P = P; pl.b = b; pl.S = (int32_t)S;

@@ -12,7 +12,7 @@ namespace awsrc {
 
 constexpr int kMaxP = 16;        // basis columns per seed
 constexpr int kMaxC = 128;       // tile length
-constexpr int kTop = 4;          // screened candidates kept per tile for the fp64 re-score
+constexpr int kTop = 2;          // screened candidates kept per tile for the fp64 re-score
 
 // splitmix64 (Steele, Lea & Flood 2014): output n of the stream started at
 // state `key`; the state advances by the golden-ratio increment before each
@@ -28,17 +28,19 @@ __host__ __device__ __forceinline__ uint64_t splitmix64(uint64_t key, uint64_t n
 //   sign[s][w]      sign words, bit j%64 of word j/64 set <=> sigma_j = -1
 //   mask[s][p][w]   bit j set <=> B_s[j, p] < 0, i.e. sigma_j xor parity(j & c_p)
 //   col[s][p]       the P selected Hadamard columns (draw order)
+//   tsign[s][j]     bit p set <=> B_s[j, p] < 0 (the mask transposed, one u16 per coordinate)
 struct BasisTables {
   uint64_t* sign;
   uint64_t* mask;
   uint8_t* col;
+  uint16_t* tsign;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline size_t basis_bytes(int S, int P) {
   return align_up((size_t)S * 2 * 8, 256) + align_up((size_t)S * P * 2 * 8, 256) +
-         align_up((size_t)S * kMaxP, 256);
+         align_up((size_t)S * kMaxP, 256) + align_up((size_t)S * kMaxC * 2, 256);
 }
 
 inline BasisTables carve_basis(void* base, int S, int P) {
@@ -49,6 +51,8 @@ inline BasisTables carve_basis(void* base, int S, int P) {
   t.mask = reinterpret_cast<uint64_t*>(p);
   p += align_up((size_t)S * P * 2 * 8, 256);
   t.col = reinterpret_cast<uint8_t*>(p);
+  p += align_up((size_t)S * kMaxP, 256);
+  t.tsign = reinterpret_cast<uint16_t*>(p);
   return t;
 }
 
@@ -100,12 +104,16 @@ hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- ranking
+// One survivor of the selection: ~(gain key) and its global tile index.
+struct __attribute__((aligned(16))) SortItem {
+  uint64_t key;
+  uint32_t tile;
+  uint32_t pad;
+};
+
 struct RankWs {
-  uint64_t* keys_a;      // [cap] sort keys (ping)
-  uint64_t* keys_b;      // [cap] (pong)
-  uint32_t* vals_a;      // [cap] global tile index (ping)
-  uint32_t* vals_b;      // [cap]
-  uint32_t* hist;        // [256 * max_blocks] digit-major block histograms / offsets
+  SortItem* items_a;     // [cap] survivors (ping)
+  SortItem* items_b;     // [cap] (pong)
   uint64_t* blk_a;       // [max_blocks + 1] per-block counts / offsets
   uint64_t* blk_b;       // [max_blocks + 1]
   uint64_t* state;       // select state: prefix, mask, remaining, eligible count, hist[256]
@@ -116,11 +124,11 @@ size_t rank_ws_bytes(size_t n_tiles, size_t k_cap);
 RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap);
 
 hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st);
-// Stable top-K of one tile segment, ordered by (gain desc, tile asc); writes
-// the global tile indices of the K records into ws.vals_a[0..K).
+// Top-K of one tile segment, ordered by (gain desc, tile asc); *sorted is set
+// to the workspace array that receives the K items in that order.
 hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
-                                const RankWs& ws, hipStream_t st);
-hipError_t launch_pack(const uint32_t* tiles, int64_t K, const uint16_t* seed, const int8_t* code,
+                                const RankWs& ws, const SortItem** sorted, hipStream_t st);
+hipError_t launch_pack(const SortItem* sorted, int64_t K, const uint16_t* seed, const int8_t* code,
                        const uint16_t* scale, int P, int b, int idx_bits, int seed_bits,
                        int L_rec, uint8_t* out, hipStream_t st);
 

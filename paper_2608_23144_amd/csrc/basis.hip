@@ -4,7 +4,8 @@
 // columns from the splitmix64 counter stream and precomputes, for every
 // selected column p, the C-bit pattern of negative entries of B_s[:, p]
 // (sigma_j xor parity(j & c_p)), which the encoder and decoder kernels use
-// instead of regenerating the basis per tile.
+// instead of regenerating the basis per tile; a second kernel transposes the
+// patterns into one u16 of P sign bits per coordinate for the decoder.
 #include "awsrc_internal.h"
 
 namespace awsrc {
@@ -68,11 +69,27 @@ __global__ void k_gen_basis(uint64_t key, int C, int P, int S, uint64_t* __restr
   }
 }
 
+// Transposed signs, one thread per (seed, coordinate j): the P sign bits of
+// row j of B_s packed into one u16.
+__global__ void k_basis_tsign(int C, int P, int S, const uint64_t* __restrict__ mask,
+                              uint16_t* __restrict__ tsign) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)S * C) return;
+  const int s = (int)(i / C), j = (int)(i % C);
+  uint32_t t = 0;
+  for (int p = 0; p < P; ++p)
+    t |= (uint32_t)((mask[((size_t)s * P + p) * 2 + (j >> 6)] >> (j & 63)) & 1ull) << p;
+  tsign[(size_t)s * kMaxC + j] = (uint16_t)t;
+}
+
 hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, BasisTables t, hipStream_t st) {
   const int threads = 64;
   const int blocks = (S + threads - 1) / threads;
   hipLaunchKernelGGL(k_gen_basis, dim3(blocks), dim3(threads), 0, st, key, C, P, S, t.sign, t.mask,
                      t.col);
+  const int64_t n = (int64_t)S * C;
+  hipLaunchKernelGGL(k_basis_tsign, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, C, P, S,
+                     t.mask, t.tsign);
   return hipGetLastError();
 }
 

@@ -5,12 +5,14 @@
 //            and a bitmap over tiles that catches a tile appearing twice
 //            (records of a valid stream touch disjoint tiles, which is what
 //            lets the apply pass run without atomics or ordering).
-// apply    - C/4 lanes per record, four consecutive weights per lane; each
+// apply    - C/8 lanes per record, eight consecutive weights per lane; each
 //            weight gets rhat_j = (1/sqrt(C)) sum_p (+-1) scale*q_p with the
-//            signs read from the precomputed negative-entry masks of B_s.
+//            signs of row j of B_s read from the transposed sign table.
 #include "awsrc_internal.h"
 
 namespace awsrc {
+
+constexpr int kLdsModules = 256;  // module tables up to this size are staged in LDS
 
 struct Rec {
   uint64_t idx;
@@ -28,9 +30,41 @@ __device__ __forceinline__ uint64_t get_bits(const uint64_t (&w)[3], int& pos, i
   return nbits == 64 ? v : (v & ((1ull << nbits) - 1ull));
 }
 
-__device__ __forceinline__ Rec parse(const uint8_t* r, const DecodeArgs& a) {
-  uint64_t w[3] = {0, 0, 0};
-  for (int k = 0; k < a.L_rec; ++k) w[k >> 3] |= (uint64_t)r[k] << (8 * (k & 7));
+// Record i of the stream, read with aligned 4-byte loads.  The record area
+// starts h = 40 + 8n bytes into an 8-byte aligned stream, so it is 4-byte
+// aligned.  A record of at most 32 + 16 + 16*8 + 16 = 192 bits (24 bytes)
+// spans at most 7 words from its first word; records whose 7 words all lie
+// in the record area load them unconditionally (independent loads in flight
+// together), the last few records take a guarded byte-wise path.
+__device__ __forceinline__ Rec parse(const DecodeArgs& a, int64_t i) {
+  const int64_t o = i * a.L_rec;
+  const int64_t total = a.K * a.L_rec;
+  const int64_t d0 = o >> 2;
+  const int sh = (int)(o & 3) * 8;
+  const uint32_t* r32 = reinterpret_cast<const uint32_t*>(a.recs);
+  uint32_t wd[7];
+  if (d0 + 7 <= (total >> 2)) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) wd[k] = r32[d0 + k];
+  } else {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) {
+      uint32_t v = 0;
+      for (int b = 0; b < 4; ++b) {
+        const int64_t at = (d0 + k) * 4 + b;
+        if (at < o + a.L_rec && at < total) v |= (uint32_t)a.recs[at] << (8 * b);
+      }
+      wd[k] = v;
+    }
+  }
+  uint64_t w[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const uint64_t lo = (uint64_t)wd[2 * k] | ((uint64_t)wd[2 * k + 1] << 32);
+    const uint64_t hi = (uint64_t)wd[2 * k + 2];
+    w[k] = sh ? ((lo >> sh) | (hi << (64 - sh))) : lo;
+  }
+  // bits beyond the record are not used: every field lies within L_rec bytes
   Rec out;
   int pos = 0;
   out.idx = get_bits(w, pos, a.idx_bits);
@@ -53,7 +87,7 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n) {
 __global__ void k_decode_validate(DecodeArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.K) return;
-  const Rec r = parse(a.recs + i * a.L_rec, a);
+  const Rec r = parse(a, i);
   const int qmax = (1 << (a.b - 1)) - 1;
   bool bad = r.idx >= a.T_total || r.seed >= (uint32_t)a.S;
   for (int p = 0; p < a.P; ++p) bad |= r.q[p] < -qmax || r.q[p] > qmax;
@@ -68,47 +102,77 @@ __global__ void k_decode_validate(DecodeArgs a) {
 
 template <int C, typename TW>
 __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
-  constexpr int LPR = C / 4;           // lanes per record
+  constexpr int LPR = C / 8;           // lanes per record, eight weights each
   constexpr int RPB = 256 / LPR;       // records per block
+  // module table staged in LDS when it is small enough (the common case)
+  __shared__ uint64_t s_off[kLdsModules + 1];
+  __shared__ int64_t s_cols[kLdsModules];
+  __shared__ void* s_ptr[kLdsModules];
   const int sub = threadIdx.x % LPR;
   const int64_t i = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
-  if (i >= a.K) return;
-  const Rec r = parse(a.recs + i * a.L_rec, a);
-  // module of this global tile index
+  const bool valid = i < a.K;
+  const Rec r = parse(a, valid ? i : a.K - 1);
+  // signs of rows 8*sub .. 8*sub+7 of B_s, one u16 of P bits per row
+  const uint4 tsv = *reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)r.seed * kMaxC + sub * 8);
+  const bool lds_tab = a.n_modules <= kLdsModules;
+  if (lds_tab) {
+    for (int m = threadIdx.x; m <= a.n_modules; m += 256) {
+      s_off[m] = a.mod_tile_off[m];
+      if (m < a.n_modules) { s_cols[m] = a.mod_cols[m]; s_ptr[m] = a.mod_ptr[m]; }
+    }
+  }
+  __syncthreads();
+  if (!valid) return;
+  const uint64_t* off = lds_tab ? s_off : a.mod_tile_off;
   int lo = 0, hi = a.n_modules - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (a.mod_tile_off[mid] <= r.idx) lo = mid; else hi = mid - 1;
+    if (off[mid] <= r.idx) lo = mid; else hi = mid - 1;
   }
-  const int64_t cols = a.mod_cols[lo];
-  const int64_t local = (int64_t)(r.idx - a.mod_tile_off[lo]);
-  const int64_t nb = cols / C;
-  const int64_t row = local / nb;
-  const int64_t blk = local - row * nb;
-  const int64_t base = row * cols + blk * C + sub * 4;
+  const int64_t cols = lds_tab ? s_cols[lo] : a.mod_cols[lo];
+  TW* W0 = static_cast<TW*>(lds_tab ? s_ptr[lo] : a.mod_ptr[lo]);
+  // tile indices and tiles per row fit in 32 bits (T_total < 2^32)
+  const uint32_t local = (uint32_t)(r.idx - off[lo]);
+  const uint32_t nb = (uint32_t)(cols / C);
+  const uint32_t row = local / nb;
+  const uint32_t blk = local - row * nb;
+  const int64_t base = (int64_t)row * cols + (int64_t)blk * C + sub * 8;
   const float sc = __half2float(__ushort_as_half((uint16_t)r.scale));
   constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
                       : (C == 64) ? 0.125f : 0.08838834764831845f;
-  const uint64_t* mk = a.basis.mask + (size_t)r.seed * a.P * 2;
-  const int j0 = sub * 4;
-  float add[4] = {0.f, 0.f, 0.f, 0.f};
+  const uint32_t tw[4] = {tsv.x, tsv.y, tsv.z, tsv.w};
+  float add[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < a.P; ++p) {
     const float ah = sc * (float)r.q[p];
-    const uint64_t m = mk[2 * p + (j0 >> 6)] >> (j0 & 63);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) add[e] += ((m >> e) & 1ull) ? -ah : ah;
+    for (int e = 0; e < 8; ++e) add[e] += ((tw[e >> 1] >> (16 * (e & 1) + p)) & 1u) ? -ah : ah;
   }
-  TW* W0 = static_cast<TW*>(a.mod_ptr[lo]);
+  if constexpr (sizeof(TW) == 4) {
+    float4* q = reinterpret_cast<float4*>(W0 + base);
+    float4 v0 = q[0], v1 = q[1];
+    v0.x += add[0] * isq; v0.y += add[1] * isq; v0.z += add[2] * isq; v0.w += add[3] * isq;
+    v1.x += add[4] * isq; v1.y += add[5] * isq; v1.z += add[6] * isq; v1.w += add[7] * isq;
+    q[0] = v0;
+    q[1] = v1;
+  } else {
+    uint4* q = reinterpret_cast<uint4*>(W0 + base);
+    const uint4 v = *q;
+    const uint32_t in[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    if constexpr (sizeof(TW) == 4) {
-      W0[base + e] = W0[base + e] + add[e] * isq;
-    } else {
-      const float w = __uint_as_float((uint32_t)W0[base + e] << 16) + add[e] * isq;
-      uint32_t u = __float_as_uint(w);
-      u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest even (finite values)
-      W0[base + e] = (TW)(u >> 16);
+    for (int k = 0; k < 4; ++k) {
+      uint32_t h2 = 0;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint32_t bits = e ? (in[k] & 0xFFFF0000u) : (in[k] << 16);
+        const float w = __uint_as_float(bits) + add[2 * k + e] * isq;
+        uint32_t u = __float_as_uint(w);
+        u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest even (finite values)
+        h2 |= (u >> 16) << (16 * e);
+      }
+      o[k] = h2;
     }
+    *q = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -126,7 +190,7 @@ hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {
 
 template <int C>
 static hipError_t apply_c(const DecodeArgs& a, hipStream_t st) {
-  constexpr int RPB = 256 / (C / 4);
+  constexpr int RPB = 256 / (C / 8);
   const unsigned blocks = (unsigned)((a.K + RPB - 1) / RPB);
   if (a.w0_dtype == AWSRC_DTYPE_F32)
     hipLaunchKernelGGL((k_decode_apply<C, float>), dim3(blocks), dim3(256), 0, st, a);

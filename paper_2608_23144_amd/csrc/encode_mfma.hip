@@ -79,7 +79,7 @@ __device__ __forceinline__ void split3(const float (&u)[8], u32x4& hi, u32x4& mi
 // 32*ks + 8*(lane/16) + e.  Rows of absent seeds or columns are zero.
 __global__ void k_mfma_frags(BasisTables bt, int C, int P, int S, u32x4* __restrict__ frag) {
   const int nks = C / 32;
-  const int64_t n = (int64_t)((S + 1) / 2) * nks * 64;
+  const int64_t n = (int64_t)((S + 1) / 2 + 2) * nks * 64;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int lane = (int)(i % 64);
@@ -166,26 +166,21 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
   const float inv_qmax = 1.0f / qmax;
   const float invC = 1.0f / C;
   const float lam = (float)a.lambda;
-  float tg[kTop];
-  int ts[kTop];
-#pragma unroll
-  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+  float tg0 = -INFINITY, tg1 = -INFINITY;
+  int ts0 = 0, ts1 = 0;
 
   // Post-processing runs in "raw" units: b is left unscaled by 1/sqrt(C) = 1/8,
   // so alpha, the scale and the gain come out 8, 8 and 64 times larger; the
   // codes and the seed order are unchanged (scaling by a power of two commutes
   // with the roundings), and the kept gains are rescaled once at the end.
+  //
+  // Software pipeline: while the vector ALUs post-process seed pair k, the
+  // matrix cores compute the projections of pair k+1 (the fragment table is
+  // padded with zero pairs, so the last iterations need no special case).
   const int n_pairs = (a.S + 1) / 2;
   const u32x4* fp = frag + lane;
-  u32x4 F0 = fp[0], F1 = fp[64];
-  for (int pair = 0; pair < n_pairs; ++pair) {
-    const bf16x8 A0 = as_bf16x8(F0);
-    const bf16x8 A1 = as_bf16x8(F1);
-    if (pair + 1 < n_pairs) {  // fragments of the next pair, in flight during this one
-      F0 = fp[(size_t)(pair + 1) * 128];
-      F1 = fp[(size_t)(pair + 1) * 128 + 64];
-    }
-    f32x4 acc[4];
+  auto project = [&](const u32x4& F0, const u32x4& F1, f32x4 (&acc)[4]) {
+    const bf16x8 A0 = as_bf16x8(F0), A1 = as_bf16x8(F1);
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
       f32x4 c = {0.f, 0.f, 0.f, 0.f};
@@ -197,25 +192,46 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
       c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(ul[nb][1]), c, 0, 0, 0);
       acc[nb] = c;
     }
-    // rows 4g..4g+3 = (seed g/2, columns 4(g&1)..+3) of tiles 16nb + n
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
+  };
+  // rows 4g..4g+3 of the product = (seed g/2, columns 4(g&1)..+3) of tiles 16nb + n
+  auto stash = [&](const f32x4 (&acc)[4]) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
       *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 64 + 16 * nb + n) * TS + 4 * (g & 1)]) = acc[nb];
+  };
+  {
+    f32x4 acc[4];
+    project(fp[0], fp[64], acc);
+    stash(acc);
+  }
+  u32x4 F0 = fp[128], F1 = fp[192];
+  for (int pair = 0; pair < n_pairs; ++pair) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    float bk[2][PB];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS]);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4]);
+      bk[k][0] = b0[0]; bk[k][1] = b0[1]; bk[k][2] = b0[2]; bk[k][3] = b0[3];
+      bk[k][4] = b1[0]; bk[k][5] = b1[1]; bk[k][6] = b1[2]; bk[k][7] = b1[3];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    // projections of the next pair (zero rows past the last seed) and the prefetch after it
+    f32x4 accN[4];
+    project(F0, F1, accN);
+    F0 = fp[(size_t)(pair + 2) * 128];
+    F1 = fp[(size_t)(pair + 2) * 128 + 64];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int s = 2 * pair + k;
-      if (s >= a.S) break;
-      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS]);
-      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4]);
-      const float bv[PB] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+      const float* bv = bk[k];
       float L[PB][PB], inv[PB], eps;
       if constexpr (PE) {
-        const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
+        const int sc_ = s < a.S ? s : a.S - 1;
+        const uint8_t* cs = a.basis.col + (size_t)sc_ * kMaxP;
         int c[PB];
 #pragma unroll
         for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
@@ -238,7 +254,10 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
             }
           }
       } else {
-        const float* f = a.colfac + ((size_t)blk * a.S + s) * stride;
+        const int sc_ = s < a.S ? s : a.S - 1;
+        // uniform across the wavefront: read through the constant address space (scalar loads)
+        const __attribute__((address_space(4))) float* f =
+            (const __attribute__((address_space(4))) float*)(a.colfac + ((size_t)blk * a.S + sc_) * stride);
 #pragma unroll
         for (int p = 0; p < PB; ++p) {
 #pragma unroll
@@ -270,7 +289,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
       float q[PB], t1 = 0.0f, qq = 0.0f;
 #pragma unroll
       for (int p = 0; p < PB; ++p) {
-        q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+        q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
         t1 += q[p] * bv[p];
         qq += q[p] * q[p];
       }
@@ -283,38 +302,39 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
         quad += y * y;
       }
       quad -= eps * qq;
-      const float gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
-      // branch-free insertion into the descending top list (earlier seeds first on ties)
-      const bool c0 = gsc > tg[0], c1 = gsc > tg[1], c2 = gsc > tg[2], c3 = gsc > tg[3];
-      tg[3] = c2 ? tg[2] : (c3 ? gsc : tg[3]);
-      ts[3] = c2 ? ts[2] : (c3 ? s : ts[3]);
-      tg[2] = c1 ? tg[1] : (c2 ? gsc : tg[2]);
-      ts[2] = c1 ? ts[1] : (c2 ? s : ts[2]);
-      tg[1] = c0 ? tg[0] : (c1 ? gsc : tg[1]);
-      ts[1] = c0 ? ts[0] : (c1 ? s : ts[1]);
-      tg[0] = c0 ? gsc : tg[0];
-      ts[0] = c0 ? s : ts[0];
+      float gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
+      gsc = s < a.S ? gsc : -INFINITY;
+      // branch-free insertion into the top two (earlier seeds first among equals)
+      const bool c0 = gsc > tg0, c1 = gsc > tg1;
+      tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
+      ts1 = c0 ? ts0 : (c1 ? s : ts1);
+      tg0 = c0 ? gsc : tg0;
+      ts0 = c0 ? s : ts0;
     }
-    // the next pair overwrites tb: finish these reads first
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
+    // interleave the 24 matrix-core instructions with the vector work above
+#pragma unroll
+    for (int i = 0; i < 24; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+    }
+    stash(accN);
   }
   if (my_valid) {
     const int64_t t = my_row * nbk_cols + blk;
-#pragma unroll
-    for (int k = 0; k < kTop; ++k) {
-      a.top_gain[t * kTop + k] = tg[k] * (1.0f / 64.0f);  // back to gain units
-      a.top_seed[t * kTop + k] = (uint16_t)ts[k];
-    }
+    a.top_gain[t * kTop + 0] = tg0 * (1.0f / 64.0f);  // back to gain units
+    a.top_gain[t * kTop + 1] = tg1 * (1.0f / 64.0f);
+    a.top_seed[t * kTop + 0] = (uint16_t)ts0;
+    a.top_seed[t * kTop + 1] = (uint16_t)ts1;
   }
 }
 
 bool screen_mfma_supported(int C, int P) { return C == 64 && P >= 1 && P <= 8; }
 
-size_t mfma_frag_bytes(int C, int S) { return (size_t)((S + 1) / 2) * (C / 32) * 64 * 16; }
+// the table carries two zero pairs past the last seed (see the pipeline above)
+size_t mfma_frag_bytes(int C, int S) { return (size_t)((S + 1) / 2 + 2) * (C / 32) * 64 * 16; }
 
 hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
-  const int64_t n = (int64_t)((a.S + 1) / 2) * (a.C / 32) * 64;
+  const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
   hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
                      static_cast<u32x4*>(frag));
   const int nb = (int)(a.cols / a.C);

@@ -7,8 +7,9 @@
 //     largest key k* and how many records equal to k* are taken;
 //  2. a stable compaction keeps every key > k* and the first such equal keys
 //     in tile order (so equal gains keep the lower tile index);
-//  3. a stable least-significant-digit radix sort of the K survivors by
-//     decreasing key leaves equal keys in increasing tile order;
+//  3. the K survivors are sorted by (decreasing key, increasing tile): chunks
+//     of 1024 by a bitonic network in LDS, then multiway merge passes that
+//     place each item by binary searches in the other runs of its group;
 //  4. records are bit-packed at fixed offsets h + i * L_rec.
 #include "awsrc_internal.h"
 
@@ -17,8 +18,10 @@ namespace awsrc {
 constexpr int kThreads = 256;
 constexpr int kRounds = 16;
 constexpr int kItems = kThreads * kRounds;  // items per block in the compaction
-constexpr int kSortRounds = 4;
-constexpr int kSortItems = kThreads * kSortRounds;  // items per block in the radix sort
+constexpr int kChunk = 1024;                // items per LDS-sorted chunk
+constexpr int kChunkThreads = 256;
+constexpr int kLogChunk = 10;
+constexpr int kFan = 16;                    // runs per multiway merge
 constexpr int kSelBits = 12;                // radix-select digit width
 constexpr int kSelBins = 1 << kSelBits;
 
@@ -238,8 +241,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
                                                             const uint64_t* __restrict__ state,
                                                             const uint64_t* __restrict__ sel_off,
                                                             const uint64_t* __restrict__ eq_off,
-                                                            uint64_t* __restrict__ keys_out,
-                                                            uint32_t* __restrict__ vals_out) {
+                                                            SortItem* __restrict__ items_out) {
   __shared__ uint32_t sh_w[kThreads / 64];
   const uint64_t prefix = state[0], mask = state[1];
   const uint64_t rem = state[2];
@@ -257,112 +259,130 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
     const bool take = gt || (eq && (eq_run + eq_rank) < rem);
     const uint32_t pos = block_scan_flag(take, sh_w, &sel_tot);
     if (take) {
-      keys_out[sel_run + pos] = ~k;  // ascending ~key = descending gain
-      vals_out[sel_run + pos] = (uint32_t)(t0 + i);
+      SortItem it;
+      it.key = ~k;  // ascending ~key = descending gain
+      it.tile = (uint32_t)(t0 + i);
+      it.pad = 0u;
+      items_out[sel_run + pos] = it;
     }
     eq_run += eq_tot;
     sel_run += sel_tot;
   }
 }
 
-// ---------------------------------------------------------------- LSD radix sort
-__global__ __launch_bounds__(kThreads) void k_sort_hist(const uint64_t* __restrict__ keys, int64_t n, int shift,
-                                                        uint32_t* __restrict__ hist, int64_t nblk) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
-  __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kSortItems;
-  for (int r = 0; r < kSortRounds; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
-    if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
-  }
-  __syncthreads();
-  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
+// ---------------------------------------------------------------- sort of the survivors
+// Items are (key, tile) pairs; tiles are distinct, so the lexicographic order
+// on the pair is a total order and equal gains come out in increasing tile
+// order without any stability argument.
+__device__ __forceinline__ bool kv_less(const SortItem& a, const SortItem& b) {
+  return a.key < b.key || (a.key == b.key && a.tile < b.tile);
 }
 
-// Exclusive scan of n u32 values in place (single block): each thread scans a
-// contiguous chunk serially, one block-wide scan combines the chunk totals.
-__global__ __launch_bounds__(1024) void k_scan_u32(uint32_t* v, int64_t n) {
-  __shared__ uint32_t sh[1024];
-  const int64_t per = (n + 1023) / 1024;
-  const int64_t b0 = threadIdx.x * per;
-  const int64_t b1 = b0 + per < n ? b0 + per : n;
-  uint32_t tot = 0;
-  for (int64_t i = b0; i < b1; ++i) tot += v[i];
-  sh[threadIdx.x] = tot;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const uint32_t y = threadIdx.x >= off ? sh[threadIdx.x - off] : 0u;
-    __syncthreads();
-    sh[threadIdx.x] += y;
-    __syncthreads();
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// In-place bitonic sort of each chunk of kChunk items in LDS; the tail chunk
+// is padded with sentinels that sort last and are not written back.  Pair q of
+// a stage with distance j compares elements i = (q with a zero inserted at bit
+// log2 j) and i + j; thread t takes pairs t and t + kChunkThreads, so for
+// j <= 64 every wavefront works inside its own two 128-element windows and a
+// wavefront-level barrier suffices between stages.
+__global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restrict__ items, int64_t n) {
+  __shared__ uint64_t sk[kChunk];
+  __shared__ uint32_t st[kChunk];
+  const int64_t base = (int64_t)blockIdx.x * kChunk;
+#pragma unroll
+  for (int r = 0; r < kChunk / kChunkThreads; ++r) {
+    const int j = r * kChunkThreads + threadIdx.x;
+    const int64_t i = base + j;
+    uint64_t key = ~0ull;
+    uint32_t tile = 0xFFFFFFFFu;
+    if (i < n) { key = items[i].key; tile = items[i].tile; }
+    sk[j] = key;
+    st[j] = tile;
   }
-  uint32_t run = sh[threadIdx.x] - tot;
-  for (int64_t i = b0; i < b1; ++i) {
-    const uint32_t x = v[i];
-    v[i] = run;
-    run += x;
+  int prev = kChunk;
+  for (int k = 2; k <= kChunk; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j > 64 || prev > 64) __syncthreads(); else wave_sync();
+#pragma unroll
+      for (int r = 0; r < kChunk / (2 * kChunkThreads); ++r) {
+        const int q = r * kChunkThreads + threadIdx.x;
+        const int i = ((q & ~(j - 1)) << 1) | (q & (j - 1));
+        const uint64_t ka = sk[i], kb = sk[i + j];
+        const uint32_t ta = st[i], tb = st[i + j];
+        const bool b_first = kb < ka || (kb == ka && tb < ta);
+        const bool sw = ((i & k) == 0) == b_first;  // ascending half: swap if b < a
+        sk[i] = sw ? kb : ka;
+        sk[i + j] = sw ? ka : kb;
+        st[i] = sw ? tb : ta;
+        st[i + j] = sw ? ta : tb;
+      }
+      prev = j;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kChunk / kChunkThreads; ++r) {
+    const int j = r * kChunkThreads + threadIdx.x;
+    const int64_t i = base + j;
+    if (i < n) {
+      SortItem x;
+      x.key = sk[j];
+      x.tile = st[j];
+      x.pad = 0u;
+      items[i] = x;
+    }
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_sort_scatter(const uint64_t* __restrict__ kin,
-                                                           const uint32_t* __restrict__ vin, int64_t n,
-                                                           int shift, const uint32_t* __restrict__ offs,
-                                                           int64_t nblk, uint64_t* __restrict__ kout,
-                                                           uint32_t* __restrict__ vout) {
-  __shared__ uint32_t run[256];
-  __shared__ uint32_t wcnt[kThreads / 64][256];
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  run[threadIdx.x] = offs[(int64_t)threadIdx.x * nblk + blockIdx.x];
-  const int64_t base = (int64_t)blockIdx.x * kSortItems;
-  for (int r = 0; r < kSortRounds; ++r) {
-    const int64_t i = base + r * kThreads + threadIdx.x;
-    const bool valid = i < n;
-    uint64_t k = 0;
-    uint32_t v = 0;
-    if (valid) { k = kin[i]; v = vin[i]; }
-    const uint32_t dg = (uint32_t)(k >> shift) & 255u;
-    uint64_t match = __ballot(valid);
+// One multiway merge pass: runs of 2^logw sorted items, groups of kFan runs.
+// An item's output slot is the first slot of its group, plus its index in its
+// own run, plus, for every other run of the group, the number of that run's
+// items that order before it: a lower bound by binary lifting, with the runs
+// of the group searched in lockstep so that their loads overlap.
+__global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__ in, int64_t n, int logw,
+                                                    SortItem* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const SortItem x = in[i];
+  const int64_t w = (int64_t)1 << logw;
+  const int64_t run = i >> logw;
+  const int64_t g0 = run - run % kFan;
+  int64_t len[kFan];
+  int64_t cnt[kFan];
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool bit = (dg >> b) & 1u;
-      const uint64_t bb = __ballot(valid && bit);
-      match &= bit ? bb : ~bb;
-    }
-    const uint32_t rank = __popcll(match & lanemask_lt());
-    const uint32_t cnt = __popcll(match);
-#pragma unroll
-    for (int q = 0; q < kThreads / 64; ++q) wcnt[q][threadIdx.x] = 0;
-    __syncthreads();
-    if (valid && rank == 0) wcnt[w][dg] = cnt;
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = run[dg] + rank;
-      for (int q = 0; q < w; ++q) pos += wcnt[q][dg];
-      kout[pos] = k;
-      vout[pos] = v;
-    }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int q = 0; q < kThreads / 64; ++q) add += wcnt[q][threadIdx.x];
-    run[threadIdx.x] += add;
-    __syncthreads();
+  for (int r = 0; r < kFan; ++r) {
+    const int64_t rem = n - ((g0 + r) << logw);
+    len[r] = (g0 + r == run || rem <= 0) ? 0 : (rem < w ? rem : w);
+    cnt[r] = 0;
   }
-  (void)lane;
+  for (int64_t step = w; step >= 1; step >>= 1) {
+#pragma unroll
+    for (int r = 0; r < kFan; ++r) {
+      if (len[r] > 0) {
+        const int64_t probe = cnt[r] + step;
+        const int64_t at = ((g0 + r) << logw) + (probe <= len[r] ? probe : len[r]) - 1;
+        const SortItem y = in[at];
+        if (probe <= len[r] && kv_less(y, x)) cnt[r] = probe;
+      }
+    }
+  }
+  int64_t pos = (g0 << logw) + (i - (run << logw));
+#pragma unroll
+  for (int r = 0; r < kFan; ++r) pos += cnt[r];
+  out[pos] = x;
 }
 
 // ---------------------------------------------------------------- workspace
 size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
   const size_t cap = k_cap ? k_cap : 1;
-  const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
-  const size_t nb_s = (cap + kSortItems - 1) / kSortItems + 1;
-  const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
+  const size_t max_blocks = (n_tiles + kItems - 1) / kItems + 1;
   size_t b = 0;
-  b += align_up(cap * 8, 256) * 2;
-  b += align_up(cap * 4, 256) * 2;
-  b += align_up(256 * max_blocks * 4, 256);
+  b += align_up(cap * sizeof(SortItem), 256) * 2;
   b += align_up((max_blocks + 1) * 8, 256) * 2;
   b += align_up((4 + kSelBins) * 8, 256);
   return b;
@@ -370,16 +390,11 @@ size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
 
 RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
   const size_t cap = k_cap ? k_cap : 1;
-  const size_t nb_c = (n_tiles + kItems - 1) / kItems + 1;
-  const size_t nb_s = (cap + kSortItems - 1) / kSortItems + 1;
-  const size_t max_blocks = nb_c > nb_s ? nb_c : nb_s;
+  const size_t max_blocks = (n_tiles + kItems - 1) / kItems + 1;
   char* p = static_cast<char*>(base);
   RankWs w;
-  w.keys_a = reinterpret_cast<uint64_t*>(p); p += align_up(cap * 8, 256);
-  w.keys_b = reinterpret_cast<uint64_t*>(p); p += align_up(cap * 8, 256);
-  w.vals_a = reinterpret_cast<uint32_t*>(p); p += align_up(cap * 4, 256);
-  w.vals_b = reinterpret_cast<uint32_t*>(p); p += align_up(cap * 4, 256);
-  w.hist = reinterpret_cast<uint32_t*>(p); p += align_up(256 * max_blocks * 4, 256);
+  w.items_a = reinterpret_cast<SortItem*>(p); p += align_up(cap * sizeof(SortItem), 256);
+  w.items_b = reinterpret_cast<SortItem*>(p); p += align_up(cap * sizeof(SortItem), 256);
   w.blk_a = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
   w.blk_b = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
   w.state = reinterpret_cast<uint64_t*>(p);
@@ -389,7 +404,8 @@ RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
 }
 
 hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
-                                const RankWs& ws, hipStream_t st) {
+                                const RankWs& ws, const SortItem** sorted, hipStream_t st) {
+  *sorted = ws.items_a;
   if (K <= 0) return hipSuccess;
   const double* g = gain + t0;
   hipLaunchKernelGGL(k_select_init, dim3(1), dim3(1024), 0, st, ws.state, K);
@@ -407,22 +423,17 @@ hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64
                      ws.blk_a, ws.blk_b);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
-                     ws.blk_a, ws.blk_b, ws.keys_a, ws.vals_a);
-  // sort the K survivors: 8 stable passes, ascending on ~key
-  const int64_t nbs = (K + kSortItems - 1) / kSortItems;
-  uint64_t* ki = ws.keys_a;
-  uint64_t* ko = ws.keys_b;
-  uint32_t* vi = ws.vals_a;
-  uint32_t* vo = ws.vals_b;
-  for (int shift = 0; shift < 64; shift += 8) {
-    hipLaunchKernelGGL(k_sort_hist, dim3((unsigned)nbs), dim3(kThreads), 0, st, ki, K, shift, ws.hist, nbs);
-    hipLaunchKernelGGL(k_scan_u32, dim3(1), dim3(1024), 0, st, ws.hist, 256 * nbs);
-    hipLaunchKernelGGL(k_sort_scatter, dim3((unsigned)nbs), dim3(kThreads), 0, st, ki, vi, K, shift,
-                       ws.hist, nbs, ko, vo);
-    uint64_t* tk = ki; ki = ko; ko = tk;
-    uint32_t* tv = vi; vi = vo; vo = tv;
+                     ws.blk_a, ws.blk_b, ws.items_a);
+  // sort the K survivors ascending on (~key, tile): LDS chunks, then multiway merges
+  hipLaunchKernelGGL(k_sort_chunks, dim3((unsigned)((K + kChunk - 1) / kChunk)), dim3(kChunkThreads), 0, st,
+                     ws.items_a, K);
+  SortItem* in = ws.items_a;
+  SortItem* out = ws.items_b;
+  for (int logw = kLogChunk; ((int64_t)1 << logw) < K; logw += 4) {
+    hipLaunchKernelGGL(k_merge_runs, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, in, K, logw, out);
+    SortItem* t = in; in = out; out = t;
   }
-  // 8 passes (even) leave the result in the "a" buffers
+  *sorted = in;
   return hipGetLastError();
 }
 
@@ -435,12 +446,12 @@ __device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v,
   pos += nbits;
 }
 
-__global__ void k_pack(const uint32_t* __restrict__ tiles, int64_t K, const uint16_t* __restrict__ seed,
+__global__ void k_pack(const SortItem* __restrict__ sorted, int64_t K, const uint16_t* __restrict__ seed,
                        const int8_t* __restrict__ code, const uint16_t* __restrict__ scale, int P, int b,
                        int idx_bits, int seed_bits, int L, uint8_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= K) return;
-  const uint32_t t = tiles[i];
+  const uint32_t t = sorted[i].tile;
   uint64_t w[3] = {0, 0, 0};
   int pos = 0;
   put_bits(w, pos, (uint64_t)t, idx_bits);
@@ -452,11 +463,11 @@ __global__ void k_pack(const uint32_t* __restrict__ tiles, int64_t K, const uint
   for (int k = 0; k < L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
 }
 
-hipError_t launch_pack(const uint32_t* tiles, int64_t K, const uint16_t* seed, const int8_t* code,
+hipError_t launch_pack(const SortItem* sorted, int64_t K, const uint16_t* seed, const int8_t* code,
                        const uint16_t* scale, int P, int b, int idx_bits, int seed_bits, int L_rec,
                        uint8_t* out, hipStream_t st) {
   if (K <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, tiles, K, seed, code,
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, sorted, K, seed, code,
                      scale, P, b, idx_bits, seed_bits, L_rec, out);
   return hipGetLastError();
 }

@@ -113,3 +113,17 @@ def test_decode_rejects_short_stream_without_device_reads():
     n = ctypes.c_size_t(0)
     st = awsrc.LIB.awsrc_decode_add(ctypes.c_void_p(16), 10, 1, None, rows, cols, 0, None, ctypes.byref(n), None)
     assert st == awsrc.AWSRC_ECORRUPT
+
+
+def test_misaligned_pointers_rejected_without_device_access():
+    # the stream is read with aligned word loads, W/W0 with 16-byte vectors
+    rows = (ctypes.c_int64 * 1)(16)
+    cols = (ctypes.c_int64 * 1)(64)
+    n = ctypes.c_size_t(0)
+    st = awsrc.LIB.awsrc_decode_add(ctypes.c_void_p(12), 4096, 1, None, rows, cols, 0, None, ctypes.byref(n), None)
+    assert st == awsrc.AWSRC_EINVAL
+    v = ctypes.c_void_p
+    st = awsrc.LIB.awsrc_backbone_rtn(v(8), 1, 4, 256, 128, v(256), v(256), v(256), None, None)
+    assert st == awsrc.AWSRC_EINVAL
+    st = awsrc.LIB.awsrc_backbone_rtn(v(256), 1, 4, 256, 128, v(258), v(256), v(256), None, None)
+    assert st == awsrc.AWSRC_EINVAL

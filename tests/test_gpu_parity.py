@@ -267,6 +267,24 @@ def test_decode_matches_oracle(C, P, b, S, dtype):
         assert np.all(np.abs(got - ref)[mask] <= tol * mag[mask] + 1e-30)
 
 
+def test_decode_many_modules():
+    """More modules than the kernel stages in LDS: the module lookup reads the
+    tables from global memory instead."""
+    C, P, b, S = 16, 4, 4, 16
+    mods = [(1 + (m % 3), 64) for m in range(300)]
+    stream, K, enc = _oracle_stream(C, P, b, S, mods, 8.0, seed=21)
+    assert K > 100
+    g = torch.Generator().manual_seed(4)
+    W0s = [torch.randn(r, c, generator=g) * 0.02 for r, c in mods]
+    want = O.decode_add(stream, [w.numpy() for w in W0s])
+    dev = [w.to(DEV) for w in W0s]
+    awsrc.awsrc_decode_add(torch.tensor(list(stream), dtype=torch.uint8, device=DEV), dev)
+    for w0, got, ref in zip(W0s, dev, want):
+        got = got.cpu().numpy()
+        w0f = w0.numpy().astype(np.float64)
+        assert np.all(np.abs(got - ref) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(ref - w0f)) + 1e-30)
+
+
 def test_decode_prefixes_and_empty_stream():
     C, P, b, S = 64, 8, 4, 256
     mods = [(64, 1024)]
