@@ -70,6 +70,57 @@ def cpu_baseline(wl, inputs, seconds: float):
                       f"fp64 numpy, 1 thread, {dt:.1f} s"}
 
 
+def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
+    """Decode-add of a large stream: records drawn at random for every tile of
+    the named workload (all gains positive), ranked globally at `bpw`, then
+    applied `reps` times onto fp32 W0 buffers of the workload's shapes (an
+    add onto the same tiles each time).  Timed with HIP events on the
+    library's stream around the apply launches only."""
+    from synth import gen_records, workload
+
+    wl = workload(name)
+    dev = torch.device("cuda:0")
+    shapes = [(m.rows, m.cols) for m in wl.modules]
+    p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                          idx_bits=wl.idx_bits)
+    rec = gen_records(wl.n_tiles, wl.P, wl.b, wl.S, seed=4242, device=dev, frac_nonpositive=0.0, frac_ties=0.0)
+    s, K, _ = awsrc.awsrc_rank_prefix(p, shapes, awsrc.AWSRC_MODE_GLOBAL, bpw, rec["seed"], rec["codes"],
+                                      rec["scale"], rec["gain"])
+    del rec
+    W0 = [torch.zeros(r, c, dtype=torch.float32, device=dev) for r, c in shapes]
+    plan, dws = awsrc.awsrc_decode_prepare(s, W0)
+    stream = torch.cuda.current_stream()
+    awsrc.awsrc_decode_apply(plan)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        awsrc.awsrc_decode_apply(plan)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = K * (plan.L_rec + 2 * wl.C * 4)
+    gbs = nbytes / (ms / 1e3) / 1e9
+    del W0, plan, dws, s
+    # device-copy ceiling: one large copy, read + write bytes
+    n = 1 << 30
+    x = torch.empty(n, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(3):
+        y.copy_(x)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 3 * 2 * 4 * n / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return {"workload": f"{name} stream at {bpw} bpw, fp32 W0", "modules": len(shapes), "records": K,
+            "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -78,6 +129,9 @@ def main() -> int:
     ap.add_argument("--workload", default="down3b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-workload", default="stack3b",
+                    help="workload whose shapes size the at-scale decode-add measurement ('' to skip)")
+    ap.add_argument("--decode-bpw", type=float, default=0.32)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         log("bench.py measures a single GPU: the codec has no cross-GPU step in this build "
@@ -189,9 +243,15 @@ def main() -> int:
         "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
         "device": torch.cuda.get_device_name(0),
     }
+    del inputs, bb, enc_out, ws
+    torch.cuda.empty_cache()
+    if args.decode_workload:
+        log(f"[bench] decode-add at scale: {args.decode_workload} at {args.decode_bpw} bpw")
+        out["decode_add_at_scale"] = decode_at_scale(awsrc, torch, args.decode_workload, args.decode_bpw, 5)
     if not args.no_cpu_baseline:
+        wl_inputs = [gen_module_inputs(wl, m, dev) for m in mods[:1]]
         log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, wl_inputs, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
 

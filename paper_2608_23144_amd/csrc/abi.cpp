@@ -289,23 +289,24 @@ namespace {
 
 // Workspace: basis tables | tile bitmap | error counter | module tables
 // (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
-// host-to-device copy fills them).
+// host-to-device copy fills them) | decoded records [K] x 32 B.
 struct DecodeLayout {
-  size_t basis, bitmap, err, tables, total;
+  size_t basis, bitmap, err, tables, dec, total;
 };
 
-DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod) {
+DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_t K) {
   DecodeLayout l;
   l.basis = align_up(basis_bytes(S, P), 256);
   l.bitmap = align_up((size_t)((T_total + 31) / 32) * 4, 256);
   l.err = 256;
   l.tables = align_up((size_t)(3 * nmod + 1) * 8, 256);
-  l.total = 256 + l.basis + l.bitmap + l.err + l.tables;
+  l.dec = align_up((size_t)K * 32, 256);
+  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec;
   return l;
 }
 
 DecodeArgs decode_args(const awsrc_decode_plan* pl) {
-  const DecodeLayout l = decode_layout(pl->S, pl->P, pl->T_total, (uint32_t)pl->n_modules);
+  const DecodeLayout l = decode_layout(pl->S, pl->P, pl->T_total, (uint32_t)pl->n_modules, pl->K);
   char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(pl->workspace), 256));
   DecodeArgs a{};
   a.recs = pl->records;
@@ -323,6 +324,8 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   a.mod_tile_off = reinterpret_cast<const uint64_t*>(ws);
   a.mod_cols = reinterpret_cast<const int64_t*>(ws + 8 * (size_t)(n + 1));
   a.mod_ptr = reinterpret_cast<void* const*>(ws + 8 * (size_t)(2 * n + 1));
+  ws += l.tables;
+  a.dec = reinterpret_cast<uint4*>(ws);
   return a;
 }
 
@@ -377,7 +380,7 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   if (toff[nmod] != T_total) return fail(AWSRC_ECORRUPT, "T_total inconsistent with the module table");
   if (ib < 32 && T_total > (1ull << ib)) return fail(AWSRC_ECORRUPT, "index field too narrow");
   const int64_t K = (int64_t)((stream_len - h) / (uint64_t)L);
-  const DecodeLayout lay = decode_layout((int)S, P, T_total, nmod);
+  const DecodeLayout lay = decode_layout((int)S, P, T_total, nmod, K);
   if (!workspace) { *ws_bytes = lay.total; return AWSRC_OK; }
   if (*ws_bytes < lay.total) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, lay.total);
   if (!plan) return fail(AWSRC_EINVAL, "plan is NULL");

@@ -147,6 +147,10 @@ struct DecodeArgs {
   BasisTables basis;
   uint32_t* bitmap;              // [ceil(T_total / 32)]
   unsigned long long* errors;    // [1]
+  // [K][2] decoded records written by validation: {tile within module,
+  // module, seed | scale << 16, sum of codes}, then the P codes as int8 (zero
+  // padded to 16)
+  uint4* dec;
 };
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st);
 hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st);

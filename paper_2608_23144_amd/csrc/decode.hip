@@ -5,6 +5,8 @@
 //            and a bitmap over tiles that catches a tile appearing twice
 //            (records of a valid stream touch disjoint tiles, which is what
 //            lets the apply pass run without atomics or ordering).
+// validate also writes each record in a decoded form (tile within its
+//            module, module, seed, scale, codes and their sum);
 // apply    - C/8 lanes per record, eight consecutive weights per lane; each
 //            weight gets rhat_j = (1/sqrt(C)) sum_p (+-1) scale*q_p with the
 //            signs of row j of B_s read from the transposed sign table.
@@ -98,81 +100,91 @@ __global__ void k_decode_validate(DecodeArgs a) {
     bad = (old & bit) != 0;
   }
   if (bad) atomicAdd(a.errors, 1ull);
-}
-
-template <int C, typename TW>
-__global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
-  constexpr int LPR = C / 8;           // lanes per record, eight weights each
-  constexpr int RPB = 256 / LPR;       // records per block
-  // module table staged in LDS when it is small enough (the common case)
-  __shared__ uint64_t s_off[kLdsModules + 1];
-  __shared__ int64_t s_cols[kLdsModules];
-  __shared__ void* s_ptr[kLdsModules];
-  const int sub = threadIdx.x % LPR;
-  const int64_t i = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
-  const bool valid = i < a.K;
-  const Rec r = parse(a, valid ? i : a.K - 1);
-  // signs of rows 8*sub .. 8*sub+7 of B_s, one u16 of P bits per row
-  const uint4 tsv = *reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)r.seed * kMaxC + sub * 8);
-  const bool lds_tab = a.n_modules <= kLdsModules;
-  if (lds_tab) {
-    for (int m = threadIdx.x; m <= a.n_modules; m += 256) {
-      s_off[m] = a.mod_tile_off[m];
-      if (m < a.n_modules) { s_cols[m] = a.mod_cols[m]; s_ptr[m] = a.mod_ptr[m]; }
-    }
-  }
-  __syncthreads();
-  if (!valid) return;
-  const uint64_t* off = lds_tab ? s_off : a.mod_tile_off;
+  // decoded form for the apply pass (only used once the whole stream is valid)
   int lo = 0, hi = a.n_modules - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= r.idx) lo = mid; else hi = mid - 1;
+    if (a.mod_tile_off[mid] <= r.idx) lo = mid; else hi = mid - 1;
   }
-  const int64_t cols = lds_tab ? s_cols[lo] : a.mod_cols[lo];
-  TW* W0 = static_cast<TW*>(lds_tab ? s_ptr[lo] : a.mod_ptr[lo]);
-  // tile indices and tiles per row fit in 32 bits (T_total < 2^32)
-  const uint32_t local = (uint32_t)(r.idx - off[lo]);
-  const uint32_t nb = (uint32_t)(cols / C);
-  const uint32_t row = local / nb;
-  const uint32_t blk = local - row * nb;
-  const int64_t base = (int64_t)row * cols + (int64_t)blk * C + sub * 8;
-  const float sc = __half2float(__ushort_as_half((uint16_t)r.scale));
+  uint32_t qw[4] = {0u, 0u, 0u, 0u};
+  int32_t tot = 0;
+  for (int p = 0; p < a.P; ++p) {
+    qw[p >> 2] |= ((uint32_t)r.q[p] & 0xFFu) << (8 * (p & 3));
+    tot += r.q[p];
+  }
+  a.dec[2 * i] = make_uint4((uint32_t)(r.idx - a.mod_tile_off[lo]), (uint32_t)lo, r.seed | (r.scale << 16),
+                            (uint32_t)tot);
+  a.dec[2 * i + 1] = make_uint4(qw[0], qw[1], qw[2], qw[3]);
+}
+
+// C/8 lanes per record, eight consecutive weights per lane.  With integer
+// codes, C * rhat_j / sqrt(C) = scale * sum_p sign_jp q_p is scale times an
+// exact integer: sum_p q_p minus twice the codes at the negative entries of
+// row j, the latter one int8 dot product per four codes against a 0/1 byte
+// mask spread from the row's sign bits.  Blocks loop over record groups so
+// that the table of W0 pointers is staged in LDS once per block.
+template <int C, typename TW, int G>
+__global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
+  constexpr int LPR = C / 8;           // lanes per record
+  constexpr int RPB = 256 / LPR;       // records per block per iteration
+  __shared__ void* s_ptr[kLdsModules];
+  const bool lds_tab = a.n_modules <= kLdsModules;
+  if (lds_tab)
+    for (int m = threadIdx.x; m < a.n_modules; m += 256) s_ptr[m] = a.mod_ptr[m];
+  __syncthreads();
+  void* const* mptr = lds_tab ? s_ptr : a.mod_ptr;
   constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
                       : (C == 64) ? 0.125f : 0.08838834764831845f;
-  const uint32_t tw[4] = {tsv.x, tsv.y, tsv.z, tsv.w};
-  float add[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int p = 0; p < a.P; ++p) {
-    const float ah = sc * (float)r.q[p];
+  const int sub = threadIdx.x % LPR;
+  for (int64_t i = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR; i < a.K; i += (int64_t)gridDim.x * RPB) {
+    const uint4 e0 = a.dec[2 * i];
+    const uint4 e1 = a.dec[2 * i + 1];
+    const uint32_t q4[4] = {e1.x, e1.y, e1.z, e1.w};
+    // signs of rows 8*sub .. 8*sub+7 of B_s, one u16 of P bits per row
+    const uint4 tsv = *reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC + sub * 8);
+    const uint32_t tw[4] = {tsv.x, tsv.y, tsv.z, tsv.w};
+    const float scl = __half2float(__ushort_as_half((uint16_t)(e0.z >> 16))) * isq;
+    const int32_t tot = (int32_t)e0.w;
+    float add[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) add[e] += ((tw[e >> 1] >> (16 * (e & 1) + p)) & 1u) ? -ah : ah;
-  }
-  if constexpr (sizeof(TW) == 4) {
-    float4* q = reinterpret_cast<float4*>(W0 + base);
-    float4 v0 = q[0], v1 = q[1];
-    v0.x += add[0] * isq; v0.y += add[1] * isq; v0.z += add[2] * isq; v0.w += add[3] * isq;
-    v1.x += add[4] * isq; v1.y += add[5] * isq; v1.z += add[6] * isq; v1.w += add[7] * isq;
-    q[0] = v0;
-    q[1] = v1;
-  } else {
-    uint4* q = reinterpret_cast<uint4*>(W0 + base);
-    const uint4 v = *q;
-    const uint32_t in[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[4];
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t ts = (tw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+      int32_t neg = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      uint32_t h2 = 0;
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const uint32_t bits = e ? (in[k] & 0xFFFF0000u) : (in[k] << 16);
-        const float w = __uint_as_float(bits) + add[2 * k + e] * isq;
-        uint32_t u = __float_as_uint(w);
-        u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest even (finite values)
-        h2 |= (u >> 16) << (16 * e);
+      for (int g = 0; g < G; ++g) {
+        const uint32_t mask = (((ts >> (4 * g)) & 0xFu) * 0x204081u) & 0x01010101u;
+        neg = __builtin_amdgcn_sdot4((int)mask, (int)q4[g], neg, false);
       }
-      o[k] = h2;
+      add[e] = (float)(tot - 2 * neg) * scl;
     }
-    *q = make_uint4(o[0], o[1], o[2], o[3]);
+    TW* W0 = static_cast<TW*>(mptr[e0.y]);
+    const int64_t base = (int64_t)e0.x * C + sub * 8;
+    if constexpr (sizeof(TW) == 4) {
+      float4* q = reinterpret_cast<float4*>(W0 + base);
+      float4 v0 = q[0], v1 = q[1];
+      v0.x += add[0]; v0.y += add[1]; v0.z += add[2]; v0.w += add[3];
+      v1.x += add[4]; v1.y += add[5]; v1.z += add[6]; v1.w += add[7];
+      q[0] = v0;
+      q[1] = v1;
+    } else {
+      uint4* q = reinterpret_cast<uint4*>(W0 + base);
+      const uint4 v = *q;
+      const uint32_t in[4] = {v.x, v.y, v.z, v.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        uint32_t h2 = 0;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const uint32_t bits = e ? (in[k] & 0xFFFF0000u) : (in[k] << 16);
+          uint32_t u = __float_as_uint(__uint_as_float(bits) + add[2 * k + e]);
+          u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest even (finite values)
+          h2 |= (u >> 16) << (16 * e);
+        }
+        o[k] = h2;
+      }
+      *q = make_uint4(o[0], o[1], o[2], o[3]);
+    }
   }
 }
 
@@ -188,15 +200,28 @@ hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int C, int G>
+static hipError_t apply_cg(const DecodeArgs& a, hipStream_t st) {
+  constexpr int RPB = 256 / (C / 8);
+  // up to eight resident blocks per CU, each looping over record groups
+  int64_t nb = (a.K + RPB - 1) / RPB;
+  if (nb > 256 * 8) nb = 256 * 8;
+  const unsigned blocks = (unsigned)nb;
+  if (a.w0_dtype == AWSRC_DTYPE_F32)
+    hipLaunchKernelGGL((k_decode_apply<C, float, G>), dim3(blocks), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_decode_apply<C, uint16_t, G>), dim3(blocks), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int C>
 static hipError_t apply_c(const DecodeArgs& a, hipStream_t st) {
-  constexpr int RPB = 256 / (C / 8);
-  const unsigned blocks = (unsigned)((a.K + RPB - 1) / RPB);
-  if (a.w0_dtype == AWSRC_DTYPE_F32)
-    hipLaunchKernelGGL((k_decode_apply<C, float>), dim3(blocks), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((k_decode_apply<C, uint16_t>), dim3(blocks), dim3(256), 0, st, a);
-  return hipGetLastError();
+  switch ((a.P + 3) / 4) {  // groups of four codes
+    case 1: return apply_cg<C, 1>(a, st);
+    case 2: return apply_cg<C, 2>(a, st);
+    case 3: return apply_cg<C, 3>(a, st);
+    default: return apply_cg<C, 4>(a, st);
+  }
 }
 
 hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st) {
