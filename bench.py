@@ -187,11 +187,11 @@ def main() -> int:
         ev[2].record(stream)
         s, K, ne = awsrc.awsrc_rank_prefix(p, shapes, mode, bpw, seed, codes, scale, gain)
         ev[3].record(stream)
-        plan, dws = awsrc.awsrc_decode_prepare(s, [b[3] for b in bb])
+        plan, dws = awsrc.awsrc_decode_prepare(s, [b[3] for b in bb], workspace=last.get("dws"))
         ev[4].record(stream)
         awsrc.awsrc_decode_apply(plan)
         ev[5].record(stream)
-        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), L=plan.L_rec)
+        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), L=plan.L_rec, dws=dws)
         if record:
             torch.cuda.synchronize()
             for k, (a, b) in zip(acc, zip(ev[:-1], ev[1:])):

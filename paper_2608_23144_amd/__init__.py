@@ -223,9 +223,10 @@ def awsrc_rank_prefix(p: awsrc_params, modules: Sequence[Tuple[int, int]], mode:
                 cap_rec = sum(awsrc_budget_bytes(bpw, r * c) // L for r, c in modules)
             stream_cap = awsrc_header_bytes(len(modules)) + min(cap_rec, T) * L
         out = torch.empty(int(stream_cap), dtype=torch.uint8, device=dev)
+    cap = out.numel() if stream_cap is None else min(int(stream_cap), out.numel())
     n = ctypes.c_size_t(workspace.numel())
     _check(LIB.awsrc_rank_prefix(ctypes.byref(p), len(modules), rows, cols, mode, bpw, _ptr(seed), _ptr(codes),
-                                 _ptr(scale), _ptr(gain), _ptr(out), out.numel(), ctypes.byref(slen),
+                                 _ptr(scale), _ptr(gain), _ptr(out), cap, ctypes.byref(slen),
                                  ctypes.byref(K), ctypes.byref(ne), _ptr(workspace), ctypes.byref(n),
                                  _stream(stream)))
     return out[: slen.value], K.value, ne.value
@@ -262,16 +263,25 @@ def awsrc_decode_add(stream_bytes: torch.Tensor, W0_list: List[torch.Tensor], st
 def awsrc_decode_prepare(stream_bytes: torch.Tensor, W0_list: List[torch.Tensor], stream_len: Optional[int] = None,
                          workspace: Optional[torch.Tensor] = None, stream=None):
     """Validate a stream and build its decode tables; returns (plan, workspace).
-    Keep both (and the stream bytes) alive while the plan is applied."""
+    Keep both (and the stream bytes) alive while the plan is applied.  A
+    workspace passed in (e.g. the one a previous plan used, once that plan is
+    no longer needed) is used directly when it is large enough, which saves
+    the size query's header read."""
     stream_len, rows, cols, ptrs, dt = _decode_args(stream_bytes, W0_list, stream_len)
-    n = ctypes.c_size_t(0)
     st = _stream(stream)
+    plan = awsrc_decode_plan()
+    if workspace is not None:
+        n = ctypes.c_size_t(workspace.numel())
+        rc = LIB.awsrc_decode_prepare(_ptr(stream_bytes), stream_len, len(W0_list), ptrs, rows, cols, dt,
+                                      ctypes.byref(plan), _ptr(workspace), ctypes.byref(n), st)
+        if rc != AWSRC_ENOSPC:
+            _check(rc)
+            return plan, workspace
+    n = ctypes.c_size_t(0)
     _check(LIB.awsrc_decode_prepare(_ptr(stream_bytes), stream_len, len(W0_list), ptrs, rows, cols, dt, None,
                                     None, ctypes.byref(n), st))
-    if workspace is None or workspace.numel() < n.value:
-        workspace = _workspace(n.value, stream_bytes.device)
+    workspace = _workspace(n.value, stream_bytes.device)
     n = ctypes.c_size_t(workspace.numel())
-    plan = awsrc_decode_plan()
     _check(LIB.awsrc_decode_prepare(_ptr(stream_bytes), stream_len, len(W0_list), ptrs, rows, cols, dt,
                                     ctypes.byref(plan), _ptr(workspace), ctypes.byref(n), st))
     return plan, workspace

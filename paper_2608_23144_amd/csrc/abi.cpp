@@ -232,27 +232,16 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
   if (stream_cap < (uint64_t)h) return fail(AWSRC_ENOSPC, "stream capacity below the header size");
 
   char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
-  uint64_t* counter = reinterpret_cast<uint64_t*>(ws);
   const RankWs rw = carve_rank(ws + 256, max_n, max_k);
   hipStream_t s = (hipStream_t)stream;
 
-  int64_t K_total = 0, elig_total = 0;
+  // every segment runs on the device back to back (K is found there); one
+  // read of the totals at the end
+  HIPCHK(launch_rank_init(rw, s));
   for (size_t i = 0; i < seg_n.size(); ++i) {
-    HIPCHK(hipMemsetAsync(counter, 0, 8, s));
-    HIPCHK(launch_count_eligible(gain + seg_t0[i], seg_n[i], counter, s));
-    uint64_t ne = 0;
-    HIPCHK(hipMemcpyAsync(&ne, counter, 8, hipMemcpyDeviceToHost, s));
-    HIPCHK(hipStreamSynchronize(s));
-    const int64_t k = (int64_t)ne < seg_cap[i] ? (int64_t)ne : seg_cap[i];
-    elig_total += (int64_t)ne;
-    if ((uint64_t)(h + (K_total + k) * L) > stream_cap) return fail(AWSRC_ENOSPC, "stream capacity %llu < %lld bytes", (unsigned long long)stream_cap, (long long)(h + (K_total + k) * L));
-    if (k > 0) {
-      const SortItem* sorted = nullptr;
-      HIPCHK(launch_select_sorted(gain, seg_t0[i], seg_n[i], k, rw, &sorted, s));
-      HIPCHK(launch_pack(sorted, k, seed, code, scale, p->P, p->b, ib, sb, (int)L,
-                         stream_out + h + K_total * L, s));
-    }
-    K_total += k;
+    const int64_t cap = seg_cap[i] < seg_n[i] ? seg_cap[i] : seg_n[i];
+    HIPCHK(launch_rank_segment(gain, seg_t0[i], seg_n[i], cap, rw, seed, code, scale, p->P, p->b, ib, sb, (int)L,
+                               (uint64_t)h, stream_cap, stream_out, s));
   }
   // header: fixed fields, then the module table
   std::vector<uint8_t> hdr;
@@ -277,10 +266,14 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
     put_le(hdr, (uint64_t)module_cols[m], 4);
   }
   HIPCHK(hipMemcpyAsync(stream_out, hdr.data(), hdr.size(), hipMemcpyHostToDevice, s));
+  uint64_t tot[3] = {0, 0, 0};
+  HIPCHK(hipMemcpyAsync(tot, rank_totals(rw), sizeof(tot), hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
+  const int64_t K_total = (int64_t)tot[0];
+  if (tot[2]) return fail(AWSRC_ENOSPC, "stream capacity %llu < %lld bytes", (unsigned long long)stream_cap, (long long)(h + K_total * L));
   *stream_len = (uint64_t)(h + K_total * L);
   *K_out = K_total;
-  if (n_eligible) *n_eligible = elig_total;
+  if (n_eligible) *n_eligible = (int64_t)tot[1];
   return AWSRC_OK;
 }
 

@@ -116,21 +116,24 @@ struct RankWs {
   SortItem* items_b;     // [cap] (pong)
   uint64_t* blk_a;       // [max_blocks + 1] per-block counts / offsets
   uint64_t* blk_b;       // [max_blocks + 1]
-  uint64_t* state;       // select state: prefix, mask, remaining, eligible count, hist[256]
+  uint64_t* state;       // [kStateWords] select state, counters, totals, histogram
   size_t cap;
   size_t max_blocks;
 };
 size_t rank_ws_bytes(size_t n_tiles, size_t k_cap);
 RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap);
 
-hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st);
-// Top-K of one tile segment, ordered by (gain desc, tile asc); *sorted is set
-// to the workspace array that receives the K items in that order.
-hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
-                                const RankWs& ws, const SortItem** sorted, hipStream_t st);
-hipError_t launch_pack(const SortItem* sorted, int64_t K, const uint16_t* seed, const int8_t* code,
-                       const uint16_t* scale, int P, int b, int idx_bits, int seed_bits,
-                       int L_rec, uint8_t* out, hipStream_t st);
+constexpr int kStateWords = 16 + 4096;  // rank state: scalars, then the select histogram
+hipError_t launch_rank_init(const RankWs& ws, hipStream_t st);
+// Top-K of one tile segment (K = min(cap, eligible), found on the device),
+// ordered by (gain desc, tile asc), packed at the segment's first free record
+// slot of the stream; no host synchronization.
+hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_t cap, const RankWs& ws,
+                               const uint16_t* seed, const int8_t* code, const uint16_t* scale, int P, int b,
+                               int idx_bits, int seed_bits, int L, uint64_t h, uint64_t stream_cap,
+                               uint8_t* stream_out, hipStream_t st);
+// Device words after all segments: [0] records, [1] eligible tiles, [2] no-space flag.
+const uint64_t* rank_totals(const RankWs& ws);
 
 // ---------------------------------------------------------------- decoding
 struct DecodeArgs {

@@ -2,15 +2,22 @@
 //
 // With a fixed record size, ordering by rho_t = gain_t / L_rec is ordering by
 // gain.  The positive fp64 gains are mapped to their IEEE bit patterns, which
-// order like the values.  For a segment of tiles and a record count K:
-//  1. radix select (8 passes of 8 bits, most significant first) finds the K-th
+// order like the values.  For a segment of tiles:
+//  0. the eligible tiles are counted and K = min(cap, eligible) is formed on
+//     the device (the host never waits for it);
+//  1. radix select (12-bit digits, most significant first) finds the K-th
 //     largest key k* and how many records equal to k* are taken;
 //  2. a stable compaction keeps every key > k* and the first such equal keys
 //     in tile order (so equal gains keep the lower tile index);
 //  3. the K survivors are sorted by (decreasing key, increasing tile): chunks
 //     of 1024 by a bitonic network in LDS, then multiway merge passes that
-//     place each item by binary searches in the other runs of its group;
-//  4. records are bit-packed at fixed offsets h + i * L_rec.
+//     place each item by searches in the other runs of its group;
+//  4. records are bit-packed at fixed offsets h + (first slot of the segment
+//     + i) * L_rec.
+// Reductions that finish a pass (K, the select pick, the compaction scan) run
+// as one-block launches, so cross-block results only pass between launches; a
+// segment is a chain of launches with no host round trip and one read of the
+// totals ends the call.
 #include "awsrc_internal.h"
 
 namespace awsrc {
@@ -22,8 +29,18 @@ constexpr int kChunk = 1024;                // items per LDS-sorted chunk
 constexpr int kChunkThreads = 256;
 constexpr int kLogChunk = 10;
 constexpr int kFan = 16;                    // runs per multiway merge
+constexpr int kLogFan = 4;
 constexpr int kSelBits = 12;                // radix-select digit width
 constexpr int kSelBins = 1 << kSelBits;
+
+// Words of RankWs::state.
+enum : int {
+  kPrefix = 0, kMask = 1, kRem = 2, kDone = 3,  // radix select of the current segment
+  kSegK = 4, kSegOff = 5,                       // records of the segment, its first record slot
+  kElig = 6, kArrive = 7,                       // per-launch accumulators, reset after use
+  kTotK = 8, kTotElig = 9, kNoSpace = 10,       // totals over the segments of one call
+  kHist = 16                                    // [kSelBins] select histogram
+};
 
 // Positive doubles order like their bit patterns; the top (sign) bit is set on
 // eligible keys so that every eligible key exceeds every ineligible (zero) key.
@@ -57,14 +74,31 @@ __device__ __forceinline__ uint32_t block_scan_flag(bool f, uint32_t* sh_w, uint
   return before + in_wave;
 }
 
-// ---------------------------------------------------------------- eligibility
-__global__ __launch_bounds__(kThreads) void k_count_eligible(const double* __restrict__ gain, int64_t n,
-                                                             uint64_t* counter) {
+__global__ void k_rank_init(uint64_t* state) {
+  for (int i = threadIdx.x; i < kStateWords; i += blockDim.x) state[i] = 0;
+}
+
+// ---------------------------------------------------------------- radix select
+// Each pass histograms the next digit of the keys that match the prefix so
+// far; a one-block pick then moves the prefix into the bin holding the
+// remaining-th largest key and clears the histogram.  When that whole bin is
+// taken the search stops early: every key in it is selected, so the lower
+// digits no longer matter.  Cross-block results only pass between launches.
+
+// First pass of a segment, fused with the eligibility count: the top digit
+// (eligible flag and exponent) of every key.
+__global__ __launch_bounds__(kThreads) void k_count_hist(const double* __restrict__ gain, int64_t n,
+                                                         uint64_t* state) {
+  __shared__ uint32_t h[kSelBins];
   __shared__ uint32_t sw[kThreads / 64];
+  for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
+  __syncthreads();
   uint32_t c = 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    c += gain[i] > 0.0 ? 1u : 0u;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+    const uint64_t k = gain_key(gain[i]);
+    c += k != 0;
+    atomicAdd(&h[k >> (64 - kSelBits)], 1u);
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
   if ((threadIdx.x & 63) == 0) sw[threadIdx.x >> 6] = c;
@@ -72,65 +106,46 @@ __global__ __launch_bounds__(kThreads) void k_count_eligible(const double* __res
   if (threadIdx.x == 0) {
     uint32_t t = 0;
     for (int k = 0; k < kThreads / 64; ++k) t += sw[k];
-    if (t) atomicAdd((unsigned long long*)counter, (unsigned long long)t);
+    if (t) atomicAdd((unsigned long long*)&state[kElig], (unsigned long long)t);
   }
+  for (int b = threadIdx.x; b < kSelBins; b += kThreads)
+    if (h[b]) atomicAdd((unsigned long long*)&state[kHist + b], (unsigned long long)h[b]);
 }
 
-hipError_t launch_count_eligible(const double* gain, int64_t n, uint64_t* counter, hipStream_t st) {
-  int64_t blocks = (n + kThreads - 1) / kThreads;
-  if (blocks > 512) blocks = 512;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_count_eligible, dim3((unsigned)blocks), dim3(kThreads), 0, st, gain, n,
-                     counter);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------- radix select
-// state: [0] prefix, [1] mask, [2] remaining, [3] done, [4 ..) histogram.
-// Each pass histograms the next digit of the keys that match the prefix so
-// far; the pick moves into the bin holding the remaining-th largest key.  When
-// that whole bin is taken the search stops early: every key in the bin is
-// selected, so the lower digits no longer matter.
-__global__ void k_select_init(uint64_t* state, int64_t K) {
-  if (threadIdx.x == 0) { state[0] = 0; state[1] = 0; state[2] = (uint64_t)K; state[3] = 0; }
-  for (int b = threadIdx.x; b < kSelBins; b += blockDim.x) state[4 + b] = 0;
-}
-
-__global__ __launch_bounds__(256) void k_select_hist(const double* __restrict__ gain, int64_t n,
-                                                     uint64_t* state, int shift, int width) {
-  if (state[3]) return;
+__global__ __launch_bounds__(kThreads) void k_select_hist(const double* __restrict__ gain, int64_t n,
+                                                          uint64_t* state, int shift, int width) {
+  if (state[kDone]) return;  // uniform: set before this launch
   __shared__ uint32_t h[kSelBins];
-  for (int b = threadIdx.x; b < kSelBins; b += blockDim.x) h[b] = 0;
+  for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
   __syncthreads();
-  const uint64_t prefix = state[0], mask = state[1];
+  const uint64_t prefix = state[kPrefix], mask = state[kMask];
   const uint64_t dm = (1ull << width) - 1ull;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
     const uint64_t k = gain_key(gain[i]);
     if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < (1 << width); b += blockDim.x)
-    if (h[b]) atomicAdd((unsigned long long*)&state[4 + b], (unsigned long long)h[b]);
+  for (int b = threadIdx.x; b < (1 << width); b += kThreads)
+    if (h[b]) atomicAdd((unsigned long long*)&state[kHist + b], (unsigned long long)h[b]);
 }
 
-// One block of 1024 threads: thread t owns bins counted from the top.
-__global__ __launch_bounds__(1024) void k_select_pick(uint64_t* state, int shift, int width) {
-  if (state[3]) return;
-  __shared__ uint64_t sc[1024];
+// One block of kThreads: thread t owns bpt consecutive bins counted from the top.
+__device__ void pick_bin(uint64_t* state, int shift, int width) {
+  __shared__ uint64_t sc[kThreads];
   __shared__ uint64_t found[3];
   const int nbins = 1 << width;
-  const int bpt = nbins >= 1024 ? nbins / 1024 : 1;
+  const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
   const int t = threadIdx.x;
-  const uint64_t rem = state[2];
+  const uint64_t rem = state[kRem];
   uint64_t local = 0;
   for (int i = 0; i < bpt; ++i) {
-    const int r = t * bpt + i;  // rank from the top
-    if (r < nbins) local += state[4 + (nbins - 1 - r)];
+    const int r = t * bpt + i;
+    if (r < nbins) local += state[kHist + (nbins - 1 - r)];
   }
   sc[t] = local;
+  if (t < 3) found[t] = 0;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
+  for (int off = 1; off < kThreads; off <<= 1) {
     const uint64_t v = t >= off ? sc[t - off] : 0;
     __syncthreads();
     sc[t] += v;
@@ -143,7 +158,7 @@ __global__ __launch_bounds__(1024) void k_select_pick(uint64_t* state, int shift
       const int r = t * bpt + i;
       if (r >= nbins) break;
       const int bin = nbins - 1 - r;
-      const uint64_t c = state[4 + bin];
+      const uint64_t c = state[kHist + bin];
       if (cum + c >= rem) {
         found[0] = (uint64_t)bin;
         found[1] = rem - cum;
@@ -155,19 +170,51 @@ __global__ __launch_bounds__(1024) void k_select_pick(uint64_t* state, int shift
   }
   __syncthreads();
   if (t == 0) {
-    state[0] |= found[0] << shift;
-    state[1] |= ((1ull << width) - 1ull) << shift;
-    state[2] = found[1];
-    state[3] = found[2];
+    state[kPrefix] |= found[0] << shift;
+    state[kMask] |= ((1ull << width) - 1ull) << shift;
+    state[kRem] = found[1];
+    state[kDone] = found[2];
   }
-  for (int b = t; b < nbins; b += 1024) state[4 + b] = 0;
+  for (int b = t; b < nbins; b += kThreads) state[kHist + b] = 0;
+}
+
+__global__ __launch_bounds__(kThreads) void k_select_pick(uint64_t* state, int shift, int width) {
+  if (state[kDone]) return;
+  pick_bin(state, shift, width);
+}
+
+// Segment start (one block): K = min(cap, eligible), the segment's first
+// record slot and the running totals, then the pick of the fused first pass.
+__global__ __launch_bounds__(kThreads) void k_segment_start(uint64_t* state, int64_t cap) {
+  __shared__ uint64_t s_k;
+  if (threadIdx.x == 0) {
+    const uint64_t ne = state[kElig];
+    const uint64_t K = ne < (uint64_t)cap ? ne : (uint64_t)cap;
+    state[kSegK] = K;
+    state[kSegOff] = state[kTotK];
+    state[kTotK] += K;
+    state[kTotElig] += ne;
+    state[kElig] = 0;
+    state[kPrefix] = 0;
+    state[kMask] = 0;
+    state[kRem] = K;
+    state[kDone] = K == 0 ? 1 : 0;
+    s_k = K;
+  }
+  __syncthreads();
+  if (s_k) {
+    pick_bin(state, 64 - kSelBits, kSelBits);
+  } else {
+    for (int b = threadIdx.x; b < kSelBins; b += kThreads) state[kHist + b] = 0;
+  }
 }
 
 // ---------------------------------------------------------------- compaction
 __global__ __launch_bounds__(kThreads) void k_compact_count(const double* __restrict__ gain, int64_t n,
                                                             const uint64_t* __restrict__ state,
                                                             uint64_t* blk_gt, uint64_t* blk_eq) {
-  const uint64_t prefix = state[0], mask = state[1];
+  if (state[kSegK] == 0) return;  // uniform
+  const uint64_t prefix = state[kPrefix], mask = state[kMask];
   uint32_t gt = 0, eq = 0;
   const int64_t base = (int64_t)blockIdx.x * kItems;
   for (int r = 0; r < kRounds; ++r) {
@@ -199,14 +246,14 @@ __global__ __launch_bounds__(kThreads) void k_compact_count(const double* __rest
 // equal keys in earlier blocks.
 __global__ __launch_bounds__(1024) void k_compact_scan(uint64_t* blk_gt, uint64_t* blk_eq, int64_t nblk,
                                                        const uint64_t* __restrict__ state) {
+  if (state[kSegK] == 0) return;
   __shared__ uint64_t sh[1024];
-  const uint64_t rem = state[2];
+  const uint64_t rem = state[kRem];
   uint64_t carry_eq = 0, carry_sel = 0;
   for (int64_t c0 = 0; c0 < nblk; c0 += 1024) {
     const int64_t i = c0 + threadIdx.x;
     const uint64_t gt = i < nblk ? blk_gt[i] : 0, eq = i < nblk ? blk_eq[i] : 0;
-    // inclusive scan of eq
-    sh[threadIdx.x] = eq;
+    sh[threadIdx.x] = eq;  // inclusive scan of the equal counts
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {
       const uint64_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
@@ -242,9 +289,10 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
                                                             const uint64_t* __restrict__ sel_off,
                                                             const uint64_t* __restrict__ eq_off,
                                                             SortItem* __restrict__ items_out) {
+  if (state[kSegK] == 0) return;  // uniform
   __shared__ uint32_t sh_w[kThreads / 64];
-  const uint64_t prefix = state[0], mask = state[1];
-  const uint64_t rem = state[2];
+  const uint64_t prefix = state[kPrefix], mask = state[kMask];
+  const uint64_t rem = state[kRem];
   uint64_t eq_run = eq_off[blockIdx.x];
   uint64_t sel_run = sel_off[blockIdx.x];
   const int64_t base = (int64_t)blockIdx.x * kItems;
@@ -275,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
 // on the pair is a total order and equal gains come out in increasing tile
 // order without any stability argument.
 __device__ __forceinline__ bool kv_less(const SortItem& a, const SortItem& b) {
-  return a.key < b.key || (a.key == b.key && a.tile < b.tile);
+  return (a.key < b.key) | ((a.key == b.key) & (a.tile < b.tile));  // no short-circuit branches
 }
 
 __device__ __forceinline__ void wave_sync() {
@@ -290,10 +338,13 @@ __device__ __forceinline__ void wave_sync() {
 // log2 j) and i + j; thread t takes pairs t and t + kChunkThreads, so for
 // j <= 64 every wavefront works inside its own two 128-element windows and a
 // wavefront-level barrier suffices between stages.
-__global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restrict__ items, int64_t n) {
+__global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restrict__ items,
+                                                               const uint64_t* __restrict__ state) {
   __shared__ uint64_t sk[kChunk];
   __shared__ uint32_t st[kChunk];
+  const int64_t n = (int64_t)state[kSegK];
   const int64_t base = (int64_t)blockIdx.x * kChunk;
+  if (base >= n) return;  // uniform per block
 #pragma unroll
   for (int r = 0; r < kChunk / kChunkThreads; ++r) {
     const int j = r * kChunkThreads + threadIdx.x;
@@ -339,41 +390,59 @@ __global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restr
   }
 }
 
-// One multiway merge pass: runs of 2^logw sorted items, groups of kFan runs.
+// One multiway merge pass: runs of 2^logw sorted items, groups of F runs.
 // An item's output slot is the first slot of its group, plus its index in its
 // own run, plus, for every other run of the group, the number of that run's
-// items that order before it: a lower bound by binary lifting, with the runs
-// of the group searched in lockstep so that their loads overlap.
-__global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__ in, int64_t n, int logw,
+// items that order before it.  That count is found digit by digit in radix
+// 2^LOGR: each level probes 2^LOGR - 1 positions of every run, all loads
+// independent and issued together (addresses clamped in range, results
+// masked), so a level costs one memory round trip.  Wide groups use binary
+// digits (F loads per level); the last pass over a few long runs uses base-8
+// digits, which cuts the number of round trips by three.
+template <int LOGR, int F>
+__global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__ in,
+                                                    const uint64_t* __restrict__ state, int logw,
                                                     SortItem* __restrict__ out) {
+  constexpr int NP = (1 << LOGR) - 1;  // probes per run per level
+  const int64_t n = (int64_t)state[kSegK];
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const SortItem x = in[i];
   const int64_t w = (int64_t)1 << logw;
   const int64_t run = i >> logw;
-  const int64_t g0 = run - run % kFan;
-  int64_t len[kFan];
-  int64_t cnt[kFan];
+  const int64_t g0 = run - run % F;
+  int64_t len[F];
+  int64_t cnt[F];
 #pragma unroll
-  for (int r = 0; r < kFan; ++r) {
+  for (int r = 0; r < F; ++r) {
     const int64_t rem = n - ((g0 + r) << logw);
     len[r] = (g0 + r == run || rem <= 0) ? 0 : (rem < w ? rem : w);
     cnt[r] = 0;
   }
-  for (int64_t step = w; step >= 1; step >>= 1) {
+  // largest power of 2^LOGR not above w: the count's top digit is then at most
+  // w / top < 2^LOGR
+  for (int64_t step = (int64_t)1 << (LOGR * (logw / LOGR)); step >= 1; step >>= LOGR) {
+    SortItem y[F][NP];
 #pragma unroll
-    for (int r = 0; r < kFan; ++r) {
-      if (len[r] > 0) {
-        const int64_t probe = cnt[r] + step;
-        const int64_t at = ((g0 + r) << logw) + (probe <= len[r] ? probe : len[r]) - 1;
-        const SortItem y = in[at];
-        if (probe <= len[r] && kv_less(y, x)) cnt[r] = probe;
+    for (int r = 0; r < F; ++r) {
+      const int64_t st = (g0 + r) << logw;
+#pragma unroll
+      for (int j = 1; j <= NP; ++j) {
+        const int64_t probe = cnt[r] + j * step;
+        y[r][j - 1] = in[len[r] > 0 ? st + (probe <= len[r] ? probe : len[r]) - 1 : i];
       }
+    }
+#pragma unroll
+    for (int r = 0; r < F; ++r) {
+      int c = 0;
+#pragma unroll
+      for (int j = 1; j <= NP; ++j) c += (int)((cnt[r] + j * step <= len[r]) & kv_less(y[r][j - 1], x));
+      cnt[r] += c * step;
     }
   }
   int64_t pos = (g0 << logw) + (i - (run << logw));
 #pragma unroll
-  for (int r = 0; r < kFan; ++r) pos += cnt[r];
+  for (int r = 0; r < F; ++r) pos += cnt[r];
   out[pos] = x;
 }
 
@@ -384,7 +453,7 @@ size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
   size_t b = 0;
   b += align_up(cap * sizeof(SortItem), 256) * 2;
   b += align_up((max_blocks + 1) * 8, 256) * 2;
-  b += align_up((4 + kSelBins) * 8, 256);
+  b += align_up((size_t)kStateWords * 8, 256);
   return b;
 }
 
@@ -403,37 +472,8 @@ RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
   return w;
 }
 
-hipError_t launch_select_sorted(const double* gain, int64_t t0, int64_t n, int64_t K,
-                                const RankWs& ws, const SortItem** sorted, hipStream_t st) {
-  *sorted = ws.items_a;
-  if (K <= 0) return hipSuccess;
-  const double* g = gain + t0;
-  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(1024), 0, st, ws.state, K);
-  int64_t hb = (n + kThreads - 1) / kThreads;
-  if (hb > 512) hb = 512;
-  // digits from the top: 12, 12, 12, 12, 12 and 4 bits
-  for (int shift = 52; shift >= 0; shift -= kSelBits) {
-    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, shift, kSelBits);
-    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(1024), 0, st, ws.state, shift, kSelBits);
-  }
-  hipLaunchKernelGGL(k_select_hist, dim3((unsigned)hb), dim3(256), 0, st, g, n, ws.state, 0, 4);
-  hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(1024), 0, st, ws.state, 0, 4);
-  const int64_t nbc = (n + kItems - 1) / kItems;
-  hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state,
-                     ws.blk_a, ws.blk_b);
-  hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
-  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
-                     ws.blk_a, ws.blk_b, ws.items_a);
-  // sort the K survivors ascending on (~key, tile): LDS chunks, then multiway merges
-  hipLaunchKernelGGL(k_sort_chunks, dim3((unsigned)((K + kChunk - 1) / kChunk)), dim3(kChunkThreads), 0, st,
-                     ws.items_a, K);
-  SortItem* in = ws.items_a;
-  SortItem* out = ws.items_b;
-  for (int logw = kLogChunk; ((int64_t)1 << logw) < K; logw += 4) {
-    hipLaunchKernelGGL(k_merge_runs, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, in, K, logw, out);
-    SortItem* t = in; in = out; out = t;
-  }
-  *sorted = in;
+hipError_t launch_rank_init(const RankWs& ws, hipStream_t st) {
+  hipLaunchKernelGGL(k_rank_init, dim3(1), dim3(256), 0, st, ws.state);
   return hipGetLastError();
 }
 
@@ -446,11 +486,19 @@ __device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v,
   pos += nbits;
 }
 
-__global__ void k_pack(const SortItem* __restrict__ sorted, int64_t K, const uint16_t* __restrict__ seed,
+// Record i of the segment goes to byte h + (first slot + i) * L of the
+// stream; a stream buffer too small for the running total raises the
+// no-space flag instead.
+__global__ void k_pack(const SortItem* __restrict__ sorted, uint64_t* state, const uint16_t* __restrict__ seed,
                        const int8_t* __restrict__ code, const uint16_t* __restrict__ scale, int P, int b,
-                       int idx_bits, int seed_bits, int L, uint8_t* __restrict__ out) {
+                       int idx_bits, int seed_bits, int L, uint64_t h, uint64_t cap, uint8_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= K) return;
+  const uint64_t K = state[kSegK], off = state[kSegOff];
+  if (i >= (int64_t)K) return;
+  if (h + (off + K) * (uint64_t)L > cap) {
+    if (i == 0) state[kNoSpace] = 1;
+    return;
+  }
   const uint32_t t = sorted[i].tile;
   uint64_t w[3] = {0, 0, 0};
   int pos = 0;
@@ -459,17 +507,58 @@ __global__ void k_pack(const SortItem* __restrict__ sorted, int64_t K, const uin
   const uint64_t cm = (1ull << b) - 1ull;
   for (int p = 0; p < P; ++p) put_bits(w, pos, (uint64_t)(int64_t)code[(int64_t)t * P + p] & cm, b);
   put_bits(w, pos, (uint64_t)scale[t], 16);
-  uint8_t* o = out + i * L;
+  uint8_t* o = out + h + (off + (uint64_t)i) * (uint64_t)L;
   for (int k = 0; k < L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
 }
 
-hipError_t launch_pack(const SortItem* sorted, int64_t K, const uint16_t* seed, const int8_t* code,
-                       const uint16_t* scale, int P, int b, int idx_bits, int seed_bits, int L_rec,
-                       uint8_t* out, hipStream_t st) {
-  if (K <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, st, sorted, K, seed, code,
-                     scale, P, b, idx_bits, seed_bits, L_rec, out);
+// One segment: count -> select -> compact -> sort -> pack, all on the device.
+// `cap` bounds K (the budget's record count, at most n); grids are sized by it
+// and kernels read the actual K from the state.
+hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_t cap, const RankWs& ws,
+                               const uint16_t* seed, const int8_t* code, const uint16_t* scale, int P, int b,
+                               int idx_bits, int seed_bits, int L, uint64_t h, uint64_t stream_cap,
+                               uint8_t* stream_out, hipStream_t st) {
+  const double* g = gain + t0;
+  int64_t cb = (n + kThreads - 1) / kThreads;
+  if (cb > 512) cb = 512;
+  if (cb < 1) cb = 1;
+  hipLaunchKernelGGL(k_count_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state);
+  hipLaunchKernelGGL(k_segment_start, dim3(1), dim3(kThreads), 0, st, ws.state, cap);
+  if (cap <= 0 || n <= 0) return hipGetLastError();
+  // remaining digits: 12, 12, 12, 12 and 4 bits
+  for (int shift = 64 - 2 * kSelBits; shift >= 0; shift -= kSelBits) {
+    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state, shift, kSelBits);
+    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(kThreads), 0, st, ws.state, shift, kSelBits);
+  }
+  hipLaunchKernelGGL(k_select_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state, 0, 4);
+  hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(kThreads), 0, st, ws.state, 0, 4);
+  const int64_t nbc = (n + kItems - 1) / kItems;
+  hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state, ws.blk_a, ws.blk_b);
+  hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
+  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
+                     ws.blk_a, ws.blk_b, ws.items_a);
+  // sort the survivors ascending on (~key, tile): LDS chunks, then multiway merges
+  hipLaunchKernelGGL(k_sort_chunks, dim3((unsigned)((cap + kChunk - 1) / kChunk)), dim3(kChunkThreads), 0, st,
+                     ws.items_a, ws.state);
+  SortItem* in = ws.items_a;
+  SortItem* out = ws.items_b;
+  for (int logw = kLogChunk; ((int64_t)1 << logw) < cap;) {
+    const dim3 grid((unsigned)((cap + 255) / 256));
+    if (cap <= ((int64_t)4 << logw)) {  // at most four runs left: one base-8 pass
+      hipLaunchKernelGGL((k_merge_runs<3, 4>), grid, dim3(256), 0, st, in, ws.state, logw, out);
+      logw += 2;
+    } else {
+      hipLaunchKernelGGL((k_merge_runs<1, kFan>), grid, dim3(256), 0, st, in, ws.state, logw, out);
+      logw += kLogFan;
+    }
+    SortItem* t = in; in = out; out = t;
+  }
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, st, in, ws.state, seed, code,
+                     scale, P, b, idx_bits, seed_bits, L, h, stream_cap, stream_out);
   return hipGetLastError();
 }
+
+// Totals of one call: records, eligible tiles, no-space flag.
+const uint64_t* rank_totals(const RankWs& ws) { return ws.state + kTotK; }
 
 }  // namespace awsrc

@@ -216,6 +216,23 @@ def test_rank_large_segment_with_ties():
         assert K == K_o and bytes(s.cpu().numpy().tobytes()) == want
 
 
+def test_rank_stream_capacity_too_small():
+    """K is found on the device; a stream buffer too small for the records is
+    reported as AWSRC_ENOSPC after the fact, with nothing written past it."""
+    p = awsrc.make_params(64, 4, 4, 64)
+    mods = [(64, 1024)]
+    rec = gen_records(1024, 4, 4, 64, seed=3, frac_nonpositive=0.0)
+    dev = {k: v.to(DEV) for k, v in rec.items()}
+    h = O.header_bytes(1)
+    L = O.record_bytes(O.Params(C=64, P=4, b=4, S=64), 1024)
+    buf = torch.full((h + 3 * L + 64,), 0xAB, dtype=torch.uint8, device=DEV)
+    with pytest.raises(awsrc.AwsrcError) as ei:
+        awsrc.awsrc_rank_prefix(p, mods, awsrc.AWSRC_MODE_GLOBAL, 8.0, dev["seed"], dev["codes"], dev["scale"],
+                                dev["gain"], stream_cap=h + 3 * L, out=buf)
+    assert ei.value.status == awsrc.AWSRC_ENOSPC
+    assert torch.all(buf[h + 3 * L:].cpu() == 0xAB)
+
+
 def test_rank_no_eligible_records():
     p = awsrc.make_params(64, 4, 4, 64)
     rec = gen_records(64, 4, 4, 64, seed=1)
@@ -302,6 +319,30 @@ def test_decode_prefixes_and_empty_stream():
             assert np.array_equal(got, W0.numpy())
         w0f = W0.numpy().astype(np.float64)
         assert np.all(np.abs(got - want) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(want - w0f)) + 1e-30)
+
+
+def test_decode_prepare_reuses_workspace():
+    """A workspace handed back to prepare is used when large enough (same
+    tensor returned) and replaced when too small; results match the oracle."""
+    C, P, b, S = 64, 8, 4, 256
+    mods = [(64, 1024)]
+    stream, K, enc = _oracle_stream(C, P, b, S, mods, 4.0, seed=6)
+    hd = O.parse_header(stream)
+    g = torch.Generator().manual_seed(5)
+    W0 = torch.randn(64, 1024, generator=g) * 0.02
+    ws = None
+    for k, expect_same in ((K // 2, False), (K // 4, True), (K, False)):
+        pre = stream[:hd["h"] + k * hd["L_rec"]]
+        dev = W0.to(DEV)
+        plan, ws2 = awsrc.awsrc_decode_prepare(torch.tensor(list(pre), dtype=torch.uint8, device=DEV), [dev],
+                                               workspace=ws)
+        assert (ws2 is ws) == expect_same
+        awsrc.awsrc_decode_apply(plan)
+        torch.cuda.synchronize()
+        ws = ws2
+        want = O.decode_add(pre, [W0.numpy()])[0]
+        w0f = W0.numpy().astype(np.float64)
+        assert np.all(np.abs(dev.cpu().numpy() - want) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(want - w0f)) + 1e-30)
 
 
 def _corrupt_cases(stream, hd):
