@@ -138,8 +138,9 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
   const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
   const size_t b_frag = screen_mfma_supported(p->C, p->P) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
-  const size_t b_tg = align_up((size_t)T * kTop * 4, 256);
-  const size_t b_ts = align_up((size_t)T * kTop * 2, 256);
+  const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode);
+  const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
+  const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
   const size_t need = b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
   if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
   if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
@@ -164,6 +165,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.top_gain = reinterpret_cast<float*>(ws);
   ws += b_tg;
   a.top_seed = reinterpret_cast<uint16_t*>(ws);
+  a.nsplit = nsplit;
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
   hipStream_t s = (hipStream_t)stream;

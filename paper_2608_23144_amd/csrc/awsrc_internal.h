@@ -85,8 +85,9 @@ struct EncodeArgs {
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
   double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
   void* frag;          // +-1 basis fragments of the matrix-core screen
-  float* top_gain;     // [T][kTop] screened gains, descending
-  uint16_t* top_seed;  // [T][kTop]
+  float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending
+  uint16_t* top_seed;  // [T][nsplit][kTop]
+  int nsplit;          // seed ranges screened by separate waves (merged in the re-score)
   uint16_t* seed_out;
   int8_t* code_out;
   uint16_t* scale_out;
@@ -98,6 +99,8 @@ bool encode_supported(int C, int P);
 bool screen_mfma_supported(int C, int P);
 int factor_pb(int C, int P);                 // padded P of the per-column factor table
 size_t mfma_frag_bytes(int C, int S);
+// Seed ranges per tile for the screen (1 unless the matrix-core screen runs).
+int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode);
 hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st);
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);

@@ -351,10 +351,30 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
   const double isq = 1.0 / sqrt((double)C);
   const int qmax = (1 << (a.b - 1)) - 1;
 
+  // merge the seed ranges' lists into the best kTop: ranges come in seed order
+  // and each list is ordered (gain desc, seed asc), so strict comparisons
+  // keep the lower seed first among equal gains
   float tg[kTop];
   int ts[kTop];
 #pragma unroll
-  for (int k = 0; k < kTop; ++k) { tg[k] = a.top_gain[t * kTop + k]; ts[k] = a.top_seed[t * kTop + k]; }
+  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+  for (int sp = 0; sp < a.nsplit; ++sp) {
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      const int64_t at = (t * a.nsplit + sp) * kTop + k;
+      float g = a.top_gain[at];
+      int sd = a.top_seed[at];
+#pragma unroll
+      for (int m = 0; m < kTop; ++m) {
+        if (g > tg[m]) {
+          const float tgm = tg[m];
+          const int tsm = ts[m];
+          tg[m] = g; ts[m] = sd;
+          g = tgm; sd = tsm;
+        }
+      }
+    }
+  }
   const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
 
   double best_g = -INFINITY;

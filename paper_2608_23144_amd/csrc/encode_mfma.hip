@@ -104,10 +104,12 @@ __global__ void k_mfma_frags(BasisTables bt, int C, int P, int S, u32x4* __restr
 
 // ----------------------------------------------------------------------------
 // Screen: one wavefront (one workgroup) = 64 consecutive rows of one column
-// block; lane = tile during the per-candidate stage.
+// block and one range of seed pairs; lane = tile during the per-candidate
+// stage.  Seed ranges are used only when a module has too few row groups to
+// fill the machine (each range costs its own tile loads and top list).
 template <bool PE>
-__global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4* __restrict__ frag,
-                                                      int stride) {
+__global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32x4* __restrict__ frag,
+                                                         int stride) {
   constexpr int C = 64;
   constexpr int PB = 8;
   constexpr int TS = 12;  // LDS stride (floats) of one tile's coefficients
@@ -115,8 +117,15 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
   __shared__ float wdl[PE ? 64 * (C + 1) : 1];
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
-  const int blk = blockIdx.x % nbk_cols;
-  const int64_t row0 = (int64_t)(blockIdx.x / nbk_cols) * 64;
+  const int nsplit = a.nsplit;
+  const int split = blockIdx.x % nsplit;
+  const int rest = blockIdx.x / nsplit;
+  const int blk = rest % nbk_cols;
+  const int64_t row0 = (int64_t)(rest / nbk_cols) * 64;
+  const int n_pairs_all = (a.S + 1) / 2;
+  const int pp = (n_pairs_all + nsplit - 1) / nsplit;
+  const int pair0 = split * pp;
+  const int pair1 = pair0 + pp < n_pairs_all ? pair0 + pp : n_pairs_all;
   const int n = lane & 15, g = lane >> 4;
 
   // ---- u = d .* r fragments for the 4 groups of 16 tiles, split in three bf16 parts
@@ -177,8 +186,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
   // Software pipeline: while the vector ALUs post-process seed pair k, the
   // matrix cores compute the projections of pair k+1 (the fragment table is
   // padded with zero pairs, so the last iterations need no special case).
-  const int n_pairs = (a.S + 1) / 2;
-  const u32x4* fp = frag + lane;
+  const u32x4* fp = frag + (size_t)pair0 * 128 + lane;
   auto project = [&](const u32x4& F0, const u32x4& F1, f32x4 (&acc)[4]) {
     const bf16x8 A0 = as_bf16x8(F0), A1 = as_bf16x8(F1);
 #pragma unroll
@@ -205,7 +213,7 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
     stash(acc);
   }
   u32x4 F0 = fp[128], F1 = fp[192];
-  for (int pair = 0; pair < n_pairs; ++pair) {
+  for (int pair = pair0; pair < pair1; ++pair) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -222,8 +230,8 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
     // projections of the next pair (zero rows past the last seed) and the prefetch after it
     f32x4 accN[4];
     project(F0, F1, accN);
-    F0 = fp[(size_t)(pair + 2) * 128];
-    F1 = fp[(size_t)(pair + 2) * 128 + 64];
+    F0 = fp[(size_t)(pair - pair0 + 2) * 128];
+    F1 = fp[(size_t)(pair - pair0 + 2) * 128 + 64];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int s = 2 * pair + k;
@@ -320,15 +328,28 @@ __global__ __launch_bounds__(64) void k_screen_mfma64(EncodeArgs a, const u32x4*
     stash(accN);
   }
   if (my_valid) {
-    const int64_t t = my_row * nbk_cols + blk;
-    a.top_gain[t * kTop + 0] = tg0 * (1.0f / 64.0f);  // back to gain units
-    a.top_gain[t * kTop + 1] = tg1 * (1.0f / 64.0f);
-    a.top_seed[t * kTop + 0] = (uint16_t)ts0;
-    a.top_seed[t * kTop + 1] = (uint16_t)ts1;
+    const int64_t at = ((my_row * nbk_cols + blk) * nsplit + split) * kTop;
+    a.top_gain[at + 0] = tg0 * (1.0f / 64.0f);  // back to gain units
+    a.top_gain[at + 1] = tg1 * (1.0f / 64.0f);
+    a.top_seed[at + 0] = (uint16_t)ts0;
+    a.top_seed[at + 1] = (uint16_t)ts1;
   }
 }
 
 bool screen_mfma_supported(int C, int P) { return C == 64 && P >= 1 && P <= 8; }
+
+// Seed ranges per tile: split only while the module's row groups would leave
+// the machine (about 2048 resident wavefronts at two per SIMD) under-filled,
+// keeping at least 16 seed pairs per range.
+int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode) {
+  (void)d_mode;
+  if (!screen_mfma_supported(C, P)) return 1;
+  const int64_t waves = (cols / C) * ((rows + 63) / 64);
+  const int pairs = (S + 1) / 2;
+  int ns = 1;
+  while (ns < 8 && waves * ns < 2048 && pairs / (2 * ns) >= 16) ns *= 2;
+  return ns;
+}
 
 // the table carries two zero pairs past the last seed (see the pipeline above)
 size_t mfma_frag_bytes(int C, int S) { return (size_t)((S + 1) / 2 + 2) * (C / 32) * 64 * 16; }
@@ -337,13 +358,12 @@ hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_
   const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
   hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
                      static_cast<u32x4*>(frag));
-  const int nb = (int)(a.cols / a.C);
-  const int64_t waves = nb * ((a.rows + 63) / 64);
+  const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
   if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL(k_screen_mfma64<true>, dim3((unsigned)waves), dim3(64), 0, st, a,
+    hipLaunchKernelGGL(k_screen_mfma64<true>, dim3((unsigned)wgs), dim3(64), 0, st, a,
                        static_cast<const u32x4*>(frag), colfac_stride(8));
   else
-    hipLaunchKernelGGL(k_screen_mfma64<false>, dim3((unsigned)waves), dim3(64), 0, st, a,
+    hipLaunchKernelGGL(k_screen_mfma64<false>, dim3((unsigned)wgs), dim3(64), 0, st, a,
                        static_cast<const u32x4*>(frag), colfac_stride(8));
   return hipGetLastError();
 }
