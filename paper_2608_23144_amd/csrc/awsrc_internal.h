@@ -57,11 +57,63 @@ inline BasisTables carve_basis(void* base, int S, int P) {
 }
 
 // Number of floats per (column block, seed) entry of the per-column factor
-// table: packed lower Cholesky factor of G = B^T D B + eps I, the reciprocal
-// diagonal, and eps.
+// table, G = B^T D B + eps I = L diag(e) L^T with L unit lower triangular:
+// the strict lower part of L packed row by row (entry (p, k), k < p, at
+// p (p - 1) / 2 + k), then 1 / e, then e.  Padded columns (p >= P) have
+// L = 0 and e = 1.
 inline int colfac_stride(int P) {
-  int n = P * (P + 1) / 2 + P + 1;
+  int n = P * (P - 1) / 2 + 2 * P;
   return (n + 3) & ~3;
+}
+
+__host__ __device__ __forceinline__ int ltri(int p, int k) { return p * (p - 1) / 2 + k; }
+
+// Screen score of one (tile, seed) from the per-column factor f (a table
+// entry as above, read through any pointer type): solves (G) alpha = b with
+// the LDL^T factor, quantizes alpha with one fp16 scale
+// (scale = f16(max |alpha| / qmax), q = clamp(rint(alpha / scale))), and
+// returns scale (2 q.b - scale q^T G q).  That is the exact gain
+// 2 a.b - a^T G0 a of the quantized fit minus scale^2 eps |q|^2 (relative
+// size ~ lambda), which the fp64 re-score of the kept seeds removes.  Uses
+// q.b = (L^T q).w with w = L^-1 b, and q^T G q = sum_k e_k (L^T q)_k^2.
+template <int PB, typename FP>
+__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
+  constexpr int LS = PB * (PB - 1) / 2;
+  float w[PB], al[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    float t = b[p];
+#pragma unroll
+    for (int k = 0; k < p; ++k) t = fmaf(-f[ltri(p, k)], w[k], t);
+    w[p] = t;
+  }
+#pragma unroll
+  for (int p = PB - 1; p >= 0; --p) {
+    float t = w[p] * f[LS + p];
+#pragma unroll
+    for (int k = p + 1; k < PB; ++k) t = fmaf(-f[ltri(k, p)], al[k], t);
+    al[p] = t;
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
+  uint16_t hb = __half_as_ushort(__float2half_rn(m * inv_qmax));
+  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;  // saturate at 65504
+  const float sc = __half2float(__ushort_as_half(hb));
+  const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+  float q[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
+  float t1 = 0.0f, quad = 0.0f;
+#pragma unroll
+  for (int k = 0; k < PB; ++k) {
+    float y = q[k];
+#pragma unroll
+    for (int i = k + 1; i < PB; ++i) y = fmaf(f[ltri(i, k)], q[i], y);
+    t1 = fmaf(y, w[k], t1);
+    quad = fmaf(f[LS + PB + k] * y, y, quad);
+  }
+  return sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
 }
 
 // ---------------------------------------------------------------- launchers

@@ -43,7 +43,6 @@ __device__ __forceinline__ float load_w_any(const void* W, int dt, int64_t i) {
   return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
 }
 
-__device__ __forceinline__ int tri(int p, int q) { return p * (p + 1) / 2 + q; }
 
 // fp16 scale of Sec. 3.2: f16(f32(v)) with saturation at 65504; returns bits.
 __device__ __forceinline__ uint16_t scale_bits_from_f32(float v) {
@@ -109,26 +108,30 @@ __global__ void k_col_factors(EncodeArgs a, int nb, int stride) {
       else g = (p == q) ? 1.0 : 0.0;
       G[p][q] = g;
     }
-  // Cholesky (G is SPD: d > 0 and the columns are orthonormal)
-  double L[PB][PB];
+  // LDL^T (G is SPD: d > 0 and the columns are orthonormal)
+  double L[PB][PB], e[PB];
 #pragma unroll
-  for (int p = 0; p < PB; ++p)
+  for (int p = 0; p < PB; ++p) {
 #pragma unroll
-    for (int q = 0; q <= p; ++q) {
+    for (int q = 0; q < p; ++q) {
       double acc = G[p][q];
 #pragma unroll
-      for (int k = 0; k < q; ++k) acc -= L[p][k] * L[q][k];
-      if (p == q) L[p][p] = sqrt(fmax(acc, 1e-300));
-      else L[p][q] = acc / L[q][q];
+      for (int k = 0; k < q; ++k) acc -= L[p][k] * L[q][k] * e[k];
+      L[p][q] = acc / e[q];
     }
+    double acc = G[p][p];
+#pragma unroll
+    for (int k = 0; k < p; ++k) acc -= L[p][k] * L[p][k] * e[k];
+    e[p] = fmax(acc, 1e-300);
+  }
   float* out = a.colfac + (size_t)idx * stride;
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
 #pragma unroll
-    for (int q = 0; q <= p; ++q) out[tri(p, q)] = (float)L[p][q];
-    out[PB * (PB + 1) / 2 + p] = (float)(1.0 / L[p][p]);
+    for (int q = 0; q < p; ++q) out[ltri(p, q)] = (float)L[p][q];
+    out[PB * (PB - 1) / 2 + p] = (float)(1.0 / e[p]);
+    out[PB * (PB - 1) / 2 + PB + p] = (float)e[p];
   }
-  out[PB * (PB + 1) / 2 + PB] = (float)eps;
 }
 
 // ----------------------------------------------------------------------------
@@ -179,14 +182,15 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
       }
       bv[p] = acc * InvSqrtC<C>::v;
     }
-    // Cholesky factor of G = B^T D B + eps I
-    float L[PB][PB], inv[PB], eps;
+    float g;
     if constexpr (PE) {
+      // Cholesky factor of G = B^T D B + eps I from the Gram gathers
+      float L[PB][PB], inv[PB];
       const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
       int c[PB];
 #pragma unroll
       for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
-      eps = (float)a.lambda * wd[0] * invC;
+      const float eps = (float)a.lambda * wd[0] * invC;
 #pragma unroll
       for (int p = 0; p < PB; ++p)
 #pragma unroll
@@ -203,57 +207,50 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
             L[p][q] = acc * inv[q];
           }
         }
+      // solve L L^T alpha = b
+      float z[PB], al[PB];
+#pragma unroll
+      for (int p = 0; p < PB; ++p) {
+        float acc = bv[p];
+#pragma unroll
+        for (int k = 0; k < p; ++k) acc -= L[p][k] * z[k];
+        z[p] = acc * inv[p];
+      }
+#pragma unroll
+      for (int p = PB - 1; p >= 0; --p) {
+        float acc = z[p];
+#pragma unroll
+        for (int k = p + 1; k < PB; ++k) acc -= L[k][p] * al[k];
+        al[p] = acc * inv[p];
+      }
+      // quantize with one fp16 scale and score
+      float m = 0.0f;
+#pragma unroll
+      for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
+      const float sc = __half2float(__ushort_as_half(scale_bits_from_f32(m * inv_qmax)));
+      g = 0.0f;
+      if (sc > 0.0f) {
+        const float isc = 1.0f / sc;
+        float q[PB], t1 = 0.0f, qq = 0.0f;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+          q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+          t1 += q[p] * bv[p];
+          qq += q[p] * q[p];
+        }
+        float quad = 0.0f;
+#pragma unroll
+        for (int k = 0; k < PB; ++k) {
+          float y = 0.0f;
+#pragma unroll
+          for (int i = k; i < PB; ++i) y += L[i][k] * q[i];
+          quad += y * y;
+        }
+        quad -= eps * qq;
+        g = sc * (2.0f * t1 - sc * quad);
+      }
     } else {
-      const float* f = a.colfac + ((size_t)blk * a.S + s) * stride;
-#pragma unroll
-      for (int p = 0; p < PB; ++p) {
-#pragma unroll
-        for (int q = 0; q <= p; ++q) L[p][q] = f[tri(p, q)];
-        inv[p] = f[PB * (PB + 1) / 2 + p];
-      }
-      eps = f[PB * (PB + 1) / 2 + PB];
-    }
-    // solve L L^T alpha = b
-    float z[PB], al[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p) {
-      float acc = bv[p];
-#pragma unroll
-      for (int k = 0; k < p; ++k) acc -= L[p][k] * z[k];
-      z[p] = acc * inv[p];
-    }
-#pragma unroll
-    for (int p = PB - 1; p >= 0; --p) {
-      float acc = z[p];
-#pragma unroll
-      for (int k = p + 1; k < PB; ++k) acc -= L[k][p] * al[k];
-      al[p] = acc * inv[p];
-    }
-    // quantize with one fp16 scale and score
-    float m = 0.0f;
-#pragma unroll
-    for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
-    const float sc = __half2float(__ushort_as_half(scale_bits_from_f32(m * inv_qmax)));
-    float g = 0.0f;
-    if (sc > 0.0f) {
-      const float isc = 1.0f / sc;
-      float q[PB], t1 = 0.0f, qq = 0.0f;
-#pragma unroll
-      for (int p = 0; p < PB; ++p) {
-        q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
-        t1 += q[p] * bv[p];
-        qq += q[p] * q[p];
-      }
-      float quad = 0.0f;
-#pragma unroll
-      for (int k = 0; k < PB; ++k) {
-        float y = 0.0f;
-#pragma unroll
-        for (int i = k; i < PB; ++i) y += L[i][k] * q[i];
-        quad += y * y;
-      }
-      quad -= eps * qq;
-      g = sc * (2.0f * t1 - sc * quad);
+      g = screen_score_ldl<PB>(bv, a.colfac + ((size_t)blk * a.S + s) * stride, qmax, inv_qmax);
     }
     // keep the best kTop, earlier (lower) seeds first among equals
     float cg = g;

@@ -47,7 +47,6 @@ __device__ __forceinline__ uint16_t scale_bits_f32(float v) {
   return hb;
 }
 
-__device__ __forceinline__ int tri2(int p, int q) { return p * (p + 1) / 2 + q; }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -213,6 +212,21 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
     stash(acc);
   }
   u32x4 F0 = fp[128], F1 = fp[192];
+  // per-column factors rotate through two register sets: the first seed's of
+  // the next pair load while the second seed of this pair is scored, and the
+  // second seed's load while the first is scored, hiding the load latency
+  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
+  typedef const __attribute__((address_space(4))) float* cfp;
+  auto fac_ptr = [&](int s) -> cfp {
+    const int sc_ = s < a.S ? s : a.S - 1;
+    return (cfp)(a.colfac + ((size_t)blk * a.S + sc_) * stride);
+  };
+  float fA[PE ? 1 : NF], fB[PE ? 1 : NF];
+  if constexpr (!PE) {
+    const cfp f0 = fac_ptr(2 * pair0);
+#pragma unroll
+    for (int i = 0; i < NF; ++i) fA[i] = f0[i];
+  }
   for (int pair = pair0; pair < pair1; ++pair) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -236,8 +250,9 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
     for (int k = 0; k < 2; ++k) {
       const int s = 2 * pair + k;
       const float* bv = bk[k];
-      float L[PB][PB], inv[PB], eps;
+      float gsc;
       if constexpr (PE) {
+        float L[PB][PB], inv[PB], eps;
         const int sc_ = s < a.S ? s : a.S - 1;
         const uint8_t* cs = a.basis.col + (size_t)sc_ * kMaxP;
         int c[PB];
@@ -261,56 +276,57 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
               L[p][q] = acc2 * inv[q];
             }
           }
-      } else {
-        const int sc_ = s < a.S ? s : a.S - 1;
-        // uniform across the wavefront: read through the constant address space (scalar loads)
-        const __attribute__((address_space(4))) float* f =
-            (const __attribute__((address_space(4))) float*)(a.colfac + ((size_t)blk * a.S + sc_) * stride);
+        float z[PB], al[PB];
 #pragma unroll
         for (int p = 0; p < PB; ++p) {
+          float t = bv[p];
 #pragma unroll
-          for (int q = 0; q <= p; ++q) L[p][q] = f[tri2(p, q)];
-          inv[p] = f[PB * (PB + 1) / 2 + p];
+          for (int kk = 0; kk < p; ++kk) t -= L[p][kk] * z[kk];
+          z[p] = t * inv[p];
         }
-        eps = f[PB * (PB + 1) / 2 + PB];
+#pragma unroll
+        for (int p = PB - 1; p >= 0; --p) {
+          float t = z[p];
+#pragma unroll
+          for (int kk = p + 1; kk < PB; ++kk) t -= L[kk][p] * al[kk];
+          al[p] = t * inv[p];
+        }
+        float m = 0.0f;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
+        const float sc = __half2float(__ushort_as_half(scale_bits_f32(m * inv_qmax)));
+        const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+        float q[PB], t1 = 0.0f, qq = 0.0f;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+          q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
+          t1 += q[p] * bv[p];
+          qq += q[p] * q[p];
+        }
+        float quad = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < PB; ++kk) {
+          float y = 0.0f;
+#pragma unroll
+          for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
+          quad += y * y;
+        }
+        quad -= eps * qq;
+        gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
+      } else {
+        // uniform across the wavefront: scalar loads through the constant address space
+        if (k == 0) {
+          const cfp fb = fac_ptr(s + 1);
+#pragma unroll
+          for (int i = 0; i < NF; ++i) fB[i] = fb[i];
+          gsc = screen_score_ldl<PB>(bk[0], fA, qmax, inv_qmax);
+        } else {
+          const cfp fa = fac_ptr(s + 1);
+#pragma unroll
+          for (int i = 0; i < NF; ++i) fA[i] = fa[i];
+          gsc = screen_score_ldl<PB>(bk[1], fB, qmax, inv_qmax);
+        }
       }
-      float z[PB], al[PB];
-#pragma unroll
-      for (int p = 0; p < PB; ++p) {
-        float t = bv[p];
-#pragma unroll
-        for (int kk = 0; kk < p; ++kk) t -= L[p][kk] * z[kk];
-        z[p] = t * inv[p];
-      }
-#pragma unroll
-      for (int p = PB - 1; p >= 0; --p) {
-        float t = z[p];
-#pragma unroll
-        for (int kk = p + 1; kk < PB; ++kk) t -= L[kk][p] * al[kk];
-        al[p] = t * inv[p];
-      }
-      float m = 0.0f;
-#pragma unroll
-      for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
-      const float sc = __half2float(__ushort_as_half(scale_bits_f32(m * inv_qmax)));
-      const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
-      float q[PB], t1 = 0.0f, qq = 0.0f;
-#pragma unroll
-      for (int p = 0; p < PB; ++p) {
-        q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
-        t1 += q[p] * bv[p];
-        qq += q[p] * q[p];
-      }
-      float quad = 0.0f;
-#pragma unroll
-      for (int kk = 0; kk < PB; ++kk) {
-        float y = 0.0f;
-#pragma unroll
-        for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
-        quad += y * y;
-      }
-      quad -= eps * qq;
-      float gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
       gsc = s < a.S ? gsc : -INFINITY;
       // branch-free insertion into the top two (earlier seeds first among equals)
       const bool c0 = gsc > tg0, c1 = gsc > tg1;
