@@ -334,8 +334,14 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
   extern __shared__ double fsh[];
   double* my = fsh + threadIdx.x * (C + 1);
   const int nb = (int)(a.cols / C);
-  const int blk = blockIdx.x % nb;
-  const int64_t row = (int64_t)(blockIdx.x / nb) * NT + threadIdx.x;
+  // Workgroups are dealt to the 8 XCDs round-robin by index: give each XCD a
+  // contiguous run of (row group, column block) items, so that neighbouring
+  // column blocks (adjacent per-tile outputs) share one L2.
+  const int64_t nwg = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, q = nwg / 8, rem = nwg % 8;
+  const int64_t w = xcd * q + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
+  const int blk = (int)(w % nb);
+  const int64_t row = (w / nb) * NT + threadIdx.x;
   if (row >= a.rows) return;
   const int64_t off = row * a.cols + (int64_t)blk * C;
   const int64_t t = row * nb + blk;

@@ -117,10 +117,17 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
   const int nsplit = a.nsplit;
-  const int split = blockIdx.x % nsplit;
-  const int rest = blockIdx.x / nsplit;
-  const int blk = rest % nbk_cols;
-  const int64_t row0 = (int64_t)(rest / nbk_cols) * 64;
+  // Workgroups are dealt to the 8 XCDs round-robin by index.  Give each XCD a
+  // contiguous run of work items in column-block-major order, so that the
+  // row groups of a column block share one L2 for their factor reads.
+  const int64_t nwg = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, q = nwg / 8, rem = nwg % 8;
+  const int64_t w = xcd * q + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
+  const int nrg = (int)((a.rows + 63) / 64);
+  const int split = (int)(w % nsplit);
+  const int64_t rest = w / nsplit;
+  const int blk = (int)(rest / nrg);
+  const int64_t row0 = (rest % nrg) * 64;
   const int n_pairs_all = (a.S + 1) / 2;
   const int pp = (n_pairs_all + nsplit - 1) / nsplit;
   const int pair0 = split * pp;
