@@ -29,6 +29,41 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# HBM bytes per launch measured with rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE
+# (one pass each; profiles/counters_*.md).  FETCH_SIZE is scaled by 2.0 and
+# WRITE_SIZE by 1.0: the ratios of a 1 GiB device copy's bytes to what the
+# same counters read for it.  An entry holds for the kernel sources it was
+# measured on (SHA-256 over the listed files); after any change to them the
+# figure is reported as null until the counters are taken again.
+MEASURED_TRAFFIC = {
+    ("encode", "down3b"): {
+        "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip"],
+        "sha256": "c8162196128d4577597864a108a16bbfb4cfa51a0a3f60b294e8ffae0486f8c5",
+        "bytes": 330677894},
+    ("backbone", "down3b"): {
+        "files": ["awsrc_internal.h", "backbone.hip"],
+        "sha256": "f7ed6ca04390a2a03408862e4e3882ab29873ad663e5330d4023c008cd6b40b3",
+        "bytes": 147301927},
+    ("decode_apply", "down3b"): {
+        "files": ["awsrc_internal.h", "decode.hip"],
+        "sha256": "6ad27f941ea8633b7e9f83360c7c02a2d1f905a7a0b9f27d140e9e7ba4d1d5d3",
+        "bytes": 22876765},
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    import hashlib
+
+    e = MEASURED_TRAFFIC.get((kernel, workload))
+    if e is None:
+        return None
+    h = hashlib.sha256()
+    for f in e["files"]:
+        with open(os.path.join(ROOT, "paper_2608_23144_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return e["bytes"] if h.hexdigest() == e["sha256"] else None
+
+
 def ops_per_candidate(C: int, P: int, per_element: bool) -> float:
     """Algorithmic fp32 operations per (tile, seed): projection (cheapest of the
     direct P*C form and a length-C fast Walsh-Hadamard transform), solve with a
@@ -233,12 +268,14 @@ def main() -> int:
                    "candidates": cand},
         "roofline": {"bound": "alu", "kernel": "awsrc_encode_tiles (basis, factors, screen, finalize)",
                      "achieved": achieved, "peak": PEAK_VALU_TOPS, "unit": "Tops/s",
-                     "frac": achieved / PEAK_VALU_TOPS, "traffic": None,
-                     "ops_per_candidate": opc},
+                     "frac": achieved / PEAK_VALU_TOPS, "traffic": measured_traffic("encode", wl.name),
+                     "traffic_unit": "bytes per launch", "ops_per_candidate": opc},
         "encode_candidates_per_s": cand / enc_s,
         "decode_add": {"records": K, "bytes": dec_bytes, "ms": stage_ms["decode_apply"], "GB/s": dec_gbs,
-                       "frac_hbm": (dec_gbs / PEAK_HBM_GBS) if dec_gbs else None},
-        "backbone": {"bytes": bb_bytes, "ms": stage_ms["backbone"], "GB/s": bb_gbs, "frac_hbm": bb_gbs / PEAK_HBM_GBS},
+                       "frac_hbm": (dec_gbs / PEAK_HBM_GBS) if dec_gbs else None,
+                       "traffic": measured_traffic("decode_apply", wl.name)},
+        "backbone": {"bytes": bb_bytes, "ms": stage_ms["backbone"], "GB/s": bb_gbs, "frac_hbm": bb_gbs / PEAK_HBM_GBS,
+                     "traffic": measured_traffic("backbone", wl.name)},
         "stage_ms": stage_ms,
         "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
         "device": torch.cuda.get_device_name(0),
