@@ -41,13 +41,6 @@ __device__ __forceinline__ float load_w_any2(const void* W, int dt, int64_t i) {
   return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
 }
 
-__device__ __forceinline__ uint16_t scale_bits_f32(float v) {
-  uint16_t hb = __half_as_ushort(__float2half_rn(v));
-  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;
-  return hb;
-}
-
-
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Exact three-way bf16 split of eight fp32 values, packed two per dword.
@@ -174,12 +167,12 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
           wd[k] = x + y;
           wd[k + h] = x - y;
         }
+    // stored divided by C, so the gathers are the Gram entries themselves
 #pragma unroll
-    for (int j = 0; j < C; ++j) wdl[lane * (C + 1) + j] = wd[j];
+    for (int j = 0; j < C; ++j) wdl[lane * (C + 1) + j] = wd[j] * (1.0f / C);
   }
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
-  const float invC = 1.0f / C;
   const float lam = (float)a.lambda;
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
@@ -256,70 +249,40 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int s = 2 * pair + k;
-      const float* bv = bk[k];
       float gsc;
       if constexpr (PE) {
-        float L[PB][PB], inv[PB], eps;
+        // this tile's G + eps I = L diag(e) L^T from the Gram gathers, row by
+        // row (E = L diag(e) kept for the current row only), in the layout of
+        // the per-column table so the same score routine applies
+        constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
+        constexpr int LS = PB * (PB - 1) / 2;
+        float f[NF];
         const int sc_ = s < a.S ? s : a.S - 1;
         const uint8_t* cs = a.basis.col + (size_t)sc_ * kMaxP;
         int c[PB];
 #pragma unroll
         for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
         const float* wrow = &wdl[lane * (C + 1)];
-        eps = lam * wrow[0] * invC;
+        const float eps = lam * wrow[0];
 #pragma unroll
-        for (int p = 0; p < PB; ++p)
+        for (int p = 0; p < PB; ++p) {
+          float E[PB];
 #pragma unroll
-          for (int q = 0; q <= p; ++q) {
-            float acc2;
-            if (p < P && q < P) acc2 = wrow[c[p] ^ c[q]] * invC + (p == q ? eps : 0.0f);
-            else acc2 = (p == q) ? 1.0f : 0.0f;
+          for (int q = 0; q < p; ++q) {
+            float t = (p < P && q < P) ? wrow[c[p] ^ c[q]] : 0.0f;
 #pragma unroll
-            for (int kk = 0; kk < q; ++kk) acc2 -= L[p][kk] * L[q][kk];
-            if (p == q) {
-              L[p][p] = sqrtf(fmaxf(acc2, 1e-30f));
-              inv[p] = __builtin_amdgcn_rcpf(L[p][p]);
-            } else {
-              L[p][q] = acc2 * inv[q];
-            }
+            for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
+            E[q] = t;
+            f[ltri(p, q)] = t * f[LS + q];
           }
-        float z[PB], al[PB];
+          float t = (p < P) ? wrow[0] + eps : 1.0f;
 #pragma unroll
-        for (int p = 0; p < PB; ++p) {
-          float t = bv[p];
-#pragma unroll
-          for (int kk = 0; kk < p; ++kk) t -= L[p][kk] * z[kk];
-          z[p] = t * inv[p];
+          for (int kk = 0; kk < p; ++kk) t = fmaf(-E[kk], f[ltri(p, kk)], t);
+          t = fmaxf(t, 1e-30f);
+          f[LS + PB + p] = t;
+          f[LS + p] = __builtin_amdgcn_rcpf(t);
         }
-#pragma unroll
-        for (int p = PB - 1; p >= 0; --p) {
-          float t = z[p];
-#pragma unroll
-          for (int kk = p + 1; kk < PB; ++kk) t -= L[kk][p] * al[kk];
-          al[p] = t * inv[p];
-        }
-        float m = 0.0f;
-#pragma unroll
-        for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
-        const float sc = __half2float(__ushort_as_half(scale_bits_f32(m * inv_qmax)));
-        const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
-        float q[PB], t1 = 0.0f, qq = 0.0f;
-#pragma unroll
-        for (int p = 0; p < PB; ++p) {
-          q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
-          t1 += q[p] * bv[p];
-          qq += q[p] * q[p];
-        }
-        float quad = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < PB; ++kk) {
-          float y = 0.0f;
-#pragma unroll
-          for (int i = kk; i < PB; ++i) y += L[i][kk] * q[i];
-          quad += y * y;
-        }
-        quad -= eps * qq;
-        gsc = sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
+        gsc = screen_score_ldl<PB>(bk[k], f, qmax, inv_qmax);
       } else {
         // uniform across the wavefront: scalar loads through the constant address space
         if (k == 0) {
