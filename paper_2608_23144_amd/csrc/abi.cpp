@@ -137,7 +137,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
   const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
-  const size_t b_frag = screen_mfma_supported(p->C, p->P) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
+  const size_t b_frag = screen_mfma_supported(p->C, p->P, d_mode) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
   const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);

@@ -148,7 +148,7 @@ struct EncodeArgs {
 };
 
 bool encode_supported(int C, int P);
-bool screen_mfma_supported(int C, int P);
+bool screen_mfma_supported(int C, int P, int d_mode);
 int factor_pb(int C, int P);                 // padded P of the per-column factor table
 size_t mfma_frag_bytes(int C, int S);
 // Seed ranges per tile for the screen (1 unless the matrix-core screen runs).

@@ -528,7 +528,7 @@ bool encode_supported(int C, int P) {
   return (C == 16 || C == 32 || C == 64 || C == 128) && P >= 1 && P <= kMaxP && P <= C;
 }
 
-int factor_pb(int C, int P) { return screen_mfma_supported(C, P) ? 8 : pad_p(P); }
+int factor_pb(int C, int P) { return screen_mfma_supported(C, P, AWSRC_D_PER_COL) ? 8 : pad_p(P); }
 
 template <int C, int PB>
 static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
@@ -596,7 +596,7 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
 #define PBSEL(C_, P_) factor_pb(C_, P_)
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_factors, a, st); }
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st) {
-  if (screen_mfma_supported(a.C, a.P)) return launch_encode_screen_mfma(a, a.frag, st);
+  if (screen_mfma_supported(a.C, a.P, a.d_mode)) return launch_encode_screen_mfma(a, a.frag, st);
   AWSRC_DISPATCH(run_screen, a, st);
 }
 #undef PBSEL

@@ -322,15 +322,178 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   }
 }
 
-bool screen_mfma_supported(int C, int P) { return C == 64 && P >= 1 && P <= 8; }
+// ----------------------------------------------------------------------------
+// C = 128, per-column weights.  The u fragments of a 128-coordinate tile take
+// twice the registers, so a wavefront holds 32 consecutive rows of one column
+// block (2 groups of 16 tiles x 4 K steps x 3 bf16 parts) and gives the two
+// seeds of a pair to its two lane halves: lane = (seed of the pair, tile).
+// The seed is then uniform per half only, so each lane reads its seed's
+// per-column factors with vector loads (two addresses per wavefront).  b is
+// scaled by 1/sqrt(128) before scoring (not a power of two, so raw units
+// would round the fp16 scale differently); each half keeps its own top two,
+// merged at the end.
+__global__ __launch_bounds__(64, 2) void k_screen_mfma128(EncodeArgs a, const u32x4* __restrict__ frag,
+                                                          int stride) {
+  constexpr int C = 128;
+  constexpr int PB = 8;
+  constexpr int NKS = C / 32;
+  constexpr int TS = 12;  // LDS stride (floats) of one lane's coefficients
+  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
+  __shared__ __attribute__((aligned(16))) float tb[64 * TS];
+  const int lane = threadIdx.x;
+  const int nbk_cols = (int)(a.cols / C);
+  const int nsplit = a.nsplit;
+  const int64_t nwg = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, q = nwg / 8, rem = nwg % 8;
+  const int64_t w = xcd * q + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
+  const int nrg = (int)((a.rows + 31) / 32);
+  const int split = (int)(w % nsplit);
+  const int64_t rest = w / nsplit;
+  const int blk = (int)(rest / nrg);
+  const int64_t row0 = (rest % nrg) * 32;
+  const int n_pairs_all = (a.S + 1) / 2;
+  const int pp = (n_pairs_all + nsplit - 1) / nsplit;
+  const int pair0 = split * pp;
+  const int pair1 = pair0 + pp < n_pairs_all ? pair0 + pp : n_pairs_all;
+  const int n = lane & 15, g = lane >> 4;
+
+  u32x4 uh[2][NKS], um[2][NKS], ul[2][NKS];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int64_t row = row0 + 16 * nb + n;
+    const bool valid = row < a.rows;
+    const int64_t rr = valid ? row : a.rows - 1;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int jc = 32 * ks + 8 * g;
+      const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
+      float u[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float r = load_w_any2(a.W, a.w_dtype, base + e) - a.W0[base + e];
+        u[e] = valid ? a.d[(int64_t)blk * C + jc + e] * r : 0.0f;
+      }
+      split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
+    }
+  }
+  const int half = lane >> 5;
+  const int64_t my_row = row0 + (lane & 31);
+  const bool my_valid = my_row < a.rows;
+  const float qmax = (float)((1 << (a.b - 1)) - 1);
+  const float inv_qmax = 1.0f / qmax;
+  constexpr float isq = 0.08838834764831845f;  // 1/sqrt(128)
+  float tg0 = -INFINITY, tg1 = -INFINITY;
+  int ts0 = 0, ts1 = 0;
+
+  const u32x4* fp = frag + (size_t)pair0 * (NKS * 64) + lane;
+  auto project = [&](const u32x4 (&F)[NKS], f32x4 (&acc)[2]) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const bf16x8 A = as_bf16x8(F[ks]);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, as_bf16x8(uh[nb][ks]), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, as_bf16x8(um[nb][ks]), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, as_bf16x8(ul[nb][ks]), c, 0, 0, 0);
+      }
+      acc[nb] = c;
+    }
+  };
+  // rows 4g..4g+3 of the product = (seed g/2 of the pair, columns 4(g&1)..+3)
+  // of tiles 16nb + n; lane (seed half, tile) reads them back
+  auto stash = [&](const f32x4 (&acc)[2]) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+      *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 32 + 16 * nb + n) * TS + 4 * (g & 1)]) = acc[nb];
+  };
+  u32x4 F[NKS];
+  {
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[ks * 64];
+    f32x4 acc[2];
+    project(F, acc);
+    stash(acc);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[NKS * 64 + ks * 64];
+  }
+  for (int pair = pair0; pair < pair1; ++pair) {
+    const int s = 2 * pair + half;
+    const int sc_ = s < a.S ? s : a.S - 1;
+    const f32x4* fv = reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + sc_) * stride);
+    float f[NF];
+#pragma unroll
+    for (int i = 0; i < NF / 4; ++i) {
+      const f32x4 v = fv[i];
+      f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    float bv[PB];
+    {
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[lane * TS]);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[lane * TS + 4]);
+      bv[0] = b0[0] * isq; bv[1] = b0[1] * isq; bv[2] = b0[2] * isq; bv[3] = b0[3] * isq;
+      bv[4] = b1[0] * isq; bv[5] = b1[1] * isq; bv[6] = b1[2] * isq; bv[7] = b1[3] * isq;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    f32x4 accN[2];
+    project(F, accN);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
+    float gsc = screen_score_ldl<PB>(bv, f, qmax, inv_qmax);
+    gsc = s < a.S ? gsc : -INFINITY;
+    // this lane's seeds increase, so strict comparisons keep the lower seed among equals
+    const bool c0 = gsc > tg0, c1 = gsc > tg1;
+    tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
+    ts1 = c0 ? ts0 : (c1 ? s : ts1);
+    tg0 = c0 ? gsc : tg0;
+    ts0 = c0 ? s : ts0;
+#pragma unroll
+    for (int i = 0; i < 24; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+    }
+    stash(accN);
+  }
+  // merge the two halves' lists of each tile: (gain desc, seed asc)
+  const float og0 = __shfl(tg0, lane + 32, 64), og1 = __shfl(tg1, lane + 32, 64);
+  const int os0 = __shfl(ts0, lane + 32, 64), os1 = __shfl(ts1, lane + 32, 64);
+  if (half == 0 && my_valid) {
+    auto better = [](float ga, int sa, float gb, int sb) { return ga > gb || (ga == gb && sa < sb); };
+    float r0, r1;
+    int q0, q1;
+    if (better(tg0, ts0, og0, os0)) {
+      r0 = tg0; q0 = ts0;
+      const bool m = better(tg1, ts1, og0, os0);
+      r1 = m ? tg1 : og0; q1 = m ? ts1 : os0;
+    } else {
+      r0 = og0; q0 = os0;
+      const bool m = better(tg0, ts0, og1, os1);
+      r1 = m ? tg0 : og1; q1 = m ? ts0 : os1;
+    }
+    const int64_t at = ((my_row * nbk_cols + blk) * nsplit + split) * kTop;
+    a.top_gain[at + 0] = r0;
+    a.top_gain[at + 1] = r1;
+    a.top_seed[at + 0] = (uint16_t)q0;
+    a.top_seed[at + 1] = (uint16_t)q1;
+  }
+}
+
+bool screen_mfma_supported(int C, int P, int d_mode) {
+  if (P < 1 || P > 8) return false;
+  return C == 64 || (C == 128 && d_mode == AWSRC_D_PER_COL);
+}
 
 // Seed ranges per tile: split only while the module's row groups would leave
 // the machine (about 2048 resident wavefronts at two per SIMD) under-filled,
 // keeping at least 16 seed pairs per range.
 int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode) {
-  (void)d_mode;
-  if (!screen_mfma_supported(C, P)) return 1;
-  const int64_t waves = (cols / C) * ((rows + 63) / 64);
+  if (!screen_mfma_supported(C, P, d_mode)) return 1;
+  const int tpw = C == 128 ? 32 : 64;  // rows per wavefront
+  const int64_t waves = (cols / C) * ((rows + tpw - 1) / tpw);
   const int pairs = (S + 1) / 2;
   int ns = 1;
   while (ns < 8 && waves * ns < 2048 && pairs / (2 * ns) >= 16) ns *= 2;
@@ -344,6 +507,12 @@ hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_
   const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
   hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
                      static_cast<u32x4*>(frag));
+  if (a.C == 128) {
+    const int64_t wgs = (a.cols / a.C) * ((a.rows + 31) / 32) * a.nsplit;
+    hipLaunchKernelGGL(k_screen_mfma128, dim3((unsigned)wgs), dim3(64), 0, st, a,
+                       static_cast<const u32x4*>(frag), colfac_stride(8));
+    return hipGetLastError();
+  }
   const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
   if (a.d_mode == AWSRC_D_PER_ELEM)
     hipLaunchKernelGGL(k_screen_mfma64<true>, dim3((unsigned)wgs), dim3(64), 0, st, a,

@@ -132,6 +132,8 @@ def test_encode_linear256_full():
     (16, 4, 4, 16, 9, 128, "col"),      # the paper's P_F operating point shape
     (64, 3, 5, 10, 20, 128, "col"),     # padded P
     (128, 2, 4, 2, 8, 256, "col"),      # the paper's U operating point shape
+    (128, 8, 4, 64, 70, 512, "col"),    # matrix-core C=128 screen: ragged 32-row waves, seed ranges
+    (128, 5, 4, 33, 40, 256, "col"),    # odd S: the last seed pair has one seed
     (64, 16, 8, 8, 4, 128, "elem"),
 ])
 def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
