@@ -331,10 +331,11 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
 // per-column factors with vector loads (two addresses per wavefront).  b is
 // scaled by 1/sqrt(128) before scoring (not a power of two, so raw units
 // would round the fp16 scale differently); each half keeps its own top two,
-// merged at the end.
-__global__ __launch_bounds__(64, 2) void k_screen_mfma128(EncodeArgs a, const u32x4* __restrict__ frag,
-                                                          int stride) {
-  constexpr int C = 128;
+// merged at the end.  (Written for any C that is a multiple of 32; at C = 64
+// it measured slower than k_screen_mfma64, which is used there.)
+template <int C>
+__global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, const u32x4* __restrict__ frag,
+                                                              int stride) {
   constexpr int PB = 8;
   constexpr int NKS = C / 32;
   constexpr int TS = 12;  // LDS stride (floats) of one lane's coefficients
@@ -381,7 +382,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma128(EncodeArgs a, const u3
   const bool my_valid = my_row < a.rows;
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
-  constexpr float isq = 0.08838834764831845f;  // 1/sqrt(128)
+  constexpr float isq = C == 64 ? 0.125f : 0.08838834764831845f;  // 1/sqrt(C)
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
 
@@ -509,7 +510,7 @@ hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_
                      static_cast<u32x4*>(frag));
   if (a.C == 128) {
     const int64_t wgs = (a.cols / a.C) * ((a.rows + 31) / 32) * a.nsplit;
-    hipLaunchKernelGGL(k_screen_mfma128, dim3((unsigned)wgs), dim3(64), 0, st, a,
+    hipLaunchKernelGGL(k_screen_mfma_halves<128>, dim3((unsigned)wgs), dim3(64), 0, st, a,
                        static_cast<const u32x4*>(frag), colfac_stride(8));
     return hipGetLastError();
   }
