@@ -258,10 +258,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
         constexpr int LS = PB * (PB - 1) / 2;
         float f[NF];
         const int sc_ = s < a.S ? s : a.S - 1;
-        const uint8_t* cs = a.basis.col + (size_t)sc_ * kMaxP;
+        // the seed's columns: two scalar dword loads (uniform across the wavefront)
+        const __attribute__((address_space(4))) uint32_t* cw =
+            (const __attribute__((address_space(4))) uint32_t*)(a.basis.col + (size_t)sc_ * kMaxP);
+        const uint32_t cw0 = cw[0], cw1 = cw[1];
         int c[PB];
 #pragma unroll
-        for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
+        for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw0 : cw1) >> (8 * (p & 3))) & 0xFFu) : 0;
         const float* wrow = &wdl[lane * (C + 1)];
         const float eps = lam * wrow[0];
 #pragma unroll
