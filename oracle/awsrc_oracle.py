@@ -33,10 +33,15 @@ Readings of points the paper leaves open (each listed in the design notes):
   scaled by 1/sqrt(C).
 * Ridge constant: eps_t = lambda * mean_j d_{t,j}; it enters the fit only,
   not the selection score.
-* Scale: fp16, scale16 = f16(f32(m / qmax)) with both roundings to nearest
-  even, m = max_p |alpha*_p|; codes q_p = clip(rint(alpha*_p / scale), +-qmax),
-  qmax = 2^(b-1) - 1; a zero m, or a scale that rounds to zero, gives an
-  all-zero record with gain 0; fp16 overflow saturates at 65504.
+* Scale, two formats (Sec. 3.2 names one power-of-two scale per tile stored
+  as an exponent of width b_e, Eq. (5); the default here is fp16):
+  - fp16: scale16 = f16(f32(m / qmax)) with both roundings to nearest even,
+    m = max_p |alpha*_p|; a zero m, or a scale that rounds to zero, gives an
+    all-zero record with gain 0; fp16 overflow saturates at 65504;
+  - pow2: scale = 2^e with e the smallest integer such that m <= qmax 2^e
+    (no code clips), clamped to [-128, 127] and stored as e + 128 in
+    b_e = 8 bits; m = 0 gives an all-zero record (field 0, gain 0).
+  Codes q_p = clip(rint(alpha*_p / scale), +-qmax), qmax = 2^(b-1) - 1.
 * Ties: the lowest seed wins among exactly equal gains; equal rho orders by
   the lower global tile index; only gain > 0 is eligible.
 * Backbone RTN-v1: asymmetric INT4, groups of 128 input columns, fp32
@@ -58,7 +63,10 @@ GOLDEN_GAMMA = 0x9E3779B97F4A7C15
 MAGIC = b"AWSR"
 STREAM_VERSION = 1
 HEADER_FIXED_BYTES = 40
+SCALE_FP16, SCALE_POW2 = 0, 1
 SCALE_BITS_FP16 = 16
+SCALE_BITS_POW2 = 8          # b_e of Eq. (5) for the power-of-two scale
+POW2_BIAS = 128
 FP16_MAX = 65504.0
 
 
@@ -76,6 +84,11 @@ class Params:
     ridge_lambda: float = 1e-6
     idx_bits: int = 32          # 0 selects ceil(log2 T_total) as in Eq. (5)
     gen_version: int = 1
+    scale_fmt: int = SCALE_FP16  # SCALE_FP16 or SCALE_POW2
+
+    @property
+    def scale_bits(self) -> int:
+        return SCALE_BITS_POW2 if self.scale_fmt == SCALE_POW2 else SCALE_BITS_FP16
 
     @property
     def qmax(self) -> int:
@@ -234,13 +247,34 @@ def fit(R: np.ndarray, Dw: np.ndarray, B: np.ndarray, ridge_lambda: float):
     return alpha, G, bvec
 
 
-def quantize(alpha: np.ndarray, b: int):
-    """Coefficient-wise b-bit RTN with one scale per tile (Sec. 3.2), fp16 scale.
+def pow2_exponent(m: float, qmax: int) -> int:
+    """Smallest integer e with m <= qmax * 2^e (m > 0), by exact comparisons."""
+    e = math.frexp(m / qmax)[1]          # m/qmax < 2^e, up to the rounding of the division
+    while m > qmax * math.ldexp(1.0, e):
+        e += 1
+    while m <= qmax * math.ldexp(1.0, e - 1):
+        e -= 1
+    return e
 
-    Returns (codes int64 [N, P], scale16 bits uint16 [N], scale value float64 [N]).
+
+def quantize(alpha: np.ndarray, b: int, scale_fmt: int = SCALE_FP16):
+    """Coefficient-wise b-bit RTN with one scale per tile (Sec. 3.2).
+
+    Returns (codes int64 [N, P], stored scale field uint16 [N] (fp16 bits, or
+    the biased exponent), scale value float64 [N]).
     """
     qmax = (1 << (b - 1)) - 1
     m = np.abs(alpha).max(axis=1)
+    if scale_fmt == SCALE_POW2:
+        e = np.array([min(127, max(-128, pow2_exponent(float(v), qmax))) if v > 0 else -POW2_BIAS for v in m],
+                     dtype=np.int64)
+        sc = np.ldexp(1.0, e)
+        empty = m == 0
+        q = np.clip(np.rint(alpha / sc[:, None]), -qmax, qmax)
+        q = np.where(empty[:, None], 0.0, q).astype(np.int64)
+        bits = (e + POW2_BIAS).astype(np.uint16)
+        sc = np.where(empty, 0.0, sc)
+        return q, bits, sc
     s32 = (m / qmax).astype(np.float32)
     with np.errstate(over="ignore"):
         s16 = s32.astype(np.float16)
@@ -268,9 +302,15 @@ def _boundary_flags(alpha, sc, qmax, tol=1e-9):
     return np.any((frac < tol) & (x < qmax + 0.5), axis=1) & (sc > 0)
 
 
-def _scale_flags(alpha, qmax, tol=1e-12):
-    """True where m/qmax lies within tol (relative) of an fp32 rounding midpoint."""
+def _scale_flags(alpha, qmax, tol=1e-12, scale_fmt=SCALE_FP16):
+    """True where the scale choice is on a knife edge: m/qmax within tol
+    (relative) of an fp32 rounding midpoint (fp16 format), or of a power of
+    two (pow2 format)."""
     m = np.abs(alpha).max(axis=1)
+    if scale_fmt == SCALE_POW2:
+        v = m / qmax
+        lg = np.log2(np.where(m > 0, v, 1.0))
+        return (np.abs(lg - np.rint(lg)) <= tol / math.log(2)) & (m > 0)
     v = m / qmax
     f = v.astype(np.float32).astype(np.float64)
     ulp = np.spacing(np.abs(v).astype(np.float32)).astype(np.float64)
@@ -310,7 +350,7 @@ def encode_tiles(R: np.ndarray, Dw: np.ndarray, params: Params,
     for s, B in enumerate(bases):
         alpha, _, _ = fit(R, Dw, B, params.ridge_lambda)
         if quantize_coeffs:
-            q, bits, sc = quantize(alpha, params.b)
+            q, bits, sc = quantize(alpha, params.b, params.scale_fmt)
             ahat = sc[:, None] * q
         else:
             q = np.zeros((N, P), dtype=np.int64)
@@ -333,7 +373,8 @@ def encode_tiles(R: np.ndarray, Dw: np.ndarray, params: Params,
         "seed": best_seed, "codes": best_codes, "scale": best_bits, "scale_value": best_sc,
         "gain": best_gain, "alpha": best_alpha, "energy": energy,
         "flag_half": _boundary_flags(best_alpha, best_sc, qmax) if quantize_coeffs else np.zeros(N, bool),
-        "flag_scale": _scale_flags(best_alpha, qmax) if quantize_coeffs else np.zeros(N, bool),
+        "flag_scale": (_scale_flags(best_alpha, qmax, scale_fmt=params.scale_fmt) if quantize_coeffs
+                       else np.zeros(N, bool)),
         "flag_tie": (best_gain - second_gain) <= 1e-6 * np.abs(best_gain),
         "flag_zero": np.abs(best_gain) <= 1e-12 * energy,
     }
@@ -346,7 +387,7 @@ def candidate(R_t: np.ndarray, D_t: np.ndarray, params: Params, s: int):
     """The full encoder chain for one (tile, seed): (codes, scale bits, gain, alpha*)."""
     B = basis_matrix(params.basis_key, s, R_t.shape[0], params.P)
     alpha, _, _ = fit(R_t[None].astype(np.float64), D_t[None].astype(np.float64), B, params.ridge_lambda)
-    q, bits, sc = quantize(alpha, params.b)
+    q, bits, sc = quantize(alpha, params.b, params.scale_fmt)
     g = weighted_gain(R_t[None].astype(np.float64), D_t[None].astype(np.float64), (sc[:, None] * q) @ B.T)
     return q[0], int(bits[0]), float(g[0]), alpha[0]
 
@@ -366,11 +407,14 @@ def index_bits(params: Params, T_total: int) -> int:
     return params.idx_bits if params.idx_bits else ceil_log2(T_total)
 
 
-def record_bytes(params: Params, T_total: int, scale_bits: int = SCALE_BITS_FP16) -> int:
+def record_bytes(params: Params, T_total: int, scale_bits: Optional[int] = None) -> int:
     """L_rec = ceil((index bits + ceil(log2 S) + scale bits + P*b) / 8)   (Eq. (5)).
 
-    The payload is ceil(log2 S) + b_e + P*b bits with b_e the scale width
-    (16 for the fp16 scale used here; Eq. (5) writes it as an exponent width)."""
+    The payload is ceil(log2 S) + b_e + P*b bits with b_e the scale width: 8
+    for the power-of-two exponent, 16 for the fp16 scale (the parameters'
+    format unless given)."""
+    if scale_bits is None:
+        scale_bits = params.scale_bits
     bits = index_bits(params, T_total) + seed_bits(params.S) + params.P * params.b + scale_bits
     return (bits + 7) // 8
 
@@ -399,11 +443,12 @@ def scope_bpw(n_bytes: int, n_weights: int) -> float:
 # Records and stream (REC-v1 / STREAM-v1)
 # --------------------------------------------------------------------------
 def pack_record(idx: int, seed: int, codes: Sequence[int], scale16: int,
-                idx_bits: int, s_bits: int, b: int, L_rec: int) -> bytes:
+                idx_bits: int, s_bits: int, b: int, L_rec: int, scale_bits: int = SCALE_BITS_FP16) -> bytes:
     """REC-v1: one little-endian, LSB-first bit stream holding the tile index
     (idx_bits), seed selector (ceil(log2 S) bits), P two's-complement b-bit
-    coefficients and the 16-bit fp16 scale, zero-padded to L_rec bytes (the
-    fields of Sec. 3.2 in the widths of Eq. (5))."""
+    coefficients and the scale field (16-bit fp16, or the 8-bit biased
+    exponent), zero-padded to L_rec bytes (the fields of Sec. 3.2 in the
+    widths of Eq. (5))."""
     v, pos = 0, 0
     assert 0 <= idx < (1 << idx_bits), "tile index does not fit its field"
     assert 0 <= seed < (1 << s_bits), "seed does not fit its field"
@@ -414,13 +459,14 @@ def pack_record(idx: int, seed: int, codes: Sequence[int], scale16: int,
     for c in codes:
         v |= (int(c) & ((1 << b) - 1)) << pos
         pos += b
-    v |= (int(scale16) & 0xFFFF) << pos
-    pos += SCALE_BITS_FP16
+    assert 0 <= int(scale16) < (1 << scale_bits), "scale does not fit its field"
+    v |= int(scale16) << pos
+    pos += scale_bits
     assert pos <= 8 * L_rec
     return v.to_bytes(L_rec, "little")
 
 
-def unpack_record(rec: bytes, idx_bits: int, s_bits: int, P: int, b: int):
+def unpack_record(rec: bytes, idx_bits: int, s_bits: int, P: int, b: int, scale_bits: int = SCALE_BITS_FP16):
     v = int.from_bytes(rec, "little")
     idx = v & ((1 << idx_bits) - 1)
     v >>= idx_bits
@@ -433,7 +479,7 @@ def unpack_record(rec: bytes, idx_bits: int, s_bits: int, P: int, b: int):
             c -= 1 << b
         codes.append(c)
         v >>= b
-    scale16 = v & 0xFFFF
+    scale16 = v & ((1 << scale_bits) - 1)
     return idx, seed, codes, scale16
 
 
@@ -441,16 +487,16 @@ def stream_header(params: Params, modules: Sequence[Tuple[int, int]], per_module
     """STREAM-v1 header: 40 fixed bytes then (rows u32, cols u32) per module.
 
     magic 'AWSR' | version u16 | flags u16 (bits 0-3 generator version,
-    bits 4-7 scale format (0 = fp16), bit 8 per-module quotas) | C u16 | P u8 |
+    bits 4-7 scale format (0 = fp16, 1 = pow2), bit 8 per-module quotas) | C u16 | P u8 |
     b u8 | S u32 | index bits u8 | seed bits u8 | scale bits u8 | L_rec u8 |
     basis key u64 | T_total u64 | n_modules u32, all little-endian.
     """
     T_total = sum(r * c // params.C for r, c in modules)
     L = record_bytes(params, T_total)
-    flags = (params.gen_version & 0xF) | ((1 if per_module else 0) << 8)
+    flags = (params.gen_version & 0xF) | ((params.scale_fmt & 0xF) << 4) | ((1 if per_module else 0) << 8)
     head = struct.pack("<4sHHHBBIBBBBQQI", MAGIC, STREAM_VERSION, flags, params.C, params.P,
                        params.b, params.S, index_bits(params, T_total), seed_bits(params.S),
-                       SCALE_BITS_FP16, L, params.basis_key & MASK64, T_total, len(modules))
+                       params.scale_bits, L, params.basis_key & MASK64, T_total, len(modules))
     assert len(head) == HEADER_FIXED_BYTES
     return head + b"".join(struct.pack("<II", r, c) for r, c in modules)
 
@@ -462,9 +508,9 @@ def parse_header(stream: bytes):
         raise ValueError("not an AWSRC stream")
     mods = [struct.unpack_from("<II", stream, HEADER_FIXED_BYTES + 8 * i) for i in range(n_mod)]
     h = header_bytes(n_mod)
-    return {"flags": flags, "C": C, "P": P, "b": b, "S": S, "idx_bits": ib, "seed_bits": sb,
-            "scale_bits": scb, "L_rec": L, "basis_key": key, "T_total": T_total,
-            "modules": mods, "h": h}
+    return {"flags": flags, "scale_fmt": (flags >> 4) & 0xF, "C": C, "P": P, "b": b, "S": S,
+            "idx_bits": ib, "seed_bits": sb, "scale_bits": scb, "L_rec": L, "basis_key": key,
+            "T_total": T_total, "modules": mods, "h": h}
 
 
 def rank_order(gain: np.ndarray, tile_ids: np.ndarray) -> np.ndarray:
@@ -512,7 +558,7 @@ def build_stream(params: Params, modules: Sequence[Tuple[int, int]], enc: Dict[s
         chosen = np.concatenate(chosen_parts) if chosen_parts else np.zeros(0, np.int64)
         K = len(chosen)
     body = b"".join(pack_record(int(t), int(enc["seed"][t]), enc["codes"][t], int(enc["scale"][t]),
-                                ib, sbits, params.b, L) for t in chosen)
+                                ib, sbits, params.b, L, params.scale_bits) for t in chosen)
     return stream_header(params, modules, per_module) + body, K, n_elig
 
 
@@ -536,14 +582,17 @@ def decode_add(stream: bytes, W0_list: Sequence[np.ndarray]) -> List[np.ndarray]
     cache: Dict[int, np.ndarray] = {}
     for k in range((len(stream) - h) // L):
         rec = stream[h + k * L: h + (k + 1) * L]
-        t, s, codes, s16 = unpack_record(rec, hd["idx_bits"], hd["seed_bits"], P, b)
+        t, s, codes, s16 = unpack_record(rec, hd["idx_bits"], hd["seed_bits"], P, b, hd["scale_bits"])
         mi = int(np.searchsorted(offsets, t, side="right") - 1)
         r_, c_ = hd["modules"][mi]
         local = t - offsets[mi]
         row, blk = divmod(int(local), c_ // C)
         if s not in cache:
             cache[s] = basis_matrix(hd["basis_key"], s, C, P)
-        sc = float(np.array([s16], dtype=np.uint16).view(np.float16)[0])
+        if hd["scale_fmt"] == SCALE_POW2:
+            sc = math.ldexp(1.0, int(s16) - POW2_BIAS)
+        else:
+            sc = float(np.array([s16], dtype=np.uint16).view(np.float16)[0])
         out[mi][row, blk * C:(blk + 1) * C] += cache[s] @ (sc * np.asarray(codes, dtype=np.float64))
     return out
 

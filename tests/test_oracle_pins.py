@@ -526,3 +526,82 @@ def test_encode_deterministic():
     b = _encode_module(W, d, p)[1]
     for k in ("seed", "codes", "scale", "gain"):
         assert np.array_equal(a[k], b[k])
+
+
+# ---------------------------------------------------------------- power-of-two scale
+def test_pow2_scale_hand_values():
+    # m = 3, qmax = 7: 7 * 2^-1 = 3.5 >= 3 > 7 * 2^-2 -> e = -1, q = rint(alpha / 0.5)
+    q, f, sc = O.quantize(np.array([[3.0, -1.0, 0.2, 0.0]]), 4, O.SCALE_POW2)
+    assert list(q[0]) == [6, -2, 0, 0] and int(f[0]) == 127 and sc[0] == 0.5
+    # m exactly on qmax * 2^e keeps that e (no clipping needed): 3.5 = 7 * 2^-1
+    q, f, sc = O.quantize(np.array([[3.5, 1.25]]), 4, O.SCALE_POW2)
+    assert list(q[0]) == [7, 2] and int(f[0]) == 127
+    # b = 3 (qmax 3): m = 10 -> 3 * 4 = 12 >= 10 > 6 -> e = 2
+    q, f, sc = O.quantize(np.array([[10.0, -5.0]]), 3, O.SCALE_POW2)
+    assert list(q[0]) == [2, -1] and int(f[0]) == 130 and sc[0] == 4.0
+    # zero tile: all-zero record, field 0
+    q, f, sc = O.quantize(np.zeros((1, 3)), 4, O.SCALE_POW2)
+    assert not q.any() and int(f[0]) == 0 and sc[0] == 0.0
+
+
+def test_pow2_scale_properties():
+    rng = np.random.default_rng(3)
+    for b in (2, 3, 4, 8):
+        qmax = (1 << (b - 1)) - 1
+        alpha = rng.standard_normal((400, 8)) * np.exp(rng.uniform(-20, 20, (400, 1)))
+        q, f, sc = O.quantize(alpha, b, O.SCALE_POW2)
+        m = np.abs(alpha).max(axis=1)
+        e = f.astype(np.int64) - O.POW2_BIAS
+        assert np.all(sc == np.ldexp(1.0, e))
+        assert np.all(m <= qmax * sc) and np.all(m > qmax * sc / 2)   # smallest such e
+        assert np.all(np.abs(alpha / sc[:, None]) <= qmax)             # nothing clips
+        assert np.all(np.abs(q) <= qmax)
+        assert np.all(np.abs(q).max(axis=1) >= (qmax + 1) // 2)
+        assert np.array_equal(q, np.rint(alpha / sc[:, None]))
+
+
+def test_pow2_paper_operating_point_record_and_stream():
+    # AWSRC-P_F: (C, P, b, S) = (16, 4, 4, 16), ceil(log2 T) index, 8-bit exponent -> 7 bytes (Sec. 4)
+    g = read_golden("paper_accounting.txt")
+    N, K = int(g["n_scope"][0]), int(g["K"][0])
+    p = O.Params(C=16, P=4, b=4, S=16, idx_bits=0, scale_fmt=O.SCALE_POW2)
+    T = N // 16
+    L = O.record_bytes(p, T)
+    assert L == int(g["record_bytes"][0]) == 7
+    assert O.header_bytes(108) + L * K == int(g["sidecar_bytes"][0])
+    # a small stream in the same format: header fields and record size
+    mods = [(4, 64)]
+    rng = np.random.default_rng(1)
+    T4 = 16
+    enc = {"seed": rng.integers(0, 16, T4), "codes": rng.integers(-7, 8, (T4, 4)),
+           "scale": rng.integers(0, 256, T4), "gain": rng.standard_normal(T4)}
+    stream, K4, ne = O.build_stream(p, mods, enc, 64.0, per_module=False)
+    hd = O.parse_header(stream)
+    assert hd["scale_fmt"] == O.SCALE_POW2 and hd["scale_bits"] == 8 and hd["idx_bits"] == 4
+    assert hd["L_rec"] == (4 + 4 + 16 + 8 + 7) // 8 == 4
+    assert len(stream) == hd["h"] + K4 * 4 and K4 == ne == int(np.sum(enc["gain"] > 0))
+
+
+def test_pow2_record_worked_example():
+    g = read_golden("rec_v1_pow2_example.txt")
+    codes = [int(c) for c in g["codes"]]
+    rec = O.pack_record(int(g["idx"][0]), int(g["seed"][0]), codes, int(g["field"][0]), 28, 4, 4, 7,
+                        scale_bits=O.SCALE_BITS_POW2)
+    assert rec == bytes(int(x, 16) for x in g["bytes"])
+    assert O.unpack_record(rec, 28, 4, 4, 4, O.SCALE_BITS_POW2) == (5, 9, codes, 125)
+
+
+def test_pow2_decode_exact_power_of_two_scaling():
+    # one record: r_hat = B_s (2^e q); orthonormal columns give |r_hat|^2 = 4^e |q|^2,
+    # and every other tile of W0 is returned unchanged
+    p = O.Params(C=16, P=4, b=4, S=16, idx_bits=0, scale_fmt=O.SCALE_POW2)
+    mods = [(2, 32)]
+    enc = {"seed": np.array([3, 0, 0, 0]), "codes": np.array([[7, -3, 0, 1]] + [[0] * 4] * 3),
+           "scale": np.array([128 - 5, 0, 0, 0]), "gain": np.array([1.0, -1.0, -1.0, -1.0])}
+    stream, K, _ = O.build_stream(p, mods, enc, 64.0, per_module=False)
+    assert K == 1
+    W0 = np.arange(64, dtype=np.float64).reshape(2, 32) / 7.0
+    out = O.decode_add(stream, [W0])[0]
+    rhat = out[0, :16] - W0[0, :16]
+    assert math.isclose(float(rhat @ rhat), 4.0 ** -5 * (49 + 9 + 0 + 1), rel_tol=1e-12)
+    assert np.array_equal(out[0, 16:], W0[0, 16:]) and np.array_equal(out[1], W0[1])
