@@ -60,7 +60,7 @@ enum {
 enum { AWSRC_DTYPE_F32 = 0, AWSRC_DTYPE_BF16 = 1 };
 enum { AWSRC_D_PER_COL = 0, AWSRC_D_PER_ELEM = 1 };
 enum { AWSRC_MODE_GLOBAL = 0, AWSRC_MODE_PER_MODULE = 1 };
-enum { AWSRC_SCALE_FP16 = 0 };
+enum { AWSRC_SCALE_FP16 = 0, AWSRC_SCALE_POW2 = 1 };
 
 /*
  * Codec parameters (the (C, P, b, S) of Sec. 3.1 plus generator and ridge).
@@ -68,9 +68,18 @@ enum { AWSRC_SCALE_FP16 = 0 };
  *  P            basis columns per seed: 1..min(C, 16).
  *  b            coefficient bits: 2..8; codes lie in [-(2^(b-1)-1), 2^(b-1)-1].
  *  S            number of seeds: 2..65536.
- *  scale_fmt    AWSRC_SCALE_FP16: one fp16 scale per tile,
- *               scale = f16(f32(max_p |alpha*_p| / qmax)), both roundings to
- *               nearest even, saturating at 65504.
+ *  scale_fmt    one scale per tile (Sec. 3.2), stored in a field of
+ *               scale_bits bits:
+ *               AWSRC_SCALE_FP16: scale = f16(f32(max_p |alpha*_p| / qmax)),
+ *               both roundings to nearest even, saturating at 65504; the
+ *               field holds the 16 fp16 bits.
+ *               AWSRC_SCALE_POW2: the power-of-two scale of Sec. 3.2,
+ *               scale = 2^e with e the smallest integer such that
+ *               max_p |alpha*_p| <= qmax 2^e (no code clips), clamped to
+ *               [-128, 127]; the field holds e + 128 in 8 bits (b_e = 8 in
+ *               Eq. (5)).
+ *               Either way an all-zero alpha* gives an all-zero record (field
+ *               0) with gain 0.
  *  idx_bits     width of the tile-index field: 1..32, or 0 for
  *               ceil(log2 T_total) as in Eq. (5).
  *  gen_version  1: B_s = diag(sigma_s) H_C[:, c_s] / sqrt(C) with H_C the
@@ -130,7 +139,8 @@ awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, in
  *  d        AWSRC_D_PER_COL: [cols] activation second moments shared by all
  *           rows; AWSRC_D_PER_ELEM: [rows, cols] per-element weights.  d > 0.
  *  cols % C == 0.  T = rows * cols / C.  W, W0 and d are 16-byte aligned.
- *  seed_out [T] u16, code_out [T, P] i8, scale_out [T] fp16 bits,
+ *  seed_out [T] u16, code_out [T, P] i8, scale_out [T] the scale field
+ *  (fp16 bits or biased exponent, by scale_fmt),
  *  gain_out [T] f64 (weighted error reduction of the stored record; an
  *  all-zero record has gain 0), alpha_or_null [T, P] fp32 unquantized fit of
  *  the chosen seed, or NULL.
@@ -161,9 +171,10 @@ awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_
  *   scale_fmt, bit 8 per-module mode) | C u16 | P u8 | b u8 | S u32 |
  *   idx_bits u8 | seed_bits u8 | scale_bits u8 | L_rec u8 | basis_key u64 |
  *   T_total u64 | n_modules u32 | then rows u32, cols u32 per module,
- * followed by K records of L_rec = ceil((idx_bits + ceil(log2 S) + P*b + 16)/8)
- * bytes: one LSB-first bit stream of tile index, seed, P two's-complement
- * b-bit codes and the fp16 scale bits, zero padded.
+ * followed by K records of L_rec = ceil((idx_bits + ceil(log2 S) + P*b +
+ * scale_bits)/8) bytes (scale_bits = 16 for fp16 scales, 8 for power-of-two
+ * exponents): one LSB-first bit stream of tile index, seed, P
+ * two's-complement b-bit codes and the scale field, zero padded.
  *  module_rows, module_cols  host arrays [n_modules]; cols % C == 0.
  *  stream_out     device buffer of stream_cap bytes; stream_cap < h + K*L_rec
  *                 gives AWSRC_ENOSPC.
@@ -193,7 +204,7 @@ awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modules,
  *  rows, cols    host arrays [n_modules]; must match the stream header.
  * The header and every record are validated before anything is written (magic,
  * version, parameters, length on a record boundary, tile index < T_total,
- * seed < S, codes within +-qmax, finite non-negative scale, no tile twice); a
+ * seed < S, codes within +-qmax, finite non-negative fp16 scale, no tile twice); a
  * failure returns AWSRC_ECORRUPT and leaves W0 unchanged.  This call
  * synchronizes with `stream` (to read the header and the validation result).
  */
@@ -205,7 +216,7 @@ awsrc_status awsrc_decode_add(const uint8_t* stream_bytes, uint64_t stream_len, 
 typedef struct awsrc_decode_plan {
   int32_t C, P, b, S;
   int32_t idx_bits, seed_bits, L_rec, n_modules;
-  int32_t w0_dtype, reserved;
+  int32_t w0_dtype, scale_fmt;
   int64_t K;
   uint64_t T_total;
   uint64_t h;

@@ -22,7 +22,7 @@ AWSRC_OK, AWSRC_EINVAL, AWSRC_ENOSPC, AWSRC_ECORRUPT, AWSRC_EDEVICE = 0, -1, -2,
 AWSRC_DTYPE_F32, AWSRC_DTYPE_BF16 = 0, 1
 AWSRC_D_PER_COL, AWSRC_D_PER_ELEM = 0, 1
 AWSRC_MODE_GLOBAL, AWSRC_MODE_PER_MODULE = 0, 1
-AWSRC_SCALE_FP16 = 0
+AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_encode_tiles",
             "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
@@ -44,14 +44,14 @@ class awsrc_params(ctypes.Structure):
 class awsrc_decode_plan(ctypes.Structure):
     _fields_ = [("C", ctypes.c_int32), ("P", ctypes.c_int32), ("b", ctypes.c_int32), ("S", ctypes.c_int32),
                 ("idx_bits", ctypes.c_int32), ("seed_bits", ctypes.c_int32), ("L_rec", ctypes.c_int32),
-                ("n_modules", ctypes.c_int32), ("w0_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("n_modules", ctypes.c_int32), ("w0_dtype", ctypes.c_int32), ("scale_fmt", ctypes.c_int32),
                 ("K", ctypes.c_int64), ("T_total", ctypes.c_uint64), ("h", ctypes.c_uint64),
                 ("records", ctypes.c_void_p), ("workspace", ctypes.c_void_p)]
 
 
 def make_params(C: int, P: int, b: int, S: int, basis_key: int = 0, ridge_lambda: float = 1e-6,
-                idx_bits: int = 32) -> awsrc_params:
-    return awsrc_params(C, P, b, S, AWSRC_SCALE_FP16, idx_bits, 1, 0, basis_key, ridge_lambda)
+                idx_bits: int = 32, scale_fmt: int = AWSRC_SCALE_FP16) -> awsrc_params:
+    return awsrc_params(C, P, b, S, scale_fmt, idx_bits, 1, 0, basis_key, ridge_lambda)
 
 
 def _load() -> ctypes.CDLL:

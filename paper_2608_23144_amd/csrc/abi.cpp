@@ -47,7 +47,8 @@ awsrc_status check_params(const awsrc_params* p) {
   if (p->P < 1 || p->P > kMaxP || p->P > p->C) return fail(AWSRC_EINVAL, "P=%d out of range 1..min(C,16)", p->P);
   if (p->b < 2 || p->b > 8) return fail(AWSRC_EINVAL, "b=%d out of range 2..8", p->b);
   if (p->S < 2 || p->S > 65536) return fail(AWSRC_EINVAL, "S=%d out of range 2..65536", p->S);
-  if (p->scale_fmt != AWSRC_SCALE_FP16) return fail(AWSRC_EINVAL, "scale_fmt=%d unsupported", p->scale_fmt);
+  if (p->scale_fmt != AWSRC_SCALE_FP16 && p->scale_fmt != AWSRC_SCALE_POW2)
+    return fail(AWSRC_EINVAL, "scale_fmt=%d unsupported", p->scale_fmt);
   if (p->idx_bits < 0 || p->idx_bits > 32) return fail(AWSRC_EINVAL, "idx_bits=%d out of range 0..32", p->idx_bits);
   if (p->gen_version != 1) return fail(AWSRC_EINVAL, "gen_version=%d unsupported", p->gen_version);
   if (p->reserved != 0) return fail(AWSRC_EINVAL, "reserved field must be 0");
@@ -59,8 +60,10 @@ int index_bits(const awsrc_params* p, uint64_t T_total) {
   return p->idx_bits ? p->idx_bits : ceil_log2_u64(T_total);
 }
 
-int64_t rec_bytes(int ib, int S, int P, int b) {
-  return (ib + ceil_log2_u64((uint64_t)S) + P * b + 16 + 7) / 8;
+int scale_field_bits(int scale_fmt) { return scale_fmt == AWSRC_SCALE_POW2 ? 8 : 16; }
+
+int64_t rec_bytes(int ib, int S, int P, int b, int scale_bits) {
+  return (ib + ceil_log2_u64((uint64_t)S) + P * b + scale_bits + 7) / 8;
 }
 
 void put_le(std::vector<uint8_t>& v, uint64_t x, int n) {
@@ -81,7 +84,7 @@ extern "C" const char* awsrc_last_error(void) { return g_err.c_str(); }
 
 extern "C" int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total) {
   if (check_params(p) != AWSRC_OK || T_total < 1) return -1;
-  return rec_bytes(index_bits(p, (uint64_t)T_total), p->S, p->P, p->b);
+  return rec_bytes(index_bits(p, (uint64_t)T_total), p->S, p->P, p->b, scale_field_bits(p->scale_fmt));
 }
 
 extern "C" int64_t awsrc_header_bytes(int32_t n_modules) {
@@ -154,6 +157,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.W = W; a.w_dtype = w_dtype; a.W0 = W0; a.d = d; a.d_mode = d_mode;
   a.rows = rows; a.cols = cols; a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
   a.lambda = p->ridge_lambda;
+  a.scale_fmt = p->scale_fmt;
   a.basis = carve_basis(ws, p->S, p->P);
   ws += b_basis;
   a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
@@ -204,7 +208,8 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
   const int ib = index_bits(p, (uint64_t)T_total);
   if (ib < 32 && (uint64_t)T_total > (1ull << ib)) return fail(AWSRC_EINVAL, "idx_bits=%d cannot address %lld tiles", ib, (long long)T_total);
   const int sb = ceil_log2_u64((uint64_t)p->S);
-  const int64_t L = rec_bytes(ib, p->S, p->P, p->b);
+  const int scb = scale_field_bits(p->scale_fmt);
+  const int64_t L = rec_bytes(ib, p->S, p->P, p->b, scb);
   if (L > 255) return fail(AWSRC_EINVAL, "record too large");
   const int64_t h = kHeaderFixed + 8 * (int64_t)n_modules;
 
@@ -242,7 +247,7 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
   HIPCHK(launch_rank_init(rw, s));
   for (size_t i = 0; i < seg_n.size(); ++i) {
     const int64_t cap = seg_cap[i] < seg_n[i] ? seg_cap[i] : seg_n[i];
-    HIPCHK(launch_rank_segment(gain, seg_t0[i], seg_n[i], cap, rw, seed, code, scale, p->P, p->b, ib, sb, (int)L,
+    HIPCHK(launch_rank_segment(gain, seg_t0[i], seg_n[i], cap, rw, seed, code, scale, p->P, p->b, ib, sb, scb, (int)L,
                                (uint64_t)h, stream_cap, stream_out, s));
   }
   // header: fixed fields, then the module table
@@ -258,7 +263,7 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
   put_le(hdr, (uint64_t)p->S, 4);
   put_le(hdr, (uint64_t)ib, 1);
   put_le(hdr, (uint64_t)sb, 1);
-  put_le(hdr, 16, 1);
+  put_le(hdr, (uint64_t)scb, 1);
   put_le(hdr, (uint64_t)L, 1);
   put_le(hdr, p->basis_key, 8);
   put_le(hdr, (uint64_t)T_total, 8);
@@ -311,6 +316,7 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   a.T_total = pl->T_total;
   a.n_modules = pl->n_modules;
   a.w0_dtype = pl->w0_dtype;
+  a.scale_fmt = pl->scale_fmt;
   a.basis = carve_basis(ws, pl->S, pl->P);
   ws += l.basis;
   a.bitmap = reinterpret_cast<uint32_t*>(ws); ws += l.bitmap;
@@ -351,12 +357,14 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   const uint64_t key = get_le(fx + 20, 8);
   const uint64_t T_total = get_le(fx + 28, 8);
   const uint32_t nmod = (uint32_t)get_le(fx + 36, 4);
-  if ((flags & 0xF) != 1 || ((flags >> 4) & 0xF) != AWSRC_SCALE_FP16 || (flags & ~0x1FFu)) return fail(AWSRC_ECORRUPT, "bad flags 0x%x", flags);
+  const int sfmt = (int)((flags >> 4) & 0xF);
+  if ((flags & 0xF) != 1 || (sfmt != AWSRC_SCALE_FP16 && sfmt != AWSRC_SCALE_POW2) || (flags & ~0x1FFu))
+    return fail(AWSRC_ECORRUPT, "bad flags 0x%x", flags);
   if (!pow2_c(C) || P < 1 || P > kMaxP || P > C || b < 2 || b > 8 || S < 2 || S > 65536)
     return fail(AWSRC_ECORRUPT, "bad codec parameters in header");
-  if (sb != ceil_log2_u64((uint64_t)S) || scb != 16 || ib > 32 || (ib == 0 && T_total > 1))
+  if (sb != ceil_log2_u64((uint64_t)S) || scb != scale_field_bits(sfmt) || ib > 32 || (ib == 0 && T_total > 1))
     return fail(AWSRC_ECORRUPT, "bad field widths in header");
-  if (L != rec_bytes(ib, (int)S, P, b)) return fail(AWSRC_ECORRUPT, "record size %d inconsistent with header", L);
+  if (L != rec_bytes(ib, (int)S, P, b, scb)) return fail(AWSRC_ECORRUPT, "record size %d inconsistent with header", L);
   if ((int32_t)nmod != n_modules) return fail(AWSRC_ECORRUPT, "header has %u modules, caller %d", nmod, n_modules);
   const uint64_t h = kHeaderFixed + 8ull * nmod;
   if ((stream_len - h) % (uint64_t)L) return fail(AWSRC_ECORRUPT, "stream does not end on a record boundary");
@@ -391,6 +399,7 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   pl.C = C; pl.P = P; pl.b = b; pl.S = (int32_t)S;
   pl.idx_bits = ib; pl.seed_bits = sb; pl.L_rec = L; pl.n_modules = (int32_t)nmod;
   pl.w0_dtype = w0_dtype;
+  pl.scale_fmt = sfmt;
   pl.K = K; pl.T_total = T_total; pl.h = h;
   pl.records = stream_bytes + h;
   pl.workspace = workspace;

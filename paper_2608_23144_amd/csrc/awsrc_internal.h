@@ -68,16 +68,37 @@ inline int colfac_stride(int P) {
 
 __host__ __device__ __forceinline__ int ltri(int p, int k) { return p * (p - 1) / 2 + k; }
 
+// Screen-precision scale of max |alpha| = m: fp16 f16(m / qmax) with
+// saturation, or the power of two 2^e, e = ceil(log2(m / qmax)), from the
+// exponent and mantissa bits of the fp32 quotient.  Returns the scale and
+// sets *isc to its reciprocal (0 when the scale is 0).
+__device__ __forceinline__ float screen_scale(float m, float inv_qmax, bool pow2, float* isc) {
+  const float x = m * inv_qmax;
+  if (pow2) {
+    const uint32_t xb = __float_as_uint(x);
+    int e = (int)((xb >> 23) & 0xFFu) - 127 + ((xb & 0x7FFFFFu) ? 1 : 0);
+    e = e < -126 ? -126 : (e > 127 ? 127 : e);
+    *isc = x > 0.0f ? __uint_as_float((uint32_t)(127 - e) << 23) : 0.0f;
+    return x > 0.0f ? __uint_as_float((uint32_t)(127 + e) << 23) : 0.0f;
+  }
+  uint16_t hb = __half_as_ushort(__float2half_rn(x));
+  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;  // saturate at 65504
+  const float sc = __half2float(__ushort_as_half(hb));
+  *isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+  return sc;
+}
+
 // Screen score of one (tile, seed) from the per-column factor f (a table
-// entry as above, read through any pointer type): solves (G) alpha = b with
-// the LDL^T factor, quantizes alpha with one fp16 scale
-// (scale = f16(max |alpha| / qmax), q = clamp(rint(alpha / scale))), and
+// entry as above, read through any pointer type): solves G alpha = b with
+// the LDL^T factor, quantizes alpha with one scale (screen_scale; pow2
+// selects the power-of-two format), q = clamp(rint(alpha / scale)), and
 // returns scale (2 q.b - scale q^T G q).  That is the exact gain
 // 2 a.b - a^T G0 a of the quantized fit minus scale^2 eps |q|^2 (relative
 // size ~ lambda), which the fp64 re-score of the kept seeds removes.  Uses
 // q.b = (L^T q).w with w = L^-1 b, and q^T G q = sum_k e_k (L^T q)_k^2.
 template <int PB, typename FP>
-__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
+__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax,
+                                                 bool pow2) {
   constexpr int LS = PB * (PB - 1) / 2;
   float w[PB], al[PB];
 #pragma unroll
@@ -97,10 +118,8 @@ __device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP
   float m = 0.0f;
 #pragma unroll
   for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
-  uint16_t hb = __half_as_ushort(__float2half_rn(m * inv_qmax));
-  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;  // saturate at 65504
-  const float sc = __half2float(__ushort_as_half(hb));
-  const float isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+  float isc;
+  const float sc = screen_scale(m, inv_qmax, pow2, &isc);
   float q[PB];
 #pragma unroll
   for (int p = 0; p < PB; ++p) q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
@@ -133,6 +152,7 @@ struct EncodeArgs {
   int64_t rows, cols;
   int C, P, b, S;
   double lambda;
+  int scale_fmt;       // AWSRC_SCALE_FP16 or AWSRC_SCALE_POW2
   BasisTables basis;
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
   double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
@@ -185,8 +205,8 @@ hipError_t launch_rank_init(const RankWs& ws, hipStream_t st);
 // slot of the stream; no host synchronization.
 hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_t cap, const RankWs& ws,
                                const uint16_t* seed, const int8_t* code, const uint16_t* scale, int P, int b,
-                               int idx_bits, int seed_bits, int L, uint64_t h, uint64_t stream_cap,
-                               uint8_t* stream_out, hipStream_t st);
+                               int idx_bits, int seed_bits, int scale_bits, int L, uint64_t h,
+                               uint64_t stream_cap, uint8_t* stream_out, hipStream_t st);
 // Device words after all segments: [0] records, [1] eligible tiles, [2] no-space flag.
 const uint64_t* rank_totals(const RankWs& ws);
 
@@ -202,6 +222,7 @@ struct DecodeArgs {
   const int64_t* mod_cols;       // [n_modules]
   void* const* mod_ptr;          // [n_modules] device pointers
   int w0_dtype;
+  int scale_fmt;                 // AWSRC_SCALE_FP16 or AWSRC_SCALE_POW2
   BasisTables basis;
   uint32_t* bitmap;              // [ceil(T_total / 32)]
   unsigned long long* errors;    // [1]

@@ -76,7 +76,7 @@ __device__ __forceinline__ Rec parse(const DecodeArgs& a, int64_t i) {
     if (c >> (a.b - 1)) c -= (int64_t)1 << a.b;
     out.q[p] = (int32_t)c;
   }
-  out.scale = (uint32_t)get_bits(w, pos, 16);
+  out.scale = (uint32_t)get_bits(w, pos, a.scale_fmt == AWSRC_SCALE_POW2 ? 8 : 16);
   return out;
 }
 
@@ -93,7 +93,8 @@ __global__ void k_decode_validate(DecodeArgs a) {
   const int qmax = (1 << (a.b - 1)) - 1;
   bool bad = r.idx >= a.T_total || r.seed >= (uint32_t)a.S;
   for (int p = 0; p < a.P; ++p) bad |= r.q[p] < -qmax || r.q[p] > qmax;
-  bad |= (r.scale & 0x8000u) != 0 || (r.scale & 0x7C00u) == 0x7C00u;  // negative, inf or NaN
+  // fp16 scale: negative, inf or NaN; every 8-bit exponent is valid
+  if (a.scale_fmt != AWSRC_SCALE_POW2) bad |= (r.scale & 0x8000u) != 0 || (r.scale & 0x7C00u) == 0x7C00u;
   if (!bad) {
     const uint32_t bit = 1u << (r.idx & 31);
     const uint32_t old = atomicOr(&a.bitmap[r.idx >> 5], bit);
@@ -143,7 +144,9 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
     // signs of rows 8*sub .. 8*sub+7 of B_s, one u16 of P bits per row
     const uint4 tsv = *reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC + sub * 8);
     const uint32_t tw[4] = {tsv.x, tsv.y, tsv.z, tsv.w};
-    const float scl = __half2float(__ushort_as_half((uint16_t)(e0.z >> 16))) * isq;
+    const uint32_t sfield = e0.z >> 16;
+    const float scl = a.scale_fmt == AWSRC_SCALE_POW2 ? ldexpf(isq, (int)sfield - 128)
+                                                      : __half2float(__ushort_as_half((uint16_t)sfield)) * isq;
     const int32_t tot = (int32_t)e0.w;
     float add[8];
 #pragma unroll

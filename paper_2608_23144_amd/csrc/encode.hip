@@ -159,6 +159,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
   if constexpr (PE) fwht<C>(wd);
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
+  const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   const float invC = 1.0f / C;
   float tg[kTop];
   int ts[kTop];
@@ -227,10 +228,10 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
       float m = 0.0f;
 #pragma unroll
       for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
-      const float sc = __half2float(__ushort_as_half(scale_bits_from_f32(m * inv_qmax)));
+      float isc;
+      const float sc = screen_scale(m, inv_qmax, pow2, &isc);
       g = 0.0f;
       if (sc > 0.0f) {
-        const float isc = 1.0f / sc;
         float q[PB], t1 = 0.0f, qq = 0.0f;
 #pragma unroll
         for (int p = 0; p < PB; ++p) {
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
         g = sc * (2.0f * t1 - sc * quad);
       }
     } else {
-      g = screen_score_ldl<PB>(bv, a.colfac + ((size_t)blk * a.S + s) * stride, qmax, inv_qmax);
+      g = screen_score_ldl<PB>(bv, a.colfac + ((size_t)blk * a.S + s) * stride, qmax, inv_qmax, pow2);
     }
     // keep the best kTop, earlier (lower) seeds first among equals
     float cg = g;
@@ -469,16 +470,27 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
       for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
       al[p] = acc * inv[p];
     }
-    // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
     double m = 0.0;
 #pragma unroll
     for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
     uint16_t bits = 0;
     double sc = 0.0;
     if (m > 0.0) {
-      bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
-      sc = (double)__half2float(__ushort_as_half(bits));
-      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
+      if (a.scale_fmt == AWSRC_SCALE_POW2) {
+        // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
+        int e;
+        frexp(m / (double)qmax, &e);
+        while (m > (double)qmax * ldexp(1.0, e)) ++e;
+        while (m <= (double)qmax * ldexp(1.0, e - 1)) --e;
+        e = e < -128 ? -128 : (e > 127 ? 127 : e);
+        bits = (uint16_t)(e + 128);
+        sc = ldexp(1.0, e);
+      } else {
+        // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
+        bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
+        sc = (double)__half2float(__ushort_as_half(bits));
+        if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
+      }
     }
     int q[PB];
     double ah[PB];

@@ -173,6 +173,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   }
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
+  const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   const float lam = (float)a.lambda;
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
@@ -285,19 +286,19 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
           f[LS + PB + p] = t;
           f[LS + p] = __builtin_amdgcn_rcpf(t);
         }
-        gsc = screen_score_ldl<PB>(bk[k], f, qmax, inv_qmax);
+        gsc = screen_score_ldl<PB>(bk[k], f, qmax, inv_qmax, pow2);
       } else {
         // uniform across the wavefront: scalar loads through the constant address space
         if (k == 0) {
           const cfp fb = fac_ptr(s + 1);
 #pragma unroll
           for (int i = 0; i < NF; ++i) fB[i] = fb[i];
-          gsc = screen_score_ldl<PB>(bk[0], fA, qmax, inv_qmax);
+          gsc = screen_score_ldl<PB>(bk[0], fA, qmax, inv_qmax, pow2);
         } else {
           const cfp fa = fac_ptr(s + 1);
 #pragma unroll
           for (int i = 0; i < NF; ++i) fA[i] = fa[i];
-          gsc = screen_score_ldl<PB>(bk[1], fB, qmax, inv_qmax);
+          gsc = screen_score_ldl<PB>(bk[1], fB, qmax, inv_qmax, pow2);
         }
       }
       gsc = s < a.S ? gsc : -INFINITY;
@@ -385,6 +386,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   const bool my_valid = my_row < a.rows;
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
+  const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   constexpr float isq = C == 64 ? 0.125f : 0.08838834764831845f;  // 1/sqrt(C)
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
@@ -447,7 +449,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     project(F, accN);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
-    float gsc = screen_score_ldl<PB>(bv, f, qmax, inv_qmax);
+    float gsc = screen_score_ldl<PB>(bv, f, qmax, inv_qmax, pow2);
     gsc = s < a.S ? gsc : -INFINITY;
     // this lane's seeds increase, so strict comparisons keep the lower seed among equals
     const bool c0 = gsc > tg0, c1 = gsc > tg1;

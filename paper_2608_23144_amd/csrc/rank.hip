@@ -491,7 +491,8 @@ __device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v,
 // no-space flag instead.
 __global__ void k_pack(const SortItem* __restrict__ sorted, uint64_t* state, const uint16_t* __restrict__ seed,
                        const int8_t* __restrict__ code, const uint16_t* __restrict__ scale, int P, int b,
-                       int idx_bits, int seed_bits, int L, uint64_t h, uint64_t cap, uint8_t* __restrict__ out) {
+                       int idx_bits, int seed_bits, int scale_bits, int L, uint64_t h, uint64_t cap,
+                       uint8_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const uint64_t K = state[kSegK], off = state[kSegOff];
   if (i >= (int64_t)K) return;
@@ -506,7 +507,7 @@ __global__ void k_pack(const SortItem* __restrict__ sorted, uint64_t* state, con
   put_bits(w, pos, (uint64_t)seed[t], seed_bits);
   const uint64_t cm = (1ull << b) - 1ull;
   for (int p = 0; p < P; ++p) put_bits(w, pos, (uint64_t)(int64_t)code[(int64_t)t * P + p] & cm, b);
-  put_bits(w, pos, (uint64_t)scale[t], 16);
+  put_bits(w, pos, (uint64_t)scale[t] & ((1ull << scale_bits) - 1ull), scale_bits);
   uint8_t* o = out + h + (off + (uint64_t)i) * (uint64_t)L;
   for (int k = 0; k < L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
 }
@@ -516,8 +517,8 @@ __global__ void k_pack(const SortItem* __restrict__ sorted, uint64_t* state, con
 // and kernels read the actual K from the state.
 hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_t cap, const RankWs& ws,
                                const uint16_t* seed, const int8_t* code, const uint16_t* scale, int P, int b,
-                               int idx_bits, int seed_bits, int L, uint64_t h, uint64_t stream_cap,
-                               uint8_t* stream_out, hipStream_t st) {
+                               int idx_bits, int seed_bits, int scale_bits, int L, uint64_t h,
+                               uint64_t stream_cap, uint8_t* stream_out, hipStream_t st) {
   const double* g = gain + t0;
   int64_t cb = (n + kThreads - 1) / kThreads;
   if (cb > 512) cb = 512;
@@ -554,7 +555,7 @@ hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_
     SortItem* t = in; in = out; out = t;
   }
   hipLaunchKernelGGL(k_pack, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, st, in, ws.state, seed, code,
-                     scale, P, b, idx_bits, seed_bits, L, h, stream_cap, stream_out);
+                     scale, P, b, idx_bits, seed_bits, scale_bits, L, h, stream_cap, stream_out);
   return hipGetLastError();
 }
 

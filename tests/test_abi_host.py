@@ -36,9 +36,17 @@ def test_abi_version():
                                           (128, 8, 3, 1024, 32, 3809280), (64, 8, 4, 512, 32, 43352064),
                                           (16, 4, 4, 16, 0, 152174592), (32, 16, 8, 65536, 0, 5),
                                           (16, 1, 2, 2, 0, 1)])
-def test_record_bytes_match_oracle(C, P, b, S, ib, T):
-    p = awsrc.make_params(C, P, b, S, idx_bits=ib)
-    assert awsrc.awsrc_record_bytes(p, T) == O.record_bytes(O.Params(C=C, P=P, b=b, S=S, idx_bits=ib), T)
+@pytest.mark.parametrize("fmt", [0, 1])
+def test_record_bytes_match_oracle(C, P, b, S, ib, T, fmt):
+    p = awsrc.make_params(C, P, b, S, idx_bits=ib, scale_fmt=fmt)
+    assert awsrc.awsrc_record_bytes(p, T) == O.record_bytes(
+        O.Params(C=C, P=P, b=b, S=S, idx_bits=ib, scale_fmt=fmt), T)
+
+
+def test_pow2_record_size_is_the_papers():
+    # AWSRC-P_F (16, 4, 4, 16), ceil(log2 T) index, 8-bit exponent: 7 bytes (Sec. 4)
+    p = awsrc.make_params(16, 4, 4, 16, idx_bits=0, scale_fmt=awsrc.AWSRC_SCALE_POW2)
+    assert awsrc.awsrc_record_bytes(p, 2434793472 // 16) == 7
 
 
 def test_header_budget_prefix_helpers():
@@ -55,7 +63,7 @@ def test_header_budget_prefix_helpers():
 
 
 @pytest.mark.parametrize("bad", [dict(C=48), dict(C=256), dict(P=0), dict(P=17), dict(b=1), dict(b=9),
-                                 dict(S=1), dict(S=65537), dict(idx_bits=33)])
+                                 dict(S=1), dict(S=65537), dict(idx_bits=33), dict(scale_fmt=2)])
 def test_invalid_params_rejected(bad):
     kw = dict(C=64, P=8, b=4, S=256, idx_bits=32)
     kw.update(bad)

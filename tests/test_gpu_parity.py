@@ -29,25 +29,25 @@ def _u16(t):
     return (t.to(torch.int32) & 0xFFFF).cpu().numpy()
 
 
-def _params(wl, **kw):
+def _params(wl, fmt=0, **kw):
     return awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                             idx_bits=wl.idx_bits, **kw)
+                             idx_bits=wl.idx_bits, scale_fmt=fmt, **kw)
 
 
-def _oparams(wl):
+def _oparams(wl, fmt=0):
     return O.Params(C=wl.C, P=wl.P, b=wl.b, S=wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                    idx_bits=wl.idx_bits)
+                    idx_bits=wl.idx_bits, scale_fmt=fmt)
 
 
-def _gpu_module(wl, m, want_alpha=True):
+def _gpu_module(wl, m, want_alpha=True, fmt=0):
     inp = gen_module_inputs(wl, m, DEV)
     codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(inp["W"])
-    enc = awsrc.awsrc_encode_tiles(_params(wl), inp["W"], W0, inp["d"], want_alpha=want_alpha)
+    enc = awsrc.awsrc_encode_tiles(_params(wl, fmt), inp["W"], W0, inp["d"], want_alpha=want_alpha)
     torch.cuda.synchronize()
     return inp, (codes, scale, zero, W0), enc
 
 
-def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx):
+def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx, fmt=0):
     """Oracle on a subset of tiles of one module, with every seed's gain kept."""
     W32 = inp["W32"].cpu().numpy()
     d = inp["d"].cpu().numpy()
@@ -55,7 +55,7 @@ def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx):
     assert np.array_equal(W0o, W0_gpu.cpu().numpy())
     R = O.tiles(O.residual(W32, W0o), wl.C)[tiles_idx]
     D = O.tile_weights(d, m.rows, m.cols, wl.C)[tiles_idx]
-    op = _oparams(wl)
+    op = _oparams(wl, fmt)
     orc = O.encode_tiles(R, D, op, keep_all=True)
     g_seed = _u16(enc["seed"])[tiles_idx]
     g_codes = enc["codes"].cpu().numpy()[tiles_idx]
@@ -143,6 +143,24 @@ def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
     T = rows * cols // C
     nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T))
     assert nd <= max(1, T // 50)
+
+
+@pytest.mark.parametrize("C,P,b,S,rows,cols,d_mode", [
+    (64, 8, 4, 32, 67, 512, "col"),     # matrix-core screen, per-column factors
+    (64, 8, 4, 32, 67, 512, "elem"),    # matrix-core screen, per-element factors
+    (128, 8, 3, 24, 40, 256, "col"),    # matrix-core C=128 screen
+    (16, 4, 4, 16, 9, 128, "col"),      # the paper's P_F operating point shape, vector screen
+    (32, 4, 4, 16, 3, 128, "elem"),     # vector screen, per-element weights
+])
+def test_encode_pow2_scale(C, P, b, S, rows, cols, d_mode):
+    """Power-of-two scale exponent (Sec. 3.2) in every screen and the re-score."""
+    wl = workload("block3b", C=C, P=P, b=b, S=S, d_mode=d_mode)
+    m = Module("t", rows, cols, 0, 3, 3)
+    inp, bb, enc = _gpu_module(wl, m, fmt=1)
+    T = rows * cols // C
+    nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T), fmt=1)
+    assert nd <= max(1, T // 50)
+    assert int(_u16(enc["scale"]).max()) < 256
 
 
 def test_encode_zero_residual_tiles():
@@ -403,6 +421,65 @@ def test_pipeline_linear256_matches_oracle():
     e1 = O.weighted_error(W32, What.cpu().numpy().astype(np.float64), d)
     kept = np.sort(orc["gain"][orc["gain"] > 0])[::-1][:K]
     assert abs((e0 - e1) - kept.sum()) <= 1e-5 * e0
+
+
+def test_pipeline_paper_pf_operating_point_pow2():
+    """The paper's P_F record: (C, P, b, S) = (16, 4, 4, 16), ceil(log2 T)-bit
+    index and an 8-bit power-of-two exponent; per-element weights, global
+    ranking.  backbone -> encode -> rank -> decode on the GPU against the same
+    chain in the oracle: identical stream bytes and repaired weights."""
+    wl = workload("block3b", C=16, P=4, b=4, S=16, d_mode="elem", idx_bits=0)
+    m = Module("t", 48, 256, 0, 4, 4)
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m, fmt=1)
+    p = _params(wl, 1)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_GLOBAL, 1.5, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    W32 = inp["W32"].cpu().numpy()
+    d = inp["d"].cpu().numpy()
+    _, _, _, W0o = O.rtn_backbone(W32)
+    op = _oparams(wl, 1)
+    orc = O.encode_tiles(O.tiles(O.residual(W32, W0o), wl.C), O.tile_weights(d, m.rows, m.cols, wl.C), op)
+    want, K_o, ne_o = O.build_stream(op, [(m.rows, m.cols)], orc, 1.5, per_module=False)
+    hd = O.parse_header(want)
+    assert hd["L_rec"] == (10 + 4 + 16 + 8 + 7) // 8 and hd["scale_bits"] == 8 and hd["scale_fmt"] == 1
+    assert (K, ne) == (K_o, ne_o) and K > 0
+    assert bytes(s.cpu().numpy().tobytes()) == want
+    What = W0.clone()
+    awsrc.awsrc_decode_add(s, [What])
+    ref = O.decode_add(want, [W0o])[0]
+    w0f = W0o.astype(np.float64)
+    assert np.all(np.abs(What.cpu().numpy() - ref) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(ref - w0f)) + 1e-30)
+
+
+def test_rank_and_decode_pow2_records():
+    """Random records in the power-of-two format: byte-identical stream, and
+    decoding onto bf16 and fp32 targets within the stated tolerances."""
+    op = O.Params(C=64, P=8, b=4, S=256, scale_fmt=1)
+    p = awsrc.make_params(64, 8, 4, 256, scale_fmt=1)
+    mods = [(16, 512), (8, 1024)]
+    T = sum(r * c // 64 for r, c in mods)
+    rec = gen_records(T, 8, 4, 256, seed=17)
+    # exponents e in [-28, 3] (fields 100..131) and some field-0 records: 2^-128
+    # is a valid (subnormal) scale whose correction is negligible
+    rec["scale"] = (100 + (rec["scale"].to(torch.int32) & 0x1F)).to(torch.int16)
+    rec["scale"][::7] = 0
+    enc = {"seed": rec["seed"].numpy().astype(np.int64) & 0xFFFF, "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    want, K_o, ne_o = O.build_stream(op, mods, enc, 4.0, per_module=False)
+    dev = {k: v.to(DEV) for k, v in rec.items()}
+    s, K, ne = awsrc.awsrc_rank_prefix(p, mods, awsrc.AWSRC_MODE_GLOBAL, 4.0, dev["seed"], dev["codes"],
+                                       dev["scale"], dev["gain"])
+    assert (K, ne) == (K_o, ne_o) and bytes(s.cpu().numpy().tobytes()) == want
+    g = torch.Generator().manual_seed(3)
+    for dtype, tol in ((torch.float32, 2.0 ** -22), (torch.bfloat16, 2.0 ** -8)):
+        W0s = [(torch.randn(r, c, generator=g) * 0.02).to(dtype) for r, c in mods]
+        refs = O.decode_add(want, [w.to(torch.float32).numpy() for w in W0s])
+        outs = [w.to(DEV) for w in W0s]
+        awsrc.awsrc_decode_add(s, outs)
+        for w0, got, ref in zip(W0s, outs, refs):
+            w0f = w0.to(torch.float32).numpy().astype(np.float64)
+            diff = np.abs(got.to(torch.float32).cpu().numpy() - ref)
+            assert np.all(diff <= tol * (np.abs(w0f) + np.abs(ref - w0f)) + 1e-30)
 
 
 def test_pipeline_down3b_properties():
