@@ -200,6 +200,38 @@ def rtn_backbone(W32: np.ndarray, group: int = 128):
             W0.reshape(rows, cols).astype(np.float32))
 
 
+def rtn_dequant(codes: np.ndarray, scale16: np.ndarray, zero: np.ndarray, group: int = 128) -> np.ndarray:
+    """W0 from the stored backbone (codes, fp16 scale bits, zero points):
+    W0 = f32(q - z) * s per group, the last step of RTN-v1, in float32."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    rows = codes.shape[0]
+    cols = codes.shape[1] * 2
+    q = np.empty((rows, cols), dtype=np.float32)
+    q[:, 0::2] = codes & 0x0F
+    q[:, 1::2] = codes >> 4
+    s = np.asarray(scale16, dtype=np.uint16).view(np.float16).astype(np.float32)
+    z = np.asarray(zero, dtype=np.float32)
+    qg = q.reshape(rows, cols // group, group)
+    return ((qg - z[..., None]) * s[..., None]).astype(np.float32).reshape(rows, cols)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 (8 significant bits, ties
+    to even), returned as float64; one rounding of the exact value."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                    # x = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+def reconstruct_bf16(stream: bytes, backbones: Sequence[Tuple[np.ndarray, np.ndarray, np.ndarray]],
+                     group: int = 128) -> List[np.ndarray]:
+    """Dense bf16 repaired weights (the evaluation form of Sec. 4): each
+    module's W0 dequantized from its stored backbone, the stream's
+    corrections added (decode_add), and the exact sum rounded to bfloat16."""
+    W0s = [rtn_dequant(c, s, z, group) for c, s, z in backbones]
+    return [bf16_round(w) for w in decode_add(stream, W0s)]
+
+
 def residual(W32: np.ndarray, W0: np.ndarray) -> np.ndarray:
     """R = W - W0 of Eq. (1), one float32 subtraction per element."""
     return (np.asarray(W32, dtype=np.float32) - np.asarray(W0, dtype=np.float32)).astype(np.float32)

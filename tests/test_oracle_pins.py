@@ -605,3 +605,37 @@ def test_pow2_decode_exact_power_of_two_scaling():
     rhat = out[0, :16] - W0[0, :16]
     assert math.isclose(float(rhat @ rhat), 4.0 ** -5 * (49 + 9 + 0 + 1), rel_tol=1e-12)
     assert np.array_equal(out[0, 16:], W0[0, 16:]) and np.array_equal(out[1], W0[1])
+
+
+# ---------------------------------------------------------------- dense bf16 reconstruction
+def test_rtn_dequant_reproduces_backbone_W0():
+    rng = np.random.default_rng(8)
+    W = (rng.standard_normal((6, 512)) * 0.02).astype(np.float32)
+    W[0, :128] = 0.25                     # degenerate group
+    for group in (64, 128, 256):
+        codes, s16, z, W0 = O.rtn_backbone(W, group=group)
+        assert np.array_equal(O.rtn_dequant(codes, s16, z, group), W0)
+
+
+def test_bf16_round_matches_torch_on_fp32_values():
+    import torch
+    rng = np.random.default_rng(9)
+    x = (rng.standard_normal(20000) * np.exp(rng.uniform(-30, 30, 20000))).astype(np.float32)
+    # exact halfway points between bf16 neighbours, both parities
+    base = np.array([1.0, 1.0078125, 3.0, -1.5], dtype=np.float32)
+    x = np.concatenate([x, base + np.ldexp(1.0, -8).astype(np.float32) * np.abs(base)])
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.bf16_round(x.astype(np.float64)), want)
+
+
+def test_reconstruct_bf16_empty_stream_is_rounded_backbone():
+    rng = np.random.default_rng(10)
+    W = (rng.standard_normal((4, 256)) * 0.02).astype(np.float32)
+    codes, s16, z, W0 = O.rtn_backbone(W)
+    p = O.Params(C=64, P=4, b=4, S=8)
+    enc = {"seed": np.zeros(16, np.int64), "codes": np.zeros((16, 4), np.int64),
+           "scale": np.zeros(16, np.int64), "gain": -np.ones(16)}
+    stream, K, _ = O.build_stream(p, [(4, 256)], enc, 8.0, per_module=False)
+    assert K == 0
+    out = O.reconstruct_bf16(stream, [(codes, s16, z)])[0]
+    assert np.array_equal(out, O.bf16_round(W0.astype(np.float64)))
