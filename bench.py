@@ -136,7 +136,9 @@ def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
     ms = e0.elapsed_time(e1) / reps
     nbytes = K * (plan.L_rec + 2 * wl.C * 4)
     gbs = nbytes / (ms / 1e3) / 1e9
-    del W0, plan, dws, s
+    del W0, plan, dws
+    rec_stats = reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps)
+    del s
     # device-copy ceiling: one large copy, read + write bytes
     n = 1 << 30
     x = torch.empty(n, dtype=torch.float32, device=dev)
@@ -151,9 +153,45 @@ def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
     copy_gbs = 3 * 2 * 4 * n / (e0.elapsed_time(e1) / 1e3) / 1e9
     del x, y
     torch.cuda.empty_cache()
+    rec_stats["frac_copy"] = rec_stats["GB/s"] / copy_gbs
     return {"workload": f"{name} stream at {bpw} bpw, fp32 W0", "modules": len(shapes), "records": K,
             "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs}
+            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs, "reconstruct_bf16": rec_stats}
+
+
+def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps):
+    """Dense bf16 reconstruction of every module from a random RTN backbone
+    (codes, fp16 scales in [1e-3, 2e-3), zero points) plus the stream `s`.
+    Algorithmic bytes: codes (1/2 B per weight), scale and zero (3 B per
+    group of 128), the records, and the bf16 output (2 B per weight).  Each
+    call synchronizes once before its two launches, and the timed region
+    (HIP events on the library's stream) includes that host round trip."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(77)
+    bbs = []
+    for r, c in shapes:
+        codes = torch.randint(0, 256, (r, c // 2), dtype=torch.uint8, device=dev, generator=g)
+        sc = (torch.rand(r, c // 128, device=dev, generator=g) * 1e-3 + 1e-3).to(torch.float16).view(torch.int16)
+        z = torch.randint(0, 16, (r, c // 128), dtype=torch.uint8, device=dev, generator=g)
+        bbs.append((codes, sc, z))
+    outs = [torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in shapes]
+    plan, ws = awsrc.awsrc_decode_prepare(s, outs)
+    stream = torch.cuda.current_stream()
+    awsrc.awsrc_reconstruct_bf16(plan, bbs, 128)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        awsrc.awsrc_reconstruct_bf16(plan, bbs, 128)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    n_w = sum(r * c for r, c in shapes)
+    nbytes = n_w // 2 + 3 * (n_w // 128) + K * plan.L_rec + 2 * n_w
+    del outs, bbs, plan, ws
+    torch.cuda.empty_cache()
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"weights": n_w, "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
 
 
 def main() -> int:
@@ -169,7 +207,7 @@ def main() -> int:
     ap.add_argument("--decode-bpw", type=float, default=0.32)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        log("bench.py measures a single GPU: the codec has no cross-GPU step in this build "
+        log("bench.py measures a single GPU: the codec has no cross-GPU step "
             "(run with --gpus 1)")
         return 2
 

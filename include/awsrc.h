@@ -243,6 +243,33 @@ awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64_t stream_l
  */
 awsrc_status awsrc_decode_apply(const awsrc_decode_plan* plan, void* stream);
 
+/*
+ * Dense bf16 repaired weights, the form the evaluation of Sec. 4 runs on:
+ * W_hat = bf16(W0 + R_hat) for every tile, with W0 = f32(q - z) * s
+ * recomputed from the stored backbone (the last step of awsrc_backbone_rtn)
+ * rather than read from a materialized fp32 W0, and R_hat the stream's
+ * corrections (Eq. (1), Sec. 3.2).  Tiles without a record get bf16(W0).
+ * The sum is formed in fp32 and rounded once to bf16, nearest even.
+ *  plan       prepared by awsrc_decode_prepare with w0_dtype AWSRC_DTYPE_BF16
+ *             and W0_ptrs naming the OUTPUT buffers [rows, cols] bf16 of each
+ *             module; their contents are never read, every element is written.
+ *  group      the backbone group (64, 128 or 256); cols % group == 0.
+ *  codes, scale_f16, zero
+ *             host arrays [n_modules] of device pointers to each module's
+ *             backbone in the layouts awsrc_backbone_rtn writes; codes
+ *             8-byte aligned, scale_f16 2-byte aligned.  C >= 16 and at
+ *             most 2^36 weights per module.
+ * The backbone pointers are staged in the plan's workspace: calls on one plan
+ * are ordered by `stream`, and calls on different streams must not share a
+ * plan.  Synchronizes with `stream` once (to read the module shapes) before
+ * one asynchronous launch.  Errors: AWSRC_EINVAL for a plan that is not
+ * prepared or not bf16, a bad group, C < 16, a NULL or misaligned backbone
+ * pointer, cols not a multiple of group, or a module over 2^36 weights.
+ */
+awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group,
+                                    const uint8_t* const* codes, const uint16_t* const* scale_f16,
+                                    const uint8_t* const* zero, void* stream);
+
 /* Host-only helpers (no device needed). */
 /* L_rec in bytes for T_total tiles; -1 if p is invalid. */
 int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total);

@@ -26,7 +26,7 @@ AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_encode_tiles",
             "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
-            "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
+            "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
 
 class AwsrcError(RuntimeError):
@@ -74,6 +74,8 @@ def _load() -> ctypes.CDLL:
         "awsrc_decode_prepare": (i32, [vp, u64, i32, ctypes.POINTER(vp), P64, P64, i32,
                                        ctypes.POINTER(awsrc_decode_plan), vp, ctypes.POINTER(sz), vp]),
         "awsrc_decode_apply": (i32, [ctypes.POINTER(awsrc_decode_plan), vp]),
+        "awsrc_reconstruct_bf16": (i32, [ctypes.POINTER(awsrc_decode_plan), i32, ctypes.POINTER(vp),
+                                         ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
         "awsrc_record_bytes": (i64, [pp, i64]),
         "awsrc_header_bytes": (i64, [i32]),
         "awsrc_budget_bytes": (i64, [ctypes.c_double, i64]),
@@ -290,3 +292,17 @@ def awsrc_decode_prepare(stream_bytes: torch.Tensor, W0_list: List[torch.Tensor]
 def awsrc_decode_apply(plan: awsrc_decode_plan, stream=None) -> None:
     """One asynchronous launch adding every record of a prepared stream onto W0."""
     _check(LIB.awsrc_decode_apply(ctypes.byref(plan), _stream(stream)))
+
+
+def awsrc_reconstruct_bf16(plan: awsrc_decode_plan, backbones: Sequence[Tuple[torch.Tensor, torch.Tensor,
+                                                                               torch.Tensor]],
+                           group: int = 128, stream=None) -> None:
+    """Dense bf16(W0 + R_hat) into the bf16 buffers the plan was prepared on;
+    `backbones` holds each module's (codes, scale, zero) as awsrc_backbone_rtn
+    returns them."""
+    if len(backbones) != plan.n_modules:
+        raise ValueError(f"{len(backbones)} backbones for a plan of {plan.n_modules} modules")
+    for bb in backbones:
+        _dev(*bb)
+    arr = [(ctypes.c_void_p * len(backbones))(*[bb[k].data_ptr() for bb in backbones]) for k in range(3)]
+    _check(LIB.awsrc_reconstruct_bf16(ctypes.byref(plan), group, arr[0], arr[1], arr[2], _stream(stream)))

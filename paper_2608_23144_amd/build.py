@@ -48,7 +48,11 @@ def _compile(src: str) -> str:
 
 
 def build(jobs: int = 0) -> str:
-    """Compile every HIP source for gfx950 and link libawsrc.so; returns its path."""
+    """Compile every HIP source for gfx950 and link libawsrc.so; returns its path.
+    A library from an earlier build is removed first, so that a failed build
+    never leaves a stale one to be loaded."""
+    if os.path.exists(LIB):
+        os.remove(LIB)
     os.makedirs(OBJ, exist_ok=True)
     srcs = [s for s in SOURCES if os.path.exists(os.path.join(CSRC, s))]
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 2)))

@@ -289,9 +289,11 @@ namespace {
 
 // Workspace: basis tables | tile bitmap | error counter | module tables
 // (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
-// host-to-device copy fills them) | decoded records [K] x 32 B.
+// host-to-device copy fills them) | decoded records [K] x 32 B | tile ->
+// record map [T_total] u32 | backbone pointer tables [3n] of the bf16
+// reconstruction.
 struct DecodeLayout {
-  size_t basis, bitmap, err, tables, dec, total;
+  size_t basis, bitmap, err, tables, dec, tmap, bbtab, total;
 };
 
 DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_t K) {
@@ -301,7 +303,9 @@ DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_
   l.err = 256;
   l.tables = align_up((size_t)(3 * nmod + 1) * 8, 256);
   l.dec = align_up((size_t)K * 32, 256);
-  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec;
+  l.tmap = align_up((size_t)T_total * 4, 256);
+  l.bbtab = align_up((size_t)3 * nmod * 8, 256);
+  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.tmap + l.bbtab;
   return l;
 }
 
@@ -327,6 +331,8 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   a.mod_ptr = reinterpret_cast<void* const*>(ws + 8 * (size_t)(2 * n + 1));
   ws += l.tables;
   a.dec = reinterpret_cast<uint4*>(ws);
+  ws += l.dec;
+  a.tmap = reinterpret_cast<uint32_t*>(ws);
   return a;
 }
 
@@ -420,6 +426,51 @@ extern "C" awsrc_status awsrc_decode_apply(const awsrc_decode_plan* plan, void* 
   if (!plan || !plan->workspace) return fail(AWSRC_EINVAL, "plan is NULL or not prepared");
   if (plan->K == 0) return AWSRC_OK;
   HIPCHK(launch_decode_apply(decode_args(plan), (hipStream_t)stream));
+  return AWSRC_OK;
+}
+
+extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group,
+                                               const uint8_t* const* codes, const uint16_t* const* scale_f16,
+                                               const uint8_t* const* zero, void* stream) {
+  if (!plan || !plan->workspace) return fail(AWSRC_EINVAL, "plan is NULL or not prepared");
+  if (plan->w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "the plan's targets must be bf16");
+  if (group != 64 && group != 128 && group != 256) return fail(AWSRC_EINVAL, "group=%d: must be 64, 128 or 256", group);
+  if (plan->C < 16) return fail(AWSRC_EINVAL, "C=%d: the reconstruction needs C >= 16", plan->C);
+  if (!codes || !scale_f16 || !zero) return fail(AWSRC_EINVAL, "backbone pointer arrays are NULL");
+  const uint32_t n = (uint32_t)plan->n_modules;
+  const DecodeArgs a = decode_args(plan);
+  std::vector<uint64_t> tabs(3 * (size_t)n);
+  for (uint32_t m = 0; m < n; ++m) {
+    if (!codes[m] || !scale_f16[m] || !zero[m]) return fail(AWSRC_EINVAL, "backbone pointer of module %u is NULL", m);
+    if (reinterpret_cast<uintptr_t>(codes[m]) & 7) return fail(AWSRC_EINVAL, "codes of module %u must be 8-byte aligned", m);
+    if (reinterpret_cast<uintptr_t>(scale_f16[m]) & 1) return fail(AWSRC_EINVAL, "scale of module %u must be 2-byte aligned", m);
+    tabs[m] = reinterpret_cast<uint64_t>(codes[m]);
+    tabs[n + m] = reinterpret_cast<uint64_t>(scale_f16[m]);
+    tabs[2 * n + m] = reinterpret_cast<uint64_t>(zero[m]);
+  }
+  // stage the pointer tables and read back the module tables (tile offsets
+  // [n+1] then cols [n]); the one synchronization covers both copies
+  const DecodeLayout l = decode_layout(plan->S, plan->P, plan->T_total, n, plan->K);
+  char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(plan->workspace), 256));
+  uint64_t* bbt = reinterpret_cast<uint64_t*>(ws + l.total - 256 - l.bbtab);
+  std::vector<uint64_t> mt(2 * (size_t)n + 1);
+  hipStream_t s = (hipStream_t)stream;
+  HIPCHK(hipMemcpyAsync(bbt, tabs.data(), tabs.size() * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(mt.data(), a.mod_tile_off, mt.size() * 8, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  for (uint32_t m = 0; m < n; ++m) {
+    const int64_t c = (int64_t)mt[n + 1 + m];
+    if (c % group) return fail(AWSRC_EINVAL, "module %u: cols %lld not a multiple of group %d", m, (long long)c, group);
+    // the kernel indexes units of 16 weights within a module with 32 bits
+    if ((mt[m + 1] - mt[m]) * (uint64_t)(plan->C / 16) >= (1ull << 32))
+      return fail(AWSRC_EINVAL, "module %u: more than 2^36 weights", m);
+  }
+  BackboneTabs bb;
+  bb.codes = reinterpret_cast<const uint8_t* const*>(bbt);
+  bb.scale = reinterpret_cast<const uint16_t* const*>(bbt + n);
+  bb.zero = reinterpret_cast<const uint8_t* const*>(bbt + 2 * n);
+  bb.gshift = group == 64 ? 6 : group == 128 ? 7 : 8;
+  HIPCHK(launch_reconstruct_bf16(a, bb, s));
   return AWSRC_OK;
 }
 

@@ -71,10 +71,13 @@ __host__ __device__ __forceinline__ int ltri(int p, int k) { return p * (p - 1) 
 // Screen-precision scale of max |alpha| = m: fp16 f16(m / qmax) with
 // saturation, or the power of two 2^e, e = ceil(log2(m / qmax)), from the
 // exponent and mantissa bits of the fp32 quotient.  Returns the scale and
-// sets *isc to its reciprocal (0 when the scale is 0).
-__device__ __forceinline__ float screen_scale(float m, float inv_qmax, bool pow2, float* isc) {
+// sets *isc to its reciprocal (0 when the scale is 0).  The format is a
+// template argument: as a run-time flag it slowed the matrix-core screens by
+// about a quarter.
+template <bool POW2>
+__device__ __forceinline__ float screen_scale(float m, float inv_qmax, float* isc) {
   const float x = m * inv_qmax;
-  if (pow2) {
+  if constexpr (POW2) {
     const uint32_t xb = __float_as_uint(x);
     int e = (int)((xb >> 23) & 0xFFu) - 127 + ((xb & 0x7FFFFFu) ? 1 : 0);
     e = e < -126 ? -126 : (e > 127 ? 127 : e);
@@ -90,15 +93,14 @@ __device__ __forceinline__ float screen_scale(float m, float inv_qmax, bool pow2
 
 // Screen score of one (tile, seed) from the per-column factor f (a table
 // entry as above, read through any pointer type): solves G alpha = b with
-// the LDL^T factor, quantizes alpha with one scale (screen_scale; pow2
+// the LDL^T factor, quantizes alpha with one scale (screen_scale; POW2
 // selects the power-of-two format), q = clamp(rint(alpha / scale)), and
 // returns scale (2 q.b - scale q^T G q).  That is the exact gain
 // 2 a.b - a^T G0 a of the quantized fit minus scale^2 eps |q|^2 (relative
 // size ~ lambda), which the fp64 re-score of the kept seeds removes.  Uses
 // q.b = (L^T q).w with w = L^-1 b, and q^T G q = sum_k e_k (L^T q)_k^2.
-template <int PB, typename FP>
-__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax,
-                                                 bool pow2) {
+template <int PB, bool POW2, typename FP>
+__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
   constexpr int LS = PB * (PB - 1) / 2;
   float w[PB], al[PB];
 #pragma unroll
@@ -119,7 +121,7 @@ __device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP
 #pragma unroll
   for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
   float isc;
-  const float sc = screen_scale(m, inv_qmax, pow2, &isc);
+  const float sc = screen_scale<POW2>(m, inv_qmax, &isc);
   float q[PB];
 #pragma unroll
   for (int p = 0; p < PB; ++p) q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
@@ -230,8 +232,20 @@ struct DecodeArgs {
   // module, seed | scale << 16, sum of codes}, then the P codes as int8 (zero
   // padded to 16)
   uint4* dec;
+  uint32_t* tmap;                // [T_total] record of each tile whose bitmap bit is set
 };
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st);
 hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st);
+
+// Stored backbone of each module (layouts of awsrc_backbone_rtn), as device
+// tables of device pointers.
+struct BackboneTabs {
+  const uint8_t* const* codes;
+  const uint16_t* const* scale;
+  const uint8_t* const* zero;
+  int gshift;  // log2 of the backbone group
+};
+// Dense bf16 reconstruction into the plan's (bf16) module buffers.
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, hipStream_t st);
 
 }  // namespace awsrc

@@ -99,6 +99,7 @@ __global__ void k_decode_validate(DecodeArgs a) {
     const uint32_t bit = 1u << (r.idx & 31);
     const uint32_t old = atomicOr(&a.bitmap[r.idx >> 5], bit);
     bad = (old & bit) != 0;
+    a.tmap[r.idx] = (uint32_t)i;
   }
   if (bad) atomicAdd(a.errors, 1ull);
   // decoded form for the apply pass (only used once the whole stream is valid)
@@ -189,6 +190,177 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
       *q = make_uint4(o[0], o[1], o[2], o[3]);
     }
   }
+}
+
+// ---------------------------------------------------------------- dense bf16 reconstruction
+// One streaming pass over every weight of every module.  Lanes own 16
+// consecutive weights: 8 bytes of codes in, 32 bytes of bf16 out, W0 =
+// f32(q - z) * s recomputed from the backbone.  A lane whose tile has a record
+// (bit set in the validation bitmap) finds it through the tile -> record map
+// and adds its 16 corrections before the single rounding to bf16, so record
+// tiles cost no extra pass over the backbone or the output.
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));  // nearest even
+}
+
+// Corrections of 16 consecutive coordinates (rows sub*16 .. sub*16+15 of
+// B_s) of record i, added onto w.  With integer codes, sqrt(C) rhat_j is the
+// scale times sum_p q_p minus twice the codes at the negative entries of row
+// j, the latter one int8 dot product per four codes against a 0/1 byte mask
+// spread from the row's sign bits.
+template <int C, int G>
+__device__ __forceinline__ void add_record16(const DecodeArgs& a, uint32_t i, int sub, float (&w)[16]) {
+  constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
+                      : (C == 64) ? 0.125f : 0.08838834764831845f;
+  const uint4 e0 = a.dec[2 * (size_t)i];
+  const uint4 e1 = a.dec[2 * (size_t)i + 1];
+  const uint32_t q4[4] = {e1.x, e1.y, e1.z, e1.w};
+  const uint4* tsp = reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC + sub * 16);
+  const uint4 ta = tsp[0], tb = tsp[1];
+  const uint32_t tw[8] = {ta.x, ta.y, ta.z, ta.w, tb.x, tb.y, tb.z, tb.w};
+  const uint32_t sfield = e0.z >> 16;
+  const float scl = a.scale_fmt == AWSRC_SCALE_POW2 ? ldexpf(isq, (int)sfield - 128)
+                                                    : __half2float(__ushort_as_half((uint16_t)sfield)) * isq;
+  const int32_t tot = (int32_t)e0.w;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const uint32_t ts = (tw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+    int32_t neg = 0;
+#pragma unroll
+    for (int gg = 0; gg < G; ++gg) {
+      const uint32_t mask = (((ts >> (4 * gg)) & 0xFu) * 0x204081u) & 0x01010101u;
+      neg = __builtin_amdgcn_sdot4((int)mask, (int)q4[gg], neg, false);
+    }
+    w[e] += (float)(tot - 2 * neg) * scl;
+  }
+}
+
+// global-address-space views: loads and stores through them are issued as
+// global (not flat) memory instructions
+#define AWSRC_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int C, int G>
+__global__ __launch_bounds__(256) void k_reconstruct(DecodeArgs a, BackboneTabs bb) {
+  constexpr int UPT = C / 16;                            // lanes per tile
+  constexpr int LOG_UPT = (C == 16) ? 0 : (C == 32) ? 1 : (C == 64) ? 2 : 3;
+  constexpr int NU = 4;                                  // units per lane per block iteration
+  constexpr int CHUNK = NU * 256;
+  __shared__ uint64_t s_off[kLdsModules + 1];
+  const bool lds_tab = a.n_modules <= kLdsModules;
+  if (lds_tab)
+    for (int m = threadIdx.x; m <= a.n_modules; m += 256) s_off[m] = a.mod_tile_off[m];
+  __syncthreads();
+  const uint64_t* off = lds_tab ? s_off : a.mod_tile_off;
+  const uint64_t n_units = a.T_total << LOG_UPT;
+  // per-lane module state, kept in registers; units only move forward, so
+  // the module walk costs at most n_modules steps per lane over the launch
+  int m = 0;
+  uint64_t m_lo = 0, m_hi = off[1] << LOG_UPT;
+  int64_t cols = a.mod_cols[0];
+  uint32_t upr = (uint32_t)(cols >> 4), gpr = (uint32_t)(cols >> bb.gshift);
+  const AWSRC_GLOBAL uint8_t* cp = (const AWSRC_GLOBAL uint8_t*)bb.codes[0];
+  const AWSRC_GLOBAL uint16_t* sp = (const AWSRC_GLOBAL uint16_t*)bb.scale[0];
+  const AWSRC_GLOBAL uint8_t* zp = (const AWSRC_GLOBAL uint8_t*)bb.zero[0];
+  AWSRC_GLOBAL uint16_t* op = (AWSRC_GLOBAL uint16_t*)a.mod_ptr[0];
+  for (uint64_t c0 = (uint64_t)blockIdx.x * CHUNK; c0 < n_units; c0 += (uint64_t)gridDim.x * CHUNK) {
+    // addresses of this lane's NU units, then all their loads, then the math
+    const AWSRC_GLOBAL u32x2_t* qa[NU];
+    const AWSRC_GLOBAL uint16_t* sa[NU];
+    const AWSRC_GLOBAL uint8_t* za[NU];
+    AWSRC_GLOBAL u32x4_t* oa[NU];
+    uint64_t tt[NU];
+    int sub[NU];
+    bool ok[NU];
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const uint64_t u = c0 + k * 256 + threadIdx.x;
+      ok[k] = u < n_units;
+      if (ok[k] && u >= m_hi) {
+        do { ++m; } while ((off[m + 1] << LOG_UPT) <= u);
+        m_lo = off[m] << LOG_UPT;
+        m_hi = off[m + 1] << LOG_UPT;
+        cols = a.mod_cols[m];
+        upr = (uint32_t)(cols >> 4);
+        gpr = (uint32_t)(cols >> bb.gshift);
+        cp = (const AWSRC_GLOBAL uint8_t*)bb.codes[m];
+        sp = (const AWSRC_GLOBAL uint16_t*)bb.scale[m];
+        zp = (const AWSRC_GLOBAL uint8_t*)bb.zero[m];
+        op = (AWSRC_GLOBAL uint16_t*)a.mod_ptr[m];
+      }
+      const uint32_t uw = (uint32_t)(u - m_lo);          // unit within the module
+      const uint32_t row = uw / upr;
+      const uint32_t col0 = (uw - row * upr) * 16;
+      const int64_t el = (int64_t)row * cols + col0;
+      const uint32_t g = row * gpr + (col0 >> bb.gshift);
+      qa[k] = (const AWSRC_GLOBAL u32x2_t*)(cp + (el >> 1));
+      sa[k] = sp + g;
+      za[k] = zp + g;
+      oa[k] = (AWSRC_GLOBAL u32x4_t*)(op + el);
+      tt[k] = u >> LOG_UPT;
+      sub[k] = (int)(uw & (UPT - 1));
+    }
+    u32x2_t q16[NU];
+    uint32_t sraw[NU], zraw[NU], bits[NU];
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      if (ok[k]) {
+        q16[k] = *qa[k];
+        sraw[k] = *sa[k];
+        zraw[k] = *za[k];
+        bits[k] = a.bitmap[tt[k] >> 5];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      if (!ok[k]) continue;
+      const float s = __half2float(__ushort_as_half((uint16_t)sraw[k]));
+      const float z = (float)zraw[k];
+      float w[16];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        w[e] = ((float)((q16[k].x >> (4 * e)) & 0xFu) - z) * s;
+        w[8 + e] = ((float)((q16[k].y >> (4 * e)) & 0xFu) - z) * s;
+      }
+      if ((bits[k] >> (tt[k] & 31)) & 1u) add_record16<C, G>(a, a.tmap[tt[k]], sub[k], w);
+      const u32x4_t lo = {bf16_pair(w[0], w[1]), bf16_pair(w[2], w[3]), bf16_pair(w[4], w[5]),
+                          bf16_pair(w[6], w[7])};
+      const u32x4_t hi = {bf16_pair(w[8], w[9]), bf16_pair(w[10], w[11]), bf16_pair(w[12], w[13]),
+                          bf16_pair(w[14], w[15])};
+      oa[k][0] = lo;
+      oa[k][1] = hi;
+    }
+  }
+}
+
+template <int C>
+static void launch_rec_c(const DecodeArgs& a, const BackboneTabs& bb, unsigned nb, hipStream_t st) {
+  switch ((a.P + 3) / 4) {
+    case 1: hipLaunchKernelGGL((k_reconstruct<C, 1>), dim3(nb), dim3(256), 0, st, a, bb); break;
+    case 2: hipLaunchKernelGGL((k_reconstruct<C, 2>), dim3(nb), dim3(256), 0, st, a, bb); break;
+    case 3: hipLaunchKernelGGL((k_reconstruct<C, 3>), dim3(nb), dim3(256), 0, st, a, bb); break;
+    default: hipLaunchKernelGGL((k_reconstruct<C, 4>), dim3(nb), dim3(256), 0, st, a, bb); break;
+  }
+}
+
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, hipStream_t st) {
+  const uint64_t n_units = a.T_total * (uint64_t)(a.C / 16);
+  uint64_t nb = (n_units + 1023) / 1024;
+  if (nb > 256 * 8) nb = 256 * 8;  // eight resident blocks per CU, grid-stride beyond
+  switch (a.C) {
+    case 16: launch_rec_c<16>(a, bb, (unsigned)nb, st); break;
+    case 32: launch_rec_c<32>(a, bb, (unsigned)nb, st); break;
+    case 64: launch_rec_c<64>(a, bb, (unsigned)nb, st); break;
+    case 128: launch_rec_c<128>(a, bb, (unsigned)nb, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {

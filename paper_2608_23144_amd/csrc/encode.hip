@@ -229,7 +229,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 #pragma unroll
       for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
       float isc;
-      const float sc = screen_scale(m, inv_qmax, pow2, &isc);
+      const float sc = pow2 ? screen_scale<true>(m, inv_qmax, &isc) : screen_scale<false>(m, inv_qmax, &isc);
       g = 0.0f;
       if (sc > 0.0f) {
         float q[PB], t1 = 0.0f, qq = 0.0f;
@@ -251,7 +251,8 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
         g = sc * (2.0f * t1 - sc * quad);
       }
     } else {
-      g = screen_score_ldl<PB>(bv, a.colfac + ((size_t)blk * a.S + s) * stride, qmax, inv_qmax, pow2);
+      const float* fs = a.colfac + ((size_t)blk * a.S + s) * stride;
+      g = pow2 ? screen_score_ldl<PB, true>(bv, fs, qmax, inv_qmax) : screen_score_ldl<PB, false>(bv, fs, qmax, inv_qmax);
     }
     // keep the best kTop, earlier (lower) seeds first among equals
     float cg = g;

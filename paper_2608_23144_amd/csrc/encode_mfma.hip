@@ -99,7 +99,7 @@ __global__ void k_mfma_frags(BasisTables bt, int C, int P, int S, u32x4* __restr
 // block and one range of seed pairs; lane = tile during the per-candidate
 // stage.  Seed ranges are used only when a module has too few row groups to
 // fill the machine (each range costs its own tile loads and top list).
-template <bool PE>
+template <bool PE, bool POW2>
 __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32x4* __restrict__ frag,
                                                          int stride) {
   constexpr int C = 64;
@@ -173,7 +173,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   }
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
-  const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   const float lam = (float)a.lambda;
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
@@ -286,19 +285,19 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
           f[LS + PB + p] = t;
           f[LS + p] = __builtin_amdgcn_rcpf(t);
         }
-        gsc = screen_score_ldl<PB>(bk[k], f, qmax, inv_qmax, pow2);
+        gsc = screen_score_ldl<PB, POW2>(bk[k], f, qmax, inv_qmax);
       } else {
         // uniform across the wavefront: scalar loads through the constant address space
         if (k == 0) {
           const cfp fb = fac_ptr(s + 1);
 #pragma unroll
           for (int i = 0; i < NF; ++i) fB[i] = fb[i];
-          gsc = screen_score_ldl<PB>(bk[0], fA, qmax, inv_qmax, pow2);
+          gsc = screen_score_ldl<PB, POW2>(bk[0], fA, qmax, inv_qmax);
         } else {
           const cfp fa = fac_ptr(s + 1);
 #pragma unroll
           for (int i = 0; i < NF; ++i) fA[i] = fa[i];
-          gsc = screen_score_ldl<PB>(bk[1], fB, qmax, inv_qmax, pow2);
+          gsc = screen_score_ldl<PB, POW2>(bk[1], fB, qmax, inv_qmax);
         }
       }
       gsc = s < a.S ? gsc : -INFINITY;
@@ -337,7 +336,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
 // would round the fp16 scale differently); each half keeps its own top two,
 // merged at the end.  (Written for any C that is a multiple of 32; at C = 64
 // it measured slower than k_screen_mfma64, which is used there.)
-template <int C>
+template <int C, bool POW2>
 __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, const u32x4* __restrict__ frag,
                                                               int stride) {
   constexpr int PB = 8;
@@ -386,7 +385,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   const bool my_valid = my_row < a.rows;
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
-  const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   constexpr float isq = C == 64 ? 0.125f : 0.08838834764831845f;  // 1/sqrt(C)
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
@@ -449,7 +447,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     project(F, accN);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
-    float gsc = screen_score_ldl<PB>(bv, f, qmax, inv_qmax, pow2);
+    float gsc = screen_score_ldl<PB, POW2>(bv, f, qmax, inv_qmax);
     gsc = s < a.S ? gsc : -INFINITY;
     // this lane's seeds increase, so strict comparisons keep the lower seed among equals
     const bool c0 = gsc > tg0, c1 = gsc > tg1;
@@ -509,24 +507,29 @@ int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode) {
 // the table carries two zero pairs past the last seed (see the pipeline above)
 size_t mfma_frag_bytes(int C, int S) { return (size_t)((S + 1) / 2 + 2) * (C / 32) * 64 * 16; }
 
-hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
-  const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
-  hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
-                     static_cast<u32x4*>(frag));
+template <bool POW2>
+static hipError_t screen_mfma_fmt(const EncodeArgs& a, void* frag, hipStream_t st) {
+  const u32x4* fr = static_cast<const u32x4*>(frag);
   if (a.C == 128) {
     const int64_t wgs = (a.cols / a.C) * ((a.rows + 31) / 32) * a.nsplit;
-    hipLaunchKernelGGL(k_screen_mfma_halves<128>, dim3((unsigned)wgs), dim3(64), 0, st, a,
-                       static_cast<const u32x4*>(frag), colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_mfma_halves<128, POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr,
+                       colfac_stride(8));
     return hipGetLastError();
   }
   const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
   if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL(k_screen_mfma64<true>, dim3((unsigned)wgs), dim3(64), 0, st, a,
-                       static_cast<const u32x4*>(frag), colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_mfma64<true, POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   else
-    hipLaunchKernelGGL(k_screen_mfma64<false>, dim3((unsigned)wgs), dim3(64), 0, st, a,
-                       static_cast<const u32x4*>(frag), colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_mfma64<false, POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   return hipGetLastError();
+}
+
+hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
+  const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
+  hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
+                     static_cast<u32x4*>(frag));
+  if (a.scale_fmt == AWSRC_SCALE_POW2) return screen_mfma_fmt<true>(a, frag, st);
+  return screen_mfma_fmt<false>(a, frag, st);
 }
 
 }  // namespace awsrc

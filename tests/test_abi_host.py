@@ -16,7 +16,7 @@ awsrc = pytest.importorskip("paper_2608_23144_amd")
 def _declared_functions():
     src = open(os.path.join(ROOT, "include", "awsrc.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(awsrc_[a-z_A-Z]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(awsrc_[a-z_A-Z0-9]+)\s*\(", src)))
 
 
 def test_every_declared_symbol_is_exported():
@@ -135,3 +135,22 @@ def test_misaligned_pointers_rejected_without_device_access():
     assert st == awsrc.AWSRC_EINVAL
     st = awsrc.LIB.awsrc_backbone_rtn(v(256), 1, 4, 256, 128, v(258), v(256), v(256), None, None)
     assert st == awsrc.AWSRC_EINVAL
+
+
+def test_reconstruct_rejects_bad_arguments_without_device_access():
+    plan = awsrc.awsrc_decode_plan()
+    v = ctypes.c_void_p
+    arr = (v * 1)(256)
+    f = awsrc.LIB.awsrc_reconstruct_bf16
+    assert f(ctypes.byref(plan), 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # not prepared
+    plan.workspace = 4096
+    plan.n_modules = 1
+    plan.w0_dtype = awsrc.AWSRC_DTYPE_F32
+    assert f(ctypes.byref(plan), 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # fp32 targets
+    plan.w0_dtype = awsrc.AWSRC_DTYPE_BF16
+    assert f(ctypes.byref(plan), 96, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # group
+    assert f(ctypes.byref(plan), 128, None, arr, arr, None) == awsrc.AWSRC_EINVAL
+    bad = (v * 1)(258)
+    assert f(ctypes.byref(plan), 128, bad, arr, arr, None) == awsrc.AWSRC_EINVAL  # codes alignment
+    odd = (v * 1)(257)
+    assert f(ctypes.byref(plan), 128, arr, odd, arr, None) == awsrc.AWSRC_EINVAL  # scale alignment

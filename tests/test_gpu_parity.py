@@ -509,3 +509,115 @@ def test_pipeline_down3b_properties():
     e0 = (dd * (W - W0.double()) ** 2).sum().item()
     e1 = (dd * (W - What.double()) ** 2).sum().item()
     assert abs((e0 - e1) - gain[order].sum()) <= 1e-6 * e0
+
+
+def _reconstruct_case(C, P, b, S, mods, group, bpw, seed, fmt=0):
+    """Oracle stream from seeded records, oracle backbones from seeded W; the
+    GPU reconstructs into bf16 buffers pre-filled with NaN patterns."""
+    op = O.Params(C=C, P=P, b=b, S=S, basis_key=0x51, scale_fmt=fmt)
+    T = sum(r * c // C for r, c in mods)
+    rec = gen_records(T, P, b, S, seed=seed)
+    if fmt == O.SCALE_POW2:
+        rec["scale"] = (100 + (rec["scale"].to(torch.int32) & 0x1F)).to(torch.int16)
+    enc = {"seed": rec["seed"].numpy().astype(np.int64) & 0xFFFF, "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    stream, K, _ = O.build_stream(op, mods, enc, bpw, per_module=False)
+    g = torch.Generator().manual_seed(seed + 1)
+    bbs = [O.rtn_backbone((torch.randn(r, c, generator=g) * 0.02).numpy(), group)[:3] for r, c in mods]
+    want = O.reconstruct_bf16(stream, bbs, group)
+    W0s = [O.rtn_dequant(cd, s16, z, group) for cd, s16, z in bbs]
+    dev_bb = [tuple(torch.from_numpy(np.ascontiguousarray(a)).to(DEV) for a in (cd, s16.view(np.int16), z))
+              for cd, s16, z in bbs]
+    outs = [torch.full((r, c), -1, dtype=torch.int16, device=DEV).view(torch.bfloat16) for r, c in mods]
+    sb = torch.tensor(list(stream), dtype=torch.uint8, device=DEV)
+    plan, ws = awsrc.awsrc_decode_prepare(sb, outs)
+    awsrc.awsrc_reconstruct_bf16(plan, dev_bb, group)
+    torch.cuda.synchronize()
+    return stream, K, W0s, want, outs
+
+
+def _check_reconstruct(C, stream, K, W0s, want, outs, mods):
+    hd = O.parse_header(stream)
+    offs = np.cumsum([0] + [r * c // C for r, c in mods])
+    touched = [np.zeros((r, c // C), bool) for r, c in mods]
+    L = hd["L_rec"]
+    for k in range(K):
+        t = O.unpack_record(stream[hd["h"] + k * L: hd["h"] + (k + 1) * L], hd["idx_bits"], hd["seed_bits"],
+                            hd["P"], hd["b"], hd["scale_bits"])[0]
+        mi = int(np.searchsorted(offs, t, side="right") - 1)
+        rr, bk = divmod(int(t - offs[mi]), mods[mi][1] // C)
+        touched[mi][rr, bk] = True
+    n_exact = n_rec = 0
+    for w0, got, ref, ex, tm in zip(W0s, outs, want, O.decode_add(stream, W0s), touched):
+        got = got.to(torch.float32).cpu().numpy().astype(np.float64)
+        mask = np.repeat(tm, C, axis=1)
+        # tiles without a record: bf16(W0), one rounding of the same fp32 value
+        assert np.array_equal(got[~mask], ref[~mask])
+        # record tiles: both sides round to bf16 once, from sums that differ by
+        # the fp32 add's rounding, so they agree to one bf16 ulp.  The oracle's
+        # fp64 correction carries its own rounding of P terms, each at most the
+        # tile's largest |rhat| (B_s has orthonormal columns): where the exact
+        # sum is zero (W0 = 0 and the integer sum cancels) the kernel returns 0
+        # and the oracle a residue below 2^-40 of that.
+        w0f = w0.astype(np.float64)
+        rh = np.abs(ex - w0f)
+        tile_max = np.repeat(rh.reshape(rh.shape[0], -1, C).max(axis=2), C, axis=1)
+        mag = np.abs(w0f) + rh
+        diff = np.abs(got - ref)
+        assert np.all(diff[mask] <= 2.0 ** -7 * np.abs(ref[mask]) + 2.0 ** -21 * mag[mask]
+                      + 2.0 ** -40 * tile_max[mask])
+        n_exact += int(np.count_nonzero(diff[mask] == 0))
+        n_rec += int(np.count_nonzero(mask))
+    assert n_rec == K * C
+    assert n_exact >= 0.98 * n_rec
+
+
+@pytest.mark.parametrize("C,P,b,S,group,mods,fmt", [
+    (64, 8, 4, 256, 128, [(33, 512), (8, 1024)], 0),
+    (64, 8, 4, 256, 128, [(33, 512), (8, 1024)], 1),
+    (16, 4, 4, 16, 64, [(5, 128), (3, 256), (1, 64)], 0),
+    (32, 5, 3, 32, 256, [(7, 256), (4, 768)], 0),
+    (128, 8, 4, 64, 256, [(9, 512)], 1),
+    (128, 16, 4, 64, 128, [(6, 1024)], 0),
+])
+def test_reconstruct_bf16_matches_oracle(C, P, b, S, group, mods, fmt):
+    stream, K, W0s, want, outs = _reconstruct_case(C, P, b, S, mods, group, 2.0, seed=5, fmt=fmt)
+    assert K > 0
+    _check_reconstruct(C, stream, K, W0s, want, outs, mods)
+
+
+def test_reconstruct_bf16_empty_stream_and_many_modules():
+    """K = 0 gives bf16(W0) everywhere; 300 modules exceed the module table
+    the dense pass stages in LDS."""
+    C, P, b, S = 16, 4, 4, 16
+    stream, K, W0s, want, outs = _reconstruct_case(C, P, b, S, [(8, 256)], 64, 0.19, seed=2)  # header only
+    assert K == 0
+    _check_reconstruct(C, stream, K, W0s, want, outs, [(8, 256)])
+    mods = [(1 + (m % 3), 64 * (1 + m % 2)) for m in range(300)]
+    stream, K, W0s, want, outs = _reconstruct_case(C, P, b, S, mods, 64, 6.0, seed=8)
+    assert K > 100
+    _check_reconstruct(C, stream, K, W0s, want, outs, mods)
+
+
+def test_reconstruct_bf16_down3b_pipeline():
+    """Full-size 3B down projection: GPU backbone, encoder and ranked stream,
+    reconstructed in bf16; matches the oracle's reconstruction of the same
+    stream and backbone, and equals decode_add onto a bf16 copy of W0 except
+    where that rounds twice."""
+    wl = WORKLOADS["down3b"]
+    m = wl.modules[0]
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m, want_alpha=False)
+    p = _params(wl)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_GLOBAL, 0.162, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    assert K > 1000
+    out = torch.empty(m.rows, m.cols, dtype=torch.bfloat16, device=DEV)
+    plan, ws = awsrc.awsrc_decode_prepare(s, [out])
+    awsrc.awsrc_reconstruct_bf16(plan, [(codes, scale, zero)], 128)
+    torch.cuda.synchronize()
+    stream = bytes(s.cpu().numpy().tobytes())
+    bb = (codes.cpu().numpy(), _u16(scale).astype(np.uint16), zero.cpu().numpy())
+    want = O.reconstruct_bf16(stream, [bb], 128)
+    W0s = [O.rtn_dequant(*bb, 128)]
+    assert np.array_equal(W0s[0], W0.cpu().numpy())
+    _check_reconstruct(wl.C, stream, K, W0s, want, [out], [(m.rows, m.cols)])
