@@ -289,11 +289,11 @@ namespace {
 
 // Workspace: basis tables | tile bitmap | error counter | module tables
 // (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
-// host-to-device copy fills them) | decoded records [K] x 32 B | tile ->
-// record map [T_total] u32 | backbone pointer tables [3n] of the bf16
-// reconstruction.
+// host-to-device copy fills them) | decoded records [K] x 32 B | for the bf16
+// reconstruction: the records in tile order [K + 1] x 32 B, prefix counts of
+// the bitmap words and their scan scratch, backbone pointer tables [3n].
 struct DecodeLayout {
-  size_t basis, bitmap, err, tables, dec, tmap, bbtab, total;
+  size_t basis, bitmap, err, tables, dec, dec_t, pre, bsum, bbtab, total;
 };
 
 DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_t K) {
@@ -303,9 +303,12 @@ DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_
   l.err = 256;
   l.tables = align_up((size_t)(3 * nmod + 1) * 8, 256);
   l.dec = align_up((size_t)K * 32, 256);
-  l.tmap = align_up((size_t)T_total * 4, 256);
+  l.dec_t = align_up((size_t)(K + 1) * 32, 256);  // entry 0 is readable even when K = 0
+  const size_t nwords = (size_t)((T_total + 31) / 32);
+  l.pre = align_up(nwords * 4, 256);
+  l.bsum = align_up(((nwords + 4095) / 4096) * 4, 256);
   l.bbtab = align_up((size_t)3 * nmod * 8, 256);
-  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.tmap + l.bbtab;
+  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.dec_t + l.pre + l.bsum + l.bbtab;
   return l;
 }
 
@@ -332,7 +335,9 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   ws += l.tables;
   a.dec = reinterpret_cast<uint4*>(ws);
   ws += l.dec;
-  a.tmap = reinterpret_cast<uint32_t*>(ws);
+  a.dec_t = reinterpret_cast<uint4*>(ws); ws += l.dec_t;
+  a.pre = reinterpret_cast<uint32_t*>(ws); ws += l.pre;
+  a.bsum = reinterpret_cast<uint32_t*>(ws);
   return a;
 }
 
@@ -448,8 +453,8 @@ extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, in
     tabs[n + m] = reinterpret_cast<uint64_t>(scale_f16[m]);
     tabs[2 * n + m] = reinterpret_cast<uint64_t>(zero[m]);
   }
-  // stage the pointer tables and read back the module tables (tile offsets
-  // [n+1] then cols [n]); the one synchronization covers both copies
+  // stage the backbone pointers and read back the module tables (tile
+  // offsets [n+1] then cols [n]); the one synchronization covers both copies
   const DecodeLayout l = decode_layout(plan->S, plan->P, plan->T_total, n, plan->K);
   char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(plan->workspace), 256));
   uint64_t* bbt = reinterpret_cast<uint64_t*>(ws + l.total - 256 - l.bbtab);
@@ -466,11 +471,9 @@ extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, in
       return fail(AWSRC_EINVAL, "module %u: more than 2^36 weights", m);
   }
   BackboneTabs bb;
-  bb.codes = reinterpret_cast<const uint8_t* const*>(bbt);
-  bb.scale = reinterpret_cast<const uint16_t* const*>(bbt + n);
-  bb.zero = reinterpret_cast<const uint8_t* const*>(bbt + 2 * n);
+  bb.ptr = bbt;
   bb.gshift = group == 64 ? 6 : group == 128 ? 7 : 8;
-  HIPCHK(launch_reconstruct_bf16(a, bb, s));
+  HIPCHK(launch_reconstruct_bf16(a, bb, mt.data(), s));
   return AWSRC_OK;
 }
 

@@ -232,20 +232,23 @@ struct DecodeArgs {
   // module, seed | scale << 16, sum of codes}, then the P codes as int8 (zero
   // padded to 16)
   uint4* dec;
-  uint32_t* tmap;                // [T_total] record of each tile whose bitmap bit is set
+  uint4* dec_t;                  // [K + 1][2] the same records in tile order (reconstruction)
+  uint32_t* pre;                 // [ceil(T_total / 32)] record tiles before each bitmap word
+  uint32_t* bsum;                // [ceil(words / 4096)] scan scratch
 };
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st);
 hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st);
 
-// Stored backbone of each module (layouts of awsrc_backbone_rtn), as device
-// tables of device pointers.
+// Stored backbone of each module for the bf16 reconstruction: device table
+// of device pointers, codes [n] | scale [n] | zero [n] (layouts of
+// awsrc_backbone_rtn), n = n_modules.
 struct BackboneTabs {
-  const uint8_t* const* codes;
-  const uint16_t* const* scale;
-  const uint8_t* const* zero;
+  const uint64_t* ptr;
   int gshift;  // log2 of the backbone group
 };
-// Dense bf16 reconstruction into the plan's (bf16) module buffers.
-hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, hipStream_t st);
+// Dense bf16 reconstruction into the plan's (bf16) module buffers; toff is a
+// host copy of the tile offsets (one launch per window of modules).
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff,
+                                   hipStream_t st);
 
 }  // namespace awsrc

@@ -4,17 +4,28 @@
 // validate - one thread per record: field ranges, finite non-negative scale,
 //            and a bitmap over tiles that catches a tile appearing twice
 //            (records of a valid stream touch disjoint tiles, which is what
-//            lets the apply pass run without atomics or ordering).
+//            lets the apply pass run without atomics or ordering);
 // validate also writes each record in a decoded form (tile within its
 //            module, module, seed, scale, codes and their sum);
 // apply    - C/8 lanes per record, eight consecutive weights per lane; each
 //            weight gets rhat_j = (1/sqrt(C)) sum_p (+-1) scale*q_p with the
-//            signs of row j of B_s read from the transposed sign table.
+//            signs of row j of B_s read from the transposed sign table;
+// reconstruct (dense bf16) - the decoded records put in tile order (prefix
+//            counts of the bitmap words give each record tile its rank), then
+//            one streaming pass over every weight.
+#include <type_traits>
+
 #include "awsrc_internal.h"
 
 namespace awsrc {
 
 constexpr int kLdsModules = 256;  // module tables up to this size are staged in LDS
+
+#define HIP_RETURN_IF(expr)            \
+  do {                                 \
+    const hipError_t e_ = (expr);      \
+    if (e_ != hipSuccess) return e_;   \
+  } while (0)
 
 struct Rec {
   uint64_t idx;
@@ -86,20 +97,25 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n) {
     p[i] = 0u;
 }
 
-__global__ void k_decode_validate(DecodeArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.K) return;
-  const Rec r = parse(a, i);
+// field checks of one record (everything but a repeated tile)
+__device__ __forceinline__ bool record_fields_ok(const DecodeArgs& a, const Rec& r) {
   const int qmax = (1 << (a.b - 1)) - 1;
   bool bad = r.idx >= a.T_total || r.seed >= (uint32_t)a.S;
   for (int p = 0; p < a.P; ++p) bad |= r.q[p] < -qmax || r.q[p] > qmax;
   // fp16 scale: negative, inf or NaN; every 8-bit exponent is valid
   if (a.scale_fmt != AWSRC_SCALE_POW2) bad |= (r.scale & 0x8000u) != 0 || (r.scale & 0x7C00u) == 0x7C00u;
+  return !bad;
+}
+
+__global__ void k_decode_validate(DecodeArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.K) return;
+  const Rec r = parse(a, i);
+  bool bad = !record_fields_ok(a, r);
   if (!bad) {
     const uint32_t bit = 1u << (r.idx & 31);
     const uint32_t old = atomicOr(&a.bitmap[r.idx >> 5], bit);
     bad = (old & bit) != 0;
-    a.tmap[r.idx] = (uint32_t)i;
   }
   if (bad) atomicAdd(a.errors, 1ull);
   // decoded form for the apply pass (only used once the whole stream is valid)
@@ -117,6 +133,98 @@ __global__ void k_decode_validate(DecodeArgs a) {
   a.dec[2 * i] = make_uint4((uint32_t)(r.idx - a.mod_tile_off[lo]), (uint32_t)lo, r.seed | (r.scale << 16),
                             (uint32_t)tot);
   a.dec[2 * i + 1] = make_uint4(qw[0], qw[1], qw[2], qw[3]);
+}
+
+// ---------------------------------------------------------------- bitmap prefix counts
+constexpr int kScanWords = 16;                    // bitmap words per thread
+constexpr int kScanThreads = 256;
+constexpr int kScanBlockWords = kScanWords * kScanThreads;
+
+// exclusive scan over the NT threads of a block; *total gets the block sum
+template <int NT>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_wave[wv] = x;
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    const uint32_t t = s_wave[w];
+    before += w < wv ? t : 0u;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
+}
+
+__device__ __forceinline__ uint32_t thread_word_count(const uint32_t* bitmap, int64_t nw, int64_t w0) {
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < kScanWords; ++k)
+    if (w0 + k < nw) c += __popc(bitmap[w0 + k]);
+  return c;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_sums(DecodeArgs a, int64_t nw) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  const int64_t w0 = (int64_t)blockIdx.x * kScanBlockWords + (int64_t)threadIdx.x * kScanWords;
+  uint32_t tot;
+  block_exclusive_scan<kScanThreads>(thread_word_count(a.bitmap, nw, w0), s_wave, &tot);
+  if (threadIdx.x == 0) a.bsum[blockIdx.x] = tot;
+}
+
+// one block: exclusive scan of the per-block sums, in place
+__global__ __launch_bounds__(1024) void k_scan_top(DecodeArgs a, int64_t nb) {
+  __shared__ uint32_t s_wave[16];
+  uint32_t carry = 0;
+  for (int64_t i0 = 0; i0 < nb; i0 += 1024) {
+    const int64_t i = i0 + threadIdx.x;
+    const uint32_t v = i < nb ? a.bsum[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan<1024>(v, s_wave, &tot);
+    if (i < nb) a.bsum[i] = carry + ex;
+    carry += tot;
+  }
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_words(DecodeArgs a, int64_t nw) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  const int64_t w0 = (int64_t)blockIdx.x * kScanBlockWords + (int64_t)threadIdx.x * kScanWords;
+  uint32_t tot;
+  uint32_t run = a.bsum[blockIdx.x] +
+                 block_exclusive_scan<kScanThreads>(thread_word_count(a.bitmap, nw, w0), s_wave, &tot);
+#pragma unroll
+  for (int k = 0; k < kScanWords; ++k) {
+    if (w0 + k < nw) {
+      const uint32_t word = a.bitmap[w0 + k];
+      a.pre[w0 + k] = run;
+      run += __popc(word);
+    }
+  }
+}
+
+// rank of record tile t among all record tiles (tile order)
+__device__ __forceinline__ uint32_t tile_rank(const DecodeArgs& a, uint64_t t) {
+  const uint32_t word = a.bitmap[t >> 5];
+  return a.pre[t >> 5] + __popc(word & ((1u << (t & 31)) - 1u));
+}
+
+// decoded record i (stream order) copied to its tile-order rank
+__global__ void k_decode_tile_order(DecodeArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.K) return;
+  const uint4 e0 = a.dec[2 * i];
+  const uint4 e1 = a.dec[2 * i + 1];
+  const uint32_t k = tile_rank(a, a.mod_tile_off[e0.y] + e0.x);
+  a.dec_t[2 * (size_t)k] = e0;
+  a.dec_t[2 * (size_t)k + 1] = e1;
 }
 
 // C/8 lanes per record, eight consecutive weights per lane.  With integer
@@ -193,12 +301,21 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------- dense bf16 reconstruction
-// One streaming pass over every weight of every module.  Lanes own 16
-// consecutive weights: 8 bytes of codes in, 32 bytes of bf16 out, W0 =
+// One streaming pass over every weight of every module.  Lanes own units of
+// kUnitW consecutive weights (kUnitW / 2 bytes of codes in, 2 kUnitW bytes of
+// bf16 out, consecutive lanes on consecutive units), W0 =
 // f32(q - z) * s recomputed from the backbone.  A lane whose tile has a record
-// (bit set in the validation bitmap) finds it through the tile -> record map
-// and adds its 16 corrections before the single rounding to bf16, so record
-// tiles cost no extra pass over the backbone or the output.
+// (bit set in the validation bitmap) reads it at the tile's rank in the
+// tile-ordered decoded records (a coalesced read: neighbouring lanes' records
+// are neighbours) and adds its corrections before the single rounding to
+// bf16.  The sign table sits in LDS when it fits.
+//
+// The loop is software-pipelined over the block's chunks so that no wait on
+// a load also waits on the stores just issued (loads and stores share one
+// in-order counter): in the iteration that computes chunk c it issues the
+// backbone loads of chunk c + step, the bitmap words of chunk c + 2 step and
+// the decoded records of chunk c + step (whose bitmap words arrived one
+// iteration earlier), and only then computes and stores chunk c.
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -208,159 +325,275 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));  // nearest even
 }
 
-// Corrections of 16 consecutive coordinates (rows sub*16 .. sub*16+15 of
-// B_s) of record i, added onto w.  With integer codes, sqrt(C) rhat_j is the
-// scale times sum_p q_p minus twice the codes at the negative entries of row
-// j, the latter one int8 dot product per four codes against a 0/1 byte mask
-// spread from the row's sign bits.
-template <int C, int G>
-__device__ __forceinline__ void add_record16(const DecodeArgs& a, uint32_t i, int sub, float (&w)[16]) {
-  constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
-                      : (C == 64) ? 0.125f : 0.08838834764831845f;
-  const uint4 e0 = a.dec[2 * (size_t)i];
-  const uint4 e1 = a.dec[2 * (size_t)i + 1];
-  const uint32_t q4[4] = {e1.x, e1.y, e1.z, e1.w};
-  const uint4* tsp = reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC + sub * 16);
-  const uint4 ta = tsp[0], tb = tsp[1];
-  const uint32_t tw[8] = {ta.x, ta.y, ta.z, ta.w, tb.x, tb.y, tb.z, tb.w};
-  const uint32_t sfield = e0.z >> 16;
-  const float scl = a.scale_fmt == AWSRC_SCALE_POW2 ? ldexpf(isq, (int)sfield - 128)
-                                                    : __half2float(__ushort_as_half((uint16_t)sfield)) * isq;
-  const int32_t tot = (int32_t)e0.w;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const uint32_t ts = (tw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-    int32_t neg = 0;
-#pragma unroll
-    for (int gg = 0; gg < G; ++gg) {
-      const uint32_t mask = (((ts >> (4 * gg)) & 0xFu) * 0x204081u) & 0x01010101u;
-      neg = __builtin_amdgcn_sdot4((int)mask, (int)q4[gg], neg, false);
-    }
-    w[e] += (float)(tot - 2 * neg) * scl;
-  }
-}
-
 // global-address-space views: loads and stores through them are issued as
 // global (not flat) memory instructions
 #define AWSRC_GLOBAL __attribute__((address_space(1)))
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-template <int C, int G>
-__global__ __launch_bounds__(256) void k_reconstruct(DecodeArgs a, BackboneTabs bb) {
-  constexpr int UPT = C / 16;                            // lanes per tile
-  constexpr int LOG_UPT = (C == 16) ? 0 : (C == 32) ? 1 : (C == 64) ? 2 : 3;
-  constexpr int NU = 4;                                  // units per lane per block iteration
-  constexpr int CHUNK = NU * 256;
-  __shared__ uint64_t s_off[kLdsModules + 1];
-  const bool lds_tab = a.n_modules <= kLdsModules;
-  if (lds_tab)
-    for (int m = threadIdx.x; m <= a.n_modules; m += 256) s_off[m] = a.mod_tile_off[m];
-  __syncthreads();
-  const uint64_t* off = lds_tab ? s_off : a.mod_tile_off;
-  const uint64_t n_units = a.T_total << LOG_UPT;
-  // per-lane module state, kept in registers; units only move forward, so
-  // the module walk costs at most n_modules steps per lane over the launch
-  int m = 0;
-  uint64_t m_lo = 0, m_hi = off[1] << LOG_UPT;
-  int64_t cols = a.mod_cols[0];
-  uint32_t upr = (uint32_t)(cols >> 4), gpr = (uint32_t)(cols >> bb.gshift);
-  const AWSRC_GLOBAL uint8_t* cp = (const AWSRC_GLOBAL uint8_t*)bb.codes[0];
-  const AWSRC_GLOBAL uint16_t* sp = (const AWSRC_GLOBAL uint16_t*)bb.scale[0];
-  const AWSRC_GLOBAL uint8_t* zp = (const AWSRC_GLOBAL uint8_t*)bb.zero[0];
-  AWSRC_GLOBAL uint16_t* op = (AWSRC_GLOBAL uint16_t*)a.mod_ptr[0];
-  for (uint64_t c0 = (uint64_t)blockIdx.x * CHUNK; c0 < n_units; c0 += (uint64_t)gridDim.x * CHUNK) {
-    // addresses of this lane's NU units, then all their loads, then the math
-    const AWSRC_GLOBAL u32x2_t* qa[NU];
-    const AWSRC_GLOBAL uint16_t* sa[NU];
-    const AWSRC_GLOBAL uint8_t* za[NU];
-    AWSRC_GLOBAL u32x4_t* oa[NU];
-    uint64_t tt[NU];
-    int sub[NU];
-    bool ok[NU];
-#pragma unroll
-    for (int k = 0; k < NU; ++k) {
-      const uint64_t u = c0 + k * 256 + threadIdx.x;
-      ok[k] = u < n_units;
-      if (ok[k] && u >= m_hi) {
-        do { ++m; } while ((off[m + 1] << LOG_UPT) <= u);
-        m_lo = off[m] << LOG_UPT;
-        m_hi = off[m + 1] << LOG_UPT;
-        cols = a.mod_cols[m];
-        upr = (uint32_t)(cols >> 4);
-        gpr = (uint32_t)(cols >> bb.gshift);
-        cp = (const AWSRC_GLOBAL uint8_t*)bb.codes[m];
-        sp = (const AWSRC_GLOBAL uint16_t*)bb.scale[m];
-        zp = (const AWSRC_GLOBAL uint8_t*)bb.zero[m];
-        op = (AWSRC_GLOBAL uint16_t*)a.mod_ptr[m];
-      }
-      const uint32_t uw = (uint32_t)(u - m_lo);          // unit within the module
-      const uint32_t row = uw / upr;
-      const uint32_t col0 = (uw - row * upr) * 16;
-      const int64_t el = (int64_t)row * cols + col0;
-      const uint32_t g = row * gpr + (col0 >> bb.gshift);
-      qa[k] = (const AWSRC_GLOBAL u32x2_t*)(cp + (el >> 1));
-      sa[k] = sp + g;
-      za[k] = zp + g;
-      oa[k] = (AWSRC_GLOBAL u32x4_t*)(op + el);
-      tt[k] = u >> LOG_UPT;
-      sub[k] = (int)(uw & (UPT - 1));
-    }
-    u32x2_t q16[NU];
-    uint32_t sraw[NU], zraw[NU], bits[NU];
-#pragma unroll
-    for (int k = 0; k < NU; ++k) {
-      if (ok[k]) {
-        q16[k] = *qa[k];
-        sraw[k] = *sa[k];
-        zraw[k] = *za[k];
-        bits[k] = a.bitmap[tt[k] >> 5];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < NU; ++k) {
-      if (!ok[k]) continue;
-      const float s = __half2float(__ushort_as_half((uint16_t)sraw[k]));
-      const float z = (float)zraw[k];
-      float w[16];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        w[e] = ((float)((q16[k].x >> (4 * e)) & 0xFu) - z) * s;
-        w[8 + e] = ((float)((q16[k].y >> (4 * e)) & 0xFu) - z) * s;
-      }
-      if ((bits[k] >> (tt[k] & 31)) & 1u) add_record16<C, G>(a, a.tmap[tt[k]], sub[k], w);
-      const u32x4_t lo = {bf16_pair(w[0], w[1]), bf16_pair(w[2], w[3]), bf16_pair(w[4], w[5]),
-                          bf16_pair(w[6], w[7])};
-      const u32x4_t hi = {bf16_pair(w[8], w[9]), bf16_pair(w[10], w[11]), bf16_pair(w[12], w[13]),
-                          bf16_pair(w[14], w[15])};
-      oa[k][0] = lo;
-      oa[k][1] = hi;
+constexpr int kRecThreads = 512;
+constexpr int kUnitW = 16;                   // weights per unit (8 or 16)
+constexpr int kLogUnitW = kUnitW == 16 ? 4 : 3;
+constexpr int kRecUnits = 2;                 // units per lane per chunk
+constexpr int kTsignLdsMax = 64 * 1024;      // sign tables up to this size are staged in LDS
+// the codes of one unit: kUnitW / 2 bytes
+using UnitCodes = std::conditional<kUnitW == 16, u32x2_t, uint32_t>::type;
+
+__device__ __forceinline__ uint32_t code_word(const u32x2_t& q, int i) { return q[i]; }
+__device__ __forceinline__ uint32_t code_word(const uint32_t& q, int) { return q; }
+
+template <int NU>
+struct RecBackbone {                         // backbone words of one chunk
+  UnitCodes q[NU];
+  uint32_t s[NU], z[NU];
+  AWSRC_GLOBAL u32x4_t* out[NU];
+  bool ok[NU];
+};
+template <int NU>
+struct RecBits {                             // bitmap word and its prefix count per unit
+  uint32_t word[NU], pre[NU];
+};
+template <int NU, int G>
+struct RecDec {                              // decoded record per unit (record 0 when none)
+  u32x2_t sw[NU];                            // seed | scale << 16, sum of codes
+  // the codes, four per word; only the words in use are loaded, so that no
+  // dead part of a load destination is ever reused while the load is in flight
+  typename std::conditional<(G <= 2), u32x2_t, u32x4_t>::type q[NU];
+  bool rec[NU];
+};
+
+// One launch covers a window of at most kLdsModules consecutive modules,
+// whose table rows (tile offset, codes, scale, zero and output pointers) are
+// staged in LDS, so that the per-lane module walk never waits on the
+// vector-memory counter.  Unit uw of a module covers its elements
+// [16 uw, 16 uw + 16) (rows are whole multiples of the group, hence of 16),
+// and its backbone group is element / group.  Every load is issued unconditionally (units
+// past the window end are clamped to its last unit and not stored).
+template <int C, int G, bool TS_LDS>
+__global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, BackboneTabs bb, int m0, int nm) {
+  constexpr int NT = kRecThreads, NU = kRecUnits;
+  constexpr int UPT = C / kUnitW;                        // lanes per tile
+  constexpr int LOG_UPT = ((C == 16) ? 4 : (C == 32) ? 5 : (C == 64) ? 6 : 7) - kLogUnitW;
+  constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
+                      : (C == 64) ? 0.125f : 0.08838834764831845f;
+  extern __shared__ __align__(16) uint64_t s_dyn[];
+  // LDS: [tile offsets nm+1 | codes nm | scale nm | zero nm | out nm] then [S][C] sign rows
+  uint64_t* s_off = s_dyn;
+  uint64_t* s_cp = s_off + nm + 1;
+  uint64_t* s_sp = s_cp + nm;
+  uint64_t* s_zp = s_sp + nm;
+  uint64_t* s_op = s_zp + nm;
+  uint16_t* s_ts = reinterpret_cast<uint16_t*>(s_dyn + ((5 * nm + 1 + 1) & ~1));
+  const uint32_t n_all = (uint32_t)a.n_modules;
+  for (int i = threadIdx.x; i <= nm; i += NT) s_off[i] = a.mod_tile_off[m0 + i];
+  for (int i = threadIdx.x; i < nm; i += NT) {
+    s_cp[i] = bb.ptr[m0 + i];
+    s_sp[i] = bb.ptr[n_all + m0 + i];
+    s_zp[i] = bb.ptr[2 * n_all + m0 + i];
+    s_op[i] = reinterpret_cast<uint64_t>(a.mod_ptr[m0 + i]);
+  }
+  if constexpr (TS_LDS) {
+    constexpr int PER_SEED = C / 8;                      // 16-byte pieces per seed
+    for (int i = threadIdx.x; i < a.S * PER_SEED; i += NT) {
+      const int sd = i / PER_SEED, j = i - sd * PER_SEED;
+      reinterpret_cast<uint4*>(s_ts)[i] = reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)sd * kMaxC)[j];
     }
   }
+  __syncthreads();
+  const uint64_t u_begin = s_off[0] << LOG_UPT, u_end = s_off[nm] << LOG_UPT;
+  const uint64_t CH = (uint64_t)NU * NT;
+  const uint64_t step = (uint64_t)gridDim.x * CH;
+  const uint64_t c0 = u_begin + (uint64_t)blockIdx.x * CH;
+
+  // per-lane module state for the backbone loads; their units only move
+  // forward, so the walk costs at most nm steps per lane per launch
+  int m = 0;
+  uint64_t m_lo = u_begin, m_hi = s_off[1] << LOG_UPT;
+
+  auto issue_backbone = [&](uint64_t c, RecBackbone<NU>& B) {
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
+      B.ok[k] = u < u_end;
+      u = B.ok[k] ? u : u_end - 1;
+      if (u >= m_hi) {
+        do { ++m; } while ((s_off[m + 1] << LOG_UPT) <= u);
+        m_lo = s_off[m] << LOG_UPT;
+        m_hi = s_off[m + 1] << LOG_UPT;
+      }
+      const uint64_t el = (u - m_lo) << kLogUnitW;       // first element of the unit
+      const uint64_t g = el >> bb.gshift;
+      B.q[k] = *((const AWSRC_GLOBAL UnitCodes*)s_cp[m] + (el >> kLogUnitW));
+      B.s[k] = ((const AWSRC_GLOBAL uint16_t*)s_sp[m])[g];
+      B.z[k] = ((const AWSRC_GLOBAL uint8_t*)s_zp[m])[g];
+      B.out[k] = (AWSRC_GLOBAL u32x4_t*)s_op[m] + (el >> 3);
+    }
+  };
+  auto issue_bits = [&](uint64_t c, RecBits<NU>& W) {
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
+      u = u < u_end ? u : u_end - 1;
+      const uint64_t w = u >> (LOG_UPT + 5);
+      W.word[k] = a.bitmap[w];
+      W.pre[k] = a.pre[w];
+    }
+  };
+  auto issue_dec = [&](uint64_t c, const RecBits<NU>& W, RecDec<NU, G>& D) {
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
+      const uint32_t sh = (uint32_t)(u >> LOG_UPT) & 31u;
+      D.rec[k] = (W.word[k] >> sh) & 1u;
+      const uint32_t r = D.rec[k] ? W.pre[k] + __popc(W.word[k] & ((1u << sh) - 1u)) : 0u;
+      const uint32_t* dp = reinterpret_cast<const uint32_t*>(a.dec_t) + 8 * (size_t)r;
+      D.sw[k] = *reinterpret_cast<const u32x2_t*>(dp + 2);
+      using QT = typename std::remove_reference<decltype(D.q[0])>::type;
+      D.q[k] = *reinterpret_cast<const QT*>(dp + 4);
+    }
+  };
+  auto compute = [&](uint64_t c, const RecBackbone<NU>& B, const RecDec<NU, G>& D) {
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      if (!B.ok[k]) continue;
+      const uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
+      const float s = __half2float(__ushort_as_half((uint16_t)B.s[k]));
+      const float z = (float)B.z[k];
+      float w[kUnitW];
+#pragma unroll
+      for (int e = 0; e < kUnitW; ++e)
+        w[e] = ((float)((code_word(B.q[k], e >> 3) >> (4 * (e & 7))) & 0xFu) - z) * s;
+      if (D.rec[k]) {
+        // rows sub*kUnitW .. of B_s: sqrt(C) rhat_j = scale (sum_p q_p - 2 sum
+        // of the codes at the negative entries of row j)
+        const int sub = (int)(u & (UPT - 1));
+        const uint32_t sd = D.sw[k].x & 0xFFFFu;
+        const uint4* trow;
+        if constexpr (TS_LDS)
+          trow = reinterpret_cast<const uint4*>(s_ts + (size_t)sd * C + sub * kUnitW);
+        else
+          trow = reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)sd * kMaxC + sub * kUnitW);
+        uint32_t tw[kUnitW / 2];
+#pragma unroll
+        for (int i = 0; i < kUnitW / 8; ++i) {
+          const uint4 t4 = trow[i];
+          tw[4 * i] = t4.x; tw[4 * i + 1] = t4.y; tw[4 * i + 2] = t4.z; tw[4 * i + 3] = t4.w;
+        }
+        uint32_t q4[4] = {D.q[k][0], D.q[k][1], 0u, 0u};
+        if constexpr (G > 2) {
+          q4[2] = D.q[k][2];
+          q4[3] = D.q[k][3];
+        }
+        const uint32_t sfield = D.sw[k].x >> 16;
+        const float scl = a.scale_fmt == AWSRC_SCALE_POW2 ? ldexpf(isq, (int)sfield - 128)
+                                                          : __half2float(__ushort_as_half((uint16_t)sfield)) * isq;
+        const int32_t tot = (int32_t)D.sw[k].y;
+#pragma unroll
+        for (int e = 0; e < kUnitW; ++e) {
+          const uint32_t ts = (tw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+          int32_t neg = 0;
+#pragma unroll
+          for (int gg = 0; gg < G; ++gg) {
+            const uint32_t mask = (((ts >> (4 * gg)) & 0xFu) * 0x204081u) & 0x01010101u;
+            neg = __builtin_amdgcn_sdot4((int)mask, (int)q4[gg], neg, false);
+          }
+          w[e] += (float)(tot - 2 * neg) * scl;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kUnitW / 8; ++i) {
+        const u32x4_t o = {bf16_pair(w[8 * i], w[8 * i + 1]), bf16_pair(w[8 * i + 2], w[8 * i + 3]),
+                           bf16_pair(w[8 * i + 4], w[8 * i + 5]), bf16_pair(w[8 * i + 6], w[8 * i + 7])};
+        B.out[k][i] = o;
+      }
+    }
+  };
+
+  // two alternating register sets for the backbone words and the records,
+  // so that nothing in flight is ever copied; the bitmap words of chunk
+  // c + step are consumed (record loads) before the words of c + 2 step are
+  // loaded into the same registers
+  RecBackbone<NU> B0, B1;
+  RecBits<NU> W;
+  RecDec<NU, G> D0, D1;
+  issue_bits(c0, W);
+  issue_backbone(c0, B0);
+  issue_dec(c0, W, D0);
+  issue_bits(c0 + step, W);
+  for (uint64_t c = c0; c < u_end; c += 2 * step) {
+    issue_backbone(c + step, B1);
+    issue_dec(c + step, W, D1);
+    issue_bits(c + 2 * step, W);
+    compute(c, B0, D0);
+    if (c + step >= u_end) break;
+    issue_backbone(c + 2 * step, B0);
+    issue_dec(c + 2 * step, W, D0);
+    issue_bits(c + 3 * step, W);
+    compute(c + step, B1, D1);
+  }
+}
+
+// dynamic LDS of one launch: module window table (rounded to 16 bytes) and
+// the sign rows when staged
+static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds) {
+  return (size_t)((5 * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
+}
+
+template <int C, int G, bool TS_LDS>
+static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
+  for (int m0 = 0; m0 < a.n_modules; m0 += kLdsModules) {
+    const int nm = a.n_modules - m0 < kLdsModules ? a.n_modules - m0 : kLdsModules;
+    const size_t lds = rec_lds_bytes(C, a.S, nm, TS_LDS);
+    int per_cu = 0;
+    HIP_RETURN_IF(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS>, kRecThreads, lds));
+    if (per_cu < 1) per_cu = 1;
+    const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / kUnitW);
+    const uint64_t chunks = (units + kRecUnits * kRecThreads - 1) / (kRecUnits * kRecThreads);
+    uint64_t nb = (uint64_t)per_cu * 256;                // resident blocks, grid-stride beyond
+    if (nb > chunks) nb = chunks;
+    if (nb < 1) continue;
+    hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb, m0, nm);
+    HIP_RETURN_IF(hipGetLastError());
+  }
+  return hipSuccess;
+}
+
+template <int C, int G>
+static hipError_t launch_rec_cg(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
+  if ((size_t)a.S * C * 2 <= (size_t)kTsignLdsMax) return launch_rec_cgt<C, G, true>(a, bb, toff, st);
+  return launch_rec_cgt<C, G, false>(a, bb, toff, st);
 }
 
 template <int C>
-static void launch_rec_c(const DecodeArgs& a, const BackboneTabs& bb, unsigned nb, hipStream_t st) {
+static hipError_t launch_rec_c(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
   switch ((a.P + 3) / 4) {
-    case 1: hipLaunchKernelGGL((k_reconstruct<C, 1>), dim3(nb), dim3(256), 0, st, a, bb); break;
-    case 2: hipLaunchKernelGGL((k_reconstruct<C, 2>), dim3(nb), dim3(256), 0, st, a, bb); break;
-    case 3: hipLaunchKernelGGL((k_reconstruct<C, 3>), dim3(nb), dim3(256), 0, st, a, bb); break;
-    default: hipLaunchKernelGGL((k_reconstruct<C, 4>), dim3(nb), dim3(256), 0, st, a, bb); break;
+    case 1: return launch_rec_cg<C, 1>(a, bb, toff, st);
+    case 2: return launch_rec_cg<C, 2>(a, bb, toff, st);
+    case 3: return launch_rec_cg<C, 3>(a, bb, toff, st);
+    default: return launch_rec_cg<C, 4>(a, bb, toff, st);
   }
 }
 
-hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, hipStream_t st) {
-  const uint64_t n_units = a.T_total * (uint64_t)(a.C / 16);
-  uint64_t nb = (n_units + 1023) / 1024;
-  if (nb > 256 * 8) nb = 256 * 8;  // eight resident blocks per CU, grid-stride beyond
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff,
+                                   hipStream_t st) {
+  if (a.K > 0) {
+    // the records in tile order: prefix counts of the bitmap words, then each
+    // decoded record copied to its rank
+    const int64_t nwords = (int64_t)((a.T_total + 31) / 32);
+    const int64_t nb = (nwords + kScanBlockWords - 1) / kScanBlockWords;
+    hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)nb), dim3(kScanThreads), 0, st, a, nwords);
+    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(1024), 0, st, a, nb);
+    hipLaunchKernelGGL(k_scan_words, dim3((unsigned)nb), dim3(kScanThreads), 0, st, a, nwords);
+    hipLaunchKernelGGL(k_decode_tile_order, dim3((unsigned)((a.K + 255) / 256)), dim3(256), 0, st, a);
+    HIP_RETURN_IF(hipGetLastError());
+  }
   switch (a.C) {
-    case 16: launch_rec_c<16>(a, bb, (unsigned)nb, st); break;
-    case 32: launch_rec_c<32>(a, bb, (unsigned)nb, st); break;
-    case 64: launch_rec_c<64>(a, bb, (unsigned)nb, st); break;
-    case 128: launch_rec_c<128>(a, bb, (unsigned)nb, st); break;
+    case 16: return launch_rec_c<16>(a, bb, toff, st);
+    case 32: return launch_rec_c<32>(a, bb, toff, st);
+    case 64: return launch_rec_c<64>(a, bb, toff, st);
+    case 128: return launch_rec_c<128>(a, bb, toff, st);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {
