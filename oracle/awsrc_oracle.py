@@ -136,6 +136,21 @@ def gen_basis(key: int, s: int, C: int, P: int) -> Tuple[np.ndarray, List[int]]:
     return sigma, cols
 
 
+def gen_permutation(key: int, s: int, C: int, P: int) -> np.ndarray:
+    """Seeded coordinate permutation of generator version 2 (the permutation of
+    Eq. (2)'s basis, Sec. 3.1): coordinate j draws the sort key word
+    ceil(C/64) + P + j of seed s (after the sign and column words), and
+    pi(j) is the rank of (key_j, j) in increasing order.  Ranking independent
+    uniform keys gives a uniform permutation (the random-keys shuffle)."""
+    n_sign_words = (C + 63) // 64
+    keys = [basis_word(key, s, n_sign_words + P + j) for j in range(C)]
+    order = sorted(range(C), key=lambda j: (keys[j], j))
+    pi = np.empty(C, dtype=np.int64)
+    for r, j in enumerate(order):
+        pi[j] = r
+    return pi
+
+
 def hadamard(C: int) -> np.ndarray:
     """Order-C Sylvester Hadamard matrix in natural order (integer entries +-1)."""
     return _hadamard(C).copy()
@@ -152,11 +167,16 @@ def _hadamard(C: int) -> np.ndarray:
     return H
 
 
-def basis_matrix(key: int, s: int, C: int, P: int) -> np.ndarray:
-    """B_s in R^{C x P}: B[j, p] = sigma_j H[j, c_p] / sqrt(C) (Eq. (2))."""
+def basis_matrix(key: int, s: int, C: int, P: int, gen_version: int = 1) -> np.ndarray:
+    """B_s in R^{C x P} (Eq. (2)): B[j, p] = sigma_j H[pi(j), c_p] / sqrt(C),
+    with pi the identity for generator version 1 and the seeded coordinate
+    permutation for version 2 (signs and columns are the same words in both)."""
+    if gen_version not in (1, 2):
+        raise ValueError("unsupported generator version")
     sigma, cols = gen_basis(key, s, C, P)
     H = _hadamard(C)
-    return (sigma[:, None] * H[:, cols]).astype(np.float64) / math.sqrt(C)
+    rows = gen_permutation(key, s, C, P) if gen_version == 2 else np.arange(C)
+    return (sigma[:, None] * H[rows][:, cols]).astype(np.float64) / math.sqrt(C)
 
 
 # --------------------------------------------------------------------------
@@ -369,7 +389,7 @@ def encode_tiles(R: np.ndarray, Dw: np.ndarray, params: Params,
     P = params.P
     qmax = params.qmax
     if bases is None:
-        bases = [basis_matrix(params.basis_key, s, C, P) for s in range(params.S)]
+        bases = [basis_matrix(params.basis_key, s, C, P, params.gen_version) for s in range(params.S)]
     n_seeds = len(bases)
     best_gain = np.full(N, -np.inf)
     second_gain = np.full(N, -np.inf)
@@ -417,7 +437,7 @@ def encode_tiles(R: np.ndarray, Dw: np.ndarray, params: Params,
 
 def candidate(R_t: np.ndarray, D_t: np.ndarray, params: Params, s: int):
     """The full encoder chain for one (tile, seed): (codes, scale bits, gain, alpha*)."""
-    B = basis_matrix(params.basis_key, s, R_t.shape[0], params.P)
+    B = basis_matrix(params.basis_key, s, R_t.shape[0], params.P, params.gen_version)
     alpha, _, _ = fit(R_t[None].astype(np.float64), D_t[None].astype(np.float64), B, params.ridge_lambda)
     q, bits, sc = quantize(alpha, params.b, params.scale_fmt)
     g = weighted_gain(R_t[None].astype(np.float64), D_t[None].astype(np.float64), (sc[:, None] * q) @ B.T)
@@ -540,7 +560,8 @@ def parse_header(stream: bytes):
         raise ValueError("not an AWSRC stream")
     mods = [struct.unpack_from("<II", stream, HEADER_FIXED_BYTES + 8 * i) for i in range(n_mod)]
     h = header_bytes(n_mod)
-    return {"flags": flags, "scale_fmt": (flags >> 4) & 0xF, "C": C, "P": P, "b": b, "S": S,
+    return {"flags": flags, "gen_version": flags & 0xF, "scale_fmt": (flags >> 4) & 0xF, "C": C, "P": P,
+            "b": b, "S": S,
             "idx_bits": ib, "seed_bits": sb, "scale_bits": scb, "L_rec": L, "basis_key": key,
             "T_total": T_total, "modules": mods, "h": h}
 
@@ -620,7 +641,7 @@ def decode_add(stream: bytes, W0_list: Sequence[np.ndarray]) -> List[np.ndarray]
         local = t - offsets[mi]
         row, blk = divmod(int(local), c_ // C)
         if s not in cache:
-            cache[s] = basis_matrix(hd["basis_key"], s, C, P)
+            cache[s] = basis_matrix(hd["basis_key"], s, C, P, hd["gen_version"])
         if hd["scale_fmt"] == SCALE_POW2:
             sc = math.ldexp(1.0, int(s16) - POW2_BIAS)
         else:

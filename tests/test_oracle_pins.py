@@ -66,6 +66,53 @@ def test_gen_basis_full_selection_is_permutation():
         assert sorted(cols) == list(range(16))
 
 
+# ---------------------------------------------------------------- generator version 2
+def test_gen_v2_worked_example():
+    g = read_golden("gen_v2_key0_s0_C4_P1.txt")
+    sigma, cols = O.gen_basis(0, 0, 4, 1)
+    assert [int(x) for x in g["sigma"]] == list(sigma) and cols == [int(c) for c in g["columns"]]
+    assert list(O.gen_permutation(0, 0, 4, 1)) == [int(x) for x in g["perm"]]
+    B = O.basis_matrix(0, 0, 4, 1, gen_version=2)
+    assert np.array_equal(B[:, 0] * 2, np.array([int(x) for x in g["basis_col0_times2"]], dtype=float))
+
+
+@pytest.mark.parametrize("C,P", [(4, 2), (16, 4), (64, 8), (128, 8), (128, 16)])
+def test_gen_v2_is_v1_with_permuted_hadamard_rows(C, P):
+    """Signs and columns are version 1's words; the permutation is a bijection
+    of the coordinates; B[j, p] sigma_j sqrt(C) = H[pi(j), c_p]; columns stay
+    orthonormal."""
+    H = O.hadamard(C)
+    for s in range(12):
+        sigma, cols = O.gen_basis(11, s, C, P)
+        pi = O.gen_permutation(11, s, C, P)
+        assert sorted(pi) == list(range(C))
+        B2 = O.basis_matrix(11, s, C, P, gen_version=2)
+        B1 = O.basis_matrix(11, s, C, P, gen_version=1)
+        assert np.array_equal(B1 * math.sqrt(C) * sigma[:, None], H[:, cols].astype(float))
+        assert np.allclose(B2 * math.sqrt(C) * sigma[:, None], H[pi][:, cols], atol=1e-12)
+        assert np.allclose(B2.T @ B2, np.eye(P), atol=1e-12)
+
+
+def test_gen_v2_permutation_uniform_and_independent_of_the_columns():
+    """C = 4, P = 1: over 48,000 seeds every one of the 24 permutations is
+    equally likely, and the permutation is independent of the column draw
+    (chi-square at p = 1e-6); a shuffle that reused or overlapped the column
+    and sign words, or a biased shuffle, fails one of these."""
+    from scipy.stats import chi2
+    perms = {p: i for i, p in enumerate(itertools.permutations(range(4)))}
+    n = 48000
+    joint = np.zeros((4, 24))
+    for s in range(n):
+        _, cols = O.gen_basis(5, s, 4, 1)
+        joint[cols[0], perms[tuple(O.gen_permutation(5, s, 4, 1))]] += 1
+    marg = joint.sum(axis=0)
+    x2 = float(np.sum((marg - n / 24) ** 2 / (n / 24)))
+    assert x2 < chi2.ppf(1 - 1e-6, 23)
+    expect = np.outer(joint.sum(axis=1), marg) / n
+    x2j = float(np.sum((joint - expect) ** 2 / expect))
+    assert x2j < chi2.ppf(1 - 1e-6, 3 * 23)
+
+
 # ---------------------------------------------------------------- Hadamard
 @pytest.mark.parametrize("C", [1, 2, 4, 8, 16, 32, 64, 128])
 def test_hadamard_orthogonal(C):
@@ -473,11 +520,13 @@ def _encode_module(W, d, p):
     return W0, enc
 
 
-def test_prefix_decodability_every_prefix():
+@pytest.mark.parametrize("gen_version", [1, 2])
+def test_prefix_decodability_every_prefix(gen_version):
     """Every record-boundary prefix decodes against the same W0: the weighted
-    error drops by exactly the listed gains, and the empty prefix is W0 itself."""
+    error drops by exactly the listed gains, and the empty prefix is W0 itself
+    (the decoder regenerates the bases of the generator the header names)."""
     W, d = _small_module()
-    p = O.Params(C=64, P=4, b=4, S=16)
+    p = O.Params(C=64, P=4, b=4, S=16, gen_version=gen_version)
     W0, enc = _encode_module(W, d, p)
     stream, K, n_elig = O.build_stream(p, [W.shape], enc, bpw=8.0, per_module=False)
     h = O.header_bytes(1)
