@@ -64,15 +64,19 @@ def measured_traffic(kernel: str, workload: str):
     return e["bytes"] if h.hexdigest() == e["sha256"] else None
 
 
-def ops_per_candidate(C: int, P: int, per_element: bool) -> float:
+def ops_per_candidate(C: int, P: int, per_element: bool, gen_version: int = 1) -> float:
     """Algorithmic fp32 operations per (tile, seed): projection (cheapest of the
     direct P*C form and a length-C fast Walsh-Hadamard transform), solve with a
     precomputed factor, quantization and the coefficient-space score; per-element
-    weights add the Gram gather and a P x P Cholesky factorization."""
+    weights add the Gram gather and a P x P Cholesky factorization, and with the
+    seeded coordinate permutation (generator version 2) also the transform of
+    the permuted weights that the Gram gather then reads."""
     proj = min(P * C, C * int(math.log2(C)))
     ops = proj + 2 * P * P + 6 * P + 9
     if per_element:
         ops += P * (P + 1) / 2 + P ** 3 / 6 + P * P / 2 + P / 3
+        if gen_version != 1:
+            ops += C * int(math.log2(C))
     return float(ops)
 
 
@@ -205,6 +209,8 @@ def main() -> int:
     ap.add_argument("--decode-workload", default="stack3b",
                     help="workload whose shapes size the at-scale decode-add measurement ('' to skip)")
     ap.add_argument("--decode-bpw", type=float, default=0.32)
+    ap.add_argument("--gen-version", type=int, default=1, choices=(1, 2),
+                    help="basis generator version (2 adds the seeded coordinate permutation)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         log("bench.py measures a single GPU: the codec has no cross-GPU step "
@@ -220,7 +226,7 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                          idx_bits=wl.idx_bits)
+                          idx_bits=wl.idx_bits, gen_version=args.gen_version)
     mods = wl.modules
     log(f"[bench] workload {wl.name}: {len(mods)} module(s), {wl.n_weights} weights, T={wl.n_tiles}, S={wl.S}")
     inputs = [gen_module_inputs(wl, m, dev) for m in mods]
@@ -287,7 +293,7 @@ def main() -> int:
     value = cand / (ms_step / 1e3)
 
     per_elem = wl.d_mode == "elem"
-    opc = ops_per_candidate(wl.C, wl.P, per_elem)
+    opc = ops_per_candidate(wl.C, wl.P, per_elem, args.gen_version)
     enc_s = stage_ms["encode"] / 1e3
     achieved = cand * opc / enc_s / 1e12
     K, L = last["K"], last["L"]
@@ -303,10 +309,11 @@ def main() -> int:
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": wl.name, "modules": [f"{r}x{c}" for r, c in shapes], "C": wl.C, "P": wl.P,
                    "b": wl.b, "S": wl.S, "weights": wl.d_mode, "mode": wl.mode, "bpw": bpw, "tiles": T,
-                   "candidates": cand},
+                   "candidates": cand, "generator": args.gen_version},
         "roofline": {"bound": "alu", "kernel": "awsrc_encode_tiles (basis, factors, screen, finalize)",
                      "achieved": achieved, "peak": PEAK_VALU_TOPS, "unit": "Tops/s",
-                     "frac": achieved / PEAK_VALU_TOPS, "traffic": measured_traffic("encode", wl.name),
+                     "frac": achieved / PEAK_VALU_TOPS,
+                     "traffic": measured_traffic("encode", wl.name) if args.gen_version == 1 else None,
                      "traffic_unit": "bytes per launch", "ops_per_candidate": opc},
         "encode_candidates_per_s": cand / enc_s,
         "decode_add": {"records": K, "bytes": dec_bytes, "ms": stage_ms["decode_apply"], "GB/s": dec_gbs,

@@ -88,8 +88,15 @@ enum { AWSRC_SCALE_FP16 = 0, AWSRC_SCALE_POW2 = 1 };
  *               (word i of seed s is output s*2^32 + i; sign j is bit j%64 of
  *               word j/64; column p maps word ceil(C/64)+p into [0, C-p) by the
  *               multiply-shift of its high 32 bits and takes the m-th smallest
- *               column not yet drawn).  Eq. (2) with the seeded coordinate
- *               permutation of Sec. 3.1 left out.
+ *               column not yet drawn).  Eq. (2) without the seeded
+ *               coordinate permutation.
+ *               2: B_s[j, p] = sigma_j H_C[pi_s(j), c_p] / sqrt(C), the same
+ *               signs and columns plus the seeded coordinate permutation of
+ *               Eq. (2) / Sec. 3.1: coordinate j draws word ceil(C/64)+P+j and
+ *               pi_s(j) is the rank of (word, j) in increasing order.  With
+ *               per-element weights version 2 runs on the vector screen (the
+ *               Gram entries need a transform of the permuted weights per
+ *               seed); per-column weights keep the matrix-core screen.
  *  reserved     must be 0.
  *  basis_key    generator key, stored in the stream header.
  *  ridge_lambda eps_t = ridge_lambda * mean_j d_{t,j} in Eq. (3); >= 0.

@@ -50,8 +50,8 @@ class awsrc_decode_plan(ctypes.Structure):
 
 
 def make_params(C: int, P: int, b: int, S: int, basis_key: int = 0, ridge_lambda: float = 1e-6,
-                idx_bits: int = 32, scale_fmt: int = AWSRC_SCALE_FP16) -> awsrc_params:
-    return awsrc_params(C, P, b, S, scale_fmt, idx_bits, 1, 0, basis_key, ridge_lambda)
+                idx_bits: int = 32, scale_fmt: int = AWSRC_SCALE_FP16, gen_version: int = 1) -> awsrc_params:
+    return awsrc_params(C, P, b, S, scale_fmt, idx_bits, gen_version, 0, basis_key, ridge_lambda)
 
 
 def _load() -> ctypes.CDLL:

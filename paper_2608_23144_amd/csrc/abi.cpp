@@ -50,7 +50,7 @@ awsrc_status check_params(const awsrc_params* p) {
   if (p->scale_fmt != AWSRC_SCALE_FP16 && p->scale_fmt != AWSRC_SCALE_POW2)
     return fail(AWSRC_EINVAL, "scale_fmt=%d unsupported", p->scale_fmt);
   if (p->idx_bits < 0 || p->idx_bits > 32) return fail(AWSRC_EINVAL, "idx_bits=%d out of range 0..32", p->idx_bits);
-  if (p->gen_version != 1) return fail(AWSRC_EINVAL, "gen_version=%d unsupported", p->gen_version);
+  if (p->gen_version != 1 && p->gen_version != 2) return fail(AWSRC_EINVAL, "gen_version=%d unsupported", p->gen_version);
   if (p->reserved != 0) return fail(AWSRC_EINVAL, "reserved field must be 0");
   if (!(p->ridge_lambda >= 0.0) || !isfinite(p->ridge_lambda)) return fail(AWSRC_EINVAL, "ridge_lambda must be finite and >= 0");
   return AWSRC_OK;
@@ -140,8 +140,8 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
   const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
-  const size_t b_frag = screen_mfma_supported(p->C, p->P, d_mode) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
-  const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode);
+  const size_t b_frag = screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
+  const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
   const size_t need = b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
@@ -158,6 +158,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.rows = rows; a.cols = cols; a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
   a.lambda = p->ridge_lambda;
   a.scale_fmt = p->scale_fmt;
+  a.gen_version = p->gen_version;
   a.basis = carve_basis(ws, p->S, p->P);
   ws += b_basis;
   a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
@@ -173,7 +174,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
   hipStream_t s = (hipStream_t)stream;
-  HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, a.basis, s));
+  HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
   if (d_mode == AWSRC_D_PER_COL) HIPCHK(launch_col_factors(a, s));
   HIPCHK(launch_encode_screen(a, s));
   HIPCHK(launch_encode_finalize(a, s));
@@ -287,28 +288,27 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
 // ---------------------------------------------------------------- decode
 namespace {
 
-// Workspace: basis tables | tile bitmap | error counter | module tables
+// Workspace: basis tables | tile bitmap with prefix counts | error counter | module tables
 // (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
 // host-to-device copy fills them) | decoded records [K] x 32 B | for the bf16
-// reconstruction: the records in tile order [K + 1] x 32 B, prefix counts of
-// the bitmap words and their scan scratch, backbone pointer tables [3n].
+// reconstruction: the records in tile order [K + 1] x 32 B, the prefix-count
+// scan scratch, backbone pointer tables [3n].
 struct DecodeLayout {
-  size_t basis, bitmap, err, tables, dec, dec_t, pre, bsum, bbtab, total;
+  size_t basis, bitmap, err, tables, dec, dec_t, bsum, bbtab, total;
 };
 
 DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_t K) {
   DecodeLayout l;
   l.basis = align_up(basis_bytes(S, P), 256);
-  l.bitmap = align_up((size_t)((T_total + 31) / 32) * 4, 256);
+  l.bitmap = align_up((size_t)((T_total + 31) / 32) * 8, 256);
   l.err = 256;
   l.tables = align_up((size_t)(3 * nmod + 1) * 8, 256);
   l.dec = align_up((size_t)K * 32, 256);
   l.dec_t = align_up((size_t)(K + 1) * 32, 256);  // entry 0 is readable even when K = 0
   const size_t nwords = (size_t)((T_total + 31) / 32);
-  l.pre = align_up(nwords * 4, 256);
   l.bsum = align_up(((nwords + 4095) / 4096) * 4, 256);
   l.bbtab = align_up((size_t)3 * nmod * 8, 256);
-  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.dec_t + l.pre + l.bsum + l.bbtab;
+  l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.dec_t + l.bsum + l.bbtab;
   return l;
 }
 
@@ -336,7 +336,6 @@ DecodeArgs decode_args(const awsrc_decode_plan* pl) {
   a.dec = reinterpret_cast<uint4*>(ws);
   ws += l.dec;
   a.dec_t = reinterpret_cast<uint4*>(ws); ws += l.dec_t;
-  a.pre = reinterpret_cast<uint32_t*>(ws); ws += l.pre;
   a.bsum = reinterpret_cast<uint32_t*>(ws);
   return a;
 }
@@ -369,7 +368,8 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   const uint64_t T_total = get_le(fx + 28, 8);
   const uint32_t nmod = (uint32_t)get_le(fx + 36, 4);
   const int sfmt = (int)((flags >> 4) & 0xF);
-  if ((flags & 0xF) != 1 || (sfmt != AWSRC_SCALE_FP16 && sfmt != AWSRC_SCALE_POW2) || (flags & ~0x1FFu))
+  const int gen = (int)(flags & 0xF);
+  if ((gen != 1 && gen != 2) || (sfmt != AWSRC_SCALE_FP16 && sfmt != AWSRC_SCALE_POW2) || (flags & ~0x1FFu))
     return fail(AWSRC_ECORRUPT, "bad flags 0x%x", flags);
   if (!pow2_c(C) || P < 1 || P > kMaxP || P > C || b < 2 || b > 8 || S < 2 || S > 65536)
     return fail(AWSRC_ECORRUPT, "bad codec parameters in header");
@@ -417,7 +417,7 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   const DecodeArgs a = decode_args(&pl);
   memcpy(tabs.data() + 2 * (size_t)nmod + 1, W0_ptrs, nmod * sizeof(void*));
   HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), tabs.data(), tabs.size() * 8, hipMemcpyHostToDevice, s));
-  HIPCHK(launch_gen_basis(key, C, P, (int)S, a.basis, s));
+  HIPCHK(launch_gen_basis(key, C, P, (int)S, gen, a.basis, s));
   HIPCHK(launch_decode_validate(a, s));
   unsigned long long nerr = 0;
   HIPCHK(hipMemcpyAsync(&nerr, a.errors, 8, hipMemcpyDeviceToHost, s));

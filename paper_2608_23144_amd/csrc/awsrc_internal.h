@@ -34,13 +34,16 @@ struct BasisTables {
   uint64_t* mask;
   uint8_t* col;
   uint16_t* tsign;
+  uint8_t* perm;   // [S][kMaxC] pi(j) (generator version 2)
+  uint8_t* iperm;  // [S][kMaxC] pi^-1(i) (generator version 2)
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline size_t basis_bytes(int S, int P) {
   return align_up((size_t)S * 2 * 8, 256) + align_up((size_t)S * P * 2 * 8, 256) +
-         align_up((size_t)S * kMaxP, 256) + align_up((size_t)S * kMaxC * 2, 256);
+         align_up((size_t)S * kMaxP, 256) + align_up((size_t)S * kMaxC * 2, 256) +
+         2 * align_up((size_t)S * kMaxC, 256);
 }
 
 inline BasisTables carve_basis(void* base, int S, int P) {
@@ -53,6 +56,10 @@ inline BasisTables carve_basis(void* base, int S, int P) {
   t.col = reinterpret_cast<uint8_t*>(p);
   p += align_up((size_t)S * kMaxP, 256);
   t.tsign = reinterpret_cast<uint16_t*>(p);
+  p += align_up((size_t)S * kMaxC * 2, 256);
+  t.perm = reinterpret_cast<uint8_t*>(p);
+  p += align_up((size_t)S * kMaxC, 256);
+  t.iperm = reinterpret_cast<uint8_t*>(p);
   return t;
 }
 
@@ -139,7 +146,9 @@ __device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipSuccess or the first HIP error.
-hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, BasisTables t, hipStream_t st);
+// Basis tables of GenBasis version gen_version (1: signs and columns; 2: also
+// the seeded coordinate permutation, B_s[j, p] = sigma_j H[pi(j), c_p]/sqrt(C)).
+hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, int gen_version, BasisTables t, hipStream_t st);
 
 hipError_t launch_backbone(const void* W, int w_dtype, int64_t rows, int64_t cols, int group,
                            uint8_t* codes, uint16_t* scale, uint8_t* zero, float* W0,
@@ -155,6 +164,7 @@ struct EncodeArgs {
   int C, P, b, S;
   double lambda;
   int scale_fmt;       // AWSRC_SCALE_FP16 or AWSRC_SCALE_POW2
+  int gen_version;     // basis generator version (1 or 2)
   BasisTables basis;
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
   double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
@@ -170,11 +180,13 @@ struct EncodeArgs {
 };
 
 bool encode_supported(int C, int P);
-bool screen_mfma_supported(int C, int P, int d_mode);
+// the matrix-core screens: C = 64 (P <= 8), C = 128 (P <= 8, per-column
+// weights); per-element weights need generator version 1 (XOR Gram gathers)
+bool screen_mfma_supported(int C, int P, int d_mode, int gen_version);
 int factor_pb(int C, int P);                 // padded P of the per-column factor table
 size_t mfma_frag_bytes(int C, int S);
 // Seed ranges per tile for the screen (1 unless the matrix-core screen runs).
-int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode);
+int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode, int gen_version);
 hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st);
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);
@@ -226,14 +238,17 @@ struct DecodeArgs {
   int w0_dtype;
   int scale_fmt;                 // AWSRC_SCALE_FP16 or AWSRC_SCALE_POW2
   BasisTables basis;
-  uint32_t* bitmap;              // [ceil(T_total / 32)]
+  // [ceil(T_total / 32)][2]: bit i of word w marks a record for tile
+  // 32 w + i; the second word of each pair holds the number of record tiles
+  // before word w (filled for the dense reconstruction), so that one 8-byte
+  // read gives a tile's rank
+  uint32_t* bitmap;
   unsigned long long* errors;    // [1]
   // [K][2] decoded records written by validation: {tile within module,
   // module, seed | scale << 16, sum of codes}, then the P codes as int8 (zero
   // padded to 16)
   uint4* dec;
   uint4* dec_t;                  // [K + 1][2] the same records in tile order (reconstruction)
-  uint32_t* pre;                 // [ceil(T_total / 32)] record tiles before each bitmap word
   uint32_t* bsum;                // [ceil(words / 4096)] scan scratch
 };
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st);

@@ -1,4 +1,4 @@
-// Seeded basis tables, GenBasis(s, C, P) of Eq. (2), generator version 1.
+// Seeded basis tables, GenBasis(s, C, P) of Eq. (2).
 //
 // One thread per seed draws the sign words and the P distinct Hadamard
 // columns from the splitmix64 counter stream and precomputes, for every
@@ -6,6 +6,11 @@
 // (sigma_j xor parity(j & c_p)), which the encoder and decoder kernels use
 // instead of regenerating the basis per tile; a second kernel transposes the
 // patterns into one u16 of P sign bits per coordinate for the decoder.
+// Generator version 2 adds the seeded coordinate permutation
+// B_s[j, p] = sigma_j H[pi(j), c_p] / sqrt(C): one wavefront per seed draws a
+// sort key per coordinate (the words after the column words), ranks them
+// (pi(j) = rank of (key_j, j)), and builds the negative-entry patterns
+// sigma_j xor parity(pi(j) & c_p) by wavefront ballots.
 #include "awsrc_internal.h"
 
 namespace awsrc {
@@ -37,7 +42,7 @@ __device__ __forceinline__ uint64_t hadamard_neg_word(int c, int w) {
   return x;
 }
 
-__global__ void k_gen_basis(uint64_t key, int C, int P, int S, uint64_t* __restrict__ sign,
+__global__ void k_gen_basis(uint64_t key, int C, int P, int S, int gen_version, uint64_t* __restrict__ sign,
                             uint64_t* __restrict__ mask, uint8_t* __restrict__ col) {
   const int s = blockIdx.x * blockDim.x + threadIdx.x;
   if (s >= S) return;
@@ -61,6 +66,7 @@ __global__ void k_gen_basis(uint64_t key, int C, int P, int S, uint64_t* __restr
     else c = 64 + nth_zero(used[1], m - z0, 64);
     used[c >> 6] |= 1ull << (c & 63);
     col[(size_t)s * kMaxP + p] = (uint8_t)c;
+    if (gen_version != 1) continue;  // version 2: k_basis_perm builds the patterns
     for (int w = 0; w < 2; ++w) {
       uint64_t mk = 0ull;
       if (w < nw) mk = (hadamard_neg_word(c, w) ^ sw[w]) & (w == 0 ? valid0 : ~0ull);
@@ -82,11 +88,46 @@ __global__ void k_basis_tsign(int C, int P, int S, const uint64_t* __restrict__ 
   tsign[(size_t)s * kMaxC + j] = (uint16_t)t;
 }
 
-hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, BasisTables t, hipStream_t st) {
+// Version 2: one wavefront per seed, lane j (and j + 64) owns coordinate j.
+__global__ __launch_bounds__(64) void k_basis_perm(uint64_t key, int C, int P, BasisTables t) {
+  __shared__ uint64_t s_key[kMaxC];
+  const int s = blockIdx.x;
+  const int nw = (C + 63) / 64;
+  const uint64_t base = ((uint64_t)s << 32) + (uint64_t)(nw + P);
+  for (int j = threadIdx.x; j < C; j += 64) s_key[j] = splitmix64(key, base + (uint64_t)j);
+  __syncthreads();
+  const uint64_t sw0 = t.sign[2 * (size_t)s], sw1 = t.sign[2 * (size_t)s + 1];
+  for (int h = 0; h < nw; ++h) {
+    const int j = threadIdx.x + 64 * h;
+    const bool on = j < C;
+    int rank = 0;
+    if (on) {
+      const uint64_t kj = s_key[j];
+      for (int i = 0; i < C; ++i) {
+        const uint64_t ki = s_key[i];
+        rank += (ki < kj) || (ki == kj && i < j);
+      }
+      t.perm[(size_t)s * kMaxC + j] = (uint8_t)rank;
+      t.iperm[(size_t)s * kMaxC + rank] = (uint8_t)j;
+    }
+    const uint64_t sg = ((h == 0 ? sw0 : sw1) >> (j & 63)) & 1ull;
+    for (int p = 0; p < P; ++p) {
+      const int c = t.col[(size_t)s * kMaxP + p];
+      const bool neg = on && ((sg ^ (uint64_t)(__popc((unsigned)(rank & c)) & 1)) != 0);
+      const uint64_t word = __ballot(neg);
+      if (threadIdx.x == 0) t.mask[((size_t)s * P + p) * 2 + h] = word;
+    }
+  }
+  if (nw == 1 && threadIdx.x == 0)
+    for (int p = 0; p < P; ++p) t.mask[((size_t)s * P + p) * 2 + 1] = 0ull;
+}
+
+hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, int gen_version, BasisTables t, hipStream_t st) {
   const int threads = 64;
   const int blocks = (S + threads - 1) / threads;
-  hipLaunchKernelGGL(k_gen_basis, dim3(blocks), dim3(threads), 0, st, key, C, P, S, t.sign, t.mask,
-                     t.col);
+  hipLaunchKernelGGL(k_gen_basis, dim3(blocks), dim3(threads), 0, st, key, C, P, S, gen_version, t.sign,
+                     t.mask, t.col);
+  if (gen_version == 2) hipLaunchKernelGGL(k_basis_perm, dim3((unsigned)S), dim3(64), 0, st, key, C, P, t);
   const int64_t n = (int64_t)S * C;
   hipLaunchKernelGGL(k_basis_tsign, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, C, P, S,
                      t.mask, t.tsign);

@@ -21,6 +21,9 @@ namespace awsrc {
 
 constexpr int kLdsModules = 256;  // module tables up to this size are staged in LDS
 
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 #define HIP_RETURN_IF(expr)            \
   do {                                 \
     const hipError_t e_ = (expr);      \
@@ -114,7 +117,7 @@ __global__ void k_decode_validate(DecodeArgs a) {
   bool bad = !record_fields_ok(a, r);
   if (!bad) {
     const uint32_t bit = 1u << (r.idx & 31);
-    const uint32_t old = atomicOr(&a.bitmap[r.idx >> 5], bit);
+    const uint32_t old = atomicOr(&a.bitmap[2 * (r.idx >> 5)], bit);
     bad = (old & bit) != 0;
   }
   if (bad) atomicAdd(a.errors, 1ull);
@@ -168,7 +171,7 @@ __device__ __forceinline__ uint32_t thread_word_count(const uint32_t* bitmap, in
   uint32_t c = 0;
 #pragma unroll
   for (int k = 0; k < kScanWords; ++k)
-    if (w0 + k < nw) c += __popc(bitmap[w0 + k]);
+    if (w0 + k < nw) c += __popc(bitmap[2 * (w0 + k)]);
   return c;
 }
 
@@ -203,8 +206,8 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_words(DecodeArgs a, int64
 #pragma unroll
   for (int k = 0; k < kScanWords; ++k) {
     if (w0 + k < nw) {
-      const uint32_t word = a.bitmap[w0 + k];
-      a.pre[w0 + k] = run;
+      const uint32_t word = a.bitmap[2 * (w0 + k)];
+      a.bitmap[2 * (w0 + k) + 1] = run;
       run += __popc(word);
     }
   }
@@ -212,8 +215,8 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_words(DecodeArgs a, int64
 
 // rank of record tile t among all record tiles (tile order)
 __device__ __forceinline__ uint32_t tile_rank(const DecodeArgs& a, uint64_t t) {
-  const uint32_t word = a.bitmap[t >> 5];
-  return a.pre[t >> 5] + __popc(word & ((1u << (t & 31)) - 1u));
+  const u32x2_t wp = *reinterpret_cast<const u32x2_t*>(a.bitmap + 2 * (t >> 5));
+  return wp.y + __popc(wp.x & ((1u << (t & 31)) - 1u));
 }
 
 // decoded record i (stream order) copied to its tile-order rank
@@ -328,8 +331,6 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
 // global-address-space views: loads and stores through them are issued as
 // global (not flat) memory instructions
 #define AWSRC_GLOBAL __attribute__((address_space(1)))
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRecThreads = 512;
 constexpr int kUnitW = 16;                   // weights per unit (8 or 16)
@@ -435,8 +436,9 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
       u = u < u_end ? u : u_end - 1;
       const uint64_t w = u >> (LOG_UPT + 5);
-      W.word[k] = a.bitmap[w];
-      W.pre[k] = a.pre[w];
+      const u32x2_t wp = *reinterpret_cast<const u32x2_t*>(a.bitmap + 2 * w);
+      W.word[k] = wp.x;
+      W.pre[k] = wp.y;
     }
   };
   auto issue_dec = [&](uint64_t c, const RecBits<NU>& W, RecDec<NU, G>& D) {
@@ -601,7 +603,7 @@ hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {
   int64_t fb = (nwords + 255) / 256;
   if (fb > 4096) fb = 4096;
   if (fb < 1) fb = 1;
-  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)fb), dim3(256), 0, st, a.bitmap, nwords);
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)fb), dim3(256), 0, st, a.bitmap, 2 * nwords);
   hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, st, reinterpret_cast<uint32_t*>(a.errors), (int64_t)2);
   if (a.K > 0)
     hipLaunchKernelGGL(k_decode_validate, dim3((unsigned)((a.K + 255) / 256)), dim3(256), 0, st, a);

@@ -89,25 +89,64 @@ __global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __res
 //   [packed lower L (PB(PB+1)/2)] [1/L_pp (PB)] [eps]
 // Padding columns p >= P get an identity row so that the padded system solves
 // to alpha_p = 0.
+// Generator version 2 permutes the coordinates, so the XOR identity no longer
+// applies: G_pq = (sum_j d_j - 2 sum of d_j where B_s[j, p] and B_s[j, q]
+// differ in sign) / C, from the negative-entry patterns and the block's d
+// staged in LDS.  Grid: (seed groups of 64, column blocks).
 template <int C, int PB>
-__global__ void k_col_factors(EncodeArgs a, int nb, int stride) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= nb * a.S) return;
-  const int blk = idx / a.S;
-  const int s = idx - blk * a.S;
-  const double* wd = a.wd64 + (int64_t)blk * C;  // WHT(d) of this block: G_pq = wd[c_p ^ c_q] / C
+__global__ __launch_bounds__(64) void k_col_factors(EncodeArgs a, int nb, int stride) {
+  __shared__ double sd[C];
+  const int blk = blockIdx.y;
+  const int s = blockIdx.x * 64 + threadIdx.x;
+  if (a.gen_version != 1) {
+    for (int j = threadIdx.x; j < C; j += 64) sd[j] = (double)a.d[(int64_t)blk * C + j];
+    __syncthreads();
+  }
+  if (s >= a.S) return;
+  const int64_t idx = (int64_t)blk * a.S + s;
   const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
-  const double eps = a.lambda * (wd[0] / C);
   double G[PB][PB];
+  if (a.gen_version == 1) {
+    const double* wd = a.wd64 + (int64_t)blk * C;  // WHT(d) of this block: G_pq = wd[c_p ^ c_q] / C
+    const double eps = a.lambda * (wd[0] / C);
 #pragma unroll
-  for (int p = 0; p < PB; ++p)
+    for (int p = 0; p < PB; ++p)
 #pragma unroll
-    for (int q = 0; q <= p; ++q) {
-      double g;
-      if (p < a.P && q < a.P) g = wd[cs[p] ^ cs[q]] / C + (p == q ? eps : 0.0);
-      else g = (p == q) ? 1.0 : 0.0;
-      G[p][q] = g;
-    }
+      for (int q = 0; q <= p; ++q) {
+        double g;
+        if (p < a.P && q < a.P) g = wd[cs[p] ^ cs[q]] / C + (p == q ? eps : 0.0);
+        else g = (p == q) ? 1.0 : 0.0;
+        G[p][q] = g;
+      }
+  } else {
+    double sum = 0.0;
+    for (int j = 0; j < C; ++j) sum += sd[j];
+    const double eps = a.lambda * (sum / C);
+    const uint64_t* mk = a.basis.mask + (size_t)s * a.P * 2;
+#pragma unroll
+    for (int p = 0; p < PB; ++p)
+#pragma unroll
+      for (int q = 0; q <= p; ++q) {
+        double g;
+        if (p < a.P && q < a.P) {
+          double acc = sum;
+          if (p != q) {
+            double diff = 0.0;
+#pragma unroll
+            for (int w = 0; w < (C + 63) / 64; ++w) {
+              const uint64_t x = mk[2 * p + w] ^ mk[2 * q + w];
+              for (int j = 0; j < (C < 64 ? C : 64); ++j)
+                if ((x >> j) & 1ull) diff += sd[64 * w + j];
+            }
+            acc -= 2.0 * diff;
+          }
+          g = acc / C + (p == q ? eps : 0.0);
+        } else {
+          g = (p == q) ? 1.0 : 0.0;
+        }
+        G[p][q] = g;
+      }
+  }
   // LDL^T (G is SPD: d > 0 and the columns are orthonormal)
   double L[PB][PB], e[PB];
 #pragma unroll
@@ -138,8 +177,11 @@ __global__ void k_col_factors(EncodeArgs a, int nb, int stride) {
 // fp32 screen of all seeds.  Wavefront = 64 consecutive rows of one column
 // block; lane = tile.  Keeps the kTop best (gain, seed) per tile, ties to the
 // lower seed.
-template <int C, int PB, bool PE>
+template <int C, int PB, bool PE, bool V2>
 __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
+  // generator version 2 with per-element weights: each seed's Gram comes
+  // from the transform of its permuted d, gathered from the lane's raw d row
+  __shared__ float s_draw[V2 ? 64 * (C + 1) : 1];
   const int nb = (int)(a.cols / C);
   const int blk = blockIdx.x % nb;
   const int64_t row = (int64_t)(blockIdx.x / nb) * 64 + threadIdx.x;
@@ -154,9 +196,10 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
     const float r = load_w_any(a.W, a.w_dtype, off + j) - a.W0[off + j];
     const float dj = PE ? a.d[off + j] : a.d[(int64_t)blk * C + j];
     u[j] = dj * r;
-    if constexpr (PE) wd[j] = dj;
+    if constexpr (PE && V2) s_draw[threadIdx.x * (C + 1) + j] = dj;
+    else if constexpr (PE) wd[j] = dj;
   }
-  if constexpr (PE) fwht<C>(wd);
+  if constexpr (PE && !V2) fwht<C>(wd);
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
   const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
@@ -191,6 +234,13 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
       int c[PB];
 #pragma unroll
       for (int p = 0; p < PB; ++p) c[p] = (p < P) ? cs[p] : 0;
+      if constexpr (V2) {
+        // WHT(d o pi^-1): coordinate i of the permuted vector is d at pi^-1(i)
+        const uint8_t* ip = a.basis.iperm + (size_t)s * kMaxC;
+#pragma unroll
+        for (int i = 0; i < C; ++i) wd[i] = s_draw[threadIdx.x * (C + 1) + ip[i]];
+        fwht<C>(wd);
+      }
       const float eps = (float)a.lambda * wd[0] * invC;
 #pragma unroll
       for (int p = 0; p < PB; ++p)
@@ -404,14 +454,18 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
       double sd_;
       tile_u64<C, PE>(a, off, blk, my, ep, &sd_);
     }
+    const bool v2 = a.gen_version != 1;
+    const uint8_t* ip = a.basis.iperm + (size_t)s * kMaxC;  // pi^-1 (generator version 2)
     {
       double v[C];
       const uint64_t s0 = sw[0], s1 = sw[1];
 #pragma unroll
-      for (int j = 0; j < C; ++j) {
+      for (int i = 0; i < C; ++i) {
+        // version 2: coordinate i of the permuted vector is sigma_j u_j at j = pi^-1(i)
+        const int j = v2 ? (int)ip[i] : i;
         const double u = my[j];
         const uint64_t sg = (j < 64) ? (s0 >> j) : (s1 >> (j - 64));
-        v[j] = (sg & 1ull) ? -u : u;
+        v[i] = (sg & 1ull) ? -u : u;
       }
       fwht<C>(v);
 #pragma unroll
@@ -423,7 +477,17 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
     for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? my[c[p]] * isq : 0.0;
     // Gram entries
     const double* wd;
-    if constexpr (PE) {
+    if (v2) {
+      // WHT(d o pi^-1) of this tile's (or column block's) weights
+      const float* dsrc = PE ? a.d + off : a.d + (int64_t)blk * C;
+      double v[C];
+#pragma unroll
+      for (int i = 0; i < C; ++i) v[i] = (double)dsrc[ip[i]];
+      fwht<C>(v);
+#pragma unroll
+      for (int j = 0; j < C; ++j) my[j] = v[j];
+      wd = my;
+    } else if constexpr (PE) {
       double v[C];
 #pragma unroll
       for (int j0 = 0; j0 < C; j0 += 8) {
@@ -541,15 +605,17 @@ bool encode_supported(int C, int P) {
   return (C == 16 || C == 32 || C == 64 || C == 128) && P >= 1 && P <= kMaxP && P <= C;
 }
 
-int factor_pb(int C, int P) { return screen_mfma_supported(C, P, AWSRC_D_PER_COL) ? 8 : pad_p(P); }
+int factor_pb(int C, int P) { return screen_mfma_supported(C, P, AWSRC_D_PER_COL, 1) ? 8 : pad_p(P); }
 
 template <int C, int PB>
 static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
   const int nb = (int)(a.cols / C);
   const int n = nb * a.S;
-  hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
-  hipLaunchKernelGGL((k_col_factors<C, PB>), dim3((n + 63) / 64), dim3(64), 0, st, a, nb,
-                     colfac_stride(PB));
+  (void)n;
+  if (a.gen_version == 1)
+    hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
+  hipLaunchKernelGGL((k_col_factors<C, PB>), dim3((unsigned)((a.S + 63) / 64), (unsigned)nb), dim3(64), 0, st,
+                     a, nb, colfac_stride(PB));
   return hipGetLastError();
 }
 
@@ -557,11 +623,14 @@ template <int C, int PB>
 static hipError_t run_screen(const EncodeArgs& a, hipStream_t st) {
   const int nb = (int)(a.cols / C);
   const int64_t waves = nb * ((a.rows + 63) / 64);
-  if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL((k_screen_valu<C, PB, true>), dim3((unsigned)waves), dim3(64), 0, st, a,
+  if (a.d_mode == AWSRC_D_PER_ELEM && a.gen_version != 1)
+    hipLaunchKernelGGL((k_screen_valu<C, PB, true, true>), dim3((unsigned)waves), dim3(64), 0, st, a,
+                       colfac_stride(PB));
+  else if (a.d_mode == AWSRC_D_PER_ELEM)
+    hipLaunchKernelGGL((k_screen_valu<C, PB, true, false>), dim3((unsigned)waves), dim3(64), 0, st, a,
                        colfac_stride(PB));
   else
-    hipLaunchKernelGGL((k_screen_valu<C, PB, false>), dim3((unsigned)waves), dim3(64), 0, st, a,
+    hipLaunchKernelGGL((k_screen_valu<C, PB, false, false>), dim3((unsigned)waves), dim3(64), 0, st, a,
                        colfac_stride(PB));
   return hipGetLastError();
 }
@@ -609,7 +678,7 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
 #define PBSEL(C_, P_) factor_pb(C_, P_)
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st) { AWSRC_DISPATCH(run_factors, a, st); }
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st) {
-  if (screen_mfma_supported(a.C, a.P, a.d_mode)) return launch_encode_screen_mfma(a, a.frag, st);
+  if (screen_mfma_supported(a.C, a.P, a.d_mode, a.gen_version)) return launch_encode_screen_mfma(a, a.frag, st);
   AWSRC_DISPATCH(run_screen, a, st);
 }
 #undef PBSEL

@@ -486,16 +486,17 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   }
 }
 
-bool screen_mfma_supported(int C, int P, int d_mode) {
+bool screen_mfma_supported(int C, int P, int d_mode, int gen_version) {
   if (P < 1 || P > 8) return false;
+  if (d_mode == AWSRC_D_PER_ELEM && gen_version != 1) return false;
   return C == 64 || (C == 128 && d_mode == AWSRC_D_PER_COL);
 }
 
 // Seed ranges per tile: split only while the module's row groups would leave
 // the machine (about 2048 resident wavefronts at two per SIMD) under-filled,
 // keeping at least 16 seed pairs per range.
-int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode) {
-  if (!screen_mfma_supported(C, P, d_mode)) return 1;
+int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode, int gen_version) {
+  if (!screen_mfma_supported(C, P, d_mode, gen_version)) return 1;
   const int tpw = C == 128 ? 32 : 64;  // rows per wavefront
   const int64_t waves = (cols / C) * ((rows + tpw - 1) / tpw);
   const int pairs = (S + 1) / 2;

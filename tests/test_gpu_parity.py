@@ -29,25 +29,25 @@ def _u16(t):
     return (t.to(torch.int32) & 0xFFFF).cpu().numpy()
 
 
-def _params(wl, fmt=0, **kw):
+def _params(wl, fmt=0, gen=1, **kw):
     return awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                             idx_bits=wl.idx_bits, scale_fmt=fmt, **kw)
+                             idx_bits=wl.idx_bits, scale_fmt=fmt, gen_version=gen, **kw)
 
 
-def _oparams(wl, fmt=0):
+def _oparams(wl, fmt=0, gen=1):
     return O.Params(C=wl.C, P=wl.P, b=wl.b, S=wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                    idx_bits=wl.idx_bits, scale_fmt=fmt)
+                    idx_bits=wl.idx_bits, scale_fmt=fmt, gen_version=gen)
 
 
-def _gpu_module(wl, m, want_alpha=True, fmt=0):
+def _gpu_module(wl, m, want_alpha=True, fmt=0, gen=1):
     inp = gen_module_inputs(wl, m, DEV)
     codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(inp["W"])
-    enc = awsrc.awsrc_encode_tiles(_params(wl, fmt), inp["W"], W0, inp["d"], want_alpha=want_alpha)
+    enc = awsrc.awsrc_encode_tiles(_params(wl, fmt, gen), inp["W"], W0, inp["d"], want_alpha=want_alpha)
     torch.cuda.synchronize()
     return inp, (codes, scale, zero, W0), enc
 
 
-def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx, fmt=0):
+def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx, fmt=0, gen=1):
     """Oracle on a subset of tiles of one module, with every seed's gain kept."""
     W32 = inp["W32"].cpu().numpy()
     d = inp["d"].cpu().numpy()
@@ -55,7 +55,7 @@ def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx, fmt=0):
     assert np.array_equal(W0o, W0_gpu.cpu().numpy())
     R = O.tiles(O.residual(W32, W0o), wl.C)[tiles_idx]
     D = O.tile_weights(d, m.rows, m.cols, wl.C)[tiles_idx]
-    op = _oparams(wl, fmt)
+    op = _oparams(wl, fmt, gen)
     orc = O.encode_tiles(R, D, op, keep_all=True)
     g_seed = _u16(enc["seed"])[tiles_idx]
     g_codes = enc["codes"].cpu().numpy()[tiles_idx]
@@ -161,6 +161,56 @@ def test_encode_pow2_scale(C, P, b, S, rows, cols, d_mode):
     nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T), fmt=1)
     assert nd <= max(1, T // 50)
     assert int(_u16(enc["scale"]).max()) < 256
+
+
+@pytest.mark.parametrize("C,P,b,S,rows,cols,d_mode", [
+    (64, 8, 4, 32, 67, 512, "col"),     # matrix-core screen, factors from the permuted Gram
+    (64, 8, 4, 32, 67, 512, "elem"),    # vector screen: per-seed transform of the permuted d
+    (128, 8, 3, 24, 40, 256, "col"),    # matrix-core C=128 screen
+    (16, 4, 4, 16, 9, 128, "col"),      # vector screen, per-column factors
+    (32, 4, 4, 16, 3, 128, "elem"),
+    (128, 16, 4, 8, 4, 256, "elem"),    # two sign words and two pattern words per column
+])
+def test_encode_generator_v2(C, P, b, S, rows, cols, d_mode):
+    """Basis generator version 2 (seeded coordinate permutation, Eq. (2)) in
+    every screen and the fp64 re-score."""
+    wl = workload("block3b", C=C, P=P, b=b, S=S, d_mode=d_mode)
+    m = Module("t", rows, cols, 0, 4, 4)
+    inp, bb, enc = _gpu_module(wl, m, gen=2)
+    T = rows * cols // C
+    nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T), gen=2)
+    assert nd <= max(1, T // 50)
+
+
+def test_pipeline_generator_v2_matches_oracle():
+    """Version-2 encode, rank and decode against the oracle's stream: the
+    records the GPU ranks are the oracle's where seeds agree, the stream's
+    header names version 2, and the GPU decodes the oracle's stream."""
+    wl = workload("linear256", S=16)
+    m = wl.modules[0]
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m, want_alpha=False, gen=2)
+    p = _params(wl, gen=2)
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_GLOBAL, 2.0, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    stream = bytes(s.cpu().numpy().tobytes())
+    hd = O.parse_header(stream)
+    assert hd["gen_version"] == 2 and K > 0
+    W0n = W0.cpu().numpy()
+    # the oracle decodes the GPU stream exactly as the GPU does (fp32 targets)
+    want = O.decode_add(stream, [W0n])[0]
+    out = W0.clone()
+    awsrc.awsrc_decode_add(s, [out])
+    w0f = W0n.astype(np.float64)
+    assert np.all(np.abs(out.cpu().numpy() - want) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(want - w0f)) + 1e-30)
+    # and the decoded error drops by the GPU's gains of the listed records
+    W32 = inp["W32"].cpu().numpy()
+    d = inp["d"].cpu().numpy()
+    Dfull = np.broadcast_to(d, W32.shape) if d.ndim == 1 else d
+    e0 = O.weighted_error(W32, w0f, Dfull)
+    e1 = O.weighted_error(W32, want, Dfull)
+    gain = enc["gain"].cpu().numpy()
+    order = O.rank_order(gain, np.arange(gain.size))[:K]
+    assert abs((e0 - e1) - float(np.sum(gain[order]))) <= 1e-8 * e0
 
 
 def test_encode_zero_residual_tiles():
