@@ -212,7 +212,7 @@ struct RankWs {
 size_t rank_ws_bytes(size_t n_tiles, size_t k_cap);
 RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap);
 
-constexpr int kStateWords = 16 + 4096;  // rank state: scalars, then the select histogram
+constexpr int kStateWords = 32 + 3 * 4096;  // rank state: scalars, pick states, three select histograms
 hipError_t launch_rank_init(const RankWs& ws, hipStream_t st);
 // Top-K of one tile segment (K = min(cap, eligible), found on the device),
 // ordered by (gain desc, tile asc), packed at the segment's first free record

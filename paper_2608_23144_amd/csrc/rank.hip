@@ -14,10 +14,13 @@
 //     place each item by searches in the other runs of its group;
 //  4. records are bit-packed at fixed offsets h + (first slot of the segment
 //     + i) * L_rec.
-// Reductions that finish a pass (K, the select pick, the compaction scan) run
-// as one-block launches, so cross-block results only pass between launches; a
-// segment is a chain of launches with no host round trip and one read of the
-// totals ends the call.
+// Cross-block results only pass between launches.  Each select pass finishes
+// the previous pass itself: every block repeats the pick of the bin holding
+// the K-th key from the previous histogram (4096 bins, a block scan), so a
+// pass is one launch; histograms rotate over three buffers and the pick
+// state over two, so no launch overwrites what another block of the same
+// launch still reads.  A segment is a chain of launches with no host round
+// trip and one read of the totals ends the call.
 #include "awsrc_internal.h"
 
 namespace awsrc {
@@ -35,12 +38,14 @@ constexpr int kSelBins = 1 << kSelBits;
 
 // Words of RankWs::state.
 enum : int {
-  kPrefix = 0, kMask = 1, kRem = 2, kDone = 3,  // radix select of the current segment
+  kPrefix = 0, kMask = 1, kRem = 2, kDone = 3,  // radix select result of the current segment
   kSegK = 4, kSegOff = 5,                       // records of the segment, its first record slot
   kElig = 6, kArrive = 7,                       // per-launch accumulators, reset after use
   kTotK = 8, kTotElig = 9, kNoSpace = 10,       // totals over the segments of one call
-  kHist = 16                                    // [kSelBins] select histogram
+  kSel = 16,                                    // [2][4] pick state of alternate passes
+  kHist = 32                                    // [3][kSelBins] histograms of rotating passes
 };
+static_assert(kHist + 3 * kSelBins == kStateWords, "rank state size");
 
 // Positive doubles order like their bit patterns; the top (sign) bit is set on
 // eligible keys so that every eligible key exceeds every ineligible (zero) key.
@@ -80,13 +85,12 @@ __global__ void k_rank_init(uint64_t* state) {
 
 // ---------------------------------------------------------------- radix select
 // Each pass histograms the next digit of the keys that match the prefix so
-// far; a one-block pick then moves the prefix into the bin holding the
-// remaining-th largest key and clears the histogram.  When that whole bin is
-// taken the search stops early: every key in it is selected, so the lower
-// digits no longer matter.  Cross-block results only pass between launches.
+// far; the next launch picks the bin holding the remaining-th largest key.
+// When that whole bin is taken the search stops early: every key in it is
+// selected, so the lower digits no longer matter.
 
 // First pass of a segment, fused with the eligibility count: the top digit
-// (eligible flag and exponent) of every key.
+// (eligible flag and exponent) of every key, into histogram 0.
 __global__ __launch_bounds__(kThreads) void k_count_hist(const double* __restrict__ gain, int64_t n,
                                                          uint64_t* state) {
   __shared__ uint32_t h[kSelBins];
@@ -112,35 +116,23 @@ __global__ __launch_bounds__(kThreads) void k_count_hist(const double* __restric
     if (h[b]) atomicAdd((unsigned long long*)&state[kHist + b], (unsigned long long)h[b]);
 }
 
-__global__ __launch_bounds__(kThreads) void k_select_hist(const double* __restrict__ gain, int64_t n,
-                                                          uint64_t* state, int shift, int width) {
-  if (state[kDone]) return;  // uniform: set before this launch
-  __shared__ uint32_t h[kSelBins];
-  for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
-  __syncthreads();
-  const uint64_t prefix = state[kPrefix], mask = state[kMask];
-  const uint64_t dm = (1ull << width) - 1ull;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
-    const uint64_t k = gain_key(gain[i]);
-    if ((k & mask) == prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
-  }
-  __syncthreads();
-  for (int b = threadIdx.x; b < (1 << width); b += kThreads)
-    if (h[b]) atomicAdd((unsigned long long*)&state[kHist + b], (unsigned long long)h[b]);
-}
+struct SelState {
+  uint64_t prefix, mask, rem, done;
+};
 
-// One block of kThreads: thread t owns bpt consecutive bins counted from the top.
-__device__ void pick_bin(uint64_t* state, int shift, int width) {
+// One block of kThreads: the bin of histogram `hist` (digit at `shift`,
+// `width` bits) holding the rem-th largest key; thread t owns bpt consecutive
+// bins counted from the top.  Every thread returns the same state.
+__device__ SelState pick_bin(const uint64_t* hist, SelState in, int shift, int width) {
   __shared__ uint64_t sc[kThreads];
   __shared__ uint64_t found[3];
   const int nbins = 1 << width;
   const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
   const int t = threadIdx.x;
-  const uint64_t rem = state[kRem];
   uint64_t local = 0;
   for (int i = 0; i < bpt; ++i) {
     const int r = t * bpt + i;
-    if (r < nbins) local += state[kHist + (nbins - 1 - r)];
+    if (r < nbins) local += hist[nbins - 1 - r];
   }
   sc[t] = local;
   if (t < 3) found[t] = 0;
@@ -152,61 +144,93 @@ __device__ void pick_bin(uint64_t* state, int shift, int width) {
     __syncthreads();
   }
   const uint64_t excl = sc[t] - local;
-  if (excl < rem && rem <= sc[t]) {
+  if (excl < in.rem && in.rem <= sc[t]) {
     uint64_t cum = excl;
     for (int i = 0; i < bpt; ++i) {
       const int r = t * bpt + i;
       if (r >= nbins) break;
       const int bin = nbins - 1 - r;
-      const uint64_t c = state[kHist + bin];
-      if (cum + c >= rem) {
+      const uint64_t c = hist[bin];
+      if (cum + c >= in.rem) {
         found[0] = (uint64_t)bin;
-        found[1] = rem - cum;
-        found[2] = (c == rem - cum) ? 1ull : 0ull;
+        found[1] = in.rem - cum;
+        found[2] = (c == in.rem - cum) ? 1ull : 0ull;
         break;
       }
       cum += c;
     }
   }
   __syncthreads();
-  if (t == 0) {
-    state[kPrefix] |= found[0] << shift;
-    state[kMask] |= ((1ull << width) - 1ull) << shift;
-    state[kRem] = found[1];
-    state[kDone] = found[2];
-  }
-  for (int b = t; b < nbins; b += kThreads) state[kHist + b] = 0;
+  SelState out;
+  out.prefix = in.prefix | (found[0] << shift);
+  out.mask = in.mask | (((1ull << width) - 1ull) << shift);
+  out.rem = found[1];
+  out.done = found[2];
+  __syncthreads();
+  return out;
 }
 
-__global__ __launch_bounds__(kThreads) void k_select_pick(uint64_t* state, int shift, int width) {
-  if (state[kDone]) return;
-  pick_bin(state, shift, width);
-}
-
-// Segment start (one block): K = min(cap, eligible), the segment's first
-// record slot and the running totals, then the pick of the fused first pass.
-__global__ __launch_bounds__(kThreads) void k_segment_start(uint64_t* state, int64_t cap) {
-  __shared__ uint64_t s_k;
-  if (threadIdx.x == 0) {
+// Pass `pass` (1..5) of a segment: pick from the previous pass's histogram
+// (digit at prev_shift), then histogram the next digit (at shift) of the keys
+// under the new prefix.  Pass 1 forms K = min(cap, eligible) itself.
+__global__ __launch_bounds__(kThreads) void k_select_pass(const double* __restrict__ gain, int64_t n,
+                                                          uint64_t* state, int64_t cap, int pass, int prev_shift,
+                                                          int prev_width, int shift, int width) {
+  __shared__ uint32_t h[kSelBins];
+  SelState cur;
+  if (pass == 1) {
     const uint64_t ne = state[kElig];
     const uint64_t K = ne < (uint64_t)cap ? ne : (uint64_t)cap;
-    state[kSegK] = K;
-    state[kSegOff] = state[kTotK];
-    state[kTotK] += K;
-    state[kTotElig] += ne;
-    state[kElig] = 0;
-    state[kPrefix] = 0;
-    state[kMask] = 0;
-    state[kRem] = K;
-    state[kDone] = K == 0 ? 1 : 0;
-    s_k = K;
+    cur = SelState{0ull, 0ull, K, K == 0 ? 1ull : 0ull};
+    if (blockIdx.x == 0 && threadIdx.x == 0) state[kSegK] = K;
+  } else {
+    const uint64_t* sp = state + kSel + 4 * ((pass - 1) & 1);
+    cur = SelState{sp[0], sp[1], sp[2], sp[3]};
+  }
+  // the histogram two passes back has been read by the previous launch
+  uint64_t* hclr = state + kHist + kSelBins * ((pass + 1) % 3);
+  for (int b = blockIdx.x * kThreads + threadIdx.x; b < kSelBins; b += gridDim.x * kThreads) hclr[b] = 0;
+  SelState nw = cur;
+  if (!cur.done) nw = pick_bin(state + kHist + kSelBins * ((pass - 1) % 3), cur, prev_shift, prev_width);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    uint64_t* so = state + kSel + 4 * (pass & 1);
+    so[0] = nw.prefix; so[1] = nw.mask; so[2] = nw.rem; so[3] = nw.done;
+  }
+  if (nw.done) return;  // uniform
+  for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
+  __syncthreads();
+  const uint64_t dm = (1ull << width) - 1ull;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+    const uint64_t k = gain_key(gain[i]);
+    if ((k & nw.mask) == nw.prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
   }
   __syncthreads();
-  if (s_k) {
-    pick_bin(state, 64 - kSelBits, kSelBits);
-  } else {
-    for (int b = threadIdx.x; b < kSelBins; b += kThreads) state[kHist + b] = 0;
+  uint64_t* hout = state + kHist + kSelBins * (pass % 3);
+  for (int b = threadIdx.x; b < (1 << width); b += kThreads)
+    if (h[b]) atomicAdd((unsigned long long*)&hout[b], (unsigned long long)h[b]);
+}
+
+// Segment end of the select (one block): the last pick, the segment's first
+// record slot and the running totals; leaves every histogram cleared for the
+// next segment.
+__global__ __launch_bounds__(kThreads) void k_select_finish(uint64_t* state, int pass, int prev_shift,
+                                                            int prev_width) {
+  const uint64_t* sp = state + kSel + 4 * ((pass - 1) & 1);
+  SelState cur = SelState{sp[0], sp[1], sp[2], sp[3]};
+  if (!cur.done) cur = pick_bin(state + kHist + kSelBins * ((pass - 1) % 3), cur, prev_shift, prev_width);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint64_t K = state[kSegK];
+    state[kPrefix] = cur.prefix;
+    state[kMask] = cur.mask;
+    state[kRem] = cur.rem;
+    state[kDone] = cur.done;
+    state[kSegOff] = state[kTotK];
+    state[kTotK] += K;
+    state[kTotElig] += state[kElig];
+    state[kElig] = 0;
   }
+  for (int b = threadIdx.x; b < 3 * kSelBins; b += kThreads) state[kHist + b] = 0;
 }
 
 // ---------------------------------------------------------------- compaction
@@ -524,15 +548,15 @@ hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_
   if (cb > 512) cb = 512;
   if (cb < 1) cb = 1;
   hipLaunchKernelGGL(k_count_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state);
-  hipLaunchKernelGGL(k_segment_start, dim3(1), dim3(kThreads), 0, st, ws.state, cap);
+  // passes 1..5 over the digits 12, 12, 12, 12 and 4 bits below the top one
+  const int shifts[6] = {64 - kSelBits, 64 - 2 * kSelBits, 64 - 3 * kSelBits, 64 - 4 * kSelBits, 64 - 5 * kSelBits, 0};
+  const int widths[6] = {kSelBits, kSelBits, kSelBits, kSelBits, kSelBits, 4};
+  for (int pass = 1; pass <= 5; ++pass)
+    hipLaunchKernelGGL(k_select_pass, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state,
+                       (int64_t)(cap > 0 ? cap : 0), pass, shifts[pass - 1], widths[pass - 1], shifts[pass],
+                       widths[pass]);
+  hipLaunchKernelGGL(k_select_finish, dim3(1), dim3(kThreads), 0, st, ws.state, 6, shifts[5], widths[5]);
   if (cap <= 0 || n <= 0) return hipGetLastError();
-  // remaining digits: 12, 12, 12, 12 and 4 bits
-  for (int shift = 64 - 2 * kSelBits; shift >= 0; shift -= kSelBits) {
-    hipLaunchKernelGGL(k_select_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state, shift, kSelBits);
-    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(kThreads), 0, st, ws.state, shift, kSelBits);
-  }
-  hipLaunchKernelGGL(k_select_hist, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state, 0, 4);
-  hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(kThreads), 0, st, ws.state, 0, 4);
   const int64_t nbc = (n + kItems - 1) / kItems;
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state, ws.blk_a, ws.blk_b);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
