@@ -29,7 +29,7 @@ constexpr int kThreads = 256;
 constexpr int kRounds = 16;
 constexpr int kItems = kThreads * kRounds;  // items per block in the compaction
 constexpr int kChunk = 1024;                // items per LDS-sorted chunk
-constexpr int kChunkThreads = 256;
+constexpr int kChunkThreads = 512;
 constexpr int kLogChunk = 10;
 constexpr int kFan = 16;                    // runs per multiway merge
 constexpr int kLogFan = 4;
@@ -124,38 +124,47 @@ struct SelState {
 // `width` bits) holding the rem-th largest key; thread t owns bpt consecutive
 // bins counted from the top.  Every thread returns the same state.
 __device__ SelState pick_bin(const uint64_t* hist, SelState in, int shift, int width) {
-  __shared__ uint64_t sc[kThreads];
+  __shared__ uint64_t s_wave[kThreads / 64];
   __shared__ uint64_t found[3];
+  constexpr int kMaxBpt = kSelBins / kThreads;
   const int nbins = 1 << width;
   const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  // this thread's bins, counted from the top, kept in registers for the search
+  uint64_t v[kMaxBpt];
   uint64_t local = 0;
-  for (int i = 0; i < bpt; ++i) {
+#pragma unroll
+  for (int i = 0; i < kMaxBpt; ++i) {
     const int r = t * bpt + i;
-    if (r < nbins) local += hist[nbins - 1 - r];
+    v[i] = (i < bpt && r < nbins) ? hist[nbins - 1 - r] : 0ull;
+    local += v[i];
   }
-  sc[t] = local;
   if (t < 3) found[t] = 0;
-  __syncthreads();
-  for (int off = 1; off < kThreads; off <<= 1) {
-    const uint64_t v = t >= off ? sc[t - off] : 0;
-    __syncthreads();
-    sc[t] += v;
-    __syncthreads();
+  // inclusive scan: within the wavefront by shuffles, then across the four
+  uint64_t x = local;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
-  const uint64_t excl = sc[t] - local;
-  if (excl < in.rem && in.rem <= sc[t]) {
+  if (lane == 63) s_wave[wv] = x;
+  __syncthreads();
+  uint64_t before = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) before += w < wv ? s_wave[w] : 0ull;
+  const uint64_t incl = before + x;
+  const uint64_t excl = incl - local;
+  if (excl < in.rem && in.rem <= incl) {
     uint64_t cum = excl;
-    for (int i = 0; i < bpt; ++i) {
-      const int r = t * bpt + i;
-      if (r >= nbins) break;
-      const int bin = nbins - 1 - r;
-      const uint64_t c = hist[bin];
-      if (cum + c >= in.rem) {
-        found[0] = (uint64_t)bin;
+    bool hit = false;
+#pragma unroll
+    for (int i = 0; i < kMaxBpt; ++i) {
+      const uint64_t c = v[i];
+      if (!hit && i < bpt && cum + c >= in.rem) {
+        found[0] = (uint64_t)(nbins - 1 - (t * bpt + i));
         found[1] = in.rem - cum;
         found[2] = (c == in.rem - cum) ? 1ull : 0ull;
-        break;
+        hit = true;
       }
       cum += c;
     }
@@ -210,35 +219,34 @@ __global__ __launch_bounds__(kThreads) void k_select_pass(const double* __restri
     if (h[b]) atomicAdd((unsigned long long*)&hout[b], (unsigned long long)h[b]);
 }
 
-// Segment end of the select (one block): the last pick, the segment's first
-// record slot and the running totals; leaves every histogram cleared for the
-// next segment.
-__global__ __launch_bounds__(kThreads) void k_select_finish(uint64_t* state, int pass, int prev_shift,
-                                                            int prev_width) {
-  const uint64_t* sp = state + kSel + 4 * ((pass - 1) & 1);
+// The select result after the last pass (pass 6's pick), as every block of the
+// first compaction launch computes it.
+__device__ SelState final_select(const uint64_t* state) {
+  const uint64_t* sp = state + kSel + 4 * (5 & 1);
   SelState cur = SelState{sp[0], sp[1], sp[2], sp[3]};
-  if (!cur.done) cur = pick_bin(state + kHist + kSelBins * ((pass - 1) % 3), cur, prev_shift, prev_width);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint64_t K = state[kSegK];
-    state[kPrefix] = cur.prefix;
-    state[kMask] = cur.mask;
-    state[kRem] = cur.rem;
-    state[kDone] = cur.done;
+  if (!cur.done) cur = pick_bin(state + kHist + kSelBins * (5 % 3), cur, 0, 4);
+  return cur;
+}
+
+// ---------------------------------------------------------------- compaction
+// Every block finishes the select itself (the last pick); block 0 records the
+// result, the segment's first record slot and the running totals.
+__global__ __launch_bounds__(kThreads) void k_compact_count(const double* __restrict__ gain, int64_t n,
+                                                            uint64_t* state, uint64_t* blk_gt, uint64_t* blk_eq) {
+  const uint64_t K = state[kSegK];
+  const SelState fin = final_select(state);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    state[kPrefix] = fin.prefix;
+    state[kMask] = fin.mask;
+    state[kRem] = fin.rem;
+    state[kDone] = fin.done;
     state[kSegOff] = state[kTotK];
     state[kTotK] += K;
     state[kTotElig] += state[kElig];
     state[kElig] = 0;
   }
-  for (int b = threadIdx.x; b < 3 * kSelBins; b += kThreads) state[kHist + b] = 0;
-}
-
-// ---------------------------------------------------------------- compaction
-__global__ __launch_bounds__(kThreads) void k_compact_count(const double* __restrict__ gain, int64_t n,
-                                                            const uint64_t* __restrict__ state,
-                                                            uint64_t* blk_gt, uint64_t* blk_eq) {
-  if (state[kSegK] == 0) return;  // uniform
-  const uint64_t prefix = state[kPrefix], mask = state[kMask];
+  if (K == 0) return;  // uniform
+  const uint64_t prefix = fin.prefix, mask = fin.mask;
   uint32_t gt = 0, eq = 0;
   const int64_t base = (int64_t)blockIdx.x * kItems;
   for (int r = 0; r < kRounds; ++r) {
@@ -265,43 +273,50 @@ __global__ __launch_bounds__(kThreads) void k_compact_count(const double* __rest
   }
 }
 
+// Inclusive scan over the 1024 threads of a block: shuffles within each
+// wavefront, then the 16 wavefront totals; *total gets the block sum.
+__device__ __forceinline__ uint64_t scan1024(uint64_t v, uint64_t* s_wave, uint64_t* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint64_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_wave[wv] = x;
+  __syncthreads();
+  uint64_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) {
+    const uint64_t t = s_wave[w];
+    before += w < wv ? t : 0ull;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x;
+}
+
 // Single block: eq offsets (exclusive scan of blk_eq) and selected offsets.
 // On exit blk_gt[b] = first output slot of block b, blk_eq[b] = number of
 // equal keys in earlier blocks.
 __global__ __launch_bounds__(1024) void k_compact_scan(uint64_t* blk_gt, uint64_t* blk_eq, int64_t nblk,
-                                                       const uint64_t* __restrict__ state) {
+                                                       uint64_t* state) {
+  // every histogram has been read: leave them cleared for the next segment
+  for (int b = threadIdx.x; b < 3 * kSelBins; b += 1024) state[kHist + b] = 0;
   if (state[kSegK] == 0) return;
-  __shared__ uint64_t sh[1024];
+  __shared__ uint64_t s_wave[16];
   const uint64_t rem = state[kRem];
   uint64_t carry_eq = 0, carry_sel = 0;
   for (int64_t c0 = 0; c0 < nblk; c0 += 1024) {
     const int64_t i = c0 + threadIdx.x;
     const uint64_t gt = i < nblk ? blk_gt[i] : 0, eq = i < nblk ? blk_eq[i] : 0;
-    sh[threadIdx.x] = eq;  // inclusive scan of the equal counts
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-      const uint64_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
-      __syncthreads();
-      sh[threadIdx.x] += v;
-      __syncthreads();
-    }
-    const uint64_t eq_excl = carry_eq + sh[threadIdx.x] - eq;
-    const uint64_t eq_tot = sh[1023];
-    __syncthreads();
+    uint64_t eq_tot, sel_tot;
+    const uint64_t eq_excl = carry_eq + scan1024(eq, s_wave, &eq_tot) - eq;
     uint64_t take_eq = 0;
     if (rem > eq_excl) take_eq = (rem - eq_excl) < eq ? (rem - eq_excl) : eq;
     const uint64_t sel = gt + take_eq;
-    sh[threadIdx.x] = sel;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-      const uint64_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
-      __syncthreads();
-      sh[threadIdx.x] += v;
-      __syncthreads();
-    }
-    const uint64_t sel_excl = carry_sel + sh[threadIdx.x] - sel;
-    const uint64_t sel_tot = sh[1023];
-    __syncthreads();
+    const uint64_t sel_excl = carry_sel + scan1024(sel, s_wave, &sel_tot) - sel;
     if (i < nblk) { blk_gt[i] = sel_excl; blk_eq[i] = eq_excl; }
     carry_eq += eq_tot;
     carry_sel += sel_tot;
@@ -342,6 +357,44 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
   }
 }
 
+// ---------------------------------------------------------------- packing
+struct PackArgs {
+  const uint16_t* seed;
+  const int8_t* code;
+  const uint16_t* scale;
+  int P, b, idx_bits, seed_bits, scale_bits, L;
+  uint64_t h, cap;
+  uint8_t* out;
+};
+
+__device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v, int nbits) {
+  if (nbits <= 0) return;
+  const int o = pos & 63, k = pos >> 6;
+  w[k] |= v << o;
+  if (o + nbits > 64) w[k + 1] |= v >> (64 - o);
+  pos += nbits;
+}
+
+// Record i of the segment (tile t) goes to byte h + (first slot + i) * L of
+// the stream; a stream buffer too small for the running total raises the
+// no-space flag instead.
+__device__ void pack_record(const PackArgs& pa, uint64_t* state, int64_t i, uint32_t t) {
+  const uint64_t K = state[kSegK], off = state[kSegOff];
+  if (pa.h + (off + K) * (uint64_t)pa.L > pa.cap) {
+    if (i == 0) state[kNoSpace] = 1;
+    return;
+  }
+  uint64_t w[3] = {0, 0, 0};
+  int pos = 0;
+  put_bits(w, pos, (uint64_t)t, pa.idx_bits);
+  put_bits(w, pos, (uint64_t)pa.seed[t], pa.seed_bits);
+  const uint64_t cm = (1ull << pa.b) - 1ull;
+  for (int p = 0; p < pa.P; ++p) put_bits(w, pos, (uint64_t)(int64_t)pa.code[(int64_t)t * pa.P + p] & cm, pa.b);
+  put_bits(w, pos, (uint64_t)pa.scale[t] & ((1ull << pa.scale_bits) - 1ull), pa.scale_bits);
+  uint8_t* o = pa.out + pa.h + (off + (uint64_t)i) * (uint64_t)pa.L;
+  for (int k = 0; k < pa.L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
+}
+
 // ---------------------------------------------------------------- sort of the survivors
 // Items are (key, tile) pairs; tiles are distinct, so the lexicographic order
 // on the pair is a total order and equal gains come out in increasing tile
@@ -359,11 +412,13 @@ __device__ __forceinline__ void wave_sync() {
 // In-place bitonic sort of each chunk of kChunk items in LDS; the tail chunk
 // is padded with sentinels that sort last and are not written back.  Pair q of
 // a stage with distance j compares elements i = (q with a zero inserted at bit
-// log2 j) and i + j; thread t takes pairs t and t + kChunkThreads, so for
-// j <= 64 every wavefront works inside its own two 128-element windows and a
-// wavefront-level barrier suffices between stages.
-__global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restrict__ items,
-                                                               const uint64_t* __restrict__ state) {
+// log2 j) and i + j; thread t takes pairs t + r kChunkThreads (one pair per
+// thread with kChunk = 2 kChunkThreads), so for j <= 64 every wavefront works
+// inside its own 128-element windows and a wavefront-level barrier suffices
+// between stages.
+// With `pack` set (the final pass) the sorted items are packed as records.
+__global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restrict__ items, uint64_t* state,
+                                                               int pack, PackArgs pa) {
   __shared__ uint64_t sk[kChunk];
   __shared__ uint32_t st[kChunk];
   const int64_t n = (int64_t)state[kSegK];
@@ -405,11 +460,15 @@ __global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restr
     const int j = r * kChunkThreads + threadIdx.x;
     const int64_t i = base + j;
     if (i < n) {
-      SortItem x;
-      x.key = sk[j];
-      x.tile = st[j];
-      x.pad = 0u;
-      items[i] = x;
+      if (pack) {
+        pack_record(pa, state, i, st[j]);
+      } else {
+        SortItem x;
+        x.key = sk[j];
+        x.tile = st[j];
+        x.pad = 0u;
+        items[i] = x;
+      }
     }
   }
 }
@@ -424,9 +483,8 @@ __global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restr
 // digits (F loads per level); the last pass over a few long runs uses base-8
 // digits, which cuts the number of round trips by three.
 template <int LOGR, int F>
-__global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__ in,
-                                                    const uint64_t* __restrict__ state, int logw,
-                                                    SortItem* __restrict__ out) {
+__global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__ in, uint64_t* state, int logw,
+                                                    SortItem* __restrict__ out, int pack, PackArgs pa) {
   constexpr int NP = (1 << LOGR) - 1;  // probes per run per level
   const int64_t n = (int64_t)state[kSegK];
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -467,7 +525,8 @@ __global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__
   int64_t pos = (g0 << logw) + (i - (run << logw));
 #pragma unroll
   for (int r = 0; r < F; ++r) pos += cnt[r];
-  out[pos] = x;
+  if (pack) pack_record(pa, state, pos, x.tile);
+  else out[pos] = x;
 }
 
 // ---------------------------------------------------------------- workspace
@@ -501,41 +560,6 @@ hipError_t launch_rank_init(const RankWs& ws, hipStream_t st) {
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- packing
-__device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v, int nbits) {
-  if (nbits <= 0) return;
-  const int o = pos & 63, k = pos >> 6;
-  w[k] |= v << o;
-  if (o + nbits > 64) w[k + 1] |= v >> (64 - o);
-  pos += nbits;
-}
-
-// Record i of the segment goes to byte h + (first slot + i) * L of the
-// stream; a stream buffer too small for the running total raises the
-// no-space flag instead.
-__global__ void k_pack(const SortItem* __restrict__ sorted, uint64_t* state, const uint16_t* __restrict__ seed,
-                       const int8_t* __restrict__ code, const uint16_t* __restrict__ scale, int P, int b,
-                       int idx_bits, int seed_bits, int scale_bits, int L, uint64_t h, uint64_t cap,
-                       uint8_t* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const uint64_t K = state[kSegK], off = state[kSegOff];
-  if (i >= (int64_t)K) return;
-  if (h + (off + K) * (uint64_t)L > cap) {
-    if (i == 0) state[kNoSpace] = 1;
-    return;
-  }
-  const uint32_t t = sorted[i].tile;
-  uint64_t w[3] = {0, 0, 0};
-  int pos = 0;
-  put_bits(w, pos, (uint64_t)t, idx_bits);
-  put_bits(w, pos, (uint64_t)seed[t], seed_bits);
-  const uint64_t cm = (1ull << b) - 1ull;
-  for (int p = 0; p < P; ++p) put_bits(w, pos, (uint64_t)(int64_t)code[(int64_t)t * P + p] & cm, b);
-  put_bits(w, pos, (uint64_t)scale[t] & ((1ull << scale_bits) - 1ull), scale_bits);
-  uint8_t* o = out + h + (off + (uint64_t)i) * (uint64_t)L;
-  for (int k = 0; k < L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
-}
-
 // One segment: count -> select -> compact -> sort -> pack, all on the device.
 // `cap` bounds K (the budget's record count, at most n); grids are sized by it
 // and kernels read the actual K from the state.
@@ -551,35 +575,45 @@ hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_
   // passes 1..5 over the digits 12, 12, 12, 12 and 4 bits below the top one
   const int shifts[6] = {64 - kSelBits, 64 - 2 * kSelBits, 64 - 3 * kSelBits, 64 - 4 * kSelBits, 64 - 5 * kSelBits, 0};
   const int widths[6] = {kSelBits, kSelBits, kSelBits, kSelBits, kSelBits, 4};
+  // fewer blocks than the counting pass: every block repeats the pick (a read
+  // of the 32 KB histogram), and the keys under the prefix thin out fast
+  int64_t sb = (n + 4 * kThreads - 1) / (4 * kThreads);
+  if (sb > 128) sb = 128;
+  if (sb < 1) sb = 1;
   for (int pass = 1; pass <= 5; ++pass)
-    hipLaunchKernelGGL(k_select_pass, dim3((unsigned)cb), dim3(kThreads), 0, st, g, n, ws.state,
+    hipLaunchKernelGGL(k_select_pass, dim3((unsigned)sb), dim3(kThreads), 0, st, g, n, ws.state,
                        (int64_t)(cap > 0 ? cap : 0), pass, shifts[pass - 1], widths[pass - 1], shifts[pass],
                        widths[pass]);
-  hipLaunchKernelGGL(k_select_finish, dim3(1), dim3(kThreads), 0, st, ws.state, 6, shifts[5], widths[5]);
-  if (cap <= 0 || n <= 0) return hipGetLastError();
-  const int64_t nbc = (n + kItems - 1) / kItems;
+  // the first compaction launch finishes the select and records the totals
+  int64_t nbc = (n + kItems - 1) / kItems;
+  if (nbc < 1) nbc = 1;
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state, ws.blk_a, ws.blk_b);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
+  if (cap <= 0 || n <= 0) return hipGetLastError();
   hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
                      ws.blk_a, ws.blk_b, ws.items_a);
-  // sort the survivors ascending on (~key, tile): LDS chunks, then multiway merges
+  // sort the survivors ascending on (~key, tile): LDS chunks, then multiway
+  // merges; the final pass packs the records instead of writing items
+  const PackArgs pa{seed, code, scale, P, b, idx_bits, seed_bits, scale_bits, L, h, stream_cap, stream_out};
+  int passes = 0;
+  for (int logw = kLogChunk; ((int64_t)1 << logw) < cap; logw += cap <= ((int64_t)4 << logw) ? 2 : kLogFan) ++passes;
   hipLaunchKernelGGL(k_sort_chunks, dim3((unsigned)((cap + kChunk - 1) / kChunk)), dim3(kChunkThreads), 0, st,
-                     ws.items_a, ws.state);
+                     ws.items_a, ws.state, passes == 0 ? 1 : 0, pa);
   SortItem* in = ws.items_a;
   SortItem* out = ws.items_b;
+  int done = 0;
   for (int logw = kLogChunk; ((int64_t)1 << logw) < cap;) {
     const dim3 grid((unsigned)((cap + 255) / 256));
+    const int last = ++done == passes ? 1 : 0;
     if (cap <= ((int64_t)4 << logw)) {  // at most four runs left: one base-8 pass
-      hipLaunchKernelGGL((k_merge_runs<3, 4>), grid, dim3(256), 0, st, in, ws.state, logw, out);
+      hipLaunchKernelGGL((k_merge_runs<3, 4>), grid, dim3(256), 0, st, in, ws.state, logw, out, last, pa);
       logw += 2;
     } else {
-      hipLaunchKernelGGL((k_merge_runs<1, kFan>), grid, dim3(256), 0, st, in, ws.state, logw, out);
+      hipLaunchKernelGGL((k_merge_runs<1, kFan>), grid, dim3(256), 0, st, in, ws.state, logw, out, last, pa);
       logw += kLogFan;
     }
     SortItem* t = in; in = out; out = t;
   }
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, st, in, ws.state, seed, code,
-                     scale, P, b, idx_bits, seed_bits, scale_bits, L, h, stream_cap, stream_out);
   return hipGetLastError();
 }
 
