@@ -38,16 +38,26 @@ def log(*a):
 MEASURED_TRAFFIC = {
     ("encode", "down3b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip"],
-        "sha256": "c8162196128d4577597864a108a16bbfb4cfa51a0a3f60b294e8ffae0486f8c5",
-        "bytes": 330677894},
+        "sha256": "263b89abc6e9c2acdc0c3266abe9f4612261cf8fdd4212ee49a5c574fc98aa21",
+        "bytes": 330032937},
     ("backbone", "down3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "f7ed6ca04390a2a03408862e4e3882ab29873ad663e5330d4023c008cd6b40b3",
-        "bytes": 147301927},
+        "sha256": "0598226f5eb11574f4cf804bc9f68f9e2e0adf0e654238f5fc8c41a76a4b0aab",
+        "bytes": 147305196},
     ("decode_apply", "down3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "6ad27f941ea8633b7e9f83360c7c02a2d1f905a7a0b9f27d140e9e7ba4d1d5d3",
-        "bytes": 22876765},
+        "sha256": "c3e9138607df8b0e9f146856025c11aedbaedda4afc1afb3326a50f8e01df8de",
+        "bytes": 22875392},
+    # the stack3b stream at 0.32 bpw of the at-scale measurement
+    ("decode_apply", "stack3b@0.32"): {
+        "files": ["awsrc_internal.h", "decode.hip"],
+        "sha256": "c3e9138607df8b0e9f146856025c11aedbaedda4afc1afb3326a50f8e01df8de",
+        "bytes": 5044000000},
+    # the whole reconstruction call: tile ordering (scans, copy) and the streaming pass
+    ("reconstruct_bf16", "stack3b@0.32"): {
+        "files": ["awsrc_internal.h", "decode.hip"],
+        "sha256": "c3e9138607df8b0e9f146856025c11aedbaedda4afc1afb3326a50f8e01df8de",
+        "bytes": 9461000000},
 }
 
 
@@ -141,7 +151,7 @@ def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
     nbytes = K * (plan.L_rec + 2 * wl.C * 4)
     gbs = nbytes / (ms / 1e3) / 1e9
     del W0, plan, dws
-    rec_stats = reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps)
+    rec_stats = reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps, bpw)
     del s
     # device-copy ceiling: one large copy, read + write bytes
     n = 1 << 30
@@ -160,10 +170,11 @@ def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
     rec_stats["frac_copy"] = rec_stats["GB/s"] / copy_gbs
     return {"workload": f"{name} stream at {bpw} bpw, fp32 W0", "modules": len(shapes), "records": K,
             "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs, "reconstruct_bf16": rec_stats}
+            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs,
+            "traffic": measured_traffic("decode_apply", f"{name}@{bpw}"), "reconstruct_bf16": rec_stats}
 
 
-def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps):
+def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps, bpw):
     """Dense bf16 reconstruction of every module from a random RTN backbone
     (codes, fp16 scales in [1e-3, 2e-3), zero points) plus the stream `s`.
     Algorithmic bytes: codes (1/2 B per weight), scale and zero (3 B per
@@ -195,7 +206,8 @@ def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps):
     del outs, bbs, plan, ws
     torch.cuda.empty_cache()
     gbs = nbytes / (ms / 1e3) / 1e9
-    return {"weights": n_w, "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
+    return {"weights": n_w, "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+            "traffic": measured_traffic("reconstruct_bf16", f"{wl.name}@{bpw}")}
 
 
 def main() -> int:
