@@ -106,17 +106,33 @@ __device__ __forceinline__ float screen_scale(float m, float inv_qmax, float* is
 // 2 a.b - a^T G0 a of the quantized fit minus scale^2 eps |q|^2 (relative
 // size ~ lambda), which the fp64 re-score of the kept seeds removes.  Uses
 // q.b = (L^T q).w with w = L^-1 b, and q^T G q = sum_k e_k (L^T q)_k^2.
-template <int PB, bool POW2, typename FP>
-__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
+//
+// Split in two: screen_fwd solves L w = b and returns b^T G^-1 b =
+// sum_k w_k^2 / e_k, the score of the unquantized optimum alpha = G^-1 b.
+// The score is a concave quadratic in the coefficient vector c = scale q,
+// 2 c.b - c^T G c, whose maximum over all c is that value, so no scale and
+// codes can score above it: a candidate whose bound is below the score a
+// tile already holds cannot enter its list.  screen_gain_w finishes the
+// score from w.
+template <int PB, typename FP>
+__device__ __forceinline__ float screen_fwd(const float (&b)[PB], const FP& f, float (&w)[PB]) {
   constexpr int LS = PB * (PB - 1) / 2;
-  float w[PB], al[PB];
+  float bound = 0.0f;
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
     float t = b[p];
 #pragma unroll
     for (int k = 0; k < p; ++k) t = fmaf(-f[ltri(p, k)], w[k], t);
     w[p] = t;
+    bound = fmaf(t * f[LS + p], t, bound);
   }
+  return bound;
+}
+
+template <int PB, bool POW2, typename FP>
+__device__ __forceinline__ float screen_gain_w(const float (&w)[PB], const FP& f, float qmax, float inv_qmax) {
+  constexpr int LS = PB * (PB - 1) / 2;
+  float al[PB];
 #pragma unroll
   for (int p = PB - 1; p >= 0; --p) {
     float t = w[p] * f[LS + p];
@@ -142,6 +158,13 @@ __device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP
     quad = fmaf(f[LS + PB + k] * y, y, quad);
   }
   return sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
+}
+
+template <int PB, bool POW2, typename FP>
+__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
+  float w[PB];
+  (void)screen_fwd<PB>(b, f, w);
+  return screen_gain_w<PB, POW2>(w, f, qmax, inv_qmax);
 }
 
 // ---------------------------------------------------------------- launchers

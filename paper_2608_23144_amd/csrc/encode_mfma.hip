@@ -95,40 +95,41 @@ __global__ void k_mfma_frags(BasisTables bt, int C, int P, int S, u32x4* __restr
 }
 
 // ----------------------------------------------------------------------------
-// Screen: one wavefront (one workgroup) = 64 consecutive rows of one column
-// block and one range of seed pairs; lane = tile during the per-candidate
-// stage.  Seed ranges are used only when a module has too few row groups to
-// fill the machine (each range costs its own tile loads and top list).
-template <bool PE, bool POW2>
-__global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32x4* __restrict__ frag,
-                                                         int stride) {
-  constexpr int C = 64;
-  constexpr int PB = 8;
-  constexpr int TS = 12;  // LDS stride (floats) of one tile's coefficients
-  __shared__ __attribute__((aligned(16))) float tb[2 * 64 * TS];
-  __shared__ float wdl[PE ? 64 * (C + 1) : 1];
-  const int lane = threadIdx.x;
-  const int nbk_cols = (int)(a.cols / C);
-  const int nsplit = a.nsplit;
+// C = 64 screens.  One wavefront (one workgroup) = 64 consecutive rows of one
+// column block and one range of seed pairs.  Seed ranges are used only when a
+// module has too few row groups to fill the machine (each range costs its own
+// tile loads and top lists).
+struct ScreenTask {
+  int blk, split, pair0, pair1;
+  int64_t row0;
+};
+
+__device__ __forceinline__ ScreenTask screen_task(const EncodeArgs& a, int rows_per_wave) {
   // Workgroups are dealt to the 8 XCDs round-robin by index.  Give each XCD a
   // contiguous run of work items in column-block-major order, so that the
   // row groups of a column block share one L2 for their factor reads.
   const int64_t nwg = gridDim.x;
   const int64_t xcd = blockIdx.x % 8, q = nwg / 8, rem = nwg % 8;
   const int64_t w = xcd * q + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
-  const int nrg = (int)((a.rows + 63) / 64);
-  const int split = (int)(w % nsplit);
-  const int64_t rest = w / nsplit;
-  const int blk = (int)(rest / nrg);
-  const int64_t row0 = (rest % nrg) * 64;
+  const int nrg = (int)((a.rows + rows_per_wave - 1) / rows_per_wave);
+  ScreenTask t;
+  t.split = (int)(w % a.nsplit);
+  const int64_t rest = w / a.nsplit;
+  t.blk = (int)(rest / nrg);
+  t.row0 = (rest % nrg) * rows_per_wave;
   const int n_pairs_all = (a.S + 1) / 2;
-  const int pp = (n_pairs_all + nsplit - 1) / nsplit;
-  const int pair0 = split * pp;
-  const int pair1 = pair0 + pp < n_pairs_all ? pair0 + pp : n_pairs_all;
-  const int n = lane & 15, g = lane >> 4;
+  const int pp = (n_pairs_all + a.nsplit - 1) / a.nsplit;
+  t.pair0 = t.split * pp;
+  t.pair1 = t.pair0 + pp < n_pairs_all ? t.pair0 + pp : n_pairs_all;
+  return t;
+}
 
-  // ---- u = d .* r fragments for the 4 groups of 16 tiles, split in three bf16 parts
-  u32x4 uh[4][2], um[4][2], ul[4][2];
+// u = d .* r fragments of the 4 groups of 16 tiles (rows row0 + 16 nb + n),
+// split in three bf16 parts; rows past the end give zeros.
+template <bool PE>
+__device__ __forceinline__ void load_u64(const EncodeArgs& a, int64_t row0, int blk, int n, int g,
+                                         u32x4 (&uh)[4][2], u32x4 (&um)[4][2], u32x4 (&ul)[4][2]) {
+  constexpr int C = 64;
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) {
     const int64_t row = row0 + 16 * nb + n;
@@ -148,11 +149,51 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
       split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
     }
   }
-  const int64_t my_row = row0 + lane;
+}
+
+// b of one seed pair for the 64 tiles: rows 4g..4g+3 of each 16 x 16 result
+// (seed g/2 of the pair, coefficients 4(g&1)..+3) for the tiles 16 nb + n.
+__device__ __forceinline__ void project64(const u32x4& F0, const u32x4& F1, const u32x4 (&uh)[4][2],
+                                          const u32x4 (&um)[4][2], const u32x4 (&ul)[4][2], f32x4 (&acc)[4]) {
+  const bf16x8 A0 = as_bf16x8(F0), A1 = as_bf16x8(F1);
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(uh[nb][0]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(um[nb][0]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(ul[nb][0]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(uh[nb][1]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(um[nb][1]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(ul[nb][1]), c, 0, 0, 0);
+    acc[nb] = c;
+  }
+}
+
+// Per-element weights: lane = tile during the per-candidate stage.  The
+// 16 x 64 result is transposed through LDS so that each lane holds the P
+// coefficients of its own tile for both seeds of the pair; each lane then
+// factors its own G + eps I from the Gram gathers and scores every candidate.
+template <bool POW2>
+__global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4* __restrict__ frag) {
+  constexpr int C = 64;
+  constexpr int PB = 8;
+  constexpr int TS = 12;  // LDS stride (floats) of one tile's coefficients
+  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
+  constexpr int LS = PB * (PB - 1) / 2;
+  __shared__ __attribute__((aligned(16))) float tb[2 * 64 * TS];
+  __shared__ float wdl[64 * (C + 1)];
+  const int lane = threadIdx.x;
+  const int nbk_cols = (int)(a.cols / C);
+  const ScreenTask tk = screen_task(a, 64);
+  const int blk = tk.blk, pair0 = tk.pair0, pair1 = tk.pair1;
+  const int n = lane & 15, g = lane >> 4;
+  u32x4 uh[4][2], um[4][2], ul[4][2];
+  load_u64<true>(a, tk.row0, blk, n, g, uh, um, ul);
+  const int64_t my_row = tk.row0 + lane;
   const bool my_valid = my_row < a.rows;
   const int64_t my_off = (my_valid ? my_row : a.rows - 1) * a.cols + (int64_t)blk * C;
   const int P = a.P;
-  if constexpr (PE) {
+  {
     // WHT of this lane's tile weights, for the Gram gathers G_pq = WHT(d)[c_p ^ c_q] / C
     float wd[C];
 #pragma unroll
@@ -186,21 +227,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   // matrix cores compute the projections of pair k+1 (the fragment table is
   // padded with zero pairs, so the last iterations need no special case).
   const u32x4* fp = frag + (size_t)pair0 * 128 + lane;
-  auto project = [&](const u32x4& F0, const u32x4& F1, f32x4 (&acc)[4]) {
-    const bf16x8 A0 = as_bf16x8(F0), A1 = as_bf16x8(F1);
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-      f32x4 c = {0.f, 0.f, 0.f, 0.f};
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(uh[nb][0]), c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(um[nb][0]), c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, as_bf16x8(ul[nb][0]), c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(uh[nb][1]), c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(um[nb][1]), c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, as_bf16x8(ul[nb][1]), c, 0, 0, 0);
-      acc[nb] = c;
-    }
-  };
-  // rows 4g..4g+3 of the product = (seed g/2, columns 4(g&1)..+3) of tiles 16nb + n
   auto stash = [&](const f32x4 (&acc)[4]) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
@@ -208,25 +234,10 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
   };
   {
     f32x4 acc[4];
-    project(fp[0], fp[64], acc);
+    project64(fp[0], fp[64], uh, um, ul, acc);
     stash(acc);
   }
   u32x4 F0 = fp[128], F1 = fp[192];
-  // per-column factors rotate through two register sets: the first seed's of
-  // the next pair load while the second seed of this pair is scored, and the
-  // second seed's load while the first is scored, hiding the load latency
-  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
-  typedef const __attribute__((address_space(4))) float* cfp;
-  auto fac_ptr = [&](int s) -> cfp {
-    const int sc_ = s < a.S ? s : a.S - 1;
-    return (cfp)(a.colfac + ((size_t)blk * a.S + sc_) * stride);
-  };
-  float fA[PE ? 1 : NF], fB[PE ? 1 : NF];
-  if constexpr (!PE) {
-    const cfp f0 = fac_ptr(2 * pair0);
-#pragma unroll
-    for (int i = 0; i < NF; ++i) fA[i] = f0[i];
-  }
   for (int pair = pair0; pair < pair1; ++pair) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -243,63 +254,45 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
     __builtin_amdgcn_wave_barrier();
     // projections of the next pair (zero rows past the last seed) and the prefetch after it
     f32x4 accN[4];
-    project(F0, F1, accN);
+    project64(F0, F1, uh, um, ul, accN);
     F0 = fp[(size_t)(pair - pair0 + 2) * 128];
     F1 = fp[(size_t)(pair - pair0 + 2) * 128 + 64];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int s = 2 * pair + k;
-      float gsc;
-      if constexpr (PE) {
-        // this tile's G + eps I = L diag(e) L^T from the Gram gathers, row by
-        // row (E = L diag(e) kept for the current row only), in the layout of
-        // the per-column table so the same score routine applies
-        constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
-        constexpr int LS = PB * (PB - 1) / 2;
-        float f[NF];
-        const int sc_ = s < a.S ? s : a.S - 1;
-        // the seed's columns: two scalar dword loads (uniform across the wavefront)
-        const __attribute__((address_space(4))) uint32_t* cw =
-            (const __attribute__((address_space(4))) uint32_t*)(a.basis.col + (size_t)sc_ * kMaxP);
-        const uint32_t cw0 = cw[0], cw1 = cw[1];
-        int c[PB];
+      // this tile's G + eps I = L diag(e) L^T from the Gram gathers, row by
+      // row (E = L diag(e) kept for the current row only), in the layout of
+      // the per-column table so the same score routine applies
+      float f[NF];
+      const int sc_ = s < a.S ? s : a.S - 1;
+      // the seed's columns: two scalar dword loads (uniform across the wavefront)
+      const __attribute__((address_space(4))) uint32_t* cw =
+          (const __attribute__((address_space(4))) uint32_t*)(a.basis.col + (size_t)sc_ * kMaxP);
+      const uint32_t cw0 = cw[0], cw1 = cw[1];
+      int c[PB];
 #pragma unroll
-        for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw0 : cw1) >> (8 * (p & 3))) & 0xFFu) : 0;
-        const float* wrow = &wdl[lane * (C + 1)];
-        const float eps = lam * wrow[0];
+      for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw0 : cw1) >> (8 * (p & 3))) & 0xFFu) : 0;
+      const float* wrow = &wdl[lane * (C + 1)];
+      const float eps = lam * wrow[0];
 #pragma unroll
-        for (int p = 0; p < PB; ++p) {
-          float E[PB];
+      for (int p = 0; p < PB; ++p) {
+        float E[PB];
 #pragma unroll
-          for (int q = 0; q < p; ++q) {
-            float t = (p < P && q < P) ? wrow[c[p] ^ c[q]] : 0.0f;
+        for (int q = 0; q < p; ++q) {
+          float t = (p < P && q < P) ? wrow[c[p] ^ c[q]] : 0.0f;
 #pragma unroll
-            for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
-            E[q] = t;
-            f[ltri(p, q)] = t * f[LS + q];
-          }
-          float t = (p < P) ? wrow[0] + eps : 1.0f;
-#pragma unroll
-          for (int kk = 0; kk < p; ++kk) t = fmaf(-E[kk], f[ltri(p, kk)], t);
-          t = fmaxf(t, 1e-30f);
-          f[LS + PB + p] = t;
-          f[LS + p] = __builtin_amdgcn_rcpf(t);
+          for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
+          E[q] = t;
+          f[ltri(p, q)] = t * f[LS + q];
         }
-        gsc = screen_score_ldl<PB, POW2>(bk[k], f, qmax, inv_qmax);
-      } else {
-        // uniform across the wavefront: scalar loads through the constant address space
-        if (k == 0) {
-          const cfp fb = fac_ptr(s + 1);
+        float t = (p < P) ? wrow[0] + eps : 1.0f;
 #pragma unroll
-          for (int i = 0; i < NF; ++i) fB[i] = fb[i];
-          gsc = screen_score_ldl<PB, POW2>(bk[0], fA, qmax, inv_qmax);
-        } else {
-          const cfp fa = fac_ptr(s + 1);
-#pragma unroll
-          for (int i = 0; i < NF; ++i) fA[i] = fa[i];
-          gsc = screen_score_ldl<PB, POW2>(bk[1], fB, qmax, inv_qmax);
-        }
+        for (int kk = 0; kk < p; ++kk) t = fmaf(-E[kk], f[ltri(p, kk)], t);
+        t = fmaxf(t, 1e-30f);
+        f[LS + PB + p] = t;
+        f[LS + p] = __builtin_amdgcn_rcpf(t);
       }
+      float gsc = screen_score_ldl<PB, POW2>(bk[k], f, qmax, inv_qmax);
       gsc = s < a.S ? gsc : -INFINITY;
       // branch-free insertion into the top two (earlier seeds first among equals)
       const bool c0 = gsc > tg0, c1 = gsc > tg1;
@@ -317,11 +310,245 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma64(EncodeArgs a, const u32
     stash(accN);
   }
   if (my_valid) {
-    const int64_t at = ((my_row * nbk_cols + blk) * nsplit + split) * kTop;
+    const int64_t at = ((my_row * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
     a.top_gain[at + 0] = tg0 * (1.0f / 64.0f);  // back to gain units
     a.top_gain[at + 1] = tg1 * (1.0f / 64.0f);
     a.top_seed[at + 0] = (uint16_t)ts0;
     a.top_seed[at + 1] = (uint16_t)ts1;
+  }
+}
+
+// Per-column weights.  The factor of G + eps I is one table entry per seed,
+// shared by every tile of the wavefront, and the projections are used where
+// the matrix cores leave them: lane (n, g) holds 4 coefficients of seed g/2
+// for the tiles 16 nb + n.  One v_permlane16_swap per pair of registers
+// trades halves between lane rows g and g^1, after which lane (n, g) holds
+// all P coefficients of seed g/2 of the pair for two tiles, 16 nb0 + n and
+// 16 (nb0 + 1) + n with nb0 = 2 (g & 1).  A lane thus scores one seed for two
+// tiles (one factor read serves both), each tile's even and odd seeds live in
+// lanes g and g^2, and the two lanes' lists are merged at the end.
+//
+// Every candidate gets the forward solve and its bound (screen_fwd); only
+// those whose bound clears the tile's current second score are scored in
+// full.  Those few would leave most lanes idle, so each lane queues its
+// survivors (w, the seed and which of its tiles) in its own LDS ring, and a
+// scoring round takes the oldest entry of every lane that has one.  The
+// threshold is the tile's second score over both of its lanes' lists: a
+// candidate below two scores already found is in neither the tile's final
+// top two nor (as those two are each in some lane's list) needed in its own
+// lane's list for the merge.  A lane's entries are scored in seed order, and
+// thresholds only rise, so the merged lists are those of scoring every
+// candidate.  The factor of 1 + 2^-9 on the bound covers its fp32 rounding
+// and that of the score (each a few ulps of the bound).
+//
+// Factor entries reach the wavefront through an LDS ring of the last NR
+// pairs (both seeds' whole entries per slot): while pair k is bounded, every
+// lane loads one 16-byte piece of pair k+1's entries (lane l takes piece
+// l % 22, so the loads and stores need no branch; lanes with the same piece
+// store the same value).  The bound reads its seed's entry from the slot of
+// pair k, a scoring round reads each entry's from the slot of its pair, and
+// rounds run before an entry's slot is reused.  Vector loads and LDS reads
+// complete in order, so the waits for them are exact.
+template <bool POW2>
+__global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x4* __restrict__ frag,
+                                                        int stride) {
+  constexpr int C = 64;
+  constexpr int PB = 8;
+  constexpr int NB = PB * (PB - 1) / 2 + PB;      // L and 1/e: what the bound reads
+  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;  // the whole entry (the full score also reads e)
+  constexpr int QD = 4;                           // queue slots per lane (a power of two), plus a spare
+  constexpr int QW = PB + 1;                      // words per entry: w, then seed + (tile << 16)
+  constexpr int NR = 16;                          // factor ring slots (pairs; a power of two)
+  constexpr float kSlack = 1.001953125f;
+  static_assert(NF % 4 == 0, "factor pieces are 16 bytes");
+  __shared__ float qb[(QD + 1) * QW * 64];
+  __shared__ __attribute__((aligned(16))) float fr[NR * 2 * NF];
+  const int lane = threadIdx.x;
+  const int nbk_cols = (int)(a.cols / C);
+  const ScreenTask tk = screen_task(a, 64);
+  const int blk = tk.blk, pair0 = tk.pair0, pair1 = tk.pair1;
+  const int n = lane & 15, g = lane >> 4;
+  const int sh = g >> 1;        // the seed of each pair this lane scores
+  const int nb0 = 2 * (g & 1);  // its tiles: 16 nb0 + n and 16 (nb0 + 1) + n
+  u32x4 uh[4][2], um[4][2], ul[4][2];
+  load_u64<false>(a, tk.row0, blk, n, g, uh, um, ul);
+  const int64_t trow0 = tk.row0 + 16 * nb0 + n;
+  const bool tv[2] = {trow0 < a.rows, trow0 + 16 < a.rows};
+  const float qmax = (float)((1 << (a.b - 1)) - 1);
+  const float inv_qmax = 1.0f / qmax;
+
+  // top two per tile; a lane's seeds increase, so strict comparisons keep the
+  // earlier seed first among equal scores
+  float tg[2][2] = {{-INFINITY, -INFINITY}, {-INFINITY, -INFINITY}};
+  int ts[2][2] = {{0, 0}, {0, 0}};
+  auto insert = [&](int t, float gsc, int s) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const bool c0 = t == j && gsc > tg[j][0], c1 = t == j && gsc > tg[j][1];
+      tg[j][1] = c0 ? tg[j][0] : (c1 ? gsc : tg[j][1]);
+      ts[j][1] = c0 ? ts[j][0] : (c1 ? s : ts[j][1]);
+      tg[j][0] = c0 ? gsc : tg[j][0];
+      ts[j][0] = c0 ? s : ts[j][0];
+    }
+  };
+  // queue: qhead, qlen, and the pair of the head entry (INT_MAX when empty)
+  int qhead = 0, qlen = 0, hp = INT_MAX;
+  auto score_round = [&]() {
+    if (qlen > 0) {
+      const float* e = &qb[qhead * (QW * 64) + lane];
+      float wv[PB];
+#pragma unroll
+      for (int i = 0; i < PB; ++i) wv[i] = e[i * 64];
+      const int code = __float_as_int(e[PB * 64]);
+      const int s = code & 0xFFFF;
+      const float* fe = &fr[((s >> 1) & (NR - 1)) * (2 * NF) + (s & 1) * NF];
+      float f[NF];
+#pragma unroll
+      for (int i = 0; i < NF / 4; ++i) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&fe[4 * i]);
+        f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+      }
+      insert(code >> 16, screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax), s);
+      qhead = (qhead + 1) & (QD - 1);
+      --qlen;
+      // the next entry's seed (any word when the queue is now empty)
+      const int nx = __float_as_int(qb[qhead * (QW * 64) + PB * 64 + lane]);
+      hp = qlen > 0 ? (nx & 0xFFFF) >> 1 : INT_MAX;
+    }
+  };
+
+  constexpr int NPC = 2 * NF / 4;  // 16-byte pieces per pair
+  const int pc = lane % NPC;
+  auto fac_piece = [&](int pr) -> f32x4 {
+    int s = 2 * pr + pc / (NF / 4);
+    s = s < a.S ? s : a.S - 1;
+    return *reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + s) * stride + 4 * (pc % (NF / 4)));
+  };
+  auto fac_store = [&](int pr, const f32x4& v) {
+    *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NF) + 4 * pc]) = v;
+  };
+
+  // Raw units and the software pipeline as in k_screen_pe64: b is left
+  // unscaled by 1/sqrt(C) = 1/8 (bound, scale and gain 8, 8 and 64 times
+  // larger, rescaled at the end), and the matrix cores project pair k+1
+  // while the vector ALUs post-process pair k.
+  const u32x4* fp = frag + (size_t)pair0 * 128 + lane;
+  // two register sets for the projections and the fragments, swapping roles
+  // every pair (the loop runs two pairs per trip, so no copies are needed)
+  f32x4 accA[4], accB[4];
+  u32x4 FA0 = fp[128], FA1 = fp[192], FB0, FB1;
+  project64(fp[0], fp[64], uh, um, ul, accA);
+  fac_store(pair0, fac_piece(pair0));
+  f32x4 fnext = fac_piece(pair0 + 1);
+  auto step = [&](int pair, const f32x4 (&acc)[4], f32x4 (&accN)[4], const u32x4& F0, const u32x4& F1,
+                  u32x4& F0n, u32x4& F1n) {
+    // orders the last pair's ring accesses before this one's
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // next pair's factors into its slot (the oldest pair's, whose entries the
+    // last pair's rounds have scored), then this pair's global loads (factors
+    // and +-1 fragments two pairs ahead) and factor reads, kept ahead of the
+    // matrix-core work by the scheduling barrier so that they have the whole
+    // pair's work to arrive
+    fac_store(pair + 1, fnext);
+    fnext = fac_piece(pair + 2);
+    F0n = fp[(size_t)(pair - pair0 + 2) * 128];
+    F1n = fp[(size_t)(pair - pair0 + 2) * 128 + 64];
+    const int s = 2 * pair + sh;
+    float f[NB];
+    {
+      const float* frow = &fr[(pair & (NR - 1)) * (2 * NF) + sh * NF];
+#pragma unroll
+      for (int i = 0; i < NB / 4; ++i) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&frow[4 * i]);
+        f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    project64(F0, F1, uh, um, ul, accN);
+    // this lane's coefficients: tile t = [lower half, upper half]
+    float bt[2][PB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[t][i]), __float_as_uint(acc[t + 2][i]),
+                                                        false, false);
+        bt[t][i] = __uint_as_float(r[0]);
+        bt[t][4 + i] = __uint_as_float(r[1]);
+      }
+    // each tile's second score over both lanes' lists (lane ^ 32 holds the
+    // other seed parity): the second largest of {a0 >= a1} and {b0 >= b1}
+    // is max(min(a0, b0), max(a1, b1))
+    float thr[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][0]), __float_as_uint(tg[t][0]), false,
+                                                       false);
+      const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][1]), __float_as_uint(tg[t][1]), false,
+                                                       false);
+      const float o0 = __uint_as_float(sh ? r0[0] : r0[1]), o1 = __uint_as_float(sh ? r1[0] : r1[1]);
+      thr[t] = fmaxf(fminf(tg[t][0], o0), fmaxf(tg[t][1], o1));
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      float wv[PB];
+      const float bnd = screen_fwd<PB>(bt[t], f, wv);
+      // a candidate that is not kept goes to the spare slot QD, so the stores
+      // need no branch (one basic block keeps the matrix-core instructions
+      // interleaved with this work); bitwise: a short-circuit would put the
+      // bound under a branch
+      const bool keep = (int)(bnd * kSlack > thr[t]) & (int)tv[t] & (int)(s < a.S);
+      float* e = &qb[(keep ? ((qhead + qlen) & (QD - 1)) : QD) * (QW * 64) + lane];
+#pragma unroll
+      for (int i = 0; i < PB; ++i) e[i * 64] = wv[i];
+      e[PB * 64] = __int_as_float(s | (t << 16));
+      hp = (keep && qlen == 0) ? pair : hp;
+      qlen += keep ? 1 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < 24; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+    // room for the next pair's two entries, and no entry of the pair whose
+    // slot the next pair refills
+    while (__ballot(qlen > QD - 2 || hp <= pair + 2 - NR) != 0) score_round();
+  };
+  int pair = pair0;
+  for (; pair + 1 < pair1; pair += 2) {
+    step(pair, accA, accB, FA0, FA1, FB0, FB1);
+    step(pair + 1, accB, accA, FB0, FB1, FA0, FA1);
+  }
+  if (pair < pair1) step(pair, accA, accB, FA0, FA1, FB0, FB1);
+  while (__ballot(qlen > 0) != 0) score_round();
+
+  // merge each tile's lists from lanes g (this seed parity) and g ^ 2 (the
+  // other): (gain desc, seed asc)
+  auto better = [](float ga, int sa, float gb, int sb) { return ga > gb || (ga == gb && sa < sb); };
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const float og0 = __shfl_xor(tg[t][0], 32, 64), og1 = __shfl_xor(tg[t][1], 32, 64);
+    const int os0 = __shfl_xor(ts[t][0], 32, 64), os1 = __shfl_xor(ts[t][1], 32, 64);
+    if (sh == 0 && tv[t]) {
+      float r0, r1;
+      int q0, q1;
+      if (better(tg[t][0], ts[t][0], og0, os0)) {
+        r0 = tg[t][0]; q0 = ts[t][0];
+        const bool m = better(tg[t][1], ts[t][1], og0, os0);
+        r1 = m ? tg[t][1] : og0; q1 = m ? ts[t][1] : os0;
+      } else {
+        r0 = og0; q0 = os0;
+        const bool m = better(tg[t][0], ts[t][0], og1, os1);
+        r1 = m ? tg[t][0] : og1; q1 = m ? ts[t][0] : os1;
+      }
+      const int64_t at = (((trow0 + 16 * t) * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
+      a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
+      a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
+      a.top_seed[at + 0] = (uint16_t)q0;
+      a.top_seed[at + 1] = (uint16_t)q1;
+    }
   }
 }
 
@@ -519,9 +746,9 @@ static hipError_t screen_mfma_fmt(const EncodeArgs& a, void* frag, hipStream_t s
   }
   const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
   if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL((k_screen_mfma64<true, POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_pe64<POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr);
   else
-    hipLaunchKernelGGL((k_screen_mfma64<false, POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_col64<POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   return hipGetLastError();
 }
 
