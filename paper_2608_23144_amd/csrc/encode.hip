@@ -83,6 +83,30 @@ __global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __res
   for (int j = 0; j < C; ++j) out[(int64_t)blk * C + j] = v[j];
 }
 
+// fp64 Cholesky factor of G + eps I for one seed: G_pq = wd[c_p ^ c_q] / C
+// (wd = WHT of the weights, read through any pointer type), G + eps I =
+// L L^T, inv_p = 1 / L_pp.  Padding columns p >= P get an identity row.
+template <int C, int PB, typename WD>
+__device__ __forceinline__ void chol64(int P, const WD& wd, const int (&c)[PB], double eps, double (&L)[PB][PB],
+                                       double (&inv)[PB]) {
+#pragma unroll
+  for (int p = 0; p < PB; ++p)
+#pragma unroll
+    for (int r = 0; r <= p; ++r) {
+      double acc;
+      if (p < P && r < P) acc = wd[c[p] ^ c[r]] / C + (p == r ? eps : 0.0);
+      else acc = (p == r) ? 1.0 : 0.0;
+#pragma unroll
+      for (int kk = 0; kk < r; ++kk) acc -= L[p][kk] * L[r][kk];
+      if (p == r) {
+        L[p][p] = sqrt(fmax(acc, 1e-300));
+        inv[p] = 1.0 / L[p][p];
+      } else {
+        L[p][r] = acc * inv[r];
+      }
+    }
+}
+
 // ----------------------------------------------------------------------------
 // Per-column factor table: for each (column block, seed), G = B^T D B + eps I
 // in fp64, its Cholesky factor stored in fp32 for the screen:
@@ -162,6 +186,25 @@ __global__ __launch_bounds__(64) void k_col_factors(EncodeArgs a, int nb, int st
 #pragma unroll
     for (int k = 0; k < p; ++k) acc -= L[p][k] * L[p][k] * e[k];
     e[p] = fmax(acc, 1e-300);
+  }
+  if (PB == kCholPB && a.chol64) {
+    // the fp64 re-score's factor of the same G, with eps = lambda * mean(d)
+    // summed in coordinate order as the re-score sums it
+    const double* wd = a.wd64 + (int64_t)blk * C;
+    double sum = 0.0;
+    for (int j = 0; j < C; ++j) sum += (double)a.d[(int64_t)blk * C + j];
+    int c[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) c[p] = (p < a.P) ? cs[p] : 0;
+    double Lc[PB][PB], inv[PB];
+    chol64<C, PB>(a.P, wd, c, a.lambda * (sum / C), Lc, inv);
+    double* fe = a.chol64 + (size_t)idx * kCholStride;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+#pragma unroll
+      for (int r = 0; r <= p; ++r) fe[p * (p + 1) / 2 + r] = Lc[p][r];
+      fe[kCholInv + p] = inv[p];
+    }
   }
   float* out = a.colfac + (size_t)idx * stride;
 #pragma unroll
@@ -380,6 +423,74 @@ __device__ __forceinline__ void tile_u64(const EncodeArgs& a, int64_t off, int b
   *sumd = sd;
 }
 
+// fp64 re-score of one candidate from its projections bv = B^T u and the
+// factor of its G + eps I: the solve for the unquantized fit al, the stored
+// scale (bits) and codes q, and the gain 2 a.b - a^T G0 a of the quantized
+// fit a = scale q (a^T G0 a = |L^T a|^2 - eps |a|^2).
+template <int PB>
+__device__ __forceinline__ double solve_score64(const EncodeArgs& a, const double (&bv)[PB], const double (&L)[PB][PB],
+                                                const double (&inv)[PB], double eps, int qmax, int (&q)[PB],
+                                                double (&al)[PB], uint16_t* bits_out) {
+  double z[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    double acc = bv[p];
+#pragma unroll
+    for (int kk = 0; kk < p; ++kk) acc -= L[p][kk] * z[kk];
+    z[p] = acc * inv[p];
+  }
+#pragma unroll
+  for (int p = PB - 1; p >= 0; --p) {
+    double acc = z[p];
+#pragma unroll
+    for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
+    al[p] = acc * inv[p];
+  }
+  double m = 0.0;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
+  uint16_t bits = 0;
+  double sc = 0.0;
+  if (m > 0.0) {
+    if (a.scale_fmt == AWSRC_SCALE_POW2) {
+      // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
+      int e;
+      frexp(m / (double)qmax, &e);
+      while (m > (double)qmax * ldexp(1.0, e)) ++e;
+      while (m <= (double)qmax * ldexp(1.0, e - 1)) --e;
+      e = e < -128 ? -128 : (e > 127 ? 127 : e);
+      bits = (uint16_t)(e + 128);
+      sc = ldexp(1.0, e);
+    } else {
+      // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
+      bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
+      sc = (double)__half2float(__ushort_as_half(bits));
+      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
+    }
+  }
+  double ah[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    double qv = 0.0;
+    if (sc > 0.0) qv = fmin(fmax(rint(al[p] / sc), (double)-qmax), (double)qmax);
+    q[p] = (int)qv;
+    ah[p] = sc * qv;
+  }
+  // gain = 2 a^T b - a^T G0 a, with a^T G0 a = |L^T a|^2 - eps |a|^2
+  double t1 = 0.0, aa = 0.0, quad = 0.0;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) { t1 += ah[p] * bv[p]; aa += ah[p] * ah[p]; }
+#pragma unroll
+  for (int kk = 0; kk < PB; ++kk) {
+    double y = 0.0;
+#pragma unroll
+    for (int i = kk; i < PB; ++i) y += L[i][kk] * ah[i];
+    quad += y * y;
+  }
+  *bits_out = bits;
+  return 2.0 * t1 - (quad - eps * aa);
+}
+
 template <int C, int PB, bool PE>
 __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __restrict__ wdb) {
   constexpr int NT = (C == 128) ? 32 : 64;  // rows per workgroup (keeps the LDS rows under 64 KiB)
@@ -503,81 +614,12 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
     } else {
       wd = wdb + (int64_t)blk * C;
     }
-    double L[PB][PB], inv[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p)
-#pragma unroll
-      for (int q = 0; q <= p; ++q) {
-        double acc;
-        if (p < P && q < P) acc = wd[c[p] ^ c[q]] / C + (p == q ? eps : 0.0);
-        else acc = (p == q) ? 1.0 : 0.0;
-#pragma unroll
-        for (int kk = 0; kk < q; ++kk) acc -= L[p][kk] * L[q][kk];
-        if (p == q) {
-          L[p][p] = sqrt(fmax(acc, 1e-300));
-          inv[p] = 1.0 / L[p][p];
-        } else {
-          L[p][q] = acc * inv[q];
-        }
-      }
-    double z[PB], al[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p) {
-      double acc = bv[p];
-#pragma unroll
-      for (int kk = 0; kk < p; ++kk) acc -= L[p][kk] * z[kk];
-      z[p] = acc * inv[p];
-    }
-#pragma unroll
-    for (int p = PB - 1; p >= 0; --p) {
-      double acc = z[p];
-#pragma unroll
-      for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
-      al[p] = acc * inv[p];
-    }
-    double m = 0.0;
-#pragma unroll
-    for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
-    uint16_t bits = 0;
-    double sc = 0.0;
-    if (m > 0.0) {
-      if (a.scale_fmt == AWSRC_SCALE_POW2) {
-        // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
-        int e;
-        frexp(m / (double)qmax, &e);
-        while (m > (double)qmax * ldexp(1.0, e)) ++e;
-        while (m <= (double)qmax * ldexp(1.0, e - 1)) --e;
-        e = e < -128 ? -128 : (e > 127 ? 127 : e);
-        bits = (uint16_t)(e + 128);
-        sc = ldexp(1.0, e);
-      } else {
-        // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
-        bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
-        sc = (double)__half2float(__ushort_as_half(bits));
-        if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
-      }
-    }
     int q[PB];
-    double ah[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p) {
-      double qv = 0.0;
-      if (sc > 0.0) qv = fmin(fmax(rint(al[p] / sc), (double)-qmax), (double)qmax);
-      q[p] = (int)qv;
-      ah[p] = sc * qv;
-    }
-    // gain = 2 a^T b - a^T G0 a, with a^T G0 a = |L^T a|^2 - eps |a|^2
-    double t1 = 0.0, aa = 0.0, quad = 0.0;
-#pragma unroll
-    for (int p = 0; p < PB; ++p) { t1 += ah[p] * bv[p]; aa += ah[p] * ah[p]; }
-#pragma unroll
-    for (int kk = 0; kk < PB; ++kk) {
-      double y = 0.0;
-#pragma unroll
-      for (int i = kk; i < PB; ++i) y += L[i][kk] * ah[i];
-      quad += y * y;
-    }
-    const double gsum = 2.0 * t1 - (quad - eps * aa);
+    double al[PB];
+    uint16_t bits;
+    double L[PB][PB], inv[PB];
+    chol64<C, PB>(P, wd, c, eps, L, inv);
+    const double gsum = solve_score64<PB>(a, bv, L, inv, eps, qmax, q, al, &bits);
     if (gsum > best_g || (gsum == best_g && s < best_s)) {
       best_g = gsum;
       best_s = s;
@@ -594,6 +636,169 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
     if (p < P) {
       a.code_out[t * P + p] = (int8_t)best_q[p];
       if (a.alpha_out) a.alpha_out[t * P + p] = best_al[p];
+    }
+  }
+}
+
+// Per-column weights, generator version 1, C = 64 (the common case).  Each
+// lane keeps its tile in registers (fp64) and transforms it in place; only
+// the gather of the P projections out of the transform goes through LDS,
+// half a wavefront at a time.  A workgroup thus needs half the LDS of
+// k_finalize, and two wavefronts fit per SIMD.  The second kept seed (a
+// near tie, rare) reloads the tile.
+template <int PB>
+__global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
+  constexpr int C = 64;
+  __shared__ double gb[32 * (C + 1)];
+  const int lane = threadIdx.x;
+  const int nb = (int)(a.cols / C);
+  // Workgroups are dealt to the 8 XCDs round-robin by index: give each XCD a
+  // contiguous run of (row group, column block) items, so that neighbouring
+  // column blocks (adjacent per-tile outputs) share one L2.
+  const int64_t nwg = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, qq = nwg / 8, rem = nwg % 8;
+  const int64_t w = xcd * qq + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
+  const int blk = (int)(w % nb);
+  const int64_t row = (w / nb) * 64 + lane;
+  const float* dcol = a.d + (int64_t)blk * C;
+  // the block's d, one coordinate per lane (C = wavefront size), staged by
+  // every lane before the rows past the end leave
+  __shared__ float dsh[C];
+  dsh[lane] = dcol[lane];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (row >= a.rows) return;  // no cross-lane exchange below but the gather's (per row pair)
+  const int64_t off = row * a.cols + (int64_t)blk * C;
+  const int64_t t = row * nb + blk;
+  const int P = a.P;
+  const double isq = 1.0 / sqrt((double)C);
+  const int qmax = (1 << (a.b - 1)) - 1;
+  double* grow = &gb[(lane & 31) * (C + 1)];
+
+  // merge the seed ranges' lists into the best kTop (as in k_finalize)
+  float tg[kTop];
+  int ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+  for (int sp = 0; sp < a.nsplit; ++sp) {
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      const int64_t at = (t * a.nsplit + sp) * kTop + k;
+      float g = a.top_gain[at];
+      int sd = a.top_seed[at];
+#pragma unroll
+      for (int m = 0; m < kTop; ++m) {
+        if (g > tg[m]) {
+          const float tgm = tg[m];
+          const int tsm = ts[m];
+          tg[m] = g; ts[m] = sd;
+          g = tgm; sd = tsm;
+        }
+      }
+    }
+  }
+
+  // Score seed s: u = d .* r in fp64 (also the tile's weighted energy e32 and
+  // sum of d), sigma .* u transformed in place, the P projections gathered
+  // through this lane's LDS row (lanes l and l + 32 share a row, so the two
+  // halves take turns, ordered by the wavefront barriers), then the solve
+  // with the block's factor for s.
+  auto score = [&](int s, float* e32, int (&q)[PB], double (&al)[PB], uint16_t* bits) -> double {
+    // r = W - W0 (fp32) first, so that only the loads and r are live, then
+    // u with the block's d from LDS
+    float rr[C];
+#pragma unroll
+    for (int j0 = 0; j0 < C; j0 += 8) {
+      float wv[8], w0[8];
+      load8_w(a.W, a.w_dtype, off + j0, wv);
+      load8_f(a.W0 + off + j0, w0);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) rr[j0 + k] = wv[k] - w0[k];
+    }
+    double u[C];
+    float e = 0.0f;
+    double sumd = 0.0;
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      const float dj = dsh[j];
+      e += dj * rr[j] * rr[j];
+      sumd += (double)dj;
+      u[j] = (double)dj * (double)rr[j];
+    }
+    // pin e and sumd here: left to the compiler, their sums sink to their
+    // uses after the transform and keep r and d live (and spilled) across it
+    asm volatile("" ::"v"(e), "v"(sumd));
+    *e32 = e;
+    const double eps = a.lambda * (sumd / C);
+    const uint64_t s0 = a.basis.sign[(size_t)s * 2];
+    int c[PB];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) c[p] = (p < P) ? a.basis.col[(size_t)s * kMaxP + p] : 0;
+#pragma unroll
+    for (int i = 0; i < C; ++i) u[i] = ((s0 >> i) & 1ull) ? -u[i] : u[i];
+    fwht<C>(u);
+    double bv[PB];
+#pragma unroll
+    for (int ph = 0; ph < 2; ++ph) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if ((lane >> 5) == ph) {
+#pragma unroll
+        for (int j = 0; j < C; ++j) grow[j] = u[j];
+#pragma unroll
+        for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? grow[c[p]] * isq : 0.0;
+      }
+    }
+    // the transform is dead from here: keep the factor loads below it
+    __builtin_amdgcn_sched_barrier(0);
+    double L[PB][PB], inv[PB];
+    // (PB <= kCholPB: the leading rows of the table's factor are this
+    // system's factor)
+    const double* fe = a.chol64 + ((size_t)blk * a.S + s) * kCholStride;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+#pragma unroll
+      for (int r = 0; r <= p; ++r) L[p][r] = fe[p * (p + 1) / 2 + r];
+      inv[p] = fe[kCholInv + p];
+    }
+    return solve_score64<PB>(a, bv, L, inv, eps, qmax, q, al, bits);
+  };
+
+  int best_q[PB];
+  double best_al[PB];
+  uint16_t best_bits;
+  float e32;
+  int best_s = ts[0];
+  double best_g = score(best_s, &e32, best_q, best_al, &best_bits);
+  // the second kept seed only when its screened gain is close to the best
+  const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
+#pragma unroll
+  for (int k = 1; k < kTop; ++k) {
+    if (tg[k] >= thr && tg[k] > -INFINITY) {
+      int q[PB];
+      double al[PB];
+      uint16_t bits;
+      float e_;
+      const double g = score(ts[k], &e_, q, al, &bits);
+      if (g > best_g || (g == best_g && ts[k] < best_s)) {
+        best_g = g;
+        best_s = ts[k];
+        best_bits = bits;
+#pragma unroll
+        for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = al[p]; }
+      }
+    }
+  }
+  a.seed_out[t] = (uint16_t)best_s;
+  a.scale_out[t] = best_bits;
+  a.gain_out[t] = best_g;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    if (p < P) {
+      a.code_out[t * P + p] = (int8_t)best_q[p];
+      if (a.alpha_out) a.alpha_out[t * P + p] = (float)best_al[p];
     }
   }
 }
@@ -644,6 +849,8 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
   if (a.d_mode == AWSRC_D_PER_ELEM) {
     hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)nullptr);
+  } else if (a.chol64) {
+    hipLaunchKernelGGL((k_finalize_col64<PB>), dim3((unsigned)groups), dim3(64), 0, st, a);
   } else {
     hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)a.wd64);

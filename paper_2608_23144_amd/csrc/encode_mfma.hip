@@ -392,7 +392,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
     }
   };
   // queue: qhead, qlen, and the pair of the head entry (INT_MAX when empty)
-  int qhead = 0, qlen = 0, hp = INT_MAX;
+  int qhead = 0, qtail = 0, qlen = 0, hp = INT_MAX;
   auto score_round = [&]() {
     if (qlen > 0) {
       const float* e = &qb[qhead * (QW * 64) + lane];
@@ -426,6 +426,22 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   };
   auto fac_store = [&](int pr, const f32x4& v) {
     *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NF) + 4 * pc]) = v;
+  };
+
+  // each tile's second score over both lanes' lists (lane ^ 32 holds the
+  // other seed parity): the second largest of {a0 >= a1} and {b0 >= b1} is
+  // max(min(a0, b0), max(a1, b1)); lists change only in scoring rounds
+  float thr[2] = {-INFINITY, -INFINITY};
+  auto update_thr = [&]() {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][0]), __float_as_uint(tg[t][0]), false,
+                                                       false);
+      const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][1]), __float_as_uint(tg[t][1]), false,
+                                                       false);
+      const float o0 = __uint_as_float(sh ? r0[0] : r0[1]), o1 = __uint_as_float(sh ? r1[0] : r1[1]);
+      thr[t] = fmaxf(fminf(tg[t][0], o0), fmaxf(tg[t][1], o1));
+    }
   };
 
   // Raw units and the software pipeline as in k_screen_pe64: b is left
@@ -478,19 +494,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
         bt[t][i] = __uint_as_float(r[0]);
         bt[t][4 + i] = __uint_as_float(r[1]);
       }
-    // each tile's second score over both lanes' lists (lane ^ 32 holds the
-    // other seed parity): the second largest of {a0 >= a1} and {b0 >= b1}
-    // is max(min(a0, b0), max(a1, b1))
-    float thr[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][0]), __float_as_uint(tg[t][0]), false,
-                                                       false);
-      const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][1]), __float_as_uint(tg[t][1]), false,
-                                                       false);
-      const float o0 = __uint_as_float(sh ? r0[0] : r0[1]), o1 = __uint_as_float(sh ? r1[0] : r1[1]);
-      thr[t] = fmaxf(fminf(tg[t][0], o0), fmaxf(tg[t][1], o1));
-    }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       float wv[PB];
@@ -500,12 +503,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
       // interleaved with this work); bitwise: a short-circuit would put the
       // bound under a branch
       const bool keep = (int)(bnd * kSlack > thr[t]) & (int)tv[t] & (int)(s < a.S);
-      float* e = &qb[(keep ? ((qhead + qlen) & (QD - 1)) : QD) * (QW * 64) + lane];
+      float* e = &qb[(keep ? qtail : QD) * (QW * 64) + lane];
 #pragma unroll
       for (int i = 0; i < PB; ++i) e[i * 64] = wv[i];
       e[PB * 64] = __int_as_float(s | (t << 16));
       hp = (keep && qlen == 0) ? pair : hp;
       qlen += keep ? 1 : 0;
+      qtail = keep ? ((qtail + 1) & (QD - 1)) : qtail;
     }
 #pragma unroll
     for (int i = 0; i < 24; ++i) {
@@ -514,7 +518,12 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
     }
     // room for the next pair's two entries, and no entry of the pair whose
     // slot the next pair refills
-    while (__ballot(qlen > QD - 2 || hp <= pair + 2 - NR) != 0) score_round();
+    if (__ballot(qlen > QD - 2 || hp <= pair + 2 - NR) != 0) {
+      do {
+        score_round();
+      } while (__ballot(qlen > QD - 2 || hp <= pair + 2 - NR) != 0);
+      update_thr();
+    }
   };
   int pair = pair0;
   for (; pair + 1 < pair1; pair += 2) {
