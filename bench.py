@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 METRIC = "encoded tile-seed candidates/sec + decode-add GB/s (fraction of roofline), 1 GPU"
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PEAK_VALU_TOPS = 78.6            # fp32 vector lane-ops/s (157.3 TFLOP/s counting FMA as 2)
+PEAK_MFMA_BF16_TFLOPS = 2500.0   # dense bf16 matrix-core flops/s
 
 
 def log(*a):
@@ -210,6 +211,32 @@ def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps, bpw):
             "traffic": measured_traffic("reconstruct_bf16", f"{wl.name}@{bpw}")}
 
 
+def mfma_screen(C: int, P: int, per_element: bool, gen_version: int) -> bool:
+    """The encoder's matrix-core screen runs (projection as exact bf16 x 3 products)."""
+    if P > 8 or (per_element and gen_version != 1):
+        return False
+    return C == 64 or (C == 128 and not per_element)
+
+
+def bound_ops_per_candidate(P: int) -> float:
+    """Vector work of the pruning bound per candidate: the forward solve with the
+    unit lower factor (P(P-1)/2), sum of w_p^2 / e_p (2P) and the comparison."""
+    return P * (P - 1) / 2 + 2 * P + 1
+
+
+def encode_split_bound(C: int, P: int, per_element: bool, gen_version: int, scored_frac: float) -> dict:
+    """Split roofline of the encoder with the projection on the matrix cores:
+    6 P C bf16 flops per candidate there (three exact bf16 parts of fp32 u),
+    and on the vector ALUs the post-projection work: every candidate's bound
+    plus, for the fraction scored in full, the rest of the unpruned count
+    (ops_per_candidate less the projection).  Without pruning the fraction is 1."""
+    proj = min(P * C, C * int(math.log2(C)))
+    full = ops_per_candidate(C, P, per_element, gen_version) - proj
+    bnd = bound_ops_per_candidate(P)
+    valu = bnd + scored_frac * (full - bnd) if scored_frac < 1.0 else full
+    return {"mfma_flops_per_candidate": 6.0 * P * C, "valu_ops_per_candidate": valu}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -307,7 +334,25 @@ def main() -> int:
     per_elem = wl.d_mode == "elem"
     opc = ops_per_candidate(wl.C, wl.P, per_elem, args.gen_version)
     enc_s = stage_ms["encode"] / 1e3
-    achieved = cand * opc / enc_s / 1e12
+    # candidates scored in full by the last step's screens (the pruned screen
+    # scores a data-dependent part; every other screen scores all)
+    scored = sum(awsrc.awsrc_encode_scored(e) for e in enc_out)
+    f_scored = scored / cand
+    if mfma_screen(wl.C, wl.P, per_elem, args.gen_version):
+        sb = encode_split_bound(wl.C, wl.P, per_elem, args.gen_version, f_scored)
+        t_mfma = cand * sb["mfma_flops_per_candidate"] / (PEAK_MFMA_BF16_TFLOPS * 1e12)
+        t_valu = cand * sb["valu_ops_per_candidate"] / (PEAK_VALU_TOPS * 1e12)
+        if t_mfma >= t_valu:
+            bound, unit, peak = "mfma", "TFLOP/s", PEAK_MFMA_BF16_TFLOPS
+            achieved = cand * sb["mfma_flops_per_candidate"] / enc_s / 1e12
+        else:
+            bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
+            achieved = cand * sb["valu_ops_per_candidate"] / enc_s / 1e12
+        split = dict(sb, scored_fraction=f_scored, t_mfma_ms=1e3 * t_mfma, t_valu_ms=1e3 * t_valu)
+    else:
+        bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
+        achieved = cand * opc / enc_s / 1e12
+        split = {"scored_fraction": f_scored}
     K, L = last["K"], last["L"]
     dec_bytes = K * (L + 2 * wl.C * 4)
     dec_gbs = dec_bytes / (stage_ms["decode_apply"] / 1e3) / 1e9 if stage_ms["decode_apply"] > 0 else None
@@ -322,11 +367,11 @@ def main() -> int:
         "config": {"workload": wl.name, "modules": [f"{r}x{c}" for r, c in shapes], "C": wl.C, "P": wl.P,
                    "b": wl.b, "S": wl.S, "weights": wl.d_mode, "mode": wl.mode, "bpw": bpw, "tiles": T,
                    "candidates": cand, "generator": args.gen_version},
-        "roofline": {"bound": "alu", "kernel": "awsrc_encode_tiles (basis, factors, screen, finalize)",
-                     "achieved": achieved, "peak": PEAK_VALU_TOPS, "unit": "Tops/s",
-                     "frac": achieved / PEAK_VALU_TOPS,
+        "roofline": {"bound": bound, "kernel": "awsrc_encode_tiles (basis, factors, screen, fp64 re-score)",
+                     "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                      "traffic": measured_traffic("encode", wl.name) if args.gen_version == 1 else None,
-                     "traffic_unit": "bytes per launch", "ops_per_candidate": opc},
+                     "traffic_unit": "bytes per launch", "split": split,
+                     "ops_per_candidate_unpruned": opc},
         "encode_candidates_per_s": cand / enc_s,
         "decode_add": {"records": K, "bytes": dec_bytes, "ms": stage_ms["decode_apply"], "GB/s": dec_gbs,
                        "frac_hbm": (dec_gbs / PEAK_HBM_GBS) if dec_gbs else None,

@@ -160,6 +160,20 @@ awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_
                                 void* workspace, size_t* ws_bytes, void* stream);
 
 /*
+ * Work statistic of the last awsrc_encode_tiles call that used `workspace`
+ * (same pointer): the number of (tile, seed) candidates scored in full in
+ * the fp32 screen, ordered on `stream` after that call.  The screen for
+ * per-column weights at C = 64 first bounds every candidate by the score of
+ * its unquantized fit (Eq. (3) without the rounding of Sec. 3.2's codes,
+ * which no quantized fit can exceed) and scores in full only those whose
+ * bound reaches the tile's current second-best score; the other screens
+ * score all T * S.  The result is the same either way; the count measures
+ * the work.  Reads 8 bytes of device memory and synchronizes the stream.
+ * EINVAL: NULL argument.
+ */
+awsrc_status awsrc_encode_scored(const void* workspace, uint64_t* scored, void* stream);
+
+/*
  * Byte-budgeted, gain-ranked record selection and serialization (Eq. (4),
  * Sec. 3.3, Eq. (5)).  The per-tile encoder outputs of n_modules modules are
  * given concatenated in module order (global tile index = tiles of earlier

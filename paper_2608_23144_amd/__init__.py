@@ -25,7 +25,7 @@ AWSRC_MODE_GLOBAL, AWSRC_MODE_PER_MODULE = 0, 1
 AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_encode_tiles",
-            "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
+            "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
             "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
 
@@ -67,6 +67,7 @@ def _load() -> ctypes.CDLL:
         "awsrc_backbone_rtn": (i32, [vp, i32, i64, i64, i32, vp, vp, vp, vp, vp]),
         "awsrc_encode_tiles": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp,
                                      ctypes.POINTER(sz), vp]),
+        "awsrc_encode_scored": (i32, [vp, ctypes.POINTER(u64), vp]),
         "awsrc_rank_prefix": (i32, [pp, i32, P64, P64, i32, ctypes.c_double, vp, vp, vp, vp, vp, u64,
                                     ctypes.POINTER(u64), P64, P64, vp, ctypes.POINTER(sz), vp]),
         "awsrc_decode_add": (i32, [vp, u64, i32, ctypes.POINTER(vp), P64, P64, i32, vp,
@@ -192,7 +193,15 @@ def awsrc_encode_tiles(p: awsrc_params, W: torch.Tensor, W0: torch.Tensor, d: to
                                   d_mode, _ptr(out["seed"]), _ptr(out["codes"]), _ptr(out["scale"]),
                                   _ptr(out["gain"]), _ptr(out.get("alpha")), _ptr(workspace),
                                   ctypes.byref(n), _stream(stream)))
+    out["workspace"] = workspace
     return out
+
+
+def awsrc_encode_scored(out: Dict[str, torch.Tensor], stream=None) -> int:
+    """Candidates scored in full by the last awsrc_encode_tiles call that filled `out`."""
+    v = ctypes.c_uint64(0)
+    _check(LIB.awsrc_encode_scored(_ptr(out["workspace"]), ctypes.byref(v), _stream(stream)))
+    return int(v.value)
 
 
 def _i64arr(v: Sequence[int]):

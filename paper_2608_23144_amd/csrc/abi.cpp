@@ -174,7 +174,8 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
-  const size_t need = b_basis + b_fac + b_wd + b_chol + b_frag + b_tg + b_ts + 256;
+  const size_t b_stats = 256;  // first: the full-score count (awsrc_encode_scored)
+  const size_t need = b_stats + b_basis + b_fac + b_wd + b_chol + b_frag + b_tg + b_ts + 256;
   if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
   if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
   if (T == 0) return AWSRC_OK;
@@ -189,6 +190,8 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.lambda = p->ridge_lambda;
   a.scale_fmt = p->scale_fmt;
   a.gen_version = p->gen_version;
+  a.scored = reinterpret_cast<unsigned long long*>(ws);
+  ws += b_stats;
   a.basis = carve_basis(ws, p->S, p->P);
   ws += b_basis;
   a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
@@ -206,10 +209,23 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
   hipStream_t s = (hipStream_t)stream;
+  HIPCHK(launch_scored_init(a, s));
   HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
   if (d_mode == AWSRC_D_PER_COL) HIPCHK(launch_col_factors(a, s));
   HIPCHK(launch_encode_screen(a, s));
   HIPCHK(launch_encode_finalize(a, s));
+  return AWSRC_OK;
+}
+
+extern "C" awsrc_status awsrc_encode_scored(const void* workspace, uint64_t* scored, void* stream) {
+  if (!workspace || !scored) return fail(AWSRC_EINVAL, "NULL argument");
+  const char* ws = reinterpret_cast<const char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* stage = pinned_staging(64);
+  if (!stage) return fail(AWSRC_EDEVICE, "pinned host staging buffer unavailable");
+  HIPCHK(hipMemcpyAsync(stage, ws, 8, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  memcpy(scored, stage, 8);
   return AWSRC_OK;
 }
 

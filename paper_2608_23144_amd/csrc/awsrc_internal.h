@@ -205,6 +205,7 @@ struct EncodeArgs {
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
   double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
   double* chol64;      // fp64 Cholesky table [nb][S][kCholStride] of the re-score, or NULL
+  unsigned long long* scored;  // count of candidates scored in full (the pruned screen adds to it)
   void* frag;          // +-1 basis fragments of the matrix-core screen
   float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending
   uint16_t* top_seed;  // [T][nsplit][kTop]
@@ -228,6 +229,11 @@ hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_
 hipError_t launch_col_factors(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_screen(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);
+// Sets *a.scored to the count of candidates the screen will score in full
+// without the pruned screen's help: 0 when it runs (it adds its own), else
+// every candidate.
+hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st);
+bool screen_pruned(int C, int P, int d_mode, int gen_version);
 
 // ---------------------------------------------------------------- ranking
 // One survivor of the selection: ~(gain key) and its global tile index.

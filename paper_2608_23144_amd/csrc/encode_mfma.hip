@@ -393,6 +393,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   };
   // queue: qhead, qlen, and the pair of the head entry (INT_MAX when empty)
   int qhead = 0, qtail = 0, qlen = 0, hp = INT_MAX;
+  int nscored = 0;  // candidates this lane scored in full
   auto score_round = [&]() {
     if (qlen > 0) {
       const float* e = &qb[qhead * (QW * 64) + lane];
@@ -411,6 +412,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
       insert(code >> 16, screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax), s);
       qhead = (qhead + 1) & (QD - 1);
       --qlen;
+      ++nscored;
       // the next entry's seed (any word when the queue is now empty)
       const int nx = __float_as_int(qb[qhead * (QW * 64) + PB * 64 + lane]);
       hp = qlen > 0 ? (nx & 0xFFFF) >> 1 : INT_MAX;
@@ -532,6 +534,10 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   }
   if (pair < pair1) step(pair, accA, accB, FA0, FA1, FB0, FB1);
   while (__ballot(qlen > 0) != 0) score_round();
+  // the wavefront's count of full scores, added once
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) nscored += __shfl_xor(nscored, m, 64);
+  if (lane == 0) atomicAdd(a.scored, (unsigned long long)nscored);
 
   // merge each tile's lists from lanes g (this seed parity) and g ^ 2 (the
   // other): (gain desc, seed asc)
@@ -739,6 +745,21 @@ int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode, i
   int ns = 1;
   while (ns < 8 && waves * ns < 2048 && pairs / (2 * ns) >= 16) ns *= 2;
   return ns;
+}
+
+bool screen_pruned(int C, int P, int d_mode, int gen_version) {
+  return C == 64 && screen_mfma_supported(C, P, d_mode, gen_version) && d_mode == AWSRC_D_PER_COL;
+}
+
+__global__ void k_scored_init(unsigned long long* p, unsigned long long v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
+hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st) {
+  const unsigned long long all = (unsigned long long)(a.rows * (a.cols / a.C)) * (unsigned long long)a.S;
+  hipLaunchKernelGGL(k_scored_init, dim3(1), dim3(64), 0, st, a.scored,
+                     screen_pruned(a.C, a.P, a.d_mode, a.gen_version) ? 0ull : all);
+  return hipGetLastError();
 }
 
 // the table carries two zero pairs past the last seed (see the pipeline above)

@@ -247,6 +247,27 @@ def test_encode_full_size_sampled(name, n_tiles):
         torch.cuda.empty_cache()
 
 
+def test_encode_scored_count():
+    """awsrc_encode_scored: the pruned screen (per-column weights, C = 64)
+    scores every tile's first pair of seeds and, on realistic data, a small
+    part of the rest; the per-element screen scores every candidate.  The
+    module has enough row groups that each wavefront searches all S seeds
+    (with seed ranges split over wavefronts, each range starts its pruning
+    afresh)."""
+    wl = WORKLOADS["down3b"]
+    m = Module("scored", 2048, 4096, 0, 1, 1)
+    inp, bb, enc = _gpu_module(wl, m)
+    T, S = m.rows * m.cols // wl.C, wl.S
+    sc = awsrc.awsrc_encode_scored(enc)
+    assert 2 * T <= sc < T * S // 8, (sc, T * S)
+    idx = np.arange(0, T, 997)
+    assert _check_encode_sample(wl, m, inp, bb[3], enc, idx) <= 1
+    wl2 = WORKLOADS["block3b"]
+    m2 = Module("scored_pe", 64, 256, 0, 1, 1)
+    _, _, enc2 = _gpu_module(wl2, m2)
+    assert awsrc.awsrc_encode_scored(enc2) == (64 * 256 // wl2.C) * wl2.S
+
+
 # ------------------------------------------------------------------ ranking
 @pytest.mark.parametrize("mode", ["global", "per_module"])
 @pytest.mark.parametrize("bpw", [0.05, 0.162, 2.0, 64.0])
