@@ -168,14 +168,12 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
   const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
-  const size_t b_chol = chol64_used(p->C, p->P, d_mode, p->gen_version)
-                            ? align_up((size_t)nb * p->S * kCholStride * 8, 256) : 0;
   const size_t b_frag = screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
   const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
   const size_t b_stats = 256;  // first: the full-score count (awsrc_encode_scored)
-  const size_t need = b_stats + b_basis + b_fac + b_wd + b_chol + b_frag + b_tg + b_ts + 256;
+  const size_t need = b_stats + b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
   if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
   if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
   if (T == 0) return AWSRC_OK;
@@ -198,8 +196,6 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   ws += b_fac;
   a.wd64 = b_wd ? reinterpret_cast<double*>(ws) : nullptr;
   ws += b_wd;
-  a.chol64 = b_chol ? reinterpret_cast<double*>(ws) : nullptr;
-  ws += b_chol;
   a.frag = b_frag ? static_cast<void*>(ws) : nullptr;
   ws += b_frag;
   a.top_gain = reinterpret_cast<float*>(ws);

@@ -73,18 +73,6 @@ inline int colfac_stride(int P) {
   return (n + 3) & ~3;
 }
 
-// The fp64 re-score's factor table: per (column block, seed), G + eps I =
-// L L^T with eps = lambda * mean(d) of the block, padded to kCholPB columns
-// (identity rows past P): the lower L packed row by row (entry (p, q),
-// q <= p, at p (p + 1) / 2 + q), then 1 / L_pp at kCholInv + p.  Built with
-// the per-column factors when the re-score uses it (per-column weights,
-// generator version 1, C = 64, P <= 8).
-constexpr int kCholPB = 8;
-constexpr int kCholInv = kCholPB * (kCholPB + 1) / 2;
-constexpr int kCholStride = kCholInv + kCholPB;
-inline bool chol64_used(int C, int P, int d_mode, int gen_version) {
-  return C == 64 && P <= 8 && d_mode == AWSRC_D_PER_COL && gen_version == 1;
-}
 
 __host__ __device__ __forceinline__ int ltri(int p, int k) { return p * (p - 1) / 2 + k; }
 
@@ -204,7 +192,6 @@ struct EncodeArgs {
   BasisTables basis;
   float* colfac;       // per-column factor table [nb][S][stride] (d_mode == PER_COL)
   double* wd64;        // per-column fp64 Walsh-Hadamard transform of d per block [nb][C]
-  double* chol64;      // fp64 Cholesky table [nb][S][kCholStride] of the re-score, or NULL
   unsigned long long* scored;  // count of candidates scored in full (the pruned screen adds to it)
   void* frag;          // +-1 basis fragments of the matrix-core screen
   float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending

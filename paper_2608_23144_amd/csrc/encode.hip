@@ -187,25 +187,6 @@ __global__ __launch_bounds__(64) void k_col_factors(EncodeArgs a, int nb, int st
     for (int k = 0; k < p; ++k) acc -= L[p][k] * L[p][k] * e[k];
     e[p] = fmax(acc, 1e-300);
   }
-  if (PB == kCholPB && a.chol64) {
-    // the fp64 re-score's factor of the same G, with eps = lambda * mean(d)
-    // summed in coordinate order as the re-score sums it
-    const double* wd = a.wd64 + (int64_t)blk * C;
-    double sum = 0.0;
-    for (int j = 0; j < C; ++j) sum += (double)a.d[(int64_t)blk * C + j];
-    int c[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p) c[p] = (p < a.P) ? cs[p] : 0;
-    double Lc[PB][PB], inv[PB];
-    chol64<C, PB>(a.P, wd, c, a.lambda * (sum / C), Lc, inv);
-    double* fe = a.chol64 + (size_t)idx * kCholStride;
-#pragma unroll
-    for (int p = 0; p < PB; ++p) {
-#pragma unroll
-      for (int r = 0; r <= p; ++r) fe[p * (p + 1) / 2 + r] = Lc[p][r];
-      fe[kCholInv + p] = inv[p];
-    }
-  }
   float* out = a.colfac + (size_t)idx * stride;
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
@@ -653,18 +634,51 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   const int lane = threadIdx.x;
   const int nb = (int)(a.cols / C);
   // Workgroups are dealt to the 8 XCDs round-robin by index: give each XCD a
-  // contiguous run of (row group, column block) items, so that neighbouring
-  // column blocks (adjacent per-tile outputs) share one L2.
+  // contiguous run of work items in column-block-major order (the block's d
+  // and weight transform stay in its L2).
   const int64_t nwg = gridDim.x;
   const int64_t xcd = blockIdx.x % 8, qq = nwg / 8, rem = nwg % 8;
   const int64_t w = xcd * qq + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
-  const int blk = (int)(w % nb);
-  const int64_t row = (w / nb) * 64 + lane;
+  const int64_t nrg = (a.rows + 63) / 64;
+  const int blk = (int)(w / nrg);
+  const int64_t row = (w % nrg) * 64 + lane;
   const float* dcol = a.d + (int64_t)blk * C;
   // the block's d, one coordinate per lane (C = wavefront size), staged by
   // every lane before the rows past the end leave
   __shared__ float dsh[C];
+  __shared__ double wdsh[C];  // WHT(d) of the block, for the Gram entries
   dsh[lane] = dcol[lane];
+  wdsh[lane] = a.wd64[(int64_t)blk * C + lane];
+  // The work item's 64 x 64 residual block r = W - W0 (fp32) through LDS:
+  // loaded with 16 lanes per row segment (4 rows per pass), so each cache
+  // line is read whole by one instruction, then each lane reads its own row.
+  // (Row-per-lane loads of 16 bytes leave each line to 8 or 16 separate
+  // instructions, and with two wavefronts per SIMD the lines in flight
+  // outgrow the L2 and are fetched again.)  The gather buffer holds the rows.
+  float* rsh = reinterpret_cast<float*>(gb);  // [64][C + 1]
+  {
+    const int64_t row0 = (w % nrg) * 64;
+    const int pc = lane & 15;
+#pragma unroll
+    for (int pass = 0; pass < 16; ++pass) {
+      const int rl = 4 * pass + (lane >> 4);
+      const int64_t rg = row0 + rl < a.rows ? row0 + rl : a.rows - 1;
+      const int64_t o = rg * a.cols + (int64_t)blk * C + 4 * pc;
+      float wv[4], w0[4];
+      if (a.w_dtype == AWSRC_DTYPE_F32) {
+        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.W) + o);
+        wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
+      } else {
+        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.W) + o);
+        wv[0] = __uint_as_float(x.x << 16); wv[1] = __uint_as_float(x.x & 0xFFFF0000u);
+        wv[2] = __uint_as_float(x.y << 16); wv[3] = __uint_as_float(x.y & 0xFFFF0000u);
+      }
+      const float4 y = *reinterpret_cast<const float4*>(a.W0 + o);
+      w0[0] = y.x; w0[1] = y.y; w0[2] = y.z; w0[3] = y.w;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rsh[rl * (C + 1) + 4 * pc + k] = wv[k] - w0[k];
+    }
+  }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -703,18 +717,24 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   // sum of d), sigma .* u transformed in place, the P projections gathered
   // through this lane's LDS row (lanes l and l + 32 share a row, so the two
   // halves take turns, ordered by the wavefront barriers), then the solve
-  // with the block's factor for s.
-  auto score = [&](int s, float* e32, int (&q)[PB], double (&al)[PB], uint16_t* bits) -> double {
-    // r = W - W0 (fp32) first, so that only the loads and r are live, then
-    // u with the block's d from LDS
+  // with the Cholesky factor of the seed's G + eps I.
+  auto score = [&](int s, bool first, float* e32, int (&q)[PB], double (&al)[PB], uint16_t* bits) -> double {
+    // r: the first seed's from the LDS rows, a second seed's (a rare near
+    // tie, after the gather has reused the buffer) loaded directly; then u
+    // with the block's d from LDS
     float rr[C];
+    if (first) {
 #pragma unroll
-    for (int j0 = 0; j0 < C; j0 += 8) {
-      float wv[8], w0[8];
-      load8_w(a.W, a.w_dtype, off + j0, wv);
-      load8_f(a.W0 + off + j0, w0);
+      for (int j = 0; j < C; ++j) rr[j] = rsh[lane * (C + 1) + j];
+    } else {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) rr[j0 + k] = wv[k] - w0[k];
+      for (int j0 = 0; j0 < C; j0 += 8) {
+        float wv[8], w0[8];
+        load8_w(a.W, a.w_dtype, off + j0, wv);
+        load8_f(a.W0 + off + j0, w0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) rr[j0 + k] = wv[k] - w0[k];
+      }
     }
     double u[C];
     float e = 0.0f;
@@ -751,18 +771,10 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
         for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? grow[c[p]] * isq : 0.0;
       }
     }
-    // the transform is dead from here: keep the factor loads below it
+    // the transform is dead from here
     __builtin_amdgcn_sched_barrier(0);
     double L[PB][PB], inv[PB];
-    // (PB <= kCholPB: the leading rows of the table's factor are this
-    // system's factor)
-    const double* fe = a.chol64 + ((size_t)blk * a.S + s) * kCholStride;
-#pragma unroll
-    for (int p = 0; p < PB; ++p) {
-#pragma unroll
-      for (int r = 0; r <= p; ++r) L[p][r] = fe[p * (p + 1) / 2 + r];
-      inv[p] = fe[kCholInv + p];
-    }
+    chol64<C, PB>(P, wdsh, c, eps, L, inv);
     return solve_score64<PB>(a, bv, L, inv, eps, qmax, q, al, bits);
   };
 
@@ -771,7 +783,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   uint16_t best_bits;
   float e32;
   int best_s = ts[0];
-  double best_g = score(best_s, &e32, best_q, best_al, &best_bits);
+  double best_g = score(best_s, true, &e32, best_q, best_al, &best_bits);
   // the second kept seed only when its screened gain is close to the best
   const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
 #pragma unroll
@@ -781,7 +793,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
       double al[PB];
       uint16_t bits;
       float e_;
-      const double g = score(ts[k], &e_, q, al, &bits);
+      const double g = score(ts[k], false, &e_, q, al, &bits);
       if (g > best_g || (g == best_g && ts[k] < best_s)) {
         best_g = g;
         best_s = ts[k];
@@ -849,8 +861,9 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
   if (a.d_mode == AWSRC_D_PER_ELEM) {
     hipLaunchKernelGGL((k_finalize<C, PB, true>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)nullptr);
-  } else if (a.chol64) {
-    hipLaunchKernelGGL((k_finalize_col64<PB>), dim3((unsigned)groups), dim3(64), 0, st, a);
+  } else if (C == 64 && PB <= 8 && a.gen_version == 1) {
+    if constexpr (C == 64 && PB <= 8)
+      hipLaunchKernelGGL((k_finalize_col64<PB>), dim3((unsigned)groups), dim3(64), 0, st, a);
   } else {
     hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)a.wd64);
