@@ -33,6 +33,10 @@ Readings of points the paper leaves open (each listed in the design notes):
   scaled by 1/sqrt(C).
 * Ridge constant: eps_t = lambda * mean_j d_{t,j}; it enters the fit only,
   not the selection score.
+* SDQ of the backbone's group scales (Sec. 3.3, Sec. 4 give only its name,
+  origin and size): blocks of 256 group scales, an int8 code per scale
+  around the block mean with one float32 mean and step per block
+  (``sdq_encode``).
 * Scale, two formats (Sec. 3.2 names one power-of-two scale per tile stored
   as an exponent of width b_e, Eq. (5); the default here is fp16):
   - fp16: scale16 = f16(f32(m / qmax)) with both roundings to nearest even,
@@ -233,6 +237,77 @@ def rtn_dequant(codes: np.ndarray, scale16: np.ndarray, zero: np.ndarray, group:
     z = np.asarray(zero, dtype=np.float32)
     qg = q.reshape(rows, cols // group, group)
     return ((qg - z[..., None]) * s[..., None]).astype(np.float32).reshape(rows, cols)
+
+
+SDQ_BLOCK = 256
+
+
+def sdq_encode(scale16: np.ndarray, block: int = SDQ_BLOCK):
+    """Scale double quantization (SDQ) of the RTN group scales (Sec. 3.3 names
+    it, after QLoRA's double quantization of the quantization constants, and
+    Sec. 4 gives its size for RTN g128: 0.068 instead of 0.125 bits per weight).
+    Reading: the fp16 group scales, flattened in row-major order, are cut into
+    blocks of `block` consecutive groups (the last block may be shorter); per
+    block of n scales s_g
+        mu    = f32(sum_g s_g / n)    (the sum in float64, g in order; one division)
+        dlt_g = f32(s_g - mu)         (one float32 rounding)
+        a     = max_g |dlt_g|
+        c_g   = rint(dlt_g * 127 / a) in [-127, 127] (float64: the product is
+                exact, one division, ties to even); every c_g = 0 when a = 0
+        step  = f32(a / 127)          (float64 division, one rounding)
+    stored as one int8 code per group and two float32 (mu, step) per block:
+    8 + 64 / block bits per group (0.0645 bits per weight at g128, block 256).
+    Returns (codes int8 [n_groups], mean float32 [n_blocks], step float32 [n_blocks])."""
+    s = np.asarray(scale16, dtype=np.uint16).reshape(-1).view(np.float16).astype(np.float64)
+    n = s.size
+    nblk = (n + block - 1) // block
+    codes = np.zeros(n, dtype=np.int8)
+    mean = np.zeros(nblk, dtype=np.float32)
+    step = np.zeros(nblk, dtype=np.float32)
+    for k in range(nblk):
+        sb = s[k * block:(k + 1) * block]
+        tot = 0.0
+        for v in sb:  # float64, in order
+            tot += float(v)
+        mu = np.float32(tot / len(sb))
+        dlt = (sb.astype(np.float32) - mu).astype(np.float32)
+        a = float(np.abs(dlt).max())
+        if a > 0.0:
+            c = np.rint(dlt.astype(np.float64) * 127.0 / a)
+            codes[k * block:k * block + len(sb)] = np.clip(c, -127, 127).astype(np.int8)
+        mean[k] = mu
+        step[k] = np.float32(a / 127.0)
+    return codes, mean, step
+
+
+def sdq_scales(codes: np.ndarray, mean: np.ndarray, step: np.ndarray, block: int = SDQ_BLOCK) -> np.ndarray:
+    """Dequantized group scales s_hat_g = f32(mu + c_g * step) of the group's
+    block (float64 sum of exact terms, one rounding to float32)."""
+    c = np.asarray(codes, dtype=np.int8).reshape(-1).astype(np.float64)
+    k = np.arange(c.size) // block
+    return (np.asarray(mean, np.float32)[k].astype(np.float64)
+            + c * np.asarray(step, np.float32)[k].astype(np.float64)).astype(np.float32)
+
+
+def rtn_dequant_sdq(codes: np.ndarray, zero: np.ndarray, sdq_codes: np.ndarray, sdq_mean: np.ndarray,
+                    sdq_step: np.ndarray, group: int = 128) -> np.ndarray:
+    """W0 of an RTN-INT4-SDQ backbone: W0 = f32(q - z) * s_hat per group, the
+    RTN-v1 codes and zero points with the SDQ-dequantized scales."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    rows = codes.shape[0]
+    cols = codes.shape[1] * 2
+    q = np.empty((rows, cols), dtype=np.float32)
+    q[:, 0::2] = codes & 0x0F
+    q[:, 1::2] = codes >> 4
+    sh = sdq_scales(sdq_codes, sdq_mean, sdq_step).reshape(rows, cols // group)
+    z = np.asarray(zero, dtype=np.float32)
+    qg = q.reshape(rows, cols // group, group)
+    return ((qg - z[..., None]) * sh[..., None]).astype(np.float32).reshape(rows, cols)
+
+
+def sdq_bits_per_weight(n_weights: int, n_groups: int, block: int = SDQ_BLOCK) -> float:
+    """Scale metadata rate of SDQ: 8 bits per group plus 64 per block."""
+    return (8 * n_groups + 64 * ((n_groups + block - 1) // block)) / n_weights
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:

@@ -688,3 +688,80 @@ def test_reconstruct_bf16_empty_stream_is_rounded_backbone():
     assert K == 0
     out = O.reconstruct_bf16(stream, [(codes, s16, z)])[0]
     assert np.array_equal(out, O.bf16_round(W0.astype(np.float64)))
+
+
+# ------------------------------------------------------------------ SDQ (Sec. 3.3, Sec. 4)
+def test_sdq_worked_example():
+    """Hand-worked block in tests/golden/sdq_block_example.txt."""
+    g = read_golden("sdq_block_example.txt")
+    s16 = np.array([float(x) for x in g["scales"]], dtype=np.float16).view(np.uint16)
+    codes, mean, step = O.sdq_encode(s16)
+    assert codes.tolist() == [int(x) for x in g["codes"]]
+    assert mean.tolist() == [float(g["mean"][0])]
+    from fractions import Fraction
+    assert step[0] == np.float32(float(Fraction(int(g["step_num"][0]), int(g["step_den"][0]))))
+
+
+def _scale_sets(rng):
+    yield rng.uniform(1e-3, 3e-3, 1000)                 # RTN g128 scales of N(0, 0.02^2) weights
+    yield np.exp(rng.normal(-6.0, 1.0, 777))            # heavy spread, partial last block
+    yield np.concatenate([np.full(256, 0.01), rng.uniform(1e-4, 1e-1, 300)])  # one constant block
+    yield rng.choice([1e-3, 2e-3], 512)                 # two values
+
+
+def test_sdq_error_bound_and_range():
+    """Rounding to the nearest code: every dequantized scale lies within half a
+    step of its scale (plus the float32 roundings of the mean, the deviation
+    and the result), the codes stay in [-127, 127], and a block whose
+    deviations are not all zero uses +-127 at its largest deviation."""
+    rng = np.random.default_rng(11)
+    for vals in _scale_sets(rng):
+        s16 = vals.astype(np.float16).view(np.uint16)
+        s = s16.view(np.float16).astype(np.float64)
+        codes, mean, step = O.sdq_encode(s16)
+        sh = O.sdq_scales(codes, mean, step).astype(np.float64)
+        k = np.arange(s.size) // O.SDQ_BLOCK
+        slack = 4 * np.finfo(np.float32).eps * np.maximum(np.abs(s), np.abs(mean[k].astype(np.float64)))
+        assert np.all(np.abs(sh - s) <= 0.5 * step[k].astype(np.float64) + slack)
+        assert codes.min() >= -127 and codes.max() <= 127
+        for b in range(mean.size):
+            cb = codes[b * O.SDQ_BLOCK:(b + 1) * O.SDQ_BLOCK]
+            if step[b] > 0:
+                assert np.abs(cb.astype(int)).max() == 127
+            else:
+                assert np.all(cb == 0)
+
+
+def test_sdq_constant_block_is_exact_and_blocks_are_independent():
+    rng = np.random.default_rng(12)
+    base = np.concatenate([np.full(256, 0.0125), rng.uniform(1e-3, 3e-3, 256)]).astype(np.float16)
+    codes, mean, step = O.sdq_encode(base.view(np.uint16))
+    assert np.all(codes[:256] == 0) and step[0] == 0
+    assert np.array_equal(O.sdq_scales(codes, mean, step)[:256], base[:256].astype(np.float32))
+    other = base.copy()
+    other[256:] = rng.uniform(1e-2, 2e-2, 256).astype(np.float16)
+    c2, m2, s2 = O.sdq_encode(other.view(np.uint16))
+    assert np.array_equal(c2[:256], codes[:256]) and m2[0] == mean[0] and s2[0] == step[0]
+
+
+def test_rtn_dequant_sdq_reduces_to_rtn_when_scales_are_exact():
+    """With every block constant, the SDQ scales equal the fp16 scales and the
+    SDQ backbone is the RTN-v1 backbone bit for bit."""
+    rng = np.random.default_rng(13)
+    W = rng.normal(0, 0.02, (4, 256 * 128)).astype(np.float32)
+    W[:, ::128] = 0.3      # same max in every group ...
+    W[:, 1::128] = -0.3    # ... and min, so every scale is 0.04
+    codes, s16, zero, W0 = O.rtn_backbone(W)
+    sc, mu, st = O.sdq_encode(s16)
+    assert np.all(sc == 0)
+    assert np.array_equal(O.rtn_dequant_sdq(codes, zero, sc, mu, st), W0)
+
+
+def test_sdq_rate():
+    """8 bits per group and 64 per block of 256: 0.0645 bits per weight at
+    g128, against 0.125 for the fp16 scales (Sec. 4 reports 0.068 for its
+    format, which it does not specify)."""
+    n_w = 2048 * 11008
+    n_g = n_w // 128
+    assert abs(O.sdq_bits_per_weight(n_w, n_g) - (8 + 64 / 256) / 128) < 1e-12
+    assert abs(16 * n_g / n_w - 0.125) < 1e-12
