@@ -237,6 +237,42 @@ def encode_split_bound(C: int, P: int, per_element: bool, gen_version: int, scor
     return {"mfma_flops_per_candidate": 6.0 * P * C, "valu_ops_per_candidate": valu}
 
 
+def sdq_timing(awsrc, torch, wl, bb, stream, reps: int = 20) -> dict:
+    """RTN-INT4-SDQ backbone (Sec. 3.3, Sec. 4): SDQ of the step's group scales
+    and W0 with the dequantized scales, timed with HIP events (outside the
+    step; the step's encoder repairs the RTN-v1 backbone).  Algorithmic bytes:
+    encode 2 B read + 1 B written per group and 8 B per block of 256; W0 0.5 B
+    of codes read and 4 B written per weight, 2 B (zero point, code) per group
+    and 8 B per block."""
+    n_w = sum(b[0].numel() * 2 for b in bb)
+    n_g = sum(b[1].numel() for b in bb)
+    n_blk = sum((b[1].numel() + 255) // 256 for b in bb)
+    sdqs = [awsrc.awsrc_sdq_encode(b[1]) for b in bb]
+    outs = [awsrc.awsrc_backbone_sdq_dequant(b[0], b[2], q) for b, q in zip(bb, sdqs)]
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    e[0].record(stream)
+    for _ in range(reps):
+        for b in bb:
+            awsrc.awsrc_sdq_encode(b[1])
+    e[1].record(stream)
+    for _ in range(reps):
+        for b, q, o in zip(bb, sdqs, outs):
+            awsrc.awsrc_backbone_sdq_dequant(b[0], b[2], q, out=o)
+    e[2].record(stream)
+    torch.cuda.synchronize()
+    enc_ms = e[0].elapsed_time(e[1]) / reps
+    deq_ms = e[1].elapsed_time(e[2]) / reps
+    enc_bytes = 3 * n_g + 8 * n_blk
+    deq_bytes = n_w // 2 + 4 * n_w + 2 * n_g + 8 * n_blk
+    return {"groups": n_g, "scale_bits_per_weight": (8 * n_g + 64 * n_blk) / n_w,
+            "fp16_scale_bits_per_weight": 16 * n_g / n_w,
+            "encode_ms": enc_ms, "dequant_ms": deq_ms, "dequant_bytes": deq_bytes,
+            "dequant_GB/s": deq_bytes / (deq_ms / 1e3) / 1e9,
+            "dequant_frac_hbm": deq_bytes / (deq_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+            "encode_bytes": enc_bytes}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -382,6 +418,7 @@ def main() -> int:
         "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
         "device": torch.cuda.get_device_name(0),
     }
+    out["backbone_sdq"] = sdq_timing(awsrc, torch, wl, bb, stream)
     del inputs, bb, enc_out, ws
     torch.cuda.empty_cache()
     if args.decode_workload:

@@ -134,6 +134,39 @@ awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64_t rows, in
                                 float* W0_or_null, void* stream);
 
 /*
+ * Scale double quantization (SDQ) of the backbone's group scales (Sec. 3.3
+ * names it, after QLoRA's double quantization of quantization constants;
+ * Sec. 4 gives its rate for RTN g128, which the format below undercuts
+ * slightly: 8 bits per group plus 64 per block, 0.0645 bits per weight).
+ * The n_groups fp16 scales (awsrc_backbone_rtn's scale_f16, row-major) are
+ * cut into blocks of 256; per block of n scales s_g:
+ *   mu = f32(sum_g s_g / n)  (fp64 sum in group order, one division),
+ *   dlt_g = f32(s_g - mu), a = max_g |dlt_g|,
+ *   code_g = rint(dlt_g * 127 / a) in [-127, 127] (fp64, ties to even; 0 if a = 0),
+ *   step = f32(a / 127).
+ * The dequantized scale is s_hat_g = f32(mu + code_g * step).
+ *  code        [n_groups] int8;  block_mean, block_step [ceil(n_groups / 256)] fp32.
+ * Device pointers; asynchronous on `stream`.  EINVAL: n_groups < 0 or NULL buffer.
+ */
+awsrc_status awsrc_sdq_encode(const uint16_t* scale_f16, int64_t n_groups, int8_t* code, float* block_mean,
+                              float* block_step, void* stream);
+
+/*
+ * W0 of an RTN-INT4-SDQ backbone (the backbone the paper's residual codecs
+ * repair, Sec. 4): W0 = f32(q - z) * s_hat per group of `group` consecutive
+ * input columns, with awsrc_backbone_rtn's codes and zero points and the
+ * SDQ-dequantized scales of awsrc_sdq_encode.
+ *  codes [rows, cols/2] u8 (4-byte aligned), zero [rows, cols/group] u8,
+ *  sdq_code [rows * cols/group] int8, block_mean / block_step per 256 groups,
+ *  W0 [rows, cols] fp32 (16-byte aligned).  cols % group == 0, group 64,
+ *  128 or 256.  Asynchronous on `stream`.  EINVAL: bad shape, group,
+ *  alignment or NULL buffer.
+ */
+awsrc_status awsrc_backbone_sdq_dequant(const uint8_t* codes, const uint8_t* zero, const int8_t* sdq_code,
+                                        const float* block_mean, const float* block_step, int64_t rows,
+                                        int64_t cols, int32_t group, float* W0, void* stream);
+
+/*
  * Encoder seed search (Sec. 3.2, Eq. (2)-(4) numerator) for every tile of one
  * module.  Tile t = row * (cols / C) + block holds r_t = f32(W - W0) over
  * columns [block*C, block*C + C) of that row and coordinate weights d_t.  For

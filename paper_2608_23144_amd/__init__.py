@@ -24,7 +24,8 @@ AWSRC_D_PER_COL, AWSRC_D_PER_ELEM = 0, 1
 AWSRC_MODE_GLOBAL, AWSRC_MODE_PER_MODULE = 0, 1
 AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
-EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_encode_tiles",
+EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_sdq_encode",
+            "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
             "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
@@ -65,6 +66,8 @@ def _load() -> ctypes.CDLL:
         "awsrc_abi_version": (i32, []),
         "awsrc_last_error": (ctypes.c_char_p, []),
         "awsrc_backbone_rtn": (i32, [vp, i32, i64, i64, i32, vp, vp, vp, vp, vp]),
+        "awsrc_sdq_encode": (i32, [vp, i64, vp, vp, vp, vp]),
+        "awsrc_backbone_sdq_dequant": (i32, [vp, vp, vp, vp, vp, i64, i64, i32, vp, vp]),
         "awsrc_encode_tiles": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp,
                                      ctypes.POINTER(sz), vp]),
         "awsrc_encode_scored": (i32, [vp, ctypes.POINTER(u64), vp]),
@@ -168,6 +171,36 @@ def encode_workspace_bytes(p: awsrc_params, W: torch.Tensor, d_mode: int) -> int
     _check(LIB.awsrc_encode_tiles(ctypes.byref(p), None, _dtype_code(W), None, rows, cols, None, d_mode,
                                   None, None, None, None, None, None, ctypes.byref(n), None))
     return n.value
+
+
+SDQ_BLOCK = 256
+
+
+def awsrc_sdq_encode(scale_f16: torch.Tensor, stream=None):
+    """SDQ of fp16 group scales (int16 bit patterns, any shape, row-major):
+    returns (codes int8 [n], block mean fp32 [nb], block step fp32 [nb])."""
+    _dev(scale_f16)
+    n = scale_f16.numel()
+    nb = (n + SDQ_BLOCK - 1) // SDQ_BLOCK
+    dev = scale_f16.device
+    codes = torch.empty(n, dtype=torch.int8, device=dev)
+    mean = torch.empty(nb, dtype=torch.float32, device=dev)
+    step = torch.empty(nb, dtype=torch.float32, device=dev)
+    _check(LIB.awsrc_sdq_encode(_ptr(scale_f16), n, _ptr(codes), _ptr(mean), _ptr(step), _stream(stream)))
+    return codes, mean, step
+
+
+def awsrc_backbone_sdq_dequant(codes: torch.Tensor, zero: torch.Tensor, sdq, group: int = 128,
+                               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """W0 [rows, cols] fp32 of the RTN-INT4-SDQ backbone (sdq = awsrc_sdq_encode's result)."""
+    sc, mean, step = sdq
+    _dev(codes, zero, sc, mean, step)
+    rows, cols = codes.shape[0], codes.shape[1] * 2
+    if out is None:
+        out = torch.empty(rows, cols, dtype=torch.float32, device=codes.device)
+    _check(LIB.awsrc_backbone_sdq_dequant(_ptr(codes), _ptr(zero), _ptr(sc), _ptr(mean), _ptr(step), rows, cols,
+                                          group, _ptr(out), _stream(stream)))
+    return out
 
 
 def awsrc_encode_tiles(p: awsrc_params, W: torch.Tensor, W0: torch.Tensor, d: torch.Tensor,

@@ -17,7 +17,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libawsrc.so")
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "basis.hip", "backbone.hip", "encode.hip", "encode_mfma.hip", "rank.hip",
+SOURCES = ["abi.cpp", "basis.hip", "backbone.hip", "sdq.hip", "encode.hip", "encode_mfma.hip", "rank.hip",
            "decode.hip"]
 
 COMMON = [
@@ -27,8 +27,8 @@ COMMON = [
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Wall", "-Wno-unused-function",
 ]
-# the backbone recipe is specified without fused multiply-add
-PER_FILE = {"backbone.hip": ["-ffp-contract=off"]}
+# the backbone and SDQ recipes are specified without fused multiply-add
+PER_FILE = {"backbone.hip": ["-ffp-contract=off"], "sdq.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

@@ -213,6 +213,29 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   return AWSRC_OK;
 }
 
+extern "C" awsrc_status awsrc_sdq_encode(const uint16_t* scale_f16, int64_t n_groups, int8_t* code,
+                                         float* block_mean, float* block_step, void* stream) {
+  if (n_groups < 0) return fail(AWSRC_EINVAL, "n_groups < 0");
+  if (n_groups == 0) return AWSRC_OK;
+  if (!scale_f16 || !code || !block_mean || !block_step) return fail(AWSRC_EINVAL, "NULL buffer");
+  HIPCHK(launch_sdq_encode(scale_f16, n_groups, code, block_mean, block_step, (hipStream_t)stream));
+  return AWSRC_OK;
+}
+
+extern "C" awsrc_status awsrc_backbone_sdq_dequant(const uint8_t* codes, const uint8_t* zero, const int8_t* sdq_code,
+                                                  const float* block_mean, const float* block_step, int64_t rows,
+                                                  int64_t cols, int32_t group, float* W0, void* stream) {
+  if (rows < 0 || cols < 0) return fail(AWSRC_EINVAL, "negative shape");
+  if (group != 64 && group != 128 && group != 256) return fail(AWSRC_EINVAL, "group must be 64, 128 or 256");
+  if (cols % group) return fail(AWSRC_EINVAL, "cols=%lld is not a multiple of group=%d", (long long)cols, group);
+  if (rows == 0 || cols == 0) return AWSRC_OK;
+  if (!codes || !zero || !sdq_code || !block_mean || !block_step || !W0) return fail(AWSRC_EINVAL, "NULL buffer");
+  if ((reinterpret_cast<uintptr_t>(codes) & 3) || (reinterpret_cast<uintptr_t>(W0) & 15))
+    return fail(AWSRC_EINVAL, "codes must be 4-byte and W0 16-byte aligned");
+  HIPCHK(launch_sdq_dequant(codes, zero, sdq_code, block_mean, block_step, rows, cols, group, W0, (hipStream_t)stream));
+  return AWSRC_OK;
+}
+
 extern "C" awsrc_status awsrc_encode_scored(const void* workspace, uint64_t* scored, void* stream) {
   if (!workspace || !scored) return fail(AWSRC_EINVAL, "NULL argument");
   const char* ws = reinterpret_cast<const char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));

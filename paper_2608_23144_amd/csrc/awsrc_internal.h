@@ -174,6 +174,13 @@ __device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP
 // the seeded coordinate permutation, B_s[j, p] = sigma_j H[pi(j), c_p]/sqrt(C)).
 hipError_t launch_gen_basis(uint64_t key, int C, int P, int S, int gen_version, BasisTables t, hipStream_t st);
 
+// Scale double quantization of the backbone's group scales (blocks of 256).
+int64_t sdq_blocks(int64_t n_groups);
+hipError_t launch_sdq_encode(const uint16_t* s16, int64_t n_groups, int8_t* code, float* mean, float* step,
+                             hipStream_t st);
+hipError_t launch_sdq_dequant(const uint8_t* codes, const uint8_t* zero, const int8_t* sc, const float* mean,
+                              const float* step, int64_t rows, int64_t cols, int group, float* W0, hipStream_t st);
+
 hipError_t launch_backbone(const void* W, int w_dtype, int64_t rows, int64_t cols, int group,
                            uint8_t* codes, uint16_t* scale, uint8_t* zero, float* W0,
                            hipStream_t st);

@@ -154,3 +154,19 @@ def test_reconstruct_rejects_bad_arguments_without_device_access():
     assert f(ctypes.byref(plan), 128, bad, arr, arr, None) == awsrc.AWSRC_EINVAL  # codes alignment
     odd = (v * 1)(257)
     assert f(ctypes.byref(plan), 128, arr, odd, arr, None) == awsrc.AWSRC_EINVAL  # scale alignment
+
+
+def test_sdq_rejects_bad_arguments_without_device_access():
+    enc = awsrc.LIB.awsrc_sdq_encode
+    assert enc(None, -1, None, None, None, None) == awsrc.AWSRC_EINVAL
+    assert enc(None, 0, None, None, None, None) == awsrc.AWSRC_OK          # nothing to do
+    assert enc(None, 5, None, None, None, None) == awsrc.AWSRC_EINVAL      # NULL buffers
+    deq = awsrc.LIB.awsrc_backbone_sdq_dequant
+    p = 4096
+    assert deq(p, p, p, p, p, 2, 256, 96, p, None) == awsrc.AWSRC_EINVAL   # group
+    assert deq(p, p, p, p, p, 2, 200, 128, p, None) == awsrc.AWSRC_EINVAL  # cols % group
+    assert deq(p, p, p, p, p, -1, 256, 128, p, None) == awsrc.AWSRC_EINVAL
+    assert deq(None, p, p, p, p, 2, 256, 128, p, None) == awsrc.AWSRC_EINVAL
+    assert deq(p + 2, p, p, p, p, 2, 256, 128, p, None) == awsrc.AWSRC_EINVAL  # codes alignment
+    assert deq(p, p, p, p, p, 2, 256, 128, p + 4, None) == awsrc.AWSRC_EINVAL  # W0 alignment
+    assert deq(p, p, p, p, p, 0, 256, 128, p, None) == awsrc.AWSRC_OK

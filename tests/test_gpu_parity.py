@@ -268,6 +268,44 @@ def test_encode_scored_count():
     assert awsrc.awsrc_encode_scored(enc2) == (64 * 256 // wl2.C) * wl2.S
 
 
+# ------------------------------------------------------------------ SDQ backbone
+@pytest.mark.parametrize("name,rows,cols", [("down3b", 64, 11008), ("down3b", 2048, 11008), ("linear256", 256, 256)])
+def test_sdq_backbone_bit_exact(name, rows, cols):
+    """SDQ codes, block means and steps of the GPU's RTN scales, and the
+    RTN-INT4-SDQ W0, bit-exact against the oracle (64 x 11008 has 5504
+    groups: 21 full blocks and one of 128)."""
+    wl = WORKLOADS[name]
+    m = Module("sdq", rows, cols, 0, 1, 1)
+    inp = gen_module_inputs(wl, m, DEV)
+    codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(inp["W"])
+    sdq = awsrc.awsrc_sdq_encode(scale)
+    W0s = awsrc.awsrc_backbone_sdq_dequant(codes, zero, sdq)
+    torch.cuda.synchronize()
+    s16 = scale.cpu().numpy().view(np.uint16)
+    oc, om, ost = O.sdq_encode(s16)
+    assert np.array_equal(sdq[0].cpu().numpy(), oc)
+    assert np.array_equal(sdq[1].cpu().numpy().view(np.uint32), om.view(np.uint32))
+    assert np.array_equal(sdq[2].cpu().numpy().view(np.uint32), ost.view(np.uint32))
+    want = O.rtn_dequant_sdq(codes.cpu().numpy(), zero.cpu().numpy(), oc, om, ost)
+    assert np.array_equal(W0s.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    # SDQ moves W0 by at most half a scale step per weight unit of (q - z)
+    assert (W0s - W0).abs().max().item() <= 15 * 0.5 * float(ost.max()) * (1 + 1e-6) + 1e-12
+
+
+def test_sdq_constant_and_degenerate_blocks():
+    """Blocks whose scales are all equal code to zero and reproduce the RTN-v1
+    W0 bit for bit; an all-zero weight matrix (every group degenerate, scale
+    1.0) does too."""
+    for W in (torch.zeros(8, 4096, device=DEV),
+              torch.linspace(-1, 1, 128, device=DEV).repeat(4, 64).contiguous()):
+        codes, scale, zero, W0 = awsrc.awsrc_backbone_rtn(W)
+        sdq = awsrc.awsrc_sdq_encode(scale)
+        W0s = awsrc.awsrc_backbone_sdq_dequant(codes, zero, sdq)
+        torch.cuda.synchronize()
+        assert torch.all(sdq[0] == 0) and torch.all(sdq[2] == 0)
+        assert torch.equal(W0s.view(torch.int32), W0.view(torch.int32))
+
+
 # ------------------------------------------------------------------ ranking
 @pytest.mark.parametrize("mode", ["global", "per_module"])
 @pytest.mark.parametrize("bpw", [0.05, 0.162, 2.0, 64.0])
@@ -492,6 +530,38 @@ def test_pipeline_linear256_matches_oracle():
     e1 = O.weighted_error(W32, What.cpu().numpy().astype(np.float64), d)
     kept = np.sort(orc["gain"][orc["gain"] > 0])[::-1][:K]
     assert abs((e0 - e1) - kept.sum()) <= 1e-5 * e0
+
+
+def test_pipeline_on_sdq_backbone_matches_oracle():
+    """The residual codec repairing the RTN-INT4-SDQ backbone (the paper's
+    Sec. 4 setting): backbone -> SDQ -> encode -> rank -> decode on the GPU
+    against the same chain in the oracle: identical stream bytes and repaired
+    weights."""
+    wl = WORKLOADS["linear256"]
+    m = wl.modules[0]
+    inp = gen_module_inputs(wl, m, DEV)
+    codes, scale, zero, _ = awsrc.awsrc_backbone_rtn(inp["W"])
+    W0 = awsrc.awsrc_backbone_sdq_dequant(codes, zero, awsrc.awsrc_sdq_encode(scale))
+    p = _params(wl)
+    enc = awsrc.awsrc_encode_tiles(p, inp["W"], W0, inp["d"])
+    s, K, ne = awsrc.awsrc_rank_prefix(p, [(m.rows, m.cols)], awsrc.AWSRC_MODE_GLOBAL, 0.162, enc["seed"],
+                                       enc["codes"], enc["scale"], enc["gain"])
+    W32 = inp["W32"].cpu().numpy()
+    d = inp["d"].cpu().numpy()
+    oc, _, oz, _ = O.rtn_backbone(W32)
+    s16 = O.rtn_backbone(W32)[1]
+    W0o = O.rtn_dequant_sdq(oc, oz, *O.sdq_encode(s16))
+    assert np.array_equal(W0.cpu().numpy(), W0o)
+    op = _oparams(wl)
+    orc = O.encode_tiles(O.tiles(O.residual(W32, W0o), wl.C), O.tile_weights(d, m.rows, m.cols, wl.C), op)
+    want, K_o, ne_o = O.build_stream(op, [(m.rows, m.cols)], orc, 0.162, per_module=False)
+    assert (K, ne) == (K_o, ne_o)
+    assert bytes(s.cpu().numpy().tobytes()) == want
+    What = W0.clone()
+    awsrc.awsrc_decode_add(s, [What])
+    ref = O.decode_add(want, [W0o])[0]
+    w0f = W0o.astype(np.float64)
+    assert np.all(np.abs(What.cpu().numpy() - ref) <= 2.0 ** -22 * (np.abs(w0f) + np.abs(ref - w0f)) + 1e-30)
 
 
 def test_pipeline_paper_pf_operating_point_pow2():
