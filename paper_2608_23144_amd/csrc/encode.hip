@@ -72,15 +72,38 @@ __device__ __forceinline__ void fwht(T (&v)[C]) {
 // fp64 Walsh-Hadamard transform of each column block's weights (per-column
 // mode): the Gram entries of every seed are gathers from it.
 template <int C>
-__global__ void k_block_wht64(const float* __restrict__ d, int nb, double* __restrict__ out) {
-  const int blk = blockIdx.x * blockDim.x + threadIdx.x;
-  if (blk >= nb) return;
-  double v[C];
+__global__ __launch_bounds__(64) void k_block_wht64(const float* __restrict__ d, int nb, double* __restrict__ out) {
+  // one wavefront per block; lane l holds coordinates l + 64 k.  Stage h of
+  // the butterfly pairs coordinates j and j ^ h: the one without bit h gets
+  // x + y, the other x - y (x the lower, y the upper), the same additions as
+  // the in-register transform, so the results are identical.
+  constexpr int V = C > 64 ? C / 64 : 1;
+  const int blk = blockIdx.x;
+  const int lane = threadIdx.x;
+  double v[V];
 #pragma unroll
-  for (int j = 0; j < C; ++j) v[j] = (double)d[(int64_t)blk * C + j];
-  fwht<C>(v);
+  for (int k = 0; k < V; ++k) {
+    const int j = lane + 64 * k;
+    v[k] = j < C ? (double)d[(int64_t)blk * C + j] : 0.0;
+  }
 #pragma unroll
-  for (int j = 0; j < C; ++j) out[(int64_t)blk * C + j] = v[j];
+  for (int h = 1; h < C && h < 64; h <<= 1) {
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const double o = __shfl_xor(v[k], h, 64);
+      v[k] = (lane & h) ? o - v[k] : v[k] + o;
+    }
+  }
+  if constexpr (V == 2) {
+    const double x = v[0], y = v[1];
+    v[0] = x + y;
+    v[1] = x - y;
+  }
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const int j = lane + 64 * k;
+    if (j < C) out[(int64_t)blk * C + j] = v[k];
+  }
 }
 
 // fp64 Cholesky factor of G + eps I for one seed: G_pq = wd[c_p ^ c_q] / C
@@ -830,7 +853,7 @@ static hipError_t run_factors(const EncodeArgs& a, hipStream_t st) {
   const int n = nb * a.S;
   (void)n;
   if (a.gen_version == 1)
-    hipLaunchKernelGGL((k_block_wht64<C>), dim3((nb + 63) / 64), dim3(64), 0, st, a.d, nb, a.wd64);
+    hipLaunchKernelGGL((k_block_wht64<C>), dim3(nb), dim3(64), 0, st, a.d, nb, a.wd64);
   hipLaunchKernelGGL((k_col_factors<C, PB>), dim3((unsigned)((a.S + 63) / 64), (unsigned)nb), dim3(64), 0, st,
                      a, nb, colfac_stride(PB));
   return hipGetLastError();
