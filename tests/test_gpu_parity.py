@@ -135,6 +135,14 @@ def test_encode_linear256_full():
     (128, 8, 4, 64, 70, 512, "col"),    # matrix-core C=128 screen: ragged 32-row waves, seed ranges
     (128, 5, 4, 33, 40, 256, "col"),    # odd S: the last seed pair has one seed
     (64, 16, 8, 8, 4, 128, "elem"),
+    # the pruned per-column screen (C = 64): odd S with ragged rows, seed
+    # ranges of 16 pairs (each starting its pruning afresh), P = 1, b = 2,
+    # and a single seed pair
+    (64, 8, 4, 33, 70, 256, "col"),
+    (64, 8, 4, 256, 130, 640, "col"),
+    (64, 1, 4, 64, 64, 128, "col"),
+    (64, 4, 2, 48, 65, 256, "col"),
+    (64, 8, 4, 2, 10, 128, "col"),
 ])
 def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
     wl = workload("block3b", C=C, P=P, b=b, S=S, d_mode=d_mode)
