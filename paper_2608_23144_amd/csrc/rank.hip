@@ -10,7 +10,7 @@
 //  2. a stable compaction keeps every key > k* and the first such equal keys
 //     in tile order (so equal gains keep the lower tile index);
 //  3. the K survivors are sorted by (decreasing key, increasing tile): chunks
-//     of 1024 by a bitonic network in LDS, then multiway merge passes that
+//     of 256 by a bitonic network in LDS, then multiway merge passes that
 //     place each item by searches in the other runs of its group;
 //  4. records are bit-packed at fixed offsets h + (first slot of the segment
 //     + i) * L_rec.
@@ -28,9 +28,9 @@ namespace awsrc {
 constexpr int kThreads = 256;
 constexpr int kRounds = 16;
 constexpr int kItems = kThreads * kRounds;  // items per block in the compaction
-constexpr int kChunk = 1024;                // items per LDS-sorted chunk
-constexpr int kChunkThreads = 512;
-constexpr int kLogChunk = 10;
+constexpr int kChunk = 256;                 // items per LDS-sorted chunk
+constexpr int kChunkThreads = 128;
+constexpr int kLogChunk = 8;
 constexpr int kFan = 16;                    // runs per multiway merge
 constexpr int kLogFan = 4;
 constexpr int kSelBits = 12;                // radix-select digit width
