@@ -39,25 +39,25 @@ def log(*a):
 MEASURED_TRAFFIC = {
     ("encode", "down3b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip"],
-        "sha256": "8078fc9ef84d1b67f958713d1513356261ba92cd658b10b2f64a731cea256f9f",
-        "bytes": 338917385},
+        "sha256": "d1168961bcc61ae6fb6cf2bf3ae78100ce94d71ebd9e7e3cf9562d862bb602a6",
+        "bytes": 338325496},
     ("backbone", "down3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "336cecc84183444cc69f0fcaecff35a844bf325351541404c8089dbde50b090c",
-        "bytes": 147301917},
+        "sha256": "41fff684ece384a9fb45ffd6bfd67999363fbd2be21caaf93253b0cf12e7bc9a",
+        "bytes": 147304767},
     ("decode_apply", "down3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2e9eefb36a6572da1c94382cfaebef3f9a8df564bd5b21747ee4316b1d3883a5",
-        "bytes": 22875581},
+        "sha256": "0673a533eb8e3675a79bdc3ce35f3e062d6994eed464224abf902f64217607ce",
+        "bytes": 22875480},
     # the stack3b stream at 0.32 bpw of the at-scale measurement
     ("decode_apply", "stack3b@0.32"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2e9eefb36a6572da1c94382cfaebef3f9a8df564bd5b21747ee4316b1d3883a5",
+        "sha256": "0673a533eb8e3675a79bdc3ce35f3e062d6994eed464224abf902f64217607ce",
         "bytes": 5044000000},
     # the whole reconstruction call: tile ordering (scans, copy) and the streaming pass
     ("reconstruct_bf16", "stack3b@0.32"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2e9eefb36a6572da1c94382cfaebef3f9a8df564bd5b21747ee4316b1d3883a5",
+        "sha256": "0673a533eb8e3675a79bdc3ce35f3e062d6994eed464224abf902f64217607ce",
         "bytes": 9469000000},
 }
 
