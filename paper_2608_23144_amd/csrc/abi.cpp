@@ -202,6 +202,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   ws += b_tg;
   a.top_seed = reinterpret_cast<uint16_t*>(ws);
   a.nsplit = nsplit;
+  a.fused_rescore = screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, nsplit) ? 1 : 0;
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
   hipStream_t s = (hipStream_t)stream;
@@ -209,7 +210,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
   if (d_mode == AWSRC_D_PER_COL) HIPCHK(launch_col_factors(a, s));
   HIPCHK(launch_encode_screen(a, s));
-  HIPCHK(launch_encode_finalize(a, s));
+  if (!a.fused_rescore) HIPCHK(launch_encode_finalize(a, s));
   return AWSRC_OK;
 }
 

@@ -204,6 +204,7 @@ struct EncodeArgs {
   float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending
   uint16_t* top_seed;  // [T][nsplit][kTop]
   int nsplit;          // seed ranges screened by separate waves (merged in the re-score)
+  int fused_rescore;   // the screen also runs the re-score (no separate launch)
   uint16_t* seed_out;
   int8_t* code_out;
   uint16_t* scale_out;
@@ -228,6 +229,9 @@ hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);
 // every candidate.
 hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st);
 bool screen_pruned(int C, int P, int d_mode, int gen_version);
+// Whether the pruned screen runs the fp64 re-score itself (one seed range per
+// tile, generator version 1).
+bool screen_fuses_rescore(int C, int P, int d_mode, int gen_version, int nsplit);
 
 // ---------------------------------------------------------------- ranking
 // One survivor of the selection: ~(gain key) and its global tile index.

@@ -26,6 +26,7 @@
 #include <math.h>
 
 #include "awsrc_internal.h"
+#include "rescore64.h"
 
 namespace awsrc {
 
@@ -44,27 +45,7 @@ __device__ __forceinline__ float load_w_any(const void* W, int dt, int64_t i) {
 }
 
 
-// fp16 scale of Sec. 3.2: f16(f32(v)) with saturation at 65504; returns bits.
-__device__ __forceinline__ uint16_t scale_bits_from_f32(float v) {
-  uint16_t hb = __half_as_ushort(__float2half_rn(v));
-  if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;
-  return hb;
-}
 
-// In-register fast Walsh-Hadamard transform, natural (Sylvester) order.
-template <int C, typename T>
-__device__ __forceinline__ void fwht(T (&v)[C]) {
-#pragma unroll
-  for (int h = 1; h < C; h <<= 1)
-#pragma unroll
-    for (int i = 0; i < C; i += 2 * h)
-#pragma unroll
-      for (int k = i; k < i + h; ++k) {
-        const T x = v[k], y = v[k + h];
-        v[k] = x + y;
-        v[k + h] = x - y;
-      }
-}
 
 }  // namespace
 
@@ -106,29 +87,6 @@ __global__ __launch_bounds__(64) void k_block_wht64(const float* __restrict__ d,
   }
 }
 
-// fp64 Cholesky factor of G + eps I for one seed: G_pq = wd[c_p ^ c_q] / C
-// (wd = WHT of the weights, read through any pointer type), G + eps I =
-// L L^T, inv_p = 1 / L_pp.  Padding columns p >= P get an identity row.
-template <int C, int PB, typename WD>
-__device__ __forceinline__ void chol64(int P, const WD& wd, const int (&c)[PB], double eps, double (&L)[PB][PB],
-                                       double (&inv)[PB]) {
-#pragma unroll
-  for (int p = 0; p < PB; ++p)
-#pragma unroll
-    for (int r = 0; r <= p; ++r) {
-      double acc;
-      if (p < P && r < P) acc = wd[c[p] ^ c[r]] / C + (p == r ? eps : 0.0);
-      else acc = (p == r) ? 1.0 : 0.0;
-#pragma unroll
-      for (int kk = 0; kk < r; ++kk) acc -= L[p][kk] * L[r][kk];
-      if (p == r) {
-        L[p][p] = sqrt(fmax(acc, 1e-300));
-        inv[p] = 1.0 / L[p][p];
-      } else {
-        L[p][r] = acc * inv[r];
-      }
-    }
-}
 
 // ----------------------------------------------------------------------------
 // Per-column factor table: for each (column block, seed), G = B^T D B + eps I
@@ -381,28 +339,6 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 // fp16-scale quantization, and the gain 2 a^T b - a^T G0 a of the quantized
 // coefficients a (G0 = G without the ridge), all in fp64.  Each lane keeps
 // its transformed vector in a private LDS row for the data-dependent gathers.
-// Loads 8 consecutive weights of W (fp32 or bf16) starting at element i.
-__device__ __forceinline__ void load8_w(const void* W, int dt, int64_t i, float (&w)[8]) {
-  if (dt == AWSRC_DTYPE_F32) {
-    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(W) + i);
-    const float4 x = p[0], y = p[1];
-    w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w; w[4] = y.x; w[5] = y.y; w[6] = y.z; w[7] = y.w;
-  } else {
-    const uint4 x = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(W) + i);
-    const uint32_t v[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      w[2 * k] = __uint_as_float(v[k] << 16);
-      w[2 * k + 1] = __uint_as_float(v[k] & 0xFFFF0000u);
-    }
-  }
-}
-
-__device__ __forceinline__ void load8_f(const float* p, float (&w)[8]) {
-  const float4 x = reinterpret_cast<const float4*>(p)[0], y = reinterpret_cast<const float4*>(p)[1];
-  w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w; w[4] = y.x; w[5] = y.y; w[6] = y.z; w[7] = y.w;
-}
-
 // u_j = d_j r_j in fp64 (exact: a product of two fp32 values) into the lane's LDS row.
 template <int C, bool PE>
 __device__ __forceinline__ void tile_u64(const EncodeArgs& a, int64_t off, int blk, double* my, float* e32,
@@ -427,73 +363,6 @@ __device__ __forceinline__ void tile_u64(const EncodeArgs& a, int64_t off, int b
   *sumd = sd;
 }
 
-// fp64 re-score of one candidate from its projections bv = B^T u and the
-// factor of its G + eps I: the solve for the unquantized fit al, the stored
-// scale (bits) and codes q, and the gain 2 a.b - a^T G0 a of the quantized
-// fit a = scale q (a^T G0 a = |L^T a|^2 - eps |a|^2).
-template <int PB>
-__device__ __forceinline__ double solve_score64(const EncodeArgs& a, const double (&bv)[PB], const double (&L)[PB][PB],
-                                                const double (&inv)[PB], double eps, int qmax, int (&q)[PB],
-                                                double (&al)[PB], uint16_t* bits_out) {
-  double z[PB];
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    double acc = bv[p];
-#pragma unroll
-    for (int kk = 0; kk < p; ++kk) acc -= L[p][kk] * z[kk];
-    z[p] = acc * inv[p];
-  }
-#pragma unroll
-  for (int p = PB - 1; p >= 0; --p) {
-    double acc = z[p];
-#pragma unroll
-    for (int kk = p + 1; kk < PB; ++kk) acc -= L[kk][p] * al[kk];
-    al[p] = acc * inv[p];
-  }
-  double m = 0.0;
-#pragma unroll
-  for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
-  uint16_t bits = 0;
-  double sc = 0.0;
-  if (m > 0.0) {
-    if (a.scale_fmt == AWSRC_SCALE_POW2) {
-      // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
-      int e;
-      frexp(m / (double)qmax, &e);
-      while (m > (double)qmax * ldexp(1.0, e)) ++e;
-      while (m <= (double)qmax * ldexp(1.0, e - 1)) --e;
-      e = e < -128 ? -128 : (e > 127 ? 127 : e);
-      bits = (uint16_t)(e + 128);
-      sc = ldexp(1.0, e);
-    } else {
-      // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
-      bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
-      sc = (double)__half2float(__ushort_as_half(bits));
-      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
-    }
-  }
-  double ah[PB];
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    double qv = 0.0;
-    if (sc > 0.0) qv = fmin(fmax(rint(al[p] / sc), (double)-qmax), (double)qmax);
-    q[p] = (int)qv;
-    ah[p] = sc * qv;
-  }
-  // gain = 2 a^T b - a^T G0 a, with a^T G0 a = |L^T a|^2 - eps |a|^2
-  double t1 = 0.0, aa = 0.0, quad = 0.0;
-#pragma unroll
-  for (int p = 0; p < PB; ++p) { t1 += ah[p] * bv[p]; aa += ah[p] * ah[p]; }
-#pragma unroll
-  for (int kk = 0; kk < PB; ++kk) {
-    double y = 0.0;
-#pragma unroll
-    for (int i = kk; i < PB; ++i) y += L[i][kk] * ah[i];
-    quad += y * y;
-  }
-  *bits_out = bits;
-  return 2.0 * t1 - (quad - eps * aa);
-}
 
 template <int C, int PB, bool PE>
 __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __restrict__ wdb) {
@@ -644,16 +513,16 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
   }
 }
 
-// Per-column weights, generator version 1, C = 64 (the common case).  Each
-// lane keeps its tile in registers (fp64) and transforms it in place; only
-// the gather of the P projections out of the transform goes through LDS,
-// half a wavefront at a time.  A workgroup thus needs half the LDS of
-// k_finalize, and two wavefronts fit per SIMD.  The second kept seed (a
-// near tie, rare) reloads the tile.
+// Per-column weights, generator version 1, C = 64 (the common case), when
+// the screen leaves the re-score to a kernel of its own (seed ranges split
+// over wavefronts): one wavefront per (row group of 64, column block) merges
+// each tile's lists over the ranges and runs rescore_block64.  Two
+// wavefronts fit per SIMD (the general k_finalize keeps a 65-double LDS row
+// per lane: one per SIMD).
 template <int PB>
 __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   constexpr int C = 64;
-  __shared__ double gb[32 * (C + 1)];
+  __shared__ __attribute__((aligned(16))) float lds[kRescoreLds];
   const int lane = threadIdx.x;
   const int nb = (int)(a.cols / C);
   // Workgroups are dealt to the 8 XCDs round-robin by index: give each XCD a
@@ -664,56 +533,12 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   const int64_t w = xcd * qq + (xcd < rem ? xcd : rem) + blockIdx.x / 8;
   const int64_t nrg = (a.rows + 63) / 64;
   const int blk = (int)(w / nrg);
-  const int64_t row = (w % nrg) * 64 + lane;
-  const float* dcol = a.d + (int64_t)blk * C;
-  // the block's d, one coordinate per lane (C = wavefront size), staged by
-  // every lane before the rows past the end leave
-  __shared__ float dsh[C];
-  __shared__ double wdsh[C];  // WHT(d) of the block, for the Gram entries
-  dsh[lane] = dcol[lane];
-  wdsh[lane] = a.wd64[(int64_t)blk * C + lane];
-  // The work item's 64 x 64 residual block r = W - W0 (fp32) through LDS:
-  // loaded with 16 lanes per row segment (4 rows per pass), so each cache
-  // line is read whole by one instruction, then each lane reads its own row.
-  // (Row-per-lane loads of 16 bytes leave each line to 8 or 16 separate
-  // instructions, and with two wavefronts per SIMD the lines in flight
-  // outgrow the L2 and are fetched again.)  The gather buffer holds the rows.
-  float* rsh = reinterpret_cast<float*>(gb);  // [64][C + 1]
-  {
-    const int64_t row0 = (w % nrg) * 64;
-    const int pc = lane & 15;
-#pragma unroll
-    for (int pass = 0; pass < 16; ++pass) {
-      const int rl = 4 * pass + (lane >> 4);
-      const int64_t rg = row0 + rl < a.rows ? row0 + rl : a.rows - 1;
-      const int64_t o = rg * a.cols + (int64_t)blk * C + 4 * pc;
-      float wv[4], w0[4];
-      if (a.w_dtype == AWSRC_DTYPE_F32) {
-        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.W) + o);
-        wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
-      } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.W) + o);
-        wv[0] = __uint_as_float(x.x << 16); wv[1] = __uint_as_float(x.x & 0xFFFF0000u);
-        wv[2] = __uint_as_float(x.y << 16); wv[3] = __uint_as_float(x.y & 0xFFFF0000u);
-      }
-      const float4 y = *reinterpret_cast<const float4*>(a.W0 + o);
-      w0[0] = y.x; w0[1] = y.y; w0[2] = y.z; w0[3] = y.w;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) rsh[rl * (C + 1) + 4 * pc + k] = wv[k] - w0[k];
-    }
-  }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  if (row >= a.rows) return;  // no cross-lane exchange below but the gather's (per row pair)
-  const int64_t off = row * a.cols + (int64_t)blk * C;
+  const int64_t row0 = (w % nrg) * 64;
+  const int64_t row = row0 + lane < a.rows ? row0 + lane : a.rows - 1;
   const int64_t t = row * nb + blk;
-  const int P = a.P;
-  const double isq = 1.0 / sqrt((double)C);
-  const int qmax = (1 << (a.b - 1)) - 1;
-  double* grow = &gb[(lane & 31) * (C + 1)];
-
-  // merge the seed ranges' lists into the best kTop (as in k_finalize)
+  // merge the seed ranges' lists into the best kTop: ranges come in seed order
+  // and each list is ordered (gain desc, seed asc), so strict comparisons
+  // keep the lower seed first among equal gains
   float tg[kTop];
   int ts[kTop];
 #pragma unroll
@@ -735,107 +560,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
       }
     }
   }
-
-  // Score seed s: u = d .* r in fp64 (also the tile's weighted energy e32 and
-  // sum of d), sigma .* u transformed in place, the P projections gathered
-  // through this lane's LDS row (lanes l and l + 32 share a row, so the two
-  // halves take turns, ordered by the wavefront barriers), then the solve
-  // with the Cholesky factor of the seed's G + eps I.
-  auto score = [&](int s, bool first, float* e32, int (&q)[PB], double (&al)[PB], uint16_t* bits) -> double {
-    // r: the first seed's from the LDS rows, a second seed's (a rare near
-    // tie, after the gather has reused the buffer) loaded directly; then u
-    // with the block's d from LDS
-    float rr[C];
-    if (first) {
-#pragma unroll
-      for (int j = 0; j < C; ++j) rr[j] = rsh[lane * (C + 1) + j];
-    } else {
-#pragma unroll
-      for (int j0 = 0; j0 < C; j0 += 8) {
-        float wv[8], w0[8];
-        load8_w(a.W, a.w_dtype, off + j0, wv);
-        load8_f(a.W0 + off + j0, w0);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) rr[j0 + k] = wv[k] - w0[k];
-      }
-    }
-    double u[C];
-    float e = 0.0f;
-    double sumd = 0.0;
-#pragma unroll
-    for (int j = 0; j < C; ++j) {
-      const float dj = dsh[j];
-      e += dj * rr[j] * rr[j];
-      sumd += (double)dj;
-      u[j] = (double)dj * (double)rr[j];
-    }
-    // pin e and sumd here: left to the compiler, their sums sink to their
-    // uses after the transform and keep r and d live (and spilled) across it
-    asm volatile("" ::"v"(e), "v"(sumd));
-    *e32 = e;
-    const double eps = a.lambda * (sumd / C);
-    const uint64_t s0 = a.basis.sign[(size_t)s * 2];
-    int c[PB];
-#pragma unroll
-    for (int p = 0; p < PB; ++p) c[p] = (p < P) ? a.basis.col[(size_t)s * kMaxP + p] : 0;
-#pragma unroll
-    for (int i = 0; i < C; ++i) u[i] = ((s0 >> i) & 1ull) ? -u[i] : u[i];
-    fwht<C>(u);
-    double bv[PB];
-#pragma unroll
-    for (int ph = 0; ph < 2; ++ph) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      if ((lane >> 5) == ph) {
-#pragma unroll
-        for (int j = 0; j < C; ++j) grow[j] = u[j];
-#pragma unroll
-        for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? grow[c[p]] * isq : 0.0;
-      }
-    }
-    // the transform is dead from here
-    __builtin_amdgcn_sched_barrier(0);
-    double L[PB][PB], inv[PB];
-    chol64<C, PB>(P, wdsh, c, eps, L, inv);
-    return solve_score64<PB>(a, bv, L, inv, eps, qmax, q, al, bits);
-  };
-
-  int best_q[PB];
-  double best_al[PB];
-  uint16_t best_bits;
-  float e32;
-  int best_s = ts[0];
-  double best_g = score(best_s, true, &e32, best_q, best_al, &best_bits);
-  // the second kept seed only when its screened gain is close to the best
-  const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
-#pragma unroll
-  for (int k = 1; k < kTop; ++k) {
-    if (tg[k] >= thr && tg[k] > -INFINITY) {
-      int q[PB];
-      double al[PB];
-      uint16_t bits;
-      float e_;
-      const double g = score(ts[k], false, &e_, q, al, &bits);
-      if (g > best_g || (g == best_g && ts[k] < best_s)) {
-        best_g = g;
-        best_s = ts[k];
-        best_bits = bits;
-#pragma unroll
-        for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = al[p]; }
-      }
-    }
-  }
-  a.seed_out[t] = (uint16_t)best_s;
-  a.scale_out[t] = best_bits;
-  a.gain_out[t] = best_g;
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    if (p < P) {
-      a.code_out[t * P + p] = (int8_t)best_q[p];
-      if (a.alpha_out) a.alpha_out[t * P + p] = (float)best_al[p];
-    }
-  }
+  rescore_block64<PB>(a, blk, row0, tg, ts, lds);
 }
 
 // ----------------------------------------------------------------------------

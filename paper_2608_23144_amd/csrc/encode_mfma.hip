@@ -27,6 +27,7 @@
 #include <math.h>
 
 #include "awsrc_internal.h"
+#include "rescore64.h"
 
 namespace awsrc {
 
@@ -349,7 +350,12 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
 // pair k, a scoring round reads each entry's from the slot of its pair, and
 // rounds run before an entry's slot is reused.  Vector loads and LDS reads
 // complete in order, so the waits for them are exact.
-template <bool POW2>
+//
+// With RPB > 0 (a wavefront screens every seed, generator version 1) the
+// kernel also runs the fp64 re-score of its 64 tiles (rescore_block64 at PB =
+// RPB), in LDS the screen no longer needs, so that the re-score's latency
+// overlaps other wavefronts' screening and the lists never leave the chip.
+template <bool POW2, int RPB>
 __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x4* __restrict__ frag,
                                                         int stride) {
   constexpr int C = 64;
@@ -361,8 +367,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   constexpr int NR = 16;                          // factor ring slots (pairs; a power of two)
   constexpr float kSlack = 1.001953125f;
   static_assert(NF % 4 == 0, "factor pieces are 16 bytes");
-  __shared__ float qb[(QD + 1) * QW * 64];
-  __shared__ __attribute__((aligned(16))) float fr[NR * 2 * NF];
+  // one LDS buffer: the factor ring and the queues while screening, the
+  // re-score's rows after (when fused)
+  constexpr int kScreenLds = NR * 2 * NF + (QD + 1) * QW * 64;
+  constexpr int kLds = RPB > 0 && kRescoreLds > kScreenLds ? kRescoreLds : kScreenLds;
+  __shared__ __attribute__((aligned(16))) float lds[kLds];
+  float* fr = lds;                  // [NR][2][NF]
+  float* qb = lds + NR * 2 * NF;    // [QD + 1][QW][64]
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
   const ScreenTask tk = screen_task(a, 64);
@@ -558,12 +569,36 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
         const bool m = better(tg[t][0], ts[t][0], og1, os1);
         r1 = m ? tg[t][0] : og1; q1 = m ? ts[t][0] : os1;
       }
-      const int64_t at = (((trow0 + 16 * t) * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
-      a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
-      a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
-      a.top_seed[at + 0] = (uint16_t)q0;
-      a.top_seed[at + 1] = (uint16_t)q1;
+      if constexpr (RPB > 0) {
+        // for the lane of the tile's row (below); the queues are drained
+        float* st = &lds[4 * (16 * (nb0 + t) + n)];
+        st[0] = r0 * (1.0f / 64.0f);  // back to gain units
+        st[1] = r1 * (1.0f / 64.0f);
+        st[2] = __int_as_float(q0);
+        st[3] = __int_as_float(q1);
+      } else {
+        const int64_t at = (((trow0 + 16 * t) * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
+        a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
+        a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
+        a.top_seed[at + 0] = (uint16_t)q0;
+        a.top_seed[at + 1] = (uint16_t)q1;
+      }
     }
+  }
+  if constexpr (RPB > 0) {
+    static_assert(kTop == 2, "two kept seeds per tile");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // lane = the tile's row in the group (rows past the end read values
+    // they never use)
+    const f32x4 v = *reinterpret_cast<const f32x4*>(&lds[4 * lane]);
+    const float mg[kTop] = {v[0], v[1]};
+    const int ms[kTop] = {__float_as_int(v[2]), __float_as_int(v[3])};
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    rescore_block64<RPB>(a, blk, tk.row0, mg, ms, lds);
   }
 }
 
@@ -751,6 +786,10 @@ bool screen_pruned(int C, int P, int d_mode, int gen_version) {
   return C == 64 && screen_mfma_supported(C, P, d_mode, gen_version) && d_mode == AWSRC_D_PER_COL;
 }
 
+bool screen_fuses_rescore(int C, int P, int d_mode, int gen_version, int nsplit) {
+  return screen_pruned(C, P, d_mode, gen_version) && gen_version == 1 && nsplit == 1;
+}
+
 __global__ void k_scored_init(unsigned long long* p, unsigned long long v) {
   if (threadIdx.x == 0) *p = v;
 }
@@ -777,8 +816,12 @@ static hipError_t screen_mfma_fmt(const EncodeArgs& a, void* frag, hipStream_t s
   const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
   if (a.d_mode == AWSRC_D_PER_ELEM)
     hipLaunchKernelGGL((k_screen_pe64<POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr);
+  else if (!a.fused_rescore)
+    hipLaunchKernelGGL((k_screen_col64<POW2, 0>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
+  else if (a.P <= 4)
+    hipLaunchKernelGGL((k_screen_col64<POW2, 4>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   else
-    hipLaunchKernelGGL((k_screen_col64<POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
+    hipLaunchKernelGGL((k_screen_col64<POW2, 8>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   return hipGetLastError();
 }
 
