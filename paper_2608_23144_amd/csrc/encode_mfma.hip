@@ -178,11 +178,16 @@ template <bool POW2>
 __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4* __restrict__ frag) {
   constexpr int C = 64;
   constexpr int PB = 8;
-  constexpr int TS = 12;  // LDS stride (floats) of one tile's coefficients
+  constexpr int TS = 8;  // LDS stride (floats) of one tile's coefficients
   constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
   constexpr int LS = PB * (PB - 1) / 2;
+  // 20 KB in all, so that eight wavefronts fit in a CU's 160 KB.  tb: a
+  // tile's two 16-byte halves trade places in every other group of 8 tiles,
+  // so that the 16-byte accesses of 16 lanes cover all banks.  wdl: lane-
+  // minor ([coordinate][lane]), so that a gather at a wavefront-uniform
+  // coordinate reads 64 consecutive words.
   __shared__ __attribute__((aligned(16))) float tb[2 * 64 * TS];
-  __shared__ float wdl[64 * (C + 1)];
+  __shared__ float wdl[C * 64];
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
   const ScreenTask tk = screen_task(a, 64);
@@ -211,7 +216,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
         }
     // stored divided by C, so the gathers are the Gram entries themselves
 #pragma unroll
-    for (int j = 0; j < C; ++j) wdl[lane * (C + 1) + j] = wd[j] * (1.0f / C);
+    for (int j = 0; j < C; ++j) wdl[j * 64 + lane] = wd[j] * (1.0f / C);
   }
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
   auto stash = [&](const f32x4 (&acc)[4]) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
-      *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 64 + 16 * nb + n) * TS + 4 * (g & 1)]) = acc[nb];
+      *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 64 + 16 * nb + n) * TS + 4 * ((g & 1) ^ ((n >> 3) & 1))]) = acc[nb];
   };
   {
     f32x4 acc[4];
@@ -246,8 +251,9 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
     float bk[2][PB];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS]);
-      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4]);
+      const int sw = 4 * ((lane >> 3) & 1);
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + sw]);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4 - sw]);
       bk[k][0] = b0[0]; bk[k][1] = b0[1]; bk[k][2] = b0[2]; bk[k][3] = b0[3];
       bk[k][4] = b1[0]; bk[k][5] = b1[1]; bk[k][6] = b1[2]; bk[k][7] = b1[3];
     }
@@ -273,14 +279,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
       int c[PB];
 #pragma unroll
       for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw0 : cw1) >> (8 * (p & 3))) & 0xFFu) : 0;
-      const float* wrow = &wdl[lane * (C + 1)];
+      const float* wrow = &wdl[lane];  // coordinate x at wrow[64 x]
       const float eps = lam * wrow[0];
 #pragma unroll
       for (int p = 0; p < PB; ++p) {
         float E[PB];
 #pragma unroll
         for (int q = 0; q < p; ++q) {
-          float t = (p < P && q < P) ? wrow[c[p] ^ c[q]] : 0.0f;
+          float t = (p < P && q < P) ? wrow[64 * (c[p] ^ c[q])] : 0.0f;
 #pragma unroll
           for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
           E[q] = t;
