@@ -551,7 +551,10 @@ static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, co
     if (per_cu < 1) per_cu = 1;
     const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / kUnitW);
     const uint64_t chunks = (units + kRecUnits * kRecThreads - 1) / (kRecUnits * kRecThreads);
-    uint64_t nb = (uint64_t)per_cu * 256;                // resident blocks, grid-stride beyond
+    // four times the blocks that fit at once, grid-stride beyond (more blocks
+    // than resident keep the CUs full to the end: 2.5% faster on the 2.8G-
+    // weight stack than resident blocks alone, no better at 16 times)
+    uint64_t nb = (uint64_t)per_cu * 256 * 4;
     if (nb > chunks) nb = chunks;
     if (nb < 1) continue;
     hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb, m0, nm);
