@@ -353,6 +353,52 @@ def test_rank_large_segment_with_ties():
         assert K == K_o and bytes(s.cpu().numpy().tobytes()) == want
 
 
+def test_rank_stack3b_scale_global_order():
+    """Global ranking at the size of the 36-layer stack (252 modules, 43.35M
+    tiles, 0.32 bpw: about 9.2M records): K from the budget, the records'
+    tile order equal to an independent numpy ordering of the eligible tiles
+    by (-gain, tile), and the packed fields of sampled records equal to the
+    encoder outputs they came from."""
+    wl = WORKLOADS["stack3b"]
+    shapes = [(m.rows, m.cols) for m in wl.modules]
+    T = wl.n_tiles
+    bpw = 0.32
+    rec = gen_records(T, wl.P, wl.b, wl.S, seed=77, device=DEV)
+    s, K, ne = awsrc.awsrc_rank_prefix(_params(wl), shapes, awsrc.AWSRC_MODE_GLOBAL, bpw, rec["seed"],
+                                       rec["codes"], rec["scale"], rec["gain"])
+    gain = rec["gain"].cpu().numpy()
+    L = O.record_bytes(_oparams(wl), T)
+    h = O.header_bytes(len(shapes))
+    N = sum(r * c for r, c in shapes)
+    assert ne == int((gain > 0).sum())
+    assert K == min(ne, (O.budget_bytes(bpw, N) - h) // L) and K > 1_000_000
+    assert len(s) == h + K * L
+    # the top K by (-gain, tile): every gain above the K-th, then the lowest
+    # tiles among those equal to it, ordered with lexsort
+    elig = np.nonzero(gain > 0)[0]
+    g = gain[elig]
+    v = -np.partition(-g, K - 1)[K - 1]
+    above = elig[g > v]
+    eq = elig[g == v]
+    chosen = np.concatenate([above, eq[:K - len(above)]])
+    want = chosen[np.lexsort((chosen, -gain[chosen]))]
+    raw = s[h:].cpu().numpy().reshape(K, L)
+    assert L >= 4 and wl.idx_bits == 32
+    got = raw[:, :4].copy().view("<u4").ravel().astype(np.int64)
+    assert np.array_equal(got, want)
+    # sampled records: seed, codes and scale of the tile they name
+    hd = O.parse_header(bytes(s[:h].cpu().numpy().tobytes()))
+    seed = rec["seed"].cpu().numpy().astype(np.int64) & 0xFFFF
+    codes = rec["codes"].cpu().numpy()
+    scale = rec["scale"].cpu().numpy().astype(np.int64) & 0xFFFF
+    for k in np.random.default_rng(3).integers(0, K, 2000):
+        t, sd, cd, sc = O.unpack_record(bytes(raw[k]), hd["idx_bits"], hd["seed_bits"], hd["P"], hd["b"],
+                                        hd["scale_bits"])
+        assert t == want[k] and sd == seed[t] and sc == scale[t] and list(cd) == codes[t].tolist()
+    del rec, s
+    torch.cuda.empty_cache()
+
+
 def test_rank_stream_capacity_too_small():
     """K is found on the device; a stream buffer too small for the records is
     reported as AWSRC_ENOSPC after the fact, with nothing written past it."""
