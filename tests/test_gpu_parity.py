@@ -237,11 +237,13 @@ def test_encode_zero_residual_tiles():
     assert np.all(_u16(enc["scale"]).reshape(64, nb)[:, :2] == 0)
 
 
-@pytest.mark.parametrize("name,n_tiles", [("down3b", 400), ("block3b", 300), ("layer32b", 60)])
+@pytest.mark.parametrize("name,n_tiles", [("down3b", 400), ("block3b", 300), ("layer32b", 60), ("stack3b", 150)])
 def test_encode_full_size_sampled(name, n_tiles):
-    """Full-size modules of the 3B / 32B workloads; the oracle checks sampled tiles."""
+    """Full-size modules of the 3B / 32B workloads (for the 36-layer stack,
+    S = 512: its first layer's k and down projections); the oracle checks
+    sampled tiles."""
     wl = WORKLOADS[name]
-    mods = wl.modules if name != "block3b" else (wl.modules[1], wl.modules[6])
+    mods = wl.modules if name not in ("block3b", "stack3b") else (wl.modules[1], wl.modules[6])
     if name == "layer32b":
         mods = (wl.modules[1], wl.modules[6])
     rng = np.random.default_rng(0)
