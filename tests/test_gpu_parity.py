@@ -153,6 +153,20 @@ def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
     assert nd <= max(1, T // 50)
 
 
+@pytest.mark.parametrize("P,S,rows,cols", [(8, 48, 70, 256), (3, 30, 64, 128), (5, 62, 129, 256)])
+def test_encode_f32_weights_one_seed_range(P, S, rows, cols):
+    """fp32 weights where one wavefront screens every seed of its tiles (fewer
+    than 32 seed pairs), so the screen also runs the fp64 re-score; ragged
+    row groups and padded P."""
+    wl = workload("linear256", P=P, S=S)
+    assert wl.w_dtype == "f32" and wl.d_mode == "col" and wl.C == 64
+    m = Module("t", rows, cols, 0, 2, 2)
+    inp, bb, enc = _gpu_module(wl, m)
+    T = rows * cols // wl.C
+    nd = _check_encode_sample(wl, m, inp, bb[3], enc, np.arange(T))
+    assert nd <= max(1, T // 50)
+
+
 @pytest.mark.parametrize("C,P,b,S,rows,cols,d_mode", [
     (64, 8, 4, 32, 67, 512, "col"),     # matrix-core screen, per-column factors
     (64, 8, 4, 32, 67, 512, "elem"),    # matrix-core screen, per-element factors
