@@ -153,13 +153,16 @@ def test_encode_small_shapes(C, P, b, S, rows, cols, d_mode):
     assert nd <= max(1, T // 50)
 
 
-@pytest.mark.parametrize("P,S,rows,cols", [(8, 48, 70, 256), (3, 30, 64, 128), (5, 62, 129, 256)])
-def test_encode_f32_weights_one_seed_range(P, S, rows, cols):
-    """fp32 weights where one wavefront screens every seed of its tiles (fewer
-    than 32 seed pairs), so the screen also runs the fp64 re-score; ragged
-    row groups and padded P."""
-    wl = workload("linear256", P=P, S=S)
-    assert wl.w_dtype == "f32" and wl.d_mode == "col" and wl.C == 64
+@pytest.mark.parametrize("P,S,rows,cols,d_mode", [(8, 48, 70, 256, "col"), (3, 30, 64, 128, "col"),
+                                                   (5, 62, 129, 256, "col"), (8, 40, 67, 256, "elem"),
+                                                   (4, 256, 64, 128, "elem")])
+def test_encode_f32_weights_one_seed_range(P, S, rows, cols, d_mode):
+    """fp32 weights on the C = 64 matrix-core screens: per-column weights where
+    one wavefront screens every seed of its tiles (fewer than 32 seed pairs),
+    so the screen also runs the fp64 re-score; per-element weights with one
+    and with several seed ranges; ragged row groups and padded P."""
+    wl = workload("linear256", P=P, S=S, d_mode=d_mode)
+    assert wl.w_dtype == "f32" and wl.d_mode == d_mode and wl.C == 64
     m = Module("t", rows, cols, 0, 2, 2)
     inp, bb, enc = _gpu_module(wl, m)
     T = rows * cols // wl.C
