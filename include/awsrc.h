@@ -6,8 +6,9 @@
  * quantizer (Eq. (1)) is cut into row-wise tiles of C input coordinates; for
  * each tile and each seed s a seeded signed-Hadamard basis B_s (Eq. (2)) is
  * fitted by activation-weighted ridge least squares (Eq. (3)), the P
- * coefficients are rounded to b bits with one scale per tile, and the seed
- * with the lowest post-quantization weighted error is kept (Sec. 3.2).
+ * coefficients are rounded to b bits with one scale per tile, and each tile
+ * keeps the seed whose rounded fit leaves the smallest weighted error
+ * (Sec. 3.2).
  * Records are ranked by weighted-error reduction per serialized byte
  * (Eq. (4), Sec. 3.3) and serialized as fixed-size records after a header
  * (Eq. (5), Sec. 3.4); the decoder regenerates B_s and adds B_s alpha_hat onto
@@ -30,7 +31,9 @@
  *    returns a text description of the calling thread's last error.
  *  - The library keeps no mutable global state besides that per-thread error
  *    text, so calls on different streams may run concurrently provided their
- *    buffers do not overlap.
+ *    buffers do not overlap.  The small host copies of a call (a stream
+ *    header, module tables, totals) go through host memory owned by that
+ *    call, and a call that synchronizes waits on its own stream only.
  *
  * Conventions fixed where the paper leaves the choice open (the generator,
  * scale format, tie rules, backbone recipe and byte layouts) are documented
@@ -219,7 +222,9 @@ awsrc_status awsrc_encode_scored(const void* workspace, uint64_t* scored, void* 
  *    stream is itself the stream of a smaller budget.
  *  AWSRC_MODE_PER_MODULE (U variant): module m keeps
  *    min(eligible_m, floor(bpw_budget * N_m / 8) / L_rec) records; sections
- *    follow module order; the header is counted once, globally.
+ *    follow module order.  The quotas cover the records only, so the whole
+ *    stream (header included) may exceed floor(bpw_budget * N / 8) bytes by
+ *    up to the header size h.
  * Stream layout (little-endian): a header of h = 40 + 8 * n_modules bytes
  *   magic "AWSR" | version u16 = 1 | flags u16 (bits 0-3 gen_version, 4-7
  *   scale_fmt, bit 8 per-module mode) | C u16 | P u8 | b u8 | S u32 |

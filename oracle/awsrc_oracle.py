@@ -14,8 +14,8 @@ Paper map (arXiv 2608.23144, "Activation-Weighted Seeded Residual Coding"):
 * Eq. (2), Sec. 3.1  B_s = GenBasis(s, C, P): normalized Hadamard columns with
   a seeded sign pattern and a seeded choice of P columns.
 * Eq. (3), Sec. 3.2  activation-weighted ridge least squares for alpha*_{t,s}.
-* Sec. 3.2            coefficient-wise b-bit RTN with one scale per tile; the
-  seed with the lowest post-quantization weighted error is kept.
+* Sec. 3.2            coefficient-wise b-bit RTN with one scale per tile; each
+  tile keeps the seed whose rounded coefficients leave the least weighted error.
 * Eq. (4), Sec. 3.3  byte-normalized gain rho_t; non-positive records are
   dropped; per-module quotas (U variant) or one global ranking (P variant)
   whose record-boundary prefixes all decode.
@@ -454,7 +454,7 @@ def encode_tiles(R: np.ndarray, Dw: np.ndarray, params: Params,
     s in 0..S-1 (or every explicit basis in `bases`) the tile is fitted
     (Eq. (3)), the coefficients are quantized, and the weighted gain of the
     quantized reconstruction (Eq. (4) numerator) is evaluated; the seed with
-    the largest gain (= lowest post-quantization weighted error) is kept, the
+    the largest gain (= least weighted error after rounding) is kept, the
     lowest seed winning exact ties.  With quantize_coeffs=False the
     unquantized fit is scored instead (used by the exact-reconstruction check).
     """

@@ -77,34 +77,6 @@ uint64_t get_le(const uint8_t* p, int n) {
 
 constexpr int kHeaderFixed = 40;
 
-// Pinned host staging for the small host <-> device copies of a call (stream
-// header, module tables, totals), so that they are plain DMA transfers
-// ordered on the stream instead of staged pageable copies.  One buffer per
-// host thread, grown on demand and never returned; every call synchronizes
-// with its stream before it returns, so the buffer is idle between calls.
-struct PinnedBuf {
-  uint8_t* p = nullptr;
-  size_t n = 0;
-};
-thread_local PinnedBuf g_pinned;
-
-uint8_t* pinned_staging(size_t n) {
-  if (g_pinned.n < n) {
-    if (g_pinned.p) {
-      if (hipDeviceSynchronize() != hipSuccess) return nullptr;  // no copy may still use it
-      if (hipHostFree(g_pinned.p) != hipSuccess) return nullptr;
-    }
-    g_pinned.p = nullptr;
-    g_pinned.n = 0;
-    const size_t m = n < 65536 ? 65536 : 2 * n;
-    void* p = nullptr;
-    if (hipHostMalloc(&p, m, hipHostMallocDefault) != hipSuccess) return nullptr;
-    g_pinned.p = static_cast<uint8_t*>(p);
-    g_pinned.n = m;
-  }
-  return g_pinned.p;
-}
-
 }  // namespace
 
 extern "C" int32_t awsrc_abi_version(void) { return AWSRC_ABI_VERSION; }
@@ -241,11 +213,10 @@ extern "C" awsrc_status awsrc_encode_scored(const void* workspace, uint64_t* sco
   if (!workspace || !scored) return fail(AWSRC_EINVAL, "NULL argument");
   const char* ws = reinterpret_cast<const char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* stage = pinned_staging(64);
-  if (!stage) return fail(AWSRC_EDEVICE, "pinned host staging buffer unavailable");
-  HIPCHK(hipMemcpyAsync(stage, ws, 8, hipMemcpyDeviceToHost, s));
+  uint64_t v = 0;
+  HIPCHK(hipMemcpyAsync(&v, ws, 8, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
-  memcpy(scored, stage, 8);
+  *scored = v;
   return AWSRC_OK;
 }
 
@@ -341,11 +312,10 @@ extern "C" awsrc_status awsrc_rank_prefix(const awsrc_params* p, int32_t n_modul
     put_le(hdr, (uint64_t)module_rows[m], 4);
     put_le(hdr, (uint64_t)module_cols[m], 4);
   }
-  uint8_t* stage = pinned_staging(align_up(hdr.size(), 64) + 64);
-  if (!stage) return fail(AWSRC_EDEVICE, "pinned host staging buffer unavailable");
-  memcpy(stage, hdr.data(), hdr.size());
-  uint64_t* tot = reinterpret_cast<uint64_t*>(stage + align_up(hdr.size(), 64));
-  HIPCHK(hipMemcpyAsync(stream_out, stage, hdr.size(), hipMemcpyHostToDevice, s));
+  // host buffers of this call (the header and the totals) stay alive until
+  // the stream synchronization below
+  uint64_t tot[3] = {0, 0, 0};
+  HIPCHK(hipMemcpyAsync(stream_out, hdr.data(), hdr.size(), hipMemcpyHostToDevice, s));
   HIPCHK(hipMemcpyAsync(tot, rank_totals(rw), 3 * sizeof(uint64_t), hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
   const int64_t K_total = (int64_t)tot[0];
@@ -425,13 +395,12 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   const uint64_t h_caller = kHeaderFixed + 8ull * (uint64_t)n_modules;
   if (stream_len < h_caller) return fail(AWSRC_ECORRUPT, "stream shorter than a header for %d modules", n_modules);
   hipStream_t s = (hipStream_t)stream;
-  // pinned staging: the header here, later the module tables and the error count
-  const size_t st_tabs = align_up(h_caller, 64), st_err = st_tabs + align_up((3 * (size_t)n_modules + 1) * 8, 64);
-  uint8_t* stage = pinned_staging(st_err + 64);
-  if (!stage) return fail(AWSRC_EDEVICE, "pinned host staging buffer unavailable");
-  HIPCHK(hipMemcpyAsync(stage, stream_bytes, h_caller, hipMemcpyDeviceToHost, s));
+  // host copies of this call (header, module tables, error count) use
+  // buffers that live until the stream is synchronized
+  std::vector<uint8_t> hbuf(h_caller);
+  HIPCHK(hipMemcpyAsync(hbuf.data(), stream_bytes, h_caller, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
-  const uint8_t* fx = stage;
+  const uint8_t* fx = hbuf.data();
   if (memcmp(fx, "AWSR", 4) != 0) return fail(AWSRC_ECORRUPT, "bad magic");
   if (get_le(fx + 4, 2) != 1) return fail(AWSRC_ECORRUPT, "unsupported stream version");
   const uint32_t flags = (uint32_t)get_le(fx + 6, 2);
@@ -490,14 +459,12 @@ extern "C" awsrc_status awsrc_decode_prepare(const uint8_t* stream_bytes, uint64
   pl.workspace = workspace;
   const DecodeArgs a = decode_args(&pl);
   memcpy(tabs.data() + 2 * (size_t)nmod + 1, W0_ptrs, nmod * sizeof(void*));
-  memcpy(stage + st_tabs, tabs.data(), tabs.size() * 8);
-  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), stage + st_tabs, tabs.size() * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(a.mod_tile_off), tabs.data(), tabs.size() * 8, hipMemcpyHostToDevice, s));
   HIPCHK(launch_gen_basis(key, C, P, (int)S, gen, a.basis, s));
   HIPCHK(launch_decode_validate(a, s));
-  unsigned long long* perr = reinterpret_cast<unsigned long long*>(stage + st_err);
-  HIPCHK(hipMemcpyAsync(perr, a.errors, 8, hipMemcpyDeviceToHost, s));
+  unsigned long long nerr = 0;
+  HIPCHK(hipMemcpyAsync(&nerr, a.errors, 8, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
-  const unsigned long long nerr = *perr;
   if (nerr) return fail(AWSRC_ECORRUPT, "%llu invalid or duplicate records", nerr);
   *plan = pl;
   return AWSRC_OK;
@@ -535,14 +502,10 @@ extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, in
   char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(plan->workspace), 256));
   uint64_t* bbt = reinterpret_cast<uint64_t*>(ws + l.total - 256 - l.bbtab);
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* stage = pinned_staging((tabs.size() + 2 * (size_t)n + 1) * 8);
-  if (!stage) return fail(AWSRC_EDEVICE, "pinned host staging buffer unavailable");
-  memcpy(stage, tabs.data(), tabs.size() * 8);
-  const uint64_t* mtp = reinterpret_cast<const uint64_t*>(stage) + tabs.size();
-  HIPCHK(hipMemcpyAsync(bbt, stage, tabs.size() * 8, hipMemcpyHostToDevice, s));
-  HIPCHK(hipMemcpyAsync(const_cast<uint64_t*>(mtp), a.mod_tile_off, (2 * (size_t)n + 1) * 8, hipMemcpyDeviceToHost, s));
+  std::vector<uint64_t> mt(2 * (size_t)n + 1, 0);
+  HIPCHK(hipMemcpyAsync(bbt, tabs.data(), tabs.size() * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(mt.data(), a.mod_tile_off, mt.size() * 8, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
-  const std::vector<uint64_t> mt(mtp, mtp + 2 * (size_t)n + 1);
   for (uint32_t m = 0; m < n; ++m) {
     const int64_t c = (int64_t)mt[n + 1 + m];
     if (c % group) return fail(AWSRC_EINVAL, "module %u: cols %lld not a multiple of group %d", m, (long long)c, group);

@@ -7,8 +7,8 @@
 // Two passes share one set of tables:
 //  * screen   - every (tile, seed) in fp32, one lane per tile; the seed loop
 //               is uniform across the wavefront, so basis patterns and the
-//               per-column factors are scalar loads.  The four best screened
-//               seeds of each tile are kept.
+//               per-column factors are scalar loads.  The two best screened
+//               seeds of each tile (kTop) are kept.
 //  * finalize - the screened seeds whose fp32 gain lies within a small margin
 //               of the best are re-scored in fp64 with the complete chain
 //               (projection, Gram matrix, Cholesky solve, quantization,

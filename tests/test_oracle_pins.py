@@ -404,8 +404,8 @@ def _brute_error(r, d, sigma, cols, lam, b):
 @pytest.mark.parametrize("C,P", [(4, 1), (4, 2), (8, 2)])
 def test_brute_force_selection(C, P):
     """Over an exhaustive basis set (every sign pattern x every ordered column
-    choice) the oracle's choice attains the minimum post-quantization weighted
-    error computed independently in plain Python."""
+    choice) the oracle's choice attains the minimum weighted error after
+    rounding, computed independently in plain Python."""
     rng = np.random.default_rng(10 + C + P)
     H = O.hadamard(C)
     signs = list(itertools.product([1, -1], repeat=C))
