@@ -78,9 +78,20 @@ def _check_encode_sample(wl, m, inp, W0_gpu, enc, tiles_idx, fmt=0, gen=1):
                 amax = np.abs(orc["alpha"][i]).max()
                 assert np.abs(g_alpha[i] - orc["alpha"][i]).max() <= 1e-4 * amax + 1e-30
         else:
+            # a tied seed: the GPU's record must be the oracle's record for
+            # that seed, byte for byte unless that candidate is itself on a
+            # rounding knife edge
             n_seed_diff += 1
-            q, bits, g, _ = O.candidate(R[i], D[i], op, s_g)
+            q, bits, g, alpha = O.candidate(R[i], D[i], op, s_g)
             assert abs(g_gain[i] - g) <= 1e-10 * e + 1e-300
+            qm, _, sc = O.quantize(alpha[None], op.b, op.scale_fmt)
+            edge = (O._boundary_flags(alpha[None], sc, op.qmax)[0]
+                    or O._scale_flags(alpha[None], op.qmax, scale_fmt=op.scale_fmt)[0])
+            if not edge:
+                assert np.array_equal(g_codes[i], q), (i, s_g, g_codes[i], q)
+                assert g_scale[i] == bits, (i, s_g, g_scale[i], bits)
+            if g_alpha is not None:
+                assert np.abs(g_alpha[i] - alpha).max() <= 1e-4 * np.abs(alpha).max() + 1e-30
     return n_seed_diff
 
 

@@ -765,3 +765,122 @@ def test_sdq_rate():
     n_g = n_w // 128
     assert abs(O.sdq_bits_per_weight(n_w, n_g) - (8 + 64 / 256) / 128) < 1e-12
     assert abs(16 * n_g / n_w - 0.125) < 1e-12
+
+
+# ------------------------------------------------ parity exemptions (flags)
+# The GPU parity tests skip the bit-exact code/scale comparison only where
+# the oracle flags a knife edge; these pins fix what the flags may cover.
+def test_boundary_flags_hand_values():
+    """A coefficient flags its tile exactly when |alpha*/scale| lies within
+    1e-9 of a rounding midpoint n + 1/2 below qmax + 1/2 (Sec. 3.2 RTN)."""
+    qmax = 7
+    sc = np.array([1.0])
+    cases = [
+        (2.5, True),                  # on the midpoint
+        (-2.5, True),                 # sign does not matter
+        (2.5 + 5e-10, True),          # just inside, above
+        (2.5 - 5e-10, True),          # just inside, below
+        (2.5 + 3e-9, False),          # just outside
+        (2.5 - 3e-9, False),
+        (2.25, False), (3.0, False), (0.0, False),
+        (7.5, False),                 # beyond qmax + 1/2: clamps either way
+        (9.5, False),
+        (6.5, True),                  # the last midpoint below qmax + 1/2
+    ]
+    for a, want in cases:
+        alpha = np.array([[0.25, a, 0.0, 1.0]])
+        assert bool(O._boundary_flags(alpha, sc, qmax)[0]) == want, a
+    # the scale divides: alpha = 0.625 with scale 0.25 is the midpoint 2.5
+    assert O._boundary_flags(np.array([[0.625]]), np.array([0.25]), qmax)[0]
+    assert not O._boundary_flags(np.array([[0.6]]), np.array([0.25]), qmax)[0]
+    # a zero scale (empty record) is never flagged
+    assert not O._boundary_flags(np.array([[0.5]]), np.array([0.0]), qmax)[0]
+
+
+def test_boundary_flags_cover_every_code_flip():
+    """Perturbing alpha* by 5e-10 of the scale (far above the fp64 re-score's
+    error, below the flag's tolerance) changes a code only on flagged tiles;
+    unflagged tiles keep their codes."""
+    rng = np.random.default_rng(123)
+    qmax, n = 7, 4000
+    sc = np.exp(rng.normal(-6, 1, n))
+    x = rng.uniform(-7.4, 7.4, (n, 8))
+    x[: n // 4, 3] = rng.integers(-7, 7, n // 4) + 0.5 + rng.uniform(-4e-10, 4e-10, n // 4)  # near midpoints
+    alpha = x * sc[:, None]
+    flags = O._boundary_flags(alpha, sc, qmax)
+    q0 = np.clip(np.rint(alpha / sc[:, None]), -qmax, qmax)
+    changed = np.zeros(n, bool)
+    for sgn in (-1.0, 1.0):
+        q1 = np.clip(np.rint((alpha + sgn * 5e-10 * sc[:, None]) / sc[:, None]), -qmax, qmax)
+        changed |= np.any(q1 != q0, axis=1)
+    assert flags[: n // 4].all()
+    assert not np.any(changed & ~flags)
+    assert not flags[n // 4:].any()
+
+
+def test_scale_flags_fp16_hand_values():
+    """fp16 scales: flagged exactly when m/qmax lies within 1e-12 (relative)
+    of an fp32 rounding midpoint, where the first of the two roundings of
+    f16(f32(m/qmax)) could go either way."""
+    qmax = 7
+    mid = 1.0 + 2.0 ** -24            # halfway between 1 and the next fp32
+    for v, want in [(mid, True), (mid + 2.0 ** -42, True), (mid - 2.0 ** -42, True),
+                    (mid + 2.0 ** -36, False), (mid - 2.0 ** -36, False),
+                    (1.0, False), (1.1, False), (0.75 + 2.0 ** -25, True), (0.75 + 3 * 2.0 ** -25, True), (0.75 + 2.0 ** -26, False)]:
+        alpha = np.array([[v * qmax, -0.5]])
+        assert bool(O._scale_flags(alpha, qmax)[0]) == want, v
+    assert not O._scale_flags(np.zeros((1, 4)), qmax)[0]
+
+
+def test_scale_flags_fp16_cover_every_rounding_flip():
+    """A relative perturbation of 1e-13 of m changes f32(m/qmax) only on
+    flagged tiles."""
+    rng = np.random.default_rng(7)
+    qmax, n = 7, 20000
+    v = np.exp(rng.normal(-7, 2, n))
+    f = v.astype(np.float32).astype(np.float64)
+    ulp = np.spacing(f.astype(np.float32)).astype(np.float64)
+    v[: n // 10] = (f + 0.5 * ulp)[: n // 10] * (1 + rng.uniform(-1e-14, 1e-14, n // 10))
+    alpha = np.stack([v * qmax, -0.5 * v * qmax], axis=1)
+    flags = O._scale_flags(alpha, qmax)
+    base = (alpha[:, 0] / qmax).astype(np.float32)
+    changed = np.zeros(n, bool)
+    for r in (1 - 1e-13, 1 + 1e-13):
+        changed |= ((alpha[:, 0] * r) / qmax).astype(np.float32) != base
+    assert flags[: n // 10].all()
+    assert changed[: n // 10].any()
+    assert not np.any(changed & ~flags)
+    assert flags[n // 10:].mean() < 1e-3
+
+
+def test_scale_flags_pow2_hand_values():
+    """Power-of-two scales: flagged exactly when m/qmax lies within 1e-12
+    (relative) of a power of two, where the exponent rule of Sec. 3.2 could
+    go either way."""
+    qmax = 7
+    for v, want in [(2.0 ** -5, True), (2.0 ** -5 * (1 + 1e-13), True), (2.0 ** -5 * (1 - 1e-13), True),
+                    (2.0 ** -5 * (1 + 1e-11), False), (2.0 ** -5 * (1 - 1e-11), False),
+                    (3.0 * 2.0 ** -6, False), (1.0, True)]:
+        alpha = np.array([[0.0, -v * qmax]])
+        assert bool(O._scale_flags(alpha, qmax, scale_fmt=O.SCALE_POW2)[0]) == want, v
+    assert not O._scale_flags(np.zeros((1, 2)), qmax, scale_fmt=O.SCALE_POW2)[0]
+
+
+@pytest.mark.parametrize("fmt,gen", [(O.SCALE_FP16, 1), (O.SCALE_POW2, 1), (O.SCALE_FP16, 2)])
+def test_candidate_matches_the_batched_search(fmt, gen):
+    """candidate() (one tile, one seed; used to check the GPU's record when it
+    picks a tied seed) equals the batched search's column for that seed, and
+    its codes and scale at the chosen seed are the search's record."""
+    rng = np.random.default_rng(31 + fmt + 10 * gen)
+    op = O.Params(C=32, P=5, b=4, S=12, basis_key=99, ridge_lambda=1e-6, scale_fmt=fmt, gen_version=gen)
+    R = rng.normal(0, 0.01, (6, 32))
+    D = np.exp(rng.normal(0, 1.5, (6, 32)))
+    out = O.encode_tiles(R, D, op, keep_all=True)
+    for i in range(6):
+        for s in range(op.S):
+            q, bits, g, alpha = O.candidate(R[i], D[i], op, s)
+            # same fp64 steps, batched or not: agreement to rounding order
+            assert abs(g - out["all_gains"][i, s]) <= 1e-12 * out["energy"][i]
+            if s == out["seed"][i]:
+                assert np.array_equal(q, out["codes"][i]) and bits == out["scale"][i]
+                assert np.allclose(alpha, out["alpha"][i], rtol=1e-12, atol=0)
