@@ -1,12 +1,17 @@
 #!/usr/bin/env python3
 """One-GPU benchmark of the AWSRC codec hot path on MI355X.
 
-A step is one pass of the whole path over one synthetic module set already
-resident in HBM: RTN-INT4 backbone, encoder seed search over all tiles and
-seeds, gain ranking + serialization under the byte budget, and decode-add of
-the resulting stream onto W0.  Prints one JSON line.
+A step is one pass of the whole path over one synthetic workload already
+resident in HBM (by default the 36-layer 3B stack: 252 modules, 2.77G
+weights, 43.35M tiles, S = 512 seeds): RTN-INT4 backbone of every module,
+the encoder's seed search over every tile and seed, one global gain ranking
+with serialization at the largest byte budget, decode-add of that stream onto
+W0, and every smaller budget's prefix of the same stream decoded (dense bf16)
+without re-encoding.  Smaller workloads are timed after it and reported under
+"extra"; the oracle's rate on a bounded row sample is "cpu_baseline".  Prints
+one JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload down3b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload stack3b]
 """
 from __future__ import annotations
 
@@ -122,34 +127,49 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(wl, inputs, seconds: float):
-    """The oracle as it stands, on a bounded sample of the same workload's
-    tiles, over worker processes (one thread each) that take contiguous
-    chunks of tiles: a pilot sizes the sample at about 2 x `seconds` of CPU
-    work in all, and the rate is the sample's candidates over the timed
-    map's wall time (the workers are started and warmed first)."""
+def cpu_baseline(wl, sample, seconds: float):
+    """The oracle as it stands, on a bounded, deterministic sample of the same
+    workload: every n-th row of every module (all of that row's tiles), with n
+    the smallest power-of-two multiple of the collected row step whose tiles a
+    pilot estimates at no more than about 2 x `seconds` of CPU work in all.
+    Worker processes (one thread each) take contiguous chunks of tiles; the
+    rate is the sample's candidates over the timed map's wall time (workers
+    started and warmed first).  `sample` holds, per module, the fp32 weights
+    and weights d of the collected rows (every `step`-th row)."""
     import multiprocessing as mp
+
+    import numpy as np
 
     from oracle import awsrc_oracle as O
 
-    m = wl.modules[0]
-    W32 = inputs[0]["W32"].cpu().numpy()
-    d = inputs[0]["d"].cpu().numpy()
     op = O.Params(C=wl.C, P=wl.P, b=wl.b, S=wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
                   idx_bits=wl.idx_bits)
-    _, _, _, W0o = O.rtn_backbone(W32)
-    R = O.tiles(O.residual(W32, W0o), wl.C)
-    D = O.tile_weights(d, m.rows, m.cols, wl.C)
+    step0 = sample["step"]
+
+    def tiles_at(k):
+        Rs, Ds = [], []
+        for m, (W32, d) in zip(wl.modules, sample["rows"]):
+            W32 = W32[::k]
+            dd = d if d.ndim == 1 else d[::k]
+            _, _, _, W0o = O.rtn_backbone(W32)
+            Rs.append(O.tiles(O.residual(W32, W0o), wl.C))
+            Ds.append(O.tile_weights(dd, W32.shape[0], m.cols, wl.C))
+        return np.concatenate(Rs), np.concatenate(Ds)
+
     # the host's CPU share for one GPU is 16 cores, whatever the affinity mask shows
     nproc = max(1, min(16, len(os.sched_getaffinity(0))))
+    R1, D1 = tiles_at(1)
     # pilot in this process: per-tile time (the oracle also pays a fixed cost per call)
-    _oracle_chunk((R[:64], D[:64], op))
-    t1 = _oracle_chunk((R[:64], D[:64], op))
-    t2 = _oracle_chunk((R[:256], D[:256], op))
+    _oracle_chunk((R1[:64], D1[:64], op))
+    t1 = _oracle_chunk((R1[:64], D1[:64], op))
+    t2 = _oracle_chunk((R1[:256], D1[:256], op))
     per_tile = max((t2 - t1) / 192, 1e-6)
-    per = int(max(256, 2.0 * seconds / nproc / per_tile))
-    n2 = int(min(R.shape[0], per * nproc))
-    per = -(-n2 // nproc)
+    k = 1
+    while R1.shape[0] / k * per_tile > 2.0 * seconds * nproc and k < 1 << 20:
+        k *= 2
+    R, D = (R1, D1) if k == 1 else tiles_at(k)
+    n2 = R.shape[0]
+    per = -(-n2 // (4 * nproc))
     jobs = [(R[i:i + per], D[i:i + per], op) for i in range(0, n2, per)]
     ctx = mp.get_context("spawn")  # fresh interpreters: nothing of this process's GPU state
     with ctx.Pool(nproc, initializer=_oracle_warm, initargs=((R[:16], D[:16], op),)) as pool:
@@ -157,102 +177,12 @@ def cpu_baseline(wl, inputs, seconds: float):
         t0 = time.perf_counter()
         pool.map(_oracle_chunk, jobs, chunksize=1)
         dt = time.perf_counter() - t0
-    return {"value": n2 * wl.S / dt, "unit": "candidates/s", "cores": nproc, "kind": "oracle",
-            "cpu": _cpu_model(),
-            "sample": f"first {n2} of {R.shape[0]} tiles of {m.name} ({m.rows}x{m.cols}), all {wl.S} seeds, "
-                      f"fp64 numpy, {len(jobs)} chunks over {nproc} worker processes of 1 thread, "
-                      f"{dt:.1f} s wall"}
-
-
-def decode_at_scale(awsrc, torch, name: str, bpw: float, reps: int):
-    """Decode-add of a large stream: records drawn at random for every tile of
-    the named workload (all gains positive), ranked globally at `bpw`, then
-    applied `reps` times onto fp32 W0 buffers of the workload's shapes (an
-    add onto the same tiles each time).  Timed with HIP events on the
-    library's stream around the apply launches only."""
-    from synth import gen_records, workload
-
-    wl = workload(name)
-    dev = torch.device("cuda:0")
-    shapes = [(m.rows, m.cols) for m in wl.modules]
-    p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                          idx_bits=wl.idx_bits)
-    rec = gen_records(wl.n_tiles, wl.P, wl.b, wl.S, seed=4242, device=dev, frac_nonpositive=0.0, frac_ties=0.0)
-    s, K, _ = awsrc.awsrc_rank_prefix(p, shapes, awsrc.AWSRC_MODE_GLOBAL, bpw, rec["seed"], rec["codes"],
-                                      rec["scale"], rec["gain"])
-    del rec
-    W0 = [torch.zeros(r, c, dtype=torch.float32, device=dev) for r, c in shapes]
-    plan, dws = awsrc.awsrc_decode_prepare(s, W0)
-    stream = torch.cuda.current_stream()
-    awsrc.awsrc_decode_apply(plan)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(reps):
-        awsrc.awsrc_decode_apply(plan)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    nbytes = K * (plan.L_rec + 2 * wl.C * 4)
-    gbs = nbytes / (ms / 1e3) / 1e9
-    del W0, plan, dws
-    rec_stats = reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps, bpw)
-    del s
-    # device-copy ceiling: one large copy, read + write bytes
-    n = 1 << 30
-    x = torch.empty(n, dtype=torch.float32, device=dev)
-    y = torch.empty_like(x)
-    y.copy_(x)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(3):
-        y.copy_(x)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbs = 3 * 2 * 4 * n / (e0.elapsed_time(e1) / 1e3) / 1e9
-    del x, y
-    torch.cuda.empty_cache()
-    rec_stats["frac_copy"] = rec_stats["GB/s"] / copy_gbs
-    return {"workload": f"{name} stream at {bpw} bpw, fp32 W0", "modules": len(shapes), "records": K,
-            "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-            "copy_GB/s": copy_gbs, "frac_copy": gbs / copy_gbs,
-            "traffic": measured_traffic("decode_apply", f"{name}@{bpw}"), "reconstruct_bf16": rec_stats}
-
-
-def reconstruct_at_scale(awsrc, torch, wl, shapes, s, K, reps, bpw):
-    """Dense bf16 reconstruction of every module from a random RTN backbone
-    (codes, fp16 scales in [1e-3, 2e-3), zero points) plus the stream `s`.
-    Algorithmic bytes: codes (1/2 B per weight), scale and zero (3 B per
-    group of 128), the records, and the bf16 output (2 B per weight).  Each
-    call synchronizes once before its two launches, and the timed region
-    (HIP events on the library's stream) includes that host round trip."""
-    dev = torch.device("cuda:0")
-    g = torch.Generator(device=dev).manual_seed(77)
-    bbs = []
-    for r, c in shapes:
-        codes = torch.randint(0, 256, (r, c // 2), dtype=torch.uint8, device=dev, generator=g)
-        sc = (torch.rand(r, c // 128, device=dev, generator=g) * 1e-3 + 1e-3).to(torch.float16).view(torch.int16)
-        z = torch.randint(0, 16, (r, c // 128), dtype=torch.uint8, device=dev, generator=g)
-        bbs.append((codes, sc, z))
-    outs = [torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in shapes]
-    plan, ws = awsrc.awsrc_decode_prepare(s, outs)
-    stream = torch.cuda.current_stream()
-    awsrc.awsrc_reconstruct_bf16(plan, bbs, 128)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(reps):
-        awsrc.awsrc_reconstruct_bf16(plan, bbs, 128)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    n_w = sum(r * c for r, c in shapes)
-    nbytes = n_w // 2 + 3 * (n_w // 128) + K * plan.L_rec + 2 * n_w
-    del outs, bbs, plan, ws
-    torch.cuda.empty_cache()
-    gbs = nbytes / (ms / 1e3) / 1e9
-    return {"weights": n_w, "bytes": nbytes, "ms": ms, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-            "traffic": measured_traffic("reconstruct_bf16", f"{wl.name}@{bpw}")}
+    rate = n2 * wl.S / dt
+    return {"value": rate, "unit": "candidates/s", "cores": nproc, "kind": "oracle", "cpu": _cpu_model(),
+            "sample": f"every {step0 * k}th row of each of the {len(wl.modules)} modules of {wl.name} (all tiles "
+                      f"of those rows): {n2} of {wl.n_tiles} tiles, all {wl.S} seeds, fp64 numpy, {len(jobs)} "
+                      f"chunks over {nproc} worker processes of 1 thread, {dt:.1f} s wall",
+            "extrapolated_full_encode_s": wl.candidates / rate}
 
 
 def mfma_screen(C: int, P: int, per_element: bool, gen_version: int) -> bool:
@@ -317,17 +247,208 @@ def sdq_timing(awsrc, torch, wl, bb, stream, reps: int = 20) -> dict:
             "encode_bytes": enc_bytes}
 
 
+class Run:
+    """One workload resident in HBM and the buffers of its step: inputs W
+    (storage dtype) and d, the backbone (codes, scales, zero points, fp32 W0),
+    the encoder's outputs concatenated in module order, one encode workspace
+    per module, and bf16 buffers for the dense reconstructions."""
+
+    def __init__(self, awsrc, torch, wl, gen_version: int, dev, sample_step: int = 0):
+        from synth import gen_module_inputs
+
+        self.wl = wl
+        self.p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
+                                   idx_bits=wl.idx_bits, gen_version=gen_version)
+        self.shapes = [(m.rows, m.cols) for m in wl.modules]
+        T = wl.n_tiles
+        self.seed = torch.empty(T, dtype=torch.int16, device=dev)
+        self.codes = torch.empty(T, wl.P, dtype=torch.int8, device=dev)
+        self.scale = torch.empty(T, dtype=torch.int16, device=dev)
+        self.gain = torch.empty(T, dtype=torch.float64, device=dev)
+        self.inputs, self.bb, self.enc_out, self.ws = [], [], [], []
+        self.sample = {"step": sample_step, "rows": []}
+        off = 0
+        for m in wl.modules:
+            inp = gen_module_inputs(wl, m, dev)
+            if sample_step:
+                d = inp["d"] if inp["d"].dim() == 1 else inp["d"][::sample_step]
+                self.sample["rows"].append((inp["W32"][::sample_step].cpu().numpy(), d.cpu().numpy()))
+            del inp["W32"]
+            self.inputs.append(inp)
+            t_m = m.rows * m.cols // wl.C
+            self.bb.append((torch.empty(m.rows, m.cols // 2, dtype=torch.uint8, device=dev),
+                            torch.empty(m.rows, m.cols // 128, dtype=torch.int16, device=dev),
+                            torch.empty(m.rows, m.cols // 128, dtype=torch.uint8, device=dev),
+                            torch.empty(m.rows, m.cols, dtype=torch.float32, device=dev)))
+            self.enc_out.append({"seed": self.seed[off:off + t_m], "codes": self.codes[off:off + t_m],
+                                 "scale": self.scale[off:off + t_m], "gain": self.gain[off:off + t_m],
+                                 "alpha": None})
+            d_mode = awsrc.AWSRC_D_PER_COL if inp["d"].dim() == 1 else awsrc.AWSRC_D_PER_ELEM
+            self.ws.append(torch.empty(max(1, awsrc.encode_workspace_bytes(self.p, inp["W"], d_mode)),
+                                       dtype=torch.uint8, device=dev))
+            off += t_m
+        self.outs = [torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in self.shapes]
+        self.mode = awsrc.AWSRC_MODE_GLOBAL if wl.mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
+        self.L = awsrc.awsrc_record_bytes(self.p, T)
+        self.h = awsrc.awsrc_header_bytes(len(self.shapes))
+        self.last = {}
+
+
+STAGES = ("backbone", "encode", "rank", "decode_prepare", "decode_apply", "reconstruct")
+
+
+def run_steps(awsrc, torch, run: Run, steps: int, warmup: int):
+    """Time `steps` steps after `warmup` untimed ones.  A step: backbone of
+    every module; encoder seed search of every module; one ranking at the
+    largest budget; decode-add of that stream in place onto the fp32 W0
+    (prepare = validation and tables, apply = the add); then every budget's
+    record-boundary prefix of the same stream decoded without re-encoding into
+    dense bf16 repaired weights (prepare + reconstruction per prefix).  Stage
+    times come from HIP events on the library's stream; the step time is the
+    host wall clock of exactly the timed steps."""
+    wl = run.wl
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)]
+    acc = dict.fromkeys(STAGES, 0.0)
+    bpw_max = max(wl.budgets)
+    N = wl.n_weights
+    last = run.last
+
+    def step(record: bool):
+        ev[0].record(stream)
+        for inp, b in zip(run.inputs, run.bb):
+            awsrc.awsrc_backbone_rtn(inp["W"], out=b)
+        ev[1].record(stream)
+        for inp, b, e, w in zip(run.inputs, run.bb, run.enc_out, run.ws):
+            awsrc.awsrc_encode_tiles(run.p, inp["W"], b[3], inp["d"], out=e, workspace=w)
+        ev[2].record(stream)
+        s, K, ne = awsrc.awsrc_rank_prefix(run.p, run.shapes, run.mode, bpw_max, run.seed, run.codes, run.scale,
+                                           run.gain, workspace=last.get("rws"))
+        ev[3].record(stream)
+        plan, dws = awsrc.awsrc_decode_prepare(s, [b[3] for b in run.bb], workspace=last.get("dws"))
+        ev[4].record(stream)
+        awsrc.awsrc_decode_apply(plan)
+        ev[5].record(stream)
+        prefixes = []
+        rcws = last.get("rcws")
+        for bpw in sorted(wl.budgets):
+            if run.mode == awsrc.AWSRC_MODE_GLOBAL:
+                kb = min(ne, (awsrc.awsrc_budget_bytes(bpw, N) - run.h) // run.L)
+            else:
+                kb = K
+            plan_b, rcws = awsrc.awsrc_decode_prepare(s, run.outs, stream_len=run.h + kb * run.L, workspace=rcws)
+            awsrc.awsrc_reconstruct_bf16(plan_b, [b[:3] for b in run.bb], 128)
+            prefixes.append((bpw, kb))
+        ev[6].record(stream)
+        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), dws=dws, rcws=rcws, prefixes=prefixes)
+        if record:
+            torch.cuda.synchronize()
+            for k, (a, b) in zip(STAGES, zip(ev[:-1], ev[1:])):
+                acc[k] += a.elapsed_time(b)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t_wall = 0.0
+    for _ in range(steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        step(True)
+        t_wall += time.perf_counter() - t0
+    return 1e3 * t_wall / steps, {k: v / steps for k, v in acc.items()}
+
+
+def encode_roofline(awsrc, run: Run, stage_ms: dict, gen_version: int) -> dict:
+    """Roofline of the encoder calls of a step (all of a workload's modules):
+    the split matrix-core / vector-ALU bound with the full-score fraction the
+    screens report, or the vector-ALU line where no matrix-core screen runs."""
+    wl = run.wl
+    cand = wl.candidates
+    per_elem = wl.d_mode == "elem"
+    opc = ops_per_candidate(wl.C, wl.P, per_elem, gen_version)
+    enc_s = stage_ms["encode"] / 1e3
+    scored = sum(awsrc.awsrc_encode_scored(e) for e in run.enc_out)
+    f_scored = scored / cand
+    if mfma_screen(wl.C, wl.P, per_elem, gen_version):
+        sb = encode_split_bound(wl.C, wl.P, per_elem, gen_version, f_scored)
+        t_mfma = cand * sb["mfma_flops_per_candidate"] / (PEAK_MFMA_BF16_TFLOPS * 1e12)
+        t_valu = cand * sb["valu_ops_per_candidate"] / (PEAK_VALU_TOPS * 1e12)
+        if t_mfma >= t_valu:
+            bound, unit, peak = "mfma", "TFLOP/s", PEAK_MFMA_BF16_TFLOPS
+            achieved = cand * sb["mfma_flops_per_candidate"] / enc_s / 1e12
+        else:
+            bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
+            achieved = cand * sb["valu_ops_per_candidate"] / enc_s / 1e12
+        split = dict(sb, scored_fraction=f_scored, t_mfma_ms=1e3 * t_mfma, t_valu_ms=1e3 * t_valu)
+    else:
+        bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
+        achieved = cand * opc / enc_s / 1e12
+        split = {"scored_fraction": f_scored}
+    return {"bound": bound, "kernel": f"awsrc_encode_tiles over the {len(wl.modules)} module(s) of a step "
+                                      "(basis, factors, screen, fp64 re-score)",
+            "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+            "traffic": measured_traffic("encode", wl.name) if gen_version == 1 else None,
+            "traffic_unit": "bytes per step (all encoder calls)", "split": split,
+            "ops_per_candidate_unpruned": opc}
+
+
+def workload_result(awsrc, run: Run, ms_step: float, stage_ms: dict, gen_version: int) -> dict:
+    wl = run.wl
+    last = run.last
+    K = last["K"]
+    L = run.L
+    dec_bytes = K * (L + 2 * wl.C * 4)  # records, and the fp32 tiles they touch read and written
+    t_call = (stage_ms["decode_prepare"] + stage_ms["decode_apply"]) / 1e3
+    t_apply = stage_ms["decode_apply"] / 1e3
+    dec_gbs = dec_bytes / t_call / 1e9 if t_call > 0 else None
+    app_gbs = dec_bytes / t_apply / 1e9 if t_apply > 0 else None
+    n_w = wl.n_weights
+    n_groups = n_w // 128
+    bb_bytes = n_w * (2 if wl.w_dtype == "bf16" else 4) + n_w // 2 + 3 * n_groups + 4 * n_w
+    bb_gbs = bb_bytes / (stage_ms["backbone"] / 1e3) / 1e9
+    # dense reconstructions: per prefix, codes 1/2 B and bf16 output 2 B per
+    # weight, scale and zero 3 B per group, plus the prefix's records
+    rc_bytes = sum(n_w // 2 + 3 * n_groups + 2 * n_w + kb * L for _, kb in last["prefixes"])
+    rc_gbs = rc_bytes / (stage_ms["reconstruct"] / 1e3) / 1e9
+    enc_s = stage_ms["encode"] / 1e3
+    return {
+        "config": {"workload": wl.name, "modules": len(wl.modules), "C": wl.C, "P": wl.P, "b": wl.b, "S": wl.S,
+                   "weights": wl.d_mode, "mode": wl.mode, "budgets_bpw": list(wl.budgets), "tiles": wl.n_tiles,
+                   "n_weights": n_w, "candidates": wl.candidates, "generator": gen_version},
+        "ms_per_step": ms_step,
+        "candidates_per_s_step": wl.candidates / (ms_step / 1e3),
+        "encode_candidates_per_s": wl.candidates / enc_s,
+        "roofline_encode": encode_roofline(awsrc, run, stage_ms, gen_version),
+        "decode_add": {"stream_bpw": max(wl.budgets), "records": K, "bytes": dec_bytes,
+                       "ms": 1e3 * t_call, "GB/s": dec_gbs,
+                       "frac_hbm": dec_gbs / PEAK_HBM_GBS if dec_gbs else None,
+                       "apply_ms": 1e3 * t_apply, "apply_GB/s": app_gbs,
+                       "apply_frac_hbm": app_gbs / PEAK_HBM_GBS if app_gbs else None,
+                       "note": "GB/s and frac_hbm over the whole awsrc_decode_add (validation + apply); "
+                               "apply_* for the add alone, as with a prepared plan reused",
+                       "traffic": measured_traffic("decode_apply", wl.name)},
+        "prefixes": [{"bpw": b, "records": kb} for b, kb in last["prefixes"]],
+        "reconstruct_bf16": {"prefixes": len(last["prefixes"]), "bytes": rc_bytes, "ms": stage_ms["reconstruct"],
+                             "GB/s": rc_gbs, "frac_hbm": rc_gbs / PEAK_HBM_GBS,
+                             "traffic": measured_traffic("reconstruct_bf16", wl.name)},
+        "backbone": {"bytes": bb_bytes, "ms": stage_ms["backbone"], "GB/s": bb_gbs,
+                     "frac_hbm": bb_gbs / PEAK_HBM_GBS, "traffic": measured_traffic("backbone", wl.name)},
+        "stage_ms": stage_ms,
+        "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="down3b")
+    ap.add_argument("--steps", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="stack3b")
+    ap.add_argument("--extra", default="down3b,block3b,layer32b",
+                    help="further workloads timed after the headline one and reported under 'extra' ('' for none)")
+    ap.add_argument("--extra-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--decode-workload", default="stack3b",
-                    help="workload whose shapes size the at-scale decode-add measurement ('' to skip)")
-    ap.add_argument("--decode-bpw", type=float, default=0.32)
     ap.add_argument("--gen-version", type=int, default=1, choices=(1, 2),
                     help="basis generator version (2 adds the seeded coordinate permutation)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -352,139 +473,55 @@ def main() -> int:
         return 0
 
     import paper_2608_23144_amd as awsrc
-    from synth import gen_module_inputs, workload
+    from synth import workload
 
-    wl = workload(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    p = awsrc.make_params(wl.C, wl.P, wl.b, wl.S, basis_key=wl.basis_key, ridge_lambda=wl.ridge_lambda,
-                          idx_bits=wl.idx_bits, gen_version=args.gen_version)
-    mods = wl.modules
-    log(f"[bench] workload {wl.name}: {len(mods)} module(s), {wl.n_weights} weights, T={wl.n_tiles}, S={wl.S}")
-    inputs = [gen_module_inputs(wl, m, dev) for m in mods]
-    T = wl.n_tiles
-    seed = torch.empty(T, dtype=torch.int16, device=dev)
-    codes = torch.empty(T, wl.P, dtype=torch.int8, device=dev)
-    scale = torch.empty(T, dtype=torch.int16, device=dev)
-    gain = torch.empty(T, dtype=torch.float64, device=dev)
-    bb, enc_out, ws = [], [], []
-    off = 0
-    for m, inp in zip(mods, inputs):
-        t_m = m.rows * m.cols // wl.C
-        bb.append((torch.empty(m.rows, m.cols // 2, dtype=torch.uint8, device=dev),
-                   torch.empty(m.rows, m.cols // 128, dtype=torch.int16, device=dev),
-                   torch.empty(m.rows, m.cols // 128, dtype=torch.uint8, device=dev),
-                   torch.empty(m.rows, m.cols, dtype=torch.float32, device=dev)))
-        enc_out.append({"seed": seed[off:off + t_m], "codes": codes[off:off + t_m], "scale": scale[off:off + t_m],
-                        "gain": gain[off:off + t_m], "alpha": None})
-        d_mode = awsrc.AWSRC_D_PER_COL if inp["d"].dim() == 1 else awsrc.AWSRC_D_PER_ELEM
-        ws.append(torch.empty(awsrc.encode_workspace_bytes(p, inp["W"], d_mode), dtype=torch.uint8, device=dev))
-        off += t_m
-    shapes = [(m.rows, m.cols) for m in mods]
-    mode = awsrc.AWSRC_MODE_GLOBAL if wl.mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
-    bpw = max(wl.budgets)
-    stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
-    acc = {"backbone": 0.0, "encode": 0.0, "rank": 0.0, "decode_prepare": 0.0, "decode_apply": 0.0}
-    last = {}
-
-    def step(record: bool):
-        ev[0].record(stream)
-        for inp, b in zip(inputs, bb):
-            awsrc.awsrc_backbone_rtn(inp["W"], out=b)
-        ev[1].record(stream)
-        for inp, b, e, w in zip(inputs, bb, enc_out, ws):
-            awsrc.awsrc_encode_tiles(p, inp["W"], b[3], inp["d"], out=e, workspace=w)
-        ev[2].record(stream)
-        s, K, ne = awsrc.awsrc_rank_prefix(p, shapes, mode, bpw, seed, codes, scale, gain)
-        ev[3].record(stream)
-        plan, dws = awsrc.awsrc_decode_prepare(s, [b[3] for b in bb], workspace=last.get("dws"))
-        ev[4].record(stream)
-        awsrc.awsrc_decode_apply(plan)
-        ev[5].record(stream)
-        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), L=plan.L_rec, dws=dws)
-        if record:
-            torch.cuda.synchronize()
-            for k, (a, b) in zip(acc, zip(ev[:-1], ev[1:])):
-                acc[k] += a.elapsed_time(b)
-
-    for _ in range(args.warmup):
-        step(False)
+    wl = workload(args.workload)
+    log(f"[bench] workload {wl.name}: {len(wl.modules)} module(s), {wl.n_weights} weights, T={wl.n_tiles}, "
+        f"S={wl.S}; generating inputs")
+    run = Run(awsrc, torch, wl, args.gen_version, dev, sample_step=0 if args.no_cpu_baseline else 256)
     torch.cuda.synchronize()
-    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
-    # wall clock over exactly K steps; stage events are read after each step
-    t_wall = 0.0
-    for _ in range(args.steps):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        step(True)
-        t_wall += time.perf_counter() - t0
-    ms_step = 1e3 * t_wall / args.steps
-    stage_ms = {k: v / args.steps for k, v in acc.items()}
-    cand = wl.candidates
-    value = cand / (ms_step / 1e3)
-
-    per_elem = wl.d_mode == "elem"
-    opc = ops_per_candidate(wl.C, wl.P, per_elem, args.gen_version)
-    enc_s = stage_ms["encode"] / 1e3
-    # candidates scored in full by the last step's screens (the pruned screen
-    # scores a data-dependent part; every other screen scores all)
-    scored = sum(awsrc.awsrc_encode_scored(e) for e in enc_out)
-    f_scored = scored / cand
-    if mfma_screen(wl.C, wl.P, per_elem, args.gen_version):
-        sb = encode_split_bound(wl.C, wl.P, per_elem, args.gen_version, f_scored)
-        t_mfma = cand * sb["mfma_flops_per_candidate"] / (PEAK_MFMA_BF16_TFLOPS * 1e12)
-        t_valu = cand * sb["valu_ops_per_candidate"] / (PEAK_VALU_TOPS * 1e12)
-        if t_mfma >= t_valu:
-            bound, unit, peak = "mfma", "TFLOP/s", PEAK_MFMA_BF16_TFLOPS
-            achieved = cand * sb["mfma_flops_per_candidate"] / enc_s / 1e12
-        else:
-            bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
-            achieved = cand * sb["valu_ops_per_candidate"] / enc_s / 1e12
-        split = dict(sb, scored_fraction=f_scored, t_mfma_ms=1e3 * t_mfma, t_valu_ms=1e3 * t_valu)
-    else:
-        bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
-        achieved = cand * opc / enc_s / 1e12
-        split = {"scored_fraction": f_scored}
-    K, L = last["K"], last["L"]
-    dec_bytes = K * (L + 2 * wl.C * 4)
-    dec_gbs = dec_bytes / (stage_ms["decode_apply"] / 1e3) / 1e9 if stage_ms["decode_apply"] > 0 else None
-    n_groups = wl.n_weights // 128
-    bb_bytes = wl.n_weights * (2 if wl.w_dtype == "bf16" else 4) + wl.n_weights // 2 + 3 * n_groups + 4 * wl.n_weights
-    bb_gbs = bb_bytes / (stage_ms["backbone"] / 1e3) / 1e9
-
+    log(f"[bench] inputs resident ({torch.cuda.memory_allocated() / 2**30:.1f} GiB); "
+        f"{args.warmup} warmup + {args.steps} timed steps")
+    ms_step, stage_ms = run_steps(awsrc, torch, run, args.steps, args.warmup)
+    res = workload_result(awsrc, run, ms_step, stage_ms, args.gen_version)
+    log(f"[bench] {wl.name}: {ms_step:.2f} ms/step, encode {stage_ms['encode']:.2f} ms")
+    stream = torch.cuda.current_stream()
     out = {
-        "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "modules": [f"{r}x{c}" for r, c in shapes], "C": wl.C, "P": wl.P,
-                   "b": wl.b, "S": wl.S, "weights": wl.d_mode, "mode": wl.mode, "bpw": bpw, "tiles": T,
-                   "candidates": cand, "generator": args.gen_version},
-        "roofline": {"bound": bound, "kernel": "awsrc_encode_tiles (basis, factors, screen, fp64 re-score)",
-                     "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-                     "traffic": measured_traffic("encode", wl.name) if args.gen_version == 1 else None,
-                     "traffic_unit": "bytes per launch", "split": split,
-                     "ops_per_candidate_unpruned": opc},
-        "encode_candidates_per_s": cand / enc_s,
-        "decode_add": {"records": K, "bytes": dec_bytes, "ms": stage_ms["decode_apply"], "GB/s": dec_gbs,
-                       "frac_hbm": (dec_gbs / PEAK_HBM_GBS) if dec_gbs else None,
-                       "traffic": measured_traffic("decode_apply", wl.name)},
-        "backbone": {"bytes": bb_bytes, "ms": stage_ms["backbone"], "GB/s": bb_gbs, "frac_hbm": bb_gbs / PEAK_HBM_GBS,
-                     "traffic": measured_traffic("backbone", wl.name)},
+        "metric": METRIC, "value": wl.candidates / (ms_step / 1e3), "unit": "candidates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": dict(res["config"], bpw=max(wl.budgets)),
+        "roofline": res["roofline_encode"],
+        "encode_candidates_per_s": res["encode_candidates_per_s"],
+        "decode_add": res["decode_add"],
+        "reconstruct_bf16": res["reconstruct_bf16"],
+        "backbone": res["backbone"],
+        "prefixes": res["prefixes"],
         "stage_ms": stage_ms,
-        "stream": {"K": K, "n_eligible": last["n_eligible"], "bytes": last["stream_len"], "L_rec": L},
+        "stream": res["stream"],
         "device": torch.cuda.get_device_name(0),
     }
-    out["backbone_sdq"] = sdq_timing(awsrc, torch, wl, bb, stream)
-    del inputs, bb, enc_out, ws
+    out["backbone_sdq"] = sdq_timing(awsrc, torch, wl, run.bb, stream)
+    sample = run.sample
+    del run
     torch.cuda.empty_cache()
-    if args.decode_workload:
-        log(f"[bench] decode-add at scale: {args.decode_workload} at {args.decode_bpw} bpw")
-        out["decode_add_at_scale"] = decode_at_scale(awsrc, torch, args.decode_workload, args.decode_bpw, 5)
+    extra = {}
+    for name in [x for x in args.extra.split(",") if x and x != wl.name]:
+        xw = workload(name)
+        log(f"[bench] extra workload {name}")
+        xr = Run(awsrc, torch, xw, args.gen_version, dev)
+        ms_x, st_x = run_steps(awsrc, torch, xr, args.extra_steps, 2)
+        extra[name] = workload_result(awsrc, xr, ms_x, st_x, args.gen_version)
+        log(f"[bench] {name}: {ms_x:.2f} ms/step, encode {st_x['encode']:.2f} ms")
+        del xr
+        torch.cuda.empty_cache()
+    if extra:
+        out["extra"] = extra
     if not args.no_cpu_baseline:
-        wl_inputs = [gen_module_inputs(wl, m, dev) for m in mods[:1]]
         log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(wl, wl_inputs, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, sample, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -17,14 +17,18 @@ def test_cpu_baseline_pool_reports_rate_cores_and_sample():
     a sample description."""
     import bench
 
-    m = Module("t", 64, 256, 0, 0, 0)
-    wl = dataclasses.replace(workload("linear256", S=8, P=4), modules=(m,))
-    inp = gen_module_inputs(wl, m, "cpu")
-    r = bench.cpu_baseline(wl, [inp], 0.2)
+    mods = (Module("t", 64, 256, 0, 0, 0), Module("u", 32, 128, 0, 1, 1))
+    wl = dataclasses.replace(workload("block3b", S=8, P=4), modules=mods)
+    rows = []
+    for m in mods:
+        inp = gen_module_inputs(wl, m, "cpu")
+        rows.append((inp["W32"][::2].numpy(), inp["d"][::2].numpy()))
+    r = bench.cpu_baseline(wl, {"step": 2, "rows": rows}, 0.2)
     assert r["kind"] == "oracle" and r["unit"] == "candidates/s" and r["value"] > 0
     assert 1 <= r["cores"] <= 16 and r["cores"] <= len(os.sched_getaffinity(0))
     assert isinstance(r["cpu"], str) and r["cpu"]
-    assert f"of {64 * 256 // 64} tiles" in r["sample"] and "worker processes" in r["sample"]
+    assert "of the 2 modules" in r["sample"] and "worker processes" in r["sample"]
+    assert r["extrapolated_full_encode_s"] > 0
 
 
 def test_bench_refuses_more_than_one_gpu():
