@@ -14,6 +14,16 @@ __device__ __forceinline__ uint16_t scale_bits_from_f32(float v) {
   return hb;
 }
 
+// The same from an fp64 quotient: round to fp32 first, then to fp16.  The
+// empty asm keeps the fp32 value opaque; without it the compiler folds the two
+// conversions into one fp64 -> fp16 rounding, which differs from the two-step
+// rounding in about 7e-5 of cases (values near an fp16 rounding midpoint).
+__device__ __forceinline__ uint16_t scale_bits_from_f64(double v) {
+  float f = __double2float_rn(v);
+  __asm__ volatile("" : "+v"(f));
+  return scale_bits_from_f32(f);
+}
+
 // In-register fast Walsh-Hadamard transform, natural (Sylvester) order.
 template <int C, typename T>
 __device__ __forceinline__ void fwht(T (&v)[C]) {
@@ -93,7 +103,7 @@ __device__ __forceinline__ double solve_score64(const EncodeArgs& a, const doubl
       sc = ldexp(1.0, e);
     } else {
       // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
-      bits = scale_bits_from_f32(__double2float_rn(m / (double)qmax));
+      bits = scale_bits_from_f64(m / (double)qmax);
       sc = (double)__half2float(__ushort_as_half(bits));
       if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
     }
