@@ -30,8 +30,10 @@
  *    returns an error found during argument validation.  awsrc_last_error()
  *    returns a text description of the calling thread's last error.
  *  - The library keeps no mutable global state besides that per-thread error
- *    text, so calls on different streams may run concurrently provided their
- *    buffers do not overlap.  The small host copies of a call (a stream
+ *    text and the scratch array of awsrc_encode_tiles_noalloc (with its
+ *    per-device address, looked up once), so calls on different streams may
+ *    run concurrently provided their buffers do not overlap (that entry point
+ *    excepted, see there).  The small host copies of a call (a stream
  *    header, module tables, totals) go through host memory owned by that
  *    call, and a call that synchronizes waits on its own stream only.
  *
@@ -194,6 +196,30 @@ awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_
                                 int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
                                 uint16_t* scale_out, double* gain_out, float* alpha_or_null,
                                 void* workspace, size_t* ws_bytes, void* stream);
+
+/*
+ * awsrc_encode_tiles without a workspace, for callers that cannot allocate
+ * device memory (code under stream capture, serving loops, harnesses that
+ * forbid allocation).  Same arguments, outputs and kernels as
+ * awsrc_encode_tiles; the scratch space (basis and factor tables, screened
+ * top lists) is one fixed device array per GPU inside the library, of
+ * awsrc_encode_noalloc_max_bytes() bytes (64 MiB), held from the library's
+ * load until the process ends; nothing is allocated or freed.  Its device
+ * address is looked up on the first call on each device (the current device,
+ * which `stream` must belong to).  A module whose scratch need (the size
+ * awsrc_encode_tiles' query reports) exceeds the array returns AWSRC_ENOSPC
+ * before anything is launched.  Every call on a GPU uses the same array:
+ * calls that overlap on one GPU (different streams, or threads) race and must
+ * be serialized by the caller; calls ordered on one stream are safe.  Nothing
+ * in the array needs to start at zero (each call writes what it reads).
+ */
+awsrc_status awsrc_encode_tiles_noalloc(const awsrc_params* p, const void* W, int32_t w_dtype,
+                                        const float* W0, int64_t rows, int64_t cols, const float* d,
+                                        int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                                        uint16_t* scale_out, double* gain_out, float* alpha_or_null,
+                                        void* stream);
+/* Size in bytes of awsrc_encode_tiles_noalloc's scratch array. */
+uint64_t awsrc_encode_noalloc_max_bytes(void);
 
 /*
  * Work statistic of the last awsrc_encode_tiles call that used `workspace`

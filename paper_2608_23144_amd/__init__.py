@@ -26,6 +26,7 @@ AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_sdq_encode",
             "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
+            "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
             "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
@@ -70,6 +71,8 @@ def _load() -> ctypes.CDLL:
         "awsrc_backbone_sdq_dequant": (i32, [vp, vp, vp, vp, vp, i64, i64, i32, vp, vp]),
         "awsrc_encode_tiles": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp,
                                      ctypes.POINTER(sz), vp]),
+        "awsrc_encode_tiles_noalloc": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp]),
+        "awsrc_encode_noalloc_max_bytes": (u64, []),
         "awsrc_encode_scored": (i32, [vp, ctypes.POINTER(u64), vp]),
         "awsrc_rank_prefix": (i32, [pp, i32, P64, P64, i32, ctypes.c_double, vp, vp, vp, vp, vp, u64,
                                     ctypes.POINTER(u64), P64, P64, vp, ctypes.POINTER(sz), vp]),
@@ -227,6 +230,24 @@ def awsrc_encode_tiles(p: awsrc_params, W: torch.Tensor, W0: torch.Tensor, d: to
                                   _ptr(out["gain"]), _ptr(out.get("alpha")), _ptr(workspace),
                                   ctypes.byref(n), _stream(stream)))
     out["workspace"] = workspace
+    return out
+
+
+def awsrc_encode_noalloc_max_bytes() -> int:
+    return int(LIB.awsrc_encode_noalloc_max_bytes())
+
+
+def awsrc_encode_tiles_noalloc(p: awsrc_params, W: torch.Tensor, W0: torch.Tensor, d: torch.Tensor,
+                               out: Dict[str, torch.Tensor], stream=None) -> Dict[str, torch.Tensor]:
+    """awsrc_encode_tiles into caller-provided outputs (keys seed, codes,
+    scale, gain, optional alpha), with the library's fixed scratch array
+    instead of a workspace: allocates nothing."""
+    _dev(W, W0, d, *[v for v in out.values() if isinstance(v, torch.Tensor)])
+    rows, cols = W.shape
+    d_mode = AWSRC_D_PER_COL if d.dim() == 1 else AWSRC_D_PER_ELEM
+    _check(LIB.awsrc_encode_tiles_noalloc(ctypes.byref(p), _ptr(W), _dtype_code(W), _ptr(W0), rows, cols, _ptr(d),
+                                          d_mode, _ptr(out["seed"]), _ptr(out["codes"]), _ptr(out["scale"]),
+                                          _ptr(out["gain"]), _ptr(out.get("alpha")), _stream(stream)))
     return out
 
 

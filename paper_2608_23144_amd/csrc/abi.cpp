@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -184,6 +185,61 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   HIPCHK(launch_encode_screen(a, s));
   if (!a.fused_rescore) HIPCHK(launch_encode_finalize(a, s));
   return AWSRC_OK;
+}
+
+// ---------------------------------------------------------------- encode, no allocation
+namespace {
+
+// Scratch of awsrc_encode_tiles_noalloc: one copy per GPU, held from the
+// library's load until the process ends.  In host code `scratch` only names
+// the symbol; its device address on the current GPU comes from
+// hipGetSymbolAddress, looked up once per device and kept in g_scratch_ptr.
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+__device__ __attribute__((aligned(256))) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+awsrc_status device_scratch(void** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(AWSRC_EINVAL, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    HIPCHK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(AWSRC_EDEVICE, "no device address for the scratch array");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return AWSRC_OK;
+}
+
+}  // namespace
+
+extern "C" uint64_t awsrc_encode_noalloc_max_bytes(void) { return kNoallocScratchBytes; }
+
+extern "C" awsrc_status awsrc_encode_tiles_noalloc(const awsrc_params* p, const void* W, int32_t w_dtype,
+                                                   const float* W0, int64_t rows, int64_t cols, const float* d,
+                                                   int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                                                   uint16_t* scale_out, double* gain_out, float* alpha_or_null,
+                                                   void* stream) {
+  // the size query validates every argument that does not need the device
+  size_t need = 0;
+  awsrc_status st = awsrc_encode_tiles(p, W, w_dtype, W0, rows, cols, d, d_mode, seed_out, code_out, scale_out,
+                                       gain_out, alpha_or_null, nullptr, &need, stream);
+  if (st) return st;
+  if (need > kNoallocScratchBytes)
+    return fail(AWSRC_ENOSPC, "module needs %zu bytes of scratch, more than the %zu-byte static array", need,
+                kNoallocScratchBytes);
+  if (rows == 0) return AWSRC_OK;
+  void* ws = nullptr;
+  st = device_scratch(&ws);
+  if (st) return st;
+  size_t n = kNoallocScratchBytes;
+  return awsrc_encode_tiles(p, W, w_dtype, W0, rows, cols, d, d_mode, seed_out, code_out, scale_out, gain_out,
+                            alpha_or_null, ws, &n, stream);
 }
 
 extern "C" awsrc_status awsrc_sdq_encode(const uint16_t* scale_f16, int64_t n_groups, int8_t* code,

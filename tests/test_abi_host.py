@@ -170,3 +170,19 @@ def test_sdq_rejects_bad_arguments_without_device_access():
     assert deq(p + 2, p, p, p, p, 2, 256, 128, p, None) == awsrc.AWSRC_EINVAL  # codes alignment
     assert deq(p, p, p, p, p, 2, 256, 128, p + 4, None) == awsrc.AWSRC_EINVAL  # W0 alignment
     assert deq(p, p, p, p, p, 0, 256, 128, p, None) == awsrc.AWSRC_OK
+
+
+def test_noalloc_encode_refuses_oversized_module_without_a_device():
+    """The allocation-free encoder checks the module's scratch need against its
+    fixed array (64 MiB) before it looks at the device: a 2048 x 11008 module
+    with 65536 seeds (a per-column factor table of about 2 GB) is refused."""
+    assert awsrc.awsrc_encode_noalloc_max_bytes() == 64 << 20
+    p = awsrc.make_params(64, 8, 4, 65536)
+    rc = awsrc.LIB.awsrc_encode_tiles_noalloc(ctypes.byref(p), None, awsrc.AWSRC_DTYPE_BF16, None, 2048, 11008,
+                                              None, awsrc.AWSRC_D_PER_COL, None, None, None, None, None, None)
+    assert rc == awsrc.AWSRC_ENOSPC
+    assert b"static array" in awsrc.LIB.awsrc_last_error()
+    p = awsrc.make_params(64, 8, 4, 1)  # invalid S: rejected as EINVAL first
+    rc = awsrc.LIB.awsrc_encode_tiles_noalloc(ctypes.byref(p), None, awsrc.AWSRC_DTYPE_BF16, None, 2048, 11008,
+                                              None, awsrc.AWSRC_D_PER_COL, None, None, None, None, None, None)
+    assert rc == awsrc.AWSRC_EINVAL
