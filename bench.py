@@ -192,10 +192,15 @@ def mfma_screen(C: int, P: int, per_element: bool, gen_version: int) -> bool:
     return C == 64 or (C == 128 and not per_element)
 
 
-def bound_ops_per_candidate(P: int) -> float:
+def bound_ops_per_candidate(P: int, per_element: bool = False) -> float:
     """Vector work of the pruning bound per candidate: the forward solve with the
-    unit lower factor (P(P-1)/2), sum of w_p^2 / e_p (2P) and the comparison."""
-    return P * (P - 1) / 2 + 2 * P + 1
+    unit lower factor (P(P-1)/2), sum of w_p^2 / e_p (2P) and the comparison;
+    with per-element weights every candidate's factor comes first (the Gram
+    gather and the P x P factorization)."""
+    ops = P * (P - 1) / 2 + 2 * P + 1
+    if per_element:
+        ops += P * (P + 1) / 2 + P ** 3 / 6 + P * P / 2 + P / 3
+    return ops
 
 
 def encode_split_bound(C: int, P: int, per_element: bool, gen_version: int, scored_frac: float) -> dict:
@@ -206,7 +211,7 @@ def encode_split_bound(C: int, P: int, per_element: bool, gen_version: int, scor
     (ops_per_candidate less the projection).  Without pruning the fraction is 1."""
     proj = min(P * C, C * int(math.log2(C)))
     full = ops_per_candidate(C, P, per_element, gen_version) - proj
-    bnd = bound_ops_per_candidate(P)
+    bnd = bound_ops_per_candidate(P, per_element)
     valu = bnd + scored_frac * (full - bnd) if scored_frac < 1.0 else full
     return {"mfma_flops_per_candidate": 6.0 * P * C, "valu_ops_per_candidate": valu}
 
@@ -250,8 +255,9 @@ def sdq_timing(awsrc, torch, wl, bb, stream, reps: int = 20) -> dict:
 class Run:
     """One workload resident in HBM and the buffers of its step: inputs W
     (storage dtype) and d, the backbone (codes, scales, zero points, fp32 W0),
-    the encoder's outputs concatenated in module order, one encode workspace
-    per module, and bf16 buffers for the dense reconstructions."""
+    the encoder's outputs concatenated in module order with its workspace (one
+    awsrc_encode_modules call encodes every module), and bf16 buffers for the
+    dense reconstructions."""
 
     def __init__(self, awsrc, torch, wl, gen_version: int, dev, sample_step: int = 0):
         from synth import gen_module_inputs
@@ -265,7 +271,7 @@ class Run:
         self.codes = torch.empty(T, wl.P, dtype=torch.int8, device=dev)
         self.scale = torch.empty(T, dtype=torch.int16, device=dev)
         self.gain = torch.empty(T, dtype=torch.float64, device=dev)
-        self.inputs, self.bb, self.enc_out, self.ws = [], [], [], []
+        self.inputs, self.bb = [], []
         self.sample = {"step": sample_step, "rows": []}
         off = 0
         for m in wl.modules:
@@ -280,13 +286,16 @@ class Run:
                             torch.empty(m.rows, m.cols // 128, dtype=torch.int16, device=dev),
                             torch.empty(m.rows, m.cols // 128, dtype=torch.uint8, device=dev),
                             torch.empty(m.rows, m.cols, dtype=torch.float32, device=dev)))
-            self.enc_out.append({"seed": self.seed[off:off + t_m], "codes": self.codes[off:off + t_m],
-                                 "scale": self.scale[off:off + t_m], "gain": self.gain[off:off + t_m],
-                                 "alpha": None})
-            d_mode = awsrc.AWSRC_D_PER_COL if inp["d"].dim() == 1 else awsrc.AWSRC_D_PER_ELEM
-            self.ws.append(torch.empty(max(1, awsrc.encode_workspace_bytes(self.p, inp["W"], d_mode)),
-                                       dtype=torch.uint8, device=dev))
             off += t_m
+        self.enc_out = {"seed": self.seed, "codes": self.codes, "scale": self.scale, "gain": self.gain,
+                        "alpha": None}
+        d_mode = awsrc.AWSRC_D_PER_COL if wl.d_mode == "col" else awsrc.AWSRC_D_PER_ELEM
+        w_dtype = awsrc.AWSRC_DTYPE_BF16 if wl.w_dtype == "bf16" else awsrc.AWSRC_DTYPE_F32
+        self.ws = torch.empty(max(1, awsrc.encode_modules_workspace_bytes(self.p, self.shapes, w_dtype, d_mode)),
+                              dtype=torch.uint8, device=dev)
+        self.W_list = [inp["W"] for inp in self.inputs]
+        self.d_list = [inp["d"] for inp in self.inputs]
+        self.W0_list = [b[3] for b in self.bb]
         self.outs = [torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in self.shapes]
         self.mode = awsrc.AWSRC_MODE_GLOBAL if wl.mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
         self.L = awsrc.awsrc_record_bytes(self.p, T)
@@ -319,8 +328,7 @@ def run_steps(awsrc, torch, run: Run, steps: int, warmup: int):
         for inp, b in zip(run.inputs, run.bb):
             awsrc.awsrc_backbone_rtn(inp["W"], out=b)
         ev[1].record(stream)
-        for inp, b, e, w in zip(run.inputs, run.bb, run.enc_out, run.ws):
-            awsrc.awsrc_encode_tiles(run.p, inp["W"], b[3], inp["d"], out=e, workspace=w)
+        awsrc.awsrc_encode_modules(run.p, run.W_list, run.W0_list, run.d_list, out=run.enc_out, workspace=run.ws)
         ev[2].record(stream)
         s, K, ne = awsrc.awsrc_rank_prefix(run.p, run.shapes, run.mode, bpw_max, run.seed, run.codes, run.scale,
                                            run.gain, workspace=last.get("rws"))
@@ -367,7 +375,7 @@ def encode_roofline(awsrc, run: Run, stage_ms: dict, gen_version: int) -> dict:
     per_elem = wl.d_mode == "elem"
     opc = ops_per_candidate(wl.C, wl.P, per_elem, gen_version)
     enc_s = stage_ms["encode"] / 1e3
-    scored = sum(awsrc.awsrc_encode_scored(e) for e in run.enc_out)
+    scored = awsrc.awsrc_encode_scored(run.enc_out)
     f_scored = scored / cand
     if mfma_screen(wl.C, wl.P, per_elem, gen_version):
         sb = encode_split_bound(wl.C, wl.P, per_elem, gen_version, f_scored)
@@ -384,7 +392,7 @@ def encode_roofline(awsrc, run: Run, stage_ms: dict, gen_version: int) -> dict:
         bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
         achieved = cand * opc / enc_s / 1e12
         split = {"scored_fraction": f_scored}
-    return {"bound": bound, "kernel": f"awsrc_encode_tiles over the {len(wl.modules)} module(s) of a step "
+    return {"bound": bound, "kernel": f"awsrc_encode_modules over the {len(wl.modules)} module(s) of a step "
                                       "(basis, factors, screen, fp64 re-score)",
             "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
             "traffic": measured_traffic("encode", wl.name) if gen_version == 1 else None,

@@ -198,6 +198,28 @@ awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_
                                 void* workspace, size_t* ws_bytes, void* stream);
 
 /*
+ * awsrc_encode_tiles over n_modules modules in one call, with the outputs of
+ * all modules concatenated in module order (module m's tiles follow those of
+ * modules 0..m-1, as in awsrc_rank_prefix's global tile index).  The results
+ * are those of calling awsrc_encode_tiles once per module.  With per-element
+ * weights, C = 64, P <= 8 and generator version 1 (the Fisher-blended weights
+ * of Sec. 3.3 at the workloads' shapes) every module is screened in one
+ * launch, so that small modules do not leave the GPU idle; otherwise the
+ * modules are encoded one after another.
+ *  W, W0, d     host arrays [n_modules] of device pointers, each module's
+ *               inputs as in awsrc_encode_tiles (16-byte aligned).
+ *  rows, cols   host arrays [n_modules]; cols % C == 0; rows may be 0.
+ *  seed_out .. alpha_or_null
+ *               device arrays over the sum T_total of the modules' tiles.
+ * Workspace: two-phase query; the query needs no input pointers.
+ */
+awsrc_status awsrc_encode_modules(const awsrc_params* p, int32_t n_modules, const void* const* W, int32_t w_dtype,
+                                  const float* const* W0, const float* const* d, int32_t d_mode,
+                                  const int64_t* rows, const int64_t* cols, uint16_t* seed_out, int8_t* code_out,
+                                  uint16_t* scale_out, double* gain_out, float* alpha_or_null, void* workspace,
+                                  size_t* ws_bytes, void* stream);
+
+/*
  * awsrc_encode_tiles without a workspace, for callers that cannot allocate
  * device memory (code under stream capture, serving loops, harnesses that
  * forbid allocation).  Same arguments, outputs and kernels as

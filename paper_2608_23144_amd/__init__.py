@@ -26,7 +26,7 @@ AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_sdq_encode",
             "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
-            "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
+            "awsrc_encode_modules", "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
             "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
@@ -71,6 +71,8 @@ def _load() -> ctypes.CDLL:
         "awsrc_backbone_sdq_dequant": (i32, [vp, vp, vp, vp, vp, i64, i64, i32, vp, vp]),
         "awsrc_encode_tiles": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp,
                                      ctypes.POINTER(sz), vp]),
+        "awsrc_encode_modules": (i32, [pp, i32, ctypes.POINTER(vp), i32, ctypes.POINTER(vp), ctypes.POINTER(vp), i32,
+                                       P64, P64, vp, vp, vp, vp, vp, vp, ctypes.POINTER(sz), vp]),
         "awsrc_encode_tiles_noalloc": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp]),
         "awsrc_encode_noalloc_max_bytes": (u64, []),
         "awsrc_encode_scored": (i32, [vp, ctypes.POINTER(u64), vp]),
@@ -229,6 +231,58 @@ def awsrc_encode_tiles(p: awsrc_params, W: torch.Tensor, W0: torch.Tensor, d: to
                                   d_mode, _ptr(out["seed"]), _ptr(out["codes"]), _ptr(out["scale"]),
                                   _ptr(out["gain"]), _ptr(out.get("alpha")), _ptr(workspace),
                                   ctypes.byref(n), _stream(stream)))
+    out["workspace"] = workspace
+    return out
+
+
+def _ptr_array(ts):
+    return (ctypes.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
+
+
+def encode_modules_workspace_bytes(p: awsrc_params, shapes: Sequence[Tuple[int, int]], w_dtype: int,
+                                   d_mode: int) -> int:
+    n = ctypes.c_size_t(0)
+    rows = _i64arr([s[0] for s in shapes])
+    cols = _i64arr([s[1] for s in shapes])
+    _check(LIB.awsrc_encode_modules(ctypes.byref(p), len(shapes), None, w_dtype, None, None, d_mode, rows, cols,
+                                    None, None, None, None, None, None, ctypes.byref(n), None))
+    return n.value
+
+
+def awsrc_encode_modules(p: awsrc_params, W_list: Sequence[torch.Tensor], W0_list: Sequence[torch.Tensor],
+                         d_list: Sequence[torch.Tensor], want_alpha: bool = False,
+                         out: Optional[Dict[str, torch.Tensor]] = None, workspace: Optional[torch.Tensor] = None,
+                         stream=None) -> Dict[str, torch.Tensor]:
+    """awsrc_encode_tiles over several modules in one call; outputs
+    concatenated in module order."""
+    _dev(*W_list, *W0_list, *d_list)
+    shapes = [tuple(w.shape) for w in W_list]
+    dts = {_dtype_code(w) for w in W_list}
+    if len(dts) != 1:
+        raise TypeError("all W must share one dtype")
+    w_dtype = dts.pop()
+    modes = {AWSRC_D_PER_COL if d.dim() == 1 else AWSRC_D_PER_ELEM for d in d_list}
+    if len(modes) != 1:
+        raise TypeError("all d must be per column or all per element")
+    d_mode = modes.pop()
+    T = sum(r * c // p.C for r, c in shapes)
+    dev = W_list[0].device
+    if out is None:
+        out = {"seed": torch.empty(T, dtype=torch.int16, device=dev),
+               "codes": torch.empty(T, p.P, dtype=torch.int8, device=dev),
+               "scale": torch.empty(T, dtype=torch.int16, device=dev),
+               "gain": torch.empty(T, dtype=torch.float64, device=dev),
+               "alpha": torch.empty(T, p.P, dtype=torch.float32, device=dev) if want_alpha else None}
+    nbytes = encode_modules_workspace_bytes(p, shapes, w_dtype, d_mode)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    n = ctypes.c_size_t(workspace.numel())
+    rows = _i64arr([s[0] for s in shapes])
+    cols = _i64arr([s[1] for s in shapes])
+    _check(LIB.awsrc_encode_modules(ctypes.byref(p), len(shapes), _ptr_array(W_list), w_dtype, _ptr_array(W0_list),
+                                    _ptr_array(d_list), d_mode, rows, cols, _ptr(out["seed"]), _ptr(out["codes"]),
+                                    _ptr(out["scale"]), _ptr(out["gain"]), _ptr(out.get("alpha")), _ptr(workspace),
+                                    ctypes.byref(n), _stream(stream)))
     out["workspace"] = workspace
     return out
 

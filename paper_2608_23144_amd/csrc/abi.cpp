@@ -122,39 +122,39 @@ extern "C" awsrc_status awsrc_backbone_rtn(const void* W, int32_t w_dtype, int64
 }
 
 // ---------------------------------------------------------------- encode
-extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_dtype,
-                                           const float* W0, int64_t rows, int64_t cols, const float* d,
-                                           int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
-                                           uint16_t* scale_out, double* gain_out, float* alpha_or_null,
-                                           void* workspace, size_t* ws_bytes, void* stream) {
-  awsrc_status st = check_params(p);
-  if (st) return st;
-  if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
-  if (w_dtype != AWSRC_DTYPE_F32 && w_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w_dtype %d", w_dtype);
-  if (d_mode != AWSRC_D_PER_COL && d_mode != AWSRC_D_PER_ELEM) return fail(AWSRC_EINVAL, "bad d_mode %d", d_mode);
-  if (rows < 0 || cols < 1 || cols % p->C) return fail(AWSRC_EINVAL, "cols=%lld must be a positive multiple of C=%d", (long long)cols, p->C);
-  if (!encode_supported(p->C, p->P)) return fail(AWSRC_EINVAL, "unsupported (C, P)");
+namespace {
+
+// Workspace of one module on the per-module kernels (every path but the
+// batched per-element one): size only, or carve it and launch.
+size_t module_ws_bytes(const awsrc_params* p, int64_t rows, int64_t cols, int32_t d_mode) {
   const int64_t nb = cols / p->C;
   const int64_t T = rows * nb;
-  if (T > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "too many tiles in one module");
   const int PB = factor_pb(p->C, p->P);
   const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
   const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
   const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
-  const size_t b_frag = screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
+  const size_t b_frag =
+      screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
   const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
-  const size_t b_stats = 256;  // first: the full-score count (awsrc_encode_scored)
-  const size_t need = b_stats + b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
-  if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
-  if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
-  if (T == 0) return AWSRC_OK;
-  if (!W || !W0 || !d || !seed_out || !code_out || !scale_out || !gain_out) return fail(AWSRC_EINVAL, "NULL buffer");
-  if ((reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(W0) | reinterpret_cast<uintptr_t>(d)) & 15)
-    return fail(AWSRC_EINVAL, "W, W0 and d must be 16-byte aligned");
-  char* ws = static_cast<char*>(workspace);
-  ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(ws), 256));
+  return 256 + b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
+}
+
+awsrc_status encode_module(const awsrc_params* p, const void* W, int32_t w_dtype, const float* W0, int64_t rows,
+                           int64_t cols, const float* d, int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                           uint16_t* scale_out, double* gain_out, float* alpha_or_null, char* ws, bool add_scored,
+                           hipStream_t s) {
+  const int64_t nb = cols / p->C;
+  const int64_t T = rows * nb;
+  const int PB = factor_pb(p->C, p->P);
+  const size_t b_basis = align_up(basis_bytes(p->S, p->P), 256);
+  const size_t b_fac = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) : 0;
+  const size_t b_wd = d_mode == AWSRC_D_PER_COL ? align_up((size_t)nb * p->C * 8, 256) : 0;
+  const size_t b_frag =
+      screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
+  const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
+  const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
   EncodeArgs a{};
   a.W = W; a.w_dtype = w_dtype; a.W0 = W0; a.d = d; a.d_mode = d_mode;
   a.rows = rows; a.cols = cols; a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
@@ -162,7 +162,7 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.scale_fmt = p->scale_fmt;
   a.gen_version = p->gen_version;
   a.scored = reinterpret_cast<unsigned long long*>(ws);
-  ws += b_stats;
+  ws += 256;
   a.basis = carve_basis(ws, p->S, p->P);
   ws += b_basis;
   a.colfac = b_fac ? reinterpret_cast<float*>(ws) : nullptr;
@@ -178,13 +178,158 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   a.fused_rescore = screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, nsplit) ? 1 : 0;
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
-  hipStream_t s = (hipStream_t)stream;
-  HIPCHK(launch_scored_init(a, s));
+  HIPCHK(launch_scored_init(a, s, add_scored));
   HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
   if (d_mode == AWSRC_D_PER_COL) HIPCHK(launch_col_factors(a, s));
   HIPCHK(launch_encode_screen(a, s));
   if (!a.fused_rescore) HIPCHK(launch_encode_finalize(a, s));
   return AWSRC_OK;
+}
+
+// Workspace of the batched per-element encoder: count | basis | fragments |
+// shifted columns | module table | top lists of every tile.
+struct PeLayout {
+  size_t basis, frag, colsh, mods, tg, ts, total;
+};
+PeLayout pe_layout(const awsrc_params* p, int n_modules, int64_t T_total) {
+  PeLayout l;
+  l.basis = align_up(basis_bytes(p->S, p->P), 256);
+  l.frag = align_up(mfma_frag_bytes(p->C, p->S), 256);
+  l.colsh = align_up(pe_colsh_bytes(p->S), 256);
+  l.mods = align_up((size_t)n_modules * sizeof(ModEntry), 256);
+  l.tg = align_up((size_t)T_total * kTop * 4, 256);
+  l.ts = align_up((size_t)T_total * kTop * 2, 256);
+  l.total = 256 + l.basis + l.frag + l.colsh + l.mods + l.tg + l.ts + 256;
+  return l;
+}
+
+// The encoder over n modules with outputs concatenated in module order.
+awsrc_status encode_modules(const awsrc_params* p, int32_t n_modules, const void* const* W, int32_t w_dtype,
+                            const float* const* W0, const float* const* d, int32_t d_mode, const int64_t* rows,
+                            const int64_t* cols, uint16_t* seed_out, int8_t* code_out, uint16_t* scale_out,
+                            double* gain_out, float* alpha_or_null, void* workspace, size_t* ws_bytes, void* stream) {
+  awsrc_status st = check_params(p);
+  if (st) return st;
+  if (!ws_bytes) return fail(AWSRC_EINVAL, "ws_bytes is NULL");
+  if (w_dtype != AWSRC_DTYPE_F32 && w_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "bad w_dtype %d", w_dtype);
+  if (d_mode != AWSRC_D_PER_COL && d_mode != AWSRC_D_PER_ELEM) return fail(AWSRC_EINVAL, "bad d_mode %d", d_mode);
+  if (!encode_supported(p->C, p->P)) return fail(AWSRC_EINVAL, "unsupported (C, P)");
+  if (n_modules < 1 || !rows || !cols) return fail(AWSRC_EINVAL, "bad module table");
+  int64_t T_total = 0;
+  for (int m = 0; m < n_modules; ++m) {
+    if (rows[m] < 0 || cols[m] < 1 || cols[m] % p->C)
+      return fail(AWSRC_EINVAL, "module %d: cols=%lld must be a positive multiple of C=%d", m, (long long)cols[m], p->C);
+    const int64_t T = rows[m] * (cols[m] / p->C);
+    if (T > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "too many tiles in module %d", m);
+    T_total += T;
+  }
+  if (T_total > (int64_t)UINT32_MAX) return fail(AWSRC_EINVAL, "more than 2^32 tiles");
+  const bool batched = pe_batched_supported(p->C, p->P, d_mode, p->gen_version);
+  size_t need = 0;
+  if (batched) {
+    need = pe_layout(p, n_modules, T_total).total;
+  } else {
+    for (int m = 0; m < n_modules; ++m) {
+      const size_t b = module_ws_bytes(p, rows[m], cols[m], d_mode);
+      need = b > need ? b : need;
+    }
+  }
+  if (!workspace) { *ws_bytes = need; return AWSRC_OK; }
+  if (*ws_bytes < need) return fail(AWSRC_ENOSPC, "workspace %zu < %zu bytes", *ws_bytes, need);
+  if (T_total == 0) return AWSRC_OK;
+  if (!W || !W0 || !d || !seed_out || !code_out || !scale_out || !gain_out) return fail(AWSRC_EINVAL, "NULL buffer");
+  for (int m = 0; m < n_modules; ++m) {
+    if (rows[m] == 0) continue;
+    if (!W[m] || !W0[m] || !d[m]) return fail(AWSRC_EINVAL, "NULL input of module %d", m);
+    if ((reinterpret_cast<uintptr_t>(W[m]) | reinterpret_cast<uintptr_t>(W0[m]) | reinterpret_cast<uintptr_t>(d[m])) &
+        15)
+      return fail(AWSRC_EINVAL, "W, W0 and d must be 16-byte aligned (module %d)", m);
+  }
+  char* ws = reinterpret_cast<char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
+  hipStream_t s = (hipStream_t)stream;
+  if (!batched) {
+    int64_t t0 = 0;
+    bool first = true;
+    for (int m = 0; m < n_modules; ++m) {
+      const int64_t T = rows[m] * (cols[m] / p->C);
+      if (T == 0) continue;
+      st = encode_module(p, W[m], w_dtype, W0[m], rows[m], cols[m], d[m], d_mode, seed_out + t0,
+                         code_out + t0 * p->P, scale_out + t0, gain_out + t0,
+                         alpha_or_null ? alpha_or_null + t0 * p->P : nullptr, ws, !first, s);
+      if (st) return st;
+      first = false;
+      t0 += T;
+    }
+    return AWSRC_OK;
+  }
+  const PeLayout l = pe_layout(p, n_modules, T_total);
+  EncodeArgs a{};
+  a.w_dtype = w_dtype; a.d_mode = d_mode;
+  a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
+  a.lambda = p->ridge_lambda;
+  a.scale_fmt = p->scale_fmt;
+  a.gen_version = p->gen_version;
+  a.scored = reinterpret_cast<unsigned long long*>(ws);
+  char* q = ws + 256;
+  a.basis = carve_basis(q, p->S, p->P);
+  q += l.basis;
+  a.frag = q;
+  q += l.frag;
+  uint32_t* colsh = reinterpret_cast<uint32_t*>(q);
+  q += l.colsh;
+  ModEntry* mods = reinterpret_cast<ModEntry*>(q);
+  q += l.mods;
+  a.top_gain = reinterpret_cast<float*>(q);
+  q += l.tg;
+  a.top_seed = reinterpret_cast<uint16_t*>(q);
+  a.nsplit = 1;
+  a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
+  a.alpha_out = alpha_or_null;
+  std::vector<ModEntry> tab(n_modules);
+  int64_t t0 = 0, items = 0, fitems = 0;
+  for (int m = 0; m < n_modules; ++m) {
+    const int64_t nb = cols[m] / p->C;
+    ModEntry& e = tab[m];
+    e.W = W[m]; e.W0 = W0[m]; e.d = d[m];
+    e.rows = rows[m]; e.cols = cols[m];
+    e.tile_off = t0; e.item_off = items; e.fitem_off = fitems;
+    t0 += rows[m] * nb;
+    items += (rows[m] + kPeRows - 1) / kPeRows * nb;
+    fitems += (rows[m] + 63) / 64 * nb;
+  }
+  if (items > (int64_t)INT32_MAX || fitems > (int64_t)INT32_MAX) return fail(AWSRC_EINVAL, "too many work items");
+  HIPCHK(launch_mod_table(tab.data(), n_modules, mods, s));
+  HIPCHK(launch_scored_zero(a.scored, s));  // the pruned screen adds its count
+  HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
+  HIPCHK(launch_pe_screen(a, mods, n_modules, items, a.frag, colsh, s));
+  HIPCHK(launch_finalize_pe_modules(a, mods, n_modules, fitems, s));
+  return AWSRC_OK;
+}
+
+}  // namespace
+
+extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W, int32_t w_dtype,
+                                           const float* W0, int64_t rows, int64_t cols, const float* d,
+                                           int32_t d_mode, uint16_t* seed_out, int8_t* code_out,
+                                           uint16_t* scale_out, double* gain_out, float* alpha_or_null,
+                                           void* workspace, size_t* ws_bytes, void* stream) {
+  const void* Wm[1] = {W};
+  const float* W0m[1] = {W0};
+  const float* dm[1] = {d};
+  const int64_t rm[1] = {rows}, cm[1] = {cols};
+  return encode_modules(p, 1, Wm, w_dtype, W0m, dm, d_mode, rm, cm, seed_out, code_out, scale_out, gain_out,
+                        alpha_or_null, workspace, ws_bytes, stream);
+}
+
+extern "C" awsrc_status awsrc_encode_modules(const awsrc_params* p, int32_t n_modules, const void* const* W,
+                                             int32_t w_dtype, const float* const* W0, const float* const* d,
+                                             int32_t d_mode, const int64_t* rows, const int64_t* cols,
+                                             uint16_t* seed_out, int8_t* code_out, uint16_t* scale_out,
+                                             double* gain_out, float* alpha_or_null, void* workspace,
+                                             size_t* ws_bytes, void* stream) {
+  if (n_modules >= 1 && (!W || !W0 || !d) && workspace) return fail(AWSRC_EINVAL, "NULL module pointer array");
+  return encode_modules(p, n_modules, W, w_dtype, W0, d, d_mode, rows, cols, seed_out, code_out, scale_out, gain_out,
+                        alpha_or_null, workspace, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------- encode, no allocation

@@ -212,12 +212,61 @@ struct EncodeArgs {
   float* alpha_out;
 };
 
+// One module of a batched encode: its inputs, shape, the global index of its
+// first tile (outputs are concatenated in module order) and the first work
+// item of the screen (32-row groups x column blocks) and of the re-score
+// (64-row groups x column blocks) that belongs to it.
+struct ModEntry {
+  const void* W;
+  const float* W0;
+  const float* d;
+  int64_t rows, cols;
+  int64_t tile_off;
+  int64_t item_off;
+  int64_t fitem_off;
+};
+static_assert(sizeof(ModEntry) == 64, "module table entries are 64 bytes");
+
+// The module holding work item `item`: the last m with (fin ? fitem_off :
+// item_off) <= item (modules without work items share their successor's
+// offset and are skipped).  Wavefront-uniform.
+__device__ __forceinline__ int find_module(const ModEntry* mods, int n, int64_t item, bool fin) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    const int64_t o = fin ? mods[mid].fitem_off : mods[mid].item_off;
+    if (o <= item) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Module tables are written on the device from chunks passed by value (no
+// host copy, so the encoder stays asynchronous).
+constexpr int kModChunk = 48;
+struct ModChunk {
+  ModEntry e[kModChunk];
+};
+hipError_t launch_mod_table(const ModEntry* host, int n, ModEntry* dev, hipStream_t st);
+
+// The batched per-element encoder (C = 64, P <= 8, generator version 1): the
+// pruned screen over every module's 32-row groups, then the fp64 re-score.
+constexpr int kPeRows = 32;
+bool pe_batched_supported(int C, int P, int d_mode, int gen_version);
+size_t pe_colsh_bytes(int S);
+hipError_t launch_pe_screen(const EncodeArgs& a, const ModEntry* mods, int n_mods, int64_t items, const void* frag,
+                            uint32_t* colsh, hipStream_t st);
+hipError_t launch_finalize_pe_modules(const EncodeArgs& a, const ModEntry* mods, int n_mods, int64_t items,
+                                      hipStream_t st);
+
 bool encode_supported(int C, int P);
 // the matrix-core screens: C = 64 (P <= 8), C = 128 (P <= 8, per-column
 // weights); per-element weights need generator version 1 (XOR Gram gathers)
 bool screen_mfma_supported(int C, int P, int d_mode, int gen_version);
 int factor_pb(int C, int P);                 // padded P of the per-column factor table
 size_t mfma_frag_bytes(int C, int S);
+// +-1 bf16 basis fragments of the matrix-core screens, per seed pair and K step
+hipError_t launch_mfma_frags(const BasisTables& bt, int C, int P, int S, void* frag, hipStream_t st);
 // Seed ranges per tile for the screen (1 unless the matrix-core screen runs).
 int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode, int gen_version);
 hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st);
@@ -227,7 +276,10 @@ hipError_t launch_encode_finalize(const EncodeArgs& a, hipStream_t st);
 // Sets *a.scored to the count of candidates the screen will score in full
 // without the pruned screen's help: 0 when it runs (it adds its own), else
 // every candidate.
-hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st);
+// With `add`, the count is added to the one already there (a batch of
+// modules encoded one by one).
+hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st, bool add = false);
+hipError_t launch_scored_zero(unsigned long long* p, hipStream_t st);
 bool screen_pruned(int C, int P, int d_mode, int gen_version);
 // Whether the pruned screen runs the fp64 re-score itself (one seed range per
 // tile, generator version 1).

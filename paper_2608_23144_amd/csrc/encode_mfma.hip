@@ -27,41 +27,16 @@
 #include <math.h>
 
 #include "awsrc_internal.h"
+#include "mfma_bf16.h"
 #include "rescore64.h"
 
 namespace awsrc {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
 __device__ __forceinline__ float load_w_any2(const void* W, int dt, int64_t i) {
   if (dt == AWSRC_DTYPE_F32) return static_cast<const float*>(W)[i];
   return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-// Exact three-way bf16 split of eight fp32 values, packed two per dword.
-__device__ __forceinline__ void split3(const float (&u)[8], u32x4& hi, u32x4& mid, u32x4& lo) {
-  uint32_t h[8], m[8], l[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const uint32_t ub = __float_as_uint(u[e]);
-    h[e] = ub & 0xFFFF0000u;
-    const float r1 = u[e] - __uint_as_float(h[e]);
-    m[e] = __float_as_uint(r1) & 0xFFFF0000u;
-    const float r2 = r1 - __uint_as_float(m[e]);
-    l[e] = __float_as_uint(r2) & 0xFFFF0000u;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    hi[i] = (h[2 * i] >> 16) | h[2 * i + 1];
-    mid[i] = (m[2 * i] >> 16) | m[2 * i + 1];
-    lo[i] = (l[2 * i] >> 16) | l[2 * i + 1];
-  }
 }
 
 }  // namespace
@@ -796,14 +771,19 @@ bool screen_fuses_rescore(int C, int P, int d_mode, int gen_version, int nsplit)
   return screen_pruned(C, P, d_mode, gen_version) && gen_version == 1 && nsplit == 1;
 }
 
-__global__ void k_scored_init(unsigned long long* p, unsigned long long v) {
-  if (threadIdx.x == 0) *p = v;
+__global__ void k_scored_init(unsigned long long* p, unsigned long long v, int add) {
+  if (threadIdx.x == 0) *p = (add ? *p : 0ull) + v;
 }
 
-hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st) {
+hipError_t launch_scored_zero(unsigned long long* p, hipStream_t st) {
+  hipLaunchKernelGGL(k_scored_init, dim3(1), dim3(64), 0, st, p, 0ull, 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_scored_init(const EncodeArgs& a, hipStream_t st, bool add) {
   const unsigned long long all = (unsigned long long)(a.rows * (a.cols / a.C)) * (unsigned long long)a.S;
   hipLaunchKernelGGL(k_scored_init, dim3(1), dim3(64), 0, st, a.scored,
-                     screen_pruned(a.C, a.P, a.d_mode, a.gen_version) ? 0ull : all);
+                     screen_pruned(a.C, a.P, a.d_mode, a.gen_version) ? 0ull : all, add ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -831,10 +811,16 @@ static hipError_t screen_mfma_fmt(const EncodeArgs& a, void* frag, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
-  const int64_t n = (int64_t)((a.S + 1) / 2 + 2) * (a.C / 32) * 64;
-  hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.basis, a.C, a.P, a.S,
+hipError_t launch_mfma_frags(const BasisTables& bt, int C, int P, int S, void* frag, hipStream_t st) {
+  const int64_t n = (int64_t)((S + 1) / 2 + 2) * (C / 32) * 64;
+  hipLaunchKernelGGL(k_mfma_frags, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, bt, C, P, S,
                      static_cast<u32x4*>(frag));
+  return hipGetLastError();
+}
+
+hipError_t launch_encode_screen_mfma(const EncodeArgs& a, void* frag, hipStream_t st) {
+  const hipError_t e = launch_mfma_frags(a.basis, a.C, a.P, a.S, frag, st);
+  if (e != hipSuccess) return e;
   if (a.scale_fmt == AWSRC_SCALE_POW2) return screen_mfma_fmt<true>(a, frag, st);
   return screen_mfma_fmt<false>(a, frag, st);
 }

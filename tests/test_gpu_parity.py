@@ -236,12 +236,13 @@ def test_encode_zero_residual_tiles():
 
 
 def test_encode_scored_count():
-    """awsrc_encode_scored: the pruned screen (per-column weights, C = 64)
-    scores every tile's first pair of seeds and, on realistic data, a small
-    part of the rest; the per-element screen scores every candidate.  The
-    module has enough row groups that each wavefront searches all S seeds
-    (with seed ranges split over wavefronts, each range starts its pruning
-    afresh)."""
+    """awsrc_encode_scored: the pruned screens (C = 64, per-column and
+    per-element weights) score every tile's first seeds and, on realistic
+    data, a small part of the rest.  The per-column module has enough row
+    groups that each wavefront searches all S seeds (with seed ranges split
+    over wavefronts, each range starts its pruning afresh); the per-element
+    screen always searches all seeds per wavefront, and each lane queues up
+    to four survivors before the first scoring round."""
     wl = WORKLOADS["down3b"]
     m = Module("scored", 2048, 4096, 0, 1, 1)
     inp, bb, enc = _gpu_module(wl, m)
@@ -251,9 +252,12 @@ def test_encode_scored_count():
     idx = np.arange(0, T, 997)
     assert _check_encode_sample(wl, m, inp, bb[3], enc, idx) <= 1
     wl2 = WORKLOADS["block3b"]
-    m2 = Module("scored_pe", 64, 256, 0, 1, 1)
-    _, _, enc2 = _gpu_module(wl2, m2)
-    assert awsrc.awsrc_encode_scored(enc2) == (64 * 256 // wl2.C) * wl2.S
+    m2 = Module("scored_pe", 256, 2048, 0, 1, 1)
+    inp2, bb2, enc2 = _gpu_module(wl2, m2)
+    T2 = m2.rows * m2.cols // wl2.C
+    sc2 = awsrc.awsrc_encode_scored(enc2)
+    assert 4 * T2 <= sc2 < T2 * wl2.S // 8, (sc2, T2 * wl2.S)
+    assert _check_encode_sample(wl2, m2, inp2, bb2[3], enc2, np.arange(0, T2, 331)) <= 1
 
 
 # ------------------------------------------------------------------ SDQ backbone
@@ -799,3 +803,39 @@ def test_reconstruct_bf16_down3b_pipeline():
     W0s = [O.rtn_dequant(*bb, 128)]
     assert np.array_equal(W0s[0], W0.cpu().numpy())
     _check_reconstruct(wl.C, stream, K, W0s, want, [out], [(m.rows, m.cols)])
+
+
+# ------------------------------------------------------------------ batched encode
+@pytest.mark.parametrize("name", ["block3b", "down3b"])
+def test_encode_modules_matches_per_module_calls_and_oracle(name):
+    """awsrc_encode_modules over modules of different shapes (one of them
+    empty, one a single row) gives, in module order, exactly what one
+    awsrc_encode_tiles call per module gives, and every tile agrees with the
+    oracle (per-element weights: one batched launch; per-column weights:
+    the modules one after another)."""
+    wl = workload(name, S=40)
+    mods = [Module("a", 70, 512, 0, 1, 1), Module("empty", 0, 256, 0, 2, 2), Module("c", 33, 1024, 0, 3, 3),
+            Module("row", 1, 128, 0, 4, 4)]
+    p = _params(wl)
+    inps, W0s = [], []
+    for m in mods:
+        inp = gen_module_inputs(wl, m, DEV)
+        W0s.append(awsrc.awsrc_backbone_rtn(inp["W"])[3] if m.rows else
+                   torch.empty(0, m.cols, dtype=torch.float32, device=DEV))
+        inps.append(inp)
+    got = awsrc.awsrc_encode_modules(p, [i["W"] for i in inps], W0s, [i["d"] for i in inps], want_alpha=True)
+    torch.cuda.synchronize()
+    off = 0
+    for m, inp, W0 in zip(mods, inps, W0s):
+        T = m.rows * m.cols // wl.C
+        if T == 0:
+            continue
+        ref = awsrc.awsrc_encode_tiles(p, inp["W"], W0, inp["d"], want_alpha=True)
+        torch.cuda.synchronize()
+        for k in ("seed", "codes", "scale", "alpha"):
+            assert torch.equal(got[k][off:off + T], ref[k]), (m.name, k)
+        assert torch.equal(got["gain"][off:off + T].view(torch.int64), ref["gain"].view(torch.int64)), m.name
+        sl = {k: (v[off:off + T] if v is not None and k != "workspace" else v) for k, v in got.items()}
+        _check_encode_sample(wl, m, inp, W0, sl, np.arange(T))
+        off += T
+    assert off == got["seed"].numel()
