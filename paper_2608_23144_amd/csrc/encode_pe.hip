@@ -97,24 +97,27 @@ __device__ __forceinline__ void project32(const u32x4& F0, const u32x4& F1, cons
 // the gathers G_pq = wdl at byte offset cs[p] ^ cs[q] ^ tl4 (cs[p] = c_p << 7)
 // and the diagonal d0 = mean_j d_j.  Padded columns (p >= P) get L = 0,
 // e = 1.
-template <int PB>
+// FULLP: P == PB, so that no column is padding (the P = 8 workloads).
+template <int PB, bool FULLP>
 __device__ __forceinline__ void factor_pe(const float* wdl, const uint32_t (&cs)[PB], uint32_t tl4, float d0,
                                           float eps, int P, float (&f)[PB * (PB - 1) / 2 + 2 * PB]) {
   constexpr int LS = PB * (PB - 1) / 2;
   const char* wb = reinterpret_cast<const char*>(wdl);
+  const float diag = d0 + eps;
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
+    const bool real = FULLP || p < P;
     float E[PB];
 #pragma unroll
     for (int q = 0; q < p; ++q) {
       const float gpq = *reinterpret_cast<const float*>(wb + (cs[p] ^ cs[q] ^ tl4));
-      float t = (p < P) ? gpq : 0.0f;
+      float t = real ? gpq : 0.0f;
 #pragma unroll
       for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
       E[q] = t;
       f[ltri(p, q)] = t * f[LS + q];
     }
-    float t = (p < P) ? d0 + eps : 1.0f;
+    float t = real ? diag : 1.0f;
 #pragma unroll
     for (int kk = 0; kk < p; ++kk) t = fmaf(-E[kk], f[ltri(p, kk)], t);
     t = fmaxf(t, 1e-30f);
@@ -141,7 +144,7 @@ __global__ void k_pe_colsh(BasisTables bt, int P, int S, int n_rows, uint32_t* _
   colsh[i] = (s < S && p < P) ? ((uint32_t)bt.col[(size_t)s * kMaxP + p] << 7) : 0u;
 }
 
-template <bool POW2>
+template <bool POW2, bool FULLP>
 __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEntry* __restrict__ mods, int n_mods,
                                                        const u32x4* __restrict__ frag,
                                                        const u32x4* __restrict__ colsh) {
@@ -216,7 +219,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       uint32_t cs[PB];
       unpack_cols<PB>(colsh[2 * (size_t)s], colsh[2 * (size_t)s + 1], cs);
       float f[NF];
-      factor_pe<PB>(wdl, cs, tl4, d0, eps, P, f);
+      factor_pe<PB, FULLP>(wdl, cs, tl4, d0, eps, P, f);
       const float gsc = screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax);
       const bool c0 = gsc > tg0, c1 = gsc > tg1;
       tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
@@ -239,11 +242,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   // so the loads two pairs ahead need no bounds).
   const int n_pairs = (a.S + 1) / 2;
   const u32x4* fp = frag + lane;
-  f32x4 acc[2];
-  project32(fp[0], fp[64], uh, um, ul, acc);
-  u32x4 F0 = fp[128], F1 = fp[192];
-  u32x4 C0 = colsh[2 * (size_t)sh], C1 = colsh[2 * (size_t)sh + 1];
-  for (int pair = 0; pair < n_pairs; ++pair) {
+  // two register sets for the projections, fragments and columns, swapping
+  // roles every pair (the loop runs two pairs per trip, so no copies)
+  f32x4 accA[2], accB[2];
+  project32(fp[0], fp[64], uh, um, ul, accA);
+  u32x4 FA0 = fp[128], FA1 = fp[192], FB0, FB1;
+  u32x4 CA0 = colsh[2 * (size_t)sh], CA1 = colsh[2 * (size_t)sh + 1], CB0, CB1;
+  auto step = [&](int pair, const f32x4 (&acc)[2], f32x4 (&accN)[2], const u32x4& F0, const u32x4& F1, u32x4& F0n,
+                  u32x4& F1n, const u32x4& C0, const u32x4& C1, u32x4& C0n, u32x4& C1n) {
     const int s = 2 * pair + sh;
     // this lane's candidate: tile tl, seed s
     float bt[PB];
@@ -257,13 +263,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     uint32_t cs[PB];
     unpack_cols<PB>(C0, C1, cs);
     // next pair's projections and columns, and the fragments two pairs ahead
-    project32(F0, F1, uh, um, ul, acc);
-    F0 = fp[(size_t)(pair + 2) * 128];
-    F1 = fp[(size_t)(pair + 2) * 128 + 64];
-    C0 = colsh[2 * (size_t)(s + 2)];
-    C1 = colsh[2 * (size_t)(s + 2) + 1];
+    project32(F0, F1, uh, um, ul, accN);
+    F0n = fp[(size_t)(pair + 2) * 128];
+    F1n = fp[(size_t)(pair + 2) * 128 + 64];
+    C0n = colsh[2 * (size_t)(s + 2)];
+    C1n = colsh[2 * (size_t)(s + 2) + 1];
     float f[NF];
-    factor_pe<PB>(wdl, cs, tl4, d0, eps, P, f);
+    factor_pe<PB, FULLP>(wdl, cs, tl4, d0, eps, P, f);
     float wv[PB];
     const float bnd = screen_fwd<PB>(bt, f, wv);
     const bool keep = (int)(bnd * kSlack > thr) & (int)valid & (int)(s < a.S);
@@ -287,7 +293,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       } while (__ballot(qlen == QD) != 0);
       update_thr();
     }
+  };
+  int pair = 0;
+  for (; pair + 1 < n_pairs; pair += 2) {
+    step(pair, accA, accB, FA0, FA1, FB0, FB1, CA0, CA1, CB0, CB1);
+    step(pair + 1, accB, accA, FB0, FB1, FA0, FA1, CB0, CB1, CA0, CA1);
   }
+  if (pair < n_pairs) step(pair, accA, accB, FA0, FA1, FB0, FB1, CA0, CA1, CB0, CB1);
   while (__ballot(qlen > 0) != 0) score_round();
 #pragma unroll
   for (int k = 32; k >= 1; k >>= 1) nscored += __shfl_xor(nscored, k, 64);
@@ -351,10 +363,14 @@ hipError_t launch_pe_screen(const EncodeArgs& a, const ModEntry* mods, int n_mod
   if (items == 0) return hipGetLastError();
   const u32x4* fr = static_cast<const u32x4*>(frag);
   const u32x4* cw = reinterpret_cast<const u32x4*>(colsh);
-  if (a.scale_fmt == AWSRC_SCALE_POW2)
-    hipLaunchKernelGGL((k_screen_pe32<true>), dim3((unsigned)items), dim3(64), 0, st, a, mods, n_mods, fr, cw);
-  else
-    hipLaunchKernelGGL((k_screen_pe32<false>), dim3((unsigned)items), dim3(64), 0, st, a, mods, n_mods, fr, cw);
+  const dim3 grid((unsigned)items), blk(64);
+  if (a.scale_fmt == AWSRC_SCALE_POW2) {
+    if (a.P == kPB) hipLaunchKernelGGL((k_screen_pe32<true, true>), grid, blk, 0, st, a, mods, n_mods, fr, cw);
+    else hipLaunchKernelGGL((k_screen_pe32<true, false>), grid, blk, 0, st, a, mods, n_mods, fr, cw);
+  } else {
+    if (a.P == kPB) hipLaunchKernelGGL((k_screen_pe32<false, true>), grid, blk, 0, st, a, mods, n_mods, fr, cw);
+    else hipLaunchKernelGGL((k_screen_pe32<false, false>), grid, blk, 0, st, a, mods, n_mods, fr, cw);
+  }
   return hipGetLastError();
 }
 
