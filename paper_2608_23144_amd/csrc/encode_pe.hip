@@ -92,17 +92,27 @@ __device__ __forceinline__ void project32(const u32x4& F0, const u32x4& F1, cons
   }
 }
 
+// The Gram gathers of one candidate: G_pq (q < p) = wdl at byte offset
+// cs[p] ^ cs[q] ^ tl4 (cs[p] = c_p << 7), packed like the strict lower factor.
+template <int PB>
+__device__ __forceinline__ void gather_pe(const float* wdl, const uint32_t (&cs)[PB], uint32_t tl4,
+                                          float (&gq)[PB * (PB - 1) / 2]) {
+  const char* wb = reinterpret_cast<const char*>(wdl);
+#pragma unroll
+  for (int p = 1; p < PB; ++p)
+#pragma unroll
+    for (int q = 0; q < p; ++q) gq[ltri(p, q)] = *reinterpret_cast<const float*>(wb + (cs[p] ^ cs[q] ^ tl4));
+}
+
 // G + eps I = L diag(e) L^T of one candidate, in the layout of the
 // per-column factor table (strict lower L by rows, then 1/e, then e), from
-// the gathers G_pq = wdl at byte offset cs[p] ^ cs[q] ^ tl4 (cs[p] = c_p << 7)
-// and the diagonal d0 = mean_j d_j.  Padded columns (p >= P) get L = 0,
-// e = 1.
-// FULLP: P == PB, so that no column is padding (the P = 8 workloads).
+// its gathers gq and the diagonal d0 = mean_j d_j.  Padded columns (p >= P)
+// get L = 0, e = 1; FULLP: P == PB, so that no column is padding (the P = 8
+// workloads).
 template <int PB, bool FULLP>
-__device__ __forceinline__ void factor_pe(const float* wdl, const uint32_t (&cs)[PB], uint32_t tl4, float d0,
-                                          float eps, int P, float (&f)[PB * (PB - 1) / 2 + 2 * PB]) {
+__device__ __forceinline__ void factor_pe(const float (&gq)[PB * (PB - 1) / 2], float d0, float eps, int P,
+                                          float (&f)[PB * (PB - 1) / 2 + 2 * PB]) {
   constexpr int LS = PB * (PB - 1) / 2;
-  const char* wb = reinterpret_cast<const char*>(wdl);
   const float diag = d0 + eps;
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
@@ -110,8 +120,7 @@ __device__ __forceinline__ void factor_pe(const float* wdl, const uint32_t (&cs)
     float E[PB];
 #pragma unroll
     for (int q = 0; q < p; ++q) {
-      const float gpq = *reinterpret_cast<const float*>(wb + (cs[p] ^ cs[q] ^ tl4));
-      float t = real ? gpq : 0.0f;
+      float t = real ? gq[ltri(p, q)] : 0.0f;
 #pragma unroll
       for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
       E[q] = t;
@@ -150,7 +159,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
                                                        const u32x4* __restrict__ colsh) {
   constexpr int C = kC, PB = kPB, NT = kNT;
   constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
-  constexpr int QD = 4;       // queue slots per lane (a power of two)
+  constexpr int NL = PB * (PB - 1) / 2;
+  constexpr int QD = 2;       // queue slots per lane (a power of two): 12.6 KB of LDS, three wavefronts per SIMD
   constexpr int QW = PB + 1;  // words per entry: w, then the seed
   constexpr float kSlack = 1.001953125f;
   __shared__ float wdl[C * NT];            // WHT(d_t) / C, [coordinate][tile]
@@ -218,8 +228,9 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       const int s = __float_as_int(e[PB * 64]);
       uint32_t cs[PB];
       unpack_cols<PB>(colsh[2 * (size_t)s], colsh[2 * (size_t)s + 1], cs);
-      float f[NF];
-      factor_pe<PB, FULLP>(wdl, cs, tl4, d0, eps, P, f);
+      float gr[NL], f[NF];
+      gather_pe<PB>(wdl, cs, tl4, gr);
+      factor_pe<PB, FULLP>(gr, d0, eps, P, f);
       const float gsc = screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax);
       const bool c0 = gsc > tg0, c1 = gsc > tg1;
       tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
@@ -251,7 +262,12 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   auto step = [&](int pair, const f32x4 (&acc)[2], f32x4 (&accN)[2], const u32x4& F0, const u32x4& F1, u32x4& F0n,
                   u32x4& F1n, const u32x4& C0, const u32x4& C1, u32x4& C0n, u32x4& C1n) {
     const int s = 2 * pair + sh;
-    // this lane's candidate: tile tl, seed s
+    // this lane's candidate: tile tl, seed s; its Gram gathers are issued
+    // first, so that their latency overlaps the rest
+    uint32_t cs[PB];
+    unpack_cols<PB>(C0, C1, cs);
+    float gq[NL];
+    gather_pe<PB>(wdl, cs, tl4, gq);
     float bt[PB];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -260,8 +276,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       bt[i] = __uint_as_float(r[0]);
       bt[4 + i] = __uint_as_float(r[1]);
     }
-    uint32_t cs[PB];
-    unpack_cols<PB>(C0, C1, cs);
     // next pair's projections and columns, and the fragments two pairs ahead
     project32(F0, F1, uh, um, ul, accN);
     F0n = fp[(size_t)(pair + 2) * 128];
@@ -269,7 +283,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     C0n = colsh[2 * (size_t)(s + 2)];
     C1n = colsh[2 * (size_t)(s + 2) + 1];
     float f[NF];
-    factor_pe<PB, FULLP>(wdl, cs, tl4, d0, eps, P, f);
+    factor_pe<PB, FULLP>(gq, d0, eps, P, f);
     float wv[PB];
     const float bnd = screen_fwd<PB>(bt, f, wv);
     const bool keep = (int)(bnd * kSlack > thr) & (int)valid & (int)(s < a.S);
