@@ -18,22 +18,25 @@
 //     l % 32, seed 2 pair + l / 32;
 //   * G_pq = WHT(d_t)[c_p xor c_q] / C (the Sylvester XOR identity) is
 //     gathered from a per-tile transform in LDS, laid out [coordinate][tile]
-//     so that a lane's gather address is (c_p << 7) ^ (c_q << 7) ^ 4 tile
-//     (one v_xor3 from a per-seed table of shifted columns), and the 32
-//     lanes of each seed read 32 distinct banks;
+//     so that a lane's gather address is the XOR of c_p << 7, c_q << 7 (a
+//     per-seed table of shifted columns) and 4 tile, and the 32 lanes of
+//     each seed read 32 distinct banks;
 //   * every candidate gets the LDL^T factor and the forward solve, whose
 //     sum_k w_k^2 / e_k = b^T (G + eps I)^-1 b bounds the score of every
 //     rounding of the fit (the score is a concave quadratic in the
-//     coefficients with that maximum); only candidates whose bound clears
-//     the tile's current second score are scored in full.  Those are few
-//     (a few percent), so each lane queues them (w and the seed) in its own
-//     LDS ring, and a scoring round refactors and scores the oldest entry of
-//     every lane that has one, whenever some lane's ring is full;
-//   * each tile's even and odd seeds live in lanes l and l ^ 32: their
-//     lists share the pruning threshold (the second score over both, by a
+//     coefficients with that maximum); only candidates whose bound reaches
+//     the re-score's window below the tile's current best are scored in
+//     full (the re-score looks at a second seed only inside that window, and
+//     its lower edge only rises).  Those are few (a few percent), so each
+//     lane queues them (w and the seed) in its own LDS ring, and a scoring
+//     round refactors and scores the oldest entry of every lane that has
+//     one, whenever some lane's ring is full;
+//   * each tile's even and odd seeds live in lanes l and l ^ 32: their lists
+//     share the pruning threshold (from the best over both, by a
 //     v_permlane32_swap after each round) and are merged at the end.  A
 //     lane's entries are scored in seed order and thresholds only rise, so
-//     the merged top two are those of scoring every candidate.
+//     the merged top two agree with those of scoring every candidate in the
+//     best and in the second wherever the second is inside the window.
 //
 // The kept lists go to the fp64 re-score (k_finalize_pe_modules).
 #include <math.h>
@@ -179,6 +182,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   const uint32_t tl4 = 4u * (uint32_t)tl;
   const int64_t my_row = row0 + tl;
   const bool valid = my_row < md.rows;
+  float energy;
   {
     // WHT of the tile's weights; lanes tl and tl + 32 both transform it and
     // each stores one half
@@ -191,6 +195,22 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
 #pragma unroll
       for (int k = 0; k < 8; ++k) wd[j0 + k] = v[k];
     }
+    // this lane's half of the tile's weighted energy sum_j d_j r_j^2 (for
+    // the pruning window below)
+    float eh = 0.0f;
+#pragma unroll
+    for (int j0 = 0; j0 < C / 2; j0 += 8) {
+      float w[8], w0[8];
+      load8_w(md.W, a.w_dtype, off + 32 * sh + j0, w);
+      load8_f(md.W0 + off + 32 * sh + j0, w0);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float r = w[k] - w0[k];
+        eh = fmaf((sh ? wd[32 + j0 + k] : wd[j0 + k]) * r, r, eh);
+      }
+    }
+    const auto re = __builtin_amdgcn_permlane32_swap(__float_as_uint(eh), __float_as_uint(eh), false, false);
+    energy = eh + __uint_as_float(sh ? re[0] : re[1]);
     fwht<C>(wd);
 #pragma unroll
     for (int j = 0; j < C / 2; ++j) wdl[(j + 32 * sh) * NT + tl] = (sh ? wd[j + 32] : wd[j]) * (1.0f / C);
@@ -211,11 +231,18 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   float tg0 = -INFINITY, tg1 = -INFINITY;
   int ts0 = 0, ts1 = 0;
   float thr = -INFINITY;
+  // The re-score takes a tile's second seed only when its screened score lies
+  // within 1e-4 |best| + 1e-7 energy of the best, so a candidate below that
+  // window of the tile's current best (over both lanes' lists) can never be
+  // needed: the window's lower edge only rises with the best.  The
+  // threshold carries a margin (1.005e-4, 1.05e-7) over the re-score's
+  // window, far above the fp32 rounding of either; in raw units the energy
+  // term is 64 times larger.
+  const float e_win = 64.0f * 1.05e-7f * energy;
   auto update_thr = [&]() {
     const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg0), __float_as_uint(tg0), false, false);
-    const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg1), __float_as_uint(tg1), false, false);
-    const float o0 = __uint_as_float(sh ? r0[0] : r0[1]), o1 = __uint_as_float(sh ? r1[0] : r1[1]);
-    thr = fmaxf(fminf(tg0, o0), fmaxf(tg1, o1));
+    const float best = fmaxf(tg0, __uint_as_float(sh ? r0[0] : r0[1]));
+    thr = best - (1.005e-4f * fabsf(best) + e_win);
   };
   int qhead = 0, qtail = 0, qlen = 0;
   int nscored = 0;
