@@ -220,6 +220,29 @@ awsrc_status awsrc_encode_modules(const awsrc_params* p, int32_t n_modules, cons
                                   size_t* ws_bytes, void* stream);
 
 /*
+ * Diagnostic of the encoder's fp32 screen: copies the screened lists that the
+ * last awsrc_encode_modules / awsrc_encode_tiles call with this workspace
+ * (and the same p, module shapes and d_mode) kept for the fp64 re-score.
+ * Per tile and seed range, kTop = 2 entries (gain in fp32, seed word), the
+ * best first: gain_out and seed_out are device arrays [T_total][*nsplit][2];
+ * with both NULL only *nsplit (seed ranges per tile) is returned.  A seed
+ * word holds the seed in bits 0-15 and, in bit 16, a flag set when the
+ * screen's fp32 rounding decisions for that candidate (the scale, a code)
+ * lay within a small tolerance of a rounding threshold, where its score may
+ * differ from the fp64 one by more than usual.  The re-score (Sec. 3.2)
+ * re-evaluates the second entry in fp64 when its screened gain lies within
+ * 1e-4 |g| + 1e-7 sum_j d_j r_j^2 of the first (3e-2 |g| + 3e-5 sum_j d_j
+ * r_j^2 if either entry is flagged), so comparing the lists with gain_out of
+ * the encode call measures the screen's error against that window.
+ * Asynchronous on `stream`.  EINVAL where the call kept no
+ * lists in the workspace: the per-column screen that runs the re-score
+ * itself (C = 64, one seed range), or several modules encoded one by one.
+ */
+awsrc_status awsrc_encode_screen_lists(const awsrc_params* p, int32_t n_modules, const int64_t* rows,
+                                       const int64_t* cols, int32_t d_mode, const void* workspace, float* gain_out,
+                                       uint32_t* seed_out, int32_t* nsplit, void* stream);
+
+/*
  * awsrc_encode_tiles without a workspace, for callers that cannot allocate
  * device memory (code under stream capture, serving loops, harnesses that
  * forbid allocation).  Same arguments, outputs and kernels as

@@ -26,7 +26,7 @@ AWSRC_SCALE_FP16, AWSRC_SCALE_POW2 = 0, 1
 
 EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsrc_sdq_encode",
             "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
-            "awsrc_encode_modules", "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
+            "awsrc_encode_modules", "awsrc_encode_screen_lists", "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
             "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
@@ -73,6 +73,7 @@ def _load() -> ctypes.CDLL:
                                      ctypes.POINTER(sz), vp]),
         "awsrc_encode_modules": (i32, [pp, i32, ctypes.POINTER(vp), i32, ctypes.POINTER(vp), ctypes.POINTER(vp), i32,
                                        P64, P64, vp, vp, vp, vp, vp, vp, ctypes.POINTER(sz), vp]),
+        "awsrc_encode_screen_lists": (i32, [pp, i32, P64, P64, i32, vp, vp, vp, ctypes.POINTER(i32), vp]),
         "awsrc_encode_tiles_noalloc": (i32, [pp, vp, i32, vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp]),
         "awsrc_encode_noalloc_max_bytes": (u64, []),
         "awsrc_encode_scored": (i32, [vp, ctypes.POINTER(u64), vp]),
@@ -285,6 +286,24 @@ def awsrc_encode_modules(p: awsrc_params, W_list: Sequence[torch.Tensor], W0_lis
                                     ctypes.byref(n), _stream(stream)))
     out["workspace"] = workspace
     return out
+
+
+def awsrc_encode_screen_lists(p: awsrc_params, shapes: Sequence[Tuple[int, int]], d_mode: int,
+                              workspace: torch.Tensor, stream=None):
+    """The fp32 screen's kept lists of the last encode with this workspace:
+    (gain f32 [T, nsplit, 2], seed word int32 [T, nsplit, 2]: seed in bits
+    0-15, bit 16 set for a candidate whose rounding was on a knife edge)."""
+    rows = _i64arr([s[0] for s in shapes])
+    cols = _i64arr([s[1] for s in shapes])
+    ns = ctypes.c_int32(0)
+    _check(LIB.awsrc_encode_screen_lists(ctypes.byref(p), len(shapes), rows, cols, d_mode, _ptr(workspace), None,
+                                         None, ctypes.byref(ns), _stream(stream)))
+    T = sum(r * c // p.C for r, c in shapes)
+    g = torch.empty(T, ns.value, 2, dtype=torch.float32, device=workspace.device)
+    sd = torch.empty(T, ns.value, 2, dtype=torch.int32, device=workspace.device)
+    _check(LIB.awsrc_encode_screen_lists(ctypes.byref(p), len(shapes), rows, cols, d_mode, _ptr(workspace), _ptr(g),
+                                         _ptr(sd), ctypes.byref(ns), _stream(stream)))
+    return g, sd
 
 
 def awsrc_encode_noalloc_max_bytes() -> int:

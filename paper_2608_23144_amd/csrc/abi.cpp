@@ -137,7 +137,7 @@ size_t module_ws_bytes(const awsrc_params* p, int64_t rows, int64_t cols, int32_
       screen_mfma_supported(p->C, p->P, d_mode, p->gen_version) ? align_up(mfma_frag_bytes(p->C, p->S), 256) : 0;
   const int nsplit = screen_nsplit(p->C, p->P, p->S, rows, cols, d_mode, p->gen_version);
   const size_t b_tg = align_up((size_t)T * nsplit * kTop * 4, 256);
-  const size_t b_ts = align_up((size_t)T * nsplit * kTop * 2, 256);
+  const size_t b_ts = align_up((size_t)T * nsplit * kTop * 4, 256);
   return 256 + b_basis + b_fac + b_wd + b_frag + b_tg + b_ts + 256;
 }
 
@@ -173,7 +173,7 @@ awsrc_status encode_module(const awsrc_params* p, const void* W, int32_t w_dtype
   ws += b_frag;
   a.top_gain = reinterpret_cast<float*>(ws);
   ws += b_tg;
-  a.top_seed = reinterpret_cast<uint16_t*>(ws);
+  a.top_seed = reinterpret_cast<uint32_t*>(ws);
   a.nsplit = nsplit;
   a.fused_rescore = screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, nsplit) ? 1 : 0;
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
@@ -198,7 +198,7 @@ PeLayout pe_layout(const awsrc_params* p, int n_modules, int64_t T_total) {
   l.colsh = align_up(pe_colsh_bytes(p->S), 256);
   l.mods = align_up((size_t)n_modules * sizeof(ModEntry), 256);
   l.tg = align_up((size_t)T_total * kTop * 4, 256);
-  l.ts = align_up((size_t)T_total * kTop * 2, 256);
+  l.ts = align_up((size_t)T_total * kTop * 4, 256);
   l.total = 256 + l.basis + l.frag + l.colsh + l.mods + l.tg + l.ts + 256;
   return l;
 }
@@ -281,7 +281,7 @@ awsrc_status encode_modules(const awsrc_params* p, int32_t n_modules, const void
   q += l.mods;
   a.top_gain = reinterpret_cast<float*>(q);
   q += l.tg;
-  a.top_seed = reinterpret_cast<uint16_t*>(q);
+  a.top_seed = reinterpret_cast<uint32_t*>(q);
   a.nsplit = 1;
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
@@ -319,6 +319,51 @@ extern "C" awsrc_status awsrc_encode_tiles(const awsrc_params* p, const void* W,
   const int64_t rm[1] = {rows}, cm[1] = {cols};
   return encode_modules(p, 1, Wm, w_dtype, W0m, dm, d_mode, rm, cm, seed_out, code_out, scale_out, gain_out,
                         alpha_or_null, workspace, ws_bytes, stream);
+}
+
+extern "C" awsrc_status awsrc_encode_screen_lists(const awsrc_params* p, int32_t n_modules, const int64_t* rows,
+                                                  const int64_t* cols, int32_t d_mode, const void* workspace,
+                                                  float* gain_out, uint32_t* seed_out, int32_t* nsplit,
+                                                  void* stream) {
+  awsrc_status st = check_params(p);
+  if (st) return st;
+  if (!workspace || !nsplit) return fail(AWSRC_EINVAL, "NULL argument");
+  if (d_mode != AWSRC_D_PER_COL && d_mode != AWSRC_D_PER_ELEM) return fail(AWSRC_EINVAL, "bad d_mode %d", d_mode);
+  if (n_modules < 1 || !rows || !cols) return fail(AWSRC_EINVAL, "bad module table");
+  int64_t T_total = 0;
+  for (int m = 0; m < n_modules; ++m) {
+    if (rows[m] < 0 || cols[m] < 1 || cols[m] % p->C) return fail(AWSRC_EINVAL, "module %d: bad shape", m);
+    T_total += rows[m] * (cols[m] / p->C);
+  }
+  const char* ws = reinterpret_cast<const char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
+  const float* tg = nullptr;
+  const uint32_t* ts = nullptr;
+  int ns = 1;
+  if (pe_batched_supported(p->C, p->P, d_mode, p->gen_version)) {
+    const PeLayout l = pe_layout(p, n_modules, T_total);
+    tg = reinterpret_cast<const float*>(ws + 256 + l.basis + l.frag + l.colsh + l.mods);
+    ts = reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(tg) + l.tg);
+  } else {
+    if (n_modules != 1) return fail(AWSRC_EINVAL, "lists of several modules on the per-module path are not kept");
+    ns = screen_nsplit(p->C, p->P, p->S, rows[0], cols[0], d_mode, p->gen_version);
+    if (screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, ns))
+      return fail(AWSRC_EINVAL, "this screen runs the re-score itself and keeps no lists");
+    const int64_t nb = cols[0] / p->C;
+    const int PB = factor_pb(p->C, p->P);
+    size_t off = 256 + align_up(basis_bytes(p->S, p->P), 256);
+    if (d_mode == AWSRC_D_PER_COL) off += align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) + align_up((size_t)nb * p->C * 8, 256);
+    if (screen_mfma_supported(p->C, p->P, d_mode, p->gen_version)) off += align_up(mfma_frag_bytes(p->C, p->S), 256);
+    tg = reinterpret_cast<const float*>(ws + off);
+    ts = reinterpret_cast<const uint32_t*>(ws + off + align_up((size_t)T_total * ns * kTop * 4, 256));
+  }
+  *nsplit = ns;
+  if (!gain_out && !seed_out) return AWSRC_OK;
+  if (!gain_out || !seed_out) return fail(AWSRC_EINVAL, "NULL output");
+  hipStream_t s = (hipStream_t)stream;
+  const size_t n = (size_t)T_total * ns * kTop;
+  HIPCHK(hipMemcpyAsync(gain_out, tg, n * 4, hipMemcpyDeviceToDevice, s));
+  HIPCHK(hipMemcpyAsync(seed_out, ts, n * 4, hipMemcpyDeviceToDevice, s));
+  return AWSRC_OK;
 }
 
 extern "C" awsrc_status awsrc_encode_modules(const awsrc_params* p, int32_t n_modules, const void* const* W,

@@ -76,25 +76,69 @@ inline int colfac_stride(int P) {
 
 __host__ __device__ __forceinline__ int ltri(int p, int k) { return p * (p - 1) / 2 + k; }
 
+// Knife edges of the fp32 screen.  The screen takes the rounding decisions of
+// Sec. 3.2 (the scale, then every code) in fp32, the re-score in fp64 with
+// the full chain; the two agree except where a decision lies within the
+// screen's rounding error of its threshold, and there the screen scores a
+// different rounding of the fit (by up to a few 1e-3 of the gain).  The
+// screen flags such candidates (bit kEdge of a list entry's seed word) so
+// that the re-score's window around them is the wide one below:
+//   scale: m / qmax within 4e-6 (relative) of an fp16 rounding midpoint, or
+//          of a power of two for the power-of-two format, or an fp16
+//          subnormal scale;
+//   codes: some |alpha_p / scale| < qmax within 1e-4 + 2e-5 |alpha_p / scale|
+//          of a half-integer.
+// The tolerances are some ten times the screen's relative error in alpha at
+// the workloads' conditioning (measured: a few 1e-7).
+constexpr uint32_t kEdge = 1u << 16;
+__host__ __device__ __forceinline__ int list_seed(uint32_t w) { return (int)(w & 0xFFFFu); }
+
+// The re-score's window below the best screened score g of a tile with
+// weighted energy e = sum_j d_j r_j^2: a second kept seed is re-scored in
+// fp64 when its screened score lies within it.  Narrow (1e-4 |g| + 1e-7 e)
+// unless one of the two is flagged as a knife edge (3e-2 |g| + 3e-5 e, ten
+// times the largest effect of a differing rounding seen).
+__host__ __device__ __forceinline__ float rescore_window(float g, float e, bool edge) {
+  return edge ? 3e-2f * fabsf(g) + 3e-5f * e : 1e-4f * fabsf(g) + 1e-7f * e;
+}
+
+__device__ __forceinline__ bool code_edge(float x, float qmax) {
+  const float ax = fabsf(x);
+  return ax < qmax && 0.5f - fabsf(x - rintf(x)) < 1e-4f + 2e-5f * ax;
+}
+
 // Screen-precision scale of max |alpha| = m: fp16 f16(m / qmax) with
 // saturation, or the power of two 2^e, e = ceil(log2(m / qmax)), from the
-// exponent and mantissa bits of the fp32 quotient.  Returns the scale and
-// sets *isc to its reciprocal (0 when the scale is 0).  The format is a
-// template argument: as a run-time flag it slowed the matrix-core screens by
-// about a quarter.
-template <bool POW2>
-__device__ __forceinline__ float screen_scale(float m, float inv_qmax, float* isc) {
-  const float x = m * inv_qmax;
+// exponent and mantissa bits of the fp32 quotient.  The caller's values may
+// be 2^RAW times the real ones (the unscaled projections of the matrix-core
+// screens); the rounding is taken on the real value, as in the re-score.
+// Returns the scale (in the caller's units), sets *isc to its reciprocal (0
+// when the scale is 0) and *edge when the choice is on a knife edge (above).
+// The format is a template argument: as a run-time flag it slowed the
+// matrix-core screens by about a quarter.
+template <bool POW2, int RAW = 0>
+__device__ __forceinline__ float screen_scale(float m, float inv_qmax, float* isc, bool* edge) {
+  const float x = m * inv_qmax * (1.0f / (float)(1 << RAW));  // real units, exact
   if constexpr (POW2) {
     const uint32_t xb = __float_as_uint(x);
-    int e = (int)((xb >> 23) & 0xFFu) - 127 + ((xb & 0x7FFFFFu) ? 1 : 0);
-    e = e < -126 ? -126 : (e > 127 ? 127 : e);
-    *isc = x > 0.0f ? __uint_as_float((uint32_t)(127 - e) << 23) : 0.0f;
-    return x > 0.0f ? __uint_as_float((uint32_t)(127 + e) << 23) : 0.0f;
+    const uint32_t mb = xb & 0x7FFFFFu;
+    int e = (int)((xb >> 23) & 0xFFu) - 127 + (mb ? 1 : 0);
+    e = e < -126 ? -126 : (e > 127 - RAW ? 127 - RAW : e);
+    *edge = x > 0.0f && (mb < 32u || mb > 0x7FFFFFu - 32u);
+    *isc = x > 0.0f ? __uint_as_float((uint32_t)(127 - e - RAW) << 23) : 0.0f;
+    return x > 0.0f ? __uint_as_float((uint32_t)(127 + e + RAW) << 23) : 0.0f;
   }
   uint16_t hb = __half_as_ushort(__float2half_rn(x));
   if ((hb & 0x7FFFu) == 0x7C00u) hb = 0x7BFFu;  // saturate at 65504
-  const float sc = __half2float(__ushort_as_half(hb));
+  const float sr = __half2float(__ushort_as_half(hb));
+  // the rounding midpoints next to sr lie half an fp16 spacing away (below a
+  // power of two the spacing underneath is half as wide)
+  const uint32_t sb = __float_as_uint(sr);
+  const int E = (int)((sb >> 23) & 0xFFu) - 127;
+  float half = __uint_as_float((uint32_t)((E - 10 < -24 ? -24 : E - 10) - 1 + 127) << 23);
+  if (x < sr && (sb & 0x7FFFFFu) == 0 && E > -14) half *= 0.5f;
+  *edge = sr > 0.0f && (fabsf(fabsf(x - sr) - half) < 4e-6f * x || E < -14);
+  const float sc = sr * (float)(1 << RAW);
   *isc = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
   return sc;
 }
@@ -107,6 +151,7 @@ __device__ __forceinline__ float screen_scale(float m, float inv_qmax, float* is
 // 2 a.b - a^T G0 a of the quantized fit minus scale^2 eps |q|^2 (relative
 // size ~ lambda), which the fp64 re-score of the kept seeds removes.  Uses
 // q.b = (L^T q).w with w = L^-1 b, and q^T G q = sum_k e_k (L^T q)_k^2.
+// *edge: a rounding decision on a knife edge (above).
 //
 // Split in two: screen_fwd solves L w = b and returns b^T G^-1 b =
 // sum_k w_k^2 / e_k, the score of the unquantized optimum alpha = G^-1 b.
@@ -130,8 +175,9 @@ __device__ __forceinline__ float screen_fwd(const float (&b)[PB], const FP& f, f
   return bound;
 }
 
-template <int PB, bool POW2, typename FP>
-__device__ __forceinline__ float screen_gain_w(const float (&w)[PB], const FP& f, float qmax, float inv_qmax) {
+template <int PB, bool POW2, int RAW, typename FP>
+__device__ __forceinline__ float screen_gain_w(const float (&w)[PB], const FP& f, float qmax, float inv_qmax,
+                                               bool* edge) {
   constexpr int LS = PB * (PB - 1) / 2;
   float al[PB];
 #pragma unroll
@@ -145,10 +191,16 @@ __device__ __forceinline__ float screen_gain_w(const float (&w)[PB], const FP& f
 #pragma unroll
   for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
   float isc;
-  const float sc = screen_scale<POW2>(m, inv_qmax, &isc);
+  bool ed;
+  const float sc = screen_scale<POW2, RAW>(m, inv_qmax, &isc, &ed);
   float q[PB];
 #pragma unroll
-  for (int p = 0; p < PB; ++p) q[p] = __builtin_amdgcn_fmed3f(rintf(al[p] * isc), -qmax, qmax);
+  for (int p = 0; p < PB; ++p) {
+    const float x = al[p] * isc;
+    q[p] = __builtin_amdgcn_fmed3f(rintf(x), -qmax, qmax);
+    ed = ed || code_edge(x, qmax);
+  }
+  *edge = ed;
   float t1 = 0.0f, quad = 0.0f;
 #pragma unroll
   for (int k = 0; k < PB; ++k) {
@@ -161,11 +213,12 @@ __device__ __forceinline__ float screen_gain_w(const float (&w)[PB], const FP& f
   return sc * (2.0f * t1 - sc * quad);  // 0 when the scale is 0 (all codes 0)
 }
 
-template <int PB, bool POW2, typename FP>
-__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax) {
+template <int PB, bool POW2, int RAW, typename FP>
+__device__ __forceinline__ float screen_score_ldl(const float (&b)[PB], const FP& f, float qmax, float inv_qmax,
+                                                  bool* edge) {
   float w[PB];
   (void)screen_fwd<PB>(b, f, w);
-  return screen_gain_w<PB, POW2>(w, f, qmax, inv_qmax);
+  return screen_gain_w<PB, POW2, RAW>(w, f, qmax, inv_qmax, edge);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -202,7 +255,7 @@ struct EncodeArgs {
   unsigned long long* scored;  // count of candidates scored in full (the pruned screen adds to it)
   void* frag;          // +-1 basis fragments of the matrix-core screen
   float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending
-  uint16_t* top_seed;  // [T][nsplit][kTop]
+  uint32_t* top_seed;  // [T][nsplit][kTop] seed | kEdge flag
   int nsplit;          // seed ranges screened by separate waves (merged in the re-score)
   int fused_rescore;   // the screen also runs the re-score (no separate launch)
   uint16_t* seed_out;

@@ -210,7 +210,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
   const bool pow2 = a.scale_fmt == AWSRC_SCALE_POW2;
   const float invC = 1.0f / C;
   float tg[kTop];
-  int ts[kTop];
+  uint32_t ts[kTop];  // seed words: seed | kEdge flag
 #pragma unroll
   for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
 
@@ -232,6 +232,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
       bv[p] = acc * InvSqrtC<C>::v;
     }
     float g;
+    bool edge = false;
     if constexpr (PE) {
       // Cholesky factor of G = B^T D B + eps I from the Gram gathers
       float L[PB][PB], inv[PB];
@@ -284,13 +285,15 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 #pragma unroll
       for (int p = 0; p < PB; ++p) m = fmaxf(m, fabsf(al[p]));
       float isc;
-      const float sc = pow2 ? screen_scale<true>(m, inv_qmax, &isc) : screen_scale<false>(m, inv_qmax, &isc);
+      const float sc = pow2 ? screen_scale<true>(m, inv_qmax, &isc, &edge) : screen_scale<false>(m, inv_qmax, &isc, &edge);
       g = 0.0f;
       if (sc > 0.0f) {
         float q[PB], t1 = 0.0f, qq = 0.0f;
 #pragma unroll
         for (int p = 0; p < PB; ++p) {
-          q[p] = fminf(fmaxf(rintf(al[p] * isc), -qmax), qmax);
+          const float x = al[p] * isc;
+          q[p] = fminf(fmaxf(rintf(x), -qmax), qmax);
+          edge = edge || code_edge(x, qmax);
           t1 += q[p] * bv[p];
           qq += q[p] * q[p];
         }
@@ -307,16 +310,17 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
       }
     } else {
       const float* fs = a.colfac + ((size_t)blk * a.S + s) * stride;
-      g = pow2 ? screen_score_ldl<PB, true>(bv, fs, qmax, inv_qmax) : screen_score_ldl<PB, false>(bv, fs, qmax, inv_qmax);
+      g = pow2 ? screen_score_ldl<PB, true, 0>(bv, fs, qmax, inv_qmax, &edge)
+               : screen_score_ldl<PB, false, 0>(bv, fs, qmax, inv_qmax, &edge);
     }
     // keep the best kTop, earlier (lower) seeds first among equals
     float cg = g;
-    int cs_ = s;
+    uint32_t cs_ = (uint32_t)s | (edge ? kEdge : 0u);
 #pragma unroll
     for (int k = 0; k < kTop; ++k) {
       if (cg > tg[k]) {
         const float tgk = tg[k];
-        const int tsk = ts[k];
+        const uint32_t tsk = ts[k];
         tg[k] = cg; ts[k] = cs_;
         cg = tgk; cs_ = tsk;
       }
@@ -327,7 +331,7 @@ __global__ __launch_bounds__(64) void k_screen_valu(EncodeArgs a, int stride) {
 #pragma unroll
     for (int k = 0; k < kTop; ++k) {
       a.top_gain[t * kTop + k] = tg[k];
-      a.top_seed[t * kTop + k] = (uint16_t)ts[k];
+      a.top_seed[t * kTop + k] = ts[k];
     }
   }
 }
@@ -385,7 +389,7 @@ __device__ __forceinline__ void finalize_tile(const EncodeArgs& a, const double*
   // and each list is ordered (gain desc, seed asc), so strict comparisons
   // keep the lower seed first among equal gains
   float tg[kTop];
-  int ts[kTop];
+  uint32_t ts[kTop];  // seed words: seed | kEdge flag
 #pragma unroll
   for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
   for (int sp = 0; sp < a.nsplit; ++sp) {
@@ -393,19 +397,19 @@ __device__ __forceinline__ void finalize_tile(const EncodeArgs& a, const double*
     for (int k = 0; k < kTop; ++k) {
       const int64_t at = (t * a.nsplit + sp) * kTop + k;
       float g = a.top_gain[at];
-      int sd = a.top_seed[at];
+      uint32_t sd = a.top_seed[at];
 #pragma unroll
       for (int m = 0; m < kTop; ++m) {
         if (g > tg[m]) {
           const float tgm = tg[m];
-          const int tsm = ts[m];
+          const uint32_t tsm = ts[m];
           tg[m] = g; ts[m] = sd;
           g = tgm; sd = tsm;
         }
       }
     }
   }
-  const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
+  const float thr = tg[0] - rescore_window(tg[0], e32, ((ts[0] | ts[1]) & kEdge) != 0);
 
   double best_g = -INFINITY;
   int best_s = 0x7FFFFFFF;
@@ -417,7 +421,7 @@ __device__ __forceinline__ void finalize_tile(const EncodeArgs& a, const double*
 
   for (int k = 0; k < kTop; ++k) {
     if (k > 0 && !(tg[k] >= thr && tg[k] > -INFINITY)) continue;
-    const int s = ts[k];
+    const int s = list_seed(ts[k]);
     const uint64_t* sw = a.basis.sign + (size_t)s * 2;
     const uint8_t* cs = a.basis.col + (size_t)s * kMaxP;
     int c[PB];
@@ -586,7 +590,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   // and each list is ordered (gain desc, seed asc), so strict comparisons
   // keep the lower seed first among equal gains
   float tg[kTop];
-  int ts[kTop];
+  uint32_t ts[kTop];  // seed words: seed | kEdge flag
 #pragma unroll
   for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
   for (int sp = 0; sp < a.nsplit; ++sp) {
@@ -594,12 +598,12 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
     for (int k = 0; k < kTop; ++k) {
       const int64_t at = (t * a.nsplit + sp) * kTop + k;
       float g = a.top_gain[at];
-      int sd = a.top_seed[at];
+      uint32_t sd = a.top_seed[at];
 #pragma unroll
       for (int m = 0; m < kTop; ++m) {
         if (g > tg[m]) {
           const float tgm = tg[m];
-          const int tsm = ts[m];
+          const uint32_t tsm = ts[m];
           tg[m] = g; ts[m] = sd;
           g = tgm; sd = tsm;
         }

@@ -145,161 +145,6 @@ __device__ __forceinline__ void project64(const u32x4& F0, const u32x4& F1, cons
   }
 }
 
-// Per-element weights: lane = tile during the per-candidate stage.  The
-// 16 x 64 result is transposed through LDS so that each lane holds the P
-// coefficients of its own tile for both seeds of the pair; each lane then
-// factors its own G + eps I from the Gram gathers and scores every candidate.
-template <bool POW2>
-__global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4* __restrict__ frag) {
-  constexpr int C = 64;
-  constexpr int PB = 8;
-  constexpr int TS = 8;  // LDS stride (floats) of one tile's coefficients
-  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
-  constexpr int LS = PB * (PB - 1) / 2;
-  // 20 KB in all, so that eight wavefronts fit in a CU's 160 KB.  tb: a
-  // tile's two 16-byte halves trade places in every other group of 8 tiles,
-  // so that the 16-byte accesses of 16 lanes cover all banks.  wdl: lane-
-  // minor ([coordinate][lane]), so that a gather at a wavefront-uniform
-  // coordinate reads 64 consecutive words.
-  __shared__ __attribute__((aligned(16))) float tb[2 * 64 * TS];
-  __shared__ float wdl[C * 64];
-  const int lane = threadIdx.x;
-  const int nbk_cols = (int)(a.cols / C);
-  const ScreenTask tk = screen_task(a, 64);
-  const int blk = tk.blk, pair0 = tk.pair0, pair1 = tk.pair1;
-  const int n = lane & 15, g = lane >> 4;
-  u32x4 uh[4][2], um[4][2], ul[4][2];
-  load_u64<true>(a, tk.row0, blk, n, g, uh, um, ul);
-  const int64_t my_row = tk.row0 + lane;
-  const bool my_valid = my_row < a.rows;
-  const int64_t my_off = (my_valid ? my_row : a.rows - 1) * a.cols + (int64_t)blk * C;
-  const int P = a.P;
-  {
-    // WHT of this lane's tile weights, for the Gram gathers G_pq = WHT(d)[c_p ^ c_q] / C
-    float wd[C];
-#pragma unroll
-    for (int j = 0; j < C; ++j) wd[j] = a.d[my_off + j];
-#pragma unroll
-    for (int h = 1; h < C; h <<= 1)
-#pragma unroll
-      for (int i = 0; i < C; i += 2 * h)
-#pragma unroll
-        for (int k = i; k < i + h; ++k) {
-          const float x = wd[k], y = wd[k + h];
-          wd[k] = x + y;
-          wd[k + h] = x - y;
-        }
-    // stored divided by C, so the gathers are the Gram entries themselves
-#pragma unroll
-    for (int j = 0; j < C; ++j) wdl[j * 64 + lane] = wd[j] * (1.0f / C);
-  }
-  const float qmax = (float)((1 << (a.b - 1)) - 1);
-  const float inv_qmax = 1.0f / qmax;
-  const float lam = (float)a.lambda;
-  float tg0 = -INFINITY, tg1 = -INFINITY;
-  int ts0 = 0, ts1 = 0;
-
-  // Post-processing runs in "raw" units: b is left unscaled by 1/sqrt(C) = 1/8,
-  // so alpha, the scale and the gain come out 8, 8 and 64 times larger; the
-  // codes and the seed order are unchanged (scaling by a power of two commutes
-  // with the roundings), and the kept gains are rescaled once at the end.
-  //
-  // Software pipeline: while the vector ALUs post-process seed pair k, the
-  // matrix cores compute the projections of pair k+1 (the fragment table is
-  // padded with zero pairs, so the last iterations need no special case).
-  const u32x4* fp = frag + (size_t)pair0 * 128 + lane;
-  auto stash = [&](const f32x4 (&acc)[4]) {
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-      *reinterpret_cast<f32x4*>(&tb[((g >> 1) * 64 + 16 * nb + n) * TS + 4 * ((g & 1) ^ ((n >> 3) & 1))]) = acc[nb];
-  };
-  {
-    f32x4 acc[4];
-    project64(fp[0], fp[64], uh, um, ul, acc);
-    stash(acc);
-  }
-  u32x4 F0 = fp[128], F1 = fp[192];
-  for (int pair = pair0; pair < pair1; ++pair) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    float bk[2][PB];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int sw = 4 * ((lane >> 3) & 1);
-      const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + sw]);
-      const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[(k * 64 + lane) * TS + 4 - sw]);
-      bk[k][0] = b0[0]; bk[k][1] = b0[1]; bk[k][2] = b0[2]; bk[k][3] = b0[3];
-      bk[k][4] = b1[0]; bk[k][5] = b1[1]; bk[k][6] = b1[2]; bk[k][7] = b1[3];
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    // projections of the next pair (zero rows past the last seed) and the prefetch after it
-    f32x4 accN[4];
-    project64(F0, F1, uh, um, ul, accN);
-    F0 = fp[(size_t)(pair - pair0 + 2) * 128];
-    F1 = fp[(size_t)(pair - pair0 + 2) * 128 + 64];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int s = 2 * pair + k;
-      // this tile's G + eps I = L diag(e) L^T from the Gram gathers, row by
-      // row (E = L diag(e) kept for the current row only), in the layout of
-      // the per-column table so the same score routine applies
-      float f[NF];
-      const int sc_ = s < a.S ? s : a.S - 1;
-      // the seed's columns: two scalar dword loads (uniform across the wavefront)
-      const __attribute__((address_space(4))) uint32_t* cw =
-          (const __attribute__((address_space(4))) uint32_t*)(a.basis.col + (size_t)sc_ * kMaxP);
-      const uint32_t cw0 = cw[0], cw1 = cw[1];
-      int c[PB];
-#pragma unroll
-      for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw0 : cw1) >> (8 * (p & 3))) & 0xFFu) : 0;
-      const float* wrow = &wdl[lane];  // coordinate x at wrow[64 x]
-      const float eps = lam * wrow[0];
-#pragma unroll
-      for (int p = 0; p < PB; ++p) {
-        float E[PB];
-#pragma unroll
-        for (int q = 0; q < p; ++q) {
-          float t = (p < P && q < P) ? wrow[64 * (c[p] ^ c[q])] : 0.0f;
-#pragma unroll
-          for (int kk = 0; kk < q; ++kk) t = fmaf(-E[kk], f[ltri(q, kk)], t);
-          E[q] = t;
-          f[ltri(p, q)] = t * f[LS + q];
-        }
-        float t = (p < P) ? wrow[0] + eps : 1.0f;
-#pragma unroll
-        for (int kk = 0; kk < p; ++kk) t = fmaf(-E[kk], f[ltri(p, kk)], t);
-        t = fmaxf(t, 1e-30f);
-        f[LS + PB + p] = t;
-        f[LS + p] = __builtin_amdgcn_rcpf(t);
-      }
-      float gsc = screen_score_ldl<PB, POW2>(bk[k], f, qmax, inv_qmax);
-      gsc = s < a.S ? gsc : -INFINITY;
-      // branch-free insertion into the top two (earlier seeds first among equals)
-      const bool c0 = gsc > tg0, c1 = gsc > tg1;
-      tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
-      ts1 = c0 ? ts0 : (c1 ? s : ts1);
-      tg0 = c0 ? gsc : tg0;
-      ts0 = c0 ? s : ts0;
-    }
-    // interleave the 24 matrix-core instructions with the vector work above
-#pragma unroll
-    for (int i = 0; i < 24; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
-    }
-    stash(accN);
-  }
-  if (my_valid) {
-    const int64_t at = ((my_row * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
-    a.top_gain[at + 0] = tg0 * (1.0f / 64.0f);  // back to gain units
-    a.top_gain[at + 1] = tg1 * (1.0f / 64.0f);
-    a.top_seed[at + 0] = (uint16_t)ts0;
-    a.top_seed[at + 1] = (uint16_t)ts1;
-  }
-}
-
 // Per-column weights.  The factor of G + eps I is one table entry per seed,
 // shared by every tile of the wavefront, and the projections are used where
 // the matrix cores leave them: lane (n, g) holds 4 coefficients of seed g/2
@@ -311,17 +156,16 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe64(EncodeArgs a, const u32x4
 // lanes g and g^2, and the two lanes' lists are merged at the end.
 //
 // Every candidate gets the forward solve and its bound (screen_fwd); only
-// those whose bound clears the tile's current second score are scored in
-// full.  Those few would leave most lanes idle, so each lane queues its
-// survivors (w, the seed and which of its tiles) in its own LDS ring, and a
-// scoring round takes the oldest entry of every lane that has one.  The
-// threshold is the tile's second score over both of its lanes' lists: a
-// candidate below two scores already found is in neither the tile's final
-// top two nor (as those two are each in some lane's list) needed in its own
-// lane's list for the merge.  A lane's entries are scored in seed order, and
-// thresholds only rise, so the merged lists are those of scoring every
-// candidate.  The factor of 1 + 2^-9 on the bound covers its fp32 rounding
-// and that of the score (each a few ulps of the bound).
+// those whose bound reaches the re-score's window below the tile's current
+// best are scored in full.  Those few would leave most lanes idle, so each
+// lane queues its survivors (w, the seed and which of its tiles) in its own
+// LDS ring, and a scoring round takes the oldest entry of every lane that
+// has one.  The threshold comes from the tile's best over both of its
+// lanes' lists (below).  A lane's entries are scored in seed order, and
+// thresholds only rise, so the merged lists agree with those of scoring
+// every candidate in the best and in the second wherever the second lies
+// inside the re-score's window.  The factor of 1 + 2^-9 on the bound covers
+// its fp32 rounding and that of the score (each a few ulps of the bound).
 //
 // Factor entries reach the wavefront through an LDS ring of the last NR
 // pairs (both seeds' whole entries per slot): while pair k is bounded, every
@@ -372,8 +216,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   // top two per tile; a lane's seeds increase, so strict comparisons keep the
   // earlier seed first among equal scores
   float tg[2][2] = {{-INFINITY, -INFINITY}, {-INFINITY, -INFINITY}};
-  int ts[2][2] = {{0, 0}, {0, 0}};
-  auto insert = [&](int t, float gsc, int s) {
+  uint32_t ts[2][2] = {{0, 0}, {0, 0}};  // seed words: seed | kEdge flag
+  auto insert = [&](int t, float gsc, uint32_t s) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const bool c0 = t == j && gsc > tg[j][0], c1 = t == j && gsc > tg[j][1];
@@ -401,7 +245,9 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
         const f32x4 v = *reinterpret_cast<const f32x4*>(&fe[4 * i]);
         f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
       }
-      insert(code >> 16, screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax), s);
+      bool edge;
+      const float gsc = screen_gain_w<PB, POW2, 3>(wv, f, qmax, inv_qmax, &edge);
+      insert(code >> 16, gsc, (uint32_t)s | (edge ? kEdge : 0u));
       qhead = (qhead + 1) & (QD - 1);
       --qlen;
       ++nscored;
@@ -422,19 +268,46 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
     *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NF) + 4 * pc]) = v;
   };
 
-  // each tile's second score over both lanes' lists (lane ^ 32 holds the
-  // other seed parity): the second largest of {a0 >= a1} and {b0 >= b1} is
-  // max(min(a0, b0), max(a1, b1)); lists change only in scoring rounds
+  // Pruning threshold of each tile: the re-score takes a second seed only
+  // when its screened score lies within rescore_window of the best, so a
+  // candidate below that window of the tile's current best (over both lanes'
+  // lists; lane ^ 32 holds the other seed parity) is never needed, and the
+  // window's lower edge only rises.  The threshold takes the window one
+  // percent wider, far above the fp32 rounding of either, and the wide
+  // window when the best is flagged as a knife edge; in raw units the energy
+  // term is 64 times larger.  Lists change only in scoring rounds.
+  float e_raw[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int64_t rr = tv[t] ? trow0 + 16 * t : a.rows - 1;
+    const int64_t o = rr * a.cols + (int64_t)blk * C;
+    float e = 0.0f;
+#pragma unroll
+    for (int j0 = 0; j0 < C; j0 += 8) {
+      float w[8], w0[8], dj[8];
+      load8_w(a.W, a.w_dtype, o + j0, w);
+      load8_f(a.W0 + o + j0, w0);
+      load8_f(a.d + (int64_t)blk * C + j0, dj);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float r = w[k] - w0[k];
+        e = fmaf(dj[k] * r, r, e);
+      }
+    }
+    e_raw[t] = 64.0f * e;
+  }
   float thr[2] = {-INFINITY, -INFINITY};
   auto update_thr = [&]() {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][0]), __float_as_uint(tg[t][0]), false,
                                                        false);
-      const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg[t][1]), __float_as_uint(tg[t][1]), false,
-                                                       false);
-      const float o0 = __uint_as_float(sh ? r0[0] : r0[1]), o1 = __uint_as_float(sh ? r1[0] : r1[1]);
-      thr[t] = fmaxf(fminf(tg[t][0], o0), fmaxf(tg[t][1], o1));
+      const auto r1 = __builtin_amdgcn_permlane32_swap(ts[t][0], ts[t][0], false, false);
+      const float og = __uint_as_float(sh ? r0[0] : r0[1]);
+      const uint32_t ow = sh ? r1[0] : r1[1];
+      const float best = fmaxf(tg[t][0], og);
+      const bool edge = ((tg[t][0] >= og ? ts[t][0] : ow) & kEdge) != 0;
+      thr[t] = best - 1.01f * rescore_window(best, e_raw[t], edge);
     }
   };
 
@@ -533,14 +406,16 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
 
   // merge each tile's lists from lanes g (this seed parity) and g ^ 2 (the
   // other): (gain desc, seed asc)
-  auto better = [](float ga, int sa, float gb, int sb) { return ga > gb || (ga == gb && sa < sb); };
+  auto better = [](float ga, uint32_t sa, float gb, uint32_t sb) {
+    return ga > gb || (ga == gb && list_seed(sa) < list_seed(sb));
+  };
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const float og0 = __shfl_xor(tg[t][0], 32, 64), og1 = __shfl_xor(tg[t][1], 32, 64);
-    const int os0 = __shfl_xor(ts[t][0], 32, 64), os1 = __shfl_xor(ts[t][1], 32, 64);
+    const uint32_t os0 = (uint32_t)__shfl_xor((int)ts[t][0], 32, 64), os1 = (uint32_t)__shfl_xor((int)ts[t][1], 32, 64);
     if (sh == 0 && tv[t]) {
       float r0, r1;
-      int q0, q1;
+      uint32_t q0, q1;
       if (better(tg[t][0], ts[t][0], og0, os0)) {
         r0 = tg[t][0]; q0 = ts[t][0];
         const bool m = better(tg[t][1], ts[t][1], og0, os0);
@@ -555,14 +430,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
         float* st = &lds[4 * (16 * (nb0 + t) + n)];
         st[0] = r0 * (1.0f / 64.0f);  // back to gain units
         st[1] = r1 * (1.0f / 64.0f);
-        st[2] = __int_as_float(q0);
-        st[3] = __int_as_float(q1);
+        st[2] = __uint_as_float(q0);
+        st[3] = __uint_as_float(q1);
       } else {
         const int64_t at = (((trow0 + 16 * t) * nbk_cols + blk) * a.nsplit + tk.split) * kTop;
         a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
         a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
-        a.top_seed[at + 0] = (uint16_t)q0;
-        a.top_seed[at + 1] = (uint16_t)q1;
+        a.top_seed[at + 0] = q0;
+        a.top_seed[at + 1] = q1;
       }
     }
   }
@@ -575,7 +450,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
     // they never use)
     const f32x4 v = *reinterpret_cast<const f32x4*>(&lds[4 * lane]);
     const float mg[kTop] = {v[0], v[1]};
-    const int ms[kTop] = {__float_as_int(v[2]), __float_as_int(v[3])};
+    const uint32_t ms[kTop] = {__float_as_uint(v[2]), __float_as_uint(v[3])};
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -645,7 +520,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   const float inv_qmax = 1.0f / qmax;
   constexpr float isq = C == 64 ? 0.125f : 0.08838834764831845f;  // 1/sqrt(C)
   float tg0 = -INFINITY, tg1 = -INFINITY;
-  int ts0 = 0, ts1 = 0;
+  uint32_t ts0 = 0, ts1 = 0;  // seed words: seed | kEdge flag
 
   const u32x4* fp = frag + (size_t)pair0 * (NKS * 64) + lane;
   auto project = [&](const u32x4 (&F)[NKS], f32x4 (&acc)[2]) {
@@ -705,14 +580,16 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     project(F, accN);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
-    float gsc = screen_score_ldl<PB, POW2>(bv, f, qmax, inv_qmax);
+    bool edge;
+    float gsc = screen_score_ldl<PB, POW2, 0>(bv, f, qmax, inv_qmax, &edge);
     gsc = s < a.S ? gsc : -INFINITY;
+    const uint32_t sw = (uint32_t)s | (edge ? kEdge : 0u);
     // this lane's seeds increase, so strict comparisons keep the lower seed among equals
     const bool c0 = gsc > tg0, c1 = gsc > tg1;
     tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
-    ts1 = c0 ? ts0 : (c1 ? s : ts1);
+    ts1 = c0 ? ts0 : (c1 ? sw : ts1);
     tg0 = c0 ? gsc : tg0;
-    ts0 = c0 ? s : ts0;
+    ts0 = c0 ? sw : ts0;
 #pragma unroll
     for (int i = 0; i < 24; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -722,11 +599,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   }
   // merge the two halves' lists of each tile: (gain desc, seed asc)
   const float og0 = __shfl(tg0, lane + 32, 64), og1 = __shfl(tg1, lane + 32, 64);
-  const int os0 = __shfl(ts0, lane + 32, 64), os1 = __shfl(ts1, lane + 32, 64);
+  const uint32_t os0 = (uint32_t)__shfl((int)ts0, lane + 32, 64), os1 = (uint32_t)__shfl((int)ts1, lane + 32, 64);
   if (half == 0 && my_valid) {
-    auto better = [](float ga, int sa, float gb, int sb) { return ga > gb || (ga == gb && sa < sb); };
+    auto better = [](float ga, uint32_t sa, float gb, uint32_t sb) {
+      return ga > gb || (ga == gb && list_seed(sa) < list_seed(sb));
+    };
     float r0, r1;
-    int q0, q1;
+    uint32_t q0, q1;
     if (better(tg0, ts0, og0, os0)) {
       r0 = tg0; q0 = ts0;
       const bool m = better(tg1, ts1, og0, os0);
@@ -739,8 +618,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     const int64_t at = ((my_row * nbk_cols + blk) * nsplit + split) * kTop;
     a.top_gain[at + 0] = r0;
     a.top_gain[at + 1] = r1;
-    a.top_seed[at + 0] = (uint16_t)q0;
-    a.top_seed[at + 1] = (uint16_t)q1;
+    a.top_seed[at + 0] = q0;
+    a.top_seed[at + 1] = q1;
   }
 }
 
@@ -800,9 +679,7 @@ static hipError_t screen_mfma_fmt(const EncodeArgs& a, void* frag, hipStream_t s
     return hipGetLastError();
   }
   const int64_t wgs = (a.cols / a.C) * ((a.rows + 63) / 64) * a.nsplit;
-  if (a.d_mode == AWSRC_D_PER_ELEM)
-    hipLaunchKernelGGL((k_screen_pe64<POW2>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr);
-  else if (!a.fused_rescore)
+  if (!a.fused_rescore)
     hipLaunchKernelGGL((k_screen_col64<POW2, 0>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));
   else if (a.P <= 4)
     hipLaunchKernelGGL((k_screen_col64<POW2, 4>), dim3((unsigned)wgs), dim3(64), 0, st, a, fr, colfac_stride(8));

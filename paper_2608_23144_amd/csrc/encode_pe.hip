@@ -232,17 +232,22 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   int ts0 = 0, ts1 = 0;
   float thr = -INFINITY;
   // The re-score takes a tile's second seed only when its screened score lies
-  // within 1e-4 |best| + 1e-7 energy of the best, so a candidate below that
-  // window of the tile's current best (over both lanes' lists) can never be
-  // needed: the window's lower edge only rises with the best.  The
-  // threshold carries a margin (1.005e-4, 1.05e-7) over the re-score's
-  // window, far above the fp32 rounding of either; in raw units the energy
-  // term is 64 times larger.
-  const float e_win = 64.0f * 1.05e-7f * energy;
+  // within rescore_window of the best, so a candidate below that window of
+  // the tile's current best (over both lanes' lists) can never be needed: the
+  // window's lower edge only rises with the best.  The threshold takes the
+  // window one percent wider, far above the fp32 rounding of either, and the
+  // wide window when the best is flagged as a knife edge (its score may be
+  // off by more than the narrow one); in raw units the energy term is 64
+  // times larger.
+  const float e_raw = 64.0f * energy;
   auto update_thr = [&]() {
     const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg0), __float_as_uint(tg0), false, false);
-    const float best = fmaxf(tg0, __uint_as_float(sh ? r0[0] : r0[1]));
-    thr = best - (1.005e-4f * fabsf(best) + e_win);
+    const auto r1 = __builtin_amdgcn_permlane32_swap(ts0, ts0, false, false);
+    const float og = __uint_as_float(sh ? r0[0] : r0[1]);
+    const uint32_t ow = sh ? r1[0] : r1[1];
+    const float best = fmaxf(tg0, og);
+    const bool edge = ((tg0 >= og ? ts0 : ow) & kEdge) != 0;
+    thr = best - 1.01f * rescore_window(best, e_raw, edge);
   };
   int qhead = 0, qtail = 0, qlen = 0;
   int nscored = 0;
@@ -258,12 +263,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       float gr[NL], f[NF];
       gather_pe<PB>(wdl, cs, tl4, gr);
       factor_pe<PB, FULLP>(gr, d0, eps, P, f);
-      const float gsc = screen_gain_w<PB, POW2>(wv, f, qmax, inv_qmax);
+      bool edge;
+      const float gsc = screen_gain_w<PB, POW2, 3>(wv, f, qmax, inv_qmax, &edge);
+      const uint32_t sw = (uint32_t)s | (edge ? kEdge : 0u);
       const bool c0 = gsc > tg0, c1 = gsc > tg1;
       tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
-      ts1 = c0 ? ts0 : (c1 ? s : ts1);
+      ts1 = c0 ? ts0 : (c1 ? sw : ts1);
       tg0 = c0 ? gsc : tg0;
-      ts0 = c0 ? s : ts0;
+      ts0 = c0 ? sw : ts0;
       qhead = (qhead + 1) & (QD - 1);
       --qlen;
       ++nscored;
@@ -349,11 +356,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   // merge the tile's even-seed (this lane) and odd-seed (lane + 32) lists
   // into (gain desc, seed asc) and store them for the re-score
   const float og0 = __shfl_xor(tg0, 32, 64), og1 = __shfl_xor(tg1, 32, 64);
-  const int os0 = __shfl_xor(ts0, 32, 64), os1 = __shfl_xor(ts1, 32, 64);
+  const uint32_t os0 = (uint32_t)__shfl_xor((int)ts0, 32, 64), os1 = (uint32_t)__shfl_xor((int)ts1, 32, 64);
   if (sh == 0 && valid) {
-    auto better = [](float ga, int sa, float gb, int sb) { return ga > gb || (ga == gb && sa < sb); };
+    auto better = [](float ga, uint32_t sa, float gb, uint32_t sb) {
+      return ga > gb || (ga == gb && list_seed(sa) < list_seed(sb));
+    };
     float r0, r1;
-    int q0, q1;
+    uint32_t q0, q1;
     if (better(tg0, ts0, og0, os0)) {
       r0 = tg0; q0 = ts0;
       const bool mm = better(tg1, ts1, og0, os0);
@@ -366,8 +375,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     const int64_t at = (md.tile_off + my_row * nbk + blk) * kTop;
     a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
     a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
-    a.top_seed[at + 0] = (uint16_t)q0;
-    a.top_seed[at + 1] = (uint16_t)q1;
+    a.top_seed[at + 0] = q0;
+    a.top_seed[at + 1] = q1;
   }
 }
 

@@ -175,7 +175,7 @@ constexpr int kRescoreLds = 64 * 65 + 64 + 2 * 64;
 // tile's row directly.
 template <int PB>
 __device__ __forceinline__ void rescore_block64(const EncodeArgs& a, int blk, int64_t row0, const float (&tg)[kTop],
-                                                const int (&ts)[kTop], float* lds) {
+                                                const uint32_t (&ts)[kTop], float* lds) {
   constexpr int C = 64;
   const int lane = threadIdx.x & 63;
   const int nb = (int)(a.cols / C);
@@ -288,10 +288,11 @@ __device__ __forceinline__ void rescore_block64(const EncodeArgs& a, int blk, in
   double best_al[PB];
   uint16_t best_bits;
   float e32;
-  int best_s = ts[0];
+  int best_s = list_seed(ts[0]);
   double best_g = score(best_s, true, &e32, best_q, best_al, &best_bits);
-  // the second kept seed only when its screened gain is close to the best
-  const float thr = tg[0] - (1e-4f * fabsf(tg[0]) + 1e-7f * e32);
+  // the second kept seed only when its screened gain lies within the
+  // re-score's window of the best (the wide one if either is a knife edge)
+  const float thr = tg[0] - rescore_window(tg[0], e32, ((ts[0] | ts[1]) & kEdge) != 0);
 #pragma unroll
   for (int k = 1; k < kTop; ++k) {
     if (tg[k] >= thr && tg[k] > -INFINITY) {
@@ -299,10 +300,11 @@ __device__ __forceinline__ void rescore_block64(const EncodeArgs& a, int blk, in
       double al[PB];
       uint16_t bits;
       float e_;
-      const double g = score(ts[k], false, &e_, q, al, &bits);
-      if (g > best_g || (g == best_g && ts[k] < best_s)) {
+      const int sk = list_seed(ts[k]);
+      const double g = score(sk, false, &e_, q, al, &bits);
+      if (g > best_g || (g == best_g && sk < best_s)) {
         best_g = g;
-        best_s = ts[k];
+        best_s = sk;
         best_bits = bits;
 #pragma unroll
         for (int p = 0; p < PB; ++p) { best_q[p] = q[p]; best_al[p] = al[p]; }

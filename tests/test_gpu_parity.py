@@ -839,3 +839,50 @@ def test_encode_modules_matches_per_module_calls_and_oracle(name):
         _check_encode_sample(wl, m, inp, W0, sl, np.arange(T))
         off += T
     assert off == got["seed"].numel()
+
+
+# ------------------------------------------------------------------ screen error vs the re-score window
+@pytest.mark.parametrize("name,rows,cols,S", [("block3b", 256, 2048, 256), ("down3b", 128, 11008, 256),
+                                              ("layer32b", 64, 5120, 1024), ("block3b", 11008, 2048, 256)])
+def test_screen_error_within_rescore_window(name, rows, cols, S):
+    """The fp32 screen's score of the seed the encoder stored against the fp64
+    gain of the stored record, over every tile where the screen's best seed
+    is the stored one: the difference stays below a tenth of the re-score's
+    window (1e-4 |g| + 1e-7 sum d r^2; 3e-2 |g| + 3e-5 sum d r^2 for a
+    candidate the screen flagged as a rounding knife edge), so the window
+    covers the screen's error tenfold.  (Per-element weights: the batched
+    screen; per column at C = 64 with seed ranges, and at C = 128: the
+    screens whose lists reach the workspace.)"""
+    wl = workload(name, S=S)
+    m = Module("win", rows, cols, 0, 1, 1)
+    inp, (codes, scale, zero, W0), enc = _gpu_module(wl, m, want_alpha=False)
+    d_mode = awsrc.AWSRC_D_PER_COL if inp["d"].dim() == 1 else awsrc.AWSRC_D_PER_ELEM
+    g32, w32 = awsrc.awsrc_encode_screen_lists(_params(wl), [(rows, cols)], d_mode, enc["workspace"])
+    torch.cuda.synchronize()
+    g32 = g32.cpu().numpy().astype(np.float64)
+    w32 = w32.cpu().numpy().astype(np.int64)
+    # best over the seed ranges: (gain desc, seed asc)
+    T, ns, _ = g32.shape
+    gg, ss, ff = g32[:, :, 0], w32[:, :, 0] & 0xFFFF, (w32[:, :, 0] >> 16) & 1
+    order = np.lexsort((ss, -gg), axis=1)[:, 0]
+    gbest, sbest, fbest = gg[np.arange(T), order], ss[np.arange(T), order], ff[np.arange(T), order]
+    g64 = enc["gain"].cpu().numpy()
+    seed = _u16(enc["seed"])
+    r = inp["W32"] - W0
+    dd = inp["d"] if inp["d"].dim() == 2 else inp["d"][None, :].expand(rows, cols)
+    e = (dd * r * r).reshape(T, wl.C).sum(dim=1).double().cpu().numpy()
+    same = seed == sbest
+    assert same.mean() > 0.99
+    narrow = 1e-4 * np.abs(g64) + 1e-7 * e
+    wide = 3e-2 * np.abs(g64) + 3e-5 * e
+    diff = np.abs(gbest - g64)
+    plain, edge = same & (fbest == 0), same & (fbest == 1)
+    rel = diff / np.maximum(np.abs(g64), 1e-30)
+    print(f"{name} {rows}x{cols} S={S}: {int(same.sum())} tiles, {int(edge.sum())} flagged; "
+          f"largest |g32 - g64| / |g64|: {rel[plain].max():.2e} unflagged "
+          f"({(diff / narrow)[plain].max():.3f} of the narrow window), "
+          f"{rel[edge].max() if edge.any() else 0.0:.2e} flagged "
+          f"({(diff / wide)[edge].max() if edge.any() else 0.0:.3f} of the wide window)")
+    assert (diff / narrow)[plain].max() <= 0.1
+    if edge.any():
+        assert (diff / wide)[edge].max() <= 0.1
