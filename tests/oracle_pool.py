@@ -121,8 +121,12 @@ def run_jobs(jobs: Sequence[tuple], nproc: Optional[int] = None) -> Dict:
     if nproc == 1 or len(jobs) == 1:
         outs = [_job(j) for j in jobs]
     else:
+        outs = []
         with mp.get_context("spawn").Pool(min(nproc, len(jobs))) as pool:
-            outs = pool.map(_job, jobs, chunksize=1)
+            # a line per finished chunk, so that a long comparison shows its progress
+            for o in pool.imap_unordered(_job, jobs, chunksize=1):
+                outs.append(o)
+                print(f"[oracle_pool] {len(outs)}/{len(jobs)} chunks, {time.perf_counter() - t0:.1f} s", flush=True)
     tot = {"tiles": 0, "seed_diff": 0, "edge": 0, "failures": 0, "report": [], "cpu_seconds": 0.0}
     for o in outs:
         for k in ("tiles", "seed_diff", "edge", "failures"):
