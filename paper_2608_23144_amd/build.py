@@ -17,7 +17,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libawsrc.so")
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "basis.hip", "backbone.hip", "sdq.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip", "rank.hip",
+SOURCES = ["abi.cpp", "basis.hip", "backbone.hip", "sdq.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip", "rescore_pe.hip", "rank.hip",
            "decode.hip"]
 
 COMMON = [

@@ -187,18 +187,24 @@ awsrc_status encode_module(const awsrc_params* p, const void* W, int32_t w_dtype
 }
 
 // Workspace of the batched per-element encoder: count | basis | fragments |
-// shifted columns | module table | top lists of every tile.
+// shifted columns | module table | top lists of every work item (32 tiles
+// each, padded where a module's rows end mid-group).
 struct PeLayout {
   size_t basis, frag, colsh, mods, tg, ts, total;
 };
-PeLayout pe_layout(const awsrc_params* p, int n_modules, int64_t T_total) {
+int64_t pe_items(const awsrc_params* p, int n_modules, const int64_t* rows, const int64_t* cols) {
+  int64_t items = 0;
+  for (int m = 0; m < n_modules; ++m) items += (rows[m] + kPeRows - 1) / kPeRows * (cols[m] / p->C);
+  return items;
+}
+PeLayout pe_layout(const awsrc_params* p, int n_modules, int64_t items) {
   PeLayout l;
   l.basis = align_up(basis_bytes(p->S, p->P), 256);
   l.frag = align_up(mfma_frag_bytes(p->C, p->S), 256);
   l.colsh = align_up(pe_colsh_bytes(p->S), 256);
   l.mods = align_up((size_t)n_modules * sizeof(ModEntry), 256);
-  l.tg = align_up((size_t)T_total * kTop * 4, 256);
-  l.ts = align_up((size_t)T_total * kTop * 4, 256);
+  l.tg = align_up((size_t)items * kPeRows * kTop * 4, 256);
+  l.ts = align_up((size_t)items * kPeRows * kTop * 4, 256);
   l.total = 256 + l.basis + l.frag + l.colsh + l.mods + l.tg + l.ts + 256;
   return l;
 }
@@ -227,7 +233,7 @@ awsrc_status encode_modules(const awsrc_params* p, int32_t n_modules, const void
   const bool batched = pe_batched_supported(p->C, p->P, d_mode, p->gen_version);
   size_t need = 0;
   if (batched) {
-    need = pe_layout(p, n_modules, T_total).total;
+    need = pe_layout(p, n_modules, pe_items(p, n_modules, rows, cols)).total;
   } else {
     for (int m = 0; m < n_modules; ++m) {
       const size_t b = module_ws_bytes(p, rows[m], cols[m], d_mode);
@@ -262,7 +268,7 @@ awsrc_status encode_modules(const awsrc_params* p, int32_t n_modules, const void
     }
     return AWSRC_OK;
   }
-  const PeLayout l = pe_layout(p, n_modules, T_total);
+  const PeLayout l = pe_layout(p, n_modules, pe_items(p, n_modules, rows, cols));
   EncodeArgs a{};
   a.w_dtype = w_dtype; a.d_mode = d_mode;
   a.C = p->C; a.P = p->P; a.b = p->b; a.S = p->S;
@@ -286,23 +292,22 @@ awsrc_status encode_modules(const awsrc_params* p, int32_t n_modules, const void
   a.seed_out = seed_out; a.code_out = code_out; a.scale_out = scale_out; a.gain_out = gain_out;
   a.alpha_out = alpha_or_null;
   std::vector<ModEntry> tab(n_modules);
-  int64_t t0 = 0, items = 0, fitems = 0;
+  int64_t t0 = 0, items = 0;
   for (int m = 0; m < n_modules; ++m) {
     const int64_t nb = cols[m] / p->C;
     ModEntry& e = tab[m];
     e.W = W[m]; e.W0 = W0[m]; e.d = d[m];
     e.rows = rows[m]; e.cols = cols[m];
-    e.tile_off = t0; e.item_off = items; e.fitem_off = fitems;
+    e.tile_off = t0; e.item_off = items; e.pad_ = 0;
     t0 += rows[m] * nb;
     items += (rows[m] + kPeRows - 1) / kPeRows * nb;
-    fitems += (rows[m] + 63) / 64 * nb;
   }
-  if (items > (int64_t)INT32_MAX || fitems > (int64_t)INT32_MAX) return fail(AWSRC_EINVAL, "too many work items");
+  if (items > (int64_t)INT32_MAX) return fail(AWSRC_EINVAL, "too many work items");
   HIPCHK(launch_mod_table(tab.data(), n_modules, mods, s));
   HIPCHK(launch_scored_zero(a.scored, s));  // the pruned screen adds its count
   HIPCHK(launch_gen_basis(p->basis_key, p->C, p->P, p->S, p->gen_version, a.basis, s));
   HIPCHK(launch_pe_screen(a, mods, n_modules, items, a.frag, colsh, s));
-  HIPCHK(launch_finalize_pe_modules(a, mods, n_modules, fitems, s));
+  HIPCHK(launch_finalize_pe_modules(a, mods, n_modules, items, s));
   return AWSRC_OK;
 }
 
@@ -336,30 +341,34 @@ extern "C" awsrc_status awsrc_encode_screen_lists(const awsrc_params* p, int32_t
     T_total += rows[m] * (cols[m] / p->C);
   }
   const char* ws = reinterpret_cast<const char*>(align_up(reinterpret_cast<uintptr_t>(workspace), 256));
-  const float* tg = nullptr;
-  const uint32_t* ts = nullptr;
-  int ns = 1;
+  hipStream_t s = (hipStream_t)stream;
   if (pe_batched_supported(p->C, p->P, d_mode, p->gen_version)) {
-    const PeLayout l = pe_layout(p, n_modules, T_total);
-    tg = reinterpret_cast<const float*>(ws + 256 + l.basis + l.frag + l.colsh + l.mods);
-    ts = reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(tg) + l.tg);
-  } else {
-    if (n_modules != 1) return fail(AWSRC_EINVAL, "lists of several modules on the per-module path are not kept");
-    ns = screen_nsplit(p->C, p->P, p->S, rows[0], cols[0], d_mode, p->gen_version);
-    if (screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, ns))
-      return fail(AWSRC_EINVAL, "this screen runs the re-score itself and keeps no lists");
-    const int64_t nb = cols[0] / p->C;
-    const int PB = factor_pb(p->C, p->P);
-    size_t off = 256 + align_up(basis_bytes(p->S, p->P), 256);
-    if (d_mode == AWSRC_D_PER_COL) off += align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) + align_up((size_t)nb * p->C * 8, 256);
-    if (screen_mfma_supported(p->C, p->P, d_mode, p->gen_version)) off += align_up(mfma_frag_bytes(p->C, p->S), 256);
-    tg = reinterpret_cast<const float*>(ws + off);
-    ts = reinterpret_cast<const uint32_t*>(ws + off + align_up((size_t)T_total * ns * kTop * 4, 256));
+    // work-item-major lists, permuted into tile order on the device
+    const int64_t items = pe_items(p, n_modules, rows, cols);
+    const PeLayout l = pe_layout(p, n_modules, items);
+    const ModEntry* mods = reinterpret_cast<const ModEntry*>(ws + 256 + l.basis + l.frag + l.colsh);
+    const float* tg = reinterpret_cast<const float*>(ws + 256 + l.basis + l.frag + l.colsh + l.mods);
+    const uint32_t* ts = reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(tg) + l.tg);
+    *nsplit = 1;
+    if (!gain_out && !seed_out) return AWSRC_OK;
+    if (!gain_out || !seed_out) return fail(AWSRC_EINVAL, "NULL output");
+    HIPCHK(launch_pe_lists_tile_order(tg, ts, mods, n_modules, items, gain_out, seed_out, s));
+    return AWSRC_OK;
   }
+  if (n_modules != 1) return fail(AWSRC_EINVAL, "lists of several modules on the per-module path are not kept");
+  const int ns = screen_nsplit(p->C, p->P, p->S, rows[0], cols[0], d_mode, p->gen_version);
+  if (screen_fuses_rescore(p->C, p->P, d_mode, p->gen_version, ns))
+    return fail(AWSRC_EINVAL, "this screen runs the re-score itself and keeps no lists");
+  const int64_t nb = cols[0] / p->C;
+  const int PB = factor_pb(p->C, p->P);
+  size_t off = 256 + align_up(basis_bytes(p->S, p->P), 256);
+  if (d_mode == AWSRC_D_PER_COL) off += align_up((size_t)nb * p->S * colfac_stride(PB) * 4, 256) + align_up((size_t)nb * p->C * 8, 256);
+  if (screen_mfma_supported(p->C, p->P, d_mode, p->gen_version)) off += align_up(mfma_frag_bytes(p->C, p->S), 256);
+  const float* tg = reinterpret_cast<const float*>(ws + off);
+  const uint32_t* ts = reinterpret_cast<const uint32_t*>(ws + off + align_up((size_t)T_total * ns * kTop * 4, 256));
   *nsplit = ns;
   if (!gain_out && !seed_out) return AWSRC_OK;
   if (!gain_out || !seed_out) return fail(AWSRC_EINVAL, "NULL output");
-  hipStream_t s = (hipStream_t)stream;
   const size_t n = (size_t)T_total * ns * kTop;
   HIPCHK(hipMemcpyAsync(gain_out, tg, n * 4, hipMemcpyDeviceToDevice, s));
   HIPCHK(hipMemcpyAsync(seed_out, ts, n * 4, hipMemcpyDeviceToDevice, s));

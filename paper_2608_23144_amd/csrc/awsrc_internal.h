@@ -255,7 +255,8 @@ struct EncodeArgs {
   unsigned long long* scored;  // count of candidates scored in full (the pruned screen adds to it)
   void* frag;          // +-1 basis fragments of the matrix-core screen
   float* top_gain;     // [T][nsplit][kTop] screened gains per seed range, descending
-  uint32_t* top_seed;  // [T][nsplit][kTop] seed | kEdge flag
+                       // (the batched per-element encoder: [item][kTop][32], see launch_pe_lists_tile_order)
+  uint32_t* top_seed;  // same layout: seed | kEdge flag
   int nsplit;          // seed ranges screened by separate waves (merged in the re-score)
   int fused_rescore;   // the screen also runs the re-score (no separate launch)
   uint16_t* seed_out;
@@ -266,9 +267,9 @@ struct EncodeArgs {
 };
 
 // One module of a batched encode: its inputs, shape, the global index of its
-// first tile (outputs are concatenated in module order) and the first work
-// item of the screen (32-row groups x column blocks) and of the re-score
-// (64-row groups x column blocks) that belongs to it.
+// first tile (outputs are concatenated in module order) and its first work
+// item (32-row groups x column blocks, the same items for the screen and the
+// re-score).
 struct ModEntry {
   const void* W;
   const float* W0;
@@ -276,19 +277,18 @@ struct ModEntry {
   int64_t rows, cols;
   int64_t tile_off;
   int64_t item_off;
-  int64_t fitem_off;
+  int64_t pad_;  // keeps entries at 64 bytes
 };
 static_assert(sizeof(ModEntry) == 64, "module table entries are 64 bytes");
 
-// The module holding work item `item`: the last m with (fin ? fitem_off :
-// item_off) <= item (modules without work items share their successor's
-// offset and are skipped).  Wavefront-uniform.
-__device__ __forceinline__ int find_module(const ModEntry* mods, int n, int64_t item, bool fin) {
+// The module holding work item `item`: the last m with item_off <= item
+// (modules without work items share their successor's offset and are
+// skipped).  Wavefront-uniform.
+__device__ __forceinline__ int find_module(const ModEntry* mods, int n, int64_t item) {
   int lo = 0, hi = n - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    const int64_t o = fin ? mods[mid].fitem_off : mods[mid].item_off;
-    if (o <= item) lo = mid;
+    if (mods[mid].item_off <= item) lo = mid;
     else hi = mid - 1;
   }
   return lo;
@@ -311,6 +311,10 @@ hipError_t launch_pe_screen(const EncodeArgs& a, const ModEntry* mods, int n_mod
                             uint32_t* colsh, hipStream_t st);
 hipError_t launch_finalize_pe_modules(const EncodeArgs& a, const ModEntry* mods, int n_mods, int64_t items,
                                       hipStream_t st);
+// The batched screen's top lists ([item][kTop][32], work-item major) in tile
+// order ([T][kTop]), for awsrc_encode_screen_lists.
+hipError_t launch_pe_lists_tile_order(const float* tg, const uint32_t* ts, const ModEntry* mods, int n_mods,
+                                      int64_t items, float* gain_out, uint32_t* seed_out, hipStream_t st);
 
 bool encode_supported(int C, int P);
 // the matrix-core screens: C = 64 (P <= 8), C = 128 (P <= 8, per-column

@@ -526,43 +526,6 @@ __global__ __launch_bounds__(64) void k_finalize(EncodeArgs a, const double* __r
   finalize_tile<C, PB, PE>(a, wdb, row, blk, my);
 }
 
-// The same re-score for the per-element batched encoder: one workgroup per
-// (module, 64-row group, column block), the module found in the module
-// table; `a` carries the outputs and top lists of all modules concatenated.
-template <int PB>
-__global__ __launch_bounds__(64) void k_finalize_pe_modules(EncodeArgs a, const ModEntry* __restrict__ mods,
-                                                            int n_mods) {
-  constexpr int C = 64;
-  extern __shared__ double fsh[];
-  double* my = fsh + threadIdx.x * (C + 1);
-  const int64_t item = blockIdx.x;
-  const int m = find_module(mods, n_mods, item, true);
-  const ModEntry md = mods[m];
-  const int nb = (int)(md.cols / C);
-  const int64_t local = item - md.fitem_off;
-  const int blk = (int)(local % nb);
-  const int64_t row = (local / nb) * 64 + threadIdx.x;
-  if (row >= md.rows) return;
-  EncodeArgs am = a;
-  am.W = md.W; am.W0 = md.W0; am.d = md.d; am.rows = md.rows; am.cols = md.cols;
-  am.seed_out += md.tile_off; am.scale_out += md.tile_off; am.gain_out += md.tile_off;
-  am.code_out += md.tile_off * a.P;
-  if (am.alpha_out) am.alpha_out += md.tile_off * a.P;
-  am.top_gain += md.tile_off * kTop; am.top_seed += md.tile_off * kTop;
-  am.nsplit = 1;
-  finalize_tile<C, PB, true>(am, nullptr, row, blk, my);
-}
-
-hipError_t launch_finalize_pe_modules(const EncodeArgs& a, const ModEntry* mods, int n_mods, int64_t items,
-                                      hipStream_t st) {
-  const size_t lds = (size_t)64 * 65 * sizeof(double);
-  if (a.P <= 4)
-    hipLaunchKernelGGL((k_finalize_pe_modules<4>), dim3((unsigned)items), dim3(64), lds, st, a, mods, n_mods);
-  else
-    hipLaunchKernelGGL((k_finalize_pe_modules<8>), dim3((unsigned)items), dim3(64), lds, st, a, mods, n_mods);
-  return hipGetLastError();
-}
-
 // Per-column weights, generator version 1, C = 64 (the common case), when
 // the screen leaves the re-score to a kernel of its own (seed ranges split
 // over wavefronts): one wavefront per (row group of 64, column block) merges

@@ -38,7 +38,7 @@
 //     the merged top two agree with those of scoring every candidate in the
 //     best and in the second wherever the second is inside the window.
 //
-// The kept lists go to the fp64 re-score (k_finalize_pe_modules).
+// The kept lists go to the fp64 re-score (k_finalize_pe_modules, rescore_pe.hip).
 #include <math.h>
 
 #include "awsrc_internal.h"
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   __shared__ float qb[QD * QW * 64];       // queues, [slot][word][lane]
   const int lane = threadIdx.x;
   const int64_t item = blockIdx.x;
-  const int m = find_module(mods, n_mods, item, false);
+  const int m = find_module(mods, n_mods, item);
   const ModEntry md = mods[m];
   const int nbk = (int)(md.cols / C);
   const int64_t local = item - md.item_off;
@@ -357,7 +357,9 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
   // into (gain desc, seed asc) and store them for the re-score
   const float og0 = __shfl_xor(tg0, 32, 64), og1 = __shfl_xor(tg1, 32, 64);
   const uint32_t os0 = (uint32_t)__shfl_xor((int)ts0, 32, 64), os1 = (uint32_t)__shfl_xor((int)ts1, 32, 64);
-  if (sh == 0 && valid) {
+  // (every lane's slot is written: rows past the module's end keep -inf and
+  // seed 0, so the re-score never reads a stale entry)
+  if (sh == 0) {
     auto better = [](float ga, uint32_t sa, float gb, uint32_t sb) {
       return ga > gb || (ga == gb && list_seed(sa) < list_seed(sb));
     };
@@ -372,11 +374,13 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
       const bool mm = better(tg0, ts0, og1, os1);
       r1 = mm ? tg0 : og1; q1 = mm ? ts0 : os1;
     }
-    const int64_t at = (md.tile_off + my_row * nbk + blk) * kTop;
-    a.top_gain[at + 0] = r0 * (1.0f / 64.0f);  // back to gain units
-    a.top_gain[at + 1] = r1 * (1.0f / 64.0f);
-    a.top_seed[at + 0] = q0;
-    a.top_seed[at + 1] = q1;
+    // work-item-major lists, [item][kTop][32 tiles], so that the stores and
+    // the re-score's loads are whole lines
+    const int64_t at = item * (kTop * NT) + tl;
+    a.top_gain[at] = r0 * (1.0f / 64.0f);  // back to gain units
+    a.top_gain[at + NT] = r1 * (1.0f / 64.0f);
+    a.top_seed[at] = q0;
+    a.top_seed[at + NT] = q1;
   }
 }
 

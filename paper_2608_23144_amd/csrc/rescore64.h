@@ -323,4 +323,29 @@ __device__ __forceinline__ void rescore_block64(const EncodeArgs& a, int blk, in
   }
 }
 
+// fp64 Cholesky factor of G + eps I for one seed from its gathered Gram
+// entries g (packed lower triangle with the diagonal, (p, r) at
+// p (p + 1) / 2 + r, unscaled transform values: G_pr = g / C), G + eps I =
+// L L^T, inv_p = 1 / L_pp.  Padding columns p >= P get an identity row.
+template <int C, int PB>
+__device__ __forceinline__ void chol64_vals(int P, const double (&g)[PB * (PB + 1) / 2], double eps,
+                                            double (&L)[PB][PB], double (&inv)[PB]) {
+#pragma unroll
+  for (int p = 0; p < PB; ++p)
+#pragma unroll
+    for (int r = 0; r <= p; ++r) {
+      double acc;
+      if (p < P && r < P) acc = g[p * (p + 1) / 2 + r] / C + (p == r ? eps : 0.0);
+      else acc = (p == r) ? 1.0 : 0.0;
+#pragma unroll
+      for (int kk = 0; kk < r; ++kk) acc -= L[p][kk] * L[r][kk];
+      if (p == r) {
+        L[p][p] = sqrt(fmax(acc, 1e-300));
+        inv[p] = 1.0 / L[p][p];
+      } else {
+        L[p][r] = acc * inv[r];
+      }
+    }
+}
+
 }  // namespace awsrc

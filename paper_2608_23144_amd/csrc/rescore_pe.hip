@@ -1,0 +1,370 @@
+// fp64 re-score of the batched per-element encoder (C = 64, P <= 8,
+// generator version 1): the kept seeds of every tile of every module are
+// re-scored with the complete chain of Sec. 3.2 in fp64 (projection through
+// the Walsh-Hadamard transform of sigma .* d .* r, Gram entries through the
+// transform of the tile's own d, Cholesky solve of Eq. (3), quantization,
+// and the gain of the quantized fit); writes the encoder outputs.
+//
+// One wavefront per (module, 32-row group, column block), the screen's work
+// items; two lanes per tile: lane l (tile l % 32) holds coordinates
+// 32 (l / 32) .. + 31.  Each lane transforms its half with the first five
+// butterfly stages of the length-64 transform in registers and stores the
+// result in its tile's LDS row; the sixth stage, T[k] = X[k % 32] +- Y[k % 32]
+// (X, Y the two halves' partial transforms, minus for k >= 32), is folded
+// into the gathers, which read only the entries the fit needs.  This is the
+// operation order of the full transform, so the values are the same; both
+// lanes of a tile then run the same solve and the lower one writes.  Per lane
+// this holds 32 doubles of a transform at a time, and the 32 gather rows
+// (16.6 KB) are written once per transform, with no turn-taking.
+#include <math.h>
+
+#include "awsrc_internal.h"
+#include "rescore64.h"
+
+namespace awsrc {
+
+namespace {
+
+constexpr int kC = 64;
+constexpr int kH = 32;                       // coordinates per lane
+constexpr int kRowD = kC + 1;                // doubles per LDS gather row
+constexpr int kLdsFloats = 2 * kPeRows * kRowD;  // the gather rows (fp64), or the r and d staging blocks (fp32)
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Transform entry k of a tile from its LDS row: X[k % 32] + Y[k % 32] for
+// k < 32, X[k % 32] - Y[k % 32] otherwise (the last butterfly stage).
+__device__ __forceinline__ double tentry(const double* row, int k) {
+  const double x = row[k & (kH - 1)], y = row[kH + (k & (kH - 1))];
+  return (k & kH) ? x - y : x + y;
+}
+
+}  // namespace
+
+// 1 / x in fp64: the hardware reciprocal refined by two Newton steps (the
+// error of the estimate squares at each step; well inside the solve's own
+// rounding).
+__device__ __forceinline__ double recip64(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  r = fma(r, fma(-x, r, 1.0), r);
+  return fma(r, fma(-x, r, 1.0), r);
+}
+
+// G + eps I = L diag(e) L^T (L unit lower triangular, strict part packed by
+// rows) in fp64 from the gathered transform values g (packed lower triangle
+// with the diagonal; G_pr = g / C); inv = 1 / e.  Padding columns p >= P get
+// L = 0, e = 1.  No square roots, one reciprocal per pivot.
+template <int PB>
+__device__ __forceinline__ void ldl64(int P, const double (&g)[PB * (PB + 1) / 2], double eps,
+                                      double (&L)[PB * (PB - 1) / 2], double (&e)[PB], double (&inv)[PB]) {
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    double E[PB];  // row p of L diag(e)
+#pragma unroll
+    for (int r = 0; r < p; ++r) {
+      double acc = (p < P && r < P) ? g[p * (p + 1) / 2 + r] * (1.0 / kC) : 0.0;
+#pragma unroll
+      for (int k = 0; k < r; ++k) acc = fma(-E[k], L[ltri(r, k)], acc);
+      E[r] = acc;
+      L[ltri(p, r)] = acc * inv[r];
+    }
+    double acc = p < P ? fma(g[p * (p + 1) / 2 + p], 1.0 / kC, eps) : 1.0;
+#pragma unroll
+    for (int k = 0; k < p; ++k) acc = fma(-E[k], L[ltri(p, k)], acc);
+    e[p] = fmax(acc, 1e-300);
+    inv[p] = recip64(e[p]);
+  }
+}
+
+// The fp64 re-score of one candidate from its projections bv = B^T u and the
+// factor of its G + eps I: the solve of Eq. (3) for the unquantized fit al,
+// the stored scale (bits) and codes q (Sec. 3.2), and the gain
+// 2 a.b - a^T G0 a of the quantized fit a = scale q, with
+// a^T G0 a = sum_k e_k ((L^T a)_k)^2 - eps |a|^2.
+template <int PB>
+__device__ __forceinline__ double solve_score_ldl(const EncodeArgs& a, const double (&bv)[PB],
+                                                  const double (&L)[PB * (PB - 1) / 2], const double (&e)[PB],
+                                                  const double (&inv)[PB], double eps, int qmax, int (&q)[PB],
+                                                  double (&al)[PB], uint16_t* bits_out) {
+  double z[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    double acc = bv[p];
+#pragma unroll
+    for (int k = 0; k < p; ++k) acc = fma(-L[ltri(p, k)], z[k], acc);
+    z[p] = acc;
+  }
+#pragma unroll
+  for (int p = PB - 1; p >= 0; --p) {
+    double acc = z[p] * inv[p];
+#pragma unroll
+    for (int k = p + 1; k < PB; ++k) acc = fma(-L[ltri(k, p)], al[k], acc);
+    al[p] = acc;
+  }
+  double m = 0.0;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
+  uint16_t bits = 0;
+  double sc = 0.0;
+  if (m > 0.0) {
+    if (a.scale_fmt == AWSRC_SCALE_POW2) {
+      // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
+      int ex;
+      frexp(m / (double)qmax, &ex);
+      while (m > (double)qmax * ldexp(1.0, ex)) ++ex;
+      while (m <= (double)qmax * ldexp(1.0, ex - 1)) --ex;
+      ex = ex < -128 ? -128 : (ex > 127 ? 127 : ex);
+      bits = (uint16_t)(ex + 128);
+      sc = ldexp(1.0, ex);
+    } else {
+      // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
+      bits = scale_bits_from_f64(m / (double)qmax);
+      sc = (double)__half2float(__ushort_as_half(bits));
+      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
+    }
+  }
+  const double isc = sc > 0.0 ? 1.0 / sc : 0.0;
+  double ah[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    const double qv = fmin(fmax(rint(al[p] * isc), (double)-qmax), (double)qmax);
+    q[p] = (int)qv;
+    ah[p] = sc * qv;
+  }
+  double t1 = 0.0, aa = 0.0, quad = 0.0;
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    t1 = fma(ah[p], bv[p], t1);
+    aa = fma(ah[p], ah[p], aa);
+  }
+#pragma unroll
+  for (int k = 0; k < PB; ++k) {
+    double y = ah[k];
+#pragma unroll
+    for (int i = k + 1; i < PB; ++i) y = fma(L[ltri(i, k)], ah[i], y);
+    quad = fma(e[k] * y, y, quad);
+  }
+  *bits_out = bits;
+  return 2.0 * t1 - (quad - eps * aa);
+}
+
+template <int PB>
+__global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, const ModEntry* __restrict__ mods,
+                                                               int n_mods) {
+  constexpr int NG = PB * (PB + 1) / 2;
+  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
+  const int lane = threadIdx.x;
+  const int tl = lane & 31, h = lane >> 5;
+  const int64_t item = blockIdx.x;
+  const int m = find_module(mods, n_mods, item);
+  const ModEntry md = mods[m];
+  const int nb = (int)(md.cols / kC);
+  const int64_t local = item - md.item_off;
+  const int blk = (int)(local % nb);
+  const int64_t row0 = (local / nb) * kPeRows;
+  const int64_t c0 = (int64_t)blk * kC;
+
+  // the tile's kept seeds (work-item-major lists; both lanes read them)
+  float tg[kTop];
+  uint32_t ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) {
+    tg[k] = a.top_gain[item * (kTop * kPeRows) + k * kPeRows + tl];
+    ts[k] = a.top_seed[item * (kTop * kPeRows) + k * kPeRows + tl];
+  }
+
+  // Stage the 32 x 64 residual and weight blocks in LDS (rows of 65 floats;
+  // 16 lanes per row segment, 4 rows per pass: each instruction reads whole
+  // cache lines); rows past the end repeat the last row.
+  float* rsh = lds;
+  float* dsh = lds + kPeRows * kRowD;
+  {
+    const int pc = lane & 15;
+#pragma unroll
+    for (int pass = 0; pass < kPeRows / 4; ++pass) {
+      const int rl = 4 * pass + (lane >> 4);
+      const int64_t rg = row0 + rl < md.rows ? row0 + rl : md.rows - 1;
+      const int64_t o = rg * md.cols + c0 + 4 * pc;
+      float w[4];
+      if (a.w_dtype == AWSRC_DTYPE_F32) {
+        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(md.W) + o);
+        w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w;
+      } else {
+        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(md.W) + o);
+        w[0] = __uint_as_float(x.x << 16); w[1] = __uint_as_float(x.x & 0xFFFF0000u);
+        w[2] = __uint_as_float(x.y << 16); w[3] = __uint_as_float(x.y & 0xFFFF0000u);
+      }
+      const float4 y = *reinterpret_cast<const float4*>(md.W0 + o);
+      const float4 z = *reinterpret_cast<const float4*>(md.d + o);
+      float* rp = rsh + rl * kRowD + 4 * pc;
+      float* dp = dsh + rl * kRowD + 4 * pc;
+      rp[0] = w[0] - y.x; rp[1] = w[1] - y.y; rp[2] = w[2] - y.z; rp[3] = w[3] - y.w;
+      dp[0] = z.x; dp[1] = z.y; dp[2] = z.z; dp[3] = z.w;
+    }
+  }
+  wave_sync();
+  float rr[kH], dd[kH];
+#pragma unroll
+  for (int j = 0; j < kH; ++j) {
+    rr[j] = rsh[tl * kRowD + kH * h + j];
+    dd[j] = dsh[tl * kRowD + kH * h + j];
+  }
+  const int64_t row = row0 + tl;
+  const bool valid = row < md.rows;
+  // the tile's weighted energy in the screen's order (each half, then the
+  // two halves added), for the re-score window; the sum of d (exact in fp64)
+  // for the ridge eps = lambda mean_j d_j
+  float e32;
+  double sumd;
+  {
+    float eh = 0.0f;
+    double sh = 0.0;
+#pragma unroll
+    for (int j = 0; j < kH; ++j) {
+      eh = fmaf(dd[j] * rr[j], rr[j], eh);
+      sh += (double)dd[j];
+    }
+    const auto re = __builtin_amdgcn_permlane32_swap(__float_as_uint(eh), __float_as_uint(eh), false, false);
+    e32 = eh + __uint_as_float(h ? re[0] : re[1]);
+    const uint64_t sb = (uint64_t)__double_as_longlong(sh);
+    const auto rl = __builtin_amdgcn_permlane32_swap((uint32_t)sb, (uint32_t)sb, false, false);
+    const auto rh = __builtin_amdgcn_permlane32_swap((uint32_t)(sb >> 32), (uint32_t)(sb >> 32), false, false);
+    const uint64_t ob = (uint64_t)(h ? rl[0] : rl[1]) | ((uint64_t)(h ? rh[0] : rh[1]) << 32);
+    const double so = __longlong_as_double((long long)ob);
+    sumd = h ? so + sh : sh + so;  // lower half first
+  }
+  const double eps = a.lambda * (sumd / kC);
+  const int P = a.P;
+  const double isq = 1.0 / sqrt((double)kC);
+  const int qmax = (1 << (a.b - 1)) - 1;
+  double* grow = reinterpret_cast<double*>(lds) + tl * kRowD;
+
+  // The second kept seed is re-scored only when its screened gain lies
+  // within the re-score's window of the best (the wide one if either is a
+  // knife edge).  The lower lane of a tile scores the best seed, the upper
+  // lane the second one where needed (else the best again).
+  const float thr = tg[0] - rescore_window(tg[0], e32, ((ts[0] | ts[1]) & kEdge) != 0);
+  const bool need = valid && tg[1] >= thr && tg[1] > -INFINITY;
+  const bool two = __ballot(need) != 0;
+  const bool mine2 = h == 1 && need;
+  // seeds index the basis tables: any value outside [0, S) (none comes from
+  // the screen) is replaced by 0 before use
+  const int s0r = list_seed(ts[0]), s1r = list_seed(ts[1]);
+  const int s0 = s0r < a.S ? s0r : 0, s1 = s1r < a.S ? s1r : 0;
+  const int s_me = mine2 ? s1 : s0;
+  int c[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) c[p] = (p < P) ? a.basis.col[(size_t)s_me * kMaxP + p] : 0;
+
+  // projections through the transform of sigma .* d .* r: the best seed's
+  // signs, then (when some tile of the wavefront needs it) the second's
+  double bv[PB];
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1 && !two) break;
+    const int sp = pass ? s1 : s0;
+    const uint32_t sw = (uint32_t)(a.basis.sign[(size_t)sp * 2] >> (kH * h));
+    double v[kH];
+#pragma unroll
+    for (int j = 0; j < kH; ++j) {
+      const double u = (double)dd[j] * (double)rr[j];
+      v[j] = ((sw >> j) & 1u) ? -u : u;
+    }
+    fwht<kH>(v);
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < kH; ++j) grow[kH * h + j] = v[j];
+    wave_sync();
+    if (mine2 == (pass == 1)) {
+#pragma unroll
+      for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? tentry(grow, c[p]) * isq : 0.0;
+    }
+  }
+  // Gram entries of this lane's seed through the transform of d
+  double g[NG];
+  {
+    double v[kH];
+#pragma unroll
+    for (int j = 0; j < kH; ++j) v[j] = (double)dd[j];
+    fwht<kH>(v);
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < kH; ++j) grow[kH * h + j] = v[j];
+    wave_sync();
+#pragma unroll
+    for (int p = 0; p < PB; ++p)
+#pragma unroll
+      for (int r = 0; r <= p; ++r) g[p * (p + 1) / 2 + r] = tentry(grow, c[p] ^ c[r]);
+  }
+  double L[PB * (PB - 1) / 2], e[PB], inv[PB];
+  ldl64<PB>(P, g, eps, L, e, inv);
+  int q[PB];
+  double al[PB];
+  uint16_t bits;
+  const double gk = solve_score_ldl<PB>(a, bv, L, e, inv, eps, qmax, q, al, &bits);
+
+  // the better of the tile's two results (ties: the lower seed) is written
+  // by the lane that holds it
+  const uint64_t gb = (uint64_t)__double_as_longlong(gk);
+  const auto xl = __builtin_amdgcn_permlane32_swap((uint32_t)gb, (uint32_t)gb, false, false);
+  const auto xh = __builtin_amdgcn_permlane32_swap((uint32_t)(gb >> 32), (uint32_t)(gb >> 32), false, false);
+  const double go = __longlong_as_double(
+      (long long)((uint64_t)(h ? xl[0] : xl[1]) | ((uint64_t)(h ? xh[0] : xh[1]) << 32)));
+  const bool second_wins = need && (h ? (gk > go || (gk == go && s1 < s0)) : (go > gk || (go == gk && s1 < s0)));
+  if (valid && (h == 1) == second_wins) {
+    const int64_t t = md.tile_off + row * nb + blk;
+    a.seed_out[t] = (uint16_t)s_me;
+    a.scale_out[t] = bits;
+    a.gain_out[t] = gk;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      if (p < P) {
+        a.code_out[t * P + p] = (int8_t)q[p];
+        if (a.alpha_out) a.alpha_out[t * P + p] = (float)al[p];
+      }
+    }
+  }
+}
+
+hipError_t launch_finalize_pe_modules(const EncodeArgs& a, const ModEntry* mods, int n_mods, int64_t items,
+                                      hipStream_t st) {
+  if (items == 0) return hipSuccess;
+  if (a.P <= 4)
+    hipLaunchKernelGGL((k_finalize_pe_modules<4>), dim3((unsigned)items), dim3(64), 0, st, a, mods, n_mods);
+  else
+    hipLaunchKernelGGL((k_finalize_pe_modules<8>), dim3((unsigned)items), dim3(64), 0, st, a, mods, n_mods);
+  return hipGetLastError();
+}
+
+__global__ void k_pe_lists_tile_order(const float* __restrict__ tg, const uint32_t* __restrict__ ts,
+                                      const ModEntry* __restrict__ mods, int n_mods, float* __restrict__ gout,
+                                      uint32_t* __restrict__ sout) {
+  const int64_t item = blockIdx.x;
+  const int tl = threadIdx.x;
+  const int m = find_module(mods, n_mods, item);
+  const ModEntry md = mods[m];
+  const int nb = (int)(md.cols / kC);
+  const int64_t local = item - md.item_off;
+  const int64_t row = (local / nb) * kPeRows + tl;
+  if (row >= md.rows) return;
+  const int64_t t = md.tile_off + row * nb + local % nb;
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) {
+    gout[t * kTop + k] = tg[item * (kTop * kPeRows) + k * kPeRows + tl];
+    sout[t * kTop + k] = ts[item * (kTop * kPeRows) + k * kPeRows + tl];
+  }
+}
+
+hipError_t launch_pe_lists_tile_order(const float* tg, const uint32_t* ts, const ModEntry* mods, int n_mods,
+                                      int64_t items, float* gain_out, uint32_t* seed_out, hipStream_t st) {
+  if (items == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pe_lists_tile_order, dim3((unsigned)items), dim3(kPeRows), 0, st, tg, ts, mods, n_mods,
+                     gain_out, seed_out);
+  return hipGetLastError();
+}
+
+}  // namespace awsrc

@@ -841,6 +841,43 @@ def test_encode_modules_matches_per_module_calls_and_oracle(name):
     assert off == got["seed"].numel()
 
 
+def test_encode_modules_ragged_groups_with_stale_workspace():
+    """Per-element batched encode of modules whose rows end inside a 32-row
+    work group, into a workspace whose bytes all start as 0xFF: the re-score
+    must read only list entries the screen wrote (every slot, rows past the
+    end included) and index the basis tables with seeds below S.  Outputs
+    equal those of the same call on a zeroed workspace and of per-module
+    calls, and agree with the oracle."""
+    wl = workload("block3b", S=24)
+    mods = [Module("a", 37, 256, 0, 1, 1), Module("b", 5, 128, 0, 2, 2), Module("c", 70, 384, 0, 3, 3)]
+    p = _params(wl)
+    inps, W0s = [], []
+    for m in mods:
+        inp = gen_module_inputs(wl, m, DEV)
+        W0s.append(awsrc.awsrc_backbone_rtn(inp["W"])[3])
+        inps.append(inp)
+    shapes = [(m.rows, m.cols) for m in mods]
+    nbytes = awsrc.encode_modules_workspace_bytes(p, shapes, awsrc.AWSRC_DTYPE_BF16, awsrc.AWSRC_D_PER_ELEM)
+    outs = []
+    for fill in (0xFF, 0x00):
+        ws = torch.full((nbytes + 512,), fill, dtype=torch.uint8, device=DEV)
+        outs.append(awsrc.awsrc_encode_modules(p, [i["W"] for i in inps], W0s, [i["d"] for i in inps],
+                                               want_alpha=True, workspace=ws))
+        torch.cuda.synchronize()
+    for k in ("seed", "codes", "scale", "gain", "alpha"):
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    off = 0
+    for m, inp, W0 in zip(mods, inps, W0s):
+        T = m.rows * m.cols // wl.C
+        ref = awsrc.awsrc_encode_tiles(p, inp["W"], W0, inp["d"], want_alpha=True)
+        torch.cuda.synchronize()
+        for k in ("seed", "codes", "scale", "gain", "alpha"):
+            assert torch.equal(outs[0][k][off:off + T], ref[k]), (m.name, k)
+        sl = {k: (v[off:off + T] if v is not None and k != "workspace" else v) for k, v in outs[0].items()}
+        _check_encode_sample(wl, m, inp, W0, sl, np.arange(T))
+        off += T
+
+
 # ------------------------------------------------------------------ screen error vs the re-score window
 @pytest.mark.parametrize("name,rows,cols,S", [("block3b", 256, 2048, 256), ("down3b", 128, 11008, 256),
                                               ("layer32b", 64, 5120, 1024), ("block3b", 11008, 2048, 256)])
