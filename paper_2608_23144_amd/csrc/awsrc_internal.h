@@ -356,6 +356,9 @@ struct RankWs {
   uint64_t* blk_a;       // [max_blocks + 1] per-block counts / offsets
   uint64_t* blk_b;       // [max_blocks + 1]
   uint64_t* state;       // [kStateWords] select state, counters, totals, histogram
+  uint32_t* rs_hist;     // [256][rs_nblk] radix-sort digit counts per block (large record caps)
+  uint32_t* rs_tot;      // [256] digit totals
+  size_t rs_nblk;
   size_t cap;
   size_t max_blocks;
 };

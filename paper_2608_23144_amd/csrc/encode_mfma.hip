@@ -101,29 +101,34 @@ __device__ __forceinline__ ScreenTask screen_task(const EncodeArgs& a, int rows_
 }
 
 // u = d .* r fragments of the 4 groups of 16 tiles (rows row0 + 16 nb + n),
-// split in three bf16 parts; rows past the end give zeros.
-template <bool PE>
+// split in three bf16 parts; rows past the end give zeros.  en[nb] returns
+// each tile's weighted energy sum_j d_j r_j^2 (summed over the four lanes
+// n, n + 16, n + 32, n + 48 that share the tile's row).
 __device__ __forceinline__ void load_u64(const EncodeArgs& a, int64_t row0, int blk, int n, int g,
-                                         u32x4 (&uh)[4][2], u32x4 (&um)[4][2], u32x4 (&ul)[4][2]) {
+                                         u32x4 (&uh)[4][2], u32x4 (&um)[4][2], u32x4 (&ul)[4][2], float (&en)[4]) {
   constexpr int C = 64;
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) {
     const int64_t row = row0 + 16 * nb + n;
     const bool valid = row < a.rows;
     const int64_t rr = valid ? row : a.rows - 1;
+    float e = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const int jc = 32 * ks + 8 * g;
       const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
       float u[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float r = load_w_any2(a.W, a.w_dtype, base + e) - a.W0[base + e];
-        const float dj = PE ? a.d[base + e] : a.d[(int64_t)blk * C + jc + e];
-        u[e] = valid ? dj * r : 0.0f;
+      for (int k = 0; k < 8; ++k) {
+        const float r = load_w_any2(a.W, a.w_dtype, base + k) - a.W0[base + k];
+        const float dj = a.d[(int64_t)blk * C + jc + k];
+        u[k] = valid ? dj * r : 0.0f;
+        e = fmaf(dj * r, r, e);
       }
       split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
     }
+    e += __shfl_xor(e, 16, 64);
+    en[nb] = e + __shfl_xor(e, 32, 64);
   }
 }
 
@@ -207,7 +212,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   const int sh = g >> 1;        // the seed of each pair this lane scores
   const int nb0 = 2 * (g & 1);  // its tiles: 16 nb0 + n and 16 (nb0 + 1) + n
   u32x4 uh[4][2], um[4][2], ul[4][2];
-  load_u64<false>(a, tk.row0, blk, n, g, uh, um, ul);
+  float en[4];
+  load_u64(a, tk.row0, blk, n, g, uh, um, ul, en);
   const int64_t trow0 = tk.row0 + 16 * nb0 + n;
   const bool tv[2] = {trow0 < a.rows, trow0 + 16 < a.rows};
   const float qmax = (float)((1 << (a.b - 1)) - 1);
@@ -276,26 +282,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   // percent wider, far above the fp32 rounding of either, and the wide
   // window when the best is flagged as a knife edge; in raw units the energy
   // term is 64 times larger.  Lists change only in scoring rounds.
-  float e_raw[2];
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int64_t rr = tv[t] ? trow0 + 16 * t : a.rows - 1;
-    const int64_t o = rr * a.cols + (int64_t)blk * C;
-    float e = 0.0f;
-#pragma unroll
-    for (int j0 = 0; j0 < C; j0 += 8) {
-      float w[8], w0[8], dj[8];
-      load8_w(a.W, a.w_dtype, o + j0, w);
-      load8_f(a.W0 + o + j0, w0);
-      load8_f(a.d + (int64_t)blk * C + j0, dj);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float r = w[k] - w0[k];
-        e = fmaf(dj[k] * r, r, e);
-      }
-    }
-    e_raw[t] = 64.0f * e;
-  }
+  const float e_raw[2] = {64.0f * en[nb0], 64.0f * en[nb0 + 1]};
   float thr[2] = {-INFINITY, -INFINITY};
   auto update_thr = [&]() {
 #pragma unroll

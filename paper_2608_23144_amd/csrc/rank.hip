@@ -529,14 +529,127 @@ __global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__
   else out[pos] = x;
 }
 
+// ---------------------------------------------------------------- radix sort of large survivor sets
+// Least-significant-digit radix sort on the 64-bit key, 8-bit digits, eight
+// stable passes (the items enter in tile order, so equal keys keep
+// increasing tiles, the same total order as the merge path).  A pass is a
+// block histogram (kRsItems items per block), a scan per digit over the
+// blocks, and a scatter in which every block places its items in index
+// order: within a wavefront by matching digits with ballots, across the
+// block's four wavefronts and its rounds through LDS counters.  The last
+// pass packs the records instead of writing items.
+constexpr int kRsBits = 8;
+constexpr int kRsBins = 1 << kRsBits;
+constexpr int kRsThreads = 256;
+constexpr int kRsRounds = 16;
+constexpr int kRsItems = kRsThreads * kRsRounds;
+constexpr int64_t kRadixMin = int64_t(1) << 20;  // record caps above this use the radix sort
+
+__global__ __launch_bounds__(kRsThreads) void k_rs_hist(const SortItem* __restrict__ in, const uint64_t* state,
+                                                        int shift, uint32_t* __restrict__ hist, int nblk) {
+  __shared__ uint32_t h[kRsBins];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t n = (int64_t)state[kSegK];
+  const int64_t base = (int64_t)blockIdx.x * kRsItems;
+  for (int r = 0; r < kRsRounds; ++r) {
+    const int64_t i = base + r * kRsThreads + threadIdx.x;
+    if (i < n) atomicAdd(&h[(uint32_t)(in[i].key >> shift) & (kRsBins - 1)], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
+}
+
+// One block per digit: exclusive scan of the digit's counts over the blocks
+// (in place), and the digit's total.
+__global__ __launch_bounds__(1024) void k_rs_scan(uint32_t* __restrict__ hist, int nblk, uint32_t* __restrict__ tot) {
+  __shared__ uint64_t s_wave[16];
+  uint32_t* row = hist + (int64_t)blockIdx.x * nblk;
+  uint64_t carry = 0;
+  for (int c0 = 0; c0 < nblk; c0 += 1024) {
+    const int i = c0 + threadIdx.x;
+    const uint64_t v = i < nblk ? row[i] : 0;
+    uint64_t t;
+    const uint64_t incl = scan1024(v, s_wave, &t);
+    if (i < nblk) row[i] = (uint32_t)(carry + incl - v);
+    carry += t;
+  }
+  if (threadIdx.x == 0) tot[blockIdx.x] = (uint32_t)carry;
+}
+
+__global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __restrict__ in, SortItem* __restrict__ out,
+                                                           uint64_t* state, int shift,
+                                                           const uint32_t* __restrict__ hist, int nblk,
+                                                           const uint32_t* __restrict__ tot, int pack, PackArgs pa) {
+  __shared__ uint32_t dbase[kRsBins];         // first slot of each digit for this block
+  __shared__ uint32_t wc[kRsThreads / 64][kRsBins];  // items per digit of each wavefront in the round
+  __shared__ uint64_t s_wave[kRsThreads / 64];
+  const int64_t n = (int64_t)state[kSegK];
+  const int64_t base = (int64_t)blockIdx.x * kRsItems;
+  if (base >= n) return;  // uniform per block
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  {
+    // digit bases: exclusive scan of the 256 totals, plus this block's prefix
+    const uint32_t v = tot[t];
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_wave[w] = x;
+    __syncthreads();
+    uint32_t before = 0;
+#pragma unroll
+    for (int k = 0; k < kRsThreads / 64; ++k) before += k < w ? (uint32_t)s_wave[k] : 0u;
+    dbase[t] = before + x - v + hist[(int64_t)t * nblk + blockIdx.x];
+  }
+  const uint64_t lt = lanemask_lt();
+  for (int r = 0; r < kRsRounds; ++r) {
+#pragma unroll
+    for (int k = 0; k < kRsThreads / 64; ++k) wc[k][t] = 0;
+    __syncthreads();
+    const int64_t i = base + r * kRsThreads + t;
+    const bool valid = i < n;
+    SortItem x;
+    x.key = 0; x.tile = 0; x.pad = 0;
+    if (valid) x = in[i];
+    const uint32_t d = (uint32_t)(x.key >> shift) & (kRsBins - 1);
+    // lanes of this wavefront holding the same digit
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < kRsBits; ++b) {
+      const uint64_t bal = __ballot((d >> b) & 1u);
+      same &= ((d >> b) & 1u) ? bal : ~bal;
+    }
+    const uint32_t rank = (uint32_t)__popcll(same & lt);
+    if (valid && rank == 0) wc[w][d] = (uint32_t)__popcll(same);
+    __syncthreads();
+    if (valid) {
+      uint32_t off = dbase[d] + rank;
+#pragma unroll
+      for (int k = 0; k < kRsThreads / 64; ++k) off += k < w ? wc[k][d] : 0u;
+      if (pack) pack_record(pa, state, (int64_t)off, x.tile);
+      else out[off] = x;
+    }
+    __syncthreads();
+    uint32_t add = 0;
+#pragma unroll
+    for (int k = 0; k < kRsThreads / 64; ++k) add += wc[k][t];
+    dbase[t] += add;
+  }
+}
+
 // ---------------------------------------------------------------- workspace
 size_t rank_ws_bytes(size_t n_tiles, size_t k_cap) {
   const size_t cap = k_cap ? k_cap : 1;
   const size_t max_blocks = (n_tiles + kItems - 1) / kItems + 1;
+  const size_t rs_blocks = (cap + kRsItems - 1) / kRsItems;
   size_t b = 0;
   b += align_up(cap * sizeof(SortItem), 256) * 2;
   b += align_up((max_blocks + 1) * 8, 256) * 2;
   b += align_up((size_t)kStateWords * 8, 256);
+  b += align_up(rs_blocks * kRsBins * 4, 256) + align_up(kRsBins * 4, 256);
   return b;
 }
 
@@ -549,7 +662,10 @@ RankWs carve_rank(void* base, size_t n_tiles, size_t k_cap) {
   w.items_b = reinterpret_cast<SortItem*>(p); p += align_up(cap * sizeof(SortItem), 256);
   w.blk_a = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
   w.blk_b = reinterpret_cast<uint64_t*>(p); p += align_up((max_blocks + 1) * 8, 256);
-  w.state = reinterpret_cast<uint64_t*>(p);
+  w.state = reinterpret_cast<uint64_t*>(p); p += align_up((size_t)kStateWords * 8, 256);
+  w.rs_nblk = (cap + kRsItems - 1) / kRsItems;
+  w.rs_hist = reinterpret_cast<uint32_t*>(p); p += align_up(w.rs_nblk * kRsBins * 4, 256);
+  w.rs_tot = reinterpret_cast<uint32_t*>(p);
   w.cap = cap;
   w.max_blocks = max_blocks;
   return w;
@@ -595,6 +711,22 @@ hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_
   // sort the survivors ascending on (~key, tile): LDS chunks, then multiway
   // merges; the final pass packs the records instead of writing items
   const PackArgs pa{seed, code, scale, P, b, idx_bits, seed_bits, scale_bits, L, h, stream_cap, stream_out};
+  if (cap > kRadixMin) {
+    const int nblk = (int)ws.rs_nblk;
+    SortItem* in = ws.items_a;
+    SortItem* out = ws.items_b;
+    for (int pass = 0; pass < 64 / kRsBits; ++pass) {
+      const int shift = pass * kRsBits;
+      const int last = pass == 64 / kRsBits - 1 ? 1 : 0;
+      hipLaunchKernelGGL(k_rs_hist, dim3((unsigned)nblk), dim3(kRsThreads), 0, st, in, ws.state, shift, ws.rs_hist,
+                         nblk);
+      hipLaunchKernelGGL(k_rs_scan, dim3(kRsBins), dim3(1024), 0, st, ws.rs_hist, nblk, ws.rs_tot);
+      hipLaunchKernelGGL(k_rs_scatter, dim3((unsigned)nblk), dim3(kRsThreads), 0, st, in, out, ws.state, shift,
+                         ws.rs_hist, nblk, ws.rs_tot, last, pa);
+      SortItem* tt = in; in = out; out = tt;
+    }
+    return hipGetLastError();
+  }
   int passes = 0;
   for (int logw = kLogChunk; ((int64_t)1 << logw) < cap; logw += cap <= ((int64_t)4 << logw) ? 2 : kLogFan) ++passes;
   hipLaunchKernelGGL(k_sort_chunks, dim3((unsigned)((cap + kChunk - 1) / kChunk)), dim3(kChunkThreads), 0, st,
