@@ -156,18 +156,19 @@ __global__ void k_pe_colsh(BasisTables bt, int P, int S, int n_rows, uint32_t* _
   colsh[i] = (s < S && p < P) ? ((uint32_t)bt.col[(size_t)s * kMaxP + p] << 7) : 0u;
 }
 
+// three wavefronts per SIMD (at most 168 VGPRs; the LDS allows twelve per CU)
 template <bool POW2, bool FULLP>
-__global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEntry* __restrict__ mods, int n_mods,
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_screen_pe32(EncodeArgs a, const ModEntry* __restrict__ mods, int n_mods,
                                                        const u32x4* __restrict__ frag,
                                                        const u32x4* __restrict__ colsh) {
   constexpr int C = kC, PB = kPB, NT = kNT;
   constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
   constexpr int NL = PB * (PB - 1) / 2;
-  constexpr int QD = 2;       // queue slots per lane (a power of two): 12.6 KB of LDS, three wavefronts per SIMD
-  constexpr int QW = PB + 1;  // words per entry: w, then the seed
+  constexpr int QC = 128;     // slots of the wavefront's queue: 12.8 KB of LDS in all, three wavefronts per SIMD
+  constexpr int QW = PB + 1;  // words per entry: w, then the seed | owner lane << 24
   constexpr float kSlack = 1.001953125f;
   __shared__ float wdl[C * NT];            // WHT(d_t) / C, [coordinate][tile]
-  __shared__ float qb[QD * QW * 64];       // queues, [slot][word][lane]
+  __shared__ float qb[QW * QC];            // the queue, [word][slot]
   const int lane = threadIdx.x;
   const int64_t item = blockIdx.x;
   const int m = find_module(mods, n_mods, item);
@@ -249,32 +250,65 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     const bool edge = ((tg0 >= og ? ts0 : ow) & kEdge) != 0;
     thr = best - 1.01f * rescore_window(best, e_raw, edge);
   };
-  int qhead = 0, qtail = 0, qlen = 0;
+  // The survivors of the bound wait in one queue for the whole wavefront,
+  // appended in step order (so each lane's own entries are in seed order);
+  // a scoring round takes the 64 oldest (or, at the end, all that are left),
+  // one per lane, and each owner lane then inserts its results into its
+  // lists in queue order.  qhead and qtail are wavefront-uniform counters.
+  int qhead = 0, qtail = 0;
   int nscored = 0;
-  auto score_round = [&]() {
-    if (qlen > 0) {
-      const float* e = &qb[qhead * (QW * 64) + lane];
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;  // lanes below this one
+  const float lam = (float)a.lambda;
+  auto score_round = [&](int cnt) {
+    const bool mine = lane < cnt;
+    const int slot = (qhead + lane) & (QC - 1);
+    int ol = 0;
+    if (mine) {
       float wv[PB];
 #pragma unroll
-      for (int i = 0; i < PB; ++i) wv[i] = e[i * 64];
-      const int s = __float_as_int(e[PB * 64]);
+      for (int i = 0; i < PB; ++i) wv[i] = qb[i * QC + slot];
+      const uint32_t word = __float_as_uint(qb[PB * QC + slot]);
+      const int es = (int)(word & 0xFFFFu);
+      ol = (int)(word >> 24);
+      const int et = ol & 31;  // the entry's tile
+      const float ed0 = wdl[et];
       uint32_t cs[PB];
-      unpack_cols<PB>(colsh[2 * (size_t)s], colsh[2 * (size_t)s + 1], cs);
+      unpack_cols<PB>(colsh[2 * (size_t)es], colsh[2 * (size_t)es + 1], cs);
       float gr[NL], f[NF];
-      gather_pe<PB>(wdl, cs, tl4, gr);
-      factor_pe<PB, FULLP>(gr, d0, eps, P, f);
+      gather_pe<PB>(wdl, cs, 4u * (uint32_t)et, gr);
+      factor_pe<PB, FULLP>(gr, ed0, lam * ed0, P, f);
       bool edge;
       const float gsc = screen_gain_w<PB, POW2, 3>(wv, f, qmax, inv_qmax, &edge);
-      const uint32_t sw = (uint32_t)s | (edge ? kEdge : 0u);
-      const bool c0 = gsc > tg0, c1 = gsc > tg1;
-      tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
-      ts1 = c0 ? ts0 : (c1 ? sw : ts1);
-      tg0 = c0 ? gsc : tg0;
-      ts0 = c0 ? sw : ts0;
-      qhead = (qhead + 1) & (QD - 1);
-      --qlen;
-      ++nscored;
+      qb[slot] = gsc;
+      qb[QC + slot] = __uint_as_float((uint32_t)es | (edge ? kEdge : 0u));
     }
+    // the round's lanes whose entry this lane owns, found by matching the
+    // owner's six bits across the wavefront
+    uint64_t mm = __ballot(mine);
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+      const uint64_t bal = __ballot((ol >> b) & 1);
+      mm &= ((lane >> b) & 1) ? bal : ~bal;
+    }
+    nscored += __popcll(mm);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    while (__ballot(mm != 0) != 0) {
+      if (mm != 0) {
+        const int r = (qhead + __builtin_ctzll(mm)) & (QC - 1);
+        const float gsc = qb[r];
+        const uint32_t sw = __float_as_uint(qb[QC + r]);
+        const bool c0 = gsc > tg0, c1 = gsc > tg1;
+        tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
+        ts1 = c0 ? ts0 : (c1 ? sw : ts1);
+        tg0 = c0 ? gsc : tg0;
+        ts0 = c0 ? sw : ts0;
+        mm &= mm - 1;
+      }
+    }
+    qhead += cnt;
+    update_thr();
   };
 
   // Raw units: b is left unscaled by 1/sqrt(C) = 1/8, so the bound, alpha,
@@ -321,26 +355,25 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     float wv[PB];
     const float bnd = screen_fwd<PB>(bt, f, wv);
     const bool keep = (int)(bnd * kSlack > thr) & (int)valid & (int)(s < a.S);
-    // stored unconditionally at the tail (a dropped candidate is overwritten
-    // by the next), kept by advancing it
-    float* e = &qb[qtail * (QW * 64) + lane];
+    // Every lane stores its candidate, the kept ones first (in lane order)
+    // from the tail on, the dropped ones after them; only the kept ones are
+    // taken in by advancing the tail.  At most 63 entries wait before a
+    // step, so the 64 slots written are free.
+    const uint64_t kb = __ballot(keep);
+    const int nk = __popcll(kb);
+    const int pos = keep ? __popcll(kb & lt) : nk + __popcll(~kb & lt);
+    const int slot = (qtail + pos) & (QC - 1);
 #pragma unroll
-    for (int i = 0; i < PB; ++i) e[i * 64] = wv[i];
-    e[PB * 64] = __int_as_float(s);
-    qlen += keep ? 1 : 0;
-    qtail = keep ? ((qtail + 1) & (QD - 1)) : qtail;
+    for (int i = 0; i < PB; ++i) qb[i * QC + slot] = wv[i];
+    qb[PB * QC + slot] = __uint_as_float((uint32_t)s | ((uint32_t)lane << 24));
+    qtail += nk;
 #pragma unroll
     for (int i = 0; i < 12; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
     }
-    // a full ring has no room for the next pair's entry
-    if (__ballot(qlen == QD) != 0) {
-      do {
-        score_round();
-      } while (__ballot(qlen == QD) != 0);
-      update_thr();
-    }
+    // a full round's worth waiting: score the 64 oldest
+    if (qtail - qhead >= 64) score_round(64);
   };
   int pair = 0;
   for (; pair + 1 < n_pairs; pair += 2) {
@@ -348,7 +381,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_pe32(EncodeArgs a, const ModEn
     step(pair + 1, accB, accA, FB0, FB1, FA0, FA1, CB0, CB1, CA0, CA1);
   }
   if (pair < n_pairs) step(pair, accA, accB, FA0, FA1, FB0, FB1, CA0, CA1, CB0, CB1);
-  while (__ballot(qlen > 0) != 0) score_round();
+  if (qtail > qhead) score_round(qtail - qhead);
 #pragma unroll
   for (int k = 32; k >= 1; k >>= 1) nscored += __shfl_xor(nscored, k, 64);
   if (lane == 0) atomicAdd(a.scored, (unsigned long long)nscored);
