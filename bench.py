@@ -59,7 +59,8 @@ MEASURED_TRAFFIC = {
         "files": ["awsrc_internal.h", "decode.hip"],
         "sha256": "057b327e7fba35e628bae904c069085ca5b059d365549ba26d800a9201b58c27",
         "bytes": 5037000000},
-    # the whole reconstruction call: tile ordering (scans, copy) and the streaming pass
+    # the whole reconstruction call (tile ordering, the streaming pass) of one
+    # 0.32 bpw stack3b stream (measured on the single-prefix call)
     ("reconstruct_bf16", "stack3b@0.32"): {
         "files": ["awsrc_internal.h", "decode.hip"],
         "sha256": "057b327e7fba35e628bae904c069085ca5b059d365549ba26d800a9201b58c27",
@@ -257,7 +258,7 @@ class Run:
     (storage dtype) and d, the backbone (codes, scales, zero points, fp32 W0),
     the encoder's outputs concatenated in module order with its workspace (one
     awsrc_encode_modules call encodes every module), and bf16 buffers for the
-    dense reconstructions."""
+    dense reconstructions (one set per budget)."""
 
     def __init__(self, awsrc, torch, wl, gen_version: int, dev, sample_step: int = 0):
         from synth import gen_module_inputs
@@ -296,7 +297,10 @@ class Run:
         self.W_list = [inp["W"] for inp in self.inputs]
         self.d_list = [inp["d"] for inp in self.inputs]
         self.W0_list = [b[3] for b in self.bb]
-        self.outs = [torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in self.shapes]
+        # one set of dense bf16 targets per budget (the nested prefixes are
+        # reconstructed in one pass)
+        self.outs = [[torch.empty(r, c, dtype=torch.bfloat16, device=dev) for r, c in self.shapes]
+                     for _ in wl.budgets]
         self.mode = awsrc.AWSRC_MODE_GLOBAL if wl.mode == "global" else awsrc.AWSRC_MODE_PER_MODULE
         self.L = awsrc.awsrc_record_bytes(self.p, T)
         self.h = awsrc.awsrc_header_bytes(len(self.shapes))
@@ -311,8 +315,9 @@ def run_steps(awsrc, torch, run: Run, steps: int, warmup: int):
     every module; encoder seed search of every module; one ranking at the
     largest budget; decode-add of that stream in place onto the fp32 W0
     (prepare = validation and tables, apply = the add); then every budget's
-    record-boundary prefix of the same stream decoded without re-encoding into
-    dense bf16 repaired weights (prepare + reconstruction per prefix).  Stage
+    record-boundary prefix of the same validated stream decoded without
+    re-encoding into dense bf16 repaired weights, one target set per budget,
+    all in one reconstruction pass over the backbone.  Stage
     times come from HIP events on the library's stream; the step time is the
     host wall clock of exactly the timed steps."""
     wl = run.wl
@@ -338,17 +343,17 @@ def run_steps(awsrc, torch, run: Run, steps: int, warmup: int):
         awsrc.awsrc_decode_apply(plan)
         ev[5].record(stream)
         prefixes = []
-        rcws = last.get("rcws")
         for bpw in sorted(wl.budgets):
             if run.mode == awsrc.AWSRC_MODE_GLOBAL:
                 kb = min(ne, (awsrc.awsrc_budget_bytes(bpw, N) - run.h) // run.L)
             else:
                 kb = K
-            plan_b, rcws = awsrc.awsrc_decode_prepare(s, run.outs, stream_len=run.h + kb * run.L, workspace=rcws)
-            awsrc.awsrc_reconstruct_bf16(plan_b, [b[:3] for b in run.bb], 128)
             prefixes.append((bpw, kb))
+        # every budget's prefix of the one validated stream, dense bf16, in one pass
+        awsrc.awsrc_reconstruct_bf16_prefixes(plan, [kb for _, kb in prefixes], run.outs,
+                                              [b[:3] for b in run.bb], 128)
         ev[6].record(stream)
-        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), dws=dws, rcws=rcws, prefixes=prefixes)
+        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), dws=dws, prefixes=prefixes)
         if record:
             torch.cuda.synchronize()
             for k, (a, b) in zip(STAGES, zip(ev[:-1], ev[1:])):
@@ -414,9 +419,11 @@ def workload_result(awsrc, run: Run, ms_step: float, stage_ms: dict, gen_version
     n_groups = n_w // 128
     bb_bytes = n_w * (2 if wl.w_dtype == "bf16" else 4) + n_w // 2 + 3 * n_groups + 4 * n_w
     bb_gbs = bb_bytes / (stage_ms["backbone"] / 1e3) / 1e9
-    # dense reconstructions: per prefix, codes 1/2 B and bf16 output 2 B per
-    # weight, scale and zero 3 B per group, plus the prefix's records
-    rc_bytes = sum(n_w // 2 + 3 * n_groups + 2 * n_w + kb * L for _, kb in last["prefixes"])
+    # dense reconstruction of every prefix in one pass: codes 1/2 B per weight
+    # and scale and zero 3 B per group read once, bf16 output 2 B per weight
+    # and prefix, the longest prefix's records
+    n_pref = len(last["prefixes"])
+    rc_bytes = n_w // 2 + 3 * n_groups + n_pref * 2 * n_w + max(kb for _, kb in last["prefixes"]) * L
     rc_gbs = rc_bytes / (stage_ms["reconstruct"] / 1e3) / 1e9
     enc_s = stage_ms["encode"] / 1e3
     return {

@@ -400,6 +400,32 @@ awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group
                                     const uint8_t* const* codes, const uint16_t* const* scale_f16,
                                     const uint8_t* const* zero, void* stream);
 
+/*
+ * Dense bf16 repaired weights of several nested prefixes of one stream in one
+ * streaming pass (Sec. 3.3: every record-boundary prefix of a ranked stream
+ * decodes without refitting; Sec. 4 evaluates each operating point as dense
+ * BF16 weights): target o receives W_hat = bf16(W0 + R_hat) with R_hat the
+ * correction of the stream's first K_out[o] records only.  The backbone and
+ * each record's correction are computed once per pass and written to every
+ * target; the result is the same as awsrc_reconstruct_bf16 of each prefix.
+ *  plan       prepared by awsrc_decode_prepare on the longest stream (any
+ *             w0_dtype: its own W0 buffers are not touched).
+ *  n_out      number of targets, 1..8.
+ *  K_out      host array [n_out]: records per target, each 0..plan->K (any
+ *             order; equal values are allowed).
+ *  out_ptrs   host array [n_out * n_modules] of device pointers, target o of
+ *             module m at o * n_modules + m: bf16 [rows, cols], 16-byte
+ *             aligned, every element written, never read; targets must not
+ *             overlap.
+ *  group, codes, scale_f16, zero   as for awsrc_reconstruct_bf16.
+ * Synchronizes once (module table read-back) before launching; EINVAL on a
+ * bad argument (nothing launched).
+ */
+awsrc_status awsrc_reconstruct_bf16_prefixes(const awsrc_decode_plan* plan, int32_t n_out, const int64_t* K_out,
+                                             void* const* out_ptrs, int32_t group, const uint8_t* const* codes,
+                                             const uint16_t* const* scale_f16, const uint8_t* const* zero,
+                                             void* stream);
+
 /* Host-only helpers (no device needed). */
 /* L_rec in bytes for T_total tiles; -1 if p is invalid. */
 int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total);

@@ -28,7 +28,7 @@ EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsr
             "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
             "awsrc_encode_modules", "awsrc_encode_screen_lists", "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
-            "awsrc_reconstruct_bf16", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
+            "awsrc_reconstruct_bf16", "awsrc_reconstruct_bf16_prefixes", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
 
 class AwsrcError(RuntimeError):
@@ -86,6 +86,9 @@ def _load() -> ctypes.CDLL:
         "awsrc_decode_apply": (i32, [ctypes.POINTER(awsrc_decode_plan), vp]),
         "awsrc_reconstruct_bf16": (i32, [ctypes.POINTER(awsrc_decode_plan), i32, ctypes.POINTER(vp),
                                          ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
+        "awsrc_reconstruct_bf16_prefixes": (i32, [ctypes.POINTER(awsrc_decode_plan), i32, P64, ctypes.POINTER(vp),
+                                                  i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                                  vp]),
         "awsrc_record_bytes": (i64, [pp, i64]),
         "awsrc_header_bytes": (i64, [i32]),
         "awsrc_budget_bytes": (i64, [ctypes.c_double, i64]),
@@ -442,3 +445,24 @@ def awsrc_reconstruct_bf16(plan: awsrc_decode_plan, backbones: Sequence[Tuple[to
         _dev(*bb)
     arr = [(ctypes.c_void_p * len(backbones))(*[bb[k].data_ptr() for bb in backbones]) for k in range(3)]
     _check(LIB.awsrc_reconstruct_bf16(ctypes.byref(plan), group, arr[0], arr[1], arr[2], _stream(stream)))
+
+
+def awsrc_reconstruct_bf16_prefixes(plan: awsrc_decode_plan, K_out: Sequence[int],
+                                    outs: Sequence[Sequence[torch.Tensor]],
+                                    backbones: Sequence[Tuple[torch.Tensor, torch.Tensor, torch.Tensor]],
+                                    group: int = 128, stream=None) -> None:
+    """Dense bf16(W0 + R_hat of the first K_out[o] records) into outs[o] (one
+    bf16 tensor per module) for every o, in one pass over the backbone."""
+    n = plan.n_modules
+    if len(backbones) != n or len(outs) != len(K_out) or any(len(o) != n for o in outs):
+        raise ValueError("need one backbone and, per prefix, one target per module")
+    for bb in backbones:
+        _dev(*bb)
+    for o in outs:
+        _dev(*o)
+        if any(t.dtype != torch.bfloat16 for t in o):
+            raise TypeError("targets must be bf16")
+    arr = [(ctypes.c_void_p * n)(*[bb[k].data_ptr() for bb in backbones]) for k in range(3)]
+    optr = (ctypes.c_void_p * (n * len(outs)))(*[t.data_ptr() for o in outs for t in o])
+    _check(LIB.awsrc_reconstruct_bf16_prefixes(ctypes.byref(plan), len(K_out), _i64arr(list(K_out)), optr, group,
+                                               arr[0], arr[1], arr[2], _stream(stream)))

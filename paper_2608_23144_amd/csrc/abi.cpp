@@ -588,7 +588,7 @@ namespace {
 // (tile offsets [n+1], cols [n] and W0 pointers [n], contiguous so that one
 // host-to-device copy fills them) | decoded records [K] x 32 B | for the bf16
 // reconstruction: the records in tile order [K + 1] x 32 B, the prefix-count
-// scan scratch, backbone pointer tables [3n].
+// scan scratch, backbone and target pointer tables [3n + 8n].
 struct DecodeLayout {
   size_t basis, bitmap, err, tables, dec, dec_t, bsum, bbtab, total;
 };
@@ -603,7 +603,7 @@ DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_
   l.dec_t = align_up((size_t)(K + 1) * 32, 256);  // entry 0 is readable even when K = 0
   const size_t nwords = (size_t)((T_total + 31) / 32);
   l.bsum = align_up(((nwords + 4095) / 4096) * 4, 256);
-  l.bbtab = align_up((size_t)3 * nmod * 8, 256);
+  l.bbtab = align_up((size_t)(3 + kMaxPrefixOutputs) * nmod * 8, 256);
   l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.dec_t + l.bsum + l.bbtab;
   return l;
 }
@@ -732,17 +732,28 @@ extern "C" awsrc_status awsrc_decode_apply(const awsrc_decode_plan* plan, void* 
   return AWSRC_OK;
 }
 
-extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group,
-                                               const uint8_t* const* codes, const uint16_t* const* scale_f16,
-                                               const uint8_t* const* zero, void* stream) {
+namespace {
+
+// The dense reconstruction of awsrc_reconstruct_bf16 (n_out == 0, the plan's
+// targets) and awsrc_reconstruct_bf16_prefixes (n_out targets of nested
+// prefixes).
+awsrc_status reconstruct(const awsrc_decode_plan* plan, int32_t n_out, const int64_t* K_out, void* const* out_ptrs,
+                         int32_t group, const uint8_t* const* codes, const uint16_t* const* scale_f16,
+                         const uint8_t* const* zero, void* stream) {
   if (!plan || !plan->workspace) return fail(AWSRC_EINVAL, "plan is NULL or not prepared");
-  if (plan->w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "the plan's targets must be bf16");
+  if (n_out == 0 && plan->w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "the plan's targets must be bf16");
   if (group != 64 && group != 128 && group != 256) return fail(AWSRC_EINVAL, "group=%d: must be 64, 128 or 256", group);
   if (plan->C < 16) return fail(AWSRC_EINVAL, "C=%d: the reconstruction needs C >= 16", plan->C);
   if (!codes || !scale_f16 || !zero) return fail(AWSRC_EINVAL, "backbone pointer arrays are NULL");
   const uint32_t n = (uint32_t)plan->n_modules;
+  uint32_t kout[kMaxPrefixOutputs] = {};
+  for (int o = 0; o < n_out; ++o) {
+    if (K_out[o] < 0 || K_out[o] > plan->K)
+      return fail(AWSRC_EINVAL, "prefix %d: K=%lld outside 0..%lld", o, (long long)K_out[o], (long long)plan->K);
+    kout[o] = (uint32_t)K_out[o];
+  }
   const DecodeArgs a = decode_args(plan);
-  std::vector<uint64_t> tabs(3 * (size_t)n);
+  std::vector<uint64_t> tabs((3 + (size_t)n_out) * n);
   for (uint32_t m = 0; m < n; ++m) {
     if (!codes[m] || !scale_f16[m] || !zero[m]) return fail(AWSRC_EINVAL, "backbone pointer of module %u is NULL", m);
     if (reinterpret_cast<uintptr_t>(codes[m]) & 7) return fail(AWSRC_EINVAL, "codes of module %u must be 8-byte aligned", m);
@@ -750,6 +761,12 @@ extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, in
     tabs[m] = reinterpret_cast<uint64_t>(codes[m]);
     tabs[n + m] = reinterpret_cast<uint64_t>(scale_f16[m]);
     tabs[2 * n + m] = reinterpret_cast<uint64_t>(zero[m]);
+    for (int o = 0; o < n_out; ++o) {
+      const void* q = out_ptrs[(size_t)o * n + m];
+      if (!q) return fail(AWSRC_EINVAL, "target %d of module %u is NULL", o, m);
+      if (reinterpret_cast<uintptr_t>(q) & 15) return fail(AWSRC_EINVAL, "target %d of module %u must be 16-byte aligned", o, m);
+      tabs[(3 + (size_t)o) * n + m] = reinterpret_cast<uint64_t>(q);
+    }
   }
   // stage the backbone pointers and read back the module tables (tile
   // offsets [n+1] then cols [n]); the one synchronization covers both copies
@@ -771,8 +788,25 @@ extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, in
   BackboneTabs bb;
   bb.ptr = bbt;
   bb.gshift = group == 64 ? 6 : group == 128 ? 7 : 8;
-  HIPCHK(launch_reconstruct_bf16(a, bb, mt.data(), s));
+  HIPCHK(launch_reconstruct_bf16(a, bb, mt.data(), n_out, kout, s));
   return AWSRC_OK;
+}
+
+}  // namespace
+
+extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group,
+                                               const uint8_t* const* codes, const uint16_t* const* scale_f16,
+                                               const uint8_t* const* zero, void* stream) {
+  return reconstruct(plan, 0, nullptr, nullptr, group, codes, scale_f16, zero, stream);
+}
+
+extern "C" awsrc_status awsrc_reconstruct_bf16_prefixes(const awsrc_decode_plan* plan, int32_t n_out,
+                                                        const int64_t* K_out, void* const* out_ptrs, int32_t group,
+                                                        const uint8_t* const* codes, const uint16_t* const* scale_f16,
+                                                        const uint8_t* const* zero, void* stream) {
+  if (n_out < 1 || n_out > kMaxPrefixOutputs) return fail(AWSRC_EINVAL, "n_out=%d: must be 1..%d", n_out, kMaxPrefixOutputs);
+  if (!K_out || !out_ptrs) return fail(AWSRC_EINVAL, "K_out or out_ptrs is NULL");
+  return reconstruct(plan, n_out, K_out, out_ptrs, group, codes, scale_f16, zero, stream);
 }
 
 extern "C" awsrc_status awsrc_decode_add(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,

@@ -414,9 +414,13 @@ struct BackboneTabs {
   const uint64_t* ptr;
   int gshift;  // log2 of the backbone group
 };
-// Dense bf16 reconstruction into the plan's (bf16) module buffers; toff is a
-// host copy of the tile offsets (one launch per window of modules).
-hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff,
-                                   hipStream_t st);
+// Dense bf16 reconstruction; toff is a host copy of the tile offsets (one
+// launch per window of modules).  n_out == 0: into the plan's (bf16) module
+// buffers with every record; else into n_out targets whose module pointer
+// rows follow the backbone's in bb.ptr, target o with the records whose
+// place in the stream is below K_out[o].
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, int n_out,
+                                   const uint32_t* K_out, hipStream_t st);
+constexpr int kMaxPrefixOutputs = 8;  // targets of one awsrc_reconstruct_bf16_prefixes call
 
 }  // namespace awsrc

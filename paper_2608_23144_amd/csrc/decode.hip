@@ -226,7 +226,10 @@ __global__ void k_decode_tile_order(DecodeArgs a) {
   const uint4 e0 = a.dec[2 * i];
   const uint4 e1 = a.dec[2 * i + 1];
   const uint32_t k = tile_rank(a, a.mod_tile_off[e0.y] + e0.x);
-  a.dec_t[2 * (size_t)k] = e0;
+  // the tile-ordered copy carries the record's place in the stream in its
+  // first word (the tile is implied by the position), for the nested-prefix
+  // reconstruction
+  a.dec_t[2 * (size_t)k] = make_uint4((uint32_t)i, e0.y, e0.z, e0.w);
   a.dec_t[2 * (size_t)k + 1] = e1;
 }
 
@@ -347,7 +350,8 @@ template <int NU>
 struct RecBackbone {                         // backbone words of one chunk
   UnitCodes q[NU];
   uint32_t s[NU], z[NU];
-  AWSRC_GLOBAL u32x4_t* out[NU];
+  uint32_t m[NU];                            // module (within the window) and first element of the unit
+  uint64_t el[NU];
   bool ok[NU];
 };
 template <int NU>
@@ -360,7 +364,19 @@ struct RecDec {                              // decoded record per unit (record 
   // the codes, four per word; only the words in use are loaded, so that no
   // dead part of a load destination is ever reused while the load is in flight
   typename std::conditional<(G <= 2), u32x2_t, u32x4_t>::type q[NU];
+  uint32_t rank[NU];                         // the record's place in the stream (nested prefixes)
   bool rec[NU];
+};
+
+// Outputs of one reconstruction launch: NO bf16 targets whose module pointer
+// rows follow the backbone's in the staged table (rows 3 + o0 ..); with
+// `ranked`, a record goes into output o only when its place in the stream is
+// below K[o] (nested prefixes of one stream), else into every output (the
+// plan's own targets, rows of mod_ptr).
+struct RecOut {
+  uint32_t K[4];
+  int o0;
+  int ranked;
 };
 
 // One launch covers a window of at most kLdsModules consecutive modules,
@@ -370,28 +386,32 @@ struct RecDec {                              // decoded record per unit (record 
 // [16 uw, 16 uw + 16) (rows are whole multiples of the group, hence of 16),
 // and its backbone group is element / group.  Every load is issued unconditionally (units
 // past the window end are clamped to its last unit and not stored).
-template <int C, int G, bool TS_LDS>
-__global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, BackboneTabs bb, int m0, int nm) {
+template <int C, int G, bool TS_LDS, int NO>
+__global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, BackboneTabs bb, RecOut ro, int m0,
+                                                             int nm) {
   constexpr int NT = kRecThreads, NU = kRecUnits;
   constexpr int UPT = C / kUnitW;                        // lanes per tile
   constexpr int LOG_UPT = ((C == 16) ? 4 : (C == 32) ? 5 : (C == 64) ? 6 : 7) - kLogUnitW;
   constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
                       : (C == 64) ? 0.125f : 0.08838834764831845f;
   extern __shared__ __align__(16) uint64_t s_dyn[];
-  // LDS: [tile offsets nm+1 | codes nm | scale nm | zero nm | out nm] then [S][C] sign rows
+  // LDS: [tile offsets nm+1 | codes nm | scale nm | zero nm | out NO x nm] then [S][C] sign rows
   uint64_t* s_off = s_dyn;
   uint64_t* s_cp = s_off + nm + 1;
   uint64_t* s_sp = s_cp + nm;
   uint64_t* s_zp = s_sp + nm;
   uint64_t* s_op = s_zp + nm;
-  uint16_t* s_ts = reinterpret_cast<uint16_t*>(s_dyn + ((5 * nm + 1 + 1) & ~1));
+  uint16_t* s_ts = reinterpret_cast<uint16_t*>(s_dyn + (((4 + NO) * nm + 1 + 1) & ~1));
   const uint32_t n_all = (uint32_t)a.n_modules;
   for (int i = threadIdx.x; i <= nm; i += NT) s_off[i] = a.mod_tile_off[m0 + i];
   for (int i = threadIdx.x; i < nm; i += NT) {
     s_cp[i] = bb.ptr[m0 + i];
     s_sp[i] = bb.ptr[n_all + m0 + i];
     s_zp[i] = bb.ptr[2 * n_all + m0 + i];
-    s_op[i] = reinterpret_cast<uint64_t>(a.mod_ptr[m0 + i]);
+#pragma unroll
+    for (int o = 0; o < NO; ++o)
+      s_op[o * nm + i] = ro.ranked ? bb.ptr[(3 + ro.o0 + o) * (size_t)n_all + m0 + i]
+                                   : reinterpret_cast<uint64_t>(a.mod_ptr[m0 + i]);
   }
   if constexpr (TS_LDS) {
     constexpr int PER_SEED = C / 8;                      // 16-byte pieces per seed
@@ -427,7 +447,8 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       B.q[k] = *((const AWSRC_GLOBAL UnitCodes*)s_cp[m] + (el >> kLogUnitW));
       B.s[k] = ((const AWSRC_GLOBAL uint16_t*)s_sp[m])[g];
       B.z[k] = ((const AWSRC_GLOBAL uint8_t*)s_zp[m])[g];
-      B.out[k] = (AWSRC_GLOBAL u32x4_t*)s_op[m] + (el >> 3);
+      B.m[k] = (uint32_t)m;
+      B.el[k] = el;
     }
   };
   auto issue_bits = [&](uint64_t c, RecBits<NU>& W) {
@@ -450,6 +471,7 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       const uint32_t r = D.rec[k] ? W.pre[k] + __popc(W.word[k] & ((1u << sh) - 1u)) : 0u;
       const uint32_t* dp = reinterpret_cast<const uint32_t*>(a.dec_t) + 8 * (size_t)r;
       D.sw[k] = *reinterpret_cast<const u32x2_t*>(dp + 2);
+      D.rank[k] = ro.ranked ? dp[0] : 0u;
       using QT = typename std::remove_reference<decltype(D.q[0])>::type;
       D.q[k] = *reinterpret_cast<const QT*>(dp + 4);
     }
@@ -465,6 +487,9 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
 #pragma unroll
       for (int e = 0; e < kUnitW; ++e)
         w[e] = ((float)((code_word(B.q[k], e >> 3) >> (4 * (e & 7))) & 0xFu) - z) * s;
+      float wr[kUnitW];
+#pragma unroll
+      for (int e = 0; e < kUnitW; ++e) wr[e] = w[e];
       if (D.rec[k]) {
         // rows sub*kUnitW .. of B_s: sqrt(C) rhat_j = scale (sum_p q_p - 2 sum
         // of the codes at the negative entries of row j)
@@ -499,14 +524,28 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
             const uint32_t mask = (((ts >> (4 * gg)) & 0xFu) * 0x204081u) & 0x01010101u;
             neg = __builtin_amdgcn_sdot4((int)mask, (int)q4[gg], neg, false);
           }
-          w[e] += (float)(tot - 2 * neg) * scl;
+          wr[e] = w[e] + (float)(tot - 2 * neg) * scl;
         }
       }
+      // the unit rounded with and (when it has a record) without the
+      // correction; each output takes one of the two
+      u32x4_t ob[kUnitW / 8], orc[kUnitW / 8];
 #pragma unroll
       for (int i = 0; i < kUnitW / 8; ++i) {
-        const u32x4_t o = {bf16_pair(w[8 * i], w[8 * i + 1]), bf16_pair(w[8 * i + 2], w[8 * i + 3]),
-                           bf16_pair(w[8 * i + 4], w[8 * i + 5]), bf16_pair(w[8 * i + 6], w[8 * i + 7])};
-        B.out[k][i] = o;
+        orc[i] = u32x4_t{bf16_pair(wr[8 * i], wr[8 * i + 1]), bf16_pair(wr[8 * i + 2], wr[8 * i + 3]),
+                         bf16_pair(wr[8 * i + 4], wr[8 * i + 5]), bf16_pair(wr[8 * i + 6], wr[8 * i + 7])};
+        if (ro.ranked)
+          ob[i] = u32x4_t{bf16_pair(w[8 * i], w[8 * i + 1]), bf16_pair(w[8 * i + 2], w[8 * i + 3]),
+                          bf16_pair(w[8 * i + 4], w[8 * i + 5]), bf16_pair(w[8 * i + 6], w[8 * i + 7])};
+        else
+          ob[i] = orc[i];
+      }
+#pragma unroll
+      for (int o = 0; o < NO; ++o) {
+        const bool with = !ro.ranked || (D.rec[k] && D.rank[k] < ro.K[o]);
+        AWSRC_GLOBAL u32x4_t* out = (AWSRC_GLOBAL u32x4_t*)s_op[o * nm + B.m[k]] + (B.el[k] >> 3);
+#pragma unroll
+        for (int i = 0; i < kUnitW / 8; ++i) out[i] = with ? orc[i] : ob[i];
       }
     }
   };
@@ -537,17 +576,25 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
 
 // dynamic LDS of one launch: module window table (rounded to 16 bytes) and
 // the sign rows when staged
-static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds) {
-  return (size_t)((5 * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
+static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds, int no) {
+  return (size_t)(((4 + no) * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
 }
 
-template <int C, int G, bool TS_LDS>
-static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
-  for (int m0 = 0; m0 < a.n_modules; m0 += kLdsModules) {
-    const int nm = a.n_modules - m0 < kLdsModules ? a.n_modules - m0 : kLdsModules;
-    const size_t lds = rec_lds_bytes(C, a.S, nm, TS_LDS);
+// module windows: the whole LDS table for one output; smaller windows for
+// several, so that two blocks still fit per CU with the sign rows staged
+template <int NO>
+constexpr int rec_window() { return NO == 1 ? kLdsModules : 128; }
+
+template <int C, int G, bool TS_LDS, int NO>
+static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
+                                 hipStream_t st) {
+  constexpr int WIN = rec_window<NO>();
+  for (int m0 = 0; m0 < a.n_modules; m0 += WIN) {
+    const int nm = a.n_modules - m0 < WIN ? a.n_modules - m0 : WIN;
+    const size_t lds = rec_lds_bytes(C, a.S, nm, TS_LDS, NO);
     int per_cu = 0;
-    HIP_RETURN_IF(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS>, kRecThreads, lds));
+    HIP_RETURN_IF(
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS, NO>, kRecThreads, lds));
     if (per_cu < 1) per_cu = 1;
     const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / kUnitW);
     const uint64_t chunks = (units + kRecUnits * kRecThreads - 1) / (kRecUnits * kRecThreads);
@@ -557,30 +604,45 @@ static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, co
     uint64_t nb = (uint64_t)per_cu * 256 * 4;
     if (nb > chunks) nb = chunks;
     if (nb < 1) continue;
-    hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb, m0, nm);
+    hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS, NO>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb, ro,
+                       m0, nm);
     HIP_RETURN_IF(hipGetLastError());
   }
   return hipSuccess;
 }
 
-template <int C, int G>
-static hipError_t launch_rec_cg(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
-  if ((size_t)a.S * C * 2 <= (size_t)kTsignLdsMax) return launch_rec_cgt<C, G, true>(a, bb, toff, st);
-  return launch_rec_cgt<C, G, false>(a, bb, toff, st);
+template <int C, int G, int NO>
+static hipError_t launch_rec_cgn(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
+                                 hipStream_t st) {
+  if ((size_t)a.S * C * 2 <= (size_t)kTsignLdsMax) return launch_rec_cgt<C, G, true, NO>(a, bb, ro, toff, st);
+  return launch_rec_cgt<C, G, false, NO>(a, bb, ro, toff, st);
 }
 
-template <int C>
-static hipError_t launch_rec_c(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, hipStream_t st) {
+template <int C, int NO>
+static hipError_t launch_rec_cn(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
+                                hipStream_t st) {
   switch ((a.P + 3) / 4) {
-    case 1: return launch_rec_cg<C, 1>(a, bb, toff, st);
-    case 2: return launch_rec_cg<C, 2>(a, bb, toff, st);
-    case 3: return launch_rec_cg<C, 3>(a, bb, toff, st);
-    default: return launch_rec_cg<C, 4>(a, bb, toff, st);
+    case 1: return launch_rec_cgn<C, 1, NO>(a, bb, ro, toff, st);
+    case 2: return launch_rec_cgn<C, 2, NO>(a, bb, ro, toff, st);
+    case 3: return launch_rec_cgn<C, 3, NO>(a, bb, ro, toff, st);
+    default: return launch_rec_cgn<C, 4, NO>(a, bb, ro, toff, st);
   }
 }
 
-hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff,
-                                   hipStream_t st) {
+// One pass: no == 1, or no == 4 (C >= 64 only).
+static hipError_t launch_rec_pass(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, int no,
+                                  const uint64_t* toff, hipStream_t st) {
+  switch (a.C) {
+    case 16: return launch_rec_cn<16, 1>(a, bb, ro, toff, st);
+    case 32: return launch_rec_cn<32, 1>(a, bb, ro, toff, st);
+    case 64: return no == 4 ? launch_rec_cn<64, 4>(a, bb, ro, toff, st) : launch_rec_cn<64, 1>(a, bb, ro, toff, st);
+    case 128: return no == 4 ? launch_rec_cn<128, 4>(a, bb, ro, toff, st) : launch_rec_cn<128, 1>(a, bb, ro, toff, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, int n_out,
+                                   const uint32_t* K_out, hipStream_t st) {
   if (a.K > 0) {
     // the records in tile order: prefix counts of the bitmap words, then each
     // decoded record copied to its rank
@@ -592,13 +654,20 @@ hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, 
     hipLaunchKernelGGL(k_decode_tile_order, dim3((unsigned)((a.K + 255) / 256)), dim3(256), 0, st, a);
     HIP_RETURN_IF(hipGetLastError());
   }
-  switch (a.C) {
-    case 16: return launch_rec_c<16>(a, bb, toff, st);
-    case 32: return launch_rec_c<32>(a, bb, toff, st);
-    case 64: return launch_rec_c<64>(a, bb, toff, st);
-    case 128: return launch_rec_c<128>(a, bb, toff, st);
-    default: return hipErrorInvalidValue;
+  if (n_out == 0) {  // the plan's own targets, every record
+    RecOut ro{};
+    return launch_rec_pass(a, bb, ro, 1, toff, st);
   }
+  for (int o0 = 0; o0 < n_out;) {
+    const int no = (a.C >= 64 && n_out - o0 >= 4) ? 4 : 1;
+    RecOut ro{};
+    ro.ranked = 1;
+    ro.o0 = o0;
+    for (int o = 0; o < no; ++o) ro.K[o] = K_out[o0 + o];
+    HIP_RETURN_IF(launch_rec_pass(a, bb, ro, no, toff, st));
+    o0 += no;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_decode_validate(const DecodeArgs& a, hipStream_t st) {

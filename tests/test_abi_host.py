@@ -156,6 +156,32 @@ def test_reconstruct_rejects_bad_arguments_without_device_access():
     assert f(ctypes.byref(plan), 128, arr, odd, arr, None) == awsrc.AWSRC_EINVAL  # scale alignment
 
 
+def test_reconstruct_prefixes_rejects_bad_arguments_without_device_access():
+    plan = awsrc.awsrc_decode_plan()
+    v = ctypes.c_void_p
+    arr = (v * 1)(256)
+    outs = (v * 2)(256, 512)
+    f = awsrc.LIB.awsrc_reconstruct_bf16_prefixes
+    K = (ctypes.c_int64 * 2)(0, 0)
+    assert f(ctypes.byref(plan), 2, K, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # not prepared
+    plan.workspace = 4096
+    plan.n_modules = 1
+    plan.C = 64
+    plan.K = 3
+    plan.w0_dtype = awsrc.AWSRC_DTYPE_F32  # any target dtype of the plan is accepted
+    assert f(ctypes.byref(plan), 0, K, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # no targets
+    assert f(ctypes.byref(plan), 9, K, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # too many
+    assert f(ctypes.byref(plan), 2, None, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL
+    assert f(ctypes.byref(plan), 2, K, None, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL
+    big = (ctypes.c_int64 * 2)(0, 4)
+    assert f(ctypes.byref(plan), 2, big, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # K > plan.K
+    neg = (ctypes.c_int64 * 2)(-1, 0)
+    assert f(ctypes.byref(plan), 2, neg, outs, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL
+    mis = (v * 2)(256, 520)
+    assert f(ctypes.byref(plan), 2, K, mis, 128, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # target alignment
+    assert f(ctypes.byref(plan), 2, K, outs, 96, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # group
+
+
 def test_sdq_rejects_bad_arguments_without_device_access():
     enc = awsrc.LIB.awsrc_sdq_encode
     assert enc(None, -1, None, None, None, None) == awsrc.AWSRC_EINVAL

@@ -765,6 +765,45 @@ def test_reconstruct_bf16_matches_oracle(C, P, b, S, group, mods, fmt):
     _check_reconstruct(C, stream, K, W0s, want, outs, mods)
 
 
+@pytest.mark.parametrize("C,P,b,S,group,mods,fmt", [
+    (64, 8, 4, 256, 128, [(33, 512), (8, 1024), (1, 128)], 0),
+    (128, 8, 3, 64, 128, [(9, 512)], 1),
+    (16, 4, 4, 16, 64, [(5, 128), (3, 256)], 0),
+])
+def test_reconstruct_bf16_prefixes_match_single_calls_and_oracle(C, P, b, S, group, mods, fmt):
+    """Nested prefixes of one stream reconstructed in one call (five targets:
+    a pass of four and a pass of one at C >= 64, single passes below; record
+    counts in no particular order, an empty prefix and the whole stream among
+    them) equal, bit for bit, one awsrc_reconstruct_bf16 of each prefix's own
+    stream, and the oracle's reconstruction of each prefix."""
+    stream, K, W0s, want_full, outs_full = _reconstruct_case(C, P, b, S, mods, group, 2.0, seed=9, fmt=fmt)
+    assert K > 8
+    hd = O.parse_header(stream)
+    h, L = hd["h"], hd["L_rec"]
+    Ks = [K // 3, 0, K, K // 2, K - 1]
+    g = torch.Generator().manual_seed(10)
+    bbs = [O.rtn_backbone((torch.randn(r, c, generator=g) * 0.02).numpy(), group)[:3] for r, c in mods]
+    dev_bb = [tuple(torch.from_numpy(np.ascontiguousarray(a)).to(DEV) for a in (cd, s16.view(np.int16), z))
+              for cd, s16, z in bbs]
+    sb = torch.tensor(list(stream), dtype=torch.uint8, device=DEV)
+    dummy = [torch.empty(r, c, dtype=torch.bfloat16, device=DEV) for r, c in mods]
+    plan, ws = awsrc.awsrc_decode_prepare(sb, dummy)
+    outs = [[torch.full((r, c), -1, dtype=torch.int16, device=DEV).view(torch.bfloat16) for r, c in mods]
+            for _ in Ks]
+    awsrc.awsrc_reconstruct_bf16_prefixes(plan, Ks, outs, dev_bb, group)
+    torch.cuda.synchronize()
+    W0o = [O.rtn_dequant(cd, s16, z, group) for cd, s16, z in bbs]
+    for k, got in zip(Ks, outs):
+        sub = stream[:h + k * L]
+        single = [torch.full((r, c), -1, dtype=torch.int16, device=DEV).view(torch.bfloat16) for r, c in mods]
+        p1, _ = awsrc.awsrc_decode_prepare(torch.tensor(list(sub), dtype=torch.uint8, device=DEV), single)
+        awsrc.awsrc_reconstruct_bf16(p1, dev_bb, group)
+        torch.cuda.synchronize()
+        for a, c in zip(got, single):
+            assert torch.equal(a.view(torch.int16), c.view(torch.int16)), k
+        _check_reconstruct(C, sub, k, W0o, O.reconstruct_bf16(sub, bbs, group), got, mods)
+
+
 def test_reconstruct_bf16_empty_stream_and_many_modules():
     """K = 0 gives bf16(W0) everywhere; 300 modules exceed the module table
     the dense pass stages in LDS."""
