@@ -545,7 +545,13 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
         const bool with = !ro.ranked || (D.rec[k] && D.rank[k] < ro.K[o]);
         AWSRC_GLOBAL u32x4_t* out = (AWSRC_GLOBAL u32x4_t*)s_op[o * nm + B.m[k]] + (B.el[k] >> 3);
 #pragma unroll
-        for (int i = 0; i < kUnitW / 8; ++i) out[i] = with ? orc[i] : ob[i];
+        for (int i = 0; i < kUnitW / 8; ++i) {
+          // a select per word (a select of the whole arrays went through scratch)
+          u32x4_t v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = with ? orc[i][j] : ob[i][j];
+          out[i] = v;
+        }
       }
     }
   };
@@ -580,10 +586,12 @@ static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds, int no) {
   return (size_t)(((4 + no) * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
 }
 
-// module windows: the whole LDS table for one output; smaller windows for
-// several, so that two blocks still fit per CU with the sign rows staged
+// module windows: 256 modules for one output, 255 for four, so that two
+// blocks still fit per CU with a 64 KB sign table staged: (4 + NO) x 8 bytes
+// per module plus 16, and the sign rows, within half of the 160 KB
 template <int NO>
-constexpr int rec_window() { return NO == 1 ? kLdsModules : 128; }
+constexpr int rec_window() { return NO == 1 ? kLdsModules : 255; }
+static_assert(2 * (((4 + 4) * 255 + 2) * 8 + kTsignLdsMax) <= 160 * 1024, "two blocks per CU");
 
 template <int C, int G, bool TS_LDS, int NO>
 static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
