@@ -98,7 +98,20 @@ __global__ __launch_bounds__(kThreads) void k_count_hist(const double* __restric
   for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
   __syncthreads();
   uint32_t c = 0;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  for (; i + 7 * stride < n; i += 8 * stride) {
+    double gv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) gv[u] = gain[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t k = gain_key(gv[u]);
+      c += k != 0;
+      atomicAdd(&h[k >> (64 - kSelBits)], 1u);
+    }
+  }
+  for (; i < n; i += stride) {
     const uint64_t k = gain_key(gain[i]);
     c += k != 0;
     atomicAdd(&h[k >> (64 - kSelBits)], 1u);
@@ -209,7 +222,21 @@ __global__ __launch_bounds__(kThreads) void k_select_pass(const double* __restri
   for (int b = threadIdx.x; b < kSelBins; b += kThreads) h[b] = 0;
   __syncthreads();
   const uint64_t dm = (1ull << width) - 1ull;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+  // eight independent loads per thread in flight (the grid is small: each
+  // block ends with up to 4096 global atomics)
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  for (; i + 7 * stride < n; i += 8 * stride) {
+    double gv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) gv[u] = gain[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t k = gain_key(gv[u]);
+      if ((k & nw.mask) == nw.prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
+    }
+  }
+  for (; i < n; i += stride) {
     const uint64_t k = gain_key(gain[i]);
     if ((k & nw.mask) == nw.prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
   }
