@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "encoded tile-seed candidates/sec + decode-add GB/s (fraction of roofline), 1 GPU"
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PEAK_VALU_TOPS = 78.6            # fp32 vector lane-ops/s (157.3 TFLOP/s counting FMA as 2)
+UNPACKED_VALU_TOPS = 39.3        # the same without packed fp32 (one op per lane per cycle), which the build disables
 PEAK_MFMA_BF16_TFLOPS = 2500.0   # dense bf16 matrix-core flops/s
 
 
@@ -397,9 +398,12 @@ def encode_roofline(awsrc, run: Run, stage_ms: dict, gen_version: int) -> dict:
         bound, unit, peak = "alu", "Tops/s", PEAK_VALU_TOPS
         achieved = cand * opc / enc_s / 1e12
         split = {"scored_fraction": f_scored}
+    extra = {}
+    if bound == "alu":
+        extra["frac_unpacked_alu"] = achieved / UNPACKED_VALU_TOPS
     return {"bound": bound, "kernel": f"awsrc_encode_modules over the {len(wl.modules)} module(s) of a step "
                                       "(basis, factors, screen, fp64 re-score)",
-            "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+            "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak, **extra,
             "traffic": measured_traffic("encode", wl.name) if gen_version == 1 else None,
             "traffic_unit": "bytes per step (all encoder calls)", "split": split,
             "ops_per_candidate_unpruned": opc}
