@@ -453,17 +453,31 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
 // The seed is then uniform per half only, so each lane reads its seed's
 // per-column factors with vector loads (two addresses per wavefront).  b is
 // scaled by 1/sqrt(128) before scoring (not a power of two, so raw units
-// would round the fp16 scale differently); each half keeps its own top two,
-// merged at the end.  (Written for any C that is a multiple of 32; at C = 64
-// it measured slower than k_screen_mfma64, which is used there.)
+// would round the fp16 scale differently).
+//
+// Every candidate gets the forward solve with its seed's factor and the bound
+// b^T (G + eps I)^-1 b on every rounding of its fit (screen_fwd); those whose
+// bound reaches the re-score window below the tile's current best (over both
+// halves) wait in one queue per wavefront, appended in step order, and a
+// scoring round takes the 64 oldest, one per lane (each reading its entry's
+// factor again), after which each owner lane inserts its results in queue
+// order (seed order), as in the per-element screen.  Each half keeps its own
+// top two, merged at the end.
 template <int C, bool POW2>
 __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, const u32x4* __restrict__ frag,
                                                               int stride) {
   constexpr int PB = 8;
   constexpr int NKS = C / 32;
   constexpr int TS = 12;  // LDS stride (floats) of one lane's coefficients
-  constexpr int NF = PB * (PB - 1) / 2 + 2 * PB;
+  constexpr int LS = PB * (PB - 1) / 2;
+  constexpr int NF = LS + 2 * PB;   // the whole factor entry (the full score also reads e)
+  constexpr int NBD = LS + PB;      // L and 1/e: what the bound reads
+  constexpr int QC = 128;           // queue slots
+  constexpr int QW = PB + 1;        // words per entry: w, then seed | owner lane << 24
+  constexpr float kSlack = 1.001953125f;
+  static_assert(NBD % 4 == 0 && NF % 4 == 0, "factor pieces are 16 bytes");
   __shared__ __attribute__((aligned(16))) float tb[64 * TS];
+  __shared__ float qb[QW * QC];
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
   const int nsplit = a.nsplit;
@@ -481,33 +495,115 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   const int pair1 = pair0 + pp < n_pairs_all ? pair0 + pp : n_pairs_all;
   const int n = lane & 15, g = lane >> 4;
 
+  // u fragments, and each tile's weighted energy sum_j d_j r_j^2 (over the
+  // four lanes n, n + 16, n + 32, n + 48 that share a row)
   u32x4 uh[2][NKS], um[2][NKS], ul[2][NKS];
+  float en[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int64_t row = row0 + 16 * nb + n;
     const bool valid = row < a.rows;
     const int64_t rr = valid ? row : a.rows - 1;
+    float e = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       const int jc = 32 * ks + 8 * g;
       const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
       float u[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float r = load_w_any2(a.W, a.w_dtype, base + e) - a.W0[base + e];
-        u[e] = valid ? a.d[(int64_t)blk * C + jc + e] * r : 0.0f;
+      for (int k = 0; k < 8; ++k) {
+        const float r = load_w_any2(a.W, a.w_dtype, base + k) - a.W0[base + k];
+        const float dj = a.d[(int64_t)blk * C + jc + k];
+        u[k] = valid ? dj * r : 0.0f;
+        e = fmaf(dj * r, r, e);
       }
       split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
     }
+    e += __shfl_xor(e, 16, 64);
+    en[nb] = e + __shfl_xor(e, 32, 64);
   }
   const int half = lane >> 5;
   const int64_t my_row = row0 + (lane & 31);
   const bool my_valid = my_row < a.rows;
+  const float energy = en[(lane >> 4) & 1];  // this lane's tile, 16 nb + n
   const float qmax = (float)((1 << (a.b - 1)) - 1);
   const float inv_qmax = 1.0f / qmax;
   constexpr float isq = C == 64 ? 0.125f : 0.08838834764831845f;  // 1/sqrt(C)
   float tg0 = -INFINITY, tg1 = -INFINITY;
   uint32_t ts0 = 0, ts1 = 0;  // seed words: seed | kEdge flag
+  float thr = -INFINITY;
+  // the pruning threshold of this lane's tile: the re-score window below the
+  // best over both halves (lane ^ 32), one percent wider, the wide one when
+  // that best is a knife edge
+  auto update_thr = [&]() {
+    const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg0), __float_as_uint(tg0), false, false);
+    const auto r1 = __builtin_amdgcn_permlane32_swap(ts0, ts0, false, false);
+    const float og = __uint_as_float(half ? r0[0] : r0[1]);
+    const uint32_t ow = half ? r1[0] : r1[1];
+    const float best = fmaxf(tg0, og);
+    const bool edge = ((tg0 >= og ? ts0 : ow) & kEdge) != 0;
+    thr = best - 1.01f * rescore_window(best, energy, edge);
+  };
+  int qhead = 0, qtail = 0;  // wavefront-uniform queue counters
+  int nscored = 0;
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  auto load_factor = [&](int s_, float (&f)[NF], int pieces) {
+    const f32x4* fv = reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + s_) * stride);
+#pragma unroll
+    for (int i = 0; i < NF / 4; ++i) {
+      if (i < pieces) {
+        const f32x4 v = fv[i];
+        f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+      }
+    }
+  };
+  auto score_round = [&](int cnt) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const bool mine = lane < cnt;
+    const int slot = (qhead + lane) & (QC - 1);
+    int ol = 0;
+    if (mine) {
+      float wv[PB];
+#pragma unroll
+      for (int i = 0; i < PB; ++i) wv[i] = qb[i * QC + slot];
+      const uint32_t word = __float_as_uint(qb[PB * QC + slot]);
+      const int es = (int)(word & 0xFFFFu);
+      ol = (int)(word >> 24);
+      float f[NF];
+      load_factor(es, f, NF / 4);
+      bool edge;
+      const float gsc = screen_gain_w<PB, POW2, 0>(wv, f, qmax, inv_qmax, &edge);
+      qb[slot] = gsc;
+      qb[QC + slot] = __uint_as_float((uint32_t)es | (edge ? kEdge : 0u));
+    }
+    uint64_t mm = __ballot(mine);
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+      const uint64_t bal = __ballot((ol >> b) & 1);
+      mm &= ((lane >> b) & 1) ? bal : ~bal;
+    }
+    nscored += __popcll(mm);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    while (__ballot(mm != 0) != 0) {
+      if (mm != 0) {
+        const int r = (qhead + __builtin_ctzll(mm)) & (QC - 1);
+        const float gsc = qb[r];
+        const uint32_t sw = __float_as_uint(qb[QC + r]);
+        const bool c0 = gsc > tg0, c1 = gsc > tg1;
+        tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
+        ts1 = c0 ? ts0 : (c1 ? sw : ts1);
+        tg0 = c0 ? gsc : tg0;
+        ts0 = c0 ? sw : ts0;
+        mm &= mm - 1;
+      }
+    }
+    qhead += cnt;
+    update_thr();
+  };
 
   const u32x4* fp = frag + (size_t)pair0 * (NKS * 64) + lane;
   auto project = [&](const u32x4 (&F)[NKS], f32x4 (&acc)[2]) {
@@ -544,13 +640,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   for (int pair = pair0; pair < pair1; ++pair) {
     const int s = 2 * pair + half;
     const int sc_ = s < a.S ? s : a.S - 1;
-    const f32x4* fv = reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + sc_) * stride);
     float f[NF];
-#pragma unroll
-    for (int i = 0; i < NF / 4; ++i) {
-      const f32x4 v = fv[i];
-      f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
-    }
+    load_factor(sc_, f, NBD / 4);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -567,23 +658,32 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     project(F, accN);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
-    bool edge;
-    float gsc = screen_score_ldl<PB, POW2, 0>(bv, f, qmax, inv_qmax, &edge);
-    gsc = s < a.S ? gsc : -INFINITY;
-    const uint32_t sw = (uint32_t)s | (edge ? kEdge : 0u);
-    // this lane's seeds increase, so strict comparisons keep the lower seed among equals
-    const bool c0 = gsc > tg0, c1 = gsc > tg1;
-    tg1 = c0 ? tg0 : (c1 ? gsc : tg1);
-    ts1 = c0 ? ts0 : (c1 ? sw : ts1);
-    tg0 = c0 ? gsc : tg0;
-    ts0 = c0 ? sw : ts0;
+    float wv[PB];
+    const float bnd = screen_fwd<PB>(bv, f, wv);
+    const bool keep = (int)(bnd * kSlack > thr) & (int)my_valid & (int)(s < a.S);
+    // every lane stores its candidate, the kept ones first from the tail on,
+    // the dropped ones after them (at most 63 wait before a step, so the 64
+    // slots written are free); the tail takes in the kept ones only
+    const uint64_t kb = __ballot(keep);
+    const int nk = __popcll(kb);
+    const int pos = keep ? __popcll(kb & lt) : nk + __popcll(~kb & lt);
+    const int qslot = (qtail + pos) & (QC - 1);
+#pragma unroll
+    for (int i = 0; i < PB; ++i) qb[i * QC + qslot] = wv[i];
+    qb[PB * QC + qslot] = __uint_as_float((uint32_t)s | ((uint32_t)lane << 24));
+    qtail += nk;
 #pragma unroll
     for (int i = 0; i < 24; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
     }
+    if (qtail - qhead >= 64) score_round(64);
     stash(accN);
   }
+  if (qtail > qhead) score_round(qtail - qhead);
+#pragma unroll
+  for (int k = 32; k >= 1; k >>= 1) nscored += __shfl_xor(nscored, k, 64);
+  if (lane == 0) atomicAdd(a.scored, (unsigned long long)nscored);
   // merge the two halves' lists of each tile: (gain desc, seed asc)
   const float og0 = __shfl(tg0, lane + 32, 64), og1 = __shfl(tg1, lane + 32, 64);
   const uint32_t os0 = (uint32_t)__shfl((int)ts0, lane + 32, 64), os1 = (uint32_t)__shfl((int)ts1, lane + 32, 64);
@@ -630,11 +730,11 @@ int screen_nsplit(int C, int P, int S, int64_t rows, int64_t cols, int d_mode, i
 }
 
 bool screen_pruned(int C, int P, int d_mode, int gen_version) {
-  return C == 64 && screen_mfma_supported(C, P, d_mode, gen_version) && d_mode == AWSRC_D_PER_COL;
+  return (C == 64 || C == 128) && screen_mfma_supported(C, P, d_mode, gen_version) && d_mode == AWSRC_D_PER_COL;
 }
 
 bool screen_fuses_rescore(int C, int P, int d_mode, int gen_version, int nsplit) {
-  return screen_pruned(C, P, d_mode, gen_version) && gen_version == 1 && nsplit == 1;
+  return C == 64 && screen_pruned(C, P, d_mode, gen_version) && gen_version == 1 && nsplit == 1;
 }
 
 __global__ void k_scored_init(unsigned long long* p, unsigned long long v, int add) {
