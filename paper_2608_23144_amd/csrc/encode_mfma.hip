@@ -476,8 +476,11 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   constexpr int QW = PB + 1;        // words per entry: w, then seed | owner lane << 24
   constexpr float kSlack = 1.001953125f;
   static_assert(NBD % 4 == 0 && NF % 4 == 0, "factor pieces are 16 bytes");
+  constexpr int NR = 4;              // factor ring slots (pairs)
+  constexpr int NPC = 2 * NBD / 4;   // 16-byte pieces of a pair's two bound entries
   __shared__ __attribute__((aligned(16))) float tb[64 * TS];
   __shared__ float qb[QW * QC];
+  __shared__ __attribute__((aligned(16))) float fr[NR * 2 * NBD];  // [slot][seed of the pair][L, 1/e]
   const int lane = threadIdx.x;
   const int nbk_cols = (int)(a.cols / C);
   const int nsplit = a.nsplit;
@@ -556,6 +559,21 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
         f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
       }
     }
+  };
+  // The bound's factor entries reach the wavefront through an LDS ring: at
+  // the step of pair k every lane loads one 16-byte piece of pair k + 2's two
+  // entries (lanes with the same piece load the same one) and stores the
+  // piece it loaded at the step before (pair k + 1's); the bound of pair k
+  // reads its seed's entry from slot k.  The wavefront barriers of every step
+  // order the stores before the reads.
+  const int pc = lane % NPC;
+  auto fac_piece = [&](int pr) -> f32x4 {
+    int s_ = 2 * pr + pc / (NBD / 4);
+    s_ = s_ < a.S ? s_ : a.S - 1;
+    return *reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + s_) * stride + 4 * (pc % (NBD / 4)));
+  };
+  auto fac_store = [&](int pr, const f32x4& v) {
+    *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NBD) + 4 * pc]) = v;
   };
   auto score_round = [&](int cnt) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -637,14 +655,25 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[NKS * 64 + ks * 64];
   }
+  fac_store(pair0, fac_piece(pair0));
+  f32x4 fnext = fac_piece(pair0 + 1);
   for (int pair = pair0; pair < pair1; ++pair) {
     const int s = 2 * pair + half;
-    const int sc_ = s < a.S ? s : a.S - 1;
-    float f[NF];
-    load_factor(sc_, f, NBD / 4);
+    // pair + 1's pieces (loaded a step ago) into the ring, pair + 2's in flight
+    fac_store(pair + 1, fnext);
+    fnext = fac_piece(pair + 2);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    float f[NF];
+    {
+      const float* fe = &fr[(pair & (NR - 1)) * (2 * NBD) + half * NBD];
+#pragma unroll
+      for (int i = 0; i < NBD / 4; ++i) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&fe[4 * i]);
+        f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+      }
+    }
     float bv[PB];
     {
       const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[lane * TS]);
