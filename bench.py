@@ -43,29 +43,28 @@ def log(*a):
 # measured on (SHA-256 over the listed files); after any change to them the
 # figure is reported as null until the counters are taken again.
 MEASURED_TRAFFIC = {
-    ("encode", "down3b"): {
-        "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "rescore64.h"],
-        "sha256": "f62d25be5634403723df27196df17c023950b2ae27656e65a4a7f591ca919ee0",
-        "bytes": 312266468},
-    ("backbone", "down3b"): {
+    # one step of the 36-layer 3B stack (profiles/counters_stack3b.md): the
+    # encode call over all 252 modules (screen 29.07 GB, fp64 re-score
+    # 32.61 GB, tables), the 252 backbone launches, the decode-add of the
+    # 0.32 bpw stream, and the reconstruction of its four nested prefixes
+    # (tile ordering and the streaming pass)
+    ("encode", "stack3b"): {
+        "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
+                  "rescore_pe.hip", "rescore64.h"],
+        "sha256": "93859c70ba09ebd77b9819f4a1ce1ed83c3fdd116a10503d198f88e71e96eb73",
+        "bytes": 61683747392},
+    ("backbone", "stack3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "45a13fcf353eda08999bbf4cb013c9277bb8ed2b76de5fa4ba077fa5d04cd960",
-        "bytes": 147301701},
-    ("decode_apply", "down3b"): {
+        "sha256": "2586f4a4ee2525c8112f6162fb034c15353c68d33c33a3e90eb8fa7da64bbee1",
+        "bytes": 18135996224},
+    ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "057b327e7fba35e628bae904c069085ca5b059d365549ba26d800a9201b58c27",
-        "bytes": 22875478},
-    # the stack3b stream at 0.32 bpw of the at-scale measurement
-    ("decode_apply", "stack3b@0.32"): {
+        "sha256": "691a07e975fd9309ea40e694ef8f23a0f87b1062c19332572ab04ddf587c598e",
+        "bytes": 5036702720},
+    ("reconstruct_bf16", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "057b327e7fba35e628bae904c069085ca5b059d365549ba26d800a9201b58c27",
-        "bytes": 5037000000},
-    # the whole reconstruction call (tile ordering, the streaming pass) of one
-    # 0.32 bpw stack3b stream (measured on the single-prefix call)
-    ("reconstruct_bf16", "stack3b@0.32"): {
-        "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "057b327e7fba35e628bae904c069085ca5b059d365549ba26d800a9201b58c27",
-        "bytes": 9336000000},
+        "sha256": "691a07e975fd9309ea40e694ef8f23a0f87b1062c19332572ab04ddf587c598e",
+        "bytes": 26482273152},
 }
 
 
