@@ -294,6 +294,18 @@ __device__ __forceinline__ int find_module(const ModEntry* mods, int n, int64_t 
   return lo;
 }
 
+// Work item of workgroup b of a one-dimensional grid of n workgroups, such
+// that each of the eight XCDs (which take workgroups round-robin, b mod 8)
+// gets one contiguous range of items: neighbouring items (the next column
+// blocks of the same rows) then share one L2, where their partial writes to
+// the same lines merge.  A bijection on [0, n).
+__device__ __forceinline__ int64_t xcd_item(int64_t b, int64_t n) {
+  constexpr int kXcd = 8;
+  const int64_t x = b % kXcd, k = b / kXcd;
+  const int64_t base = n / kXcd, rem = n % kXcd;
+  return x * base + (x < rem ? x : rem) + k;
+}
+
 // Module tables are written on the device from chunks passed by value (no
 // host copy, so the encoder stays asynchronous).
 constexpr int kModChunk = 48;

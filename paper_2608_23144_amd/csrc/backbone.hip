@@ -72,8 +72,11 @@ __global__ __launch_bounds__(256) void k_backbone_rtn(const TW* __restrict__ W, 
     }
     if (valid) {
       if (W0) {
-        reinterpret_cast<float4*>(W0 + base)[0] = make_float4(o[0], o[1], o[2], o[3]);
-        reinterpret_cast<float4*>(W0 + base)[1] = make_float4(o[4], o[5], o[6], o[7]);
+        // streaming stores: W0 is written once and read by later launches
+        typedef float f32x4_nt __attribute__((ext_vector_type(4)));
+        f32x4_nt* wp = reinterpret_cast<f32x4_nt*>(W0 + base);
+        __builtin_nontemporal_store(f32x4_nt{o[0], o[1], o[2], o[3]}, wp);
+        __builtin_nontemporal_store(f32x4_nt{o[4], o[5], o[6], o[7]}, wp + 1);
       }
       *reinterpret_cast<uint32_t*>(codes + (base >> 1)) = packed;
       if (sub == 0) {

@@ -159,7 +159,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
   const int lane = threadIdx.x;
   const int tl = lane & 31, h = lane >> 5;
-  const int64_t item = blockIdx.x;
+  const int64_t item = xcd_item(blockIdx.x, gridDim.x);
   const int m = find_module(mods, n_mods, item);
   const ModEntry md = mods[m];
   const int nb = (int)(md.cols / kC);
@@ -320,12 +320,23 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
     a.seed_out[t] = (uint16_t)s_me;
     a.scale_out[t] = bits;
     a.gain_out[t] = gk;
+    // the codes in one store when they fill an aligned word (P = 8 or 4)
+    int8_t* cp = a.code_out + t * P;
+    if (P == PB && (PB == 8 || PB == 4) && (reinterpret_cast<uintptr_t>(cp) & (PB - 1)) == 0) {
+      uint64_t w = 0;
 #pragma unroll
-    for (int p = 0; p < PB; ++p) {
-      if (p < P) {
-        a.code_out[t * P + p] = (int8_t)q[p];
-        if (a.alpha_out) a.alpha_out[t * P + p] = (float)al[p];
-      }
+      for (int p = 0; p < PB; ++p) w |= (uint64_t)(uint8_t)q[p] << (8 * p);
+      if (PB == 8) *reinterpret_cast<uint64_t*>(cp) = w;
+      else *reinterpret_cast<uint32_t*>(cp) = (uint32_t)w;
+    } else {
+#pragma unroll
+      for (int p = 0; p < PB; ++p)
+        if (p < P) cp[p] = (int8_t)q[p];
+    }
+    if (a.alpha_out) {
+#pragma unroll
+      for (int p = 0; p < PB; ++p)
+        if (p < P) a.alpha_out[t * P + p] = (float)al[p];
     }
   }
 }
