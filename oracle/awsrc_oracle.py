@@ -327,6 +327,18 @@ def reconstruct_bf16(stream: bytes, backbones: Sequence[Tuple[np.ndarray, np.nda
     return [bf16_round(w) for w in decode_add(stream, W0s)]
 
 
+def reconstruct_bf16_sdq(stream: bytes, backbones: Sequence[Tuple[np.ndarray, np.ndarray, np.ndarray, np.ndarray,
+                                                                     np.ndarray]],
+                         group: int = 128) -> List[np.ndarray]:
+    """Dense bf16 repaired weights on the RTN-INT4-SDQ backbone (the backbone
+    Sec. 4 evaluates with the codecs): each module's W0 dequantized from its
+    codes, zero points and SDQ scale codes (codes, zero, sdq_codes, sdq_mean,
+    sdq_step per module, as rtn_dequant_sdq takes them), the stream's
+    corrections added (decode_add), and the exact sum rounded to bfloat16."""
+    W0s = [rtn_dequant_sdq(c, z, sc, mu, st, group) for c, z, sc, mu, st in backbones]
+    return [bf16_round(w) for w in decode_add(stream, W0s)]
+
+
 def residual(W32: np.ndarray, W0: np.ndarray) -> np.ndarray:
     """R = W - W0 of Eq. (1), one float32 subtraction per element."""
     return (np.asarray(W32, dtype=np.float32) - np.asarray(W0, dtype=np.float32)).astype(np.float32)

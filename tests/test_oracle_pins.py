@@ -757,6 +757,55 @@ def test_rtn_dequant_sdq_reduces_to_rtn_when_scales_are_exact():
     assert np.array_equal(O.rtn_dequant_sdq(codes, zero, sc, mu, st), W0)
 
 
+def test_reconstruct_bf16_sdq_reduces_to_fp16_path_when_scales_are_exact():
+    """With every SDQ block constant the SDQ scales equal the fp16 ones, so the
+    SDQ reconstruction of a stream with records equals the fp16-scale
+    reconstruction (an independent path through rtn_dequant) bit for bit."""
+    rng = np.random.default_rng(14)
+    W = rng.normal(0, 0.02, (4, 128 * 128)).astype(np.float32)
+    W[:, ::128] = 0.3
+    W[:, 1::128] = -0.3
+    codes, s16, zero, W0 = O.rtn_backbone(W)
+    sc, mu, st = O.sdq_encode(s16)
+    assert np.all(sc == 0)
+    p = O.Params(C=64, P=4, b=4, S=8)
+    T = 4 * 128 * 128 // 64
+    enc = {"seed": rng.integers(0, 8, T), "codes": rng.integers(-7, 8, (T, 4)),
+           "scale": np.full(T, 0x2000), "gain": rng.uniform(0, 1, T)}
+    stream, K, _ = O.build_stream(p, [(4, 128 * 128)], enc, 0.05, per_module=False)
+    assert K > 0
+    a = O.reconstruct_bf16_sdq(stream, [(codes, zero, sc, mu, st)])[0]
+    b = O.reconstruct_bf16(stream, [(codes, s16, zero)])[0]
+    assert np.array_equal(a, b)
+
+
+def test_reconstruct_bf16_sdq_changes_only_record_tiles():
+    """Against the rounded SDQ backbone, a stream changes exactly the tiles it
+    holds records for (each by its correction B_s scale q, checked through the
+    norm identity of the orthonormal columns before rounding)."""
+    rng = np.random.default_rng(15)
+    W = rng.normal(0, 0.02, (3, 512)).astype(np.float32)
+    codes, s16, zero, _ = O.rtn_backbone(W)
+    sc, mu, st = O.sdq_encode(s16)
+    W0s = O.rtn_dequant_sdq(codes, zero, sc, mu, st).astype(np.float64)
+    p = O.Params(C=64, P=4, b=4, S=8)
+    T = 3 * 512 // 64
+    gain = -np.ones(T)
+    gain[[2, 17]] = [2.0, 1.0]
+    enc = {"seed": np.full(T, 5), "codes": np.tile([3, -2, 0, 7], (T, 1)),
+           "scale": np.full(T, 0x3C00), "gain": gain}   # fp16 1.0
+    stream, K, _ = O.build_stream(p, [(3, 512)], enc, 64.0, per_module=False)
+    assert K == 2
+    out = O.reconstruct_bf16_sdq(stream, [(codes, zero, sc, mu, st)])[0]
+    base = O.bf16_round(W0s)
+    changed = {int(t) for t in np.nonzero((out != base).reshape(T, 64).any(axis=1))[0]}
+    assert changed <= {2, 17} and changed
+    exact = O.decode_add(stream, [W0s])[0] - W0s
+    for t in (2, 17):
+        r = exact.reshape(T, 64)[t]
+        assert math.isclose(float(r @ r), 9 + 4 + 0 + 49, rel_tol=1e-12)  # scale 1, orthonormal B_s
+
+
 def test_sdq_rate():
     """8 bits per group and 64 per block of 256: 0.0645 bits per weight at
     g128, against 0.125 for the fp16 scales (Sec. 4 reports 0.068 for its
