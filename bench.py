@@ -217,13 +217,17 @@ def encode_split_bound(C: int, P: int, per_element: bool, gen_version: int, scor
     return {"mfma_flops_per_candidate": 6.0 * P * C, "valu_ops_per_candidate": valu}
 
 
-def sdq_timing(awsrc, torch, wl, bb, stream, reps: int = 20) -> dict:
+def sdq_timing(awsrc, torch, wl, run, stream, reps: int = 20) -> dict:
     """RTN-INT4-SDQ backbone (Sec. 3.3, Sec. 4): SDQ of the step's group scales
-    and W0 with the dequantized scales, timed with HIP events (outside the
-    step; the step's encoder repairs the RTN-v1 backbone).  Algorithmic bytes:
-    encode 2 B read + 1 B written per group and 8 B per block of 256; W0 0.5 B
-    of codes read and 4 B written per weight, 2 B (zero point, code) per group
-    and 8 B per block."""
+    and W0 with the dequantized scales, and the dense bf16 reconstruction of
+    the step's four prefixes on that backbone (the evaluation form Sec. 4
+    uses), timed with HIP events (outside the step; the step's encoder
+    repairs the RTN-v1 backbone).  Algorithmic bytes: encode 2 B read + 1 B
+    written per group and 8 B per block of 256; W0 0.5 B of codes read and
+    4 B written per weight, 2 B (zero point, code) per group and 8 B per
+    block; reconstruction as the step's, with 2 B per group for the zero
+    point and scale code and 8 B per block."""
+    bb = run.bb
     n_w = sum(b[0].numel() * 2 for b in bb)
     n_g = sum(b[1].numel() for b in bb)
     n_blk = sum((b[1].numel() + 255) // 256 for b in bb)
@@ -245,7 +249,25 @@ def sdq_timing(awsrc, torch, wl, bb, stream, reps: int = 20) -> dict:
     deq_ms = e[1].elapsed_time(e[2]) / reps
     enc_bytes = 3 * n_g + 8 * n_blk
     deq_bytes = n_w // 2 + 4 * n_w + 2 * n_g + 8 * n_blk
-    return {"groups": n_g, "scale_bits_per_weight": (8 * n_g + 64 * n_blk) / n_w,
+    rc = {}
+    last = run.last
+    if "plan" in last:
+        sbb = [(b[0], b[2], q[0], q[1], q[2]) for b, q in zip(bb, sdqs)]
+        ks = [kb for _, kb in last["prefixes"]]
+        r_reps = 5
+        awsrc.awsrc_reconstruct_bf16_sdq(last["plan"], sbb, K_out=ks, outs=run.outs)
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        for _ in range(r_reps):
+            awsrc.awsrc_reconstruct_bf16_sdq(last["plan"], sbb, K_out=ks, outs=run.outs)
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        rc_ms = e[0].elapsed_time(e[1]) / r_reps
+        rc_bytes = n_w // 2 + 2 * n_g + 8 * n_blk + len(ks) * 2 * n_w + max(ks) * run.L
+        rc = {"reconstruct_prefixes": len(ks), "reconstruct_ms": rc_ms, "reconstruct_bytes": rc_bytes,
+              "reconstruct_GB/s": rc_bytes / (rc_ms / 1e3) / 1e9,
+              "reconstruct_frac_hbm": rc_bytes / (rc_ms / 1e3) / 1e9 / PEAK_HBM_GBS}
+    return {**rc, "groups": n_g, "scale_bits_per_weight": (8 * n_g + 64 * n_blk) / n_w,
             "fp16_scale_bits_per_weight": 16 * n_g / n_w,
             "encode_ms": enc_ms, "dequant_ms": deq_ms, "dequant_bytes": deq_bytes,
             "dequant_GB/s": deq_bytes / (deq_ms / 1e3) / 1e9,
@@ -353,7 +375,7 @@ def run_steps(awsrc, torch, run: Run, steps: int, warmup: int):
         awsrc.awsrc_reconstruct_bf16_prefixes(plan, [kb for _, kb in prefixes], run.outs,
                                               [b[:3] for b in run.bb], 128)
         ev[6].record(stream)
-        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), dws=dws, prefixes=prefixes)
+        last.update(K=K, n_eligible=ne, stream_len=int(s.numel()), dws=dws, prefixes=prefixes, plan=plan, s=s)
         if record:
             torch.cuda.synchronize()
             for k, (a, b) in zip(STAGES, zip(ev[:-1], ev[1:])):
@@ -521,7 +543,7 @@ def main() -> int:
         "stream": res["stream"],
         "device": torch.cuda.get_device_name(0),
     }
-    out["backbone_sdq"] = sdq_timing(awsrc, torch, wl, run.bb, stream)
+    out["backbone_sdq"] = sdq_timing(awsrc, torch, wl, run, stream)
     sample = run.sample
     del run
     torch.cuda.empty_cache()

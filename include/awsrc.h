@@ -426,6 +426,28 @@ awsrc_status awsrc_reconstruct_bf16_prefixes(const awsrc_decode_plan* plan, int3
                                              const uint16_t* const* scale_f16, const uint8_t* const* zero,
                                              void* stream);
 
+/*
+ * Dense bf16 repaired weights on the RTN-INT4-SDQ backbone (Sec. 4 evaluates
+ * the codecs on RTN-INT4-SDQ as dense BF16 weights): as
+ * awsrc_reconstruct_bf16 (n_out == 0) or awsrc_reconstruct_bf16_prefixes
+ * (n_out 1..8), with each group's scale the SDQ scale
+ * s_hat_g = f32(mu_b + code_g * step_b) of awsrc_backbone_sdq_dequant instead
+ * of an fp16 scale, so W0 = f32(q - z) * s_hat exactly as that call writes it.
+ *  n_out, K_out, out_ptrs   0 and NULLs: into the plan's own (bf16) W0
+ *             buffers with every record; else as for the prefixes call.
+ *  sdq_code   host array [n_modules] of device pointers: int8 [rows * cols/group]
+ *             (awsrc_sdq_encode's codes of the module's scales, row-major).
+ *  sdq_mean, sdq_step   host arrays [n_modules] of device pointers: fp32
+ *             [ceil(groups / 256)] each, 4-byte aligned.
+ *  group, codes, zero   as for awsrc_reconstruct_bf16.
+ * Synchronizes once (module table read-back) before launching; EINVAL on a
+ * bad argument (nothing launched).
+ */
+awsrc_status awsrc_reconstruct_bf16_sdq(const awsrc_decode_plan* plan, int32_t n_out, const int64_t* K_out,
+                                        void* const* out_ptrs, int32_t group, const uint8_t* const* codes,
+                                        const int8_t* const* sdq_code, const float* const* sdq_mean,
+                                        const float* const* sdq_step, const uint8_t* const* zero, void* stream);
+
 /* Host-only helpers (no device needed). */
 /* L_rec in bytes for T_total tiles; -1 if p is invalid. */
 int64_t awsrc_record_bytes(const awsrc_params* p, int64_t T_total);

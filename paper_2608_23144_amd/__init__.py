@@ -28,7 +28,7 @@ EXPORTED = ("awsrc_abi_version", "awsrc_last_error", "awsrc_backbone_rtn", "awsr
             "awsrc_backbone_sdq_dequant", "awsrc_encode_tiles",
             "awsrc_encode_modules", "awsrc_encode_screen_lists", "awsrc_encode_tiles_noalloc", "awsrc_encode_noalloc_max_bytes",
             "awsrc_encode_scored", "awsrc_rank_prefix", "awsrc_decode_add", "awsrc_decode_prepare", "awsrc_decode_apply",
-            "awsrc_reconstruct_bf16", "awsrc_reconstruct_bf16_prefixes", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
+            "awsrc_reconstruct_bf16", "awsrc_reconstruct_bf16_prefixes", "awsrc_reconstruct_bf16_sdq", "awsrc_record_bytes", "awsrc_header_bytes", "awsrc_budget_bytes", "awsrc_prefix_K")
 
 
 class AwsrcError(RuntimeError):
@@ -89,6 +89,9 @@ def _load() -> ctypes.CDLL:
         "awsrc_reconstruct_bf16_prefixes": (i32, [ctypes.POINTER(awsrc_decode_plan), i32, P64, ctypes.POINTER(vp),
                                                   i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                                   vp]),
+        "awsrc_reconstruct_bf16_sdq": (i32, [ctypes.POINTER(awsrc_decode_plan), i32, P64, ctypes.POINTER(vp), i32,
+                                             ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                             ctypes.POINTER(vp), ctypes.POINTER(vp), vp]),
         "awsrc_record_bytes": (i64, [pp, i64]),
         "awsrc_header_bytes": (i64, [i32]),
         "awsrc_budget_bytes": (i64, [ctypes.c_double, i64]),
@@ -466,3 +469,37 @@ def awsrc_reconstruct_bf16_prefixes(plan: awsrc_decode_plan, K_out: Sequence[int
     optr = (ctypes.c_void_p * (n * len(outs)))(*[t.data_ptr() for o in outs for t in o])
     _check(LIB.awsrc_reconstruct_bf16_prefixes(ctypes.byref(plan), len(K_out), _i64arr(list(K_out)), optr, group,
                                                arr[0], arr[1], arr[2], _stream(stream)))
+
+
+def awsrc_reconstruct_bf16_sdq(plan: awsrc_decode_plan,
+                               backbones: Sequence[Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor,
+                                                         torch.Tensor]],
+                               K_out: Optional[Sequence[int]] = None,
+                               outs: Optional[Sequence[Sequence[torch.Tensor]]] = None,
+                               group: int = 128, stream=None) -> None:
+    """Dense bf16 repaired weights on the RTN-INT4-SDQ backbone: `backbones`
+    holds each module's (codes, zero, sdq_code, sdq_mean, sdq_step), the RTN
+    codes and zero points with awsrc_sdq_encode's outputs for its scales.
+    Without K_out / outs: into the bf16 buffers the plan was prepared on, every
+    record; else outs[o] receives the first K_out[o] records' prefix."""
+    n = plan.n_modules
+    if len(backbones) != n:
+        raise ValueError(f"{len(backbones)} backbones for a plan of {n} modules")
+    for bb in backbones:
+        _dev(*bb)
+    if (K_out is None) != (outs is None):
+        raise ValueError("K_out and outs go together")
+    arr = [(ctypes.c_void_p * n)(*[bb[k].data_ptr() for bb in backbones]) for k in range(5)]
+    if outs is None:
+        n_out, kp, optr = 0, None, None
+    else:
+        if len(outs) != len(K_out) or any(len(o) != n for o in outs):
+            raise ValueError("need, per prefix, one target per module")
+        for o in outs:
+            _dev(*o)
+            if any(t.dtype != torch.bfloat16 for t in o):
+                raise TypeError("targets must be bf16")
+        n_out, kp = len(K_out), _i64arr(list(K_out))
+        optr = (ctypes.c_void_p * (n * n_out))(*[t.data_ptr() for o in outs for t in o])
+    _check(LIB.awsrc_reconstruct_bf16_sdq(ctypes.byref(plan), n_out, kp, optr, group, arr[0], arr[2], arr[3], arr[4],
+                                          arr[1], _stream(stream)))

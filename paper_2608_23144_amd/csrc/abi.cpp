@@ -603,7 +603,7 @@ DecodeLayout decode_layout(int S, int P, uint64_t T_total, uint32_t nmod, int64_
   l.dec_t = align_up((size_t)(K + 1) * 32, 256);  // entry 0 is readable even when K = 0
   const size_t nwords = (size_t)((T_total + 31) / 32);
   l.bsum = align_up(((nwords + 4095) / 4096) * 4, 256);
-  l.bbtab = align_up((size_t)(3 + kMaxPrefixOutputs) * nmod * 8, 256);
+  l.bbtab = align_up((size_t)kBbRows * nmod * 8, 256);
   l.total = 256 + l.basis + l.bitmap + l.err + l.tables + l.dec + l.dec_t + l.bsum + l.bbtab;
   return l;
 }
@@ -737,14 +737,18 @@ namespace {
 // The dense reconstruction of awsrc_reconstruct_bf16 (n_out == 0, the plan's
 // targets) and awsrc_reconstruct_bf16_prefixes (n_out targets of nested
 // prefixes).
+// scale: fp16 scales, or (sdq_mean and sdq_step not NULL) SDQ scale codes
 awsrc_status reconstruct(const awsrc_decode_plan* plan, int32_t n_out, const int64_t* K_out, void* const* out_ptrs,
-                         int32_t group, const uint8_t* const* codes, const uint16_t* const* scale_f16,
-                         const uint8_t* const* zero, void* stream) {
+                         int32_t group, const uint8_t* const* codes, const void* const* scale,
+                         const float* const* sdq_mean, const float* const* sdq_step, const uint8_t* const* zero,
+                         void* stream) {
+  const bool sdq = sdq_mean || sdq_step;
+  if (sdq && !(sdq_mean && sdq_step)) return fail(AWSRC_EINVAL, "SDQ block mean and step arrays: both or neither");
   if (!plan || !plan->workspace) return fail(AWSRC_EINVAL, "plan is NULL or not prepared");
   if (n_out == 0 && plan->w0_dtype != AWSRC_DTYPE_BF16) return fail(AWSRC_EINVAL, "the plan's targets must be bf16");
   if (group != 64 && group != 128 && group != 256) return fail(AWSRC_EINVAL, "group=%d: must be 64, 128 or 256", group);
   if (plan->C < 16) return fail(AWSRC_EINVAL, "C=%d: the reconstruction needs C >= 16", plan->C);
-  if (!codes || !scale_f16 || !zero) return fail(AWSRC_EINVAL, "backbone pointer arrays are NULL");
+  if (!codes || !scale || !zero) return fail(AWSRC_EINVAL, "backbone pointer arrays are NULL");
   const uint32_t n = (uint32_t)plan->n_modules;
   uint32_t kout[kMaxPrefixOutputs] = {};
   for (int o = 0; o < n_out; ++o) {
@@ -753,14 +757,22 @@ awsrc_status reconstruct(const awsrc_decode_plan* plan, int32_t n_out, const int
     kout[o] = (uint32_t)K_out[o];
   }
   const DecodeArgs a = decode_args(plan);
-  std::vector<uint64_t> tabs((3 + (size_t)n_out) * n);
+  std::vector<uint64_t> tabs((size_t)kBbRows * n, 0);
   for (uint32_t m = 0; m < n; ++m) {
-    if (!codes[m] || !scale_f16[m] || !zero[m]) return fail(AWSRC_EINVAL, "backbone pointer of module %u is NULL", m);
+    if (!codes[m] || !scale[m] || !zero[m]) return fail(AWSRC_EINVAL, "backbone pointer of module %u is NULL", m);
     if (reinterpret_cast<uintptr_t>(codes[m]) & 7) return fail(AWSRC_EINVAL, "codes of module %u must be 8-byte aligned", m);
-    if (reinterpret_cast<uintptr_t>(scale_f16[m]) & 1) return fail(AWSRC_EINVAL, "scale of module %u must be 2-byte aligned", m);
+    if (!sdq && (reinterpret_cast<uintptr_t>(scale[m]) & 1))
+      return fail(AWSRC_EINVAL, "scale of module %u must be 2-byte aligned", m);
     tabs[m] = reinterpret_cast<uint64_t>(codes[m]);
-    tabs[n + m] = reinterpret_cast<uint64_t>(scale_f16[m]);
+    tabs[n + m] = reinterpret_cast<uint64_t>(scale[m]);
     tabs[2 * n + m] = reinterpret_cast<uint64_t>(zero[m]);
+    if (sdq) {
+      if (!sdq_mean[m] || !sdq_step[m]) return fail(AWSRC_EINVAL, "SDQ block table of module %u is NULL", m);
+      if ((reinterpret_cast<uintptr_t>(sdq_mean[m]) | reinterpret_cast<uintptr_t>(sdq_step[m])) & 3)
+        return fail(AWSRC_EINVAL, "SDQ block tables of module %u must be 4-byte aligned", m);
+      tabs[(size_t)kBbRowSdqMean * n + m] = reinterpret_cast<uint64_t>(sdq_mean[m]);
+      tabs[(size_t)kBbRowSdqStep * n + m] = reinterpret_cast<uint64_t>(sdq_step[m]);
+    }
     for (int o = 0; o < n_out; ++o) {
       const void* q = out_ptrs[(size_t)o * n + m];
       if (!q) return fail(AWSRC_EINVAL, "target %d of module %u is NULL", o, m);
@@ -788,6 +800,7 @@ awsrc_status reconstruct(const awsrc_decode_plan* plan, int32_t n_out, const int
   BackboneTabs bb;
   bb.ptr = bbt;
   bb.gshift = group == 64 ? 6 : group == 128 ? 7 : 8;
+  bb.sdq = sdq ? 1 : 0;
   HIPCHK(launch_reconstruct_bf16(a, bb, mt.data(), n_out, kout, s));
   return AWSRC_OK;
 }
@@ -797,7 +810,8 @@ awsrc_status reconstruct(const awsrc_decode_plan* plan, int32_t n_out, const int
 extern "C" awsrc_status awsrc_reconstruct_bf16(const awsrc_decode_plan* plan, int32_t group,
                                                const uint8_t* const* codes, const uint16_t* const* scale_f16,
                                                const uint8_t* const* zero, void* stream) {
-  return reconstruct(plan, 0, nullptr, nullptr, group, codes, scale_f16, zero, stream);
+  return reconstruct(plan, 0, nullptr, nullptr, group, codes, reinterpret_cast<const void* const*>(scale_f16), nullptr,
+                     nullptr, zero, stream);
 }
 
 extern "C" awsrc_status awsrc_reconstruct_bf16_prefixes(const awsrc_decode_plan* plan, int32_t n_out,
@@ -806,7 +820,20 @@ extern "C" awsrc_status awsrc_reconstruct_bf16_prefixes(const awsrc_decode_plan*
                                                         const uint8_t* const* zero, void* stream) {
   if (n_out < 1 || n_out > kMaxPrefixOutputs) return fail(AWSRC_EINVAL, "n_out=%d: must be 1..%d", n_out, kMaxPrefixOutputs);
   if (!K_out || !out_ptrs) return fail(AWSRC_EINVAL, "K_out or out_ptrs is NULL");
-  return reconstruct(plan, n_out, K_out, out_ptrs, group, codes, scale_f16, zero, stream);
+  return reconstruct(plan, n_out, K_out, out_ptrs, group, codes, reinterpret_cast<const void* const*>(scale_f16),
+                     nullptr, nullptr, zero, stream);
+}
+
+extern "C" awsrc_status awsrc_reconstruct_bf16_sdq(const awsrc_decode_plan* plan, int32_t n_out, const int64_t* K_out,
+                                                   void* const* out_ptrs, int32_t group, const uint8_t* const* codes,
+                                                   const int8_t* const* sdq_code, const float* const* sdq_mean,
+                                                   const float* const* sdq_step, const uint8_t* const* zero,
+                                                   void* stream) {
+  if (n_out < 0 || n_out > kMaxPrefixOutputs) return fail(AWSRC_EINVAL, "n_out=%d: must be 0..%d", n_out, kMaxPrefixOutputs);
+  if (n_out > 0 && (!K_out || !out_ptrs)) return fail(AWSRC_EINVAL, "K_out or out_ptrs is NULL");
+  if (!sdq_code || !sdq_mean || !sdq_step) return fail(AWSRC_EINVAL, "SDQ pointer arrays are NULL");
+  return reconstruct(plan, n_out, K_out, out_ptrs, group, codes, reinterpret_cast<const void* const*>(sdq_code),
+                     sdq_mean, sdq_step, zero, stream);
 }
 
 extern "C" awsrc_status awsrc_decode_add(const uint8_t* stream_bytes, uint64_t stream_len, int32_t n_modules,

@@ -422,10 +422,19 @@ hipError_t launch_decode_apply(const DecodeArgs& a, hipStream_t st);
 // Stored backbone of each module for the bf16 reconstruction: device table
 // of device pointers, codes [n] | scale [n] | zero [n] (layouts of
 // awsrc_backbone_rtn), n = n_modules.
+// Device table of backbone pointers, rows of n_modules entries: codes, scale
+// (fp16, or the SDQ scale codes), zero points, the kMaxPrefixOutputs target
+// rows, then (SDQ) the block means and steps.
 struct BackboneTabs {
   const uint64_t* ptr;
   int gshift;  // log2 of the backbone group
+  int sdq;     // scales are SDQ codes with per-block mean and step
 };
+constexpr int kMaxPrefixOutputs = 8;  // targets of one awsrc_reconstruct_bf16_prefixes call
+constexpr int kBbRowSdqMean = 3 + kMaxPrefixOutputs;
+constexpr int kBbRowSdqStep = 4 + kMaxPrefixOutputs;
+constexpr int kBbRows = 5 + kMaxPrefixOutputs;
+constexpr int kSdqBlock = 256;        // groups per SDQ block (mean and step)
 // Dense bf16 reconstruction; toff is a host copy of the tile offsets (one
 // launch per window of modules).  n_out == 0: into the plan's (bf16) module
 // buffers with every record; else into n_out targets whose module pointer
@@ -433,6 +442,5 @@ struct BackboneTabs {
 // place in the stream is below K_out[o].
 hipError_t launch_reconstruct_bf16(const DecodeArgs& a, const BackboneTabs& bb, const uint64_t* toff, int n_out,
                                    const uint32_t* K_out, hipStream_t st);
-constexpr int kMaxPrefixOutputs = 8;  // targets of one awsrc_reconstruct_bf16_prefixes call
 
 }  // namespace awsrc

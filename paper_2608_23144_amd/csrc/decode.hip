@@ -349,7 +349,8 @@ __device__ __forceinline__ uint32_t code_word(const uint32_t& q, int) { return q
 template <int NU>
 struct RecBackbone {                         // backbone words of one chunk
   UnitCodes q[NU];
-  uint32_t s[NU], z[NU];
+  uint32_t s[NU], z[NU];                     // fp16 scale bits, or the SDQ scale code (sign-extended)
+  float mu[NU], st[NU];                      // SDQ: the mean and step of the scale code's block
   uint32_t m[NU];                            // module (within the window) and first element of the unit
   uint64_t el[NU];
   bool ok[NU];
@@ -386,7 +387,7 @@ struct RecOut {
 // [16 uw, 16 uw + 16) (rows are whole multiples of the group, hence of 16),
 // and its backbone group is element / group.  Every load is issued unconditionally (units
 // past the window end are clamped to its last unit and not stored).
-template <int C, int G, bool TS_LDS, int NO>
+template <int C, int G, bool TS_LDS, int NO, bool SDQ>
 __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, BackboneTabs bb, RecOut ro, int m0,
                                                              int nm) {
   constexpr int NT = kRecThreads, NU = kRecUnits;
@@ -395,13 +396,17 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
   constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
                       : (C == 64) ? 0.125f : 0.08838834764831845f;
   extern __shared__ __align__(16) uint64_t s_dyn[];
-  // LDS: [tile offsets nm+1 | codes nm | scale nm | zero nm | out NO x nm] then [S][C] sign rows
+  // LDS: [tile offsets nm+1 | codes nm | scale nm | zero nm | out NO x nm
+  // | SDQ: block means nm | block steps nm] then [S][C] sign rows
+  constexpr int NROW = 4 + NO + (SDQ ? 2 : 0);
   uint64_t* s_off = s_dyn;
   uint64_t* s_cp = s_off + nm + 1;
   uint64_t* s_sp = s_cp + nm;
   uint64_t* s_zp = s_sp + nm;
   uint64_t* s_op = s_zp + nm;
-  uint16_t* s_ts = reinterpret_cast<uint16_t*>(s_dyn + (((4 + NO) * nm + 1 + 1) & ~1));
+  uint64_t* s_mp = s_op + NO * nm;
+  uint64_t* s_tp = s_mp + nm;
+  uint16_t* s_ts = reinterpret_cast<uint16_t*>(s_dyn + ((NROW * nm + 1 + 1) & ~1));
   const uint32_t n_all = (uint32_t)a.n_modules;
   for (int i = threadIdx.x; i <= nm; i += NT) s_off[i] = a.mod_tile_off[m0 + i];
   for (int i = threadIdx.x; i < nm; i += NT) {
@@ -412,6 +417,10 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
     for (int o = 0; o < NO; ++o)
       s_op[o * nm + i] = ro.ranked ? bb.ptr[(3 + ro.o0 + o) * (size_t)n_all + m0 + i]
                                    : reinterpret_cast<uint64_t>(a.mod_ptr[m0 + i]);
+    if constexpr (SDQ) {
+      s_mp[i] = bb.ptr[(size_t)kBbRowSdqMean * n_all + m0 + i];
+      s_tp[i] = bb.ptr[(size_t)kBbRowSdqStep * n_all + m0 + i];
+    }
   }
   if constexpr (TS_LDS) {
     constexpr int PER_SEED = C / 8;                      // 16-byte pieces per seed
@@ -445,7 +454,13 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       const uint64_t el = (u - m_lo) << kLogUnitW;       // first element of the unit
       const uint64_t g = el >> bb.gshift;
       B.q[k] = *((const AWSRC_GLOBAL UnitCodes*)s_cp[m] + (el >> kLogUnitW));
-      B.s[k] = ((const AWSRC_GLOBAL uint16_t*)s_sp[m])[g];
+      if constexpr (SDQ) {
+        B.s[k] = (uint32_t)(int32_t)((const AWSRC_GLOBAL int8_t*)s_sp[m])[g];
+        B.mu[k] = ((const AWSRC_GLOBAL float*)s_mp[m])[g / kSdqBlock];
+        B.st[k] = ((const AWSRC_GLOBAL float*)s_tp[m])[g / kSdqBlock];
+      } else {
+        B.s[k] = ((const AWSRC_GLOBAL uint16_t*)s_sp[m])[g];
+      }
       B.z[k] = ((const AWSRC_GLOBAL uint8_t*)s_zp[m])[g];
       B.m[k] = (uint32_t)m;
       B.el[k] = el;
@@ -481,7 +496,13 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
     for (int k = 0; k < NU; ++k) {
       if (!B.ok[k]) continue;
       const uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
-      const float s = __half2float(__ushort_as_half((uint16_t)B.s[k]));
+      // the group's scale: fp16, or the SDQ scale f32(mu + code step) (both
+      // terms and their sum exact in fp64, so one rounding)
+      float s;
+      if constexpr (SDQ)
+        s = (float)((double)B.mu[k] + (double)(int32_t)B.s[k] * (double)B.st[k]);
+      else
+        s = __half2float(__ushort_as_half((uint16_t)B.s[k]));
       const float z = (float)B.z[k];
       float w[kUnitW];
 #pragma unroll
@@ -582,27 +603,29 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
 
 // dynamic LDS of one launch: module window table (rounded to 16 bytes) and
 // the sign rows when staged
-static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds, int no) {
-  return (size_t)(((4 + no) * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
+static size_t rec_lds_bytes(int C, int S, int nm, bool ts_lds, int no, bool sdq) {
+  return (size_t)(((4 + no + (sdq ? 2 : 0)) * nm + 1 + 1) & ~1) * 8 + (ts_lds ? (size_t)S * C * 2 : 0);
 }
 
 // module windows: 256 modules for one output, 255 for four, so that two
 // blocks still fit per CU with a 64 KB sign table staged: (4 + NO) x 8 bytes
 // per module plus 16, and the sign rows, within half of the 160 KB
-template <int NO>
-constexpr int rec_window() { return NO == 1 ? kLdsModules : 255; }
+template <int NO, bool SDQ>
+constexpr int rec_window() { return SDQ ? (NO == 1 ? kLdsModules : 200) : (NO == 1 ? kLdsModules : 255); }
 static_assert(2 * (((4 + 4) * 255 + 2) * 8 + kTsignLdsMax) <= 160 * 1024, "two blocks per CU");
+static_assert(2 * (((4 + 4 + 2) * 200 + 2) * 8 + kTsignLdsMax) <= 160 * 1024, "two blocks per CU (SDQ)");
+static_assert(2 * (((4 + 1 + 2) * kLdsModules + 2) * 8 + kTsignLdsMax) <= 160 * 1024, "two blocks per CU (SDQ)");
 
-template <int C, int G, bool TS_LDS, int NO>
+template <int C, int G, bool TS_LDS, int NO, bool SDQ>
 static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
                                  hipStream_t st) {
-  constexpr int WIN = rec_window<NO>();
+  constexpr int WIN = rec_window<NO, SDQ>();
   for (int m0 = 0; m0 < a.n_modules; m0 += WIN) {
     const int nm = a.n_modules - m0 < WIN ? a.n_modules - m0 : WIN;
-    const size_t lds = rec_lds_bytes(C, a.S, nm, TS_LDS, NO);
+    const size_t lds = rec_lds_bytes(C, a.S, nm, TS_LDS, NO, SDQ);
     int per_cu = 0;
     HIP_RETURN_IF(
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS, NO>, kRecThreads, lds));
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS, NO, SDQ>, kRecThreads, lds));
     if (per_cu < 1) per_cu = 1;
     const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / kUnitW);
     const uint64_t chunks = (units + kRecUnits * kRecThreads - 1) / (kRecUnits * kRecThreads);
@@ -612,29 +635,35 @@ static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, co
     uint64_t nb = (uint64_t)per_cu * 256 * 4;
     if (nb > chunks) nb = chunks;
     if (nb < 1) continue;
-    hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS, NO>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb, ro,
-                       m0, nm);
+    hipLaunchKernelGGL((k_reconstruct<C, G, TS_LDS, NO, SDQ>), dim3((unsigned)nb), dim3(kRecThreads), lds, st, a, bb,
+                       ro, m0, nm);
     HIP_RETURN_IF(hipGetLastError());
   }
   return hipSuccess;
 }
 
-template <int C, int G, int NO>
+template <int C, int G, int NO, bool SDQ>
 static hipError_t launch_rec_cgn(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
                                  hipStream_t st) {
-  if ((size_t)a.S * C * 2 <= (size_t)kTsignLdsMax) return launch_rec_cgt<C, G, true, NO>(a, bb, ro, toff, st);
-  return launch_rec_cgt<C, G, false, NO>(a, bb, ro, toff, st);
+  if ((size_t)a.S * C * 2 <= (size_t)kTsignLdsMax) return launch_rec_cgt<C, G, true, NO, SDQ>(a, bb, ro, toff, st);
+  return launch_rec_cgt<C, G, false, NO, SDQ>(a, bb, ro, toff, st);
+}
+
+template <int C, int NO, bool SDQ>
+static hipError_t launch_rec_cns(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
+                                 hipStream_t st) {
+  switch ((a.P + 3) / 4) {
+    case 1: return launch_rec_cgn<C, 1, NO, SDQ>(a, bb, ro, toff, st);
+    case 2: return launch_rec_cgn<C, 2, NO, SDQ>(a, bb, ro, toff, st);
+    case 3: return launch_rec_cgn<C, 3, NO, SDQ>(a, bb, ro, toff, st);
+    default: return launch_rec_cgn<C, 4, NO, SDQ>(a, bb, ro, toff, st);
+  }
 }
 
 template <int C, int NO>
 static hipError_t launch_rec_cn(const DecodeArgs& a, const BackboneTabs& bb, const RecOut& ro, const uint64_t* toff,
                                 hipStream_t st) {
-  switch ((a.P + 3) / 4) {
-    case 1: return launch_rec_cgn<C, 1, NO>(a, bb, ro, toff, st);
-    case 2: return launch_rec_cgn<C, 2, NO>(a, bb, ro, toff, st);
-    case 3: return launch_rec_cgn<C, 3, NO>(a, bb, ro, toff, st);
-    default: return launch_rec_cgn<C, 4, NO>(a, bb, ro, toff, st);
-  }
+  return bb.sdq ? launch_rec_cns<C, NO, true>(a, bb, ro, toff, st) : launch_rec_cns<C, NO, false>(a, bb, ro, toff, st);
 }
 
 // One pass: no == 1, or no == 4 (C >= 64 only).

@@ -22,8 +22,6 @@ namespace awsrc {
 
 namespace {
 
-constexpr int kSdqBlock = 256;
-
 // One wavefront per block: the scales go through LDS so that lane 0 can sum
 // them in order (the order fixes the rounding when the fp64 sum is inexact).
 __global__ __launch_bounds__(64) void k_sdq_encode(const uint16_t* __restrict__ s16, int64_t n, int8_t* __restrict__ code,

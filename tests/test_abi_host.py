@@ -182,6 +182,30 @@ def test_reconstruct_prefixes_rejects_bad_arguments_without_device_access():
     assert f(ctypes.byref(plan), 2, K, outs, 96, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # group
 
 
+def test_reconstruct_sdq_rejects_bad_arguments_without_device_access():
+    plan = awsrc.awsrc_decode_plan()
+    v = ctypes.c_void_p
+    arr = (v * 1)(256)
+    f = awsrc.LIB.awsrc_reconstruct_bf16_sdq
+    K = (ctypes.c_int64 * 1)(0)
+    outs = (v * 1)(256)
+    assert f(ctypes.byref(plan), 0, None, None, 128, arr, arr, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # not prepared
+    plan.workspace = 4096
+    plan.n_modules = 1
+    plan.C = 64
+    plan.K = 3
+    plan.w0_dtype = awsrc.AWSRC_DTYPE_BF16
+    assert f(ctypes.byref(plan), 9, K, outs, 128, arr, arr, arr, arr, arr, None) == awsrc.AWSRC_EINVAL    # n_out
+    assert f(ctypes.byref(plan), 1, None, outs, 128, arr, arr, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # K_out
+    assert f(ctypes.byref(plan), 0, None, None, 128, arr, None, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # codes
+    assert f(ctypes.byref(plan), 0, None, None, 128, arr, arr, None, arr, arr, None) == awsrc.AWSRC_EINVAL  # mean
+    mis = (v * 1)(258)
+    assert f(ctypes.byref(plan), 0, None, None, 128, arr, arr, mis, arr, arr, None) == awsrc.AWSRC_EINVAL   # align
+    assert f(ctypes.byref(plan), 0, None, None, 96, arr, arr, arr, arr, arr, None) == awsrc.AWSRC_EINVAL    # group
+    plan.w0_dtype = awsrc.AWSRC_DTYPE_F32
+    assert f(ctypes.byref(plan), 0, None, None, 128, arr, arr, arr, arr, arr, None) == awsrc.AWSRC_EINVAL  # fp32 plan
+
+
 def test_sdq_rejects_bad_arguments_without_device_access():
     enc = awsrc.LIB.awsrc_sdq_encode
     assert enc(None, -1, None, None, None, None) == awsrc.AWSRC_EINVAL

@@ -804,6 +804,49 @@ def test_reconstruct_bf16_prefixes_match_single_calls_and_oracle(C, P, b, S, gro
         _check_reconstruct(C, sub, k, W0o, O.reconstruct_bf16(sub, bbs, group), got, mods)
 
 
+@pytest.mark.parametrize("C,P,b,S,group,mods,fmt", [
+    (64, 8, 4, 256, 128, [(33, 512), (300, 1024), (1, 128)], 0),   # ten SDQ blocks, a partial last one
+    (16, 4, 4, 16, 64, [(5, 128), (3, 256)], 0),
+    (64, 4, 4, 32, 128, [(2 + m % 3, 128 * (1 + m % 2)) for m in range(230)], 1),  # two module windows
+])
+def test_reconstruct_bf16_sdq_matches_oracle(C, P, b, S, group, mods, fmt):
+    """Dense bf16 reconstruction on the RTN-INT4-SDQ backbone: into the plan's
+    own targets (every record) and into four nested prefixes in one call,
+    against the oracle's SDQ reconstruction of each prefix."""
+    op = O.Params(C=C, P=P, b=b, S=S, basis_key=0x51, scale_fmt=fmt)
+    T = sum(r * c // C for r, c in mods)
+    rec = gen_records(T, P, b, S, seed=21)
+    if fmt == O.SCALE_POW2:
+        rec["scale"] = (100 + (rec["scale"].to(torch.int32) & 0x1F)).to(torch.int16)
+    enc = {"seed": rec["seed"].numpy().astype(np.int64) & 0xFFFF, "codes": rec["codes"].numpy().astype(np.int64),
+           "scale": rec["scale"].numpy().astype(np.int64) & 0xFFFF, "gain": rec["gain"].numpy()}
+    stream, K, _ = O.build_stream(op, mods, enc, 2.0, per_module=False)
+    assert K > 8
+    g = torch.Generator().manual_seed(22)
+    bbs = []
+    for r, c in mods:
+        cd, s16, z, _ = O.rtn_backbone((torch.randn(r, c, generator=g) * 0.02).numpy(), group)
+        sc, mu, st = O.sdq_encode(s16)
+        bbs.append((cd, z, sc, mu, st))
+    dev_bb = [tuple(torch.from_numpy(np.ascontiguousarray(a)).to(DEV) for a in bb) for bb in bbs]
+    W0s = [O.rtn_dequant_sdq(cd, z, sc, mu, st, group) for cd, z, sc, mu, st in bbs]
+    sb = torch.tensor(list(stream), dtype=torch.uint8, device=DEV)
+    outs = [torch.full((r, c), -1, dtype=torch.int16, device=DEV).view(torch.bfloat16) for r, c in mods]
+    plan, ws = awsrc.awsrc_decode_prepare(sb, outs)
+    awsrc.awsrc_reconstruct_bf16_sdq(plan, dev_bb, group=group)
+    torch.cuda.synchronize()
+    _check_reconstruct(C, stream, K, W0s, O.reconstruct_bf16_sdq(stream, bbs, group), outs, mods)
+    hd = O.parse_header(stream)
+    h, L = hd["h"], hd["L_rec"]
+    Ks = [K // 3, 0, K, K // 2]
+    pre = [[torch.full((r, c), -1, dtype=torch.int16, device=DEV).view(torch.bfloat16) for r, c in mods] for _ in Ks]
+    awsrc.awsrc_reconstruct_bf16_sdq(plan, dev_bb, K_out=Ks, outs=pre, group=group)
+    torch.cuda.synchronize()
+    for k, got in zip(Ks, pre):
+        sub = stream[:h + k * L]
+        _check_reconstruct(C, sub, k, W0s, O.reconstruct_bf16_sdq(sub, bbs, group), got, mods)
+
+
 def test_reconstruct_bf16_empty_stream_and_many_modules():
     """K = 0 gives bf16(W0) everywhere; 300 modules exceed the module table
     the dense pass stages in LDS."""
