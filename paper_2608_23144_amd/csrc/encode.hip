@@ -576,6 +576,195 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col64(EncodeArgs a) {
   rescore_block64<PB>(a, blk, row0, tg, ts, lds);
 }
 
+// Per-column weights, generator version 1, C = 128 (the C = 128 screen's
+// lists): one wavefront per (16-row group, column block), four lanes per
+// tile.  Lane l works on tile l % 16 and its coordinates 32 (l / 16) .. + 31:
+// it forms sigma .* d .* r for them in fp64 and runs the first five butterfly
+// stages of the length-128 transform on them in registers; the last two
+// stages, which combine the four quarters, are folded into the gathers of
+// the P projections (the same additions in the same order as the full
+// transform, so the same values).  The Gram entries come from the column
+// block's fp64 weight transform, eps from the sum of the block's d in
+// coordinate order, and the solve is the per-element re-score's (LDL^T with
+// refined reciprocals).  Work items go row group major (the next item is the next column
+// block of the same rows, whose outputs share cache lines), in contiguous
+// ranges per XCD.
+constexpr int kQ128 = 33;                  // doubles per quarter in a gather row (padded)
+constexpr int kRow128 = 4 * kQ128 + 1;     // doubles per gather row
+
+__device__ __forceinline__ double tentry128(const double* row, int k) {
+  const int kk = k & 31, q = k >> 5;
+  const double x0 = row[kk], x1 = row[kQ128 + kk], x2 = row[2 * kQ128 + kk], x3 = row[3 * kQ128 + kk];
+  // stage h = 32, then h = 64
+  const double y0 = x0 + x1, y1 = x0 - x1, y2 = x2 + x3, y3 = x2 - x3;
+  return q == 0 ? y0 + y2 : q == 1 ? y1 + y3 : q == 2 ? y0 - y2 : y1 - y3;
+}
+
+template <int PB>
+__global__ __launch_bounds__(64, 2) void k_finalize_col128(EncodeArgs a) {
+  constexpr int C = 128, NTL = 16, H = 32;
+  __shared__ __attribute__((aligned(16))) double gsh[NTL * kRow128];  // r staging (fp32), then gather rows
+  __shared__ float dsh[C];
+  __shared__ double wdsh[C];
+  const int lane = threadIdx.x;
+  const int tl = lane & (NTL - 1), qd = lane >> 4;
+  const int nb = (int)(a.cols / C);
+  const int64_t w = xcd_item(blockIdx.x, gridDim.x);
+  const int blk = (int)(w % nb);
+  const int64_t row0 = (w / nb) * NTL;
+  const int64_t row = row0 + tl;
+  const bool valid = row < a.rows;
+  for (int j = lane; j < C; j += 64) {
+    dsh[j] = a.d[(int64_t)blk * C + j];
+    wdsh[j] = a.wd64[(int64_t)blk * C + j];
+  }
+  // the 16 x 128 residual block, 32 lanes per row (4 coordinates each), two
+  // rows per pass; rows past the end repeat the last row
+  float* rsh = reinterpret_cast<float*>(gsh);
+  {
+    const int pc = lane & 31;
+#pragma unroll
+    for (int pass = 0; pass < NTL / 2; ++pass) {
+      const int rl = 2 * pass + (lane >> 5);
+      const int64_t rg = row0 + rl < a.rows ? row0 + rl : a.rows - 1;
+      const int64_t o = rg * a.cols + (int64_t)blk * C + 4 * pc;
+      float wv[4];
+      if (a.w_dtype == AWSRC_DTYPE_F32) {
+        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.W) + o);
+        wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
+      } else {
+        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.W) + o);
+        wv[0] = __uint_as_float(x.x << 16); wv[1] = __uint_as_float(x.x & 0xFFFF0000u);
+        wv[2] = __uint_as_float(x.y << 16); wv[3] = __uint_as_float(x.y & 0xFFFF0000u);
+      }
+      const float4 y = *reinterpret_cast<const float4*>(a.W0 + o);
+      float* rp = rsh + rl * (C + 1) + 4 * pc;
+      rp[0] = wv[0] - y.x; rp[1] = wv[1] - y.y; rp[2] = wv[2] - y.z; rp[3] = wv[3] - y.w;
+    }
+  }
+  __syncthreads();
+  float rr[H];
+#pragma unroll
+  for (int j = 0; j < H; ++j) rr[j] = rsh[tl * (C + 1) + H * qd + j];
+  // the tile's weighted energy (each lane's quarter, then the quarters
+  // added), for the re-score window; eps from the block's d summed in
+  // coordinate order
+  float e32;
+  {
+    float eq = 0.0f;
+#pragma unroll
+    for (int j = 0; j < H; ++j) {
+      const float dj = dsh[H * qd + j];
+      eq = fmaf(dj * rr[j], rr[j], eq);
+    }
+    eq += __shfl_xor(eq, 16, 64);
+    e32 = eq + __shfl_xor(eq, 32, 64);
+  }
+  double sumd = 0.0;  // in order, one value at a time (left unrolled, all 128 are held in registers)
+#pragma unroll 1
+  for (int j = 0; j < C; ++j) sumd += (double)dsh[j];
+  const double eps = a.lambda * (sumd / C);
+  const int P = a.P;
+  const double isq = 1.0 / sqrt((double)C);
+  const int qmax = (1 << (a.b - 1)) - 1;
+  const int64_t t = (valid ? row : a.rows - 1) * nb + blk;
+
+  // merge the seed ranges' lists into the best kTop (as finalize_tile)
+  float tg[kTop];
+  uint32_t ts[kTop];
+#pragma unroll
+  for (int k = 0; k < kTop; ++k) { tg[k] = -INFINITY; ts[k] = 0; }
+  for (int sp = 0; sp < a.nsplit; ++sp) {
+#pragma unroll
+    for (int k = 0; k < kTop; ++k) {
+      const int64_t at = (t * a.nsplit + sp) * kTop + k;
+      float g = a.top_gain[at];
+      uint32_t sd = a.top_seed[at];
+#pragma unroll
+      for (int m = 0; m < kTop; ++m) {
+        if (g > tg[m]) {
+          const float tgm = tg[m];
+          const uint32_t tsm = ts[m];
+          tg[m] = g; ts[m] = sd;
+          g = tgm; sd = tsm;
+        }
+      }
+    }
+  }
+  // the second kept seed is re-scored when its screened gain lies within the
+  // window of the best; lanes of quarter 0 score the best seed, lanes of
+  // quarter 1 the second one where needed (else the best again)
+  const float thr = tg[0] - rescore_window(tg[0], e32, ((ts[0] | ts[1]) & kEdge) != 0);
+  const bool need = valid && tg[1] >= thr && tg[1] > -INFINITY;
+  const bool two = __ballot(need) != 0;
+  const int s0r = list_seed(ts[0]), s1r = list_seed(ts[1]);
+  const int s0 = s0r < a.S ? s0r : 0, s1 = s1r < a.S ? s1r : 0;
+  const bool mine2 = qd == 1 && need;
+  const int s_me = mine2 ? s1 : s0;
+  int c[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) c[p] = (p < P) ? a.basis.col[(size_t)s_me * kMaxP + p] : 0;
+  double* grow = gsh + tl * kRow128;
+  double bv[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) bv[p] = 0.0;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1 && !two) break;
+    const int sp_ = pass ? s1 : s0;
+    const uint32_t sw = (uint32_t)(a.basis.sign[(size_t)sp_ * 2 + (qd >> 1)] >> (H * (qd & 1)));
+    double v[H];
+#pragma unroll
+    for (int j = 0; j < H; ++j) {
+      const double u = (double)dsh[H * qd + j] * (double)rr[j];
+      v[j] = ((sw >> j) & 1u) ? -u : u;
+    }
+    fwht<H>(v);
+    __syncthreads();  // the staging rows (pass 0) or the previous gathers are done
+#pragma unroll
+    for (int j = 0; j < H; ++j) grow[kQ128 * qd + j] = v[j];
+    __syncthreads();
+    // quarter 0 gathers from the best seed's pass, quarter 1 from the second
+    // seed's pass where its tile needs it, else from the best seed's
+    if (qd < 2 && (pass == 1) == mine2) {
+#pragma unroll
+      for (int p = 0; p < PB; ++p) bv[p] = (p < P) ? tentry128(grow, c[p]) * isq : 0.0;
+    }
+  }
+  // quarters 0 and 1 solve (the best seed, and the second or the best again)
+  double gk = -INFINITY;
+  int q[PB];
+  double al[PB];
+  uint16_t bits = 0;
+  if (qd < 2) {
+    double g[PB * (PB + 1) / 2];
+#pragma unroll
+    for (int p = 0; p < PB; ++p)
+#pragma unroll
+      for (int r = 0; r <= p; ++r) g[p * (p + 1) / 2 + r] = wdsh[c[p] ^ c[r]];
+    double L[PB * (PB - 1) / 2], e[PB], inv[PB];
+    ldl64<C, PB>(P, g, eps, L, e, inv);
+    gk = solve_score_ldl<PB>(a, bv, L, e, inv, eps, qmax, q, al, &bits);
+  }
+  // the better of the two results (ties: the lower seed) is written by the
+  // lane that holds it
+  const double go = __shfl_xor(gk, 16, 64);
+  const bool second_wins =
+      need && (qd == 1 ? (gk > go || (gk == go && s1 < s0)) : (go > gk || (go == gk && s1 < s0)));
+  if (valid && qd < 2 && (qd == 1) == second_wins) {
+    a.seed_out[t] = (uint16_t)s_me;
+    a.scale_out[t] = bits;
+    a.gain_out[t] = gk;
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      if (p < P) {
+        a.code_out[t * P + p] = (int8_t)q[p];
+        if (a.alpha_out) a.alpha_out[t * P + p] = (float)al[p];
+      }
+    }
+  }
+}
+
 // ----------------------------------------------------------------------------
 static int pad_p(int P) { return P <= 4 ? 4 : (P <= 8 ? 8 : 16); }
 
@@ -625,6 +814,11 @@ static hipError_t run_finalize(const EncodeArgs& a, hipStream_t st) {
   } else if (C == 64 && PB <= 8 && a.gen_version == 1) {
     if constexpr (C == 64 && PB <= 8)
       hipLaunchKernelGGL((k_finalize_col64<PB>), dim3((unsigned)groups), dim3(64), 0, st, a);
+  } else if (C == 128 && PB == 8 && a.gen_version == 1) {
+    if constexpr (C == 128 && PB == 8) {
+      const int64_t items = nb * ((a.rows + 15) / 16);
+      hipLaunchKernelGGL((k_finalize_col128<PB>), dim3((unsigned)items), dim3(64), 0, st, a);
+    }
   } else {
     hipLaunchKernelGGL((k_finalize<C, PB, false>), dim3((unsigned)groups), dim3(NT), lds, st, a,
                        (const double*)a.wd64);

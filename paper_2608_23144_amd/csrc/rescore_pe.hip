@@ -45,113 +45,6 @@ __device__ __forceinline__ double tentry(const double* row, int k) {
 
 }  // namespace
 
-// 1 / x in fp64: the hardware reciprocal refined by two Newton steps (the
-// error of the estimate squares at each step; well inside the solve's own
-// rounding).
-__device__ __forceinline__ double recip64(double x) {
-  double r = __builtin_amdgcn_rcp(x);
-  r = fma(r, fma(-x, r, 1.0), r);
-  return fma(r, fma(-x, r, 1.0), r);
-}
-
-// G + eps I = L diag(e) L^T (L unit lower triangular, strict part packed by
-// rows) in fp64 from the gathered transform values g (packed lower triangle
-// with the diagonal; G_pr = g / C); inv = 1 / e.  Padding columns p >= P get
-// L = 0, e = 1.  No square roots, one reciprocal per pivot.
-template <int PB>
-__device__ __forceinline__ void ldl64(int P, const double (&g)[PB * (PB + 1) / 2], double eps,
-                                      double (&L)[PB * (PB - 1) / 2], double (&e)[PB], double (&inv)[PB]) {
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    double E[PB];  // row p of L diag(e)
-#pragma unroll
-    for (int r = 0; r < p; ++r) {
-      double acc = (p < P && r < P) ? g[p * (p + 1) / 2 + r] * (1.0 / kC) : 0.0;
-#pragma unroll
-      for (int k = 0; k < r; ++k) acc = fma(-E[k], L[ltri(r, k)], acc);
-      E[r] = acc;
-      L[ltri(p, r)] = acc * inv[r];
-    }
-    double acc = p < P ? fma(g[p * (p + 1) / 2 + p], 1.0 / kC, eps) : 1.0;
-#pragma unroll
-    for (int k = 0; k < p; ++k) acc = fma(-E[k], L[ltri(p, k)], acc);
-    e[p] = fmax(acc, 1e-300);
-    inv[p] = recip64(e[p]);
-  }
-}
-
-// The fp64 re-score of one candidate from its projections bv = B^T u and the
-// factor of its G + eps I: the solve of Eq. (3) for the unquantized fit al,
-// the stored scale (bits) and codes q (Sec. 3.2), and the gain
-// 2 a.b - a^T G0 a of the quantized fit a = scale q, with
-// a^T G0 a = sum_k e_k ((L^T a)_k)^2 - eps |a|^2.
-template <int PB>
-__device__ __forceinline__ double solve_score_ldl(const EncodeArgs& a, const double (&bv)[PB],
-                                                  const double (&L)[PB * (PB - 1) / 2], const double (&e)[PB],
-                                                  const double (&inv)[PB], double eps, int qmax, int (&q)[PB],
-                                                  double (&al)[PB], uint16_t* bits_out) {
-  double z[PB];
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    double acc = bv[p];
-#pragma unroll
-    for (int k = 0; k < p; ++k) acc = fma(-L[ltri(p, k)], z[k], acc);
-    z[p] = acc;
-  }
-#pragma unroll
-  for (int p = PB - 1; p >= 0; --p) {
-    double acc = z[p] * inv[p];
-#pragma unroll
-    for (int k = p + 1; k < PB; ++k) acc = fma(-L[ltri(k, p)], al[k], acc);
-    al[p] = acc;
-  }
-  double m = 0.0;
-#pragma unroll
-  for (int p = 0; p < PB; ++p) m = fmax(m, fabs(al[p]));
-  uint16_t bits = 0;
-  double sc = 0.0;
-  if (m > 0.0) {
-    if (a.scale_fmt == AWSRC_SCALE_POW2) {
-      // smallest e with m <= qmax 2^e, by exact comparisons; field e + 128
-      int ex;
-      frexp(m / (double)qmax, &ex);
-      while (m > (double)qmax * ldexp(1.0, ex)) ++ex;
-      while (m <= (double)qmax * ldexp(1.0, ex - 1)) --ex;
-      ex = ex < -128 ? -128 : (ex > 127 ? 127 : ex);
-      bits = (uint16_t)(ex + 128);
-      sc = ldexp(1.0, ex);
-    } else {
-      // fp16 scale: f16(f32(m / qmax)), both round-to-nearest-even
-      bits = scale_bits_from_f64(m / (double)qmax);
-      sc = (double)__half2float(__ushort_as_half(bits));
-      if (!(sc > 0.0)) { bits = 0; sc = 0.0; }
-    }
-  }
-  const double isc = sc > 0.0 ? 1.0 / sc : 0.0;
-  double ah[PB];
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    const double qv = fmin(fmax(rint(al[p] * isc), (double)-qmax), (double)qmax);
-    q[p] = (int)qv;
-    ah[p] = sc * qv;
-  }
-  double t1 = 0.0, aa = 0.0, quad = 0.0;
-#pragma unroll
-  for (int p = 0; p < PB; ++p) {
-    t1 = fma(ah[p], bv[p], t1);
-    aa = fma(ah[p], ah[p], aa);
-  }
-#pragma unroll
-  for (int k = 0; k < PB; ++k) {
-    double y = ah[k];
-#pragma unroll
-    for (int i = k + 1; i < PB; ++i) y = fma(L[ltri(i, k)], ah[i], y);
-    quad = fma(e[k] * y, y, quad);
-  }
-  *bits_out = bits;
-  return 2.0 * t1 - (quad - eps * aa);
-}
-
 template <int PB>
 __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, const ModEntry* __restrict__ mods,
                                                                int n_mods) {
@@ -301,7 +194,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
       for (int r = 0; r <= p; ++r) g[p * (p + 1) / 2 + r] = tentry(grow, c[p] ^ c[r]);
   }
   double L[PB * (PB - 1) / 2], e[PB], inv[PB];
-  ldl64<PB>(P, g, eps, L, e, inv);
+  ldl64<kC, PB>(P, g, eps, L, e, inv);
   int q[PB];
   double al[PB];
   uint16_t bits;
