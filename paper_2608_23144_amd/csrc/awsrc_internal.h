@@ -355,11 +355,13 @@ bool screen_pruned(int C, int P, int d_mode, int gen_version);
 bool screen_fuses_rescore(int C, int P, int d_mode, int gen_version, int nsplit);
 
 // ---------------------------------------------------------------- ranking
-// One survivor of the selection: ~(gain key) and its global tile index.
+// One survivor of the selection: ~(gain key), its global tile index, and
+// the tile's seed | scale << 16 (carried by the radix sort so that packing
+// gathers only the codes).
 struct __attribute__((aligned(16))) SortItem {
   uint64_t key;
   uint32_t tile;
-  uint32_t pad;
+  uint32_t aux;
 };
 
 struct RankWs {

@@ -350,7 +350,10 @@ __global__ __launch_bounds__(1024) void k_compact_scan(uint64_t* blk_gt, uint64_
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_compact_write(const double* __restrict__ gain, int64_t t0, int64_t n,
+// gain: the segment's gains (from tile t0); seed, scale: every tile's
+__global__ __launch_bounds__(kThreads) void k_compact_write(const double* __restrict__ gain,
+                                                            const uint16_t* __restrict__ seed,
+                                                            const uint16_t* __restrict__ scale, int64_t t0, int64_t n,
                                                             const uint64_t* __restrict__ state,
                                                             const uint64_t* __restrict__ sel_off,
                                                             const uint64_t* __restrict__ eq_off,
@@ -376,7 +379,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_write(const double* __rest
       SortItem it;
       it.key = ~k;  // ascending ~key = descending gain
       it.tile = (uint32_t)(t0 + i);
-      it.pad = 0u;
+      it.aux = (uint32_t)seed[t0 + i] | ((uint32_t)scale[t0 + i] << 16);
       items_out[sel_run + pos] = it;
     }
     eq_run += eq_tot;
@@ -405,7 +408,10 @@ __device__ __forceinline__ void put_bits(uint64_t (&w)[3], int& pos, uint64_t v,
 // Record i of the segment (tile t) goes to byte h + (first slot + i) * L of
 // the stream; a stream buffer too small for the running total raises the
 // no-space flag instead.
-__device__ void pack_record(const PackArgs& pa, uint64_t* state, int64_t i, uint32_t t) {
+// Record i of the stream from tile t; aux = the tile's seed | scale << 16.
+// A record at a 4-byte aligned place whose size is a multiple of 4 goes out
+// as whole words.
+__device__ void pack_record(const PackArgs& pa, uint64_t* state, int64_t i, uint32_t t, uint32_t aux) {
   const uint64_t K = state[kSegK], off = state[kSegOff];
   if (pa.h + (off + K) * (uint64_t)pa.L > pa.cap) {
     if (i == 0) state[kNoSpace] = 1;
@@ -414,12 +420,22 @@ __device__ void pack_record(const PackArgs& pa, uint64_t* state, int64_t i, uint
   uint64_t w[3] = {0, 0, 0};
   int pos = 0;
   put_bits(w, pos, (uint64_t)t, pa.idx_bits);
-  put_bits(w, pos, (uint64_t)pa.seed[t], pa.seed_bits);
+  put_bits(w, pos, (uint64_t)(aux & 0xFFFFu), pa.seed_bits);
   const uint64_t cm = (1ull << pa.b) - 1ull;
   for (int p = 0; p < pa.P; ++p) put_bits(w, pos, (uint64_t)(int64_t)pa.code[(int64_t)t * pa.P + p] & cm, pa.b);
-  put_bits(w, pos, (uint64_t)pa.scale[t] & ((1ull << pa.scale_bits) - 1ull), pa.scale_bits);
+  put_bits(w, pos, (uint64_t)(aux >> 16) & ((1ull << pa.scale_bits) - 1ull), pa.scale_bits);
   uint8_t* o = pa.out + pa.h + (off + (uint64_t)i) * (uint64_t)pa.L;
-  for (int k = 0; k < pa.L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
+  if (((reinterpret_cast<uintptr_t>(o) | (uintptr_t)pa.L) & 3) == 0) {
+    uint32_t* o32 = reinterpret_cast<uint32_t*>(o);
+    for (int k = 0; k < pa.L / 4; ++k) o32[k] = (uint32_t)(w[k >> 1] >> (32 * (k & 1)));
+  } else {
+    for (int k = 0; k < pa.L; ++k) o[k] = (uint8_t)(w[k >> 3] >> (8 * (k & 7)));
+  }
+}
+
+// the same, with the seed and scale read from the encoder outputs
+__device__ __forceinline__ void pack_record(const PackArgs& pa, uint64_t* state, int64_t i, uint32_t t) {
+  pack_record(pa, state, i, t, (uint32_t)pa.seed[t] | ((uint32_t)pa.scale[t] << 16));
 }
 
 // ---------------------------------------------------------------- sort of the survivors
@@ -493,7 +509,7 @@ __global__ __launch_bounds__(kChunkThreads) void k_sort_chunks(SortItem* __restr
         SortItem x;
         x.key = sk[j];
         x.tile = st[j];
-        x.pad = 0u;
+        x.aux = 0u;  // the merge passes pack from the encoder outputs
         items[i] = x;
       }
     }
@@ -639,7 +655,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
     const int64_t i = base + r * kRsThreads + t;
     const bool valid = i < n;
     SortItem x;
-    x.key = 0; x.tile = 0; x.pad = 0;
+    x.key = 0; x.tile = 0; x.aux = 0;
     if (valid) x = in[i];
     const uint32_t d = (uint32_t)(x.key >> shift) & (kRsBins - 1);
     // lanes of this wavefront holding the same digit
@@ -656,7 +672,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
       uint32_t off = dbase[d] + rank;
 #pragma unroll
       for (int k = 0; k < kRsThreads / 64; ++k) off += k < w ? wc[k][d] : 0u;
-      if (pack) pack_record(pa, state, (int64_t)off, x.tile);
+      if (pack) pack_record(pa, state, (int64_t)off, x.tile, x.aux);
       else out[off] = x;
     }
     __syncthreads();
@@ -733,7 +749,7 @@ hipError_t launch_rank_segment(const double* gain, int64_t t0, int64_t n, int64_
   hipLaunchKernelGGL(k_compact_count, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, n, ws.state, ws.blk_a, ws.blk_b);
   hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(1024), 0, st, ws.blk_a, ws.blk_b, nbc, ws.state);
   if (cap <= 0 || n <= 0) return hipGetLastError();
-  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, t0, n, ws.state,
+  hipLaunchKernelGGL(k_compact_write, dim3((unsigned)nbc), dim3(kThreads), 0, st, g, seed, scale, t0, n, ws.state,
                      ws.blk_a, ws.blk_b, ws.items_a);
   // sort the survivors ascending on (~key, tile): LDS chunks, then multiway
   // merges; the final pass packs the records instead of writing items
