@@ -44,27 +44,45 @@ def log(*a):
 # figure is reported as null until the counters are taken again.
 MEASURED_TRAFFIC = {
     # one step of the 36-layer 3B stack (profiles/counters_stack3b.md): the
-    # encode call over all 252 modules (screen 29.07 GB, fp64 re-score
-    # 32.61 GB, tables), the 252 backbone launches, the decode-add of the
-    # 0.32 bpw stream, and the reconstruction of its four nested prefixes
-    # (tile ordering and the streaming pass)
+    # encode call over all 252 modules (screen 29.76 GB, fp64 re-score
+    # 29.32 GB, tables), the 252 backbone launches, the decode-add of the
+    # 0.32 bpw stream, the reconstruction of its four nested prefixes (tile
+    # ordering and the streaming pass), and the same on the SDQ backbone
     ("encode", "stack3b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
                   "rescore_pe.hip", "rescore64.h"],
-        "sha256": "93859c70ba09ebd77b9819f4a1ce1ed83c3fdd116a10503d198f88e71e96eb73",
-        "bytes": 61683747392},
+        "sha256": "6a74401cf2fe5daef9e39015ad9140785d1ccd09f03f8d675f761820e73b37d5",
+        "bytes": 59077351520},
     ("backbone", "stack3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "2586f4a4ee2525c8112f6162fb034c15353c68d33c33a3e90eb8fa7da64bbee1",
-        "bytes": 18135996224},
+        "sha256": "b074178e7b2d45f0ef5bb61505337dabac7ef556a8d0eca21ff5d4bed0d1c8e7",
+        "bytes": 19295865376},
     ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "691a07e975fd9309ea40e694ef8f23a0f87b1062c19332572ab04ddf587c598e",
-        "bytes": 5036702720},
+        "sha256": "8a4d4666a3da9bea031699bc4a01457eee17b6e5b3dec62e130501885ee3fa98",
+        "bytes": 5036683904},
     ("reconstruct_bf16", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "691a07e975fd9309ea40e694ef8f23a0f87b1062c19332572ab04ddf587c598e",
-        "bytes": 26482273152},
+        "sha256": "8a4d4666a3da9bea031699bc4a01457eee17b6e5b3dec62e130501885ee3fa98",
+        "bytes": 26473087584},
+    ("reconstruct_bf16_sdq", "stack3b"): {
+        "files": ["awsrc_internal.h", "decode.hip"],
+        "sha256": "8a4d4666a3da9bea031699bc4a01457eee17b6e5b3dec62e130501885ee3fa98",
+        "bytes": 26296352864},
+    # one step of the 32B layer (profiles/counters_layer32b.md)
+    ("encode", "layer32b"): {
+        "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
+                  "rescore_pe.hip", "rescore64.h"],
+        "sha256": "6a74401cf2fe5daef9e39015ad9140785d1ccd09f03f8d675f761820e73b37d5",
+        "bytes": 8017005056},
+    ("backbone", "layer32b"): {
+        "files": ["awsrc_internal.h", "backbone.hip"],
+        "sha256": "b074178e7b2d45f0ef5bb61505337dabac7ef556a8d0eca21ff5d4bed0d1c8e7",
+        "bytes": 3513942560},
+    ("decode_apply", "layer32b"): {
+        "files": ["awsrc_internal.h", "decode.hip"],
+        "sha256": "8a4d4666a3da9bea031699bc4a01457eee17b6e5b3dec62e130501885ee3fa98",
+        "bytes": 951871616},
 }
 
 
@@ -266,7 +284,8 @@ def sdq_timing(awsrc, torch, wl, run, stream, reps: int = 20) -> dict:
         rc_bytes = n_w // 2 + 2 * n_g + 8 * n_blk + len(ks) * 2 * n_w + max(ks) * run.L
         rc = {"reconstruct_prefixes": len(ks), "reconstruct_ms": rc_ms, "reconstruct_bytes": rc_bytes,
               "reconstruct_GB/s": rc_bytes / (rc_ms / 1e3) / 1e9,
-              "reconstruct_frac_hbm": rc_bytes / (rc_ms / 1e3) / 1e9 / PEAK_HBM_GBS}
+              "reconstruct_frac_hbm": rc_bytes / (rc_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+              "reconstruct_traffic": measured_traffic("reconstruct_bf16_sdq", wl.name)}
     return {**rc, "groups": n_g, "scale_bits_per_weight": (8 * n_g + 64 * n_blk) / n_w,
             "fp16_scale_bits_per_weight": 16 * n_g / n_w,
             "encode_ms": enc_ms, "dequant_ms": deq_ms, "dequant_bytes": deq_bytes,
