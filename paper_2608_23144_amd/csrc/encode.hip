@@ -619,27 +619,25 @@ __global__ __launch_bounds__(64, 2) void k_finalize_col128(EncodeArgs a) {
     wdsh[j] = a.wd64[(int64_t)blk * C + j];
   }
   // the 16 x 128 residual block, 32 lanes per row (4 coordinates each), two
-  // rows per pass; rows past the end repeat the last row
+  // rows per pass, every load issued before any is used; rows past the end
+  // repeat the last row
   float* rsh = reinterpret_cast<float*>(gsh);
   {
     const int pc = lane & 31;
+    constexpr int NP = NTL / 2;
+    int64_t o[NP];
 #pragma unroll
-    for (int pass = 0; pass < NTL / 2; ++pass) {
+    for (int pass = 0; pass < NP; ++pass) {
       const int rl = 2 * pass + (lane >> 5);
       const int64_t rg = row0 + rl < a.rows ? row0 + rl : a.rows - 1;
-      const int64_t o = rg * a.cols + (int64_t)blk * C + 4 * pc;
-      float wv[4];
-      if (a.w_dtype == AWSRC_DTYPE_F32) {
-        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.W) + o);
-        wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
-      } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.W) + o);
-        wv[0] = __uint_as_float(x.x << 16); wv[1] = __uint_as_float(x.x & 0xFFFF0000u);
-        wv[2] = __uint_as_float(x.y << 16); wv[3] = __uint_as_float(x.y & 0xFFFF0000u);
-      }
-      const float4 y = *reinterpret_cast<const float4*>(a.W0 + o);
-      float* rp = rsh + rl * (C + 1) + 4 * pc;
-      rp[0] = wv[0] - y.x; rp[1] = wv[1] - y.y; rp[2] = wv[2] - y.z; rp[3] = wv[3] - y.w;
+      o[pass] = rg * a.cols + (int64_t)blk * C + 4 * pc;
+    }
+    float rv[NP][4];
+    load_residual4<NP>(a.W, a.w_dtype, a.W0, o, rv);
+#pragma unroll
+    for (int pass = 0; pass < NP; ++pass) {
+      float* rp = rsh + (2 * pass + (lane >> 5)) * (C + 1) + 4 * pc;
+      rp[0] = rv[pass][0]; rp[1] = rv[pass][1]; rp[2] = rv[pass][2]; rp[3] = rv[pass][3];
     }
   }
   __syncthreads();

@@ -32,15 +32,6 @@
 
 namespace awsrc {
 
-namespace {
-
-__device__ __forceinline__ float load_w_any2(const void* W, int dt, int64_t i) {
-  if (dt == AWSRC_DTYPE_F32) return static_cast<const float*>(W)[i];
-  return __uint_as_float((uint32_t)static_cast<const uint16_t*>(W)[i] << 16);
-}
-
-}  // namespace
-
 // ----------------------------------------------------------------------------
 // +-1 basis fragments: frag[pair][ks][lane] = 8 bf16 (4 dwords) of row
 // m = lane % 16 (seed 2*pair + m/8, column m % 8) at coordinates
@@ -104,25 +95,52 @@ __device__ __forceinline__ ScreenTask screen_task(const EncodeArgs& a, int rows_
 // split in three bf16 parts; rows past the end give zeros.  en[nb] returns
 // each tile's weighted energy sum_j d_j r_j^2 (summed over the four lanes
 // n, n + 16, n + 32, n + 48 that share the tile's row).
-__device__ __forceinline__ void load_u64(const EncodeArgs& a, int64_t row0, int blk, int n, int g,
-                                         u32x4 (&uh)[4][2], u32x4 (&um)[4][2], u32x4 (&ul)[4][2], float (&en)[4]) {
-  constexpr int C = 64;
+// The u fragments of NB x 16 tiles (rows row0 + 16 nb + n) over the C = 32
+// NKS coordinates of column block blk, per-column weights: lane (n, g) holds
+// coordinates 32 ks + 8 g .. + 7 of each of its NB rows, split exactly in
+// three bf16 parts; en[nb] gets the tile's weighted energy sum_j d_j r_j^2
+// (over the four lanes n, n + 16, n + 32, n + 48 that share a row).  Every
+// load is issued before any is used: the residual as 2 NB NKS chunks of four
+// weights, the column weights as 2 NKS chunks (the same for every row).
+template <int C, int NB>
+__device__ __forceinline__ void load_u_col(const EncodeArgs& a, int64_t row0, int blk, int n, int g,
+                                           u32x4 (&uh)[NB][C / 32], u32x4 (&um)[NB][C / 32],
+                                           u32x4 (&ul)[NB][C / 32], float (&en)[NB]) {
+  constexpr int NKS = C / 32;
+  constexpr int NCH = 2 * NB * NKS;
+  int64_t o[NCH];
+  bool valid[NB];
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     const int64_t row = row0 + 16 * nb + n;
-    const bool valid = row < a.rows;
-    const int64_t rr = valid ? row : a.rows - 1;
+    valid[nb] = row < a.rows;
+    const int64_t rr = valid[nb] ? row : a.rows - 1;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int64_t base = rr * a.cols + (int64_t)blk * C + 32 * ks + 8 * g;
+      o[2 * (nb * NKS + ks)] = base;
+      o[2 * (nb * NKS + ks) + 1] = base + 4;
+    }
+  }
+  gf32x4 dv[2 * NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    dv[2 * ks] = gload4f(a.d + (int64_t)blk * C + 32 * ks + 8 * g);
+    dv[2 * ks + 1] = gload4f(a.d + (int64_t)blk * C + 32 * ks + 8 * g + 4);
+  }
+  float rv[NCH][4];
+  load_residual4<NCH>(a.W, a.w_dtype, a.W0, o, rv);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
     float e = 0.0f;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int jc = 32 * ks + 8 * g;
-      const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
+    for (int ks = 0; ks < NKS; ++ks) {
       float u[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float r = load_w_any2(a.W, a.w_dtype, base + k) - a.W0[base + k];
-        const float dj = a.d[(int64_t)blk * C + jc + k];
-        u[k] = valid ? dj * r : 0.0f;
+        const float r = rv[2 * (nb * NKS + ks) + (k >> 2)][k & 3];
+        const float dj = dv[2 * ks + (k >> 2)][k & 3];
+        u[k] = valid[nb] ? dj * r : 0.0f;
         e = fmaf(dj * r, r, e);
       }
       split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
@@ -213,7 +231,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   const int nb0 = 2 * (g & 1);  // its tiles: 16 nb0 + n and 16 (nb0 + 1) + n
   u32x4 uh[4][2], um[4][2], ul[4][2];
   float en[4];
-  load_u64(a, tk.row0, blk, n, g, uh, um, ul, en);
+  load_u_col<64, 4>(a, tk.row0, blk, n, g, uh, um, ul, en);
   const int64_t trow0 = tk.row0 + 16 * nb0 + n;
   const bool tv[2] = {trow0 < a.rows, trow0 + 16 < a.rows};
   const float qmax = (float)((1 << (a.b - 1)) - 1);
@@ -502,29 +520,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   // four lanes n, n + 16, n + 32, n + 48 that share a row)
   u32x4 uh[2][NKS], um[2][NKS], ul[2][NKS];
   float en[2];
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int64_t row = row0 + 16 * nb + n;
-    const bool valid = row < a.rows;
-    const int64_t rr = valid ? row : a.rows - 1;
-    float e = 0.0f;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const int jc = 32 * ks + 8 * g;
-      const int64_t base = rr * a.cols + (int64_t)blk * C + jc;
-      float u[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float r = load_w_any2(a.W, a.w_dtype, base + k) - a.W0[base + k];
-        const float dj = a.d[(int64_t)blk * C + jc + k];
-        u[k] = valid ? dj * r : 0.0f;
-        e = fmaf(dj * r, r, e);
-      }
-      split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
-    }
-    e += __shfl_xor(e, 16, 64);
-    en[nb] = e + __shfl_xor(e, 32, 64);
-  }
+  load_u_col<C, 2>(a, row0, blk, n, g, uh, um, ul, en);
   const int half = lane >> 5;
   const int64_t my_row = row0 + (lane & 31);
   const bool my_valid = my_row < a.rows;

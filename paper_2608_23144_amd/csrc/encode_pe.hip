@@ -58,23 +58,39 @@ constexpr int kNT = kPeRows;  // tiles per wavefront
 // end give zeros.
 __device__ __forceinline__ void load_u32rows(const ModEntry& md, int w_dtype, int64_t row0, int blk, int n, int g,
                                              u32x4 (&uh)[2][2], u32x4 (&um)[2][2], u32x4 (&ul)[2][2]) {
+  // the four (nb, ks) segments of 8 weights as eight chunks of four; every
+  // load is issued before any is used
+  int64_t o[8];
+  bool valid[2];
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int64_t row = row0 + 16 * nb + n;
-    const bool valid = row < md.rows;
-    const int64_t rr = valid ? row : md.rows - 1;
+    valid[nb] = row < md.rows;
+    const int64_t rr = valid[nb] ? row : md.rows - 1;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const int64_t base = rr * md.cols + (int64_t)blk * kC + 32 * ks + 8 * g;
-      float w[8], w0[8], dj[8], u[8];
-      load8_w(md.W, w_dtype, base, w);
-      load8_f(md.W0 + base, w0);
-      load8_f(md.d + base, dj);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) u[e] = valid ? dj[e] * (w[e] - w0[e]) : 0.0f;
-      split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
+      o[4 * nb + 2 * ks] = base;
+      o[4 * nb + 2 * ks + 1] = base + 4;
     }
   }
+  gf32x4 dv[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) dv[c] = gload4f(md.d + o[c]);
+  float rv[8][4];
+  load_residual4<8>(md.W, w_dtype, md.W0, o, rv);
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      float u[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = 4 * nb + 2 * ks + (e >> 2);
+        u[e] = valid[nb] ? dv[c][e & 3] * rv[c][e & 3] : 0.0f;
+      }
+      split3(u, uh[nb][ks], um[nb][ks], ul[nb][ks]);
+    }
 }
 
 // b of one seed pair for the 32 tiles: acc[nb] holds rows 4g..4g+3 (seed g/2
@@ -199,15 +215,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     // this lane's half of the tile's weighted energy sum_j d_j r_j^2 (for
     // the pruning window below)
     float eh = 0.0f;
+    {
+      int64_t o[C / 8];  // this lane's half in chunks of four, all loads issued first
 #pragma unroll
-    for (int j0 = 0; j0 < C / 2; j0 += 8) {
-      float w[8], w0[8];
-      load8_w(md.W, a.w_dtype, off + 32 * sh + j0, w);
-      load8_f(md.W0 + off + 32 * sh + j0, w0);
+      for (int k = 0; k < C / 8; ++k) o[k] = off + 32 * sh + 4 * k;
+      float rv[C / 8][4];
+      load_residual4<C / 8>(md.W, a.w_dtype, md.W0, o, rv);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float r = w[k] - w0[k];
-        eh = fmaf((sh ? wd[32 + j0 + k] : wd[j0 + k]) * r, r, eh);
+      for (int j = 0; j < C / 2; ++j) {
+        const float r = rv[j >> 2][j & 3];
+        eh = fmaf((sh ? wd[32 + j] : wd[j]) * r, r, eh);
       }
     }
     const auto re = __builtin_amdgcn_permlane32_swap(__float_as_uint(eh), __float_as_uint(eh), false, false);

@@ -239,6 +239,52 @@ __device__ __forceinline__ double solve_score_ldl(const EncodeArgs& a, const dou
   return 2.0 * t1 - (quad - eps * aa);
 }
 
+// Loads through a global-address-space view: global (not flat) loads, which
+// count on the vector-memory counter only, so that a wait for them does not
+// also wait for LDS work.
+typedef float gf32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t gu32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ gf32x4 gload4f(const float* p) {
+  return *(const __attribute__((address_space(1))) gf32x4*)(p);
+}
+__device__ __forceinline__ gu32x2 gload2u(const uint16_t* p) {
+  return *(const __attribute__((address_space(1))) gu32x2*)(p);
+}
+
+// Four consecutive weights of W (fp32 or bf16) and of W0 at each of NP
+// element offsets: every load is issued before any is used (one wait for
+// all of them; the dtype branch is taken once, outside the loads), and
+// r = f32(W - W0).
+template <int NP>
+__device__ __forceinline__ void load_residual4(const void* W, int w_dtype, const float* W0, const int64_t (&o)[NP],
+                                               float (&r)[NP][4]) {
+  gf32x4 y[NP];
+  if (w_dtype == AWSRC_DTYPE_F32) {
+    gf32x4 x[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) x[p] = gload4f(static_cast<const float*>(W) + o[p]);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) y[p] = gload4f(W0 + o[p]);
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[p][k] = x[p][k] - y[p][k];
+  } else {
+    gu32x2 x[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) x[p] = gload2u(static_cast<const uint16_t*>(W) + o[p]);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) y[p] = gload4f(W0 + o[p]);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      r[p][0] = __uint_as_float(x[p][0] << 16) - y[p][0];
+      r[p][1] = __uint_as_float(x[p][0] & 0xFFFF0000u) - y[p][1];
+      r[p][2] = __uint_as_float(x[p][1] << 16) - y[p][2];
+      r[p][3] = __uint_as_float(x[p][1] & 0xFFFF0000u) - y[p][3];
+    }
+  }
+}
+
 // Loads 8 consecutive weights of W (fp32 or bf16) starting at element i.
 __device__ __forceinline__ void load8_w(const void* W, int dt, int64_t i, float (&w)[8]) {
   if (dt == AWSRC_DTYPE_F32) {
@@ -295,24 +341,20 @@ __device__ __forceinline__ void rescore_block64(const EncodeArgs& a, int blk, in
   wdsh[lane] = a.wd64[(int64_t)blk * C + lane];
   {
     const int pc = lane & 15;
+    int64_t o[16];
 #pragma unroll
     for (int pass = 0; pass < 16; ++pass) {
       const int rl = 4 * pass + (lane >> 4);
       const int64_t rg = row0 + rl < a.rows ? row0 + rl : a.rows - 1;
-      const int64_t o = rg * a.cols + (int64_t)blk * C + 4 * pc;
-      float wv[4], w0[4];
-      if (a.w_dtype == AWSRC_DTYPE_F32) {
-        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.W) + o);
-        wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
-      } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.W) + o);
-        wv[0] = __uint_as_float(x.x << 16); wv[1] = __uint_as_float(x.x & 0xFFFF0000u);
-        wv[2] = __uint_as_float(x.y << 16); wv[3] = __uint_as_float(x.y & 0xFFFF0000u);
-      }
-      const float4 y = *reinterpret_cast<const float4*>(a.W0 + o);
-      w0[0] = y.x; w0[1] = y.y; w0[2] = y.z; w0[3] = y.w;
+      o[pass] = rg * a.cols + (int64_t)blk * C + 4 * pc;
+    }
+    float rv[16][4];
+    load_residual4<16>(a.W, a.w_dtype, a.W0, o, rv);  // every load issued before any is used
 #pragma unroll
-      for (int k = 0; k < 4; ++k) rsh[rl * (C + 1) + 4 * pc + k] = wv[k] - w0[k];
+    for (int pass = 0; pass < 16; ++pass) {
+      const int rl = 4 * pass + (lane >> 4);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rsh[rl * (C + 1) + 4 * pc + k] = rv[pass][k];
     }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

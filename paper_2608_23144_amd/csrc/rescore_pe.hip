@@ -77,26 +77,27 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
   float* dsh = lds + kPeRows * kRowD;
   {
     const int pc = lane & 15;
+    constexpr int NP = kPeRows / 4;
+    int64_t o[NP];
 #pragma unroll
-    for (int pass = 0; pass < kPeRows / 4; ++pass) {
+    for (int pass = 0; pass < NP; ++pass) {
       const int rl = 4 * pass + (lane >> 4);
       const int64_t rg = row0 + rl < md.rows ? row0 + rl : md.rows - 1;
-      const int64_t o = rg * md.cols + c0 + 4 * pc;
-      float w[4];
-      if (a.w_dtype == AWSRC_DTYPE_F32) {
-        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(md.W) + o);
-        w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w;
-      } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(md.W) + o);
-        w[0] = __uint_as_float(x.x << 16); w[1] = __uint_as_float(x.x & 0xFFFF0000u);
-        w[2] = __uint_as_float(x.y << 16); w[3] = __uint_as_float(x.y & 0xFFFF0000u);
-      }
-      const float4 y = *reinterpret_cast<const float4*>(md.W0 + o);
-      const float4 z = *reinterpret_cast<const float4*>(md.d + o);
+      o[pass] = rg * md.cols + c0 + 4 * pc;
+    }
+    // the weights' loads go out with the residual's, before any wait
+    gf32x4 z[NP];
+#pragma unroll
+    for (int pass = 0; pass < NP; ++pass) z[pass] = gload4f(md.d + o[pass]);
+    float rv[NP][4];
+    load_residual4<NP>(md.W, a.w_dtype, md.W0, o, rv);
+#pragma unroll
+    for (int pass = 0; pass < NP; ++pass) {
+      const int rl = 4 * pass + (lane >> 4);
       float* rp = rsh + rl * kRowD + 4 * pc;
       float* dp = dsh + rl * kRowD + 4 * pc;
-      rp[0] = w[0] - y.x; rp[1] = w[1] - y.y; rp[2] = w[2] - y.z; rp[3] = w[3] - y.w;
-      dp[0] = z.x; dp[1] = z.y; dp[2] = z.z; dp[3] = z.w;
+      rp[0] = rv[pass][0]; rp[1] = rv[pass][1]; rp[2] = rv[pass][2]; rp[3] = rv[pass][3];
+      dp[0] = z[pass][0]; dp[1] = z[pass][1]; dp[2] = z[pass][2]; dp[3] = z[pass][3];
     }
   }
   wave_sync();
