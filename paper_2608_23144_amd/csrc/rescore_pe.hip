@@ -70,6 +70,9 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
     ts[k] = a.top_seed[item * (kTop * kPeRows) + k * kPeRows + tl];
   }
 
+  int bs[2];
+  uint2 bcol[2];
+  uint32_t bsgn[2];
   // Stage the 32 x 64 residual and weight blocks in LDS (rows of 65 floats;
   // 16 lanes per row segment, 4 rows per pass: each instruction reads whole
   // cache lines); rows past the end repeat the last row.
@@ -91,6 +94,19 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
     for (int pass = 0; pass < NP; ++pass) z[pass] = gload4f(md.d + o[pass]);
     float rv[NP][4];
     load_residual4<NP>(md.W, a.w_dtype, md.W0, o, rv);
+    // the basis entries of both kept seeds (columns, this lane's sign word)
+    // go out while the block is in flight; seeds outside [0, S) (none comes
+    // from the screen) are replaced by 0 before use
+    {
+      const int s0r = list_seed(ts[0]), s1r = list_seed(ts[1]);
+      bs[0] = s0r < a.S ? s0r : 0;
+      bs[1] = s1r < a.S ? s1r : 0;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        bcol[k] = *reinterpret_cast<const uint2*>(a.basis.col + (size_t)bs[k] * kMaxP);
+        bsgn[k] = (uint32_t)(a.basis.sign[(size_t)bs[k] * 2] >> (kH * h));
+      }
+    }
 #pragma unroll
     for (int pass = 0; pass < NP; ++pass) {
       const int rl = 4 * pass + (lane >> 4);
@@ -147,12 +163,14 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
   const bool mine2 = h == 1 && need;
   // seeds index the basis tables: any value outside [0, S) (none comes from
   // the screen) is replaced by 0 before use
-  const int s0r = list_seed(ts[0]), s1r = list_seed(ts[1]);
-  const int s0 = s0r < a.S ? s0r : 0, s1 = s1r < a.S ? s1r : 0;
+  const int s0 = bs[0], s1 = bs[1];
   const int s_me = mine2 ? s1 : s0;
   int c[PB];
+  {
+    const uint2 cw = mine2 ? bcol[1] : bcol[0];
 #pragma unroll
-  for (int p = 0; p < PB; ++p) c[p] = (p < P) ? a.basis.col[(size_t)s_me * kMaxP + p] : 0;
+    for (int p = 0; p < PB; ++p) c[p] = (p < P) ? (int)(((p < 4 ? cw.x : cw.y) >> (8 * (p & 3))) & 0xFFu) : 0;
+  }
 
   // projections through the transform of sigma .* d .* r: the best seed's
   // signs, then (when some tile of the wavefront needs it) the second's
@@ -160,8 +178,7 @@ __global__ __launch_bounds__(64, 2) void k_finalize_pe_modules(EncodeArgs a, con
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
     if (pass == 1 && !two) break;
-    const int sp = pass ? s1 : s0;
-    const uint32_t sw = (uint32_t)(a.basis.sign[(size_t)sp * 2] >> (kH * h));
+    const uint32_t sw = pass ? bsgn[1] : bsgn[0];
     double v[kH];
 #pragma unroll
     for (int j = 0; j < kH; ++j) {
