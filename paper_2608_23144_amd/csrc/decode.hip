@@ -110,7 +110,16 @@ __device__ __forceinline__ bool record_fields_ok(const DecodeArgs& a, const Rec&
   return !bad;
 }
 
-__global__ void k_decode_validate(DecodeArgs a) {
+// The module table (tile offsets) is staged in LDS when it has at most
+// kLdsModules + 1 entries, so that each record's binary search for its module
+// reads no global memory.
+__global__ __launch_bounds__(256) void k_decode_validate(DecodeArgs a) {
+  __shared__ uint64_t s_off[kLdsModules + 1];
+  const bool lds_tab = a.n_modules <= kLdsModules;
+  if (lds_tab)
+    for (int m = threadIdx.x; m <= a.n_modules; m += blockDim.x) s_off[m] = a.mod_tile_off[m];
+  __syncthreads();
+  const uint64_t* toff = lds_tab ? s_off : a.mod_tile_off;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.K) return;
   const Rec r = parse(a, i);
@@ -125,7 +134,7 @@ __global__ void k_decode_validate(DecodeArgs a) {
   int lo = 0, hi = a.n_modules - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (a.mod_tile_off[mid] <= r.idx) lo = mid; else hi = mid - 1;
+    if (toff[mid] <= r.idx) lo = mid; else hi = mid - 1;
   }
   uint32_t qw[4] = {0u, 0u, 0u, 0u};
   int32_t tot = 0;
@@ -133,7 +142,7 @@ __global__ void k_decode_validate(DecodeArgs a) {
     qw[p >> 2] |= ((uint32_t)r.q[p] & 0xFFu) << (8 * (p & 3));
     tot += r.q[p];
   }
-  a.dec[2 * i] = make_uint4((uint32_t)(r.idx - a.mod_tile_off[lo]), (uint32_t)lo, r.seed | (r.scale << 16),
+  a.dec[2 * i] = make_uint4((uint32_t)(r.idx - toff[lo]), (uint32_t)lo, r.seed | (r.scale << 16),
                             (uint32_t)tot);
   a.dec[2 * i + 1] = make_uint4(qw[0], qw[1], qw[2], qw[3]);
 }

@@ -648,15 +648,23 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
     dbase[t] = before + x - v + hist[(int64_t)t * nblk + blockIdx.x];
   }
   const uint64_t lt = lanemask_lt();
+  // every round's item is loaded before the first round (one wait, not one
+  // per round)
+  SortItem xs[kRsRounds];
+#pragma unroll
+  for (int r = 0; r < kRsRounds; ++r) {
+    const int64_t i = base + r * kRsThreads + t;
+    xs[r].key = 0; xs[r].tile = 0; xs[r].aux = 0;
+    if (i < n) xs[r] = in[i];
+  }
+#pragma unroll
   for (int r = 0; r < kRsRounds; ++r) {
 #pragma unroll
     for (int k = 0; k < kRsThreads / 64; ++k) wc[k][t] = 0;
     __syncthreads();
     const int64_t i = base + r * kRsThreads + t;
     const bool valid = i < n;
-    SortItem x;
-    x.key = 0; x.tile = 0; x.aux = 0;
-    if (valid) x = in[i];
+    const SortItem x = xs[r];
     const uint32_t d = (uint32_t)(x.key >> shift) & (kRsBins - 1);
     // lanes of this wavefront holding the same digit
     uint64_t same = __ballot(valid);
