@@ -85,9 +85,15 @@ __device__ __forceinline__ Rec parse(const DecodeArgs& a, int64_t i) {
   int pos = 0;
   out.idx = get_bits(w, pos, a.idx_bits);
   out.seed = (uint32_t)get_bits(w, pos, a.seed_bits);
-  for (int p = 0; p < a.P; ++p) {
-    int64_t c = (int64_t)get_bits(w, pos, a.b);
-    if (c >> (a.b - 1)) c -= (int64_t)1 << a.b;
+  // loops over the fixed maximum with a guard keep every index static (a
+  // loop bounded by P would put the codes in scratch memory)
+#pragma unroll
+  for (int p = 0; p < kMaxP; ++p) {
+    int64_t c = 0;
+    if (p < a.P) {
+      c = (int64_t)get_bits(w, pos, a.b);
+      if (c >> (a.b - 1)) c -= (int64_t)1 << a.b;
+    }
     out.q[p] = (int32_t)c;
   }
   out.scale = (uint32_t)get_bits(w, pos, a.scale_fmt == AWSRC_SCALE_POW2 ? 8 : 16);
@@ -104,7 +110,8 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n) {
 __device__ __forceinline__ bool record_fields_ok(const DecodeArgs& a, const Rec& r) {
   const int qmax = (1 << (a.b - 1)) - 1;
   bool bad = r.idx >= a.T_total || r.seed >= (uint32_t)a.S;
-  for (int p = 0; p < a.P; ++p) bad |= r.q[p] < -qmax || r.q[p] > qmax;
+#pragma unroll
+  for (int p = 0; p < kMaxP; ++p) bad |= p < a.P && (r.q[p] < -qmax || r.q[p] > qmax);
   // fp16 scale: negative, inf or NaN; every 8-bit exponent is valid
   if (a.scale_fmt != AWSRC_SCALE_POW2) bad |= (r.scale & 0x8000u) != 0 || (r.scale & 0x7C00u) == 0x7C00u;
   return !bad;
@@ -138,7 +145,9 @@ __global__ __launch_bounds__(256) void k_decode_validate(DecodeArgs a) {
   }
   uint32_t qw[4] = {0u, 0u, 0u, 0u};
   int32_t tot = 0;
-  for (int p = 0; p < a.P; ++p) {
+#pragma unroll
+  for (int p = 0; p < kMaxP; ++p) {
+    if (p >= a.P) continue;
     qw[p >> 2] |= ((uint32_t)r.q[p] & 0xFFu) << (8 * (p & 3));
     tot += r.q[p];
   }
@@ -229,12 +238,17 @@ __device__ __forceinline__ uint32_t tile_rank(const DecodeArgs& a, uint64_t t) {
 }
 
 // decoded record i (stream order) copied to its tile-order rank
-__global__ void k_decode_tile_order(DecodeArgs a) {
+__global__ __launch_bounds__(256) void k_decode_tile_order(DecodeArgs a) {
+  __shared__ uint64_t s_off[kLdsModules];  // module tile offsets (first kLdsModules)
+  const bool lds_tab = a.n_modules <= kLdsModules;
+  if (lds_tab)
+    for (int m = threadIdx.x; m < a.n_modules; m += blockDim.x) s_off[m] = a.mod_tile_off[m];
+  __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.K) return;
   const uint4 e0 = a.dec[2 * i];
   const uint4 e1 = a.dec[2 * i + 1];
-  const uint32_t k = tile_rank(a, a.mod_tile_off[e0.y] + e0.x);
+  const uint32_t k = tile_rank(a, (lds_tab ? s_off[e0.y] : a.mod_tile_off[e0.y]) + e0.x);
   // the tile-ordered copy carries the record's place in the stream in its
   // first word (the tile is implied by the position), for the nested-prefix
   // reconstruction

@@ -595,9 +595,16 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_hist(const SortItem* __restri
   __syncthreads();
   const int64_t n = (int64_t)state[kSegK];
   const int64_t base = (int64_t)blockIdx.x * kRsItems;
+  uint64_t keys[kRsRounds];  // every load issued before the first count
+#pragma unroll
   for (int r = 0; r < kRsRounds; ++r) {
     const int64_t i = base + r * kRsThreads + threadIdx.x;
-    if (i < n) atomicAdd(&h[(uint32_t)(in[i].key >> shift) & (kRsBins - 1)], 1u);
+    keys[r] = i < n ? in[i].key : 0;
+  }
+#pragma unroll
+  for (int r = 0; r < kRsRounds; ++r) {
+    const int64_t i = base + r * kRsThreads + threadIdx.x;
+    if (i < n) atomicAdd(&h[(uint32_t)(keys[r] >> shift) & (kRsBins - 1)], 1u);
   }
   __syncthreads();
   hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
