@@ -102,6 +102,13 @@ __host__ __device__ __forceinline__ float rescore_window(float g, float e, bool 
   return edge ? 3e-2f * fabsf(g) + 3e-5f * e : 1e-4f * fabsf(g) + 1e-7f * e;
 }
 
+// The screens' pruning threshold lowered by a relative 2^-9: a candidate is
+// scored in full when its bound exceeds it.  The margin covers the fp32
+// rounding of the bound and of the score (each a few ulps of the bound); it
+// is applied to the threshold, which changes only in scoring rounds, rather
+// than to every candidate's bound.
+__device__ __forceinline__ float slack_thr(float thr) { return thr - fabsf(thr) * 0x1p-9f; }
+
 __device__ __forceinline__ bool code_edge(float x, float qmax) {
   const float ax = fabsf(x);
   return ax < qmax && 0.5f - fabsf(x - rintf(x)) < 1e-4f + 2e-5f * ax;

@@ -187,8 +187,8 @@ __device__ __forceinline__ void project64(const u32x4& F0, const u32x4& F1, cons
 // lanes' lists (below).  A lane's entries are scored in seed order, and
 // thresholds only rise, so the merged lists agree with those of scoring
 // every candidate in the best and in the second wherever the second lies
-// inside the re-score's window.  The factor of 1 + 2^-9 on the bound covers
-// its fp32 rounding and that of the score (each a few ulps of the bound).
+// inside the re-score's window.  The threshold is lowered by a relative
+// 2^-9 (slack_thr) for the fp32 rounding of the bound and the score.
 //
 // Factor entries reach the wavefront through an LDS ring of the last NR
 // pairs (both seeds' whole entries per slot): while pair k is bounded, every
@@ -213,7 +213,6 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
   constexpr int QD = 4;                           // queue slots per lane (a power of two), plus a spare
   constexpr int QW = PB + 1;                      // words per entry: w, then seed + (tile << 16)
   constexpr int NR = 16;                          // factor ring slots (pairs; a power of two)
-  constexpr float kSlack = 1.001953125f;
   static_assert(NF % 4 == 0, "factor pieces are 16 bytes");
   // one LDS buffer: the factor ring and the queues while screening, the
   // re-score's rows after (when fused)
@@ -283,10 +282,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
 
   constexpr int NPC = 2 * NF / 4;  // 16-byte pieces per pair
   const int pc = lane % NPC;
+  // the piece's seed within its pair and its byte offset in the seed's entry;
+  // the block's rows of the table from a wavefront-uniform base
+  const int psel = pc / (NF / 4);
+  const uint32_t pofs = 16u * (uint32_t)(pc % (NF / 4)), strideB = 4u * (uint32_t)stride;
+  const char* fac_blk = reinterpret_cast<const char*>(a.colfac + (size_t)blk * a.S * stride);
   auto fac_piece = [&](int pr) -> f32x4 {
-    int s = 2 * pr + pc / (NF / 4);
-    s = s < a.S ? s : a.S - 1;
-    return *reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + s) * stride + 4 * (pc % (NF / 4)));
+    const int s = min(2 * pr + psel, a.S - 1);
+    return *reinterpret_cast<const f32x4*>(fac_blk + __umul24((uint32_t)s, strideB) + pofs);
   };
   auto fac_store = [&](int pr, const f32x4& v) {
     *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NF) + 4 * pc]) = v;
@@ -312,7 +315,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
       const uint32_t ow = sh ? r1[0] : r1[1];
       const float best = fmaxf(tg[t][0], og);
       const bool edge = ((tg[t][0] >= og ? ts[t][0] : ow) & kEdge) != 0;
-      thr[t] = best - 1.01f * rescore_window(best, e_raw[t], edge);
+      thr[t] = slack_thr(best - 1.01f * rescore_window(best, e_raw[t], edge));
     }
   };
 
@@ -374,7 +377,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
       // need no branch (one basic block keeps the matrix-core instructions
       // interleaved with this work); bitwise: a short-circuit would put the
       // bound under a branch
-      const bool keep = (int)(bnd * kSlack > thr[t]) & (int)tv[t] & (int)(s < a.S);
+      const bool keep = (int)(bnd > thr[t]) & (int)tv[t] & (int)(s < a.S);
       float* e = &qb[(keep ? qtail : QD) * (QW * 64) + lane];
 #pragma unroll
       for (int i = 0; i < PB; ++i) e[i * 64] = wv[i];
@@ -469,9 +472,11 @@ __global__ __launch_bounds__(64, 2) void k_screen_col64(EncodeArgs a, const u32x
 // block (2 groups of 16 tiles x 4 K steps x 3 bf16 parts) and gives the two
 // seeds of a pair to its two lane halves: lane = (seed of the pair, tile).
 // The seed is then uniform per half only, so each lane reads its seed's
-// per-column factors with vector loads (two addresses per wavefront).  b is
-// scaled by 1/sqrt(128) before scoring (not a power of two, so raw units
-// would round the fp16 scale differently).
+// per-column factors with vector loads (two addresses per wavefront).  The
+// bound works on raw b (without the 1/sqrt(128) of the basis), so it comes
+// out C times larger and the threshold is scaled by C instead; a scoring
+// round scales b by 1/sqrt(128) and solves again (not a power of two, so
+// raw units would round the fp16 scale differently).
 //
 // Every candidate gets the forward solve with its seed's factor and the bound
 // b^T (G + eps I)^-1 b on every rounding of its fit (screen_fwd); those whose
@@ -491,8 +496,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   constexpr int NF = LS + 2 * PB;   // the whole factor entry (the full score also reads e)
   constexpr int NBD = LS + PB;      // L and 1/e: what the bound reads
   constexpr int QC = 128;           // queue slots
-  constexpr int QW = PB + 1;        // words per entry: w, then seed | owner lane << 24
-  constexpr float kSlack = 1.001953125f;
+  constexpr int QW = PB + 1;        // words per entry: raw b, then seed | owner lane << 24
   static_assert(NBD % 4 == 0 && NF % 4 == 0, "factor pieces are 16 bytes");
   constexpr int NR = 4;              // factor ring slots (pairs)
   constexpr int NPC = 2 * NBD / 4;   // 16-byte pieces of a pair's two bound entries
@@ -533,7 +537,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   float thr = -INFINITY;
   // the pruning threshold of this lane's tile: the re-score window below the
   // best over both halves (lane ^ 32), one percent wider, the wide one when
-  // that best is a knife edge
+  // that best is a knife edge; in units of the raw bound (C times the bound
+  // of the scaled b)
   auto update_thr = [&]() {
     const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(tg0), __float_as_uint(tg0), false, false);
     const auto r1 = __builtin_amdgcn_permlane32_swap(ts0, ts0, false, false);
@@ -541,7 +546,7 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     const uint32_t ow = half ? r1[0] : r1[1];
     const float best = fmaxf(tg0, og);
     const bool edge = ((tg0 >= og ? ts0 : ow) & kEdge) != 0;
-    thr = best - 1.01f * rescore_window(best, energy, edge);
+    thr = slack_thr(best - 1.01f * rescore_window(best, energy, edge)) * (float)C;
   };
   int qhead = 0, qtail = 0;  // wavefront-uniform queue counters
   int nscored = 0;
@@ -563,10 +568,14 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
   // reads its seed's entry from slot k.  The wavefront barriers of every step
   // order the stores before the reads.
   const int pc = lane % NPC;
+  // the piece's seed within its pair and its byte offset in the seed's entry;
+  // the block's rows of the table from a wavefront-uniform base
+  const int psel = pc / (NBD / 4);
+  const uint32_t pofs = 16u * (uint32_t)(pc % (NBD / 4)), strideB = 4u * (uint32_t)stride;
+  const char* fac_blk = reinterpret_cast<const char*>(a.colfac + (size_t)blk * a.S * stride);
   auto fac_piece = [&](int pr) -> f32x4 {
-    int s_ = 2 * pr + pc / (NBD / 4);
-    s_ = s_ < a.S ? s_ : a.S - 1;
-    return *reinterpret_cast<const f32x4*>(a.colfac + ((size_t)blk * a.S + s_) * stride + 4 * (pc % (NBD / 4)));
+    const int s_ = min(2 * pr + psel, a.S - 1);
+    return *reinterpret_cast<const f32x4*>(fac_blk + __umul24((uint32_t)s_, strideB) + pofs);
   };
   auto fac_store = [&](int pr, const f32x4& v) {
     *reinterpret_cast<f32x4*>(&fr[(pr & (NR - 1)) * (2 * NBD) + 4 * pc]) = v;
@@ -579,16 +588,16 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     const int slot = (qhead + lane) & (QC - 1);
     int ol = 0;
     if (mine) {
-      float wv[PB];
+      float bs[PB];
 #pragma unroll
-      for (int i = 0; i < PB; ++i) wv[i] = qb[i * QC + slot];
+      for (int i = 0; i < PB; ++i) bs[i] = qb[i * QC + slot] * isq;
       const uint32_t word = __float_as_uint(qb[PB * QC + slot]);
       const int es = (int)(word & 0xFFFFu);
       ol = (int)(word >> 24);
       float f[NF];
       load_factor(es, f, NF / 4);
       bool edge;
-      const float gsc = screen_gain_w<PB, POW2, 0>(wv, f, qmax, inv_qmax, &edge);
+      const float gsc = screen_score_ldl<PB, POW2, 0>(bs, f, qmax, inv_qmax, &edge);
       qb[slot] = gsc;
       qb[QC + slot] = __uint_as_float((uint32_t)es | (edge ? kEdge : 0u));
     }
@@ -674,8 +683,8 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     {
       const f32x4 b0 = *reinterpret_cast<const f32x4*>(&tb[lane * TS]);
       const f32x4 b1 = *reinterpret_cast<const f32x4*>(&tb[lane * TS + 4]);
-      bv[0] = b0[0] * isq; bv[1] = b0[1] * isq; bv[2] = b0[2] * isq; bv[3] = b0[3] * isq;
-      bv[4] = b1[0] * isq; bv[5] = b1[1] * isq; bv[6] = b1[2] * isq; bv[7] = b1[3] * isq;
+      bv[0] = b0[0]; bv[1] = b0[1]; bv[2] = b0[2]; bv[3] = b0[3];
+      bv[4] = b1[0]; bv[5] = b1[1]; bv[6] = b1[2]; bv[7] = b1[3];
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -685,16 +694,16 @@ __global__ __launch_bounds__(64, 2) void k_screen_mfma_halves(EncodeArgs a, cons
     for (int ks = 0; ks < NKS; ++ks) F[ks] = fp[(size_t)(pair - pair0 + 2) * (NKS * 64) + ks * 64];
     float wv[PB];
     const float bnd = screen_fwd<PB>(bv, f, wv);
-    const bool keep = (int)(bnd * kSlack > thr) & (int)my_valid & (int)(s < a.S);
-    // every lane stores its candidate, the kept ones first from the tail on,
-    // the dropped ones after them (at most 63 wait before a step, so the 64
-    // slots written are free); the tail takes in the kept ones only
+    const bool keep = (int)(bnd > thr) & (int)my_valid & (int)(s < a.S);
+    // every lane stores its candidate (raw b), the kept ones first from the
+    // tail on, the dropped ones after them (at most 63 wait before a step, so
+    // the 64 slots written are free); the tail takes in the kept ones only
     const uint64_t kb = __ballot(keep);
     const int nk = __popcll(kb);
     const int pos = keep ? __popcll(kb & lt) : nk + __popcll(~kb & lt);
     const int qslot = (qtail + pos) & (QC - 1);
 #pragma unroll
-    for (int i = 0; i < PB; ++i) qb[i * QC + qslot] = wv[i];
+    for (int i = 0; i < PB; ++i) qb[i * QC + qslot] = bv[i];
     qb[PB * QC + qslot] = __uint_as_float((uint32_t)s | ((uint32_t)lane << 24));
     qtail += nk;
 #pragma unroll

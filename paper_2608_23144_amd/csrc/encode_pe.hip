@@ -182,7 +182,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   constexpr int NL = PB * (PB - 1) / 2;
   constexpr int QC = 128;     // slots of the wavefront's queue: 12.8 KB of LDS in all, three wavefronts per SIMD
   constexpr int QW = PB + 1;  // words per entry: w, then the seed | owner lane << 24
-  constexpr float kSlack = 1.001953125f;
   __shared__ float wdl[C * NT];            // WHT(d_t) / C, [coordinate][tile]
   __shared__ float qb[QW * QC];            // the queue, [word][slot]
   const int lane = threadIdx.x;
@@ -265,7 +264,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     const uint32_t ow = sh ? r1[0] : r1[1];
     const float best = fmaxf(tg0, og);
     const bool edge = ((tg0 >= og ? ts0 : ow) & kEdge) != 0;
-    thr = best - 1.01f * rescore_window(best, e_raw, edge);
+    thr = slack_thr(best - 1.01f * rescore_window(best, e_raw, edge));
   };
   // The survivors of the bound wait in one queue for the whole wavefront,
   // appended in step order (so each lane's own entries are in seed order);
@@ -371,7 +370,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     factor_pe<PB, FULLP>(gq, d0, eps, P, f);
     float wv[PB];
     const float bnd = screen_fwd<PB>(bt, f, wv);
-    const bool keep = (int)(bnd * kSlack > thr) & (int)valid & (int)(s < a.S);
+    const bool keep = (int)(bnd > thr) & (int)valid & (int)(s < a.S);
     // Every lane stores its candidate, the kept ones first (in lane order)
     // from the tail on, the dropped ones after them; only the kept ones are
     // taken in by advancing the tail.  At most 63 entries wait before a
