@@ -359,7 +359,12 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
 #define AWSRC_GLOBAL __attribute__((address_space(1)))
 
 constexpr int kRecThreads = 512;
-constexpr int kUnitW = 16;                   // weights per unit (8 or 16)
+// weights per unit (8 or 16).  8: a unit's 16 output bytes per target are one
+// store, and consecutive lanes' stores are adjacent, so a wavefront's store
+// covers 1 KB without gaps.  With 16 (two 16-byte stores per lane, 32 bytes
+// apart) the address and data units of the CUs, not memory, bounded the pass
+// (busy 99% of its cycles), and it ran 20% slower.
+constexpr int kUnitW = 8;
 constexpr int kLogUnitW = kUnitW == 16 ? 4 : 3;
 constexpr int kRecUnits = 2;                 // units per lane per chunk
 constexpr int kTsignLdsMax = 64 * 1024;      // sign tables up to this size are staged in LDS
