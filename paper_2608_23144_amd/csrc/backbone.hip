@@ -1,7 +1,7 @@
 // Backbone quantizer W0 = Q(W) of Eq. (1): asymmetric RTN-INT4 per group of
 // consecutive input columns (Sec. 4 uses RTN with group size 128).
 //
-// Lanes own 8 consecutive weights; the lanes of one group reduce min/max with
+// Lanes own 8 weights of one group; the lanes of a group reduce min/max with
 // butterfly shuffles, and every load and store is a wide coalesced access.
 // Arithmetic is fp32 with correctly rounded division (this file is built
 // without FMA contraction), so codes, scales and zero points are bit-exact
@@ -10,9 +10,14 @@
 
 namespace awsrc {
 
-// Each lane owns 8 consecutive weights; LPG = group/8 lanes share one group, so
-// a wavefront covers 64/LPG groups per iteration with 16-byte loads of bf16 W
-// (32-byte for fp32), 32-byte W0 stores and one 4-byte store of 8 codes.
+// LPG = group/8 lanes share one group, and lane sub of a group owns elements
+// 4 sub .. 4 sub + 3 of each half of it, so that the group's lanes cover each
+// half with adjacent accesses: per half, an 8-byte load of bf16 W (16-byte for
+// fp32), a 16-byte W0 store and a 2-byte store of 4 codes, and every W0
+// store instruction writes whole 64-byte pieces.  (With 8 consecutive weights
+// per lane, its two 16-byte W0 stores 32 bytes apart kept the CUs' address
+// and data units busy longer than memory.)  A wavefront covers 64/LPG groups
+// per iteration.
 template <int LPG, typename TW>
 __global__ __launch_bounds__(256) void k_backbone_rtn(const TW* __restrict__ W, int64_t rows,
                                                       int64_t cols, uint8_t* __restrict__ codes,
@@ -32,19 +37,21 @@ __global__ __launch_bounds__(256) void k_backbone_rtn(const TW* __restrict__ W, 
     const bool valid = g < n_groups;
     const int64_t gg = valid ? g : n_groups - 1;
     const int64_t row = gg / gpr;
-    const int64_t base = row * cols + (gg - row * gpr) * G + (int64_t)sub * 8;
-    float w[8];
-    if constexpr (sizeof(TW) == 4) {
-      const float4 x = reinterpret_cast<const float4*>(W + base)[0];
-      const float4 y = reinterpret_cast<const float4*>(W + base)[1];
-      w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w; w[4] = y.x; w[5] = y.y; w[6] = y.z; w[7] = y.w;
-    } else {
-      const uint4 x = *reinterpret_cast<const uint4*>(W + base);
-      const uint32_t v[4] = {x.x, x.y, x.z, x.w};
+    // this lane's run in the first half of the group; the second is G/2 on
+    const int64_t base = row * cols + (gg - row * gpr) * G + (int64_t)sub * 4;
+    float w[8];  // w[0..3]: first half, w[4..7]: second half
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        w[2 * k] = __uint_as_float(v[k] << 16);
-        w[2 * k + 1] = __uint_as_float(v[k] & 0xFFFF0000u);
+    for (int h = 0; h < 2; ++h) {
+      const int64_t b = base + h * (G / 2);
+      if constexpr (sizeof(TW) == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(W + b);
+        w[4 * h] = x.x; w[4 * h + 1] = x.y; w[4 * h + 2] = x.z; w[4 * h + 3] = x.w;
+      } else {
+        const uint2 x = *reinterpret_cast<const uint2*>(W + b);
+        w[4 * h] = __uint_as_float(x.x << 16);
+        w[4 * h + 1] = __uint_as_float(x.x & 0xFFFF0000u);
+        w[4 * h + 2] = __uint_as_float(x.y << 16);
+        w[4 * h + 3] = __uint_as_float(x.y & 0xFFFF0000u);
       }
     }
     float mn = w[0], mx = w[0];
@@ -67,18 +74,19 @@ __global__ __launch_bounds__(256) void k_backbone_rtn(const TW* __restrict__ W, 
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float qf = degenerate ? 0.0f : fminf(fmaxf(rintf(w[e] / s) + z, 0.0f), 15.0f);
-      packed |= (uint32_t)qf << (4 * e);  // even column in the low nibble of each byte
+      packed |= (uint32_t)qf << (4 * e);  // even column in the low nibble of each byte (per half)
       o[e] = (qf - z) * s;
     }
     if (valid) {
       if (W0) {
         // streaming stores: W0 is written once and read by later launches
         typedef float f32x4_nt __attribute__((ext_vector_type(4)));
-        f32x4_nt* wp = reinterpret_cast<f32x4_nt*>(W0 + base);
-        __builtin_nontemporal_store(f32x4_nt{o[0], o[1], o[2], o[3]}, wp);
-        __builtin_nontemporal_store(f32x4_nt{o[4], o[5], o[6], o[7]}, wp + 1);
+        __builtin_nontemporal_store(f32x4_nt{o[0], o[1], o[2], o[3]}, reinterpret_cast<f32x4_nt*>(W0 + base));
+        __builtin_nontemporal_store(f32x4_nt{o[4], o[5], o[6], o[7]},
+                                    reinterpret_cast<f32x4_nt*>(W0 + base + G / 2));
       }
-      *reinterpret_cast<uint32_t*>(codes + (base >> 1)) = packed;
+      *reinterpret_cast<uint16_t*>(codes + (base >> 1)) = (uint16_t)packed;
+      *reinterpret_cast<uint16_t*>(codes + ((base + G / 2) >> 1)) = (uint16_t)(packed >> 16);
       if (sub == 0) {
         scale[g] = hb;
         zero[g] = (uint8_t)z;
