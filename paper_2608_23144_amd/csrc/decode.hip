@@ -279,9 +279,20 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
     const uint4 e0 = a.dec[2 * i];
     const uint4 e1 = a.dec[2 * i + 1];
     const uint32_t q4[4] = {e1.x, e1.y, e1.z, e1.w};
-    // signs of rows 8*sub .. 8*sub+7 of B_s, one u16 of P bits per row
-    const uint4 tsv = *reinterpret_cast<const uint4*>(a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC + sub * 8);
-    const uint32_t tw[4] = {tsv.x, tsv.y, tsv.z, tsv.w};
+    // signs of this lane's eight rows of B_s, one u16 of P bits per row: rows
+    // 8 sub .. 8 sub + 7 (bf16 targets), or rows 4 sub .. 4 sub + 3 of each
+    // half of the tile (fp32 targets, so that the 16-byte accesses of the
+    // record's lanes are adjacent)
+    const uint16_t* trow = a.basis.tsign + (size_t)(e0.z & 0xFFFFu) * kMaxC;
+    uint32_t tw[4];
+    if constexpr (sizeof(TW) == 4) {
+      const uint2 t0 = *reinterpret_cast<const uint2*>(trow + sub * 4);
+      const uint2 t1 = *reinterpret_cast<const uint2*>(trow + C / 2 + sub * 4);
+      tw[0] = t0.x; tw[1] = t0.y; tw[2] = t1.x; tw[3] = t1.y;
+    } else {
+      const uint4 tsv = *reinterpret_cast<const uint4*>(trow + sub * 8);
+      tw[0] = tsv.x; tw[1] = tsv.y; tw[2] = tsv.z; tw[3] = tsv.w;
+    }
     const uint32_t sfield = e0.z >> 16;
     const float scl = a.scale_fmt == AWSRC_SCALE_POW2 ? ldexpf(isq, (int)sfield - 128)
                                                       : __half2float(__ushort_as_half((uint16_t)sfield)) * isq;
@@ -299,16 +310,16 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
       add[e] = (float)(tot - 2 * neg) * scl;
     }
     TW* W0 = static_cast<TW*>(mptr[e0.y]);
-    const int64_t base = (int64_t)e0.x * C + sub * 8;
     if constexpr (sizeof(TW) == 4) {
-      float4* q = reinterpret_cast<float4*>(W0 + base);
-      float4 v0 = q[0], v1 = q[1];
+      float4* q0 = reinterpret_cast<float4*>(W0 + (int64_t)e0.x * C + sub * 4);
+      float4* q1 = q0 + C / 8;  // the same place in the tile's second half
+      float4 v0 = *q0, v1 = *q1;
       v0.x += add[0]; v0.y += add[1]; v0.z += add[2]; v0.w += add[3];
       v1.x += add[4]; v1.y += add[5]; v1.z += add[6]; v1.w += add[7];
-      q[0] = v0;
-      q[1] = v1;
+      *q0 = v0;
+      *q1 = v1;
     } else {
-      uint4* q = reinterpret_cast<uint4*>(W0 + base);
+      uint4* q = reinterpret_cast<uint4*>(W0 + (int64_t)e0.x * C + sub * 8);
       const uint4 v = *q;
       const uint32_t in[4] = {v.x, v.y, v.z, v.w};
       uint32_t o[4];

@@ -71,25 +71,25 @@ __global__ __launch_bounds__(64) void k_sdq_encode(const uint16_t* __restrict__ 
   }
 }
 
-// W0 = f32(q - z) * s_hat per group; each thread writes 8 consecutive weights
-// (4 code bytes in, 32 bytes out).
+// W0 = f32(q - z) * s_hat per group; each thread writes 4 consecutive weights
+// (2 code bytes in, one 16-byte store out), so that a wavefront's stores are
+// adjacent (8 weights per thread, as two stores 32 bytes apart, kept the
+// CUs' address units busier than memory).
 __global__ __launch_bounds__(256) void k_sdq_dequant(const uint8_t* __restrict__ codes, const uint8_t* __restrict__ zero,
                                                      const int8_t* __restrict__ sc, const float* __restrict__ mean,
-                                                     const float* __restrict__ step, int64_t n8, int group,
+                                                     const float* __restrict__ step, int64_t n4, int group,
                                                      float* __restrict__ W0) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t w0 = 8 * i;        // first weight (row-major; groups never straddle rows)
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t w0 = 4 * i;        // first weight (row-major; groups never straddle rows)
     const int64_t g = w0 / group;    // global group index
     const int64_t blk = g / kSdqBlock;
     const float sh = (float)((double)mean[blk] + (double)sc[g] * (double)step[blk]);
     const float z = (float)zero[g];
-    const uint32_t q4 = *reinterpret_cast<const uint32_t*>(codes + 4 * i);
-    float o[8];
+    const uint32_t q2 = *reinterpret_cast<const uint16_t*>(codes + 2 * i);
+    float o[4];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = ((float)((q4 >> (4 * k)) & 0xFu) - z) * sh;
-    float4* out = reinterpret_cast<float4*>(W0 + w0);
-    out[0] = make_float4(o[0], o[1], o[2], o[3]);
-    out[1] = make_float4(o[4], o[5], o[6], o[7]);
+    for (int k = 0; k < 4; ++k) o[k] = ((float)((q2 >> (4 * k)) & 0xFu) - z) * sh;
+    *reinterpret_cast<float4*>(W0 + w0) = make_float4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -106,11 +106,11 @@ hipError_t launch_sdq_encode(const uint16_t* s16, int64_t n_groups, int8_t* code
 
 hipError_t launch_sdq_dequant(const uint8_t* codes, const uint8_t* zero, const int8_t* sc, const float* mean,
                               const float* step, int64_t rows, int64_t cols, int group, float* W0, hipStream_t st) {
-  const int64_t n8 = rows * cols / 8;
-  if (n8 <= 0) return hipSuccess;
-  int64_t nb = (n8 + 255) / 256;
-  if (nb > 256 * 16) nb = 256 * 16;
-  hipLaunchKernelGGL(k_sdq_dequant, dim3((unsigned)nb), dim3(256), 0, st, codes, zero, sc, mean, step, n8, group, W0);
+  const int64_t n4 = rows * cols / 4;
+  if (n4 <= 0) return hipSuccess;
+  int64_t nb = (n4 + 255) / 256;
+  if (nb > 256 * 32) nb = 256 * 32;
+  hipLaunchKernelGGL(k_sdq_dequant, dim3((unsigned)nb), dim3(256), 0, st, codes, zero, sc, mean, step, n4, group, W0);
   return hipGetLastError();
 }
 
