@@ -44,45 +44,45 @@ def log(*a):
 # figure is reported as null until the counters are taken again.
 MEASURED_TRAFFIC = {
     # one step of the 36-layer 3B stack (profiles/counters_stack3b.md): the
-    # encode call over all 252 modules (screen 29.73 GB, fp64 re-score
+    # encode call over all 252 modules (screen 29.74 GB, fp64 re-score
     # 29.31 GB, tables), the 252 backbone launches, the decode-add of the
     # 0.32 bpw stream, the reconstruction of its four nested prefixes (tile
     # ordering and the streaming pass), and the same on the SDQ backbone
     ("encode", "stack3b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
                   "rescore_pe.hip", "rescore64.h"],
-        "sha256": "7f55fe52df88c7b843d16fa7bbb3fcc3da8719fbd21894e1fbbca4eabaae7f8d",
-        "bytes": 59048077440},
+        "sha256": "f5cd199c3a5245c6611d36b08ee9fe96bce500bab8f26b718433d744bcd47246",
+        "bytes": 59053364832},
     ("backbone", "stack3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "b074178e7b2d45f0ef5bb61505337dabac7ef556a8d0eca21ff5d4bed0d1c8e7",
-        "bytes": 19295810080},
+        "sha256": "dcb4f93b7f42ea7e4e107e5aa5283970870690d71ac7c8e85eee85eea5c2df24",
+        "bytes": 18135252320},
     ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "ac49670e34955b2158c3dfcdfcc64266705d944c319903a97f67a2afa887957d",
-        "bytes": 5036550528},
+        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
+        "bytes": 5031887360},
     ("reconstruct_bf16", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "ac49670e34955b2158c3dfcdfcc64266705d944c319903a97f67a2afa887957d",
-        "bytes": 26355010560},
+        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
+        "bytes": 26205043040},
     ("reconstruct_bf16_sdq", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "ac49670e34955b2158c3dfcdfcc64266705d944c319903a97f67a2afa887957d",
-        "bytes": 26164824768},
+        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
+        "bytes": 26145284832},
     # one step of the 32B layer (profiles/counters_layer32b.md)
     ("encode", "layer32b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
                   "rescore_pe.hip", "rescore64.h"],
-        "sha256": "7f55fe52df88c7b843d16fa7bbb3fcc3da8719fbd21894e1fbbca4eabaae7f8d",
-        "bytes": 8118968640},
+        "sha256": "f5cd199c3a5245c6611d36b08ee9fe96bce500bab8f26b718433d744bcd47246",
+        "bytes": 8115737536},
     ("backbone", "layer32b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "b074178e7b2d45f0ef5bb61505337dabac7ef556a8d0eca21ff5d4bed0d1c8e7",
-        "bytes": 3518908416},
+        "sha256": "dcb4f93b7f42ea7e4e107e5aa5283970870690d71ac7c8e85eee85eea5c2df24",
+        "bytes": 3185498720},
     ("decode_apply", "layer32b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "ac49670e34955b2158c3dfcdfcc64266705d944c319903a97f67a2afa887957d",
-        "bytes": 951908096},
+        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
+        "bytes": 951638528},
 }
 
 
