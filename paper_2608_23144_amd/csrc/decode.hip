@@ -23,6 +23,7 @@ constexpr int kLdsModules = 256;  // module tables up to this size are staged in
 
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_a8_t __attribute__((ext_vector_type(4), aligned(8)));  // 8-byte aligned
 
 #define HIP_RETURN_IF(expr)            \
   do {                                 \
@@ -524,10 +525,16 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       D.rec[k] = (W.word[k] >> sh) & 1u;
       const uint32_t r = D.rec[k] ? W.pre[k] + __popc(W.word[k] & ((1u << sh) - 1u)) : 0u;
       const uint32_t* dp = reinterpret_cast<const uint32_t*>(a.dec_t) + 8 * (size_t)r;
-      D.sw[k] = *reinterpret_cast<const u32x2_t*>(dp + 2);
       D.rank[k] = ro.ranked ? dp[0] : 0u;
-      using QT = typename std::remove_reference<decltype(D.q[0])>::type;
-      D.q[k] = *reinterpret_cast<const QT*>(dp + 4);
+      if constexpr (G <= 2) {
+        // words 2..5 (seed | scale, sum of codes, the two code words) in one load
+        const u32x4_a8_t v = *reinterpret_cast<const u32x4_a8_t*>(dp + 2);
+        D.sw[k] = u32x2_t{v[0], v[1]};
+        D.q[k] = u32x2_t{v[2], v[3]};
+      } else {
+        D.sw[k] = *reinterpret_cast<const u32x2_t*>(dp + 2);
+        D.q[k] = *reinterpret_cast<const u32x4_t*>(dp + 4);
+      }
     }
   };
   auto compute = [&](uint64_t c, const RecBackbone<NU>& B, const RecDec<NU, G>& D) {
