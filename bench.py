@@ -59,16 +59,16 @@ MEASURED_TRAFFIC = {
         "bytes": 18135252320},
     ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
-        "bytes": 5031887360},
+        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
+        "bytes": 5032710912},
     ("reconstruct_bf16", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
-        "bytes": 26205043040},
+        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
+        "bytes": 26212469184},
     ("reconstruct_bf16_sdq", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
-        "bytes": 26145284832},
+        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
+        "bytes": 26144040768},
     # one step of the 32B layer (profiles/counters_layer32b.md)
     ("encode", "layer32b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
@@ -81,8 +81,8 @@ MEASURED_TRAFFIC = {
         "bytes": 3185498720},
     ("decode_apply", "layer32b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "2916ecdd958ca45c6cfaea9efc473bd495259bbb216c5f76e1806dea07a4df43",
-        "bytes": 951638528},
+        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
+        "bytes": 951671296},
 }
 
 
