@@ -577,10 +577,12 @@ __global__ __launch_bounds__(256) void k_merge_runs(const SortItem* __restrict__
 // stable passes (the items enter in tile order, so equal keys keep
 // increasing tiles, the same total order as the merge path).  A pass is a
 // block histogram (kRsItems items per block), a scan per digit over the
-// blocks, and a scatter in which every block places its items in index
-// order: within a wavefront by matching digits with ballots, across the
-// block's four wavefronts and its rounds through LDS counters.  The last
-// pass packs the records instead of writing items.
+// blocks, and a scatter in which every block first orders its items by digit
+// in LDS (index order within a digit: within a wavefront by matching digits
+// with ballots, across the block's four wavefronts and its rounds through LDS
+// counters) and then writes them in that order, so that each digit's run of
+// the block goes out as adjacent stores rather than one scattered 16-byte
+// store per lane.  The last pass packs the records instead of writing items.
 constexpr int kRsBits = 8;
 constexpr int kRsBins = 1 << kRsBits;
 constexpr int kRsThreads = 256;
@@ -632,15 +634,18 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
                                                            const uint32_t* __restrict__ hist, int nblk,
                                                            const uint32_t* __restrict__ tot, int pack, PackArgs pa) {
   __shared__ uint32_t dbase[kRsBins];         // first slot of each digit for this block
+  __shared__ uint32_t lstart[kRsBins];        // first place of each digit in the block's digit order
+  __shared__ uint32_t lcur[kRsBins];          // next place of each digit in that order
   __shared__ uint32_t wc[kRsThreads / 64][kRsBins];  // items per digit of each wavefront in the round
   __shared__ uint64_t s_wave[kRsThreads / 64];
+  __shared__ SortItem s_items[kRsItems];      // the block's items in digit order (stable within a digit)
   const int64_t n = (int64_t)state[kSegK];
   const int64_t base = (int64_t)blockIdx.x * kRsItems;
   if (base >= n) return;  // uniform per block
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  {
-    // digit bases: exclusive scan of the 256 totals, plus this block's prefix
-    const uint32_t v = tot[t];
+  // exclusive scan of one value per digit (thread t holds digit t's) over the
+  // block's 256 threads
+  auto scan256 = [&](uint32_t v) -> uint32_t {
     uint32_t x = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -652,8 +657,11 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
     uint32_t before = 0;
 #pragma unroll
     for (int k = 0; k < kRsThreads / 64; ++k) before += k < w ? (uint32_t)s_wave[k] : 0u;
-    dbase[t] = before + x - v + hist[(int64_t)t * nblk + blockIdx.x];
-  }
+    __syncthreads();  // s_wave is reused by the next scan
+    return before + x - v;
+  };
+  // digit bases: exclusive scan of the 256 totals, plus this block's prefix
+  dbase[t] = scan256(tot[t]) + hist[(int64_t)t * nblk + blockIdx.x];
   const uint64_t lt = lanemask_lt();
   // every round's item is loaded before the first round (one wait, not one
   // per round)
@@ -664,6 +672,20 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
     xs[r].key = 0; xs[r].tile = 0; xs[r].aux = 0;
     if (i < n) xs[r] = in[i];
   }
+  // the block's count of each digit, then where each digit's run starts in
+  // the block's digit order
+  lcur[t] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kRsRounds; ++r)
+    if (base + r * kRsThreads + t < n) atomicAdd(&lcur[(uint32_t)(xs[r].key >> shift) & (kRsBins - 1)], 1u);
+  __syncthreads();
+  const uint32_t ls = scan256(lcur[t]);
+  lstart[t] = ls;
+  lcur[t] = ls;
+  // place every item in the block's digit order: within a wavefront by
+  // matching digits with ballots, across the block's wavefronts and its
+  // rounds through LDS counters (index order within a digit)
 #pragma unroll
   for (int r = 0; r < kRsRounds; ++r) {
 #pragma unroll
@@ -684,17 +706,31 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_scatter(const SortItem* __res
     if (valid && rank == 0) wc[w][d] = (uint32_t)__popcll(same);
     __syncthreads();
     if (valid) {
-      uint32_t off = dbase[d] + rank;
+      uint32_t lp = lcur[d] + rank;
 #pragma unroll
-      for (int k = 0; k < kRsThreads / 64; ++k) off += k < w ? wc[k][d] : 0u;
-      if (pack) pack_record(pa, state, (int64_t)off, x.tile, x.aux);
-      else out[off] = x;
+      for (int k = 0; k < kRsThreads / 64; ++k) lp += k < w ? wc[k][d] : 0u;
+      s_items[lp] = x;
     }
     __syncthreads();
     uint32_t add = 0;
 #pragma unroll
     for (int k = 0; k < kRsThreads / 64; ++k) add += wc[k][t];
-    dbase[t] += add;
+    lcur[t] += add;
+  }
+  __syncthreads();
+  // write the block's items in digit order: consecutive threads take
+  // consecutive items, so each digit's run goes out as adjacent stores
+  const int64_t m = n - base < kRsItems ? n - base : kRsItems;
+#pragma unroll 4
+  for (int r = 0; r < kRsRounds; ++r) {
+    const int j = r * kRsThreads + t;
+    if (j < m) {
+      const SortItem x = s_items[j];
+      const uint32_t d = (uint32_t)(x.key >> shift) & (kRsBins - 1);
+      const uint32_t off = dbase[d] + ((uint32_t)j - lstart[d]);
+      if (pack) pack_record(pa, state, (int64_t)off, x.tile, x.aux);
+      else out[off] = x;
+    }
   }
 }
 
