@@ -343,7 +343,7 @@ __global__ __launch_bounds__(256) void k_decode_apply(DecodeArgs a) {
 
 // ---------------------------------------------------------------- dense bf16 reconstruction
 // One streaming pass over every weight of every module.  Lanes own units of
-// kUnitW consecutive weights (kUnitW / 2 bytes of codes in, 2 kUnitW bytes of
+// UW consecutive weights (UW / 2 bytes of codes in, 2 UW bytes of
 // bf16 out, consecutive lanes on consecutive units), W0 =
 // f32(q - z) * s recomputed from the backbone.  A lane whose tile has a record
 // (bit set in the validation bitmap) reads it at the tile's rank in the
@@ -371,24 +371,27 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
 #define AWSRC_GLOBAL __attribute__((address_space(1)))
 
 constexpr int kRecThreads = 512;
-// weights per unit (8 or 16).  8: a unit's 16 output bytes per target are one
-// store, and consecutive lanes' stores are adjacent, so a wavefront's store
-// covers 1 KB without gaps.  With 16 (two 16-byte stores per lane, 32 bytes
-// apart) the address and data units of the CUs, not memory, bounded the pass
-// (busy 99% of its cycles), and it ran 20% slower.
-constexpr int kUnitW = 8;
-constexpr int kLogUnitW = kUnitW == 16 ? 4 : 3;
+// Weights per unit of a pass with NO targets.  Four targets: 8, so that a
+// unit's 16 output bytes per target are one store and consecutive lanes'
+// stores are adjacent (a wavefront's store covers 1 KB without gaps); with 16
+// (two 16-byte stores per lane and target, 32 bytes apart) the address and
+// data units of the CUs, not memory, bounded the pass (busy 99% of its
+// cycles), and it ran 20% slower.  One target: 16, which halves the loads per
+// weight where stores are fewer (4-7% faster at C = 128, even at C = 64).
+template <int NO>
+constexpr int rec_unit_w() { return NO == 1 ? 16 : 8; }
 constexpr int kRecUnits = 2;                 // units per lane per chunk
 constexpr int kTsignLdsMax = 64 * 1024;      // sign tables up to this size are staged in LDS
-// the codes of one unit: kUnitW / 2 bytes
-using UnitCodes = std::conditional<kUnitW == 16, u32x2_t, uint32_t>::type;
+// the codes of one unit of UW weights: UW / 2 bytes
+template <int UW>
+using UnitCodes = typename std::conditional<UW == 16, u32x2_t, uint32_t>::type;
 
 __device__ __forceinline__ uint32_t code_word(const u32x2_t& q, int i) { return q[i]; }
 __device__ __forceinline__ uint32_t code_word(const uint32_t& q, int) { return q; }
 
-template <int NU>
+template <int NU, int UW>
 struct RecBackbone {                         // backbone words of one chunk
-  UnitCodes q[NU];
+  UnitCodes<UW> q[NU];
   uint32_t s[NU], z[NU];                     // fp16 scale bits, or the SDQ scale code (sign-extended)
   float mu[NU], st[NU];                      // SDQ: the mean and step of the scale code's block
   uint32_t m[NU];                            // module (within the window) and first element of the unit
@@ -431,6 +434,8 @@ template <int C, int G, bool TS_LDS, int NO, bool SDQ>
 __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, BackboneTabs bb, RecOut ro, int m0,
                                                              int nm) {
   constexpr int NT = kRecThreads, NU = kRecUnits;
+  constexpr int kUnitW = rec_unit_w<NO>();               // weights per unit
+  constexpr int kLogUnitW = kUnitW == 16 ? 4 : 3;
   constexpr int UPT = C / kUnitW;                        // lanes per tile
   constexpr int LOG_UPT = ((C == 16) ? 4 : (C == 32) ? 5 : (C == 64) ? 6 : 7) - kLogUnitW;
   constexpr float isq = (C == 16) ? 0.25f : (C == 32) ? 0.17677669529663688f
@@ -480,7 +485,7 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
   int m = 0;
   uint64_t m_lo = u_begin, m_hi = s_off[1] << LOG_UPT;
 
-  auto issue_backbone = [&](uint64_t c, RecBackbone<NU>& B) {
+  auto issue_backbone = [&](uint64_t c, RecBackbone<NU, kUnitW>& B) {
 #pragma unroll
     for (int k = 0; k < NU; ++k) {
       uint64_t u = c + (uint64_t)(k * NT) + threadIdx.x;
@@ -493,7 +498,7 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       }
       const uint64_t el = (u - m_lo) << kLogUnitW;       // first element of the unit
       const uint64_t g = el >> bb.gshift;
-      B.q[k] = *((const AWSRC_GLOBAL UnitCodes*)s_cp[m] + (el >> kLogUnitW));
+      B.q[k] = *((const AWSRC_GLOBAL UnitCodes<kUnitW>*)s_cp[m] + (el >> kLogUnitW));
       if constexpr (SDQ) {
         B.s[k] = (uint32_t)(int32_t)((const AWSRC_GLOBAL int8_t*)s_sp[m])[g];
         B.mu[k] = ((const AWSRC_GLOBAL float*)s_mp[m])[g / kSdqBlock];
@@ -537,7 +542,7 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
       }
     }
   };
-  auto compute = [&](uint64_t c, const RecBackbone<NU>& B, const RecDec<NU, G>& D) {
+  auto compute = [&](uint64_t c, const RecBackbone<NU, kUnitW>& B, const RecDec<NU, G>& D) {
 #pragma unroll
     for (int k = 0; k < NU; ++k) {
       if (!B.ok[k]) continue;
@@ -627,7 +632,7 @@ __global__ __launch_bounds__(kRecThreads) void k_reconstruct(DecodeArgs a, Backb
   // so that nothing in flight is ever copied; the bitmap words of chunk
   // c + step are consumed (record loads) before the words of c + 2 step are
   // loaded into the same registers
-  RecBackbone<NU> B0, B1;
+  RecBackbone<NU, kUnitW> B0, B1;
   RecBits<NU> W;
   RecDec<NU, G> D0, D1;
   issue_bits(c0, W);
@@ -673,7 +678,7 @@ static hipError_t launch_rec_cgt(const DecodeArgs& a, const BackboneTabs& bb, co
     HIP_RETURN_IF(
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_reconstruct<C, G, TS_LDS, NO, SDQ>, kRecThreads, lds));
     if (per_cu < 1) per_cu = 1;
-    const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / kUnitW);
+    const uint64_t units = (toff[m0 + nm] - toff[m0]) * (uint64_t)(C / rec_unit_w<NO>());
     const uint64_t chunks = (units + kRecUnits * kRecThreads - 1) / (kRecUnits * kRecThreads);
     // four times the blocks that fit at once, grid-stride beyond (more blocks
     // than resident keep the CUs full to the end: 2.5% faster on the 2.8G-
