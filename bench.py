@@ -59,16 +59,16 @@ MEASURED_TRAFFIC = {
         "bytes": 18135252320},
     ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
-        "bytes": 5032710912},
+        "sha256": "714d9fc777f576f347fc8ca0e18b6a2edc15cf7e84d2c2ff7b727c84c5f3c69c",
+        "bytes": 5032715136},
     ("reconstruct_bf16", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
-        "bytes": 26212469184},
+        "sha256": "714d9fc777f576f347fc8ca0e18b6a2edc15cf7e84d2c2ff7b727c84c5f3c69c",
+        "bytes": 26212606368},
     ("reconstruct_bf16_sdq", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
-        "bytes": 26144040768},
+        "sha256": "714d9fc777f576f347fc8ca0e18b6a2edc15cf7e84d2c2ff7b727c84c5f3c69c",
+        "bytes": 26142208960},
     # one step of the 32B layer (profiles/counters_layer32b.md)
     ("encode", "layer32b"): {
         "files": ["awsrc_internal.h", "basis.hip", "encode.hip", "encode_mfma.hip", "encode_pe.hip",
@@ -81,8 +81,8 @@ MEASURED_TRAFFIC = {
         "bytes": 3185498720},
     ("decode_apply", "layer32b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
-        "sha256": "eee03c0087be31eb6223ced661f4e32dda08578003022cbf20a5d37c13f12761",
-        "bytes": 951671296},
+        "sha256": "714d9fc777f576f347fc8ca0e18b6a2edc15cf7e84d2c2ff7b727c84c5f3c69c",
+        "bytes": 951661440},
 }
 
 
