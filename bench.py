@@ -55,7 +55,7 @@ MEASURED_TRAFFIC = {
         "bytes": 59053364832},
     ("backbone", "stack3b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "dcb4f93b7f42ea7e4e107e5aa5283970870690d71ac7c8e85eee85eea5c2df24",
+        "sha256": "dd09c1f2caf969e853367c60ca0066165bb345dae7435d5e68306dc76e166f06",
         "bytes": 18135252320},
     ("decode_apply", "stack3b"): {
         "files": ["awsrc_internal.h", "decode.hip"],
@@ -77,7 +77,7 @@ MEASURED_TRAFFIC = {
         "bytes": 8115737536},
     ("backbone", "layer32b"): {
         "files": ["awsrc_internal.h", "backbone.hip"],
-        "sha256": "dcb4f93b7f42ea7e4e107e5aa5283970870690d71ac7c8e85eee85eea5c2df24",
+        "sha256": "dd09c1f2caf969e853367c60ca0066165bb345dae7435d5e68306dc76e166f06",
         "bytes": 3185498720},
     ("decode_apply", "layer32b"): {
         "files": ["awsrc_internal.h", "decode.hip"],

